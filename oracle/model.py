@@ -1,0 +1,228 @@
+"""Llama-family decoder, rollout and teacher-forced scoring, in fp64.
+
+The paper's policy and its frozen reference are Llama3 decoders (Sec. VI-C);
+GRPO samples K completions per prompt from the policy (Alg. 1, sampling step)
+and needs log pi(x|c) of each sampled token under the policy and the reference
+(Eq. 1 and the KL term).  The decoder here is the family's standard
+definition, per layer:
+
+    h = R1(rmsnorm(x) * g_attn)
+    q, k, v = h Wq^T, h Wk^T, h Wv^T         (q, k rotated by RoPE, then R2)
+    o_h = softmax_j(q_h . k_{kv(h), j} / sqrt(hd)) v_{kv(h), j}   over j <= i
+    x += R3(o) Wo^T
+    h = R1(rmsnorm(x) * g_mlp)
+    x += R4(silu(h Wg^T) * (h Wu^T)) Wd^T
+
+and logits = R5(rmsnorm(x) * g_final) W_head^T.  kv(h) = floor(h * H_kv / H)
+(grouped-query attention).  R1..R5 are bf16 round-to-nearest-even applied only
+for bf16 models (weights stored in bf16); fp32 models have no rounding points.
+Everything else is fp64.
+
+``forward`` is the plain full-sequence definition.  ``decode_layer`` is the
+same layer for one new token per sequence against a KV cache; the test suite
+pins it to ``forward`` (cached decode equals full recompute).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .numerics import bf16_bits_to_f64, rmsnorm, round_bf16, rope, silu
+from .sampler import log_softmax, sample_token
+
+
+def _ident(x):
+    return x
+
+
+def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """q [T, H, hd], k/v [T, Hkv, hd] -> o [T, H, hd]; query i sees keys j <= i.
+
+    Query head h reads key/value head floor(h * Hkv / H) (grouped-query attention).
+    """
+    T, H, hd = q.shape
+    Hk = k.shape[1]
+    causal = np.tril(np.ones((T, T), bool))
+    o = np.empty((T, H, hd))
+    for hh in range(H):
+        g = hh * Hk // H
+        s = (q[:, hh, :] @ k[:, g, :].T) / np.sqrt(hd)
+        s = np.where(causal, s, -np.inf)
+        pr = np.exp(s - s.max(axis=1, keepdims=True))
+        pr /= pr.sum(axis=1, keepdims=True)
+        o[:, hh, :] = pr @ v[:, g, :]
+    return o
+
+
+class OracleModel:
+    """cfg: any object with the decoder shape attributes (n_layers, d_model, ...)."""
+
+    def __init__(self, cfg, weights: dict, round_points: bool = True):
+        self.cfg = cfg
+        self.w = weights
+        self.bf16 = np.asarray(weights["tok_emb"]).dtype == np.uint16
+        self.R = round_bf16 if (self.bf16 and round_points) else _ident
+        self._f64 = {}
+
+    # -- weights --------------------------------------------------------------
+    def mat(self, name: str) -> np.ndarray:
+        if name not in self._f64:
+            a = np.asarray(self.w[name])
+            self._f64[name] = bf16_bits_to_f64(a) if a.dtype == np.uint16 else a.astype(np.float64)
+        return self._f64[name]
+
+    def drop_cache(self):
+        self._f64.clear()
+
+    def embed(self, tokens) -> np.ndarray:
+        a = np.asarray(self.w["tok_emb"])[np.asarray(tokens)]
+        return bf16_bits_to_f64(a) if a.dtype == np.uint16 else a.astype(np.float64)
+
+    # -- full-sequence forward (the definition) -------------------------------
+    def forward(self, tokens, return_hidden: bool = False):
+        """tokens [T] of one sequence -> logits [T, V], per-layer (k, v) [Hkv, T, hd]."""
+        c, R = self.cfg, self.R
+        T = len(tokens)
+        H, Hk, hd = c.n_heads, c.n_kv_heads, c.head_dim
+        pos = np.arange(T)
+        x = self.embed(tokens)
+        kv, hidden = [], [x.copy()]
+        for l in range(c.n_layers):
+            p = f"l{l}."
+            h = R(rmsnorm(x, self.mat(p + "attn_norm"), c.rms_eps))
+            q = (h @ self.mat(p + "wq").T).reshape(T, H, hd)
+            k = (h @ self.mat(p + "wk").T).reshape(T, Hk, hd)
+            v = (h @ self.mat(p + "wv").T).reshape(T, Hk, hd)
+            q = R(rope(q, pos, c.rope_theta))
+            k = R(rope(k, pos, c.rope_theta))
+            v = R(v)
+            o = causal_attention(q, k, v)
+            x = x + R(o.reshape(T, H * hd)) @ self.mat(p + "wo").T
+            h = R(rmsnorm(x, self.mat(p + "mlp_norm"), c.rms_eps))
+            a = R(silu(h @ self.mat(p + "w_gate").T) * (h @ self.mat(p + "w_up").T))
+            x = x + a @ self.mat(p + "w_down").T
+            kv.append((k.transpose(1, 0, 2).copy(), v.transpose(1, 0, 2).copy()))
+            hidden.append(x.copy())
+        logits = self.head(x)
+        if return_hidden:
+            return logits, kv, hidden
+        return logits, kv
+
+    def head(self, x: np.ndarray) -> np.ndarray:
+        """Final RMSNorm + LM head: [n, d] -> [n, V]."""
+        h = self.R(rmsnorm(x, self.mat("final_norm"), self.cfg.rms_eps))
+        return h @ self.mat("lm_head").T
+
+    # -- one decode layer against a KV cache ---------------------------------
+    def decode_layer(self, l: int, x: np.ndarray, pos: np.ndarray, K: np.ndarray,
+                     V: np.ndarray):
+        """x [B, d] residual in, pos [B], K/V [B, Hkv, >pos, hd] caches of layer l.
+
+        Entries of K/V before each sequence's pos are read as given; the new
+        token's k, v are computed, written at pos and returned with the
+        updated residual.
+        """
+        c, R = self.cfg, self.R
+        B = x.shape[0]
+        H, Hk, hd = c.n_heads, c.n_kv_heads, c.head_dim
+        p = f"l{l}."
+        h = R(rmsnorm(x, self.mat(p + "attn_norm"), c.rms_eps))
+        q = (h @ self.mat(p + "wq").T).reshape(B, H, hd)
+        k = (h @ self.mat(p + "wk").T).reshape(B, Hk, hd)
+        v = (h @ self.mat(p + "wv").T).reshape(B, Hk, hd)
+        o = np.empty((B, H, hd))
+        k_new = np.empty((B, Hk, hd))
+        v_new = np.empty((B, Hk, hd))
+        for b in range(B):
+            pb = int(pos[b])
+            qb = R(rope(q[b:b + 1], np.array([pb]), c.rope_theta))[0]
+            kb = R(rope(k[b:b + 1], np.array([pb]), c.rope_theta))[0]
+            vb = R(v[b])
+            K[b, :, pb, :] = kb
+            V[b, :, pb, :] = vb
+            k_new[b], v_new[b] = kb, vb
+            for hh in range(H):
+                g = hh * Hk // H
+                s = K[b, g, : pb + 1, :] @ qb[hh] / np.sqrt(hd)
+                pr = np.exp(s - s.max())
+                pr /= pr.sum()
+                o[b, hh] = pr @ V[b, g, : pb + 1, :]
+        x = x + R(o.reshape(B, H * hd)) @ self.mat(p + "wo").T
+        h = R(rmsnorm(x, self.mat(p + "mlp_norm"), c.rms_eps))
+        a = R(silu(h @ self.mat(p + "w_gate").T) * (h @ self.mat(p + "w_up").T))
+        x = x + a @ self.mat(p + "w_down").T
+        return x, k_new, v_new
+
+    def decode(self, tokens, pos, K: np.ndarray, V: np.ndarray, return_hidden: bool = False):
+        """One decode step for B sequences; K/V [L, B, Hkv, Tmax, hd] updated in place."""
+        x = self.embed(tokens)
+        hidden = [x.copy()]
+        for l in range(self.cfg.n_layers):
+            x, _, _ = self.decode_layer(l, x, np.asarray(pos), K[l], V[l])
+            hidden.append(x.copy())
+        logits = self.head(x)
+        return (logits, hidden) if return_hidden else logits
+
+    # -- GRPO rollout: K samples per prompt -----------------------------------
+    def rollout(self, prompts, group: int, new_tokens: int, temperature: float, top_k: int,
+                seed: int, forced=None, keep_logits: bool = False, seq_ids=None):
+        """Sample ``group`` completions of ``new_tokens`` tokens for every prompt.
+
+        Sequence id of sample g of prompt p is p*group + g; the first token is
+        generation step 0 (drawn from the prompt's last position), later tokens
+        are steps 1..new_tokens-1 of cached decode.  ``forced`` [B, Tn] feeds the
+        given tokens back instead of the oracle's own (teacher-forced replay);
+        the oracle's own decision and its margin are still returned.
+        """
+        c = self.cfg
+        prompts = np.asarray(prompts)
+        P, Tp = prompts.shape
+        B = P * group
+        Tmax = Tp + new_tokens - 1
+        L, Hk, hd = c.n_layers, c.n_kv_heads, c.head_dim
+        K = np.zeros((L, B, Hk, max(Tmax, Tp), hd))
+        V = np.zeros_like(K)
+        toks = np.zeros((B, new_tokens), np.int64)
+        own = np.zeros((B, new_tokens), np.int64)
+        logp = np.zeros((B, new_tokens))
+        margin = np.zeros((B, new_tokens))
+        logits_all = [] if keep_logits else None
+        sid = np.arange(B) if seq_ids is None else np.asarray(seq_ids)
+        first = np.zeros((B, c.vocab))
+        for p in range(P):
+            lg, kv = self.forward(prompts[p])
+            for g in range(group):
+                b = p * group + g
+                for l in range(L):
+                    K[l, b, :, :Tp] = kv[l][0]
+                    V[l, b, :, :Tp] = kv[l][1]
+                first[b] = lg[-1]
+        cur = first
+        for s in range(new_tokens):
+            if s > 0:
+                pos = np.full(B, Tp + s - 1)
+                cur = self.decode(toks[:, s - 1], pos, K, V)
+            if keep_logits:
+                logits_all.append(cur.copy())
+            for b in range(B):
+                t, lp, m = sample_token(cur[b], temperature, top_k, seed, s, int(sid[b]))
+                own[b, s], margin[b, s] = t, m
+                toks[b, s] = t if forced is None else int(forced[b, s])
+                z = cur[b] / (temperature if temperature > 0 else 1.0)
+                logp[b, s] = lp if forced is None else float(log_softmax(z)[toks[b, s]])
+        out = dict(tokens=toks, own_tokens=own, logp=logp, margin=margin, K=K, V=V)
+        if keep_logits:
+            out["logits"] = np.stack(logits_all, axis=1)
+        return out
+
+    # -- teacher-forced scoring -----------------------------------------------
+    def score(self, tokens, score_from: int, temperature: float) -> np.ndarray:
+        """logp[n, j - score_from] = log_softmax(l_{j-1} / T)[tok_j] for j in [score_from, T)."""
+        tokens = np.asarray(tokens)
+        N, T = tokens.shape
+        Tt = temperature if temperature > 0 else 1.0
+        out = np.zeros((N, T - score_from))
+        for n in range(N):
+            lg, _ = self.forward(tokens[n])
+            ls = log_softmax(lg[score_from - 1:T - 1] / Tt)
+            out[n] = ls[np.arange(T - score_from), tokens[n, score_from:]]
+        return out
