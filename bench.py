@@ -1,0 +1,198 @@
+#!/usr/bin/env python3
+"""GRPO hot-path benchmark on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+prompt prefill + G-sample decode (the rollout), teacher-forced scoring of the
+completions under the policy and the frozen reference, group advantages and the
+clipped-ratio + KL token loss.  Prints ONE JSON line.
+
+  value      sampled (rollout) tokens per second of whole steps
+  roofline   the dominant kernel's algorithmic bytes / its measured duration
+  cpu_baseline  the CPU oracle on a bounded sample of the same workload
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def decode_bytes_per_step(w, ctx_avg: float) -> float:
+    """Algorithmic HBM bytes of one decode step: every weight once (embedding rows
+    aside), the KV of every context position once, the new K/V written."""
+    c = w.model
+    es = c.elem_bytes
+    weights = (c.n_params() - c.vocab * c.d_model) * es + w.batch * c.d_model * es
+    kv_tok = c.kv_bytes_per_token()
+    return weights + w.batch * ctx_avg * kv_tok + w.batch * kv_tok
+
+
+def score_flops(w) -> float:
+    """Algorithmic flops of scoring one model over the batch."""
+    c = w.model
+    T, N = w.total_len, w.batch
+    per_tok = 2 * (c.d_model * (c.q_dim + 2 * c.kv_dim) + c.q_dim * c.d_model
+                   + 3 * c.d_model * c.d_ffn)
+    attn = 2 * 2 * c.n_layers * c.n_heads * c.head_dim * (T * (T + 1) / 2)
+    head = 2 * c.vocab * c.d_model * (T - w.prompt_len)
+    return c.n_layers * per_tok * N * T + attn * N + head * N
+
+
+def cpu_baseline(w, host, budget_s: float = 15.0) -> dict:
+    """The oracle (fp64 NumPy) on a bounded sample: decode steps of up to 8
+    sequences at the prompt-length context, all layers + LM head + sampler."""
+    import numpy as np
+    import oracle
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except Exception:
+        cores = os.cpu_count() or 1
+    c = w.model
+    nb = min(8, w.batch)
+    ctx = w.prompt_len
+    om = oracle.OracleModel(c, host)
+    rng = np.random.default_rng(0)
+    x0 = om.embed(rng.integers(0, c.vocab, nb))
+    t0 = time.perf_counter()
+    steps = 0
+    while True:
+        x = x0.copy()
+        for l in range(c.n_layers):
+            K = rng.standard_normal((nb, c.n_kv_heads, ctx + 1, c.head_dim)) * 0.5
+            V = rng.standard_normal((nb, c.n_kv_heads, ctx + 1, c.head_dim)) * 0.5
+            x, _, _ = om.decode_layer(l, x, np.full(nb, ctx), K, V)
+            om.drop_cache()
+        lg = om.head(x)
+        om.drop_cache()
+        for b in range(nb):
+            oracle.sample_token(lg[b], w.temperature, w.top_k, 1, steps, b)
+        steps += 1
+        if time.perf_counter() - t0 >= budget_s or steps >= 64:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": nb * steps / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{steps} decode step(s) of {nb} sequences at context {ctx}: all "
+                      f"{c.n_layers} layers, LM head and sampler in fp64 NumPy ({dt:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="7b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the hot path is built and measured on a single MI355X.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2510_17158_amd import api, synth
+    from paper_2510_17158_amd.runner import GrpoIteration
+    from paper_2510_17158_amd.workloads import get
+
+    w = get(args.workload)
+    c = w.model
+    torch.cuda.set_device(0)
+    t = time.perf_counter()
+    host = synth.make_weights(c, w.master_seed)
+    pol = api.Model(c, api.upload_weights(c, host))
+    ref = None
+    if w.score:
+        ref_host = synth.make_weights(c, w.master_seed, ref=True)
+        ref = api.Model(c, api.upload_weights(c, ref_host))
+        del ref_host
+    it = GrpoIteration(w, pol, ref, synth.make_prompts(w), synth.make_rewards(w),
+                       synth.make_seed(w))
+    torch.cuda.synchronize()
+    log(f"[bench] set-up {time.perf_counter() - t:.1f} s  workload {w.name}")
+
+    def step(ev=None):
+        if ev: ev[0].record()
+        it.prefill()
+        if ev: ev[1].record()
+        it.decode()
+        if ev: ev[2].record()
+        it.assemble()
+        if w.score:
+            it.score()
+        else:
+            it.lp_pol.copy_(it.logp_old)
+        if ev: ev[3].record()
+        it.grpo()
+        if ev: ev[4].record()
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+    phases = np.zeros(4)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        step(ev)
+        torch.cuda.synchronize()
+        phases += [ev[j].elapsed_time(ev[j + 1]) for j in range(4)]
+        log(f"[bench] step {i + 1}/{args.steps} done")
+    wall = time.perf_counter() - t0
+    phases /= args.steps
+    ms_step = wall * 1e3 / args.steps
+    gen = w.batch * w.new_tokens
+    n_dec = w.new_tokens - 1
+    dec_ms = phases[1] / max(n_dec, 1)
+    ctx_avg = w.prompt_len + n_dec / 2.0
+    dec_bytes = decode_bytes_per_step(w, ctx_avg)
+    n_models = 2 if w.score else 0
+    out = {
+        "metric": "rollout tokens/s on 1 MI355X (G samples/prompt) + % of HBM roofline",
+        "value": gen * args.steps / wall,
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if c.dtype == 1 else "f32",
+        "data": "synthetic (seeded random-init weights, code-like prompts with tool spans)",
+        "config": {"workload": w.name, "layers": c.n_layers, "d_model": c.d_model,
+                   "prompts": w.n_prompts, "group": w.group, "prompt_len": w.prompt_len,
+                   "new_tokens": w.new_tokens, "batch": w.batch,
+                   "scored_models": n_models},
+        "phases_ms": {"prefill": phases[0], "decode": phases[1], "score": phases[2],
+                      "advantages_loss": phases[3]},
+        "rollout_tokens_per_s": gen / ((phases[0] + phases[1]) / 1e3),
+        "decode_step_ms": dec_ms,
+        "decode_step_gbs": dec_bytes / (dec_ms / 1e3) / 1e9,
+        "decode_step_hbm_frac": dec_bytes / (dec_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+    }
+    if w.score:
+        sf = score_flops(w)
+        out["scored_tokens_per_s"] = n_models * w.batch * w.total_len / (phases[2] / 1e3)
+        out["score_tflops"] = n_models * sf / (phases[2] / 1e3) / 1e12
+        out["score_mfma_frac"] = out["score_tflops"] / BF16_PEAK_TFLOPS
+    out["roofline"] = {"bound": "hbm", "achieved": out["decode_step_gbs"], "peak": HBM_PEAK_GBS,
+                       "unit": "GB/s", "frac": out["decode_step_hbm_frac"], "traffic": None,
+                       "kernel": "decode step (all kernels)"}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, host, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,198 @@
+/*
+ * grpo_hip.h — C-ABI of the GRPO rollout / scoring / loss hot path on MI355X.
+ *
+ * The paper fine-tunes a Llama-family decoder with GRPO (Sec. VI-A, Alg. 1):
+ * each iteration samples K completions per prompt from the policy, scores
+ * them, normalises rewards within each group into advantages and applies the
+ * clipped-ratio objective with a KL penalty towards a frozen reference copy
+ * (Eq. 1).  Sec. I and Sec. VI-C name sample generation as the step that
+ * dominates training time.  This library exposes that path as HIP kernels for
+ * gfx950:
+ *
+ *   grpo_prefill          prompt forward + first sampled token of each group
+ *                         member (Alg. 1, sampling step, generation step 0)
+ *   grpo_rollout_step     n_steps batched decode steps (Alg. 1, sampling step)
+ *   grpo_score_sequences  teacher-forced log pi(x_t | c, x_<t) (Eq. 1, KL term)
+ *   grpo_advantages       group-normalised rewards w(x) (Alg. 1, normalisation)
+ *   grpo_token_loss       clipped-ratio + KL per-token loss, its gradient with
+ *                         respect to logp, and statistics (Eq. 1, GRPO form)
+ *
+ * Conventions
+ *  - Every tensor pointer is a DEVICE pointer owned by the caller.  The library
+ *    allocates no device memory: scratch space comes from the caller's
+ *    workspace (size from grpo_workspace_bytes).  A model handle keeps the
+ *    weight pointers (host copies of the pointer values, not of the weights);
+ *    the weights must outlive the handle.
+ *  - Every compute call is asynchronous on `stream` (a hipStream_t passed as
+ *    void*, NULL = the null stream).  Device faults surface at the caller's
+ *    next synchronisation.
+ *  - Every call returns 0 (GRPO_OK) or a negative grpo_status.  Arguments are
+ *    validated on the host BEFORE anything is enqueued, so a rejected call
+ *    leaves no partial work; grpo_last_error() returns a thread-local message.
+ *  - Outputs never alias inputs.  Results are bit-deterministic for identical
+ *    inputs and launch configuration: fixed-order reductions, no float atomics.
+ *  - Weight matrices are row-major [out, in] (nn.Linear layout).  The model
+ *    dtype (fp32 or bf16) is the dtype of every weight and of the KV cache.
+ *
+ * Precision contract (bf16 models): weights and KV in bf16; residual stream,
+ * accumulation, softmax, logits and log-probs in fp32; bf16 round-to-nearest-
+ * even at the inputs of the matrix products (normed activations, q/k after
+ * RoPE and v, attention output, SwiGLU output, final normed state).  fp32
+ * models round nowhere.
+ */
+#ifndef GRPO_HIP_H
+#define GRPO_HIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum grpo_status {
+  GRPO_OK = 0,
+  GRPO_INVALID_ARG = -1,          /* null pointer, bad size or range            */
+  GRPO_UNSUPPORTED = -2,          /* shape/dtype outside what the kernels cover */
+  GRPO_WORKSPACE_TOO_SMALL = -3,  /* ws_bytes below grpo_workspace_bytes(...)   */
+  GRPO_HIP_ERROR = -4,            /* a HIP runtime call failed                  */
+  GRPO_KV_CAPACITY = -5           /* positions would run past the KV capacity   */
+};
+
+enum grpo_dtype { GRPO_F32 = 0, GRPO_BF16 = 1 };
+
+/* Workspace kinds for grpo_workspace_bytes. */
+enum grpo_op { GRPO_OP_PREFILL = 0, GRPO_OP_ROLLOUT = 1, GRPO_OP_SCORE = 2, GRPO_OP_LOSS = 3 };
+
+/* Decoder shape.  Llama family: RMSNorm, RoPE (half-split pairs (i, i+hd/2),
+ * angle pos * rope_theta^(-2i/hd)), grouped-query attention (query head h reads
+ * kv head floor(h*n_kv_heads/n_heads)), SwiGLU MLP, untied LM head, no biases.
+ * Supported: head_dim in {64, 128}; n_heads a multiple of n_kv_heads; d_model,
+ * n_heads*head_dim and d_ffn multiples of 64 (of 32 for fp32 models). */
+typedef struct grpo_config {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
+  float rms_eps, rope_theta;
+  int32_t dtype; /* enum grpo_dtype */
+} grpo_config;
+
+/* Device pointers to the weights.  Per-layer entries are HOST arrays of
+ * n_layers device pointers; the handle copies those arrays. */
+typedef struct grpo_weights {
+  const void* tok_emb;            /* [vocab, d]                       */
+  const void* const* attn_norm;   /* L x [d]                          */
+  const void* const* wq;          /* L x [n_heads*hd, d]              */
+  const void* const* wk;          /* L x [n_kv_heads*hd, d]           */
+  const void* const* wv;          /* L x [n_kv_heads*hd, d]           */
+  const void* const* wo;          /* L x [d, n_heads*hd]              */
+  const void* const* mlp_norm;    /* L x [d]                          */
+  const void* const* w_gate;      /* L x [d_ffn, d]                   */
+  const void* const* w_up;        /* L x [d_ffn, d]                   */
+  const void* const* w_down;      /* L x [d, d_ffn]                   */
+  const void* final_norm;         /* [d]                              */
+  const void* lm_head;            /* [vocab, d]                       */
+} grpo_weights;
+
+/* Sampler.  z = logits / temperature.  temperature == 0 is greedy (lowest id
+ * among the maxima; logp then uses temperature 1).  top_k > 0 restricts the
+ * draw to the top_k logits ordered by (value desc, id asc).  Otherwise
+ * Gumbel-max: token = lowest id among the maxima over the allowed set of
+ * z_i - ln(-ln u_i), u_i = (2*(w >> 9) + 1) * 2^-24, w = word (i & 3) of
+ * Philox4x32-10(key = (seed mod 2^32, seed >> 32), ctr = (i >> 2, step, seq, 0)).
+ * The log-prob is always the full-vocabulary log_softmax(z)[token]. */
+typedef struct grpo_sampling {
+  float temperature;
+  int32_t top_k;
+  uint64_t seed;
+} grpo_sampling;
+
+typedef struct grpo_model grpo_model;
+
+/* Creates a handle over caller-owned weights.  Validates the shape (see
+ * grpo_config).  Returns GRPO_INVALID_ARG / GRPO_UNSUPPORTED on bad input. */
+int grpo_model_create(const grpo_config* cfg, const grpo_weights* w, grpo_model** out);
+int grpo_model_destroy(grpo_model* m);
+
+/* Bytes of a KV cache for n_seqs sequences of max_len positions.  Layout:
+ * [n_layers][2 (K, V)][n_seqs][n_kv_heads][max_len][head_dim], model dtype.
+ * Returns 0 for invalid arguments. */
+size_t grpo_kv_cache_bytes(const grpo_config* cfg, int32_t n_seqs, int32_t max_len);
+
+/* Workspace bytes of one call (0 for invalid arguments):
+ *   GRPO_OP_PREFILL: n_rows = prompts P, seq_len = prompt length Tp
+ *   GRPO_OP_ROLLOUT: n_rows = batch B,   seq_len = KV capacity max_len
+ *   GRPO_OP_SCORE:   n_rows = sequences N, seq_len = T
+ *   GRPO_OP_LOSS:    n_rows = sequences N, seq_len = Tr (model may be NULL) */
+size_t grpo_workspace_bytes(const grpo_model* m, int32_t op, int32_t n_rows, int32_t seq_len);
+
+/* Thread-local message of the last failed call on this thread ("" if none). */
+const char* grpo_last_error(void);
+
+/* Rollout generation step 0 (Alg. 1, sampling step): causal forward over every
+ * prompt (once per prompt, not per sample), its K/V written into the G cache
+ * slots p*G .. p*G+G-1, then G draws from the last position's logits with
+ * Philox sequence id p*G+g and step 0.
+ *   prompts   int32 [P, Tp] token ids in [0, vocab)
+ *   kv        cache of n_seqs >= P*G sequences, max_len >= Tp
+ *   tok_out   int32 [P*G] sampled tokens;  logp_out  fp32 [P*G]
+ *   logits_dbg NULL or fp32 [P, vocab]: the last-position logits
+ * Ids outside [0, vocab) are clamped by the kernels (memory safety only). */
+int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
+                 const int32_t* prompts, int32_t P, int32_t Tp, int32_t G,
+                 const grpo_sampling* s, int32_t* tok_out, float* logp_out, float* logits_dbg,
+                 void* ws, size_t ws_bytes, void* stream);
+
+/* n_steps decode steps for batch rows 0..B-1 (cache slots 0..B-1, Philox
+ * sequence id = row).  Per step: token tok[b] enters at position pos[b] (its
+ * K/V written there), attention over positions 0..pos[b], the next token is
+ * drawn with Philox step step0+s and written to tok[b] and tok_out[b, s], its
+ * log-prob to logp_out[b, s]; pos[b] += 1.
+ *   pos, tok   int32 [B] device, in/out
+ *   max_pos    host hint: the largest pos[b] on entry.  The call is rejected
+ *              with GRPO_KV_CAPACITY unless max_pos + n_steps <= max_len; the
+ *              kernels additionally never touch positions >= max_len.
+ *   tok_out    int32 [B, n_steps];  logp_out  fp32 [B, n_steps]
+ *   logits_dbg NULL or fp32 [B, vocab]: logits of the last step
+ *   hidden_dbg NULL or fp32 [n_layers+1, B, d]: residual stream entering each
+ *              layer and leaving the last one, for the last step */
+int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len, int32_t B,
+                      int32_t* pos, int32_t* tok, int32_t max_pos, int32_t step0, int32_t n_steps,
+                      const grpo_sampling* s, int32_t* tok_out, float* logp_out,
+                      float* logits_dbg, float* hidden_dbg, void* ws, size_t ws_bytes,
+                      void* stream);
+
+/* Teacher-forced scoring (Eq. 1's log pi and the KL term's reference): for
+ * j in [score_from, T): logp_out[n, j - score_from] =
+ * log_softmax(logits at position j-1 / temperature)[tokens[n, j]]
+ * (temperature 0 is read as 1).  tokens int32 [N, T]; 1 <= score_from < T. */
+int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, int32_t T,
+                         int32_t score_from, float temperature, float* logp_out, void* ws,
+                         size_t ws_bytes, void* stream);
+
+/* Group advantages (Alg. 1, normalisation step): for each of the P groups of
+ * G >= 2 rewards, A = (r - mean) / (sample std (divisor G-1) + eps); a group
+ * whose rewards are all equal gets A = 0.  rewards, adv_out fp32 [P*G]. */
+int grpo_advantages(const float* rewards, int32_t P, int32_t G, float eps, float* adv_out,
+                    void* stream);
+
+/* GRPO token loss (Eq. 1 in the clipped form of Sec. VI-A):
+ *   rho = exp(logp - logp_old); s = min(rho*A, clip(rho, 1-clip_eps, 1+clip_eps)*A)
+ *   kl  = exp(d) - d - 1, d = logp_ref - logp;  l = -s + beta*kl
+ * agg 0: mean of each sequence's masked tokens, then mean over sequences;
+ * agg 1: mean over all masked tokens.
+ *   logp, logp_old, logp_ref fp32 [N, Tr]; mask uint8 [N, Tr] (1 = trained);
+ *   adv fp32 [N]
+ *   loss_out    fp32 [1]
+ *   tok_loss    NULL or fp32 [N, Tr]: l where mask, else 0
+ *   dloss_dlogp NULL or fp32 [N, Tr]: d loss / d logp (0 where not mask)
+ *   stats       NULL or fp32 [4]: masked-token mean kl, fraction of tokens the
+ *               clip zeroes, mean ratio, count of non-finite l
+ * Arithmetic is fp64 inside; outputs fp32. */
+int grpo_token_loss(const float* logp, const float* logp_old, const float* logp_ref,
+                    const uint8_t* mask, const float* adv, int32_t N, int32_t Tr, float clip_eps,
+                    float beta, int32_t agg, float* loss_out, float* tok_loss, float* dloss_dlogp,
+                    float* stats, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GRPO_HIP_H */

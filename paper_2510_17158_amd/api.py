@@ -1,0 +1,224 @@
+"""ctypes binding of libgrpo_hip.so (declared in include/grpo_hip.h).
+
+Argument marshalling only: every step of the hot path runs in the library's
+HIP kernels.  torch supplies device memory (tensors on ``cuda``) and the
+stream; nothing here computes.  The functions keep the C names without the
+``grpo_`` prefix and raise ``GrpoError`` on a negative status.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+import torch
+
+from .workloads import DTYPE_F32, ModelConfig
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgrpo_hip.so")
+
+OK, INVALID_ARG, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP_ERROR, KV_CAPACITY = 0, -1, -2, -3, -4, -5
+OP_PREFILL, OP_ROLLOUT, OP_SCORE, OP_LOSS = 0, 1, 2, 3
+
+
+class GrpoError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"grpo status {code}: {msg}")
+        self.code = code
+
+
+class Config(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_ffn", C.c_int32),
+                ("vocab", C.c_int32), ("rms_eps", C.c_float), ("rope_theta", C.c_float),
+                ("dtype", C.c_int32)]
+
+
+_PP = C.POINTER(C.c_void_p)
+
+
+class Weights(C.Structure):
+    _fields_ = [("tok_emb", C.c_void_p), ("attn_norm", _PP), ("wq", _PP), ("wk", _PP),
+                ("wv", _PP), ("wo", _PP), ("mlp_norm", _PP), ("w_gate", _PP), ("w_up", _PP),
+                ("w_down", _PP), ("final_norm", C.c_void_p), ("lm_head", C.c_void_p)]
+
+
+class Sampling(C.Structure):
+    _fields_ = [("temperature", C.c_float), ("top_k", C.c_int32), ("seed", C.c_uint64)]
+
+
+_lib = None
+
+_VP, _I32, _F32, _SZ = C.c_void_p, C.c_int32, C.c_float, C.c_size_t
+_SIGS = {
+    "grpo_model_create": (_I32, [C.POINTER(Config), C.POINTER(Weights), C.POINTER(_VP)]),
+    "grpo_model_destroy": (_I32, [_VP]),
+    "grpo_kv_cache_bytes": (_SZ, [C.POINTER(Config), _I32, _I32]),
+    "grpo_workspace_bytes": (_SZ, [_VP, _I32, _I32, _I32]),
+    "grpo_last_error": (C.c_char_p, []),
+    "grpo_prefill": (_I32, [_VP, _VP, _I32, _I32, _VP, _I32, _I32, _I32, C.POINTER(Sampling),
+                            _VP, _VP, _VP, _VP, _SZ, _VP]),
+    "grpo_rollout_step": (_I32, [_VP, _VP, _I32, _I32, _I32, _VP, _VP, _I32, _I32, _I32,
+                                 C.POINTER(Sampling), _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
+    "grpo_score_sequences": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _VP, _VP, _SZ, _VP]),
+    "grpo_advantages": (_I32, [_VP, _I32, _I32, _F32, _VP, _VP]),
+    "grpo_token_loss": (_I32, [_VP, _VP, _VP, _VP, _VP, _I32, _I32, _F32, _F32, _I32, _VP, _VP,
+                               _VP, _VP, _VP, _SZ, _VP]),
+}
+
+
+def lib() -> C.CDLL:
+    """The in-tree HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} missing: run __graft_entry__.build() first")
+        L = C.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype, f.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != OK:
+        raise GrpoError(rc, lib().grpo_last_error().decode())
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if isinstance(t, torch.Tensor):
+        if t.device.type != "cuda":
+            raise ValueError("device tensors only")
+        if not t.is_contiguous():
+            raise ValueError("contiguous tensors only")
+        return t.data_ptr()
+    return int(t)
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return int(getattr(stream, "cuda_stream", stream))
+
+
+def config_struct(cfg: ModelConfig) -> Config:
+    return Config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.d_ffn,
+                  cfg.vocab, cfg.rms_eps, cfg.rope_theta, cfg.dtype)
+
+
+def upload_weights(cfg: ModelConfig, host: dict, device="cuda") -> dict:
+    """Host weights (uint16 bf16 bits or float32) -> device tensors of the model dtype."""
+    out = {}
+    for k, a in host.items():
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            t = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16)
+        else:
+            t = torch.from_numpy(a.astype(np.float32, copy=False))
+        out[k] = t.to(device, non_blocking=False)
+    return out
+
+
+class Model:
+    """A model handle over device weight tensors (which it keeps alive)."""
+
+    def __init__(self, cfg: ModelConfig, weights: dict):
+        self.cfg = cfg
+        self.weights = weights
+        L = cfg.n_layers
+
+        def arr(t):
+            a = (C.c_void_p * L)(*[_ptr(weights[f"l{i}.{t}"]) for i in range(L)])
+            return a
+
+        self._arrays = {t: arr(t) for t in ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm",
+                                            "w_gate", "w_up", "w_down")}
+        cast = lambda a: C.cast(a, _PP)  # noqa: E731
+        w = Weights(_ptr(weights["tok_emb"]), *[cast(self._arrays[t]) for t in (
+            "attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down")],
+            _ptr(weights["final_norm"]), _ptr(weights["lm_head"]))
+        self._cfg_s = config_struct(cfg)
+        h = C.c_void_p()
+        _check(lib().grpo_model_create(C.byref(self._cfg_s), C.byref(w), C.byref(h)))
+        self.handle = h
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().grpo_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def act_dtype(self):
+        return torch.float32 if self.cfg.dtype == DTYPE_F32 else torch.bfloat16
+
+
+def kv_cache_bytes(cfg: ModelConfig, n_seqs: int, max_len: int) -> int:
+    return lib().grpo_kv_cache_bytes(C.byref(config_struct(cfg)), n_seqs, max_len)
+
+
+def workspace_bytes(model: Model | None, op: int, n_rows: int, seq_len: int) -> int:
+    return lib().grpo_workspace_bytes(model.handle if model else None, op, n_rows, seq_len)
+
+
+def alloc_workspace(model: Model | None, op: int, n_rows: int, seq_len: int, device="cuda"):
+    n = workspace_bytes(model, op, n_rows, seq_len)
+    if n == 0:
+        raise GrpoError(INVALID_ARG, "workspace size query failed")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def alloc_kv(cfg: ModelConfig, n_seqs: int, max_len: int, device="cuda"):
+    n = kv_cache_bytes(cfg, n_seqs, max_len)
+    if n == 0:
+        raise GrpoError(INVALID_ARG, "kv size query failed")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def prefill(model: Model, kv, n_seqs: int, max_len: int, prompts, G: int, sampling: Sampling,
+            tok_out, logp_out, logits_dbg=None, ws=None, stream=None):
+    P, Tp = prompts.shape
+    _check(lib().grpo_prefill(model.handle, _ptr(kv), n_seqs, max_len, _ptr(prompts), P, Tp, G,
+                              C.byref(sampling), _ptr(tok_out), _ptr(logp_out), _ptr(logits_dbg),
+                              _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def rollout_step(model: Model, kv, n_seqs: int, max_len: int, pos, tok, max_pos: int, step0: int,
+                 n_steps: int, sampling: Sampling, tok_out, logp_out, logits_dbg=None,
+                 hidden_dbg=None, ws=None, stream=None):
+    B = pos.numel()
+    _check(lib().grpo_rollout_step(model.handle, _ptr(kv), n_seqs, max_len, B, _ptr(pos),
+                                   _ptr(tok), max_pos, step0, n_steps, C.byref(sampling),
+                                   _ptr(tok_out), _ptr(logp_out), _ptr(logits_dbg),
+                                   _ptr(hidden_dbg), _ptr(ws), ws.numel() if ws is not None else 0,
+                                   _stream(stream)))
+
+
+def score_sequences(model: Model, tokens, score_from: int, temperature: float, logp_out, ws=None,
+                    stream=None):
+    N, T = tokens.shape
+    _check(lib().grpo_score_sequences(model.handle, _ptr(tokens), N, T, score_from, temperature,
+                                      _ptr(logp_out), _ptr(ws),
+                                      ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def advantages(rewards, P: int, G: int, eps: float, adv_out, stream=None):
+    _check(lib().grpo_advantages(_ptr(rewards), P, G, eps, _ptr(adv_out), _stream(stream)))
+
+
+def token_loss(logp, logp_old, logp_ref, mask, adv, clip_eps: float, beta: float, agg: int,
+               loss_out, tok_loss=None, dloss_dlogp=None, stats=None, ws=None, stream=None):
+    N, Tr = logp.shape
+    _check(lib().grpo_token_loss(_ptr(logp), _ptr(logp_old), _ptr(logp_ref), _ptr(mask), _ptr(adv),
+                                 N, Tr, clip_eps, beta, agg, _ptr(loss_out), _ptr(tok_loss),
+                                 _ptr(dloss_dlogp), _ptr(stats), _ptr(ws),
+                                 ws.numel() if ws is not None else 0, _stream(stream)))

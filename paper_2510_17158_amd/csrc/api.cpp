@@ -1,0 +1,553 @@
+// libgrpo_hip: the C-ABI of include/grpo_hip.h.
+//
+// Host side only: argument validation (before anything is enqueued), workspace
+// layout, and the order in which the kernels of kernels.h run for prefill,
+// decode steps, scoring and the GRPO loss.  No device memory is allocated here.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "grpo_hip.h"
+#include "kernels.h"
+
+using namespace grpo;
+
+struct grpo_model {
+  grpo_config cfg;
+  const void* tok_emb;
+  std::vector<const void*> attn_norm, wq, wk, wv, wo, mlp_norm, w_gate, w_up, w_down;
+  const void* final_norm;
+  const void* lm_head;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIPCHK(expr)                                                                  \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess) return fail(GRPO_HIP_ERROR, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int kSkinnyMax = 128;        // rows handled by the decode GEMM
+constexpr int kSkinnyTargetWGs = 512;  // split-K target grid of the decode GEMM
+constexpr int kScoreTokens = 65536;    // rows per scoring chunk (sequences * T)
+constexpr size_t kLogitBytes = size_t(1) << 30;  // LM-head logits per scoring sub-chunk
+
+// bump allocator over the caller's workspace; base == nullptr only measures
+struct Bump {
+  char* base;
+  size_t off = 0;
+  explicit Bump(void* b) : base((char*)b) {}
+  template <class T>
+  T* take(size_t n) {
+    if (n == 0) return nullptr;
+    off = (off + 255) & ~size_t(255);
+    T* p = base ? (T*)(base + off) : nullptr;
+    off += n * sizeof(T);
+    return p;
+  }
+};
+
+int esize(const grpo_config& c) { return c.dtype == GRPO_F32 ? 4 : 2; }
+int qdim(const grpo_config& c) { return c.n_heads * c.head_dim; }
+int kvdim(const grpo_config& c) { return c.n_kv_heads * c.head_dim; }
+
+int check_config(const grpo_config* c) {
+  if (!c) return fail(GRPO_INVALID_ARG, "config is NULL");
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_heads < 1 || c->n_kv_heads < 1 ||
+      c->head_dim < 1 || c->d_ffn < 1 || c->vocab < 1)
+    return fail(GRPO_INVALID_ARG, "config sizes must be positive");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f))
+    return fail(GRPO_INVALID_ARG, "rms_eps must be >= 0 and rope_theta > 0");
+  if (c->dtype != GRPO_F32 && c->dtype != GRPO_BF16)
+    return fail(GRPO_UNSUPPORTED, "dtype %d is neither GRPO_F32 nor GRPO_BF16", c->dtype);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(GRPO_UNSUPPORTED, "head_dim %d not in {64, 128}", c->head_dim);
+  if (c->n_heads % c->n_kv_heads)
+    return fail(GRPO_UNSUPPORTED, "n_heads %d not a multiple of n_kv_heads %d", c->n_heads,
+                c->n_kv_heads);
+  if (c->n_heads / c->n_kv_heads > 8)
+    return fail(GRPO_UNSUPPORTED, "more than 8 query heads per kv head");
+  const int mult = c->dtype == GRPO_F32 ? 32 : 128;
+  if (c->d_model % mult || qdim(*c) % mult || c->d_ffn % mult)
+    return fail(GRPO_UNSUPPORTED, "d_model, n_heads*head_dim and d_ffn must be multiples of %d",
+                mult);
+  return GRPO_OK;
+}
+
+struct Layer {
+  void* k;
+  void* v;
+};
+Layer kv_layer(const grpo_model* m, void* kv, int l, int n_seqs, int max_len) {
+  const grpo_config& c = m->cfg;
+  const size_t per = (size_t)n_seqs * c.n_kv_heads * max_len * c.head_dim * esize(c);
+  char* base = (char*)kv + (size_t)l * 2 * per;
+  return Layer{base, base + per};
+}
+
+// ---- one GEMM: fp32 path, decode GEMM for few rows, tiled otherwise ----
+struct GemmScratch {
+  float* part;
+  int* counters;
+};
+
+int run_gemm(const grpo_model* m, const void* X, int ldx, int M, WStack W, int N, int K, int epi,
+             EpiArgs ep, GemmScratch s, hipStream_t st) {
+  hipError_t e;
+  if (m->cfg.dtype == GRPO_F32) {
+    e = gemm_f32((const float*)X, ldx, M, W, N, K, epi, ep, st);
+  } else if (M <= kSkinnyMax) {
+    const SkinnyPlan p = skinny_plan(M, N, K, epi, kSkinnyTargetWGs);
+    e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, N, K, epi, ep, p, s.part, s.counters, st);
+  } else {
+    e = gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, N, K, epi, ep, st);
+  }
+  if (e != hipSuccess) return fail(GRPO_HIP_ERROR, "GEMM launch failed: %s", hipGetErrorString(e));
+  return GRPO_OK;
+}
+
+// scratch of the decode GEMM for up to B rows, over every GEMM shape of the model
+void skinny_scratch(const grpo_config& c, int B, size_t* part, size_t* counters) {
+  *part = 0;
+  *counters = 0;
+  if (c.dtype == GRPO_F32) return;
+  const int d = c.d_model, f = c.d_ffn;
+  const int shapes[5][3] = {{qdim(c) + 2 * kvdim(c), d, EPI_STORE},
+                            {d, qdim(c), EPI_RESID},
+                            {f, d, EPI_SWIGLU},
+                            {d, f, EPI_RESID},
+                            {c.vocab, d, EPI_STORE}};
+  const int bmax = std::min(std::max(B, 1), kSkinnyMax);
+  const int nbmax = bmax <= 16 ? 16 : bmax <= 32 ? 32 : bmax <= 64 ? 64 : 128;
+  for (int rows = 16; rows <= nbmax; rows *= 2) {
+    for (auto& sh : shapes) {
+      const SkinnyPlan p = skinny_plan(rows, sh[0], sh[1], sh[2], kSkinnyTargetWGs);
+      *part = std::max(*part, p.part_floats);
+      *counters = std::max(*counters, (size_t)p.counters);
+    }
+  }
+}
+
+// ---- workspace layouts ----
+struct StepWS {   // activations of `rows` token rows
+  float* x; void* h; float* qkv; void* q; void* o; void* a;
+  GemmScratch g;
+};
+
+StepWS take_step(Bump& b, const grpo_config& c, int rows, int gemm_rows) {
+  StepWS w;
+  const int es = esize(c);
+  w.x = b.take<float>((size_t)rows * c.d_model);
+  w.h = b.take<char>((size_t)rows * c.d_model * es);
+  w.qkv = b.take<float>((size_t)rows * (qdim(c) + 2 * kvdim(c)));
+  w.q = b.take<char>((size_t)rows * qdim(c) * es);
+  w.o = b.take<char>((size_t)rows * qdim(c) * es);
+  w.a = b.take<char>((size_t)rows * c.d_ffn * es);
+  size_t part, cnt;
+  skinny_scratch(c, gemm_rows, &part, &cnt);
+  w.g.part = b.take<float>(part);
+  w.g.counters = b.take<int>(cnt + 1);
+  return w;
+}
+
+struct RolloutWS {
+  StepWS s;
+  float* logits;
+  float* attn_part;
+  size_t n_counters;
+};
+RolloutWS take_rollout(Bump& b, const grpo_config& c, int B, int max_len) {
+  RolloutWS w;
+  w.s = take_step(b, c, B, B);
+  w.logits = b.take<float>((size_t)B * c.vocab);
+  const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.head_dim, max_len);
+  w.attn_part = b.take<float>(c.dtype == GRPO_F32 ? 0 : ap.part_floats);
+  size_t part, cnt;
+  skinny_scratch(c, B, &part, &cnt);
+  w.n_counters = cnt + 1;
+  return w;
+}
+
+struct PrefillWS {
+  StepWS s;
+  uint16_t* vt;
+  void* hl;
+  float* logits;
+  size_t n_counters;
+};
+int round8(int t) { return (t + 7) / 8 * 8; }
+PrefillWS take_prefill(Bump& b, const grpo_config& c, int P, int Tp) {
+  PrefillWS w;
+  const size_t M = (size_t)P * Tp;
+  w.s = take_step(b, c, (int)M, (int)std::max<size_t>(M, P));
+  w.vt = b.take<uint16_t>(c.dtype == GRPO_F32 ? 0 : (size_t)P * kvdim(c) * round8(Tp));
+  w.hl = b.take<char>((size_t)P * c.d_model * esize(c));
+  w.logits = b.take<float>((size_t)P * c.vocab);
+  size_t part, cnt;
+  skinny_scratch(c, (int)std::max<size_t>(M, P), &part, &cnt);
+  w.n_counters = cnt + 1;
+  return w;
+}
+
+struct ScoreWS {
+  int chunk;         // sequences per chunk
+  int sub_rows;      // LM-head rows per logits sub-chunk
+  StepWS s;
+  void* kbuf; void* vbuf; uint16_t* vt;
+  void* hs;
+  float* logits;
+  size_t n_counters;
+};
+ScoreWS take_score(Bump& b, const grpo_config& c, int N, int T) {
+  ScoreWS w;
+  w.chunk = std::max(1, std::min(N, kScoreTokens / std::max(T, 1)));
+  const size_t M = (size_t)w.chunk * T;
+  w.sub_rows = (int)std::max<size_t>(64, std::min<size_t>(8192, kLogitBytes / ((size_t)c.vocab * 4)));
+  w.s = take_step(b, c, (int)M, (int)std::max<size_t>(M, w.sub_rows));
+  const size_t kvn = (size_t)w.chunk * kvdim(c) * T;
+  w.kbuf = b.take<char>(kvn * esize(c));
+  w.vbuf = b.take<char>(c.dtype == GRPO_F32 ? kvn * 4 : 0);
+  w.vt = b.take<uint16_t>(c.dtype == GRPO_F32 ? 0 : (size_t)w.chunk * kvdim(c) * round8(T));
+  w.hs = b.take<char>((size_t)w.sub_rows * c.d_model * esize(c));
+  w.logits = b.take<float>((size_t)w.sub_rows * c.vocab);
+  size_t part, cnt;
+  skinny_scratch(c, (int)std::max<size_t>(M, w.sub_rows), &part, &cnt);
+  w.n_counters = cnt + 1;
+  return w;
+}
+
+WStack qkv_stack(const grpo_model* m, int l) {
+  const grpo_config& c = m->cfg;
+  return WStack{{m->wq[l], m->wk[l], m->wv[l]}, qdim(c), qdim(c) + kvdim(c)};
+}
+WStack one(const void* w) { return WStack{{w, w, w}, 0x7fffffff, 0x7fffffff}; }
+WStack gate_up(const grpo_model* m, int l) {
+  return WStack{{m->w_gate[l], m->w_up[l], m->w_up[l]}, m->cfg.d_ffn, 2 * m->cfg.d_ffn};
+}
+
+// Layers of a many-row forward (prefill or scoring).  Rows are sequence-major
+// (row = seq * T + t).  K/V go to kc/vc (cache layout with n_slots slots of
+// k_len positions; sequence s at slot s * G) and V also transposed to vt.
+int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slots, int k_len,
+                 void* kv_or_null, void* kbuf, void* vbuf, uint16_t* vt, hipStream_t st) {
+  const grpo_config& c = m->cfg;
+  const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
+  const int N = M / T;
+  for (int l = 0; l < c.n_layers; ++l) {
+    void *kl = kbuf, *vl = vbuf;
+    if (kv_or_null) {
+      Layer L = kv_layer(m, kv_or_null, l, n_slots, k_len);
+      kl = L.k;
+      vl = L.v;
+    }
+    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), m->attn_norm[l], M, d, c.rms_eps, w.h, d,
+                   st));
+    int rc = run_gemm(m, w.h, d, M, qkv_stack(m, l), qd + 2 * kvd, d, EPI_STORE,
+                      EpiArgs{w.qkv, nullptr, qd + 2 * kvd}, w.g, st);
+    if (rc) return rc;
+    RopeArgs ra{};
+    ra.mode = 1; ra.T = T; ra.G = G; ra.pos_arr = nullptr;
+    ra.n_heads = c.n_heads; ra.n_kv = c.n_kv_heads; ra.hd = c.head_dim; ra.theta = c.rope_theta;
+    ra.kcache = kl; ra.vcache = vl; ra.n_seqs = n_slots; ra.max_len = k_len;
+    ra.vt = vt; ra.vt_len = round8(T);
+    HIPCHK(rope_kv(c.dtype, w.qkv, M, w.q, ra, st));
+    HIPCHK(attn_prefill(c.dtype, w.q, kl, c.dtype == GRPO_F32 ? vl : (const void*)vt, N, T,
+                        c.n_heads, c.n_kv_heads, c.head_dim, k_len, G, w.o, st));
+    rc = run_gemm(m, w.o, qd, M, one(m->wo[l]), d, qd, EPI_RESID, EpiArgs{w.x, nullptr, d}, w.g,
+                  st);
+    if (rc) return rc;
+    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), m->mlp_norm[l], M, d, c.rms_eps, w.h, d,
+                   st));
+    rc = run_gemm(m, w.h, d, M, gate_up(m, l), f, d, EPI_SWIGLU, EpiArgs{nullptr, w.a, f}, w.g, st);
+    if (rc) return rc;
+    rc = run_gemm(m, w.a, f, M, one(m->w_down[l]), d, f, EPI_RESID, EpiArgs{w.x, nullptr, d}, w.g,
+                  st);
+    if (rc) return rc;
+  }
+  return GRPO_OK;
+}
+
+int check_sampling(const grpo_sampling* s, int vocab) {
+  if (!s) return fail(GRPO_INVALID_ARG, "sampling is NULL");
+  if (!(s->temperature >= 0.f) || s->temperature == INFINITY)
+    return fail(GRPO_INVALID_ARG, "temperature must be finite and >= 0");
+  if (s->top_k < 0 || s->top_k > vocab) return fail(GRPO_INVALID_ARG, "top_k outside [0, vocab]");
+  return GRPO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* grpo_last_error(void) { return g_err.c_str(); }
+
+int grpo_model_create(const grpo_config* cfg, const grpo_weights* w, grpo_model** out) {
+  if (!out) return fail(GRPO_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (int rc = check_config(cfg)) return rc;
+  if (!w) return fail(GRPO_INVALID_ARG, "weights is NULL");
+  if (!w->tok_emb || !w->final_norm || !w->lm_head)
+    return fail(GRPO_INVALID_ARG, "tok_emb, final_norm and lm_head must be set");
+  const void* const* arrays[9] = {w->attn_norm, w->wq, w->wk, w->wv, w->wo,
+                                  w->mlp_norm, w->w_gate, w->w_up, w->w_down};
+  for (auto a : arrays) {
+    if (!a) return fail(GRPO_INVALID_ARG, "a per-layer weight array is NULL");
+    for (int l = 0; l < cfg->n_layers; ++l)
+      if (!a[l]) return fail(GRPO_INVALID_ARG, "layer %d has a NULL weight pointer", l);
+  }
+  grpo_model* m = new grpo_model;
+  m->cfg = *cfg;
+  m->tok_emb = w->tok_emb;
+  m->final_norm = w->final_norm;
+  m->lm_head = w->lm_head;
+  std::vector<const void*>* dst[9] = {&m->attn_norm, &m->wq, &m->wk, &m->wv, &m->wo,
+                                      &m->mlp_norm, &m->w_gate, &m->w_up, &m->w_down};
+  for (int i = 0; i < 9; ++i) dst[i]->assign(arrays[i], arrays[i] + cfg->n_layers);
+  *out = m;
+  g_err.clear();
+  return GRPO_OK;
+}
+
+int grpo_model_destroy(grpo_model* m) {
+  delete m;
+  return GRPO_OK;
+}
+
+size_t grpo_kv_cache_bytes(const grpo_config* cfg, int32_t n_seqs, int32_t max_len) {
+  if (check_config(cfg) || n_seqs < 1 || max_len < 1) return 0;
+  return (size_t)cfg->n_layers * 2 * n_seqs * cfg->n_kv_heads * max_len * cfg->head_dim *
+         esize(*cfg);
+}
+
+size_t grpo_workspace_bytes(const grpo_model* m, int32_t op, int32_t n_rows, int32_t seq_len) {
+  if (n_rows < 1 || seq_len < 1) return 0;
+  Bump b(nullptr);
+  if (op == GRPO_OP_LOSS) {
+    b.take<double>((size_t)n_rows * 9);
+    return b.off;
+  }
+  if (!m) return 0;
+  switch (op) {
+    case GRPO_OP_PREFILL: take_prefill(b, m->cfg, n_rows, seq_len); break;
+    case GRPO_OP_ROLLOUT: take_rollout(b, m->cfg, n_rows, seq_len); break;
+    case GRPO_OP_SCORE: take_score(b, m->cfg, n_rows, seq_len); break;
+    default: return 0;
+  }
+  return b.off;
+}
+
+int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
+                 const int32_t* prompts, int32_t P, int32_t Tp, int32_t G, const grpo_sampling* s,
+                 int32_t* tok_out, float* logp_out, float* logits_dbg, void* ws, size_t ws_bytes,
+                 void* stream) {
+  if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
+  const grpo_config& c = m->cfg;
+  if (!kv || !prompts || !tok_out || !logp_out || !ws)
+    return fail(GRPO_INVALID_ARG, "kv, prompts, tok_out, logp_out and ws must be set");
+  if (P < 1 || Tp < 1 || G < 1) return fail(GRPO_INVALID_ARG, "P, Tp and G must be >= 1");
+  if ((long)P * G > n_seqs) return fail(GRPO_INVALID_ARG, "P*G = %ld exceeds n_seqs %d", (long)P * G, n_seqs);
+  if (Tp > max_len) return fail(GRPO_KV_CAPACITY, "prompt length %d exceeds max_len %d", Tp, max_len);
+  if ((long)P * Tp > (1L << 30)) return fail(GRPO_UNSUPPORTED, "P*Tp too large");
+  if (c.dtype == GRPO_F32 && Tp > 16384) return fail(GRPO_UNSUPPORTED, "fp32 prompts above 16384");
+  if (int rc = check_sampling(s, c.vocab)) return rc;
+  const size_t need = grpo_workspace_bytes(m, GRPO_OP_PREFILL, P, Tp);
+  if (ws_bytes < need)
+    return fail(GRPO_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
+  hipStream_t st = (hipStream_t)stream;
+  Bump b(ws);
+  PrefillWS w = take_prefill(b, c, P, Tp);
+  const int M = P * Tp, d = c.d_model;
+  HIPCHK(fill_i32(w.s.g.counters, w.n_counters, 0, st));
+  HIPCHK(embed(c.dtype, m->tok_emb, prompts, M, d, c.vocab, w.s.x, st));
+  if (int rc = forward_rows(m, w.s, M, Tp, G, n_seqs, max_len, kv, nullptr, nullptr, w.vt, st))
+    return rc;
+  HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{0, 1, Tp, Tp - 1}, m->final_norm, P, d, c.rms_eps, w.hl,
+                 d, st));
+  if (int rc = run_gemm(m, w.hl, d, P, one(m->lm_head), c.vocab, d, EPI_STORE,
+                        EpiArgs{w.logits, nullptr, c.vocab}, w.s.g, st))
+    return rc;
+  SampleArgs sa{};
+  sa.temperature = s->temperature; sa.top_k = s->top_k; sa.seed = s->seed; sa.step = 0;
+  sa.G = G; sa.tok_out = tok_out; sa.logp_out = logp_out; sa.out_stride = 1;
+  HIPCHK(sample(w.logits, P, c.vocab, c.vocab, sa, st));
+  if (logits_dbg)
+    HIPCHK(hipMemcpyAsync(logits_dbg, w.logits, (size_t)P * c.vocab * 4, hipMemcpyDeviceToDevice, st));
+  g_err.clear();
+  return GRPO_OK;
+}
+
+int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len, int32_t B,
+                      int32_t* pos, int32_t* tok, int32_t max_pos, int32_t step0, int32_t n_steps,
+                      const grpo_sampling* s, int32_t* tok_out, float* logp_out,
+                      float* logits_dbg, float* hidden_dbg, void* ws, size_t ws_bytes,
+                      void* stream) {
+  if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
+  const grpo_config& c = m->cfg;
+  if (!kv || !pos || !tok || !tok_out || !logp_out || !ws)
+    return fail(GRPO_INVALID_ARG, "kv, pos, tok, tok_out, logp_out and ws must be set");
+  if (B < 1 || n_steps < 1 || max_len < 1) return fail(GRPO_INVALID_ARG, "B, n_steps, max_len must be >= 1");
+  if (B > n_seqs) return fail(GRPO_INVALID_ARG, "B %d exceeds n_seqs %d", B, n_seqs);
+  if (max_pos < 0 || step0 < 0) return fail(GRPO_INVALID_ARG, "max_pos and step0 must be >= 0");
+  if ((long)max_pos + n_steps > max_len)
+    return fail(GRPO_KV_CAPACITY, "max_pos %d + n_steps %d exceeds max_len %d", max_pos, n_steps,
+                max_len);
+  if (c.dtype == GRPO_F32 && max_len > 16384) return fail(GRPO_UNSUPPORTED, "fp32 caches above 16384");
+  if (int rc = check_sampling(s, c.vocab)) return rc;
+  const size_t need = grpo_workspace_bytes(m, GRPO_OP_ROLLOUT, B, max_len);
+  if (ws_bytes < need)
+    return fail(GRPO_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
+  hipStream_t st = (hipStream_t)stream;
+  Bump b(ws);
+  RolloutWS w = take_rollout(b, c, B, max_len);
+  const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
+  const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.head_dim, max_len);
+  HIPCHK(fill_i32(w.s.g.counters, w.n_counters, 0, st));
+  for (int step = 0; step < n_steps; ++step) {
+    const bool last = step == n_steps - 1;
+    HIPCHK(embed(c.dtype, m->tok_emb, tok, B, d, c.vocab, w.s.x, st));
+    for (int l = 0; l < c.n_layers; ++l) {
+      if (last && hidden_dbg)
+        HIPCHK(hipMemcpyAsync(hidden_dbg + (size_t)l * B * d, w.s.x, (size_t)B * d * 4,
+                              hipMemcpyDeviceToDevice, st));
+      Layer L = kv_layer(m, kv, l, n_seqs, max_len);
+      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), m->attn_norm[l], B, d, c.rms_eps,
+                     w.s.h, d, st));
+      if (int rc = run_gemm(m, w.s.h, d, B, qkv_stack(m, l), qd + 2 * kvd, d, EPI_STORE,
+                            EpiArgs{w.s.qkv, nullptr, qd + 2 * kvd}, w.s.g, st))
+        return rc;
+      RopeArgs ra{};
+      ra.mode = 0; ra.T = 1; ra.G = 1; ra.pos_arr = pos;
+      ra.n_heads = c.n_heads; ra.n_kv = c.n_kv_heads; ra.hd = c.head_dim; ra.theta = c.rope_theta;
+      ra.kcache = L.k; ra.vcache = L.v; ra.n_seqs = n_seqs; ra.max_len = max_len;
+      ra.vt = nullptr; ra.vt_len = 0;
+      HIPCHK(rope_kv(c.dtype, w.s.qkv, B, w.s.q, ra, st));
+      HIPCHK(attn_decode(c.dtype, w.s.q, L.k, L.v, pos, B, c.n_heads, c.n_kv_heads, c.head_dim,
+                         n_seqs, max_len, ap, w.attn_part, w.s.o, st));
+      if (int rc = run_gemm(m, w.s.o, qd, B, one(m->wo[l]), d, qd, EPI_RESID,
+                            EpiArgs{w.s.x, nullptr, d}, w.s.g, st))
+        return rc;
+      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), m->mlp_norm[l], B, d, c.rms_eps,
+                     w.s.h, d, st));
+      if (int rc = run_gemm(m, w.s.h, d, B, gate_up(m, l), f, d, EPI_SWIGLU,
+                            EpiArgs{nullptr, w.s.a, f}, w.s.g, st))
+        return rc;
+      if (int rc = run_gemm(m, w.s.a, f, B, one(m->w_down[l]), d, f, EPI_RESID,
+                            EpiArgs{w.s.x, nullptr, d}, w.s.g, st))
+        return rc;
+    }
+    if (last && hidden_dbg)
+      HIPCHK(hipMemcpyAsync(hidden_dbg + (size_t)c.n_layers * B * d, w.s.x, (size_t)B * d * 4,
+                            hipMemcpyDeviceToDevice, st));
+    HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), m->final_norm, B, d, c.rms_eps, w.s.h, d,
+                   st));
+    if (int rc = run_gemm(m, w.s.h, d, B, one(m->lm_head), c.vocab, d, EPI_STORE,
+                          EpiArgs{w.logits, nullptr, c.vocab}, w.s.g, st))
+      return rc;
+    SampleArgs sa{};
+    sa.temperature = s->temperature; sa.top_k = s->top_k; sa.seed = s->seed;
+    sa.step = step0 + step; sa.G = 1;
+    sa.tok_out = tok_out + step; sa.logp_out = logp_out + step; sa.out_stride = n_steps;
+    sa.tok_state = tok; sa.pos_state = pos;
+    HIPCHK(sample(w.logits, B, c.vocab, c.vocab, sa, st));
+    if (last && logits_dbg)
+      HIPCHK(hipMemcpyAsync(logits_dbg, w.logits, (size_t)B * c.vocab * 4,
+                            hipMemcpyDeviceToDevice, st));
+  }
+  g_err.clear();
+  return GRPO_OK;
+}
+
+int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, int32_t T,
+                         int32_t score_from, float temperature, float* logp_out, void* ws,
+                         size_t ws_bytes, void* stream) {
+  if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
+  const grpo_config& c = m->cfg;
+  if (!tokens || !logp_out || !ws) return fail(GRPO_INVALID_ARG, "tokens, logp_out and ws must be set");
+  if (N < 1 || T < 2) return fail(GRPO_INVALID_ARG, "N must be >= 1 and T >= 2");
+  if (score_from < 1 || score_from >= T)
+    return fail(GRPO_INVALID_ARG, "score_from %d outside [1, T)", score_from);
+  if (!(temperature >= 0.f) || temperature == INFINITY)
+    return fail(GRPO_INVALID_ARG, "temperature must be finite and >= 0");
+  if (c.dtype == GRPO_F32 && T > 16384) return fail(GRPO_UNSUPPORTED, "fp32 sequences above 16384");
+  if ((long)T > kScoreTokens) return fail(GRPO_UNSUPPORTED, "T above %d", kScoreTokens);
+  const size_t need = grpo_workspace_bytes(m, GRPO_OP_SCORE, N, T);
+  if (ws_bytes < need)
+    return fail(GRPO_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
+  hipStream_t st = (hipStream_t)stream;
+  Bump b(ws);
+  ScoreWS w = take_score(b, c, N, T);
+  const int d = c.d_model, Ts = T - score_from;
+  HIPCHK(fill_i32(w.s.g.counters, w.n_counters, 0, st));
+  for (int n0 = 0; n0 < N; n0 += w.chunk) {
+    const int C = std::min(w.chunk, N - n0);
+    const int M = C * T;
+    const int32_t* tk = tokens + (size_t)n0 * T;
+    HIPCHK(embed(c.dtype, m->tok_emb, tk, M, d, c.vocab, w.s.x, st));
+    if (int rc = forward_rows(m, w.s, M, T, 1, C, T, nullptr, w.kbuf,
+                              c.dtype == GRPO_F32 ? w.vbuf : nullptr, w.vt, st))
+      return rc;
+    const int R = C * Ts;
+    for (int i0 = 0; i0 < R; i0 += w.sub_rows) {
+      const int rc_rows = std::min(w.sub_rows, R - i0);
+      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{i0, Ts, T, score_from - 1}, m->final_norm, rc_rows,
+                     d, c.rms_eps, w.hs, d, st));
+      if (int rc = run_gemm(m, w.hs, d, rc_rows, one(m->lm_head), c.vocab, d, EPI_STORE,
+                            EpiArgs{w.logits, nullptr, c.vocab}, w.s.g, st))
+        return rc;
+      HIPCHK(token_logprob(w.logits, rc_rows, c.vocab, c.vocab, tk, T, score_from, Ts, i0,
+                           temperature, logp_out + (size_t)n0 * Ts + i0, st));
+    }
+  }
+  g_err.clear();
+  return GRPO_OK;
+}
+
+int grpo_advantages(const float* rewards, int32_t P, int32_t G, float eps, float* adv_out,
+                    void* stream) {
+  if (!rewards || !adv_out) return fail(GRPO_INVALID_ARG, "rewards and adv_out must be set");
+  if (P < 1) return fail(GRPO_INVALID_ARG, "P must be >= 1");
+  if (G < 2) return fail(GRPO_INVALID_ARG, "a group needs G >= 2 samples");
+  if (!(eps >= 0.f)) return fail(GRPO_INVALID_ARG, "eps must be >= 0");
+  HIPCHK(advantages(rewards, P, G, eps, adv_out, (hipStream_t)stream));
+  g_err.clear();
+  return GRPO_OK;
+}
+
+int grpo_token_loss(const float* logp, const float* logp_old, const float* logp_ref,
+                    const uint8_t* mask, const float* adv, int32_t N, int32_t Tr, float clip_eps,
+                    float beta, int32_t agg, float* loss_out, float* tok_loss, float* dloss_dlogp,
+                    float* stats, void* ws, size_t ws_bytes, void* stream) {
+  if (!logp || !logp_old || !logp_ref || !mask || !adv || !loss_out || !ws)
+    return fail(GRPO_INVALID_ARG, "logp, logp_old, logp_ref, mask, adv, loss_out, ws must be set");
+  if (N < 1 || Tr < 1) return fail(GRPO_INVALID_ARG, "N and Tr must be >= 1");
+  if (!(clip_eps >= 0.f && clip_eps < 1.f)) return fail(GRPO_INVALID_ARG, "clip_eps outside [0, 1)");
+  if (!(beta >= 0.f)) return fail(GRPO_INVALID_ARG, "beta must be >= 0");
+  if (agg != 0 && agg != 1) return fail(GRPO_INVALID_ARG, "agg must be 0 or 1");
+  const size_t need = grpo_workspace_bytes(nullptr, GRPO_OP_LOSS, N, Tr);
+  if (ws_bytes < need)
+    return fail(GRPO_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
+  HIPCHK(token_loss(logp, logp_old, logp_ref, mask, adv, N, Tr, clip_eps, beta, agg, loss_out,
+                    tok_loss, dloss_dlogp, stats, (double*)ws, (hipStream_t)stream));
+  g_err.clear();
+  return GRPO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,160 @@
+// Embedding gather, RMSNorm, rotary embedding + KV-cache write, and the
+// teacher-forced token log-probability.  All are bandwidth-trivial next to the
+// weight and KV streams; they exist as separate kernels so that every rounding
+// point of the precision contract sits in one obvious place.
+#include "common.h"
+#include "kernels.h"
+
+namespace grpo {
+
+namespace {
+
+template <typename T>
+__global__ void k_embed(const T* emb, const int32_t* tok, int d, int vocab, float* x) {
+  const int m = blockIdx.x;
+  const int t = clampi(tok[m], 0, vocab - 1);
+  const T* e = emb + (size_t)t * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) x[(size_t)m * d + i] = ldf(e, i);
+}
+
+// h = round(x * (1 / sqrt(mean(x^2) + eps)) * g); one workgroup per row
+template <typename T>
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* x, int ldx, RowMap rm, const T* g,
+                                                 int d, float eps, T* out, int ldo) {
+  __shared__ float sh[4];
+  const int m = blockIdx.x;
+  const int gi = rm.i0 + m;
+  const size_t src = (size_t)(gi / rm.per) * rm.stride + rm.off + gi % rm.per;
+  const float* xr = x + src * ldx;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) ss = fmaf(xr[i], xr[i], ss);
+  ss = block_sum<256>(ss, sh);
+  const float r = 1.f / sqrtf(ss / (float)d + eps);
+  for (int i = threadIdx.x; i < d; i += 256) stf(out, (size_t)m * ldo + i, xr[i] * r * ldf(g, i));
+}
+
+// one thread per (row, head, rotation pair); q heads first, then k heads, then v
+template <typename T>
+__global__ void k_rope_kv(const float* qkv, int M, T* q_out, RopeArgs a) {
+  const int half = a.hd / 2;
+  const int heads = a.n_heads + 2 * a.n_kv;
+  const size_t total = (size_t)M * heads * half;
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int i = (int)(idx % half);
+  const int h = (int)((idx / half) % heads);
+  const int m = (int)(idx / ((size_t)half * heads));
+  int seq, pos;
+  if (a.mode == 0) { seq = m; pos = a.pos_arr[m]; }
+  else { seq = m / a.T; pos = m % a.T; }
+  const int ldq = heads * a.hd;
+  const float* src = qkv + (size_t)m * ldq + h * a.hd;
+  float lo = src[i], hi = src[i + half];
+  if (h < a.n_heads + a.n_kv) {
+    // angle in fp64: pos * theta^(-2i/hd), then cos/sin rounded to fp32
+    const double inv = pow((double)a.theta, -2.0 * (double)i / (double)a.hd);
+    double sd, cd;
+    sincos((double)pos * inv, &sd, &cd);
+    const float c = (float)cd, s = (float)sd;
+    const float l2 = lo * c - hi * s;
+    const float h2 = hi * c + lo * s;
+    lo = l2; hi = h2;
+  }
+  if (h < a.n_heads) {
+    T* qo = q_out + (size_t)m * a.n_heads * a.hd + h * a.hd;
+    stf(qo, i, lo);
+    stf(qo, i + half, hi);
+    return;
+  }
+  if (pos < 0 || pos >= a.max_len) return;
+  const bool is_v = h >= a.n_heads + a.n_kv;
+  const int g = is_v ? h - a.n_heads - a.n_kv : h - a.n_heads;
+  T* base = (T*)(is_v ? a.vcache : a.kcache);
+  for (int r = 0; base && r < a.G; ++r) {
+    const int slot = seq * a.G + r;
+    if (slot >= a.n_seqs) break;
+    T* dst = base + (((size_t)slot * a.n_kv + g) * a.max_len + pos) * a.hd;
+    stf(dst, i, lo);
+    stf(dst, i + half, hi);
+  }
+  if (is_v && a.vt && pos < a.vt_len) {
+    bf16_t* vt = a.vt + ((size_t)seq * a.n_kv + g) * a.hd * a.vt_len;
+    vt[(size_t)i * a.vt_len + pos] = f2bf(lo);
+    vt[(size_t)(i + half) * a.vt_len + pos] = f2bf(hi);
+  }
+}
+
+__global__ void k_fill_i32(int32_t* p, size_t n, int32_t v) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// logp[r] = z[r, target] - LSE(z[r, :]), one workgroup per row, fp32
+__global__ __launch_bounds__(256) void k_token_logprob(const float* logits, int V, int ld,
+                                                       const int32_t* tokens, int T,
+                                                       int score_from, int Ts, int i0, float temp,
+                                                       float* logp) {
+  __shared__ float sh[4];
+  const int r = blockIdx.x;
+  const int gi = i0 + r;
+  const int tgt = tokens[(size_t)(gi / Ts) * T + score_from + gi % Ts];
+  const float* l = logits + (size_t)r * ld;
+  float mx = -INFINITY;
+  for (int i = threadIdx.x; i < V; i += 256) mx = fmaxf(mx, l[i] / temp);
+  mx = block_max<256>(mx, sh);
+  float s = 0.f;
+  for (int i = threadIdx.x; i < V; i += 256) s += __expf(l[i] / temp - mx);
+  s = block_sum<256>(s, sh);
+  if (threadIdx.x == 0) {
+    const int t = clampi(tgt, 0, V - 1);
+    logp[r] = l[t] / temp - (mx + logf(s));
+  }
+}
+
+}  // namespace
+
+hipError_t embed(int dtype, const void* emb, const int32_t* tok, int M, int d, int vocab, float* x,
+                 hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (dtype == 0) k_embed<float><<<M, 256, 0, st>>>((const float*)emb, tok, d, vocab, x);
+  else k_embed<bf16_t><<<M, 256, 0, st>>>((const bf16_t*)emb, tok, d, vocab, x);
+  return hipGetLastError();
+}
+
+hipError_t rmsnorm(int dtype, const float* x, int ldx, RowMap rows, const void* g, int M, int d,
+                   float eps, void* out, int ldo, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (dtype == 0)
+    k_rmsnorm<float><<<M, 256, 0, st>>>(x, ldx, rows, (const float*)g, d, eps, (float*)out, ldo);
+  else
+    k_rmsnorm<bf16_t><<<M, 256, 0, st>>>(x, ldx, rows, (const bf16_t*)g, d, eps, (bf16_t*)out,
+                                         ldo);
+  return hipGetLastError();
+}
+
+hipError_t fill_i32(int32_t* p, size_t n, int32_t v, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  k_fill_i32<<<(int)((n + 255) / 256), 256, 0, st>>>(p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeArgs& a,
+                   hipStream_t st) {
+  const size_t total = (size_t)M * (a.n_heads + 2 * a.n_kv) * (a.hd / 2);
+  if (total == 0) return hipSuccess;
+  const int grid = (int)((total + 255) / 256);
+  if (dtype == 0) k_rope_kv<float><<<grid, 256, 0, st>>>(qkv, M, (float*)q_out, a);
+  else k_rope_kv<bf16_t><<<grid, 256, 0, st>>>(qkv, M, (bf16_t*)q_out, a);
+  return hipGetLastError();
+}
+
+hipError_t token_logprob(const float* logits, int R, int V, int ld, const int32_t* tokens, int T,
+                         int score_from, int Ts, int i0, float temperature, float* logp,
+                         hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  const float t = temperature > 0.f ? temperature : 1.f;
+  k_token_logprob<<<R, 256, 0, st>>>(logits, V, ld, tokens, T, score_from, Ts, i0, t, logp);
+  return hipGetLastError();
+}
+
+}  // namespace grpo

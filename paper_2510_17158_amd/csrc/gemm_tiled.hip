@@ -1,0 +1,271 @@
+// Tiled GEMM for many rows (prompt prefill and teacher-forced scoring):
+// C[M, N] = X[M, K] . W[N, K]^T, bf16 in, fp32 accumulate, on MFMA.
+//
+// Both operands are K-contiguous, which is the layout the bf16 MFMA wants for
+// both A and B.  A workgroup of 4 waves computes a 128x128 tile (2x2 waves of
+// 64x64, each 4x4 v_mfma_f32_16x16x32_bf16 blocks) over K in steps of 64; the
+// X and W tiles are staged through LDS (rows padded by 16 bytes against bank
+// conflicts), double-buffered, the next tile's global loads in flight while the
+// current one is multiplied.  Output tiles are walked in groups of 8 row-tiles
+// so that neighbouring workgroups share weight tiles in L2.
+//
+// SwiGLU epilogue: each wave's 64 columns are 32 gate rows and the 32 up rows of
+// the same outputs, so silu(gate) * up is formed in registers.
+#include "common.h"
+#include "kernels.h"
+
+namespace grpo {
+
+namespace {
+
+constexpr int NT = 256, BM = 128, BN = 128, BK = 64, LROW = BK + 8;
+
+struct TArgs {
+  const bf16_t* X; int ldx; int M;
+  const bf16_t* w0; const bf16_t* w1; const bf16_t* w2; int n1, n2;
+  int N, K, tiles_m, tiles_n;
+  float* out_f32; bf16_t* out_act; int ld_out;
+};
+
+template <int EPI>
+__device__ __forceinline__ const bf16_t* tile_wrow(const TArgs& a, int tn, int r) {
+  if (EPI == EPI_SWIGLU) {
+    // B-tile row r: wave half wn = r / 64, within it 32 gate rows then 32 up rows
+    const int wn = r >> 6, q = r & 63;
+    const int n = min(tn * 64 + wn * 32 + (q & 31), a.n1 - 1);
+    return (q < 32 ? a.w0 + (size_t)n * a.K : a.w1 + (size_t)n * a.K);
+  }
+  const int n = min(tn * BN + r, a.N - 1);
+  if (n < a.n1) return a.w0 + (size_t)n * a.K;
+  if (n < a.n2) return a.w1 + (size_t)(n - a.n1) * a.K;
+  return a.w2 + (size_t)(n - a.n2) * a.K;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LROW];
+  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * LROW];
+  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // grouped tile order: 8 row-tiles share each column-tile sweep
+  const int bid = blockIdx.x;
+  const int group = 8;
+  const int per_group = group * a.tiles_n;
+  const int g = bid / per_group;
+  const int first_m = g * group;
+  const int gsize = min(a.tiles_m - first_m, group);
+  const int tm = first_m + (bid % per_group) % gsize;
+  const int tn = (bid % per_group) / gsize;
+
+  // loader mapping: 4 x 16-byte loads per operand per thread (128 rows x 64 cols)
+  const bf16_t* ap[4];
+  const bf16_t* bp[4];
+  int lr[4], lc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int e = (tid + i * NT) * 8;
+    lr[i] = e / BK;
+    lc[i] = e % BK;
+    const int m = min(tm * BM + lr[i], a.M - 1);
+    ap[i] = a.X + (size_t)m * a.ldx + lc[i];
+    bp[i] = tile_wrow<EPI>(a, tn, lr[i]) + lc[i];
+  }
+  u32x4_t ra[4], rb[4];
+
+  f32x4_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+
+  const int nk = a.K / BK;
+  {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ra[i] = *(const u32x4_t*)(ap[i] + 0);
+      rb[i] = *(const u32x4_t*)(bp[i] + 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      *(u32x4_t*)(&As[0][lr[i] * LROW + lc[i]]) = ra[i];
+      *(u32x4_t*)(&Bs[0][lr[i] * LROW + lc[i]]) = rb[i];
+    }
+  }
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        ra[i] = *(const u32x4_t*)(ap[i] + (kt + 1) * BK);
+        rb[i] = *(const u32x4_t*)(bp[i] + (kt + 1) * BK);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < BK / 32; ++s) {
+      bf16x8_t af[4], bfr[4];
+      const int col = s * 32 + (lane >> 4) * 8;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[i] = *(const bf16x8_t*)(&As[buf][(wm * 64 + i * 16 + (lane & 15)) * LROW + col]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        bfr[j] = *(const bf16x8_t*)(&Bs[buf][(wn * 64 + j * 16 + (lane & 15)) * LROW + col]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      *(u32x4_t*)(&As[buf ^ 1][lr[i] * LROW + lc[i]]) = ra[i];
+      *(u32x4_t*)(&Bs[buf ^ 1][lr[i] * LROW + lc[i]]) = rb[i];
+    }
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue ----
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int m = tm * BM + wm * 64 + i * 16 + (lane >> 4) * 4 + v;
+      if (m >= a.M) continue;
+      if (EPI == EPI_SWIGLU) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int n = tn * 64 + wn * 32 + j * 16 + (lane & 15);
+          if (n < a.n1) {
+            const float gt = acc[i][j][v], up = acc[i][j + 2][v];
+            a.out_act[(size_t)m * a.ld_out + n] = f2bf(gt / (1.f + __expf(-gt)) * up);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = tn * BN + wn * 64 + j * 16 + (lane & 15);
+          if (n < a.N) {
+            float* o = a.out_f32 + (size_t)m * a.ld_out + n;
+            if (EPI == EPI_RESID) *o += acc[i][j][v];
+            else *o = acc[i][j][v];
+          }
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 GEMM for fp32 models (VALU, 64x64 tiles, 4x4 outputs per thread).
+struct FArgs {
+  const float* X; int ldx; int M;
+  const float* w0; const float* w1; const float* w2; int n1, n2;
+  int N, K, epi;
+  float* out_f32; float* out_act; int ld_out;
+};
+
+__device__ __forceinline__ const float* frow(const FArgs& a, int n) {
+  if (n < a.n1) return a.w0 + (size_t)n * a.K;
+  if (n < a.n2) return a.w1 + (size_t)(n - a.n1) * a.K;
+  return a.w2 + (size_t)(n - a.n2) * a.K;
+}
+
+__global__ __launch_bounds__(256) void k_gemm_f32(FArgs a) {
+  __shared__ float xs[16][65];
+  __shared__ float ws[16][65];
+  const int tid = threadIdx.x;
+  const int tx = tid % 16, ty = tid / 16;
+  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  const bool swiglu = a.epi == EPI_SWIGLU;
+  float acc[4][4] = {};
+  float acc2[4][4] = {};
+  for (int k0 = 0; k0 < a.K; k0 += 16) {
+    for (int pass = 0; pass < (swiglu ? 2 : 1); ++pass) {
+      for (int i = tid; i < 64 * 16; i += 256) {
+        const int r = i / 16, c = i % 16;
+        const int m = min(m0 + r, a.M - 1);
+        xs[c][r] = a.X[(size_t)m * a.ldx + k0 + c];
+        const int n = n0 + r;
+        float wv = 0.f;
+        if (swiglu) {
+          if (n < a.n1) wv = (pass == 0 ? a.w0 : a.w1)[(size_t)n * a.K + k0 + c];
+        } else if (n < a.N) {
+          wv = frow(a, n)[k0 + c];
+        }
+        ws[c][r] = wv;
+      }
+      __syncthreads();
+      float (*ac)[4] = pass == 0 ? acc : acc2;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        float xv[4], wv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) xv[i] = xs[k][ty * 4 + i];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) wv[j] = ws[k][tx * 4 + j];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) ac[i][j] = fmaf(xv[i], wv[j], ac[i][j]);
+      }
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + ty * 4 + i;
+    if (m >= a.M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + tx * 4 + j;
+      if (swiglu) {
+        if (n < a.n1) {
+          const float gt = acc[i][j];
+          a.out_act[(size_t)m * a.ld_out + n] = gt / (1.f + __expf(-gt)) * acc2[i][j];
+        }
+      } else if (n < a.N) {
+        float* o = a.out_f32 + (size_t)m * a.ld_out + n;
+        if (a.epi == EPI_RESID) *o += acc[i][j];
+        else *o = acc[i][j];
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, int K, int epi,
+                           EpiArgs ep, hipStream_t st) {
+  TArgs a;
+  a.X = X; a.ldx = ldx; a.M = M;
+  a.w0 = (const bf16_t*)W.w[0]; a.w1 = (const bf16_t*)W.w[1]; a.w2 = (const bf16_t*)W.w[2];
+  a.n1 = W.n1; a.n2 = W.n2; a.N = N; a.K = K;
+  a.tiles_m = (M + BM - 1) / BM;
+  a.tiles_n = epi == EPI_SWIGLU ? (N + 63) / 64 : (N + BN - 1) / BN;
+  a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;
+  const int grid = a.tiles_m * a.tiles_n;
+  switch (epi) {
+    case EPI_STORE: k_gemm_tiled<EPI_STORE><<<grid, NT, 0, st>>>(a); break;
+    case EPI_RESID: k_gemm_tiled<EPI_RESID><<<grid, NT, 0, st>>>(a); break;
+    default: k_gemm_tiled<EPI_SWIGLU><<<grid, NT, 0, st>>>(a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t gemm_f32(const float* X, int ldx, int M, WStack W, int N, int K, int epi, EpiArgs ep,
+                    hipStream_t st) {
+  FArgs a;
+  a.X = X; a.ldx = ldx; a.M = M;
+  a.w0 = (const float*)W.w[0]; a.w1 = (const float*)W.w[1]; a.w2 = (const float*)W.w[2];
+  a.n1 = W.n1; a.n2 = W.n2; a.N = N; a.K = K; a.epi = epi;
+  a.out_f32 = ep.out_f32; a.out_act = (float*)ep.out_act; a.ld_out = ep.ld_out;
+  dim3 grid((N + 63) / 64, (M + 63) / 64);
+  k_gemm_f32<<<grid, 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace grpo

@@ -1,0 +1,172 @@
+// GRPO group advantages and the clipped-ratio + KL token loss.
+//
+// Both are microsecond-scale next to rollout and scoring; they run in fp64
+// internally so the per-token KL estimator exp(d) - d - 1 (a difference of
+// nearly equal numbers when d is small) keeps its relative accuracy, and every
+// reduction is a fixed-order tree: per-row sums, then one workgroup over rows.
+#include "common.h"
+#include "kernels.h"
+
+namespace grpo {
+
+namespace {
+
+__global__ void k_advantages(const float* __restrict__ r, int P, int G, float eps,
+                             float* __restrict__ adv) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= P) return;
+  const float* rg = r + (size_t)p * G;
+  double mean = 0.0, mx = -INFINITY, mn = INFINITY;
+  for (int i = 0; i < G; ++i) {
+    const double v = rg[i];
+    mean += v;
+    mx = fmax(mx, v);
+    mn = fmin(mn, v);
+  }
+  mean /= G;
+  double ss = 0.0;
+  for (int i = 0; i < G; ++i) {
+    const double dv = (double)rg[i] - mean;
+    ss += dv * dv;
+  }
+  const double sd = sqrt(ss / (G - 1));
+  const bool degenerate = (mx == mn);
+  for (int i = 0; i < G; ++i)
+    adv[(size_t)p * G + i] = degenerate ? 0.f : (float)(((double)rg[i] - mean) / (sd + (double)eps));
+}
+
+struct TokTerms {
+  double ell, dl, kl, rho;
+  bool clip_hit;
+};
+
+__device__ __forceinline__ TokTerms tok_terms(float lp, float lo, float lr, float A, float ceps,
+                                              float beta) {
+  TokTerms t;
+  const double rho = exp((double)lp - (double)lo);
+  const double a = A;
+  const double clipped = fmin(fmax(rho, 1.0 - (double)ceps), 1.0 + (double)ceps);
+  const double un = rho * a, cl = clipped * a;
+  const bool unclipped = un <= cl;
+  const double s = unclipped ? un : cl;
+  const double d = (double)lr - (double)lp;
+  const double em1 = expm1(d);
+  t.kl = em1 - d;
+  t.ell = -s + (double)beta * t.kl;
+  t.dl = -(unclipped ? un : 0.0) - (double)beta * em1;
+  t.rho = rho;
+  t.clip_hit = !unclipped;
+  return t;
+}
+
+// row sums: [sum m*l, count, sum m*kl, clip hits, sum m*rho, non-finite]
+__global__ __launch_bounds__(256) void k_loss_rows(const float* lp, const float* lo,
+                                                   const float* lr, const uint8_t* mask,
+                                                   const float* adv, int Tr, float ceps,
+                                                   float beta, float* tok_loss, double* row_ws) {
+  __shared__ double sh[6][4];
+  const int n = blockIdx.x;
+  const float A = adv[n];
+  double acc[6] = {0, 0, 0, 0, 0, 0};
+  for (int t = threadIdx.x; t < Tr; t += 256) {
+    const size_t i = (size_t)n * Tr + t;
+    const bool m = mask[i] != 0;
+    float out = 0.f;
+    if (m) {
+      const TokTerms tt = tok_terms(lp[i], lo[i], lr[i], A, ceps, beta);
+      acc[0] += tt.ell;
+      acc[1] += 1.0;
+      acc[2] += tt.kl;
+      acc[3] += tt.clip_hit ? 1.0 : 0.0;
+      acc[4] += tt.rho;
+      acc[5] += isfinite(tt.ell) ? 0.0 : 1.0;
+      out = (float)tt.ell;
+    }
+    if (tok_loss) tok_loss[i] = out;
+  }
+  const int w = threadIdx.x / 64, l = threadIdx.x % 64;
+#pragma unroll
+  for (int k = 0; k < 6; ++k) {
+    const double v = wave_sum_d(acc[k]);
+    if (l == 0) sh[k][w] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < 6) {
+    const int k = threadIdx.x;
+    row_ws[(size_t)n * 8 + k] = ((sh[k][0] + sh[k][1]) + sh[k][2]) + sh[k][3];
+  }
+}
+
+// one workgroup: loss, statistics and the per-row gradient weights
+__global__ __launch_bounds__(256) void k_loss_final(const double* row_ws, int N, int agg,
+                                                    float* loss, float* stats, double* wts) {
+  __shared__ double sh[6][4];
+  __shared__ double s_tot[6];
+  double acc[6] = {0, 0, 0, 0, 0, 0};
+  for (int n = threadIdx.x; n < N; n += 256) {
+    const double* r = row_ws + (size_t)n * 8;
+    acc[0] += agg == 0 ? r[0] / fmax(1.0, r[1]) : r[0];
+    for (int k = 1; k < 6; ++k) acc[k] += r[k];
+  }
+  const int w = threadIdx.x / 64, l = threadIdx.x % 64;
+#pragma unroll
+  for (int k = 0; k < 6; ++k) {
+    const double v = wave_sum_d(acc[k]);
+    if (l == 0) sh[k][w] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < 6) {
+    const int k = threadIdx.x;
+    s_tot[k] = ((sh[k][0] + sh[k][1]) + sh[k][2]) + sh[k][3];
+  }
+  __syncthreads();
+  const double ntok = fmax(1.0, s_tot[1]);
+  if (threadIdx.x == 0) {
+    loss[0] = (float)(agg == 0 ? s_tot[0] / (double)N : s_tot[0] / ntok);
+    if (stats) {
+      stats[0] = (float)(s_tot[2] / ntok);
+      stats[1] = (float)(s_tot[3] / ntok);
+      stats[2] = (float)(s_tot[4] / ntok);
+      stats[3] = (float)s_tot[5];
+    }
+  }
+  for (int n = threadIdx.x; n < N; n += 256)
+    wts[n] = agg == 0 ? 1.0 / ((double)N * fmax(1.0, row_ws[(size_t)n * 8 + 1])) : 1.0 / ntok;
+}
+
+__global__ __launch_bounds__(256) void k_loss_grad(const float* lp, const float* lo,
+                                                   const float* lr, const uint8_t* mask,
+                                                   const float* adv, int Tr, float ceps,
+                                                   float beta, const double* wts, float* dl) {
+  const int n = blockIdx.x;
+  const double w = wts[n];
+  const float A = adv[n];
+  for (int t = threadIdx.x; t < Tr; t += 256) {
+    const size_t i = (size_t)n * Tr + t;
+    float g = 0.f;
+    if (mask[i]) g = (float)(tok_terms(lp[i], lo[i], lr[i], A, ceps, beta).dl * w);
+    dl[i] = g;
+  }
+}
+
+}  // namespace
+
+hipError_t advantages(const float* r, int P, int G, float eps, float* adv, hipStream_t st) {
+  if (P <= 0) return hipSuccess;
+  k_advantages<<<(P + 63) / 64, 64, 0, st>>>(r, P, G, eps, adv);
+  return hipGetLastError();
+}
+
+hipError_t token_loss(const float* lp, const float* lo, const float* lr, const uint8_t* mask,
+                      const float* adv, int N, int Tr, float clip_eps, float beta, int agg,
+                      float* loss, float* tok_loss, float* dl, float* stats, double* row_ws,
+                      hipStream_t st) {
+  if (N <= 0) return hipSuccess;
+  double* wts = row_ws + (size_t)N * 8;
+  k_loss_rows<<<N, 256, 0, st>>>(lp, lo, lr, mask, adv, Tr, clip_eps, beta, tok_loss, row_ws);
+  k_loss_final<<<1, 256, 0, st>>>(row_ws, N, agg, loss, stats, wts);
+  if (dl) k_loss_grad<<<N, 256, 0, st>>>(lp, lo, lr, mask, adv, Tr, clip_eps, beta, wts, dl);
+  return hipGetLastError();
+}
+
+}  // namespace grpo

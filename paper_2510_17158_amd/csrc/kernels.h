@@ -1,0 +1,119 @@
+// Host-side launchers of the HIP kernels (internal interface of libgrpo_hip).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace grpo {
+
+enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+
+// Up to three weight matrices stacked along the output dimension: output row r
+// belongs to w[0] for r < n1, to w[1] for n1 <= r < n2, else to w[2].
+struct WStack {
+  const void* w[3];
+  int n1, n2;
+};
+
+struct EpiArgs {
+  float* out_f32;       // EPI_STORE: [rows, ld_out] fp32;  EPI_RESID: residual [rows, ld_out]
+  void* out_act;        // EPI_SWIGLU: [rows, ld_out] activation dtype
+  int ld_out;
+};
+
+// ---- decode GEMM: Y[B, N] = X[B, K] . W[N, K]^T for B <= 128 (bf16 MFMA) ----
+// For EPI_SWIGLU, N is d_ffn and W stacks (gate, up) with n1 = N.
+struct SkinnyPlan {
+  int nb;        // padded batch (16, 32, 64, 128)
+  int kc;        // K chunk staged in LDS
+  int tiles;     // output tiles
+  int splits;    // split-K factor
+  size_t part_floats;  // partial-sum scratch (floats)
+  int counters;        // tile counters (ints)
+};
+SkinnyPlan skinny_plan(int B, int N, int K, int epi, int target_wgs);
+hipError_t gemm_skinny_bf16(const uint16_t* X, int ldx, int B, WStack W, int N, int K, int epi,
+                            EpiArgs ep, const SkinnyPlan& p, float* part, int* counters,
+                            hipStream_t st);
+
+// ---- tiled GEMM for many rows (prefill / scoring): bf16 MFMA -----------------
+hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, int K, int epi,
+                           EpiArgs ep, hipStream_t st);
+
+// ---- fp32 GEMM (fp32 models; VALU) -------------------------------------------
+hipError_t gemm_f32(const float* X, int ldx, int M, WStack W, int N, int K, int epi, EpiArgs ep,
+                    hipStream_t st);
+
+// ---- elementwise ---------------------------------------------------------------
+// x[m, :] = emb[tok[m]] (fp32).  tok ids clamped to [0, vocab).
+hipError_t embed(int dtype, const void* emb, const int32_t* tok, int M, int d, int vocab, float* x,
+                 hipStream_t st);
+// Source row of output row m: ((i0 + m) / per) * stride + off + (i0 + m) % per.
+struct RowMap {
+  int i0, per, stride, off;
+  static RowMap identity() { return RowMap{0, 0x7fffffff, 0, 0}; }
+};
+// out[m] = round(x[src(m)] / sqrt(mean(x^2) + eps) * g).
+hipError_t rmsnorm(int dtype, const float* x, int ldx, RowMap rows, const void* g, int M, int d,
+                   float eps, void* out, int ldo, hipStream_t st);
+hipError_t fill_i32(int32_t* p, size_t n, int32_t v, hipStream_t st);
+// Rotary embedding + cache write.  qkv fp32 [M, q_dim + 2 kv_dim].  Row m is
+// (seq, pos): mode 0: seq = m, pos = pos_arr[m];  mode 1: seq = m / T, pos = m % T.
+// q_out: [M, q_dim] act.  K/V written to cache slots seq*G + g (g < G) at pos
+// (positions >= max_len skipped).  vt (optional) gets V transposed:
+// [seq][n_kv][hd][vt_len] for the prefill/scoring attention.
+struct RopeArgs {
+  int mode, T, G;
+  const int32_t* pos_arr;
+  int n_heads, n_kv, hd;
+  float theta;
+  void* kcache; void* vcache;   // layer base of K and V: [n_seqs][n_kv][max_len][hd]; V may be NULL
+  int n_seqs, max_len;
+  uint16_t* vt; int vt_len;
+};
+hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeArgs& a,
+                   hipStream_t st);
+
+// ---- attention -------------------------------------------------------------------
+// Decode: q act [B, H, hd]; cache layer base K/V [n_seqs][n_kv][max_len][hd];
+// attends positions 0..pos[b].  out act [B, H*hd].
+struct DecodeAttnPlan { int tc; int splits; size_t part_floats; };
+DecodeAttnPlan decode_attn_plan(int B, int H, int hd, int max_len);
+hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
+                       const int32_t* pos, int B, int H, int n_kv, int hd, int n_seqs, int max_len,
+                       const DecodeAttnPlan& p, float* part, void* out, hipStream_t st);
+// Causal attention over N sequences of T rows: q act [N*T, H*hd]; K in cache
+// layout [n][n_kv][k_len][hd] (sequence n at slot n*k_stride_seq), Vt
+// [n][n_kv][hd][T] (bf16 path) or V in cache layout (fp32 path).  out act [N*T, H*hd].
+hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_or_vt, int N,
+                        int T, int H, int n_kv, int hd, int k_len, int k_seq_stride,
+                        void* out, hipStream_t st);
+
+// ---- sampling / log-probs ---------------------------------------------------------
+// logits fp32 [R, V] (row stride ld).  Row r makes G draws; draw g uses Philox
+// sequence id q = r*G + g and writes tok_out[q*out_stride], logp_out[q*out_stride].
+struct SampleArgs {
+  float temperature; int top_k; uint64_t seed;
+  int step;               // Philox step word
+  int G;                  // draws per row (prefill: G samples per prompt)
+  int32_t* tok_out; float* logp_out;  // [R*G], element stride out_stride
+  int out_stride;
+  int32_t* tok_state;     // optional [R*G]: also store token here
+  int32_t* pos_state;     // optional [R*G]: pos += 1
+};
+hipError_t sample(const float* logits, int R, int V, int ld, const SampleArgs& a, hipStream_t st);
+// Teacher-forced log-prob of scored row m (global index gi = i0 + m over
+// sequences of Ts scored positions): n = gi / Ts, j = score_from + gi % Ts,
+// logp[m] = z[m, tokens[n*T + j]] - LSE(z[m, :]), z = logits / temperature.
+hipError_t token_logprob(const float* logits, int R, int V, int ld, const int32_t* tokens, int T,
+                         int score_from, int Ts, int i0, float temperature, float* logp,
+                         hipStream_t st);
+
+// ---- GRPO ---------------------------------------------------------------------------
+hipError_t advantages(const float* r, int P, int G, float eps, float* adv, hipStream_t st);
+hipError_t token_loss(const float* lp, const float* lo, const float* lr, const uint8_t* mask,
+                      const float* adv, int N, int Tr, float clip_eps, float beta, int agg,
+                      float* loss, float* tok_loss, float* dl, float* stats, double* row_ws,
+                      hipStream_t st);
+
+}  // namespace grpo

@@ -1,0 +1,176 @@
+// Next-token sampling over the LM-head logits and its log-probability.
+//
+// One workgroup per (row, draw).  The row is read from L2 a few times:
+//   1. max and arg-max of z = l / T (lowest id among equal maxima),
+//   2. sum of exp(z - max) -> log-sum-exp (full vocabulary),
+//   3. with top_k > 0: radix select (four 8-bit passes, LDS histograms with
+//      integer atomics) of the k-th largest logit, ties at the cut ordered by id,
+//   4. Gumbel-max over the allowed ids with Philox4x32-10 draws: one Philox
+//      block per 4 consecutive ids, u = (2*(w >> 9) + 1) * 2^-24,
+//      key = z - ln(-ln u); the largest key wins, the lowest id among equals.
+// Every reduction is in a fixed order, so draws are bit-deterministic.
+#include "common.h"
+#include "kernels.h"
+
+namespace grpo {
+
+namespace {
+
+constexpr int NT = 256;
+
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+  }
+  return c;
+}
+
+__device__ __forceinline__ uint32_t order_key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// (value desc, id asc) arg-max merge
+__device__ __forceinline__ void better(float& bv, int& bi, float v, int i) {
+  if (v > bv || (v == bv && i < bi)) { bv = v; bi = i; }
+}
+
+__device__ __forceinline__ void block_argmax(float& bv, int& bi, float* shv, int* shi) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(bv, o, 64);
+    const int oi = __shfl_xor(bi, o, 64);
+    better(bv, bi, ov, oi);
+  }
+  const int w = threadIdx.x / 64;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) { shv[w] = bv; shi[w] = bi; }
+  __syncthreads();
+  bv = shv[0]; bi = shi[0];
+  for (int i = 1; i < NT / 64; ++i) better(bv, bi, shv[i], shi[i]);
+}
+
+__global__ __launch_bounds__(NT) void k_sample(const float* __restrict__ logits, int V, int ld,
+                                               SampleArgs a) {
+  __shared__ float sh[4];
+  __shared__ float shv[4];
+  __shared__ int shi[4];
+  __shared__ int hist[256];
+  __shared__ uint32_t s_prefix;
+  __shared__ int s_krem, s_eq, s_cut;
+  const int r = blockIdx.x, gdraw = blockIdx.y;
+  const int seq = r * a.G + gdraw;
+  const float* l = logits + (size_t)r * ld;
+  const int tid = threadIdx.x;
+  const bool greedy = !(a.temperature > 0.f);
+  const float T = greedy ? 1.f : a.temperature;
+
+  // 1-2: max / arg-max and log-sum-exp of z
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int i = tid; i < V; i += NT) better(bv, bi, l[i], i);
+  block_argmax(bv, bi, shv, shi);
+  const float zmax = bv / T;
+  float s = 0.f;
+  for (int i = tid; i < V; i += NT) s += __expf(l[i] / T - zmax);
+  s = block_sum<NT>(s, sh);
+  const float lse = zmax + logf(s);
+
+  int tok = bi;
+  if (!greedy) {
+    // 3: top-k cut
+    uint32_t thr = 0;
+    int cut = 0x7fffffff;
+    const bool use_k = a.top_k > 0 && a.top_k < V;
+    if (use_k) {
+      uint32_t prefix = 0, pmask = 0;
+      int krem = a.top_k;
+      for (int shift = 24; shift >= 0; shift -= 8) {
+        for (int i = tid; i < 256; i += NT) hist[i] = 0;
+        __syncthreads();
+        for (int i = tid; i < V; i += NT) {
+          const uint32_t u = order_key(l[i]);
+          if ((u & pmask) == prefix) atomicAdd(&hist[(u >> shift) & 255], 1);
+        }
+        __syncthreads();
+        if (tid == 0) {
+          int cum = 0, sel = 0;
+          for (int bin = 255; bin >= 0; --bin) {
+            if (cum + hist[bin] >= krem) { sel = bin; break; }
+            cum += hist[bin];
+          }
+          s_krem = krem - cum;
+          s_eq = hist[sel];
+          s_prefix = prefix | ((uint32_t)sel << shift);
+        }
+        __syncthreads();
+        krem = s_krem;
+        prefix = s_prefix;
+        pmask |= 255u << shift;
+        __syncthreads();
+      }
+      thr = prefix;
+      // ids equal to the cut value: keep the lowest krem of them
+      if (tid == 0) {
+        int c = 0x7fffffff;
+        if (s_eq > krem) {
+          int seen = 0;
+          for (int i = 0; i < V; ++i)
+            if (order_key(l[i]) == thr && ++seen == krem) { c = i; break; }
+        }
+        s_cut = c;
+      }
+      __syncthreads();
+      cut = s_cut;
+    }
+    // 4: Gumbel-max over the allowed ids
+    const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
+    float gv = -INFINITY;
+    int gi = 0x7fffffff;
+    const int nblk = (V + 3) / 4;
+    for (int c = tid; c < nblk; c += NT) {
+      const uint4 w = philox4x32_10(make_uint4((uint32_t)c, (uint32_t)a.step, (uint32_t)seq, 0u),
+                                    k0, k1);
+      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = 4 * c + j;
+        if (i >= V) break;
+        const float li = l[i];
+        if (use_k) {
+          const uint32_t u = order_key(li);
+          if (!(u > thr || (u == thr && i <= cut))) continue;
+        }
+        const float uu = (float)(2u * (ws[j] >> 9) + 1u) * 5.9604644775390625e-8f;  // 2^-24
+        const float key = li / T - logf(-logf(uu));
+        better(gv, gi, key, i);
+      }
+    }
+    block_argmax(gv, gi, shv, shi);
+    tok = gi;
+  }
+  if (tid == 0) {
+    tok = clampi(tok, 0, V - 1);
+    a.tok_out[(size_t)seq * a.out_stride] = tok;
+    a.logp_out[(size_t)seq * a.out_stride] = l[tok] / T - lse;
+    if (a.tok_state) a.tok_state[seq] = tok;
+    if (a.pos_state) a.pos_state[seq] += 1;
+  }
+}
+
+}  // namespace
+
+hipError_t sample(const float* logits, int R, int V, int ld, const SampleArgs& a, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  dim3 grid(R, a.G);
+  k_sample<<<grid, NT, 0, st>>>(logits, V, ld, a);
+  return hipGetLastError();
+}
+
+}  // namespace grpo
