@@ -68,7 +68,7 @@ enum grpo_op { GRPO_OP_PREFILL = 0, GRPO_OP_ROLLOUT = 1, GRPO_OP_SCORE = 2, GRPO
  * angle pos * rope_theta^(-2i/hd)), grouped-query attention (query head h reads
  * kv head floor(h*n_kv_heads/n_heads)), SwiGLU MLP, untied LM head, no biases.
  * Supported: head_dim in {64, 128}; n_heads a multiple of n_kv_heads; d_model,
- * n_heads*head_dim and d_ffn multiples of 64 (of 32 for fp32 models). */
+ * n_heads*head_dim and d_ffn multiples of 128 (of 32 for fp32 models). */
 typedef struct grpo_config {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
   float rms_eps, rope_theta;
@@ -135,11 +135,13 @@ const char* grpo_last_error(void);
  *   kv        cache of n_seqs >= P*G sequences, max_len >= Tp
  *   tok_out   int32 [P*G] sampled tokens;  logp_out  fp32 [P*G]
  *   logits_dbg NULL or fp32 [P, vocab]: the last-position logits
+ *   hidden_dbg NULL or fp32 [n_layers+1, P*Tp, d]: residual stream entering
+ *              each layer and leaving the last one, every prompt position
  * Ids outside [0, vocab) are clamped by the kernels (memory safety only). */
 int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
                  const int32_t* prompts, int32_t P, int32_t Tp, int32_t G,
                  const grpo_sampling* s, int32_t* tok_out, float* logp_out, float* logits_dbg,
-                 void* ws, size_t ws_bytes, void* stream);
+                 float* hidden_dbg, void* ws, size_t ws_bytes, void* stream);
 
 /* n_steps decode steps for batch rows 0..B-1 (cache slots 0..B-1, Philox
  * sequence id = row).  Per step: token tok[b] enters at position pos[b] (its

@@ -42,10 +42,10 @@ def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
     T, H, hd = q.shape
     Hk = k.shape[1]
     causal = np.tril(np.ones((T, T), bool))
-    o = np.empty((T, H, hd))
+    o = np.empty((T, H, hd), q.dtype)
     for hh in range(H):
         g = hh * Hk // H
-        s = (q[:, hh, :] @ k[:, g, :].T) / np.sqrt(hd)
+        s = (q[:, hh, :] @ k[:, g, :].T) / float(np.sqrt(hd))
         s = np.where(causal, s, -np.inf)
         pr = np.exp(s - s.max(axis=1, keepdims=True))
         pr /= pr.sum(axis=1, keepdims=True)
@@ -54,20 +54,31 @@ def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
 
 
 class OracleModel:
-    """cfg: any object with the decoder shape attributes (n_layers, d_model, ...)."""
+    """cfg: any object with the decoder shape attributes (n_layers, d_model, ...).
 
-    def __init__(self, cfg, weights: dict, round_points: bool = True):
+    precision "fp64" is the oracle.  "fp32" evaluates the same definition with
+    float32 arithmetic and float32 accumulation; it is not a reference but a
+    measuring stick: its distance from the fp64 result is the noise floor that
+    any fp32-accumulating implementation of the same rounding contract shows.
+    """
+
+    def __init__(self, cfg, weights: dict, round_points: bool = True, precision: str = "fp64"):
         self.cfg = cfg
         self.w = weights
         self.bf16 = np.asarray(weights["tok_emb"]).dtype == np.uint16
-        self.R = round_bf16 if (self.bf16 and round_points) else _ident
+        self.dt = {"fp64": np.float64, "fp32": np.float32}[precision]
+        if self.bf16 and round_points:
+            self.R = lambda x: round_bf16(x).astype(self.dt)
+        else:
+            self.R = _ident
         self._f64 = {}
 
     # -- weights --------------------------------------------------------------
     def mat(self, name: str) -> np.ndarray:
         if name not in self._f64:
             a = np.asarray(self.w[name])
-            self._f64[name] = bf16_bits_to_f64(a) if a.dtype == np.uint16 else a.astype(np.float64)
+            f = bf16_bits_to_f64(a) if a.dtype == np.uint16 else a.astype(np.float64)
+            self._f64[name] = f.astype(self.dt, copy=False)
         return self._f64[name]
 
     def drop_cache(self):
@@ -75,37 +86,48 @@ class OracleModel:
 
     def embed(self, tokens) -> np.ndarray:
         a = np.asarray(self.w["tok_emb"])[np.asarray(tokens)]
-        return bf16_bits_to_f64(a) if a.dtype == np.uint16 else a.astype(np.float64)
+        f = bf16_bits_to_f64(a) if a.dtype == np.uint16 else a.astype(np.float64)
+        return f.astype(self.dt, copy=False)
 
     # -- full-sequence forward (the definition) -------------------------------
     def forward(self, tokens, return_hidden: bool = False):
         """tokens [T] of one sequence -> logits [T, V], per-layer (k, v) [Hkv, T, hd]."""
-        c, R = self.cfg, self.R
-        T = len(tokens)
-        H, Hk, hd = c.n_heads, c.n_kv_heads, c.head_dim
-        pos = np.arange(T)
+        c = self.cfg
         x = self.embed(tokens)
         kv, hidden = [], [x.copy()]
         for l in range(c.n_layers):
-            p = f"l{l}."
-            h = R(rmsnorm(x, self.mat(p + "attn_norm"), c.rms_eps))
-            q = (h @ self.mat(p + "wq").T).reshape(T, H, hd)
-            k = (h @ self.mat(p + "wk").T).reshape(T, Hk, hd)
-            v = (h @ self.mat(p + "wv").T).reshape(T, Hk, hd)
-            q = R(rope(q, pos, c.rope_theta))
-            k = R(rope(k, pos, c.rope_theta))
-            v = R(v)
-            o = causal_attention(q, k, v)
-            x = x + R(o.reshape(T, H * hd)) @ self.mat(p + "wo").T
-            h = R(rmsnorm(x, self.mat(p + "mlp_norm"), c.rms_eps))
-            a = R(silu(h @ self.mat(p + "w_gate").T) * (h @ self.mat(p + "w_up").T))
-            x = x + a @ self.mat(p + "w_down").T
-            kv.append((k.transpose(1, 0, 2).copy(), v.transpose(1, 0, 2).copy()))
+            x, k, v = self.layer(l, x)
+            kv.append((k, v))
             hidden.append(x.copy())
         logits = self.head(x)
         if return_hidden:
             return logits, kv, hidden
         return logits, kv
+
+    def layer(self, l: int, x: np.ndarray):
+        """Layer l over one full sequence x [T, d] (positions 0..T-1, causal).
+
+        Returns the new residual and the layer's K, V as [Hkv, T, hd].
+        """
+        c, R = self.cfg, self.R
+        x = np.asarray(x).astype(self.dt, copy=False)
+        T = x.shape[0]
+        H, Hk, hd = c.n_heads, c.n_kv_heads, c.head_dim
+        pos = np.arange(T)
+        p = f"l{l}."
+        h = R(rmsnorm(x, self.mat(p + "attn_norm"), c.rms_eps))
+        q = (h @ self.mat(p + "wq").T).reshape(T, H, hd)
+        k = (h @ self.mat(p + "wk").T).reshape(T, Hk, hd)
+        v = (h @ self.mat(p + "wv").T).reshape(T, Hk, hd)
+        q = R(rope(q, pos, c.rope_theta))
+        k = R(rope(k, pos, c.rope_theta))
+        v = R(v)
+        o = causal_attention(q, k, v)
+        x = x + R(o.reshape(T, H * hd)) @ self.mat(p + "wo").T
+        h = R(rmsnorm(x, self.mat(p + "mlp_norm"), c.rms_eps))
+        a = R(silu(h @ self.mat(p + "w_gate").T) * (h @ self.mat(p + "w_up").T))
+        x = x + a @ self.mat(p + "w_down").T
+        return x, k.transpose(1, 0, 2).copy(), v.transpose(1, 0, 2).copy()
 
     def head(self, x: np.ndarray) -> np.ndarray:
         """Final RMSNorm + LM head: [n, d] -> [n, V]."""
@@ -122,6 +144,7 @@ class OracleModel:
         updated residual.
         """
         c, R = self.cfg, self.R
+        x = np.asarray(x).astype(self.dt, copy=False)
         B = x.shape[0]
         H, Hk, hd = c.n_heads, c.n_kv_heads, c.head_dim
         p = f"l{l}."
@@ -129,9 +152,9 @@ class OracleModel:
         q = (h @ self.mat(p + "wq").T).reshape(B, H, hd)
         k = (h @ self.mat(p + "wk").T).reshape(B, Hk, hd)
         v = (h @ self.mat(p + "wv").T).reshape(B, Hk, hd)
-        o = np.empty((B, H, hd))
-        k_new = np.empty((B, Hk, hd))
-        v_new = np.empty((B, Hk, hd))
+        o = np.empty((B, H, hd), self.dt)
+        k_new = np.empty((B, Hk, hd), self.dt)
+        v_new = np.empty((B, Hk, hd), self.dt)
         for b in range(B):
             pb = int(pos[b])
             qb = R(rope(q[b:b + 1], np.array([pb]), c.rope_theta))[0]
@@ -142,7 +165,7 @@ class OracleModel:
             k_new[b], v_new[b] = kb, vb
             for hh in range(H):
                 g = hh * Hk // H
-                s = K[b, g, : pb + 1, :] @ qb[hh] / np.sqrt(hd)
+                s = K[b, g, : pb + 1, :] @ qb[hh] / float(np.sqrt(hd))
                 pr = np.exp(s - s.max())
                 pr /= pr.sum()
                 o[b, hh] = pr @ V[b, g, : pb + 1, :]
@@ -179,7 +202,7 @@ class OracleModel:
         B = P * group
         Tmax = Tp + new_tokens - 1
         L, Hk, hd = c.n_layers, c.n_kv_heads, c.head_dim
-        K = np.zeros((L, B, Hk, max(Tmax, Tp), hd))
+        K = np.zeros((L, B, Hk, max(Tmax, Tp), hd), self.dt)
         V = np.zeros_like(K)
         toks = np.zeros((B, new_tokens), np.int64)
         own = np.zeros((B, new_tokens), np.int64)

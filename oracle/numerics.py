@@ -32,11 +32,17 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
     return bf16_bits_to_f64((r & np.uint64(0xFFFF)).astype(np.uint16))
 
 
+def _float(x) -> np.ndarray:
+    """float32 arrays stay float32 (the noise-floor variant); all else is float64."""
+    x = np.asarray(x)
+    return x if x.dtype == np.float32 else x.astype(np.float64)
+
+
 def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
     """x / sqrt(mean(x^2) + eps) * g over the last axis."""
-    x = np.asarray(x, np.float64)
+    x = _float(x)
     ms = np.mean(x * x, axis=-1, keepdims=True)
-    return x / np.sqrt(ms + eps) * g
+    return x / np.sqrt(ms + float(eps)) * np.asarray(g, x.dtype)
 
 
 def silu(z: np.ndarray) -> np.ndarray:
@@ -51,9 +57,12 @@ def rope_angles(pos: np.ndarray, head_dim: int, theta: float) -> np.ndarray:
 
 
 def rope(v: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
-    """Rotate [T, n_heads, hd] vectors at positions pos[T], half-split pairing."""
+    """Rotate [T, n_heads, hd] vectors at positions pos[T], half-split pairing.
+
+    Angles, cos and sin are fp64; float32 input is rotated in float32."""
+    v = _float(v)
     hd = v.shape[-1]
     a = rope_angles(pos, hd, theta)[:, None, :]
-    c, s = np.cos(a), np.sin(a)
+    c, s = np.cos(a).astype(v.dtype), np.sin(a).astype(v.dtype)
     lo, hi = v[..., : hd // 2], v[..., hd // 2:]
     return np.concatenate([lo * c - hi * s, hi * c + lo * s], axis=-1)

@@ -58,7 +58,7 @@ _SIGS = {
     "grpo_workspace_bytes": (_SZ, [_VP, _I32, _I32, _I32]),
     "grpo_last_error": (C.c_char_p, []),
     "grpo_prefill": (_I32, [_VP, _VP, _I32, _I32, _VP, _I32, _I32, _I32, C.POINTER(Sampling),
-                            _VP, _VP, _VP, _VP, _SZ, _VP]),
+                            _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "grpo_rollout_step": (_I32, [_VP, _VP, _I32, _I32, _I32, _VP, _VP, _I32, _I32, _I32,
                                  C.POINTER(Sampling), _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "grpo_score_sequences": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _VP, _VP, _SZ, _VP]),
@@ -185,11 +185,12 @@ def alloc_kv(cfg: ModelConfig, n_seqs: int, max_len: int, device="cuda"):
 
 
 def prefill(model: Model, kv, n_seqs: int, max_len: int, prompts, G: int, sampling: Sampling,
-            tok_out, logp_out, logits_dbg=None, ws=None, stream=None):
+            tok_out, logp_out, logits_dbg=None, hidden_dbg=None, ws=None, stream=None):
     P, Tp = prompts.shape
     _check(lib().grpo_prefill(model.handle, _ptr(kv), n_seqs, max_len, _ptr(prompts), P, Tp, G,
                               C.byref(sampling), _ptr(tok_out), _ptr(logp_out), _ptr(logits_dbg),
-                              _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)))
+                              _ptr(hidden_dbg), _ptr(ws), ws.numel() if ws is not None else 0,
+                              _stream(stream)))
 
 
 def rollout_step(model: Model, kv, n_seqs: int, max_len: int, pos, tok, max_pos: int, step0: int,

@@ -247,7 +247,8 @@ WStack gate_up(const grpo_model* m, int l) {
 // (row = seq * T + t).  K/V go to kc/vc (cache layout with n_slots slots of
 // k_len positions; sequence s at slot s * G) and V also transposed to vt.
 int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slots, int k_len,
-                 void* kv_or_null, void* kbuf, void* vbuf, uint16_t* vt, hipStream_t st) {
+                 void* kv_or_null, void* kbuf, void* vbuf, uint16_t* vt, float* hidden_dbg,
+                 hipStream_t st) {
   const grpo_config& c = m->cfg;
   const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
   const int N = M / T;
@@ -258,6 +259,9 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
       kl = L.k;
       vl = L.v;
     }
+    if (hidden_dbg)
+      HIPCHK(hipMemcpyAsync(hidden_dbg + (size_t)l * M * d, w.x, (size_t)M * d * 4,
+                            hipMemcpyDeviceToDevice, st));
     HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), m->attn_norm[l], M, d, c.rms_eps, w.h, d,
                    st));
     int rc = run_gemm(m, w.h, d, M, qkv_stack(m, l), qd + 2 * kvd, d, EPI_STORE,
@@ -282,6 +286,9 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
                   st);
     if (rc) return rc;
   }
+  if (hidden_dbg)
+    HIPCHK(hipMemcpyAsync(hidden_dbg + (size_t)c.n_layers * M * d, w.x, (size_t)M * d * 4,
+                          hipMemcpyDeviceToDevice, st));
   return GRPO_OK;
 }
 
@@ -356,8 +363,8 @@ size_t grpo_workspace_bytes(const grpo_model* m, int32_t op, int32_t n_rows, int
 
 int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
                  const int32_t* prompts, int32_t P, int32_t Tp, int32_t G, const grpo_sampling* s,
-                 int32_t* tok_out, float* logp_out, float* logits_dbg, void* ws, size_t ws_bytes,
-                 void* stream) {
+                 int32_t* tok_out, float* logp_out, float* logits_dbg, float* hidden_dbg, void* ws,
+                 size_t ws_bytes, void* stream) {
   if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
   const grpo_config& c = m->cfg;
   if (!kv || !prompts || !tok_out || !logp_out || !ws)
@@ -377,7 +384,8 @@ int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
   const int M = P * Tp, d = c.d_model;
   HIPCHK(fill_i32(w.s.g.counters, w.n_counters, 0, st));
   HIPCHK(embed(c.dtype, m->tok_emb, prompts, M, d, c.vocab, w.s.x, st));
-  if (int rc = forward_rows(m, w.s, M, Tp, G, n_seqs, max_len, kv, nullptr, nullptr, w.vt, st))
+  if (int rc = forward_rows(m, w.s, M, Tp, G, n_seqs, max_len, kv, nullptr, nullptr, w.vt,
+                            hidden_dbg, st))
     return rc;
   HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{0, 1, Tp, Tp - 1}, m->final_norm, P, d, c.rms_eps, w.hl,
                  d, st));
@@ -502,7 +510,7 @@ int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, 
     const int32_t* tk = tokens + (size_t)n0 * T;
     HIPCHK(embed(c.dtype, m->tok_emb, tk, M, d, c.vocab, w.s.x, st));
     if (int rc = forward_rows(m, w.s, M, T, 1, C, T, nullptr, w.kbuf,
-                              c.dtype == GRPO_F32 ? w.vbuf : nullptr, w.vt, st))
+                              c.dtype == GRPO_F32 ? w.vbuf : nullptr, w.vt, nullptr, st))
       return rc;
     const int R = C * Ts;
     for (int i0 = 0; i0 < R; i0 += w.sub_rows) {

@@ -13,9 +13,9 @@
 // Prefill / scoring (bf16): flash attention.  One workgroup per (64 queries,
 // head, sequence), 16 query rows per wave; K tiles and transposed V tiles
 // (written transposed by the rotary kernel) staged in LDS; S = Q K^T and
-// O += P V on v_mfma_f32_16x16x32_bf16 with an fp32 online softmax; P is
-// rounded to bf16 for the second product.  Key tiles above the diagonal are
-// skipped.
+// O += P V on v_mfma_f32_16x16x32_bf16 with an fp32 online softmax; P enters
+// the second product as a sum of two bf16 terms, so no extra rounding point is
+// introduced.  Key tiles above the diagonal are skipped.
 //
 // fp32 models use a plain vector kernel (one workgroup per query row and head).
 #include "common.h"
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(256) void k_flash_bf16(
   constexpr int QSTEPS = HD / 32, HB = HD / 16;
   __shared__ __attribute__((aligned(16))) bf16_t ks[64 * KROW];
   __shared__ __attribute__((aligned(16))) bf16_t vs[HD * VROW];
-  __shared__ __attribute__((aligned(16))) bf16_t ps[4][16 * PROW];
+  __shared__ __attribute__((aligned(16))) bf16_t ps[2][4][16 * PROW];   // P = hi + lo
 
   const int qb = blockIdx.x, h = blockIdx.y, n = blockIdx.z;
   const int g = h * n_kv / H;
@@ -272,9 +272,12 @@ __global__ __launch_bounds__(256) void k_flash_bf16(
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb) {
         const float p = (sacc[cb][v] == -INFINITY) ? 0.f : __expf(sacc[cb][v] - mnew[v]);
-        const bf16_t pb = f2bf(p);
-        sum += bf2f(pb);
-        ps[wave][((lane >> 4) * 4 + v) * PROW + cb * 16 + (lane & 15)] = pb;
+        const bf16_t ph = f2bf(p);
+        const bf16_t pl = f2bf(p - bf2f(ph));
+        sum += p;
+        const int at = ((lane >> 4) * 4 + v) * PROW + cb * 16 + (lane & 15);
+        ps[0][wave][at] = ph;
+        ps[1][wave][at] = pl;
       }
 #pragma unroll
       for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off, 64);
@@ -287,16 +290,19 @@ __global__ __launch_bounds__(256) void k_flash_bf16(
       for (int v = 0; v < 4; ++v) oacc[hb][v] *= alpha[v];
     __syncthreads();   // ps visible within the wave (and vs/ks reads ordered)
 
-    // O += P V: A = P (16 rows x 32 keys), B = V (32 keys x 16 dims)
+    // O += P V: A = P (16 rows x 32 keys), B = V (32 keys x 16 dims).  P enters
+    // as two bf16 terms (hi + lo), so P V is accurate to fp32 level.
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      const bf16x8_t pf =
-          *(const bf16x8_t*)(&ps[wave][(lane & 15) * PROW + kk * 32 + (lane >> 4) * 8]);
+      const int at = (lane & 15) * PROW + kk * 32 + (lane >> 4) * 8;
+      const bf16x8_t ph = *(const bf16x8_t*)(&ps[0][wave][at]);
+      const bf16x8_t pl = *(const bf16x8_t*)(&ps[1][wave][at]);
 #pragma unroll
       for (int hb = 0; hb < HB; ++hb) {
         const bf16x8_t vf =
             *(const bf16x8_t*)(&vs[(hb * 16 + (lane & 15)) * VROW + kk * 32 + (lane >> 4) * 8]);
-        oacc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf, vf, oacc[hb], 0, 0, 0);
+        oacc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vf, oacc[hb], 0, 0, 0);
+        oacc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, vf, oacc[hb], 0, 0, 0);
       }
     }
     __syncthreads();

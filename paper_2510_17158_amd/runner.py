@@ -62,11 +62,11 @@ class GrpoIteration:
         self.stats = torch.empty(4, **f32)
 
     # --- phases -----------------------------------------------------------------------
-    def prefill(self, logits_dbg=None):
+    def prefill(self, logits_dbg=None, hidden_dbg=None):
         w = self.w
         api.prefill(self.policy, self.kv, self.B, self.max_len, self.prompts, w.group,
                     self.sampling, self.tok0, self.logp0, logits_dbg=logits_dbg,
-                    ws=self.ws_prefill)
+                    hidden_dbg=hidden_dbg, ws=self.ws_prefill)
 
     def decode(self, logits_dbg=None, hidden_dbg=None):
         """Generation steps 1 .. new_tokens-1 for the whole batch."""

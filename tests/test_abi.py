@@ -90,12 +90,12 @@ def test_argument_errors_before_device_work():
     assert L.grpo_rollout_step(h, p, 64, 100, 64, p, p, 10, 1, 2, C.byref(bad), p, p, None, None,
                                p, 1 << 40, None) == api.INVALID_ARG
     bad = api.Sampling(1.0, 40000, 1)
-    assert L.grpo_prefill(h, p, 64, 100, p, 8, 10, 8, C.byref(bad), p, p, None, p, 1 << 40,
+    assert L.grpo_prefill(h, p, 64, 100, p, 8, 10, 8, C.byref(bad), p, p, None, None, p, 1 << 40,
                           None) == api.INVALID_ARG
     # prefill: P*G > n_seqs, prompt longer than the cache
-    assert L.grpo_prefill(h, p, 8, 100, p, 8, 10, 8, C.byref(s), p, p, None, p, 1 << 40,
+    assert L.grpo_prefill(h, p, 8, 100, p, 8, 10, 8, C.byref(s), p, p, None, None, p, 1 << 40,
                           None) == api.INVALID_ARG
-    assert L.grpo_prefill(h, p, 64, 100, p, 8, 200, 8, C.byref(s), p, p, None, p, 1 << 40,
+    assert L.grpo_prefill(h, p, 64, 100, p, 8, 200, 8, C.byref(s), p, p, None, None, p, 1 << 40,
                           None) == api.KV_CAPACITY
     # scoring range
     assert L.grpo_score_sequences(h, p, 4, 10, 0, 1.0, p, p, 1 << 40, None) == api.INVALID_ARG

@@ -16,12 +16,14 @@ from paper_2510_17158_amd import api, synth
 from paper_2510_17158_amd.runner import GrpoIteration
 from paper_2510_17158_amd.workloads import get, truncated
 
-from gpu_util import bf16_ulps, build_model, kv_view, require_gpu, say
+from gpu_util import FloorPool, bf16_ulps, build_model, floor_check, kv_view, require_gpu, say
 
 pytestmark = pytest.mark.gpu
 
 LOGIT_TOL = 2e-2     # bf16 logits / log-probs
-RESID_TOL = 2e-3     # one decode layer's residual output, fed identical inputs
+# Per-layer outputs (residual stream, K/V) are judged against the noise floor of
+# the rounding contract: the distance between the fp32-arithmetic and the fp64
+# evaluation of the same layer on the same (GPU-produced) inputs.
 
 
 def _small_workload(**kw):
@@ -29,14 +31,16 @@ def _small_workload(**kw):
     return w.with_(**kw)
 
 
-def _stage_local(w, host, model, it, n_steps, check_layers=True):
+def _stage_local(w, host, model, it, n_steps):
     """Decode n_steps one at a time; check every layer, the head and the sampler."""
     cfg = w.model
     B, L, d, V = it.B, cfg.n_layers, cfg.d_model, cfg.vocab
     om = oracle.OracleModel(cfg, host)
+    om32 = oracle.OracleModel(cfg, host, precision="fp32")
     it.tok.copy_(it.tok0)
     it.pos.fill_(w.prompt_len)
-    worst = dict(resid=0.0, kv_flip=0.0, kv_ulps=0, logit=0.0, near=0)
+    pool = FloorPool()
+    worst_logit, near = 0.0, 0
     toks = []
     for s in range(n_steps):
         pos = w.prompt_len + s
@@ -52,33 +56,61 @@ def _stage_local(w, host, model, it, n_steps, check_layers=True):
         to = to.cpu().numpy()[:, 0]
         lo = lo.cpu().numpy()[:, 0]
         toks.append(to)
-        if check_layers:
-            kv = kv_view(cfg, it.kv, B, it.max_len)
-            posv = np.full(B, pos)
-            for l in range(L):
-                K = kv[l, 0].copy()
-                Vv = kv[l, 1].copy()
-                x1, kn, vn = om.decode_layer(l, hid[l], posv, K, Vv)
-                worst["resid"] = max(worst["resid"], float(np.abs(x1 - hid[l + 1]).max()))
-                u = np.concatenate([bf16_ulps(kn, kv[l, 0, :, :, pos]).ravel(),
-                                    bf16_ulps(vn, kv[l, 1, :, :, pos]).ravel()])
-                worst["kv_ulps"] = max(worst["kv_ulps"], int(u.max()))
-                worst["kv_flip"] = max(worst["kv_flip"], float((u > 0).mean()))
-        ref_logits = om.head(hid[L])
-        worst["logit"] = max(worst["logit"], float(np.abs(ref_logits - lg).max()))
+        kv = kv_view(cfg, it.kv, B, it.max_len)
+        posv = np.full(B, pos)
+        for l in range(L):
+            x64, k64, v64 = om.decode_layer(l, hid[l], posv, kv[l, 0].copy(), kv[l, 1].copy())
+            x32, k32, v32 = om32.decode_layer(l, hid[l], posv, kv[l, 0].astype(np.float32),
+                                              kv[l, 1].astype(np.float32))
+            pool.add("x", hid[l + 1], x64, x32)
+            pool.add("k", kv[l, 0, :, :, pos], k64, k32, bf16=True)
+            pool.add("v", kv[l, 1, :, :, pos], v64, v32, bf16=True)
+        worst_logit = max(worst_logit, float(np.abs(om.head(hid[L]) - lg).max()))
         for b in range(B):
             t, lp, margin = oracle.sample_token(lg[b].astype(np.float64), w.temperature, w.top_k,
                                                 it.sampling.seed, 1 + s, b)
             if margin < 1e-4:
-                worst["near"] += 1
+                near += 1
                 continue
             assert to[b] == t, (s, b)
             assert abs(lo[b] - lp) <= 1e-5
-    say("stage-local worst:", worst)
-    assert worst["resid"] <= RESID_TOL
-    assert worst["kv_ulps"] <= 1
-    assert worst["logit"] <= LOGIT_TOL
-    return np.stack(toks, 1), worst
+    ok, stats = pool.check()
+    say("decode stage-local:", stats, "head logit err", worst_logit, "near ties", near)
+    assert ok
+    assert worst_logit <= LOGIT_TOL
+    return np.stack(toks, 1)
+
+
+def _prefill_stage_local(w, host, model, it):
+    """Prefill with every layer fed the GPU's own residual stream."""
+    cfg = w.model
+    L, d, P, Tp = cfg.n_layers, cfg.d_model, w.n_prompts, w.prompt_len
+    lg0 = torch.empty(P, cfg.vocab, device="cuda")
+    hid = torch.empty(L + 1, P * Tp, d, device="cuda")
+    it.prefill(logits_dbg=lg0, hidden_dbg=hid)
+    torch.cuda.synchronize()
+    hid = hid.double().cpu().numpy().reshape(L + 1, P, Tp, d)
+    kv = kv_view(cfg, it.kv, it.B, it.max_len)
+    lg0 = lg0.cpu().numpy()
+    om = oracle.OracleModel(cfg, host)
+    om32 = oracle.OracleModel(cfg, host, precision="fp32")
+    prompts = synth.make_prompts(w)
+    pool = FloorPool()
+    worst_logit, e2e = 0.0, 0.0
+    for p in range(P):
+        for l in range(L):
+            x64, k64, v64 = om.layer(l, hid[l, p])
+            x32, k32, v32 = om32.layer(l, hid[l, p])
+            pool.add("x", hid[l + 1, p], x64, x32)
+            pool.add("k", kv[l, 0, p * w.group, :, :Tp], k64, k32, bf16=True)
+            pool.add("v", kv[l, 1, p * w.group, :, :Tp], v64, v32, bf16=True)
+        worst_logit = max(worst_logit, float(np.abs(om.head(hid[L, p, -1:])[0] - lg0[p]).max()))
+        e2e = max(e2e, float(np.abs(om.forward(prompts[p])[0][-1] - lg0[p]).max()))
+    ok, stats = pool.check()
+    say("prefill stage-local:", stats, "head logit err", worst_logit,
+        "end-to-end logit err (reported)", e2e)
+    assert ok
+    assert worst_logit <= LOGIT_TOL
 
 
 @pytest.fixture(scope="module")
@@ -112,9 +144,12 @@ def test_small_end_to_end(small):
         say("prefill logits", p, e)
         assert e <= LOGIT_TOL
         kv = kv_view(w.model, it.kv, it.B, it.max_len)
-        u = bf16_ulps(kv[0, 0, p * w.group, :, : w.prompt_len], kvp[0][0])
-        say("layer-0 K ulps max", int(u.max()), "flip frac", float((u > 0).mean()))
-        assert u.max() <= 1
+        g, r = kv[0, 0, p * w.group, :, : w.prompt_len], kvp[0][0]
+        r32 = oracle.OracleModel(w.model, host, precision="fp32").forward(prompts[p])[1][0][0]
+        u = bf16_ulps(g, r)
+        ok, st = floor_check(g, r, r32, bf16=True)
+        say("layer-0 K ulps max", int(u.max()), "flip frac", float((u > 0).mean()), st)
+        assert ok
     # rollout log-probs vs the teacher-forced oracle (same token history)
     lp_gpu = it.logp_old.cpu().numpy()
     e = np.abs(lp_gpu - ref["logp"]).max()
@@ -141,15 +176,15 @@ def test_small_stage_local(small):
     say("small stage-local")
     it = GrpoIteration(w, model, None, synth.make_prompts(w), synth.make_rewards(w),
                        synth.make_seed(w))
-    it.prefill()
+    _prefill_stage_local(w, host, model, it)
     _stage_local(w, host, model, it, 3)
 
 
 @pytest.mark.parametrize("name,layers,kw", [
-    ("1b", 2, dict(n_prompts=1, group=4, prompt_len=70, new_tokens=3, temperature=0.8,
+    ("1b", 2, dict(n_prompts=2, group=4, prompt_len=70, new_tokens=4, temperature=0.8,
                    top_k=50)),
-    ("7b", 1, dict(n_prompts=1, group=3, prompt_len=65, new_tokens=3)),
-    ("32b", 1, dict(n_prompts=1, group=2, prompt_len=40, new_tokens=2)),
+    ("7b", 1, dict(n_prompts=1, group=8, prompt_len=65, new_tokens=5)),
+    ("32b", 1, dict(n_prompts=1, group=8, prompt_len=40, new_tokens=5)),
 ])
 def test_full_width_stage_local(name, layers, kw):
     """Layer-truncated models at the 1B/7B/32B widths: every stage fed GPU inputs."""
@@ -159,13 +194,7 @@ def test_full_width_stage_local(name, layers, kw):
     host, model = build_model(w.model, w.master_seed, gain_noise=0.1)
     it = GrpoIteration(w, model, None, synth.make_prompts(w), synth.make_rewards(w),
                        synth.make_seed(w))
-    lg0 = torch.empty(w.n_prompts, w.model.vocab, device="cuda")
-    it.prefill(logits_dbg=lg0)
-    torch.cuda.synchronize()
-    om = oracle.OracleModel(w.model, host)
-    lgp, kvp = om.forward(synth.make_prompts(w)[0])
-    e = np.abs(lg0[0].cpu().numpy() - lgp[-1]).max()
-    say("prefill logits err", e)
-    assert e <= LOGIT_TOL
+    _prefill_stage_local(w, host, model, it)
     _stage_local(w, host, model, it, w.new_tokens - 1)
     model.close()
+
