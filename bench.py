@@ -50,6 +50,33 @@ def score_flops(w) -> float:
     return c.n_layers * per_tok * N * T + attn * N + head * N
 
 
+def kernel_bytes(w) -> dict:
+    """Algorithmic HBM bytes of one step, per decode-side kernel name.
+
+    gemm_decode: every QKV, O and down-projection weight once per decode step,
+    the LM head once per decode step and once for the prefill draw, plus the
+    activation rows read and the fp32 products written.
+    gemm_decode_swiglu: the gate and up weights once per decode step plus a.
+    attn_decode: the K and V of every context position of every sequence per
+    layer, context = position + 1."""
+    c = w.model
+    es = c.elem_bytes
+    B, L, d, f, V = w.batch, c.n_layers, c.d_model, c.d_ffn, c.vocab
+    n_dec = w.new_tokens - 1
+    qkv, o, down = (c.q_dim + 2 * c.kv_dim) * d, d * c.q_dim, d * f
+    gemm_w = L * (qkv + o + down) * es + V * d * es
+    gemm_act = L * B * ((d + c.q_dim + f) * es + (c.q_dim + 2 * c.kv_dim + 2 * d) * 4) \
+        + B * (d * es + V * 4)
+    swiglu = L * (2 * f * d * es + B * (d * es + f * es))
+    kv_layer_tok = 2 * c.kv_dim * es
+    ctx_sum = sum(w.prompt_len + s for s in range(1, n_dec + 1))   # context of decode step s
+    return {
+        "gemm_decode": n_dec * (gemm_w + gemm_act) + V * d * es + w.n_prompts * (d * es + V * 4),
+        "gemm_decode_swiglu": n_dec * swiglu,
+        "attn_decode": L * B * kv_layer_tok * ctx_sum,
+    }
+
+
 def cpu_baseline(w, host, budget_s: float = 15.0) -> dict:
     """The oracle (fp64 NumPy) on a bounded sample: decode steps of up to 8
     sequences at the prompt-length context, all layers + LM head + sampler."""
@@ -95,6 +122,10 @@ def main():
     ap.add_argument("--workload", default="7b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--new-tokens", type=int, default=None,
+                    help="override the workload's sampled tokens (profiling runs)")
+    ap.add_argument("--prompt-len", type=int, default=None,
+                    help="override the workload's prompt length (profiling runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -109,6 +140,10 @@ def main():
     from paper_2510_17158_amd.workloads import get
 
     w = get(args.workload)
+    if args.new_tokens:
+        w = w.with_(new_tokens=args.new_tokens)
+    if args.prompt_len:
+        w = w.with_(prompt_len=args.prompt_len)
     c = w.model
     torch.cuda.set_device(0)
     t = time.perf_counter()
@@ -186,9 +221,24 @@ def main():
         out["scored_tokens_per_s"] = n_models * w.batch * w.total_len / (phases[2] / 1e3)
         out["score_tflops"] = n_models * sf / (phases[2] / 1e3) / 1e12
         out["score_mfma_frac"] = out["score_tflops"] / BF16_PEAK_TFLOPS
-    out["roofline"] = {"bound": "hbm", "achieved": out["decode_step_gbs"], "peak": HBM_PEAK_GBS,
-                       "unit": "GB/s", "frac": out["decode_step_hbm_frac"], "traffic": None,
-                       "kernel": "decode step (all kernels)"}
+    # per-kernel times from a profiled replica of the step (HIP events around
+    # every launch, on the launch stream); the dominant decode kernel sets the
+    # roofline line
+    api.profile_begin()
+    step()
+    torch.cuda.synchronize()
+    prof = api.profile_end()
+    out["kernels_ms"] = {k: {"launches": n, "total_ms": t, "avg_us": 1e3 * t / n}
+                         for k, (n, t) in sorted(prof.items(), key=lambda kv: -kv[1][1])}
+    kb = kernel_bytes(w)
+    dom = max(kb, key=lambda k: prof.get(k, (0, 0.0))[1])
+    n, t = prof[dom]
+    out["roofline"] = {"bound": "hbm", "achieved": kb[dom] / (t / 1e3) / 1e9,
+                       "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                       "frac": kb[dom] / (t / 1e3) / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                       "kernel": dom, "launches": n, "avg_us": 1e3 * t / n,
+                       "algorithmic_bytes_per_launch": kb[dom] / n}
+    out["decode_kernels_gbs"] = {k: kb[k] / (prof[k][1] / 1e3) / 1e9 for k in kb if k in prof}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, host, args.cpu_budget)
     print(json.dumps(out), flush=True)

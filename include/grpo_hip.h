@@ -153,6 +153,10 @@ int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
  *              with GRPO_KV_CAPACITY unless max_pos + n_steps <= max_len; the
  *              kernels additionally never touch positions >= max_len.
  *   tok_out    int32 [B, n_steps];  logp_out  fp32 [B, n_steps]
+ * With n_steps >= 2 and no debug output the step is captured once as a HIP
+ * graph and replayed n_steps times; the graph is kept in the model handle and
+ * recaptured when an argument changes, so a handle must not be used from two
+ * threads at once.
  *   logits_dbg NULL or fp32 [B, vocab]: logits of the last step
  *   hidden_dbg NULL or fp32 [n_layers+1, B, d]: residual stream entering each
  *              layer and leaving the last one, for the last step */
@@ -193,6 +197,16 @@ int grpo_token_loss(const float* logp, const float* logp_old, const float* logp_
                     const uint8_t* mask, const float* adv, int32_t N, int32_t Tr, float clip_eps,
                     float beta, int32_t agg, float* loss_out, float* tok_loss, float* dloss_dlogp,
                     float* stats, void* ws, size_t ws_bytes, void* stream);
+
+/* Kernel timing for benchmarks.  Between grpo_profile_begin and
+ * grpo_profile_end every kernel launch of the library is bracketed by HIP
+ * events on its stream (decode steps run without graph replay meanwhile).
+ * grpo_profile_end synchronises those events and writes NUL-terminated JSON
+ * {"kernel": [launches, total_ms], ...} into json (len bytes); it returns
+ * GRPO_INVALID_ARG if the text does not fit.  Process-wide; not for use while
+ * other threads launch library work. */
+int grpo_profile_begin(void);
+int grpo_profile_end(char* json, size_t len);
 
 #ifdef __cplusplus
 }

@@ -65,6 +65,8 @@ _SIGS = {
     "grpo_advantages": (_I32, [_VP, _I32, _I32, _F32, _VP, _VP]),
     "grpo_token_loss": (_I32, [_VP, _VP, _VP, _VP, _VP, _I32, _I32, _F32, _F32, _I32, _VP, _VP,
                                _VP, _VP, _VP, _SZ, _VP]),
+    "grpo_profile_begin": (_I32, []),
+    "grpo_profile_end": (_I32, [C.c_char_p, _SZ]),
 }
 
 
@@ -223,3 +225,15 @@ def token_loss(logp, logp_old, logp_ref, mask, adv, clip_eps: float, beta: float
                                  N, Tr, clip_eps, beta, agg, _ptr(loss_out), _ptr(tok_loss),
                                  _ptr(dloss_dlogp), _ptr(stats), _ptr(ws),
                                  ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def profile_begin():
+    _check(lib().grpo_profile_begin())
+
+
+def profile_end() -> dict:
+    """Per-kernel {name: (launches, total_ms)} since profile_begin()."""
+    import json
+    buf = C.create_string_buffer(1 << 16)
+    _check(lib().grpo_profile_end(buf, len(buf)))
+    return {k: tuple(v) for k, v in json.loads(buf.value.decode()).items()}

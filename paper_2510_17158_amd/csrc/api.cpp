@@ -6,9 +6,15 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
+#include <cstdint>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
+#include <deque>
+#include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -17,13 +23,82 @@
 
 using namespace grpo;
 
+// A decode step captured as a HIP graph, replayed n_steps times; recaptured
+// when any argument of the call changes.
+struct DecodeGraph {
+  hipGraphExec_t exec = nullptr;
+  hipStream_t capture = nullptr;
+  std::vector<uint64_t> key;
+};
+
 struct grpo_model {
   grpo_config cfg;
   const void* tok_emb;
   std::vector<const void*> attn_norm, wq, wk, wv, wo, mlp_norm, w_gate, w_up, w_down;
   const void* final_norm;
   const void* lm_head;
+  DecodeGraph graph;
 };
+
+// ---- kernel timing (grpo_profile_begin / grpo_profile_end) ----
+namespace {
+struct ProfRec {
+  const char* name;
+  hipEvent_t e0, e1;
+};
+std::atomic<bool> g_prof{false};
+std::mutex g_prof_mu;
+std::deque<ProfRec> g_prof_pending;
+std::vector<hipEvent_t> g_prof_free;
+std::map<std::string, std::pair<long, double>> g_prof_acc;
+
+hipEvent_t prof_event() {
+  if (!g_prof_free.empty()) {
+    hipEvent_t e = g_prof_free.back();
+    g_prof_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// accumulate finished records until at most `keep` are pending (lock held)
+void prof_drain(size_t keep) {
+  while (g_prof_pending.size() > keep) {
+    ProfRec r = g_prof_pending.front();
+    g_prof_pending.pop_front();
+    float ms = 0.f;
+    if (hipEventSynchronize(r.e1) == hipSuccess && hipEventElapsedTime(&ms, r.e0, r.e1) == hipSuccess) {
+      auto& a = g_prof_acc[r.name];
+      a.first += 1;
+      a.second += ms;
+    }
+    g_prof_free.push_back(r.e0);
+    g_prof_free.push_back(r.e1);
+  }
+}
+}  // namespace
+
+namespace grpo {
+bool profiling() { return g_prof.load(std::memory_order_relaxed); }
+
+Prof::Prof(const char* n, hipStream_t s) : name(n), st(s), ev0(nullptr) {
+  if (!profiling()) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  hipEvent_t e = prof_event();
+  if (e && hipEventRecord(e, s) == hipSuccess) ev0 = e;
+}
+
+Prof::~Prof() {
+  if (!ev0) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  hipEvent_t e1 = prof_event();
+  if (!e1 || hipEventRecord(e1, st) != hipSuccess) return;
+  g_prof_pending.push_back(ProfRec{name, (hipEvent_t)ev0, e1});
+  if (g_prof_pending.size() > 8192) prof_drain(4096);
+}
+}  // namespace grpo
 
 namespace {
 
@@ -103,47 +178,89 @@ Layer kv_layer(const grpo_model* m, void* kv, int l, int n_seqs, int max_len) {
   return Layer{base, base + per};
 }
 
-// ---- one GEMM: fp32 path, decode GEMM for few rows, tiled otherwise ----
+// ---- GEMMs: fp32 path, decode GEMM for few rows, tiled otherwise ----
+// The decode GEMM leaves split-K partial products for the consuming kernel
+// (RMSNorm adds residual partials, RoPE adds QKV partials).
 struct GemmScratch {
-  float* part;
-  int* counters;
+  float* part;   // decode-GEMM partial products
 };
 
-int run_gemm(const grpo_model* m, const void* X, int ldx, int M, WStack W, int N, int K, int epi,
-             EpiArgs ep, GemmScratch s, hipStream_t st) {
-  hipError_t e;
-  if (m->cfg.dtype == GRPO_F32) {
-    e = gemm_f32((const float*)X, ldx, M, W, N, K, epi, ep, st);
-  } else if (M <= kSkinnyMax) {
-    const SkinnyPlan p = skinny_plan(M, N, K, epi, kSkinnyTargetWGs);
-    e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, N, K, epi, ep, p, s.part, s.counters, st);
-  } else {
-    e = gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, N, K, epi, ep, st);
-  }
-  if (e != hipSuccess) return fail(GRPO_HIP_ERROR, "GEMM launch failed: %s", hipGetErrorString(e));
-  return GRPO_OK;
+int gemm_fail(hipError_t e) {
+  return fail(GRPO_HIP_ERROR, "GEMM launch failed: %s", hipGetErrorString(e));
 }
 
-// scratch of the decode GEMM for up to B rows, over every GEMM shape of the model
-void skinny_scratch(const grpo_config& c, int B, size_t* part, size_t* counters) {
-  *part = 0;
-  *counters = 0;
-  if (c.dtype == GRPO_F32) return;
-  const int d = c.d_model, f = c.d_ffn;
-  const int shapes[5][3] = {{qdim(c) + 2 * kvdim(c), d, EPI_STORE},
-                            {d, qdim(c), EPI_RESID},
-                            {f, d, EPI_SWIGLU},
-                            {d, f, EPI_RESID},
-                            {c.vocab, d, EPI_STORE}};
-  const int bmax = std::min(std::max(B, 1), kSkinnyMax);
-  const int nbmax = bmax <= 16 ? 16 : bmax <= 32 ? 32 : bmax <= 64 ? 64 : 128;
-  for (int rows = 16; rows <= nbmax; rows *= 2) {
-    for (auto& sh : shapes) {
-      const SkinnyPlan p = skinny_plan(rows, sh[0], sh[1], sh[2], kSkinnyTargetWGs);
-      *part = std::max(*part, p.part_floats);
-      *counters = std::max(*counters, (size_t)p.counters);
-    }
+// x[M, N] += X W^T.  For the decode GEMM the product is left in *pend.
+int gemm_resid(const grpo_model* m, const void* X, int ldx, int M, WStack W, int N, int K,
+               float* x, GemmScratch s, Partials* pend, hipStream_t st) {
+  hipError_t e;
+  *pend = Partials{nullptr, 0, 0, N};
+  if (m->cfg.dtype == GRPO_F32) {
+    e = gemm_f32((const float*)X, ldx, M, W, N, K, EPI_RESID, EpiArgs{x, nullptr, N}, st);
+  } else if (M <= kSkinnyMax) {
+    const SkinnyPlan p = skinny_plan(M, N, K, EPI_PARTIAL, kSkinnyTargetWGs);
+    e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, N, K, EPI_PARTIAL,
+                         EpiArgs{s.part, nullptr, N}, p, st);
+    *pend = Partials{s.part, p.splits, (size_t)M * N, N};
+  } else {
+    e = gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, N, K, EPI_RESID, EpiArgs{x, nullptr, N}, st);
   }
+  return e == hipSuccess ? GRPO_OK : gemm_fail(e);
+}
+
+// out[M, N] = X W^T, possibly as *splits partial arrays *stride floats apart
+// (the first at `out` when there is one split, else in the scratch).
+int gemm_store(const grpo_model* m, const void* X, int ldx, int M, WStack W, int N, int K,
+               float* out, GemmScratch s, int max_splits, const float** res, int* splits,
+               size_t* stride, hipStream_t st) {
+  hipError_t e;
+  *res = out;
+  *splits = 1;
+  *stride = 0;
+  if (m->cfg.dtype == GRPO_F32) {
+    e = gemm_f32((const float*)X, ldx, M, W, N, K, EPI_STORE, EpiArgs{out, nullptr, N}, st);
+  } else if (M <= kSkinnyMax) {
+    const SkinnyPlan p = skinny_plan(M, N, K, EPI_PARTIAL, kSkinnyTargetWGs, max_splits);
+    float* dst = p.splits == 1 ? out : s.part;
+    e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, N, K, EPI_PARTIAL,
+                         EpiArgs{dst, nullptr, N}, p, st);
+    *res = dst;
+    *splits = p.splits;
+    *stride = (size_t)M * N;
+  } else {
+    e = gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, N, K, EPI_STORE, EpiArgs{out, nullptr, N}, st);
+  }
+  return e == hipSuccess ? GRPO_OK : gemm_fail(e);
+}
+
+// a[M, f] = silu(X Wg^T) * (X Wu^T), rounded to the activation dtype
+int gemm_swiglu(const grpo_model* m, const void* X, int ldx, int M, WStack W, int f, int K,
+                void* a, hipStream_t st) {
+  hipError_t e;
+  if (m->cfg.dtype == GRPO_F32) {
+    e = gemm_f32((const float*)X, ldx, M, W, f, K, EPI_SWIGLU, EpiArgs{nullptr, a, f}, st);
+  } else if (M <= kSkinnyMax) {
+    const SkinnyPlan p = skinny_plan(M, f, K, EPI_SWIGLU, kSkinnyTargetWGs);
+    e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, f, K, EPI_SWIGLU, EpiArgs{nullptr, a, f},
+                         p, st);
+  } else {
+    e = gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, f, K, EPI_SWIGLU, EpiArgs{nullptr, a, f}, st);
+  }
+  return e == hipSuccess ? GRPO_OK : gemm_fail(e);
+}
+
+// partial-product scratch of the decode GEMM for up to B rows, over the split
+// shapes of the model (QKV, O and down projections)
+size_t skinny_scratch(const grpo_config& c, int B) {
+  if (c.dtype == GRPO_F32) return 0;
+  const int rows = std::min(std::max(B, 1), kSkinnyMax);
+  const int d = c.d_model, f = c.d_ffn;
+  const int shapes[3][2] = {{qdim(c) + 2 * kvdim(c), d}, {d, qdim(c)}, {d, f}};
+  size_t part = 0;
+  for (auto& sh : shapes) {
+    const SkinnyPlan p = skinny_plan(rows, sh[0], sh[1], EPI_PARTIAL, kSkinnyTargetWGs);
+    part = std::max(part, (size_t)p.splits * rows * sh[0]);
+  }
+  return part;
 }
 
 // ---- workspace layouts ----
@@ -161,10 +278,7 @@ StepWS take_step(Bump& b, const grpo_config& c, int rows, int gemm_rows) {
   w.q = b.take<char>((size_t)rows * qdim(c) * es);
   w.o = b.take<char>((size_t)rows * qdim(c) * es);
   w.a = b.take<char>((size_t)rows * c.d_ffn * es);
-  size_t part, cnt;
-  skinny_scratch(c, gemm_rows, &part, &cnt);
-  w.g.part = b.take<float>(part);
-  w.g.counters = b.take<int>(cnt + 1);
+  w.g.part = b.take<float>(skinny_scratch(c, gemm_rows));
   return w;
 }
 
@@ -172,7 +286,7 @@ struct RolloutWS {
   StepWS s;
   float* logits;
   float* attn_part;
-  size_t n_counters;
+  int32_t* step_ctr;   // decode steps done by the replayed graph
 };
 RolloutWS take_rollout(Bump& b, const grpo_config& c, int B, int max_len) {
   RolloutWS w;
@@ -180,9 +294,7 @@ RolloutWS take_rollout(Bump& b, const grpo_config& c, int B, int max_len) {
   w.logits = b.take<float>((size_t)B * c.vocab);
   const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.head_dim, max_len);
   w.attn_part = b.take<float>(c.dtype == GRPO_F32 ? 0 : ap.part_floats);
-  size_t part, cnt;
-  skinny_scratch(c, B, &part, &cnt);
-  w.n_counters = cnt + 1;
+  w.step_ctr = b.take<int32_t>(1);
   return w;
 }
 
@@ -191,7 +303,6 @@ struct PrefillWS {
   uint16_t* vt;
   void* hl;
   float* logits;
-  size_t n_counters;
 };
 int round8(int t) { return (t + 7) / 8 * 8; }
 PrefillWS take_prefill(Bump& b, const grpo_config& c, int P, int Tp) {
@@ -201,9 +312,6 @@ PrefillWS take_prefill(Bump& b, const grpo_config& c, int P, int Tp) {
   w.vt = b.take<uint16_t>(c.dtype == GRPO_F32 ? 0 : (size_t)P * kvdim(c) * round8(Tp));
   w.hl = b.take<char>((size_t)P * c.d_model * esize(c));
   w.logits = b.take<float>((size_t)P * c.vocab);
-  size_t part, cnt;
-  skinny_scratch(c, (int)std::max<size_t>(M, P), &part, &cnt);
-  w.n_counters = cnt + 1;
   return w;
 }
 
@@ -214,7 +322,6 @@ struct ScoreWS {
   void* kbuf; void* vbuf; uint16_t* vt;
   void* hs;
   float* logits;
-  size_t n_counters;
 };
 ScoreWS take_score(Bump& b, const grpo_config& c, int N, int T) {
   ScoreWS w;
@@ -228,9 +335,6 @@ ScoreWS take_score(Bump& b, const grpo_config& c, int N, int T) {
   w.vt = b.take<uint16_t>(c.dtype == GRPO_F32 ? 0 : (size_t)w.chunk * kvdim(c) * round8(T));
   w.hs = b.take<char>((size_t)w.sub_rows * c.d_model * esize(c));
   w.logits = b.take<float>((size_t)w.sub_rows * c.vocab);
-  size_t part, cnt;
-  skinny_scratch(c, (int)std::max<size_t>(M, w.sub_rows), &part, &cnt);
-  w.n_counters = cnt + 1;
   return w;
 }
 
@@ -243,6 +347,11 @@ WStack gate_up(const grpo_model* m, int l) {
   return WStack{{m->w_gate[l], m->w_up[l], m->w_up[l]}, m->cfg.d_ffn, 2 * m->cfg.d_ffn};
 }
 
+int copy_rows(float* dst, const float* x, size_t n, hipStream_t st) {
+  HIPCHK(hipMemcpyAsync(dst, x, n * 4, hipMemcpyDeviceToDevice, st));
+  return GRPO_OK;
+}
+
 // Layers of a many-row forward (prefill or scoring).  Rows are sequence-major
 // (row = seq * T + t).  K/V go to kc/vc (cache layout with n_slots slots of
 // k_len positions; sequence s at slot s * G) and V also transposed to vt.
@@ -252,6 +361,8 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
   const grpo_config& c = m->cfg;
   const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
   const int N = M / T;
+  Partials pend{nullptr, 0, 0, d};
+  int rc;
   for (int l = 0; l < c.n_layers; ++l) {
     void *kl = kbuf, *vl = vbuf;
     if (kv_or_null) {
@@ -259,36 +370,37 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
       kl = L.k;
       vl = L.v;
     }
-    if (hidden_dbg)
-      HIPCHK(hipMemcpyAsync(hidden_dbg + (size_t)l * M * d, w.x, (size_t)M * d * 4,
-                            hipMemcpyDeviceToDevice, st));
-    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), m->attn_norm[l], M, d, c.rms_eps, w.h, d,
-                   st));
-    int rc = run_gemm(m, w.h, d, M, qkv_stack(m, l), qd + 2 * kvd, d, EPI_STORE,
-                      EpiArgs{w.qkv, nullptr, qd + 2 * kvd}, w.g, st);
-    if (rc) return rc;
+    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), pend, m->attn_norm[l], M, d, c.rms_eps,
+                   w.h, d, st));
+    if (hidden_dbg && (rc = copy_rows(hidden_dbg + (size_t)l * M * d, w.x, (size_t)M * d, st)))
+      return rc;
+    const float* qsrc;
+    int qs;
+    size_t qstride;
+    if ((rc = gemm_store(m, w.h, d, M, qkv_stack(m, l), qd + 2 * kvd, d, w.qkv, w.g, kMaxSplits,
+                         &qsrc, &qs, &qstride, st)))
+      return rc;
     RopeArgs ra{};
     ra.mode = 1; ra.T = T; ra.G = G; ra.pos_arr = nullptr;
     ra.n_heads = c.n_heads; ra.n_kv = c.n_kv_heads; ra.hd = c.head_dim; ra.theta = c.rope_theta;
     ra.kcache = kl; ra.vcache = vl; ra.n_seqs = n_slots; ra.max_len = k_len;
-    ra.vt = vt; ra.vt_len = round8(T);
-    HIPCHK(rope_kv(c.dtype, w.qkv, M, w.q, ra, st));
+    ra.vt = c.dtype == GRPO_F32 ? nullptr : vt; ra.vt_len = round8(T);
+    ra.splits = qs; ra.split_stride = qstride;
+    HIPCHK(rope_kv(c.dtype, qsrc, M, w.q, ra, st));
     HIPCHK(attn_prefill(c.dtype, w.q, kl, c.dtype == GRPO_F32 ? vl : (const void*)vt, N, T,
                         c.n_heads, c.n_kv_heads, c.head_dim, k_len, G, w.o, st));
-    rc = run_gemm(m, w.o, qd, M, one(m->wo[l]), d, qd, EPI_RESID, EpiArgs{w.x, nullptr, d}, w.g,
-                  st);
-    if (rc) return rc;
-    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), m->mlp_norm[l], M, d, c.rms_eps, w.h, d,
-                   st));
-    rc = run_gemm(m, w.h, d, M, gate_up(m, l), f, d, EPI_SWIGLU, EpiArgs{nullptr, w.a, f}, w.g, st);
-    if (rc) return rc;
-    rc = run_gemm(m, w.a, f, M, one(m->w_down[l]), d, f, EPI_RESID, EpiArgs{w.x, nullptr, d}, w.g,
-                  st);
-    if (rc) return rc;
+    if ((rc = gemm_resid(m, w.o, qd, M, one(m->wo[l]), d, qd, w.x, w.g, &pend, st))) return rc;
+    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), pend, m->mlp_norm[l], M, d, c.rms_eps,
+                   w.h, d, st));
+    if ((rc = gemm_swiglu(m, w.h, d, M, gate_up(m, l), f, d, w.a, st))) return rc;
+    if ((rc = gemm_resid(m, w.a, f, M, one(m->w_down[l]), d, f, w.x, w.g, &pend, st))) return rc;
   }
-  if (hidden_dbg)
-    HIPCHK(hipMemcpyAsync(hidden_dbg + (size_t)c.n_layers * M * d, w.x, (size_t)M * d * 4,
-                          hipMemcpyDeviceToDevice, st));
+  if (pend.splits)   // fold the last layer's partial products into the residual stream
+    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), pend, nullptr, M, d, c.rms_eps, nullptr, 0,
+                   st));
+  if (hidden_dbg && (rc = copy_rows(hidden_dbg + (size_t)c.n_layers * M * d, w.x, (size_t)M * d,
+                                    st)))
+    return rc;
   return GRPO_OK;
 }
 
@@ -334,7 +446,42 @@ int grpo_model_create(const grpo_config* cfg, const grpo_weights* w, grpo_model*
 }
 
 int grpo_model_destroy(grpo_model* m) {
+  if (!m) return GRPO_OK;
+  if (m->graph.exec) {
+    (void)hipDeviceSynchronize();
+    (void)hipGraphExecDestroy(m->graph.exec);
+  }
+  if (m->graph.capture) (void)hipStreamDestroy(m->graph.capture);
   delete m;
+  return GRPO_OK;
+}
+
+int grpo_profile_begin(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_acc.clear();
+  g_prof.store(true);
+  return GRPO_OK;
+}
+
+int grpo_profile_end(char* json, size_t len) {
+  std::string out = "{";
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof.store(false);
+    prof_drain(0);
+    bool first = true;
+    for (auto& kv : g_prof_acc) {
+      char buf[256];
+      snprintf(buf, sizeof buf, "%s\"%s\": [%ld, %.6f]", first ? "" : ", ", kv.first.c_str(),
+               kv.second.first, kv.second.second);
+      out += buf;
+      first = false;
+    }
+  }
+  out += "}";
+  if (!json || len == 0) return fail(GRPO_INVALID_ARG, "json buffer is NULL");
+  if (out.size() + 1 > len) return fail(GRPO_INVALID_ARG, "json buffer too small (%zu)", out.size() + 1);
+  memcpy(json, out.c_str(), out.size() + 1);
   return GRPO_OK;
 }
 
@@ -382,16 +529,21 @@ int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
   Bump b(ws);
   PrefillWS w = take_prefill(b, c, P, Tp);
   const int M = P * Tp, d = c.d_model;
-  HIPCHK(fill_i32(w.s.g.counters, w.n_counters, 0, st));
   HIPCHK(embed(c.dtype, m->tok_emb, prompts, M, d, c.vocab, w.s.x, st));
   if (int rc = forward_rows(m, w.s, M, Tp, G, n_seqs, max_len, kv, nullptr, nullptr, w.vt,
                             hidden_dbg, st))
     return rc;
-  HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{0, 1, Tp, Tp - 1}, m->final_norm, P, d, c.rms_eps, w.hl,
-                 d, st));
-  if (int rc = run_gemm(m, w.hl, d, P, one(m->lm_head), c.vocab, d, EPI_STORE,
-                        EpiArgs{w.logits, nullptr, c.vocab}, w.s.g, st))
-    return rc;
+  const Partials none{nullptr, 0, 0, d};
+  HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{0, 1, Tp, Tp - 1}, none, m->final_norm, P, d, c.rms_eps,
+                 w.hl, d, st));
+  {
+    const float* res;
+    int ns;
+    size_t nst;
+    if (int rc = gemm_store(m, w.hl, d, P, one(m->lm_head), c.vocab, d, w.logits, w.s.g, 1, &res,
+                            &ns, &nst, st))
+      return rc;
+  }
   SampleArgs sa{};
   sa.temperature = s->temperature; sa.top_k = s->top_k; sa.seed = s->seed; sa.step = 0;
   sa.G = G; sa.tok_out = tok_out; sa.logp_out = logp_out; sa.out_stride = 1;
@@ -427,58 +579,114 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
   RolloutWS w = take_rollout(b, c, B, max_len);
   const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
   const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.head_dim, max_len);
-  HIPCHK(fill_i32(w.s.g.counters, w.n_counters, 0, st));
-  for (int step = 0; step < n_steps; ++step) {
+  // One decode step on stream `ss`.  In graph mode the Philox step and the output
+  // column come from the device step counter (advanced by the embedding kernel).
+  auto enqueue_step = [&](hipStream_t ss, bool graph, int step) -> int {
     const bool last = step == n_steps - 1;
-    HIPCHK(embed(c.dtype, m->tok_emb, tok, B, d, c.vocab, w.s.x, st));
+    float* hdbg = last ? hidden_dbg : nullptr;
+    int rc;
+    hipStream_t st = ss;
+    HIPCHK(embed(c.dtype, m->tok_emb, tok, B, d, c.vocab, w.s.x, st, graph ? w.step_ctr : nullptr));
+    Partials pend{nullptr, 0, 0, d};
     for (int l = 0; l < c.n_layers; ++l) {
-      if (last && hidden_dbg)
-        HIPCHK(hipMemcpyAsync(hidden_dbg + (size_t)l * B * d, w.s.x, (size_t)B * d * 4,
-                              hipMemcpyDeviceToDevice, st));
       Layer L = kv_layer(m, kv, l, n_seqs, max_len);
-      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), m->attn_norm[l], B, d, c.rms_eps,
-                     w.s.h, d, st));
-      if (int rc = run_gemm(m, w.s.h, d, B, qkv_stack(m, l), qd + 2 * kvd, d, EPI_STORE,
-                            EpiArgs{w.s.qkv, nullptr, qd + 2 * kvd}, w.s.g, st))
+      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), pend, m->attn_norm[l], B, d,
+                     c.rms_eps, w.s.h, d, st));
+      if (hdbg && (rc = copy_rows(hdbg + (size_t)l * B * d, w.s.x, (size_t)B * d, st))) return rc;
+      const float* qsrc;
+      int qs;
+      size_t qstride;
+      if ((rc = gemm_store(m, w.s.h, d, B, qkv_stack(m, l), qd + 2 * kvd, d, w.s.qkv, w.s.g,
+                           kMaxSplits, &qsrc, &qs, &qstride, st)))
         return rc;
       RopeArgs ra{};
       ra.mode = 0; ra.T = 1; ra.G = 1; ra.pos_arr = pos;
       ra.n_heads = c.n_heads; ra.n_kv = c.n_kv_heads; ra.hd = c.head_dim; ra.theta = c.rope_theta;
       ra.kcache = L.k; ra.vcache = L.v; ra.n_seqs = n_seqs; ra.max_len = max_len;
       ra.vt = nullptr; ra.vt_len = 0;
-      HIPCHK(rope_kv(c.dtype, w.s.qkv, B, w.s.q, ra, st));
+      ra.splits = qs; ra.split_stride = qstride;
+      HIPCHK(rope_kv(c.dtype, qsrc, B, w.s.q, ra, st));
       HIPCHK(attn_decode(c.dtype, w.s.q, L.k, L.v, pos, B, c.n_heads, c.n_kv_heads, c.head_dim,
                          n_seqs, max_len, ap, w.attn_part, w.s.o, st));
-      if (int rc = run_gemm(m, w.s.o, qd, B, one(m->wo[l]), d, qd, EPI_RESID,
-                            EpiArgs{w.s.x, nullptr, d}, w.s.g, st))
+      if ((rc = gemm_resid(m, w.s.o, qd, B, one(m->wo[l]), d, qd, w.s.x, w.s.g, &pend, st)))
         return rc;
-      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), m->mlp_norm[l], B, d, c.rms_eps,
+      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), pend, m->mlp_norm[l], B, d, c.rms_eps,
                      w.s.h, d, st));
-      if (int rc = run_gemm(m, w.s.h, d, B, gate_up(m, l), f, d, EPI_SWIGLU,
-                            EpiArgs{nullptr, w.s.a, f}, w.s.g, st))
-        return rc;
-      if (int rc = run_gemm(m, w.s.a, f, B, one(m->w_down[l]), d, f, EPI_RESID,
-                            EpiArgs{w.s.x, nullptr, d}, w.s.g, st))
+      if ((rc = gemm_swiglu(m, w.s.h, d, B, gate_up(m, l), f, d, w.s.a, st))) return rc;
+      if ((rc = gemm_resid(m, w.s.a, f, B, one(m->w_down[l]), d, f, w.s.x, w.s.g, &pend, st)))
         return rc;
     }
-    if (last && hidden_dbg)
-      HIPCHK(hipMemcpyAsync(hidden_dbg + (size_t)c.n_layers * B * d, w.s.x, (size_t)B * d * 4,
-                            hipMemcpyDeviceToDevice, st));
-    HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), m->final_norm, B, d, c.rms_eps, w.s.h, d,
-                   st));
-    if (int rc = run_gemm(m, w.s.h, d, B, one(m->lm_head), c.vocab, d, EPI_STORE,
-                          EpiArgs{w.logits, nullptr, c.vocab}, w.s.g, st))
+    HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), pend, m->final_norm, B, d, c.rms_eps,
+                   w.s.h, d, st));
+    if (hdbg && (rc = copy_rows(hdbg + (size_t)c.n_layers * B * d, w.s.x, (size_t)B * d, st)))
       return rc;
+    {
+      const float* res;
+      int ns;
+      size_t nst;
+      if ((rc = gemm_store(m, w.s.h, d, B, one(m->lm_head), c.vocab, d, w.logits, w.s.g, 1, &res,
+                           &ns, &nst, st)))
+        return rc;
+    }
     SampleArgs sa{};
     sa.temperature = s->temperature; sa.top_k = s->top_k; sa.seed = s->seed;
-    sa.step = step0 + step; sa.G = 1;
-    sa.tok_out = tok_out + step; sa.logp_out = logp_out + step; sa.out_stride = n_steps;
+    sa.G = 1; sa.out_stride = n_steps;
     sa.tok_state = tok; sa.pos_state = pos;
+    if (graph) {
+      sa.step = step0; sa.step_ctr = w.step_ctr;
+      sa.tok_out = tok_out; sa.logp_out = logp_out;
+    } else {
+      sa.step = step0 + step; sa.step_ctr = nullptr;
+      sa.tok_out = tok_out + step; sa.logp_out = logp_out + step;
+    }
     HIPCHK(sample(w.logits, B, c.vocab, c.vocab, sa, st));
     if (last && logits_dbg)
       HIPCHK(hipMemcpyAsync(logits_dbg, w.logits, (size_t)B * c.vocab * 4,
                             hipMemcpyDeviceToDevice, st));
+    return GRPO_OK;
+  };
+
+  const bool use_graph = n_steps >= 2 && !hidden_dbg && !logits_dbg && !profiling() &&
+                         !getenv("GRPO_NO_GRAPH");
+  if (!use_graph) {
+    for (int step = 0; step < n_steps; ++step)
+      if (int rc = enqueue_step(st, false, step)) return rc;
+    g_err.clear();
+    return GRPO_OK;
   }
+  grpo_model* mm = const_cast<grpo_model*>(m);
+  DecodeGraph& dg = mm->graph;
+  const std::vector<uint64_t> key = {
+      (uint64_t)(uintptr_t)kv, (uint64_t)n_seqs, (uint64_t)max_len, (uint64_t)B,
+      (uint64_t)(uintptr_t)pos, (uint64_t)(uintptr_t)tok, (uint64_t)step0, (uint64_t)n_steps,
+      (uint64_t)(uintptr_t)tok_out, (uint64_t)(uintptr_t)logp_out, (uint64_t)(uintptr_t)ws,
+      (uint64_t)*(const uint32_t*)&s->temperature, (uint64_t)(uint32_t)s->top_k, s->seed};
+  HIPCHK(fill_i32(w.step_ctr, 1, -1, st));   // the first replay's embedding makes it 0
+  if (!dg.exec || dg.key != key) {
+    if (dg.exec) {
+      HIPCHK(hipStreamSynchronize(st));
+      HIPCHK(hipGraphExecDestroy(dg.exec));
+      dg.exec = nullptr;
+    }
+    if (!dg.capture) HIPCHK(hipStreamCreateWithFlags(&dg.capture, hipStreamNonBlocking));
+    HIPCHK(hipStreamBeginCapture(dg.capture, hipStreamCaptureModeThreadLocal));
+    const int rc = enqueue_step(dg.capture, true, 0);
+    hipGraph_t graph = nullptr;
+    const hipError_t ce = hipStreamEndCapture(dg.capture, &graph);
+    if (rc) {
+      if (graph) (void)hipGraphDestroy(graph);
+      return rc;
+    }
+    if (ce != hipSuccess) return fail(GRPO_HIP_ERROR, "graph capture: %s", hipGetErrorString(ce));
+    const hipError_t ie = hipGraphInstantiate(&dg.exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (ie != hipSuccess) {
+      dg.exec = nullptr;
+      return fail(GRPO_HIP_ERROR, "graph instantiate: %s", hipGetErrorString(ie));
+    }
+    dg.key = key;
+  }
+  for (int step = 0; step < n_steps; ++step) HIPCHK(hipGraphLaunch(dg.exec, st));
   g_err.clear();
   return GRPO_OK;
 }
@@ -503,7 +711,7 @@ int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, 
   Bump b(ws);
   ScoreWS w = take_score(b, c, N, T);
   const int d = c.d_model, Ts = T - score_from;
-  HIPCHK(fill_i32(w.s.g.counters, w.n_counters, 0, st));
+  const Partials none{nullptr, 0, 0, d};
   for (int n0 = 0; n0 < N; n0 += w.chunk) {
     const int C = std::min(w.chunk, N - n0);
     const int M = C * T;
@@ -515,10 +723,13 @@ int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, 
     const int R = C * Ts;
     for (int i0 = 0; i0 < R; i0 += w.sub_rows) {
       const int rc_rows = std::min(w.sub_rows, R - i0);
-      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{i0, Ts, T, score_from - 1}, m->final_norm, rc_rows,
-                     d, c.rms_eps, w.hs, d, st));
-      if (int rc = run_gemm(m, w.hs, d, rc_rows, one(m->lm_head), c.vocab, d, EPI_STORE,
-                            EpiArgs{w.logits, nullptr, c.vocab}, w.s.g, st))
+      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{i0, Ts, T, score_from - 1}, none, m->final_norm,
+                     rc_rows, d, c.rms_eps, w.hs, d, st));
+      const float* res;
+      int ns;
+      size_t nst;
+      if (int rc = gemm_store(m, w.hs, d, rc_rows, one(m->lm_head), c.vocab, d, w.logits, w.s.g, 1,
+                              &res, &ns, &nst, st))
         return rc;
       HIPCHK(token_logprob(w.logits, rc_rows, c.vocab, c.vocab, tk, T, score_from, Ts, i0,
                            temperature, logp_out + (size_t)n0 * Ts + i0, st));

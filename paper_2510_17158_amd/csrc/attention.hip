@@ -383,6 +383,7 @@ hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
   const float scale = 1.f / sqrtf((float)hd);
   if (dtype == 0) {
     dim3 grid(B, H);
+    Prof pf("attn_f32", st);
     k_attn_rows_f32<<<grid, 256, max_len * sizeof(float), st>>>(
         (const float*)q, H * hd, (const float*)kc, (const float*)vc, pos, 1, 1, H, n_kv, hd,
         max_len, scale, (float*)out);
@@ -392,18 +393,25 @@ hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
   float* part_ml = part + (size_t)B * H * p.splits * hd;
   dim3 grid(p.splits, n_kv, B);
   dim3 cgrid(H, B);
-  if (hd == 128) {
-    k_attn_decode_bf16<128><<<grid, 256, 0, st>>>((const bf16_t*)q, (const bf16_t*)kc,
-                                                  (const bf16_t*)vc, pos, H, n_kv, max_len,
-                                                  p.splits, scale, part_o, part_ml);
-    k_attn_combine<128><<<cgrid, 128, 0, st>>>(part_o, part_ml, pos, H, max_len, p.splits,
+  {
+    Prof pf("attn_decode", st);
+    if (hd == 128)
+      k_attn_decode_bf16<128><<<grid, 256, 0, st>>>((const bf16_t*)q, (const bf16_t*)kc,
+                                                    (const bf16_t*)vc, pos, H, n_kv, max_len,
+                                                    p.splits, scale, part_o, part_ml);
+    else
+      k_attn_decode_bf16<64><<<grid, 256, 0, st>>>((const bf16_t*)q, (const bf16_t*)kc,
+                                                   (const bf16_t*)vc, pos, H, n_kv, max_len,
+                                                   p.splits, scale, part_o, part_ml);
+  }
+  {
+    Prof pf("attn_combine", st);
+    if (hd == 128)
+      k_attn_combine<128><<<cgrid, 128, 0, st>>>(part_o, part_ml, pos, H, max_len, p.splits,
+                                                 (bf16_t*)out);
+    else
+      k_attn_combine<64><<<cgrid, 64, 0, st>>>(part_o, part_ml, pos, H, max_len, p.splits,
                                                (bf16_t*)out);
-  } else {
-    k_attn_decode_bf16<64><<<grid, 256, 0, st>>>((const bf16_t*)q, (const bf16_t*)kc,
-                                                 (const bf16_t*)vc, pos, H, n_kv, max_len,
-                                                 p.splits, scale, part_o, part_ml);
-    k_attn_combine<64><<<cgrid, 64, 0, st>>>(part_o, part_ml, pos, H, max_len, p.splits,
-                                             (bf16_t*)out);
   }
   return hipGetLastError();
 }
@@ -415,6 +423,7 @@ hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_o
   const float scale = 1.f / sqrtf((float)hd);
   if (dtype == 0) {
     dim3 grid(N * T, H);
+    Prof pf("attn_f32", st);
     k_attn_rows_f32<<<grid, 256, T * sizeof(float), st>>>(
         (const float*)q, H * hd, (const float*)k, (const float*)v_or_vt, nullptr, T, k_seq_stride,
         H, n_kv, hd, k_len, scale, (float*)out);
@@ -422,6 +431,7 @@ hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_o
   }
   const int vt_len = (T + 7) / 8 * 8;
   dim3 grid((T + 63) / 64, H, N);
+  Prof pf("flash_attn", st);
   if (hd == 128)
     k_flash_bf16<128><<<grid, 256, 0, st>>>((const bf16_t*)q, (const bf16_t*)k,
                                             (const bf16_t*)v_or_vt, T, H, n_kv, k_len,

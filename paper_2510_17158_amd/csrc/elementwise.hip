@@ -10,24 +10,38 @@ namespace grpo {
 namespace {
 
 template <typename T>
-__global__ void k_embed(const T* emb, const int32_t* tok, int d, int vocab, float* x) {
+__global__ void k_embed(const T* emb, const int32_t* tok, int d, int vocab, float* x,
+                        int32_t* ctr) {
   const int m = blockIdx.x;
+  if (ctr && m == 0 && threadIdx.x == 0) *ctr += 1;
   const int t = clampi(tok[m], 0, vocab - 1);
   const T* e = emb + (size_t)t * d;
   for (int i = threadIdx.x; i < d; i += blockDim.x) x[(size_t)m * d + i] = ldf(e, i);
 }
 
+// x += pending split-K partials (split order), then
 // h = round(x * (1 / sqrt(mean(x^2) + eps)) * g); one workgroup per row
 template <typename T>
-__global__ __launch_bounds__(256) void k_rmsnorm(const float* x, int ldx, RowMap rm, const T* g,
-                                                 int d, float eps, T* out, int ldo) {
+__global__ __launch_bounds__(256) void k_rmsnorm(float* x, int ldx, RowMap rm, Partials pp,
+                                                 const T* g, int d, float eps, T* out, int ldo) {
   __shared__ float sh[4];
   const int m = blockIdx.x;
   const int gi = rm.i0 + m;
   const size_t src = (size_t)(gi / rm.per) * rm.stride + rm.off + gi % rm.per;
-  const float* xr = x + src * ldx;
+  float* xr = x + src * ldx;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) ss = fmaf(xr[i], xr[i], ss);
+  if (pp.splits > 0) {
+    const float* pr = pp.part + src * pp.ld;
+    for (int i = threadIdx.x; i < d; i += 256) {
+      float v = xr[i];
+      for (int s = 0; s < pp.splits; ++s) v += pr[s * pp.split_stride + i];
+      xr[i] = v;
+      ss = fmaf(v, v, ss);
+    }
+  } else {
+    for (int i = threadIdx.x; i < d; i += 256) ss = fmaf(xr[i], xr[i], ss);
+  }
+  if (!g) return;
   ss = block_sum<256>(ss, sh);
   const float r = 1.f / sqrtf(ss / (float)d + eps);
   for (int i = threadIdx.x; i < d; i += 256) stf(out, (size_t)m * ldo + i, xr[i] * r * ldf(g, i));
@@ -50,11 +64,19 @@ __global__ void k_rope_kv(const float* qkv, int M, T* q_out, RopeArgs a) {
   const int ldq = heads * a.hd;
   const float* src = qkv + (size_t)m * ldq + h * a.hd;
   float lo = src[i], hi = src[i + half];
+  for (int sp = 1; sp < a.splits; ++sp) {
+    lo += src[sp * a.split_stride + i];
+    hi += src[sp * a.split_stride + i + half];
+  }
   if (h < a.n_heads + a.n_kv) {
-    // angle in fp64: pos * theta^(-2i/hd), then cos/sin rounded to fp32
+    // angle pos * theta^(-2i/hd) in fp64, reduced to [-pi, pi] in fp64 (keeps
+    // sincos on its short path), cos/sin rounded to fp32
     const double inv = pow((double)a.theta, -2.0 * (double)i / (double)a.hd);
+    const double two_pi = 6.283185307179586476925286766559;
+    double ang = (double)pos * inv;
+    ang -= rint(ang / two_pi) * two_pi;
     double sd, cd;
-    sincos((double)pos * inv, &sd, &cd);
+    sincos(ang, &sd, &cd);
     const float c = (float)cd, s = (float)sd;
     const float l2 = lo * c - hi * s;
     const float h2 = hi * c + lo * s;
@@ -114,26 +136,30 @@ __global__ __launch_bounds__(256) void k_token_logprob(const float* logits, int 
 }  // namespace
 
 hipError_t embed(int dtype, const void* emb, const int32_t* tok, int M, int d, int vocab, float* x,
-                 hipStream_t st) {
+                 hipStream_t st, int32_t* ctr) {
   if (M <= 0) return hipSuccess;
-  if (dtype == 0) k_embed<float><<<M, 256, 0, st>>>((const float*)emb, tok, d, vocab, x);
-  else k_embed<bf16_t><<<M, 256, 0, st>>>((const bf16_t*)emb, tok, d, vocab, x);
+  Prof pf("embed", st);
+  if (dtype == 0) k_embed<float><<<M, 256, 0, st>>>((const float*)emb, tok, d, vocab, x, ctr);
+  else k_embed<bf16_t><<<M, 256, 0, st>>>((const bf16_t*)emb, tok, d, vocab, x, ctr);
   return hipGetLastError();
 }
 
-hipError_t rmsnorm(int dtype, const float* x, int ldx, RowMap rows, const void* g, int M, int d,
-                   float eps, void* out, int ldo, hipStream_t st) {
+hipError_t rmsnorm(int dtype, float* x, int ldx, RowMap rows, Partials p, const void* g, int M,
+                   int d, float eps, void* out, int ldo, hipStream_t st) {
   if (M <= 0) return hipSuccess;
+  Prof pf("rmsnorm", st);
   if (dtype == 0)
-    k_rmsnorm<float><<<M, 256, 0, st>>>(x, ldx, rows, (const float*)g, d, eps, (float*)out, ldo);
+    k_rmsnorm<float><<<M, 256, 0, st>>>(x, ldx, rows, p, (const float*)g, d, eps, (float*)out,
+                                        ldo);
   else
-    k_rmsnorm<bf16_t><<<M, 256, 0, st>>>(x, ldx, rows, (const bf16_t*)g, d, eps, (bf16_t*)out,
-                                         ldo);
+    k_rmsnorm<bf16_t><<<M, 256, 0, st>>>(x, ldx, rows, p, (const bf16_t*)g, d, eps,
+                                         (bf16_t*)out, ldo);
   return hipGetLastError();
 }
 
 hipError_t fill_i32(int32_t* p, size_t n, int32_t v, hipStream_t st) {
   if (n == 0) return hipSuccess;
+  Prof pf("fill", st);
   k_fill_i32<<<(int)((n + 255) / 256), 256, 0, st>>>(p, n, v);
   return hipGetLastError();
 }
@@ -143,6 +169,7 @@ hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeAr
   const size_t total = (size_t)M * (a.n_heads + 2 * a.n_kv) * (a.hd / 2);
   if (total == 0) return hipSuccess;
   const int grid = (int)((total + 255) / 256);
+  Prof pf("rope_kv", st);
   if (dtype == 0) k_rope_kv<float><<<grid, 256, 0, st>>>(qkv, M, (float*)q_out, a);
   else k_rope_kv<bf16_t><<<grid, 256, 0, st>>>(qkv, M, (bf16_t*)q_out, a);
   return hipGetLastError();
@@ -153,6 +180,7 @@ hipError_t token_logprob(const float* logits, int R, int V, int ld, const int32_
                          hipStream_t st) {
   if (R <= 0) return hipSuccess;
   const float t = temperature > 0.f ? temperature : 1.f;
+  Prof pf("token_logprob", st);
   k_token_logprob<<<R, 256, 0, st>>>(logits, V, ld, tokens, T, score_from, Ts, i0, t, logp);
   return hipGetLastError();
 }

@@ -12,9 +12,10 @@
 // of one weight row per chunk with 16-byte loads, one chunk ahead of the MFMAs.
 // The contraction order inside a chunk is permuted (lane group g covers
 // k in [g*KC/4, (g+1)*KC/4)); X is read with the same permutation, so the sum is
-// unchanged.  Split-K workgroups write fp32 partials; the last one to finish a
-// tile (integer counter) adds them in split order and runs the epilogue, so the
-// result is deterministic.
+// unchanged.  Split-K workgroups write fp32 partial products [split][B][N]; the
+// kernel that consumes the product (RMSNorm with the residual add, or RoPE)
+// adds the splits in split order.  No cross-workgroup synchronisation, no
+// atomics, and the result is deterministic.
 #include "common.h"
 #include "kernels.h"
 
@@ -29,7 +30,6 @@ struct SkArgs {
   const bf16_t* w0; const bf16_t* w1; const bf16_t* w2; int n1, n2;
   int N, K, kper, tiles, splits;
   float* out_f32; bf16_t* out_act; int ld_out;
-  float* part; int* counters;
 };
 
 __device__ __forceinline__ const bf16_t* wrow(const SkArgs& a, int r) {
@@ -47,7 +47,6 @@ __global__ __launch_bounds__(NT) void k_gemm_skinny(SkArgs a) {
   constexpr int XV = NB * KC / 8 / NT;   // 16-byte X loads per thread per chunk
   static_assert(NLD >= 1 && XV >= 1, "chunk too small");
   __shared__ __attribute__((aligned(16))) bf16_t xs[2][NB * XROW];
-  __shared__ int s_last;
 
   const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
   const int tile = blockIdx.x % a.tiles;
@@ -138,25 +137,6 @@ __global__ __launch_bounds__(NT) void k_gemm_skinny(SkArgs a) {
     }
   __syncthreads();
 
-  if (a.splits > 1) {
-    float* my = a.part + ((size_t)ks * a.tiles + tile) * (64 * NB);
-    for (int i = tid; i < 64 * NB; i += NT) my[i] = ct[i];
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_last = (atomicAdd(&a.counters[tile], 1) == a.splits - 1);
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    for (int i = tid; i < 64 * NB; i += NT) {
-      float t = 0.f;
-      for (int s = 0; s < a.splits; ++s)
-        t += __builtin_nontemporal_load(a.part + ((size_t)s * a.tiles + tile) * (64 * NB) + i);
-      ct[i] = t;
-    }
-    if (tid == 0) a.counters[tile] = 0;   // ready for the next launch
-    __syncthreads();
-  }
-
   // ---- epilogue: consecutive threads take consecutive output columns ----
   if (EPI == EPI_SWIGLU) {
     for (int i = tid; i < 32 * NB; i += NT) {
@@ -169,31 +149,31 @@ __global__ __launch_bounds__(NT) void k_gemm_skinny(SkArgs a) {
       }
     }
   } else {
+    // this split's partial product: out[ks][b][n]
+    float* out = a.out_f32 + (size_t)ks * a.B * a.ld_out;
     for (int i = tid; i < 64 * NB; i += NT) {
       const int r = i % 64, b = i / 64;
       const int n = tile * 64 + r;
-      if (b < a.B && n < a.N) {
-        float* o = a.out_f32 + (size_t)b * a.ld_out + n;
-        if (EPI == EPI_RESID) *o += ct[r * NB + b];
-        else *o = ct[r * NB + b];
-      }
+      if (b < a.B && n < a.N) out[(size_t)b * a.ld_out + n] = ct[r * NB + b];
     }
   }
 }
 
 template <int NB, int KC>
 hipError_t launch_nb(const SkArgs& a, int epi, int grid, hipStream_t st) {
-  switch (epi) {
-    case EPI_STORE: k_gemm_skinny<NB, KC, EPI_STORE><<<grid, NT, 0, st>>>(a); break;
-    case EPI_RESID: k_gemm_skinny<NB, KC, EPI_RESID><<<grid, NT, 0, st>>>(a); break;
-    default: k_gemm_skinny<NB, KC, EPI_SWIGLU><<<grid, NT, 0, st>>>(a); break;
+  if (epi == EPI_SWIGLU) {
+    Prof pf("gemm_decode_swiglu", st);
+    k_gemm_skinny<NB, KC, EPI_SWIGLU><<<grid, NT, 0, st>>>(a);
+  } else {
+    Prof pf("gemm_decode", st);
+    k_gemm_skinny<NB, KC, EPI_PARTIAL><<<grid, NT, 0, st>>>(a);
   }
   return hipGetLastError();
 }
 
 }  // namespace
 
-SkinnyPlan skinny_plan(int B, int N, int K, int epi, int target_wgs) {
+SkinnyPlan skinny_plan(int B, int N, int K, int epi, int target_wgs, int max_splits) {
   SkinnyPlan p{};
   p.nb = B <= 16 ? 16 : B <= 32 ? 32 : B <= 64 ? 64 : 128;
   p.kc = p.nb == 128 ? 128 : 256;
@@ -203,26 +183,23 @@ SkinnyPlan skinny_plan(int B, int N, int K, int epi, int target_wgs) {
   const int nchunk = K / p.kc;
   p.splits = 1;
   if (target_wgs <= 0) target_wgs = 512;
-  for (int d = 1; d <= nchunk && d <= 16; ++d) {
+  // SwiGLU needs complete gate and up sums in one workgroup: never split
+  for (int d = 1; epi != EPI_SWIGLU && d <= nchunk && d <= max_splits; ++d) {
     if (nchunk % d) continue;
     p.splits = d;
     if ((long)p.tiles * d >= target_wgs) break;
   }
-  p.part_floats = p.splits > 1 ? (size_t)p.splits * p.tiles * 64 * p.nb : 0;
-  p.counters = p.tiles;
   return p;
 }
 
 hipError_t gemm_skinny_bf16(const uint16_t* X, int ldx, int B, WStack W, int N, int K, int epi,
-                            EpiArgs ep, const SkinnyPlan& p, float* part, int* counters,
-                            hipStream_t st) {
+                            EpiArgs ep, const SkinnyPlan& p, hipStream_t st) {
   SkArgs a;
   a.X = X; a.ldx = ldx; a.B = B;
   a.w0 = (const bf16_t*)W.w[0]; a.w1 = (const bf16_t*)W.w[1]; a.w2 = (const bf16_t*)W.w[2];
   a.n1 = W.n1; a.n2 = W.n2;
   a.N = N; a.K = K; a.kper = K / p.splits; a.tiles = p.tiles; a.splits = p.splits;
   a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;
-  a.part = part; a.counters = counters;
   const int grid = p.tiles * p.splits;
   if (p.kc == 256) {
     switch (p.nb) {

@@ -248,6 +248,7 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
   a.tiles_n = epi == EPI_SWIGLU ? (N + 63) / 64 : (N + BN - 1) / BN;
   a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;
   const int grid = a.tiles_m * a.tiles_n;
+  Prof pf(epi == EPI_SWIGLU ? "gemm_tiled_swiglu" : "gemm_tiled", st);
   switch (epi) {
     case EPI_STORE: k_gemm_tiled<EPI_STORE><<<grid, NT, 0, st>>>(a); break;
     case EPI_RESID: k_gemm_tiled<EPI_RESID><<<grid, NT, 0, st>>>(a); break;
@@ -264,6 +265,7 @@ hipError_t gemm_f32(const float* X, int ldx, int M, WStack W, int N, int K, int 
   a.n1 = W.n1; a.n2 = W.n2; a.N = N; a.K = K; a.epi = epi;
   a.out_f32 = ep.out_f32; a.out_act = (float*)ep.out_act; a.ld_out = ep.ld_out;
   dim3 grid((N + 63) / 64, (M + 63) / 64);
+  Prof pf("gemm_f32", st);
   k_gemm_f32<<<grid, 256, 0, st>>>(a);
   return hipGetLastError();
 }

@@ -153,6 +153,7 @@ __global__ __launch_bounds__(256) void k_loss_grad(const float* lp, const float*
 
 hipError_t advantages(const float* r, int P, int G, float eps, float* adv, hipStream_t st) {
   if (P <= 0) return hipSuccess;
+  Prof pf("advantages", st);
   k_advantages<<<(P + 63) / 64, 64, 0, st>>>(r, P, G, eps, adv);
   return hipGetLastError();
 }
@@ -163,6 +164,7 @@ hipError_t token_loss(const float* lp, const float* lo, const float* lr, const u
                       hipStream_t st) {
   if (N <= 0) return hipSuccess;
   double* wts = row_ws + (size_t)N * 8;
+  Prof pf("token_loss", st);
   k_loss_rows<<<N, 256, 0, st>>>(lp, lo, lr, mask, adv, Tr, clip_eps, beta, tok_loss, row_ws);
   k_loss_final<<<1, 256, 0, st>>>(row_ws, N, agg, loss, stats, wts);
   if (dl) k_loss_grad<<<N, 256, 0, st>>>(lp, lo, lr, mask, adv, Tr, clip_eps, beta, wts, dl);

@@ -6,7 +6,23 @@
 
 namespace grpo {
 
-enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+// Kernel timing for benchmarks: while profiling is on (grpo_profile_begin),
+// each launch is bracketed by HIP events on its stream and accumulated under
+// its name.  Off, a Prof costs one relaxed flag read.
+struct Prof {
+  Prof(const char* name, hipStream_t st);
+  ~Prof();
+  const char* name;
+  hipStream_t st;
+  void* ev0;
+};
+bool profiling();
+
+// STORE: out = X W^T;  RESID: out += X W^T;  SWIGLU: out = silu(gate) * up;
+// PARTIAL (decode GEMM only): out[split] = this split's share of X W^T, the
+// consumer adds the splits.
+enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_PARTIAL = 3 };
+constexpr int kMaxSplits = 16;
 
 // Up to three weight matrices stacked along the output dimension: output row r
 // belongs to w[0] for r < n1, to w[1] for n1 <= r < n2, else to w[2].
@@ -22,19 +38,17 @@ struct EpiArgs {
 };
 
 // ---- decode GEMM: Y[B, N] = X[B, K] . W[N, K]^T for B <= 128 (bf16 MFMA) ----
-// For EPI_SWIGLU, N is d_ffn and W stacks (gate, up) with n1 = N.
+// epi is EPI_PARTIAL (out_f32 [splits][B][ld_out]) or EPI_SWIGLU (N = d_ffn, W
+// stacks (gate, up) with n1 = N, out_act [B][ld_out], never split).
 struct SkinnyPlan {
   int nb;        // padded batch (16, 32, 64, 128)
   int kc;        // K chunk staged in LDS
   int tiles;     // output tiles
-  int splits;    // split-K factor
-  size_t part_floats;  // partial-sum scratch (floats)
-  int counters;        // tile counters (ints)
+  int splits;    // split-K factor (partial products written)
 };
-SkinnyPlan skinny_plan(int B, int N, int K, int epi, int target_wgs);
+SkinnyPlan skinny_plan(int B, int N, int K, int epi, int target_wgs, int max_splits = kMaxSplits);
 hipError_t gemm_skinny_bf16(const uint16_t* X, int ldx, int B, WStack W, int N, int K, int epi,
-                            EpiArgs ep, const SkinnyPlan& p, float* part, int* counters,
-                            hipStream_t st);
+                            EpiArgs ep, const SkinnyPlan& p, hipStream_t st);
 
 // ---- tiled GEMM for many rows (prefill / scoring): bf16 MFMA -----------------
 hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, int K, int epi,
@@ -46,18 +60,28 @@ hipError_t gemm_f32(const float* X, int ldx, int M, WStack W, int N, int K, int 
 
 // ---- elementwise ---------------------------------------------------------------
 // x[m, :] = emb[tok[m]] (fp32).  tok ids clamped to [0, vocab).
+// ctr (optional): thread 0 adds 1 to *ctr (the decode step counter of a replayed graph).
 hipError_t embed(int dtype, const void* emb, const int32_t* tok, int M, int d, int vocab, float* x,
-                 hipStream_t st);
+                 hipStream_t st, int32_t* ctr = nullptr);
 // Source row of output row m: ((i0 + m) / per) * stride + off + (i0 + m) % per.
 struct RowMap {
   int i0, per, stride, off;
   static RowMap identity() { return RowMap{0, 0x7fffffff, 0, 0}; }
 };
-// out[m] = round(x[src(m)] / sqrt(mean(x^2) + eps) * g).
-hipError_t rmsnorm(int dtype, const float* x, int ldx, RowMap rows, const void* g, int M, int d,
-                   float eps, void* out, int ldo, hipStream_t st);
+// Pending split-K partial products of a residual GEMM: part[s*split_stride + row*ld + i].
+struct Partials {
+  const float* part;
+  int splits;            // 0: nothing pending
+  size_t split_stride;   // floats between splits
+  int ld;
+};
+// With p.splits > 0, first x[src(m)] += sum_s part (split order, written back).
+// Then, if g != NULL, out[m] = round(x[src(m)] / sqrt(mean(x^2) + eps) * g).
+hipError_t rmsnorm(int dtype, float* x, int ldx, RowMap rows, Partials p, const void* g, int M,
+                   int d, float eps, void* out, int ldo, hipStream_t st);
 hipError_t fill_i32(int32_t* p, size_t n, int32_t v, hipStream_t st);
-// Rotary embedding + cache write.  qkv fp32 [M, q_dim + 2 kv_dim].  Row m is
+// Rotary embedding + cache write.  qkv fp32 [M, q_dim + 2 kv_dim], or the sum
+// of `splits` such arrays split_stride floats apart (decode GEMM partials).  Row m is
 // (seq, pos): mode 0: seq = m, pos = pos_arr[m];  mode 1: seq = m / T, pos = m % T.
 // q_out: [M, q_dim] act.  K/V written to cache slots seq*G + g (g < G) at pos
 // (positions >= max_len skipped).  vt (optional) gets V transposed:
@@ -70,6 +94,7 @@ struct RopeArgs {
   void* kcache; void* vcache;   // layer base of K and V: [n_seqs][n_kv][max_len][hd]; V may be NULL
   int n_seqs, max_len;
   uint16_t* vt; int vt_len;
+  int splits; size_t split_stride;
 };
 hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeArgs& a,
                    hipStream_t st);
@@ -100,6 +125,7 @@ struct SampleArgs {
   int out_stride;
   int32_t* tok_state;     // optional [R*G]: also store token here
   int32_t* pos_state;     // optional [R*G]: pos += 1
+  const int32_t* step_ctr;  // optional: Philox step = step + *step_ctr, outputs at column *step_ctr
 };
 hipError_t sample(const float* logits, int R, int V, int ld, const SampleArgs& a, hipStream_t st);
 // Teacher-forced log-prob of scored row m (global index gi = i0 + m over

@@ -66,6 +66,8 @@ __global__ __launch_bounds__(NT) void k_sample(const float* __restrict__ logits,
   __shared__ int s_krem, s_eq, s_cut;
   const int r = blockIdx.x, gdraw = blockIdx.y;
   const int seq = r * a.G + gdraw;
+  const int col = a.step_ctr ? *a.step_ctr : 0;
+  const int step = a.step + col;
   const float* l = logits + (size_t)r * ld;
   const int tid = threadIdx.x;
   const bool greedy = !(a.temperature > 0.f);
@@ -135,7 +137,7 @@ __global__ __launch_bounds__(NT) void k_sample(const float* __restrict__ logits,
     int gi = 0x7fffffff;
     const int nblk = (V + 3) / 4;
     for (int c = tid; c < nblk; c += NT) {
-      const uint4 w = philox4x32_10(make_uint4((uint32_t)c, (uint32_t)a.step, (uint32_t)seq, 0u),
+      const uint4 w = philox4x32_10(make_uint4((uint32_t)c, (uint32_t)step, (uint32_t)seq, 0u),
                                     k0, k1);
       const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
@@ -157,8 +159,8 @@ __global__ __launch_bounds__(NT) void k_sample(const float* __restrict__ logits,
   }
   if (tid == 0) {
     tok = clampi(tok, 0, V - 1);
-    a.tok_out[(size_t)seq * a.out_stride] = tok;
-    a.logp_out[(size_t)seq * a.out_stride] = l[tok] / T - lse;
+    a.tok_out[(size_t)seq * a.out_stride + col] = tok;
+    a.logp_out[(size_t)seq * a.out_stride + col] = l[tok] / T - lse;
     if (a.tok_state) a.tok_state[seq] = tok;
     if (a.pos_state) a.pos_state[seq] += 1;
   }
@@ -169,6 +171,7 @@ __global__ __launch_bounds__(NT) void k_sample(const float* __restrict__ logits,
 hipError_t sample(const float* logits, int R, int V, int ld, const SampleArgs& a, hipStream_t st) {
   if (R <= 0) return hipSuccess;
   dim3 grid(R, a.G);
+  Prof pf("sample", st);
   k_sample<<<grid, NT, 0, st>>>(logits, V, ld, a);
   return hipGetLastError();
 }

@@ -198,3 +198,37 @@ def test_full_width_stage_local(name, layers, kw):
     _stage_local(w, host, model, it, w.new_tokens - 1)
     model.close()
 
+
+
+def test_small_graph_replay_matches_eager(small, monkeypatch):
+    w, host, model = small
+    it = GrpoIteration(w, model, None, synth.make_prompts(w), synth.make_rewards(w),
+                       synth.make_seed(w))
+    outs = []
+    for flag in (None, "1"):
+        if flag:
+            monkeypatch.setenv("GRPO_NO_GRAPH", flag)
+        else:
+            monkeypatch.delenv("GRPO_NO_GRAPH", raising=False)
+        it.prefill()
+        it.decode()
+        torch.cuda.synchronize()
+        outs.append((it.tok_dec.cpu().numpy().copy(), it.logp_dec.cpu().numpy().copy()))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+
+
+def test_profile_counts_launches(small):
+    w, host, model = small
+    it = GrpoIteration(w, model, None, synth.make_prompts(w), synth.make_rewards(w),
+                       synth.make_seed(w))
+    api.profile_begin()
+    it.prefill()
+    it.decode()
+    torch.cuda.synchronize()
+    prof = api.profile_end()
+    say("profile", prof)
+    L, n = w.model.n_layers, w.new_tokens - 1
+    assert prof["attn_decode"][0] == L * n
+    assert prof["gemm_decode_swiglu"][0] == L * n
+    assert all(t >= 0 for _, t in prof.values())

@@ -157,3 +157,25 @@ def test_tiny_resume_and_determinism(tiny):
                      it.sampling, o2, l2, ws=it.ws_roll)
     torch.cuda.synchronize()
     assert np.array_equal(np.concatenate([o1.cpu().numpy(), o2.cpu().numpy()], 1), a)
+
+
+def test_graph_replay_matches_eager(tiny, monkeypatch):
+    """The captured-and-replayed decode step gives the eager step's bits."""
+    w, host, model = tiny
+    w = w.with_(temperature=1.0, new_tokens=7)
+    it = GrpoIteration(w, model, None, synth.make_prompts(w), synth.make_rewards(w), 31)
+    outs = []
+    for flag in (None, "1", None):
+        if flag:
+            monkeypatch.setenv("GRPO_NO_GRAPH", flag)
+        else:
+            monkeypatch.delenv("GRPO_NO_GRAPH", raising=False)
+        it.prefill()
+        it.decode()
+        torch.cuda.synchronize()
+        outs.append((it.tok_dec.cpu().numpy().copy(), it.logp_dec.cpu().numpy().copy(),
+                     it.pos.cpu().numpy().copy()))
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            np.testing.assert_array_equal(a, b)
+    assert np.all(outs[0][2] == w.prompt_len + w.new_tokens - 1)
