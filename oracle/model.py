@@ -56,17 +56,23 @@ def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
 class OracleModel:
     """cfg: any object with the decoder shape attributes (n_layers, d_model, ...).
 
-    precision "fp64" is the oracle.  "fp32" evaluates the same definition with
-    float32 arithmetic and float32 accumulation; it is not a reference but a
-    measuring stick: its distance from the fp64 result is the noise floor that
-    any fp32-accumulating implementation of the same rounding contract shows.
+    precision "fp64" is the oracle.  "fp32" and "fp32-seq" evaluate the same
+    definition with float32 arithmetic; they are not references but measuring
+    sticks: their distance from the fp64 result is the noise floor that an
+    fp32-accumulating implementation of the same rounding contract shows.
+    "fp32" takes BLAS's summation order for the weight products; "fp32-seq"
+    adds 32-term float32 partial products one after the other along the
+    contraction, the order in which matrix-core instructions accumulate.
     """
+
+    MM_CHUNK = 32
 
     def __init__(self, cfg, weights: dict, round_points: bool = True, precision: str = "fp64"):
         self.cfg = cfg
         self.w = weights
         self.bf16 = np.asarray(weights["tok_emb"]).dtype == np.uint16
-        self.dt = {"fp64": np.float64, "fp32": np.float32}[precision]
+        self.dt = {"fp64": np.float64, "fp32": np.float32, "fp32-seq": np.float32}[precision]
+        self.seq_mm = precision == "fp32-seq"
         if self.bf16 and round_points:
             self.R = lambda x: round_bf16(x).astype(self.dt)
         else:
@@ -83,6 +89,17 @@ class OracleModel:
 
     def drop_cache(self):
         self._f64.clear()
+
+    def mm(self, h: np.ndarray, name: str) -> np.ndarray:
+        """h @ W^T for the weight matrix `name` ([out, in])."""
+        W = self.mat(name)
+        if not self.seq_mm:
+            return h @ W.T
+        K = W.shape[1]
+        acc = np.zeros(h.shape[:-1] + (W.shape[0],), np.float32)
+        for k0 in range(0, K, self.MM_CHUNK):
+            acc += h[..., k0:k0 + self.MM_CHUNK] @ W[:, k0:k0 + self.MM_CHUNK].T
+        return acc
 
     def embed(self, tokens) -> np.ndarray:
         a = np.asarray(self.w["tok_emb"])[np.asarray(tokens)]
@@ -116,23 +133,23 @@ class OracleModel:
         pos = np.arange(T)
         p = f"l{l}."
         h = R(rmsnorm(x, self.mat(p + "attn_norm"), c.rms_eps))
-        q = (h @ self.mat(p + "wq").T).reshape(T, H, hd)
-        k = (h @ self.mat(p + "wk").T).reshape(T, Hk, hd)
-        v = (h @ self.mat(p + "wv").T).reshape(T, Hk, hd)
+        q = self.mm(h, p + "wq").reshape(T, H, hd)
+        k = self.mm(h, p + "wk").reshape(T, Hk, hd)
+        v = self.mm(h, p + "wv").reshape(T, Hk, hd)
         q = R(rope(q, pos, c.rope_theta))
         k = R(rope(k, pos, c.rope_theta))
         v = R(v)
         o = causal_attention(q, k, v)
-        x = x + R(o.reshape(T, H * hd)) @ self.mat(p + "wo").T
+        x = x + self.mm(R(o.reshape(T, H * hd)), p + "wo")
         h = R(rmsnorm(x, self.mat(p + "mlp_norm"), c.rms_eps))
-        a = R(silu(h @ self.mat(p + "w_gate").T) * (h @ self.mat(p + "w_up").T))
-        x = x + a @ self.mat(p + "w_down").T
+        a = R(silu(self.mm(h, p + "w_gate")) * self.mm(h, p + "w_up"))
+        x = x + self.mm(a, p + "w_down")
         return x, k.transpose(1, 0, 2).copy(), v.transpose(1, 0, 2).copy()
 
     def head(self, x: np.ndarray) -> np.ndarray:
         """Final RMSNorm + LM head: [n, d] -> [n, V]."""
         h = self.R(rmsnorm(x, self.mat("final_norm"), self.cfg.rms_eps))
-        return h @ self.mat("lm_head").T
+        return self.mm(h, "lm_head")
 
     # -- one decode layer against a KV cache ---------------------------------
     def decode_layer(self, l: int, x: np.ndarray, pos: np.ndarray, K: np.ndarray,
@@ -149,9 +166,9 @@ class OracleModel:
         H, Hk, hd = c.n_heads, c.n_kv_heads, c.head_dim
         p = f"l{l}."
         h = R(rmsnorm(x, self.mat(p + "attn_norm"), c.rms_eps))
-        q = (h @ self.mat(p + "wq").T).reshape(B, H, hd)
-        k = (h @ self.mat(p + "wk").T).reshape(B, Hk, hd)
-        v = (h @ self.mat(p + "wv").T).reshape(B, Hk, hd)
+        q = self.mm(h, p + "wq").reshape(B, H, hd)
+        k = self.mm(h, p + "wk").reshape(B, Hk, hd)
+        v = self.mm(h, p + "wv").reshape(B, Hk, hd)
         o = np.empty((B, H, hd), self.dt)
         k_new = np.empty((B, Hk, hd), self.dt)
         v_new = np.empty((B, Hk, hd), self.dt)
@@ -169,10 +186,10 @@ class OracleModel:
                 pr = np.exp(s - s.max())
                 pr /= pr.sum()
                 o[b, hh] = pr @ V[b, g, : pb + 1, :]
-        x = x + R(o.reshape(B, H * hd)) @ self.mat(p + "wo").T
+        x = x + self.mm(R(o.reshape(B, H * hd)), p + "wo")
         h = R(rmsnorm(x, self.mat(p + "mlp_norm"), c.rms_eps))
-        a = R(silu(h @ self.mat(p + "w_gate").T) * (h @ self.mat(p + "w_up").T))
-        x = x + a @ self.mat(p + "w_down").T
+        a = R(silu(self.mm(h, p + "w_gate")) * self.mm(h, p + "w_up"))
+        x = x + self.mm(a, p + "w_down")
         return x, k_new, v_new
 
     def decode(self, tokens, pos, K: np.ndarray, V: np.ndarray, return_hidden: bool = False):

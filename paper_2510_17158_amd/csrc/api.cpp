@@ -121,7 +121,16 @@ int fail(int code, const char* fmt, ...) {
   } while (0)
 
 constexpr int kSkinnyMax = 128;        // rows handled by the decode GEMM
-constexpr int kSkinnyTargetWGs = 512;  // split-K target grid of the decode GEMM
+// split-K target grid of the decode GEMM (GRPO_DECODE_WGS overrides, for tuning)
+int skinny_target() {
+  static const int v = [] {
+    const char* e = getenv("GRPO_DECODE_WGS");
+    const int x = e ? atoi(e) : 0;
+    return x > 0 ? x : 512;
+  }();
+  return v;
+}
+#define kSkinnyTargetWGs skinny_target()
 constexpr int kScoreTokens = 65536;    // rows per scoring chunk (sequences * T)
 constexpr size_t kLogitBytes = size_t(1) << 30;  // LM-head logits per scoring sub-chunk
 
@@ -160,6 +169,7 @@ int check_config(const grpo_config* c) {
                 c->n_kv_heads);
   if (c->n_heads / c->n_kv_heads > 8)
     return fail(GRPO_UNSUPPORTED, "more than 8 query heads per kv head");
+  if (c->d_model > 8192) return fail(GRPO_UNSUPPORTED, "d_model above 8192");
   const int mult = c->dtype == GRPO_F32 ? 32 : 128;
   if (c->d_model % mult || qdim(*c) % mult || c->d_ffn % mult)
     return fail(GRPO_UNSUPPORTED, "d_model, n_heads*head_dim and d_ffn must be multiples of %d",

@@ -28,6 +28,9 @@ namespace {
 constexpr int TC = 256;  // decode positions per split
 
 // ---------------------------------------------------------------- decode, bf16
+// All K and V loads of the split are issued before any arithmetic (K straight
+// into MFMA operand registers, V into the registers P.V consumes), so the
+// workgroup keeps its whole 2 x 64 KB tile in flight.
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
@@ -36,12 +39,11 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   constexpr int QSTEPS = HD / 32;     // MFMA k-steps over the head dim
   constexpr int LPT = HD / 8;         // lanes per position in P.V
   constexpr int PPW = 64 / LPT;       // positions per wave per P.V step
+  constexpr int NV = TC / (4 * PPW);  // V loads per lane
   constexpr int MAXG = 8;
-  __shared__ float sc[MAXG][TC];
   __shared__ __attribute__((aligned(16))) float pt[TC][MAXG];
   __shared__ float red[4][MAXG * HD];
-  __shared__ float sh[4];
-  __shared__ float s_m[MAXG], s_l[MAXG];
+  __shared__ float wm[4][MAXG], wl[4][MAXG];
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int GQ = H / n_kv;
@@ -52,12 +54,27 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   const size_t head_base = ((size_t)b * n_kv + g) * max_len;
   const bf16_t* kb = kc + head_base * HD;
   const bf16_t* vb = vc + head_base * HD;
-
-  // ---- S = K Q^T on MFMA: A = 16 positions x 32 dims, B = 32 dims x 16 heads ----
   const int lg = lane >> 4;           // lane group: owns dims [lg*HD/4, (lg+1)*HD/4)
+  const int j = lane & 15;            // query head of this lane's MFMA column
+  const int ts = lane / LPT, hg = lane % LPT;
+
+  // ---- issue every load of the split ----
+  u32x4_t kreg[4][QSTEPS];
+#pragma unroll
+  for (int grp = 0; grp < 4; ++grp) {
+    const int t = min(t0 + wave * 64 + grp * 16 + j, ctx - 1);
+    const bf16_t* kp = kb + (size_t)t * HD + lg * (HD / 4);
+#pragma unroll
+    for (int st = 0; st < QSTEPS; ++st) kreg[grp][st] = *(const u32x4_t*)(kp + st * 8);
+  }
+  u32x4_t vreg[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int t = min(t0 + k * 4 * PPW + wave * PPW + ts, ctx - 1);
+    vreg[k] = *(const u32x4_t*)(vb + (size_t)t * HD + hg * 8);
+  }
   bf16x8_t qf[QSTEPS];
   {
-    const int j = lane & 15;
     const bf16_t* qp = q + ((size_t)b * H + g * GQ + min(j, GQ - 1)) * HD + lg * (HD / 4);
 #pragma unroll
     for (int st = 0; st < QSTEPS; ++st) {
@@ -66,93 +83,101 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
       qf[st] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
+
+  // ---- S = K Q^T on MFMA: lane holds positions grp*16 + 4*lg + v of head j ----
+  float sv[4][4];
+  float mx = -INFINITY;
 #pragma unroll
   for (int grp = 0; grp < 4; ++grp) {
-    const int tl = wave * 64 + grp * 16 + (lane & 15);
-    const int t = min(t0 + tl, ctx - 1);
-    const bf16_t* kp = kb + (size_t)t * HD + lg * (HD / 4);
-    u32x4_t kv[QSTEPS];
-#pragma unroll
-    for (int st = 0; st < QSTEPS; ++st) kv[st] = *(const u32x4_t*)(kp + st * 8);
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int st = 0; st < QSTEPS; ++st)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kv[st]), qf[st],
-                                                    acc, 0, 0, 0);
-    const int j = lane & 15;
-    if (j < GQ) {
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kreg[grp][st]),
+                                                    qf[st], acc, 0, 0, 0);
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int tt = wave * 64 + grp * 16 + lg * 4 + v;
-        sc[j][tt] = (t0 + tt < ctx) ? acc[v] * scale : -INFINITY;
-      }
+    for (int v = 0; v < 4; ++v) {
+      const int tt = wave * 64 + grp * 16 + lg * 4 + v;
+      const float sc = (t0 + tt < ctx) ? acc[v] * scale : -INFINITY;
+      sv[grp][v] = sc;
+      mx = fmaxf(mx, sc);
     }
   }
+  // per-head max: over this lane's 16 values, then the 4 lane groups, then the waves
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  if (lg == 0 && j < MAXG) wm[wave][j] = mx;
+  __syncthreads();
+  const float m = (j < GQ) ? fmaxf(fmaxf(wm[0][j], wm[1][j]), fmaxf(wm[2][j], wm[3][j])) : 0.f;
+  float sum = 0.f;
+#pragma unroll
+  for (int grp = 0; grp < 4; ++grp)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const float p = (sv[grp][v] == -INFINITY) ? 0.f : __expf(sv[grp][v] - m);
+      sum += p;
+      if (j < GQ) pt[wave * 64 + grp * 16 + lg * 4 + v][j] = p;
+    }
+  sum += __shfl_xor(sum, 16, 64);
+  sum += __shfl_xor(sum, 32, 64);
+  if (lg == 0 && j < MAXG) wl[wave][j] = sum;
   __syncthreads();
 
-  // ---- softmax statistics per head over this split ----
-  for (int j = 0; j < GQ; ++j) {
-    const float s = sc[j][tid];
-    const float m = block_max<256>(s, sh);
-    const float e = (s == -INFINITY) ? 0.f : __expf(s - m);
-    const float l = block_sum<256>(e, sh);
-    pt[tid][j] = e;
-    if (tid == 0) { s_m[j] = m; s_l[j] = l; }
-  }
-  __syncthreads();
-
-  // ---- o = P V on the vector units ----
-  const int ts = lane / LPT, hg = lane % LPT;
+  // ---- o = P V on the vector units, V already in registers ----
   float o[MAXG][8];
 #pragma unroll
-  for (int j = 0; j < MAXG; ++j)
+  for (int jj = 0; jj < MAXG; ++jj)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[j][e] = 0.f;
-  const int nvalid = min(TC, ctx - t0);
-  for (int tt = wave * PPW + ts; tt < nvalid; tt += 4 * PPW) {
-    const u32x4_t raw = *(const u32x4_t*)(vb + (size_t)(t0 + tt) * HD + hg * 8);
+    for (int e = 0; e < 8; ++e) o[jj][e] = 0.f;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int tt = k * 4 * PPW + wave * PPW + ts;
+    const u32x4_t raw = vreg[k];
     float v[8];
-    v[0] = __uint_as_float(raw[0] << 16); v[1] = __uint_as_float(raw[0] & 0xffff0000u);
-    v[2] = __uint_as_float(raw[1] << 16); v[3] = __uint_as_float(raw[1] & 0xffff0000u);
-    v[4] = __uint_as_float(raw[2] << 16); v[5] = __uint_as_float(raw[2] & 0xffff0000u);
-    v[6] = __uint_as_float(raw[3] << 16); v[7] = __uint_as_float(raw[3] & 0xffff0000u);
 #pragma unroll
-    for (int j = 0; j < MAXG; ++j) {
-      if (j < GQ) {
-        const float p = pt[tt][j];
+    for (int e = 0; e < 4; ++e) {
+      v[2 * e] = __uint_as_float(raw[e] << 16);
+      v[2 * e + 1] = __uint_as_float(raw[e] & 0xffff0000u);
+    }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[j][e] = fmaf(p, v[e], o[j][e]);
+    for (int jj = 0; jj < MAXG; ++jj) {
+      if (jj < GQ) {
+        const float p = pt[tt][jj];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[jj][e] = fmaf(p, v[e], o[jj][e]);
       }
     }
   }
   // reduce the positions of a wave (lanes with equal hg), then the 4 waves
 #pragma unroll
-  for (int j = 0; j < MAXG; ++j) {
-    if (j < GQ) {
+  for (int jj = 0; jj < MAXG; ++jj) {
+    if (jj < GQ) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        float x = o[j][e];
+        float x = o[jj][e];
 #pragma unroll
         for (int off = LPT; off < 64; off <<= 1) x += __shfl_xor(x, off, 64);
-        o[j][e] = x;
+        o[jj][e] = x;
       }
     }
   }
   if (ts == 0) {
 #pragma unroll
-    for (int j = 0; j < MAXG; ++j)
-      if (j < GQ) {
+    for (int jj = 0; jj < MAXG; ++jj)
+      if (jj < GQ) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) red[wave][j * HD + hg * 8 + e] = o[j][e];
+        for (int e = 0; e < 8; ++e) red[wave][jj * HD + hg * 8 + e] = o[jj][e];
       }
   }
   __syncthreads();
   for (int i = tid; i < GQ * HD; i += 256) {
-    const int j = i / HD, e = i % HD;
+    const int jj = i / HD, e = i % HD;
     const float x = red[0][i] + red[1][i] + red[2][i] + red[3][i];
-    const size_t row = ((size_t)b * H + g * GQ + j) * S + split;
+    const size_t row = ((size_t)b * H + g * GQ + jj) * S + split;
     part_o[row * HD + e] = x;
-    if (e == 0) { part_ml[row * 2] = s_m[j]; part_ml[row * 2 + 1] = s_l[j]; }
+    if (e == 0) {
+      part_ml[row * 2] = fmaxf(fmaxf(wm[0][jj], wm[1][jj]), fmaxf(wm[2][jj], wm[3][jj]));
+      part_ml[row * 2 + 1] = (wl[0][jj] + wl[1][jj]) + (wl[2][jj] + wl[3][jj]);
+    }
   }
 }
 

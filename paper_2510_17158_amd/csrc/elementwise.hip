@@ -20,31 +20,95 @@ __global__ void k_embed(const T* emb, const int32_t* tok, int d, int vocab, floa
 }
 
 // x += pending split-K partials (split order), then
-// h = round(x * (1 / sqrt(mean(x^2) + eps)) * g); one workgroup per row
+// h = round(x * (1 / sqrt(mean(x^2) + eps)) * g); one workgroup per row.
+// Rows are read as float4 with every load of a thread issued before any use
+// (the row and its partials are a few hundred KB in L2: latency, not bandwidth,
+// bounds this kernel).  d must be a multiple of 4 and at most 4 * NT * VPT.
+constexpr int NORM_NT = 512, NORM_VPT = 4;
+
 template <typename T>
-__global__ __launch_bounds__(256) void k_rmsnorm(float* x, int ldx, RowMap rm, Partials pp,
-                                                 const T* g, int d, float eps, T* out, int ldo) {
-  __shared__ float sh[4];
+__device__ __forceinline__ void store4(T* out, size_t i, float4 v);
+template <>
+__device__ __forceinline__ void store4<float>(float* out, size_t i, float4 v) {
+  *(float4*)(out + i) = v;
+}
+template <>
+__device__ __forceinline__ void store4<bf16_t>(bf16_t* out, size_t i, float4 v) {
+  const uint32_t lo = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+  const uint32_t hi = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  *(uint2*)(out + i) = make_uint2(lo, hi);
+}
+template <typename T>
+__device__ __forceinline__ float4 load4(const T* g, size_t i);
+template <>
+__device__ __forceinline__ float4 load4<float>(const float* g, size_t i) {
+  return *(const float4*)(g + i);
+}
+template <>
+__device__ __forceinline__ float4 load4<bf16_t>(const bf16_t* g, size_t i) {
+  const uint2 u = *(const uint2*)(g + i);
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+}
+
+template <typename T>
+__global__ __launch_bounds__(NORM_NT) void k_rmsnorm(float* x, int ldx, RowMap rm, Partials pp,
+                                                     const T* g, int d, float eps, T* out,
+                                                     int ldo) {
+  __shared__ float sh[NORM_NT / 64];
   const int m = blockIdx.x;
   const int gi = rm.i0 + m;
   const size_t src = (size_t)(gi / rm.per) * rm.stride + rm.off + gi % rm.per;
   float* xr = x + src * ldx;
-  float ss = 0.f;
+  const int n4 = d / 4;
+  float4 v[NORM_VPT];
+#pragma unroll
+  for (int k = 0; k < NORM_VPT; ++k) {
+    const int i4 = threadIdx.x + k * NORM_NT;
+    v[k] = i4 < n4 ? *(const float4*)(xr + 4 * i4) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
   if (pp.splits > 0) {
     const float* pr = pp.part + src * pp.ld;
-    for (int i = threadIdx.x; i < d; i += 256) {
-      float v = xr[i];
-      for (int s = 0; s < pp.splits; ++s) v += pr[s * pp.split_stride + i];
-      xr[i] = v;
-      ss = fmaf(v, v, ss);
+    for (int sp = 0; sp < pp.splits; ++sp) {
+      float4 t[NORM_VPT];
+#pragma unroll
+      for (int k = 0; k < NORM_VPT; ++k) {
+        const int i4 = threadIdx.x + k * NORM_NT;
+        t[k] = i4 < n4 ? *(const float4*)(pr + sp * pp.split_stride + 4 * i4)
+                       : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int k = 0; k < NORM_VPT; ++k) {
+        v[k].x += t[k].x; v[k].y += t[k].y; v[k].z += t[k].z; v[k].w += t[k].w;
+      }
     }
-  } else {
-    for (int i = threadIdx.x; i < d; i += 256) ss = fmaf(xr[i], xr[i], ss);
+#pragma unroll
+    for (int k = 0; k < NORM_VPT; ++k) {
+      const int i4 = threadIdx.x + k * NORM_NT;
+      if (i4 < n4) *(float4*)(xr + 4 * i4) = v[k];
+    }
   }
   if (!g) return;
-  ss = block_sum<256>(ss, sh);
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < NORM_VPT; ++k) {
+    ss = fmaf(v[k].x, v[k].x, ss);
+    ss = fmaf(v[k].y, v[k].y, ss);
+    ss = fmaf(v[k].z, v[k].z, ss);
+    ss = fmaf(v[k].w, v[k].w, ss);
+  }
+  ss = block_sum<NORM_NT>(ss, sh);
   const float r = 1.f / sqrtf(ss / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += 256) stf(out, (size_t)m * ldo + i, xr[i] * r * ldf(g, i));
+#pragma unroll
+  for (int k = 0; k < NORM_VPT; ++k) {
+    const int i4 = threadIdx.x + k * NORM_NT;
+    if (i4 < n4) {
+      const float4 gv = load4(g, 4 * (size_t)i4);
+      store4(out, (size_t)m * ldo + 4 * i4,
+             make_float4(v[k].x * r * gv.x, v[k].y * r * gv.y, v[k].z * r * gv.z,
+                         v[k].w * r * gv.w));
+    }
+  }
 }
 
 // one thread per (row, head, rotation pair); q heads first, then k heads, then v
@@ -147,13 +211,14 @@ hipError_t embed(int dtype, const void* emb, const int32_t* tok, int M, int d, i
 hipError_t rmsnorm(int dtype, float* x, int ldx, RowMap rows, Partials p, const void* g, int M,
                    int d, float eps, void* out, int ldo, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  Prof pf("rmsnorm", st);
+  Prof pf(M <= 128 ? "rmsnorm" : "rmsnorm_rows", st);
+  if (d % 4 || d > 4 * NORM_NT * NORM_VPT) return hipErrorInvalidValue;
   if (dtype == 0)
-    k_rmsnorm<float><<<M, 256, 0, st>>>(x, ldx, rows, p, (const float*)g, d, eps, (float*)out,
-                                        ldo);
+    k_rmsnorm<float><<<M, NORM_NT, 0, st>>>(x, ldx, rows, p, (const float*)g, d, eps,
+                                            (float*)out, ldo);
   else
-    k_rmsnorm<bf16_t><<<M, 256, 0, st>>>(x, ldx, rows, p, (const bf16_t*)g, d, eps,
-                                         (bf16_t*)out, ldo);
+    k_rmsnorm<bf16_t><<<M, NORM_NT, 0, st>>>(x, ldx, rows, p, (const bf16_t*)g, d, eps,
+                                             (bf16_t*)out, ldo);
   return hipGetLastError();
 }
 
@@ -169,7 +234,7 @@ hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeAr
   const size_t total = (size_t)M * (a.n_heads + 2 * a.n_kv) * (a.hd / 2);
   if (total == 0) return hipSuccess;
   const int grid = (int)((total + 255) / 256);
-  Prof pf("rope_kv", st);
+  Prof pf(a.mode == 0 ? "rope_kv" : "rope_kv_rows", st);
   if (dtype == 0) k_rope_kv<float><<<grid, 256, 0, st>>>(qkv, M, (float*)q_out, a);
   else k_rope_kv<bf16_t><<<grid, 256, 0, st>>>(qkv, M, (bf16_t*)q_out, a);
   return hipGetLastError();

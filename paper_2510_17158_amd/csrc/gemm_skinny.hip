@@ -9,7 +9,8 @@
 // Work split: a workgroup of 4 waves owns 64 weight rows (a 32-row output tile of
 // (gate, up) pairs for SwiGLU) and one K range.  The activation chunk X[:, k..k+KC)
 // is staged once in LDS and shared by the 4 waves; each lane streams 2*KC/4 bytes
-// of one weight row per chunk with 16-byte loads, one chunk ahead of the MFMAs.
+// of one weight row per chunk with 16-byte loads, up to three chunks ahead of the
+// MFMAs.
 // The contraction order inside a chunk is permuted (lane group g covers
 // k in [g*KC/4, (g+1)*KC/4)); X is read with the same permutation, so the sum is
 // unchanged.  Split-K workgroups write fp32 partial products [split][B][N]; the
@@ -45,6 +46,7 @@ __global__ __launch_bounds__(NT) void k_gemm_skinny(SkArgs a) {
   constexpr int NLD = LPR / 8;           // 16-byte loads per lane per chunk
   constexpr int XROW = KC + 8;           // padded LDS row (elements)
   constexpr int XV = NB * KC / 8 / NT;   // 16-byte X loads per thread per chunk
+  constexpr int WSTAGES = NB >= 128 ? 3 : 4;
   static_assert(NLD >= 1 && XV >= 1, "chunk too small");
   __shared__ __attribute__((aligned(16))) bf16_t xs[2][NB * XROW];
 
@@ -89,25 +91,34 @@ __global__ __launch_bounds__(NT) void k_gemm_skinny(SkArgs a) {
 #pragma unroll
   for (int j = 0; j < NJ; ++j) acc[j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
-  u32x4_t wcur[NLD], wnxt[NLD], xr[XV];
+  // WSTAGES weight stages in registers: chunk c is multiplied while chunks
+  // c+1 .. c+WSTAGES-1 are in flight.  X chunk c+1 is requested before the
+  // youngest weight chunk so that waiting for X (needed at the end of the
+  // iteration) does not wait for the younger weight loads.
+  u32x4_t wst[WSTAGES][NLD], xr[XV];
 #pragma unroll
-  for (int i = 0; i < NLD; ++i) wcur[i] = *(const u32x4_t*)(wp + i * 8);
-  load_x(0, xr);
+  for (int p = 0; p < WSTAGES - 1; ++p) {
+    if (p < nchunk) {
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) wst[p][i] = *(const u32x4_t*)(wp + p * KC + i * 8);
+    }
+    if (p == 0) load_x(0, xr);
+  }
   store_x(0, xr);
   __syncthreads();
 
   for (int c = 0; c < nchunk; ++c) {
     const int buf = c & 1;
-    const bool more = c + 1 < nchunk;
-    if (more) {
+    if (c + 1 < nchunk) load_x(c + 1, xr);
+    if (c + WSTAGES - 1 < nchunk) {
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) wnxt[i] = *(const u32x4_t*)(wp + (c + 1) * KC + i * 8);
-      load_x(c + 1, xr);
+      for (int i = 0; i < NLD; ++i)
+        wst[WSTAGES - 1][i] = *(const u32x4_t*)(wp + (c + WSTAGES - 1) * KC + i * 8);
     }
     const bf16_t* xb = &xs[buf][0];
 #pragma unroll
     for (int s = 0; s < NLD; ++s) {
-      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, wcur[s]);
+      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, wst[0][s]);
       const int col = (lane >> 4) * LPR + s * 8;
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
@@ -116,11 +127,11 @@ __global__ __launch_bounds__(NT) void k_gemm_skinny(SkArgs a) {
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc[j], 0, 0, 0);
       }
     }
-    if (more) {
-      store_x(buf ^ 1, xr);
+    if (c + 1 < nchunk) store_x(buf ^ 1, xr);
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) wcur[i] = wnxt[i];
-    }
+    for (int p = 0; p < WSTAGES - 1; ++p)
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) wst[p][i] = wst[p + 1][i];
     __syncthreads();
   }
 
@@ -176,9 +187,7 @@ hipError_t launch_nb(const SkArgs& a, int epi, int grid, hipStream_t st) {
 SkinnyPlan skinny_plan(int B, int N, int K, int epi, int target_wgs, int max_splits) {
   SkinnyPlan p{};
   p.nb = B <= 16 ? 16 : B <= 32 ? 32 : B <= 64 ? 64 : 128;
-  p.kc = p.nb == 128 ? 128 : 256;
-  if (K % p.kc) p.kc = 128;
-  if (K % p.kc) p.kc = 64;
+  p.kc = 128;
   p.tiles = epi == EPI_SWIGLU ? (N + 31) / 32 : (N + 63) / 64;
   const int nchunk = K / p.kc;
   p.splits = 1;
@@ -201,13 +210,7 @@ hipError_t gemm_skinny_bf16(const uint16_t* X, int ldx, int B, WStack W, int N, 
   a.N = N; a.K = K; a.kper = K / p.splits; a.tiles = p.tiles; a.splits = p.splits;
   a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;
   const int grid = p.tiles * p.splits;
-  if (p.kc == 256) {
-    switch (p.nb) {
-      case 16: return launch_nb<16, 256>(a, epi, grid, st);
-      case 32: return launch_nb<32, 256>(a, epi, grid, st);
-      case 64: return launch_nb<64, 256>(a, epi, grid, st);
-    }
-  } else if (p.kc == 128) {
+  if (p.kc == 128) {
     switch (p.nb) {
       case 16: return launch_nb<16, 128>(a, epi, grid, st);
       case 32: return launch_nb<32, 128>(a, epi, grid, st);

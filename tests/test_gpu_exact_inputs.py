@@ -28,7 +28,8 @@ def _ulp_bf16(r):
 
 
 @pytest.mark.parametrize("name,B,Tp", [("small", 8, 130), ("small", 64, 20), ("small", 5, 33),
-                                       ("small", 100, 9), ("7b", 64, 12), ("7b", 16, 70)])
+                                       ("small", 100, 9), ("7b", 64, 12), ("7b", 16, 70),
+                                       ("7b", 16, 8), ("7b", 100, 1), ("32b", 8, 5)])
 def test_kv_projection_exact_inputs(name, B, Tp):
     require_gpu()
     base = get(name)
@@ -79,4 +80,44 @@ def test_kv_projection_exact_inputs(name, B, Tp):
                     r[tuple(idx[0])])
     say(worst)
     assert all(v == 0 for k_, v in worst.items() if k_.endswith("_bad"))
+    model.close()
+
+
+@pytest.mark.parametrize("name,B", [("7b", 100), ("7b", 300), ("small", 64)])
+def test_rmsnorm_output_through_selection_projection(name, B):
+    """W_k and W_v select coordinates of the normed activation h, so the K/V cache
+    at position 0 (where RoPE is the identity) holds the GPU's h itself: it must be
+    the bf16 rounding of the oracle's h except where the fp64 value lies within
+    fp32 error of a rounding midpoint."""
+    require_gpu()
+    base = get(name)
+    cfg = dataclasses.replace(base.model, n_layers=1)
+    w = dataclasses.replace(truncated(base, 1), model=cfg, n_prompts=B, group=1, prompt_len=1,
+                            new_tokens=2, temperature=0.0, top_k=0)
+    say("norm through selection", name, B)
+    host = synth.make_weights(cfg, 7 + B, gain_noise=0.1)
+    kvd, d = cfg.kv_dim, cfg.d_model
+    one = np.uint16(0x3F80)
+    for t, off in (("wk", 0), ("wv", kvd)):
+        m = np.zeros((kvd, d), np.uint16)
+        m[np.arange(kvd), off + np.arange(kvd)] = one
+        host[f"l0.{t}"] = m
+    dev = api.upload_weights(cfg, host)
+    model = api.Model(cfg, dev)
+    prompts = np.random.default_rng(B).integers(0, cfg.vocab, (B, 1)).astype(np.int32)
+    it = GrpoIteration(w, model, None, prompts, np.zeros(B, np.float32), 5)
+    it.prefill()
+    torch.cuda.synchronize()
+    kv = kv_view(cfg, it.kv, B, it.max_len)
+    got = np.concatenate([kv[0, 0, :, :, 0].reshape(B, kvd), kv[0, 1, :, :, 0].reshape(B, kvd)], 1)
+    om = oracle.OracleModel(cfg, host, round_points=False)
+    h64 = oracle.rmsnorm(om.embed(prompts[:, 0]), om.mat("l0.attn_norm"), cfg.rms_eps)[:, :2 * kvd]
+    ref = oracle.round_bf16(h64)
+    diff = got != ref
+    # distance of the fp64 value from the nearest rounding midpoint, in ulps
+    ulp = _ulp_bf16(ref)
+    mid_dist = np.abs(np.abs(h64 - ref) - 0.5 * ulp) / ulp
+    say("h flips", int(diff.sum()), "of", diff.size, "closest midpoint of a flip",
+        float(mid_dist[diff].max()) if diff.any() else None)
+    assert not np.any(diff & (mid_dist > 1e-3))
     model.close()

@@ -37,6 +37,7 @@ def _stage_local(w, host, model, it, n_steps):
     B, L, d, V = it.B, cfg.n_layers, cfg.d_model, cfg.vocab
     om = oracle.OracleModel(cfg, host)
     om32 = oracle.OracleModel(cfg, host, precision="fp32")
+    om32s = oracle.OracleModel(cfg, host, precision="fp32-seq")
     it.tok.copy_(it.tok0)
     it.pos.fill_(w.prompt_len)
     pool = FloorPool()
@@ -60,11 +61,11 @@ def _stage_local(w, host, model, it, n_steps):
         posv = np.full(B, pos)
         for l in range(L):
             x64, k64, v64 = om.decode_layer(l, hid[l], posv, kv[l, 0].copy(), kv[l, 1].copy())
-            x32, k32, v32 = om32.decode_layer(l, hid[l], posv, kv[l, 0].astype(np.float32),
-                                              kv[l, 1].astype(np.float32))
-            pool.add("x", hid[l + 1], x64, x32)
-            pool.add("k", kv[l, 0, :, :, pos], k64, k32, bf16=True)
-            pool.add("v", kv[l, 1, :, :, pos], v64, v32, bf16=True)
+            f32 = [m.decode_layer(l, hid[l], posv, kv[l, 0].astype(np.float32),
+                                  kv[l, 1].astype(np.float32)) for m in (om32, om32s)]
+            pool.add("x", hid[l + 1], x64, [r[0] for r in f32])
+            pool.add("k", kv[l, 0, :, :, pos], k64, [r[1] for r in f32], bf16=True)
+            pool.add("v", kv[l, 1, :, :, pos], v64, [r[2] for r in f32], bf16=True)
         worst_logit = max(worst_logit, float(np.abs(om.head(hid[L]) - lg).max()))
         for b in range(B):
             t, lp, margin = oracle.sample_token(lg[b].astype(np.float64), w.temperature, w.top_k,
@@ -94,16 +95,17 @@ def _prefill_stage_local(w, host, model, it):
     lg0 = lg0.cpu().numpy()
     om = oracle.OracleModel(cfg, host)
     om32 = oracle.OracleModel(cfg, host, precision="fp32")
+    om32s = oracle.OracleModel(cfg, host, precision="fp32-seq")
     prompts = synth.make_prompts(w)
     pool = FloorPool()
     worst_logit, e2e = 0.0, 0.0
     for p in range(P):
         for l in range(L):
             x64, k64, v64 = om.layer(l, hid[l, p])
-            x32, k32, v32 = om32.layer(l, hid[l, p])
-            pool.add("x", hid[l + 1, p], x64, x32)
-            pool.add("k", kv[l, 0, p * w.group, :, :Tp], k64, k32, bf16=True)
-            pool.add("v", kv[l, 1, p * w.group, :, :Tp], v64, v32, bf16=True)
+            f32 = [m.layer(l, hid[l, p]) for m in (om32, om32s)]
+            pool.add("x", hid[l + 1, p], x64, [r[0] for r in f32])
+            pool.add("k", kv[l, 0, p * w.group, :, :Tp], k64, [r[1] for r in f32], bf16=True)
+            pool.add("v", kv[l, 1, p * w.group, :, :Tp], v64, [r[2] for r in f32], bf16=True)
         worst_logit = max(worst_logit, float(np.abs(om.head(hid[L, p, -1:])[0] - lg0[p]).max()))
         e2e = max(e2e, float(np.abs(om.forward(prompts[p])[0][-1] - lg0[p]).max()))
     ok, stats = pool.check()
@@ -145,7 +147,8 @@ def test_small_end_to_end(small):
         assert e <= LOGIT_TOL
         kv = kv_view(w.model, it.kv, it.B, it.max_len)
         g, r = kv[0, 0, p * w.group, :, : w.prompt_len], kvp[0][0]
-        r32 = oracle.OracleModel(w.model, host, precision="fp32").forward(prompts[p])[1][0][0]
+        r32 = [oracle.OracleModel(w.model, host, precision=pr).forward(prompts[p])[1][0][0]
+               for pr in ("fp32", "fp32-seq")]
         u = bf16_ulps(g, r)
         ok, st = floor_check(g, r, r32, bf16=True)
         say("layer-0 K ulps max", int(u.max()), "flip frac", float((u > 0).mean()), st)
@@ -183,8 +186,8 @@ def test_small_stage_local(small):
 @pytest.mark.parametrize("name,layers,kw", [
     ("1b", 2, dict(n_prompts=2, group=4, prompt_len=70, new_tokens=4, temperature=0.8,
                    top_k=50)),
-    ("7b", 1, dict(n_prompts=1, group=8, prompt_len=65, new_tokens=5)),
-    ("32b", 1, dict(n_prompts=1, group=8, prompt_len=40, new_tokens=5)),
+    ("7b", 1, dict(n_prompts=1, group=8, prompt_len=120, new_tokens=5)),
+    ("32b", 1, dict(n_prompts=1, group=8, prompt_len=96, new_tokens=5)),
 ])
 def test_full_width_stage_local(name, layers, kw):
     """Layer-truncated models at the 1B/7B/32B widths: every stage fed GPU inputs."""

@@ -187,3 +187,7 @@ def test_fp32_noise_floor_variant():
     np.testing.assert_allclose(b0, a0, rtol=0, atol=1e-5 * np.abs(a0).max())
     # with them, most bf16 intermediate values still agree exactly
     assert np.mean(kva[1][0] == kvb[1][0]) > 0.95
+    # the matrix-core-order variant sums the same terms in another order
+    c0, _ = OracleModel(cfg, w, round_points=False, precision="fp32-seq").forward(tokens)
+    assert c0.dtype == np.float32
+    np.testing.assert_allclose(c0, a0, rtol=0, atol=1e-5 * np.abs(a0).max())
