@@ -126,7 +126,18 @@ def main():
                     help="override the workload's sampled tokens (profiling runs)")
     ap.add_argument("--prompt-len", type=int, default=None,
                     help="override the workload's prompt length (profiling runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only copy a 1 GiB device buffer 4 times (HBM counter calibration)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": 1 << 30, "copies": 4}), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
               "the hot path is built and measured on a single MI355X.", file=sys.stderr)
