@@ -302,7 +302,7 @@ RolloutWS take_rollout(Bump& b, const grpo_config& c, int B, int max_len) {
   RolloutWS w;
   w.s = take_step(b, c, B, B);
   w.logits = b.take<float>((size_t)B * c.vocab);
-  const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.head_dim, max_len);
+  const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.n_kv_heads, c.head_dim, max_len);
   w.attn_part = b.take<float>(c.dtype == GRPO_F32 ? 0 : ap.part_floats);
   w.step_ctr = b.take<int32_t>(1);
   return w;
@@ -588,7 +588,7 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
   Bump b(ws);
   RolloutWS w = take_rollout(b, c, B, max_len);
   const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
-  const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.head_dim, max_len);
+  const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.n_kv_heads, c.head_dim, max_len);
   // One decode step on stream `ss`.  In graph mode the Philox step and the output
   // column come from the device step counter (advanced by the embedding kernel).
   auto enqueue_step = [&](hipStream_t ss, bool graph, int step) -> int {

@@ -102,8 +102,10 @@ hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeAr
 // ---- attention -------------------------------------------------------------------
 // Decode: q act [B, H, hd]; cache layer base K/V [n_seqs][n_kv][max_len][hd];
 // attends positions 0..pos[b].  out act [B, H*hd].
+// tc: context positions per span (a multiple of 128); splits: spans per (sequence,
+// kv head); part_floats: fp32 scratch for the span merge (0 with a single span).
 struct DecodeAttnPlan { int tc; int splits; size_t part_floats; };
-DecodeAttnPlan decode_attn_plan(int B, int H, int hd, int max_len);
+DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len);
 hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
                        const int32_t* pos, int B, int H, int n_kv, int hd, int n_seqs, int max_len,
                        const DecodeAttnPlan& p, float* part, void* out, hipStream_t st);

@@ -4,7 +4,8 @@ end to end at the small shape (12 layers, d 768, GQA 12/4) where the bf16
 logit tolerance 2e-2 holds literally.
 
 Prompt length 300 spans three 128-row GEMM tiles, five 64-row attention blocks
-and two 256-position decode splits, each with a ragged tail."""
+and three 128-position decode spans (8 sequences x 4 kv heads is too few pairs
+for a single span), each with a ragged tail."""
 import dataclasses
 
 import numpy as np
@@ -235,3 +236,30 @@ def test_profile_counts_launches(small):
     assert prof["attn_decode"][0] == L * n
     assert prof["gemm_decode_swiglu"][0] == L * n
     assert all(t >= 0 for _, t in prof.values())
+
+
+def test_decode_span_count_does_not_change_results(small):
+    """A KV capacity far above the context gives more decode spans, several of
+    them empty; the logits agree with the tight-capacity run up to the order of
+    the fp32 merge."""
+    w, host, model = small
+    w = w.with_(new_tokens=2)          # one decode step after the prefill draw
+    cfg = w.model
+    outs = []
+    for cap in (None, 2000):
+        it = GrpoIteration(w, model, None, synth.make_prompts(w), synth.make_rewards(w), 11)
+        max_len = it.max_len
+        if cap:
+            max_len = cap
+            it.kv = api.alloc_kv(cfg, it.B, cap)
+            it.ws_roll = api.alloc_workspace(model, api.OP_ROLLOUT, it.B, cap)
+            it.max_len = cap
+        say("span check, kv capacity", max_len)
+        it.prefill()
+        lg = torch.empty(it.B, cfg.vocab, device="cuda")
+        it.decode(logits_dbg=lg)
+        torch.cuda.synchronize()
+        outs.append((lg.cpu().numpy(), it.tok_dec.cpu().numpy()))
+    err = np.abs(outs[0][0] - outs[1][0]).max()
+    say("max |dlogit| between capacities", err)
+    assert err <= 1e-3
