@@ -201,7 +201,7 @@ int gemm_fail(hipError_t e) {
 
 // x[M, N] += X W^T.  For the decode GEMM the product is left in *pend.
 int gemm_resid(const grpo_model* m, const void* X, int ldx, int M, WStack W, int N, int K,
-               float* x, GemmScratch s, Partials* pend, hipStream_t st) {
+               float* x, GemmScratch s, Partials* pend, hipStream_t st, const char* name) {
   hipError_t e;
   *pend = Partials{nullptr, 0, 0, N};
   if (m->cfg.dtype == GRPO_F32) {
@@ -209,7 +209,7 @@ int gemm_resid(const grpo_model* m, const void* X, int ldx, int M, WStack W, int
   } else if (M <= kSkinnyMax) {
     const SkinnyPlan p = skinny_plan(M, N, K, EPI_PARTIAL, kSkinnyTargetWGs);
     e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, N, K, EPI_PARTIAL,
-                         EpiArgs{s.part, nullptr, N}, p, st);
+                         EpiArgs{s.part, nullptr, N, name}, p, st);
     *pend = Partials{s.part, p.splits, (size_t)M * N, N};
   } else {
     e = gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, N, K, EPI_RESID, EpiArgs{x, nullptr, N}, st);
@@ -221,7 +221,7 @@ int gemm_resid(const grpo_model* m, const void* X, int ldx, int M, WStack W, int
 // (the first at `out` when there is one split, else in the scratch).
 int gemm_store(const grpo_model* m, const void* X, int ldx, int M, WStack W, int N, int K,
                float* out, GemmScratch s, int max_splits, const float** res, int* splits,
-               size_t* stride, hipStream_t st) {
+               size_t* stride, hipStream_t st, const char* name) {
   hipError_t e;
   *res = out;
   *splits = 1;
@@ -232,7 +232,7 @@ int gemm_store(const grpo_model* m, const void* X, int ldx, int M, WStack W, int
     const SkinnyPlan p = skinny_plan(M, N, K, EPI_PARTIAL, kSkinnyTargetWGs, max_splits);
     float* dst = p.splits == 1 ? out : s.part;
     e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, N, K, EPI_PARTIAL,
-                         EpiArgs{dst, nullptr, N}, p, st);
+                         EpiArgs{dst, nullptr, N, name}, p, st);
     *res = dst;
     *splits = p.splits;
     *stride = (size_t)M * N;
@@ -250,8 +250,8 @@ int gemm_swiglu(const grpo_model* m, const void* X, int ldx, int M, WStack W, in
     e = gemm_f32((const float*)X, ldx, M, W, f, K, EPI_SWIGLU, EpiArgs{nullptr, a, f}, st);
   } else if (M <= kSkinnyMax) {
     const SkinnyPlan p = skinny_plan(M, f, K, EPI_SWIGLU, kSkinnyTargetWGs);
-    e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, f, K, EPI_SWIGLU, EpiArgs{nullptr, a, f},
-                         p, st);
+    e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, f, K, EPI_SWIGLU,
+                         EpiArgs{nullptr, a, f, "gemm_decode_swiglu"}, p, st);
   } else {
     e = gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, f, K, EPI_SWIGLU, EpiArgs{nullptr, a, f}, st);
   }
@@ -388,7 +388,7 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
     int qs;
     size_t qstride;
     if ((rc = gemm_store(m, w.h, d, M, qkv_stack(m, l), qd + 2 * kvd, d, w.qkv, w.g, kMaxSplits,
-                         &qsrc, &qs, &qstride, st)))
+                         &qsrc, &qs, &qstride, st, "gemm_decode_qkv")))
       return rc;
     RopeArgs ra{};
     ra.mode = 1; ra.T = T; ra.G = G; ra.pos_arr = nullptr;
@@ -399,11 +399,13 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
     HIPCHK(rope_kv(c.dtype, qsrc, M, w.q, ra, st));
     HIPCHK(attn_prefill(c.dtype, w.q, kl, c.dtype == GRPO_F32 ? vl : (const void*)vt, N, T,
                         c.n_heads, c.n_kv_heads, c.head_dim, k_len, G, w.o, st));
-    if ((rc = gemm_resid(m, w.o, qd, M, one(m->wo[l]), d, qd, w.x, w.g, &pend, st))) return rc;
+    if ((rc = gemm_resid(m, w.o, qd, M, one(m->wo[l]), d, qd, w.x, w.g, &pend, st,
+                          "gemm_decode_o"))) return rc;
     HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), pend, m->mlp_norm[l], M, d, c.rms_eps,
                    w.h, d, st));
     if ((rc = gemm_swiglu(m, w.h, d, M, gate_up(m, l), f, d, w.a, st))) return rc;
-    if ((rc = gemm_resid(m, w.a, f, M, one(m->w_down[l]), d, f, w.x, w.g, &pend, st))) return rc;
+    if ((rc = gemm_resid(m, w.a, f, M, one(m->w_down[l]), d, f, w.x, w.g, &pend, st,
+                          "gemm_decode_down"))) return rc;
   }
   if (pend.splits)   // fold the last layer's partial products into the residual stream
     HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), pend, nullptr, M, d, c.rms_eps, nullptr, 0,
@@ -551,7 +553,7 @@ int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
     int ns;
     size_t nst;
     if (int rc = gemm_store(m, w.hl, d, P, one(m->lm_head), c.vocab, d, w.logits, w.s.g, 1, &res,
-                            &ns, &nst, st))
+                            &ns, &nst, st, "gemm_decode_lm_head"))
       return rc;
   }
   SampleArgs sa{};
@@ -607,7 +609,7 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
       int qs;
       size_t qstride;
       if ((rc = gemm_store(m, w.s.h, d, B, qkv_stack(m, l), qd + 2 * kvd, d, w.s.qkv, w.s.g,
-                           kMaxSplits, &qsrc, &qs, &qstride, st)))
+                           kMaxSplits, &qsrc, &qs, &qstride, st, "gemm_decode_qkv")))
         return rc;
       RopeArgs ra{};
       ra.mode = 0; ra.T = 1; ra.G = 1; ra.pos_arr = pos;
@@ -618,12 +620,14 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
       HIPCHK(rope_kv(c.dtype, qsrc, B, w.s.q, ra, st));
       HIPCHK(attn_decode(c.dtype, w.s.q, L.k, L.v, pos, B, c.n_heads, c.n_kv_heads, c.head_dim,
                          n_seqs, max_len, ap, w.attn_part, w.s.o, st));
-      if ((rc = gemm_resid(m, w.s.o, qd, B, one(m->wo[l]), d, qd, w.s.x, w.s.g, &pend, st)))
+      if ((rc = gemm_resid(m, w.s.o, qd, B, one(m->wo[l]), d, qd, w.s.x, w.s.g, &pend, st,
+                          "gemm_decode_o")))
         return rc;
       HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), pend, m->mlp_norm[l], B, d, c.rms_eps,
                      w.s.h, d, st));
       if ((rc = gemm_swiglu(m, w.s.h, d, B, gate_up(m, l), f, d, w.s.a, st))) return rc;
-      if ((rc = gemm_resid(m, w.s.a, f, B, one(m->w_down[l]), d, f, w.s.x, w.s.g, &pend, st)))
+      if ((rc = gemm_resid(m, w.s.a, f, B, one(m->w_down[l]), d, f, w.s.x, w.s.g, &pend, st,
+                          "gemm_decode_down")))
         return rc;
     }
     HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), pend, m->final_norm, B, d, c.rms_eps,
@@ -635,7 +639,7 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
       int ns;
       size_t nst;
       if ((rc = gemm_store(m, w.s.h, d, B, one(m->lm_head), c.vocab, d, w.logits, w.s.g, 1, &res,
-                           &ns, &nst, st)))
+                           &ns, &nst, st, "gemm_decode_lm_head")))
         return rc;
     }
     SampleArgs sa{};
@@ -739,7 +743,7 @@ int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, 
       int ns;
       size_t nst;
       if (int rc = gemm_store(m, w.hs, d, rc_rows, one(m->lm_head), c.vocab, d, w.logits, w.s.g, 1,
-                              &res, &ns, &nst, st))
+                              &res, &ns, &nst, st, "gemm_decode_lm_head"))
         return rc;
       HIPCHK(token_logprob(w.logits, rc_rows, c.vocab, c.vocab, tk, T, score_from, Ts, i0,
                            temperature, logp_out + (size_t)n0 * Ts + i0, st));

@@ -11,8 +11,9 @@
 // is staged once in LDS and shared by the 4 waves; each lane streams 2*KC/4 bytes
 // of one weight row per chunk with 16-byte loads, up to three chunks ahead of the
 // MFMAs.
-// The contraction order inside a chunk is permuted (lane group g covers
-// k in [g*KC/4, (g+1)*KC/4)); X is read with the same permutation, so the sum is
+// The contraction order inside a chunk is permuted (MFMA step s of lane group g
+// covers the 8 elements at 32 s + 8 g, so a load instruction reads 64 contiguous
+// bytes of a weight row); X is read with the same permutation, so the sum is
 // unchanged.  Split-K workgroups write fp32 partial products [split][B][N]; the
 // kernel that consumes the product (RMSNorm with the residual add, or RoPE)
 // adds the splits in split order.  No cross-workgroup synchronisation, no
@@ -31,6 +32,7 @@ struct SkArgs {
   const bf16_t* w0; const bf16_t* w1; const bf16_t* w2; int n1, n2;
   int N, K, kper, tiles, splits;
   float* out_f32; bf16_t* out_act; int ld_out;
+  const char* name;
 };
 
 __device__ __forceinline__ const bf16_t* wrow(const SkArgs& a, int r) {
@@ -64,7 +66,7 @@ __global__ __launch_bounds__(NT) void k_gemm_skinny(SkArgs a) {
   } else {
     row = min(tile * 64 + wave * 16 + (lane & 15), a.N - 1);
   }
-  const bf16_t* wp = wrow(a, row) + k0 + (lane >> 4) * LPR;
+  const bf16_t* wp = wrow(a, row) + k0 + (lane >> 4) * 8;
 
   // X staging: thread -> (batch row, 8-element column group)
   auto load_x = [&](int c, u32x4_t* xr) {
@@ -100,7 +102,7 @@ __global__ __launch_bounds__(NT) void k_gemm_skinny(SkArgs a) {
   for (int p = 0; p < WSTAGES - 1; ++p) {
     if (p < nchunk) {
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) wst[p][i] = *(const u32x4_t*)(wp + p * KC + i * 8);
+      for (int i = 0; i < NLD; ++i) wst[p][i] = *(const u32x4_t*)(wp + p * KC + i * 32);
     }
     if (p == 0) load_x(0, xr);
   }
@@ -113,13 +115,13 @@ __global__ __launch_bounds__(NT) void k_gemm_skinny(SkArgs a) {
     if (c + WSTAGES - 1 < nchunk) {
 #pragma unroll
       for (int i = 0; i < NLD; ++i)
-        wst[WSTAGES - 1][i] = *(const u32x4_t*)(wp + (c + WSTAGES - 1) * KC + i * 8);
+        wst[WSTAGES - 1][i] = *(const u32x4_t*)(wp + (c + WSTAGES - 1) * KC + i * 32);
     }
     const bf16_t* xb = &xs[buf][0];
 #pragma unroll
     for (int s = 0; s < NLD; ++s) {
       const bf16x8_t av = __builtin_bit_cast(bf16x8_t, wst[0][s]);
-      const int col = (lane >> 4) * LPR + s * 8;
+      const int col = s * 32 + (lane >> 4) * 8;
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         const int b = (lane & 15) + 16 * j;
@@ -173,10 +175,10 @@ __global__ __launch_bounds__(NT) void k_gemm_skinny(SkArgs a) {
 template <int NB, int KC>
 hipError_t launch_nb(const SkArgs& a, int epi, int grid, hipStream_t st) {
   if (epi == EPI_SWIGLU) {
-    Prof pf("gemm_decode_swiglu", st);
+    Prof pf(a.name ? a.name : "gemm_decode_swiglu", st);
     k_gemm_skinny<NB, KC, EPI_SWIGLU><<<grid, NT, 0, st>>>(a);
   } else {
-    Prof pf("gemm_decode", st);
+    Prof pf(a.name ? a.name : "gemm_decode", st);
     k_gemm_skinny<NB, KC, EPI_PARTIAL><<<grid, NT, 0, st>>>(a);
   }
   return hipGetLastError();
@@ -209,6 +211,7 @@ hipError_t gemm_skinny_bf16(const uint16_t* X, int ldx, int B, WStack W, int N, 
   a.n1 = W.n1; a.n2 = W.n2;
   a.N = N; a.K = K; a.kper = K / p.splits; a.tiles = p.tiles; a.splits = p.splits;
   a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;
+  a.name = ep.name;
   const int grid = p.tiles * p.splits;
   if (p.kc == 128) {
     switch (p.nb) {

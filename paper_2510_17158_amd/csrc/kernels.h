@@ -35,6 +35,7 @@ struct EpiArgs {
   float* out_f32;       // EPI_STORE: [rows, ld_out] fp32;  EPI_RESID: residual [rows, ld_out]
   void* out_act;        // EPI_SWIGLU: [rows, ld_out] activation dtype
   int ld_out;
+  const char* name = nullptr;  // kernel-timing label of a decode GEMM (a string literal)
 };
 
 // ---- decode GEMM: Y[B, N] = X[B, K] . W[N, K]^T for B <= 128 (bf16 MFMA) ----

@@ -17,7 +17,8 @@ from paper_2510_17158_amd import api, synth
 from paper_2510_17158_amd.runner import GrpoIteration
 from paper_2510_17158_amd.workloads import get, truncated
 
-from gpu_util import FloorPool, bf16_ulps, build_model, floor_check, kv_view, require_gpu, say
+from gpu_util import (FloorPool, bf16_ulps, build_model, floor_check, h_flip_allowance,
+                      kv_view, require_gpu, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -64,9 +65,10 @@ def _stage_local(w, host, model, it, n_steps):
             x64, k64, v64 = om.decode_layer(l, hid[l], posv, kv[l, 0].copy(), kv[l, 1].copy())
             f32 = [m.decode_layer(l, hid[l], posv, kv[l, 0].astype(np.float32),
                                   kv[l, 1].astype(np.float32)) for m in (om32, om32s)]
+            ak, av = h_flip_allowance(om, cfg, l, hid[l])
             pool.add("x", hid[l + 1], x64, [r[0] for r in f32])
-            pool.add("k", kv[l, 0, :, :, pos], k64, [r[1] for r in f32], bf16=True)
-            pool.add("v", kv[l, 1, :, :, pos], v64, [r[2] for r in f32], bf16=True)
+            pool.add("k", kv[l, 0, :, :, pos], k64, [r[1] for r in f32], bf16=True, allow=ak)
+            pool.add("v", kv[l, 1, :, :, pos], v64, [r[2] for r in f32], bf16=True, allow=av)
         worst_logit = max(worst_logit, float(np.abs(om.head(hid[L]) - lg).max()))
         for b in range(B):
             t, lp, margin = oracle.sample_token(lg[b].astype(np.float64), w.temperature, w.top_k,
@@ -104,9 +106,12 @@ def _prefill_stage_local(w, host, model, it):
         for l in range(L):
             x64, k64, v64 = om.layer(l, hid[l, p])
             f32 = [m.layer(l, hid[l, p]) for m in (om32, om32s)]
+            ak, av = h_flip_allowance(om, cfg, l, hid[l, p])      # [Tp, n_kv, hd]
             pool.add("x", hid[l + 1, p], x64, [r[0] for r in f32])
-            pool.add("k", kv[l, 0, p * w.group, :, :Tp], k64, [r[1] for r in f32], bf16=True)
-            pool.add("v", kv[l, 1, p * w.group, :, :Tp], v64, [r[2] for r in f32], bf16=True)
+            pool.add("k", kv[l, 0, p * w.group, :, :Tp], k64, [r[1] for r in f32], bf16=True,
+                     allow=ak.transpose(1, 0, 2))
+            pool.add("v", kv[l, 1, p * w.group, :, :Tp], v64, [r[2] for r in f32], bf16=True,
+                     allow=av.transpose(1, 0, 2))
         worst_logit = max(worst_logit, float(np.abs(om.head(hid[L, p, -1:])[0] - lg0[p]).max()))
         e2e = max(e2e, float(np.abs(om.forward(prompts[p])[0][-1] - lg0[p]).max()))
     ok, stats = pool.check()
