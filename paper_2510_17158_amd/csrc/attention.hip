@@ -15,12 +15,10 @@
 // otherwise each span writes (max, sum, unnormalised o) and a second kernel
 // merges the spans in span order.
 //
-// Prefill / scoring (bf16): flash attention.  One workgroup per (64 queries,
-// head, sequence), 16 query rows per wave; K tiles and transposed V tiles
-// (written transposed by the rotary kernel) staged in LDS; S = Q K^T and
-// O += P V on v_mfma_f32_16x16x32_bf16 with an fp32 online softmax; P enters
-// the second product as a sum of two bf16 terms, so no extra rounding point is
-// introduced.  Key tiles above the diagonal are skipped.
+// Prefill / scoring (bf16): flash attention, one workgroup per (32 queries, kv
+// head, sequence) with one wave per query head of the group sharing the K and
+// V^T tiles (V^T is written transposed by the rotary kernel); details at the
+// kernel.
 //
 // fp32 models use a plain vector kernel (one workgroup per query row and head).
 #include <algorithm>
@@ -260,146 +258,248 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const float* __restrict__ p
 }
 
 // ----------------------------------------------------------- flash attention, bf16
-template <int HD>
-__global__ __launch_bounds__(256) void k_flash_bf16(
+// One workgroup per (32 query rows, kv head, sequence) with one wave per query
+// head of the group: every K / V^T tile is staged in LDS once for all of them.
+// Each wave computes S^T = K Q^T (keys as MFMA rows, its 32 queries as two
+// 16-column blocks), so a query's scores sit in the lanes of one column and the
+// online-softmax statistics are per lane.  Inside each 32-key step the key order
+// of the two 16-row MFMA blocks is permuted (block b, row i -> key
+// 8 (i >> 2) + 4 b + (i & 3)) so that a lane's eight scores of a column are keys
+// 8 g .. 8 g + 7: exactly the B operand of O^T += V^T P^T, which therefore never
+// leaves registers.  P enters that product as two bf16 terms (hi + lo), so no
+// rounding point is added.  K and V^T tiles of 64 keys are double-buffered in
+// LDS and prefetched into registers one tile ahead; one barrier per tile.  The
+// latest query blocks (the most key tiles under the causal mask) start first.
+template <int HD, int GQ>
+__global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) void k_flash_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ vt,
     int T, int H, int n_kv, int k_len, int k_seq_stride, int vt_len, float scale,
     bf16_t* __restrict__ out) {
-  constexpr int KROW = HD + 8, VROW = 64 + 8, PROW = 64 + 8;
+  constexpr int NT = 64 * GQ;
+  constexpr int KROW = HD + 8, VROW = 64 + 8;
   constexpr int QSTEPS = HD / 32, HB = HD / 16;
-  __shared__ __attribute__((aligned(16))) bf16_t ks[64 * KROW];
-  __shared__ __attribute__((aligned(16))) bf16_t vs[HD * VROW];
-  __shared__ __attribute__((aligned(16))) bf16_t ps[2][4][16 * PROW];   // P = hi + lo
+  constexpr int KP = 64 * HD / 8, VP = HD * 8;          // 16-byte pieces of a K / V^T tile
+  constexpr int KPT = (KP + NT - 1) / NT, VPT = (VP + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) bf16_t ks[2][64 * KROW];
+  __shared__ __attribute__((aligned(16))) bf16_t vs[2][HD * VROW];
 
-  const int qb = blockIdx.x, h = blockIdx.y, n = blockIdx.z;
-  const int g = h * n_kv / H;
+  const int qblk = gridDim.x - 1 - blockIdx.x;
+  const int g = blockIdx.y, n = blockIdx.z;
   const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
+  const int h = g * GQ + wave;
   const int ldq = H * HD;
-  const int r0 = qb * 64 + wave * 16;
+  const int q0 = qblk * 32;
+  const int lq = lane & 15, lg = lane >> 4;
 
-  bf16x8_t qf[QSTEPS];
-  {
-    const int r = min(r0 + (lane & 15), T - 1);
-    const bf16_t* qp = q + ((size_t)n * T + r) * ldq + h * HD + (lane >> 4) * 8;
+  // Q as the B operand: column lq of block qb = query q0 + 16 qb + lq; MFMA step st
+  // takes the 8-element piece (4 st + lg) of the head dimension
+  bf16x8_t qf[2][QSTEPS];
 #pragma unroll
-    for (int st = 0; st < QSTEPS; ++st) qf[st] = *(const bf16x8_t*)(qp + st * 32);
+  for (int qb = 0; qb < 2; ++qb) {
+    const int r = min(q0 + qb * 16 + lq, T - 1);
+    const bf16_t* qp = q + ((size_t)n * T + r) * ldq + h * HD + lg * 8;
+#pragma unroll
+    for (int st = 0; st < QSTEPS; ++st) qf[qb][st] = *(const bf16x8_t*)(qp + st * 32);
   }
   const bf16_t* kbase = k + ((size_t)n * k_seq_stride * n_kv + g) * (size_t)k_len * HD;
   const bf16_t* vbase = vt + ((size_t)n * n_kv + g) * (size_t)HD * vt_len;
 
-  f32x4_t oacc[HB];
+  u32x4_t kr[KPT], vr[VPT];
+  auto load_tile = [&](int t) {
 #pragma unroll
-  for (int i = 0; i < HB; ++i) oacc[i] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-  float mrow[4], lrow[4];
-#pragma unroll
-  for (int v = 0; v < 4; ++v) { mrow[v] = -1e30f; lrow[v] = 0.f; }
-
-  const int last_kb = min(qb, (T - 1) / 64);
-  for (int kb = 0; kb <= last_kb; ++kb) {
-    // stage K [64 keys][HD] and Vt [HD][64 keys]
-    for (int i = tid; i < 64 * HD / 8; i += 256) {
-      const int r = i / (HD / 8), c = (i % (HD / 8)) * 8;
-      const int key = min(kb * 64 + r, T - 1);
-      *(u32x4_t*)(&ks[r * KROW + c]) = *(const u32x4_t*)(kbase + (size_t)key * HD + c);
+    for (int i = 0; i < KPT; ++i) {
+      const int pi = tid + i * NT;
+      if (pi < KP) {
+        const int r = pi / (HD / 8), c = (pi % (HD / 8)) * 8;
+        const int key = min(t * 64 + r, T - 1);
+        kr[i] = *(const u32x4_t*)(kbase + (size_t)key * HD + c);
+      }
     }
-    for (int i = tid; i < HD * 8; i += 256) {
-      const int r = i / 8, c = (i % 8) * 8;
-      const int key0 = kb * 64 + c;
-      u32x4_t v = (u32x4_t){0u, 0u, 0u, 0u};
-      if (key0 < T) {
-        v = *(const u32x4_t*)(vbase + (size_t)r * vt_len + key0);
-        const int nv = T - key0;   // keys past T are zeroed
-        if (nv < 8) {
-          uint32_t w[4] = {v[0], v[1], v[2], v[3]};
 #pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (e >= nv) w[e / 2] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-          v = (u32x4_t){w[0], w[1], w[2], w[3]};
+    for (int i = 0; i < VPT; ++i) {
+      const int pi = tid + i * NT;
+      if (pi < VP) {
+        const int r = pi / 8, c = (pi % 8) * 8;
+        const int key0 = t * 64 + c;
+        u32x4_t v = (u32x4_t){0u, 0u, 0u, 0u};
+        if (key0 < T) {
+          v = *(const u32x4_t*)(vbase + (size_t)r * vt_len + key0);
+          const int nv = T - key0;   // keys past T are zeroed (their P is 0, V must be finite)
+          if (nv < 8) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (e >= nv) v[e / 2] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+          }
+        }
+        vr[i] = v;
+      }
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int pi = tid + i * NT;
+      if (pi < KP) {
+        const int r = pi / (HD / 8), c = (pi % (HD / 8)) * 8;
+        *(u32x4_t*)(&ks[buf][r * KROW + c]) = kr[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int pi = tid + i * NT;
+      if (pi < VP) {
+        const int r = pi / 8, c = (pi % 8) * 8;
+        *(u32x4_t*)(&vs[buf][r * VROW + c]) = vr[i];
+      }
+    }
+  };
+
+  f32x4_t oacc[HB][2];
+#pragma unroll
+  for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) oacc[hb][qb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  float mq[2] = {-1e30f, -1e30f}, lq_sum[2] = {0.f, 0.f};
+
+  const int qlast = min(q0 + 31, T - 1);
+  const int n_tiles = qlast / 64 + 1;
+  load_tile(0);
+  store_tile(0);
+  if (n_tiles > 1) load_tile(1);
+  __syncthreads();
+
+  for (int t = 0; t < n_tiles; ++t) {
+    const bf16_t* ksb = &ks[t & 1][0];
+    const bf16_t* vsb = &vs[t & 1][0];
+    const int k0 = t * 64;
+    // S^T for the two 32-key steps: sacc[s2][b][qb], lane rows 4 lg + v -> key
+    // k0 + 32 s2 + 8 lg + 4 b + v, column lq -> query q0 + 16 qb + lq
+    f32x4_t sacc[2][2][2];
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int kr_ = 32 * s2 + 8 * (lq >> 2) + 4 * b + (lq & 3);   // this lane's A row
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) sacc[s2][b][qb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int st = 0; st < QSTEPS; ++st) {
+          const bf16x8_t kf = *(const bf16x8_t*)(ksb + kr_ * KROW + (st * 4 + lg) * 8);
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+            sacc[s2][b][qb] =
+                __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][st], sacc[s2][b][qb], 0, 0, 0);
         }
       }
-      *(u32x4_t*)(&vs[r * VROW + c]) = v;
-    }
-    __syncthreads();
-
-    // S = Q K^T: 16 rows x 64 keys per wave
-    f32x4_t sacc[4];
+    // online softmax per query column: tile maximum and rescale first, then per
+    // 32-key step the P^T operands (hi, lo) and their products with V^T
+    const bool full = k0 + 63 <= q0 && k0 + 63 < T;   // no key of the tile is masked
+    float mnew[2], psum[2] = {0.f, 0.f};
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) {
-      sacc[cb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    for (int qb = 0; qb < 2; ++qb) {
+      const int qrow = q0 + qb * 16 + lq;
+      float mx = -INFINITY;
 #pragma unroll
-      for (int st = 0; st < QSTEPS; ++st) {
-        const bf16x8_t kf =
-            *(const bf16x8_t*)(&ks[(cb * 16 + (lane & 15)) * KROW + st * 32 + (lane >> 4) * 8]);
-        sacc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[st], kf, sacc[cb], 0, 0, 0);
-      }
-    }
-    // online softmax; lane holds rows 4*(lane>>4)+v, keys cb*16 + (lane&15)
-    float mnew[4], alpha[4];
+      for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = r0 + (lane >> 4) * 4 + v;
-      float mx = -1e30f;
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) {
-        const int key = kb * 64 + cb * 16 + (lane & 15);
-        float s = sacc[cb][v] * scale;
-        s = (key <= row && key < T) ? s : -INFINITY;
-        sacc[cb][v] = s;
-        mx = fmaxf(mx, s);
-      }
+          for (int v = 0; v < 4; ++v) {
+            const int key = k0 + 32 * s2 + 8 * lg + 4 * b + v;
+            float sc = sacc[s2][b][qb][v] * scale;
+            if (!full) sc = (key <= qrow && key < T) ? sc : -INFINITY;
+            sacc[s2][b][qb][v] = sc;
+            mx = fmaxf(mx, sc);
+          }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      mnew[qb] = fmaxf(mq[qb], mx);
+      const float alpha = __expf(mq[qb] - mnew[qb]);
+      mq[qb] = mnew[qb];
+      lq_sum[qb] *= alpha;
 #pragma unroll
-      for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
-      mnew[v] = fmaxf(mrow[v], mx);
-      alpha[v] = __expf(mrow[v] - mnew[v]);
-      float sum = 0.f;
+      for (int hb = 0; hb < HB; ++hb)
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) {
-        const float p = (sacc[cb][v] == -INFINITY) ? 0.f : __expf(sacc[cb][v] - mnew[v]);
-        const bf16_t ph = f2bf(p);
-        const bf16_t pl = f2bf(p - bf2f(ph));
-        sum += p;
-        const int at = ((lane >> 4) * 4 + v) * PROW + cb * 16 + (lane & 15);
-        ps[0][wave][at] = ph;
-        ps[1][wave][at] = pl;
-      }
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off, 64);
-      lrow[v] = lrow[v] * alpha[v] + sum;
-      mrow[v] = mnew[v];
+        for (int v = 0; v < 4; ++v) oacc[hb][qb][v] *= alpha;
     }
 #pragma unroll
-    for (int hb = 0; hb < HB; ++hb)
+    for (int s2 = 0; s2 < 2; ++s2) {
+      bf16x8_t ph[2], pl[2];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) oacc[hb][v] *= alpha[v];
-    __syncthreads();   // ps visible within the wave (and vs/ks reads ordered)
-
-    // O += P V: A = P (16 rows x 32 keys), B = V (32 keys x 16 dims).  P enters
-    // as two bf16 terms (hi + lo), so P V is accurate to fp32 level.
+      for (int qb = 0; qb < 2; ++qb) {
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int at = (lane & 15) * PROW + kk * 32 + (lane >> 4) * 8;
-      const bf16x8_t ph = *(const bf16x8_t*)(&ps[0][wave][at]);
-      const bf16x8_t pl = *(const bf16x8_t*)(&ps[1][wave][at]);
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const float sv = sacc[s2][b][qb][v];
+            const float p = (sv == -INFINITY) ? 0.f : __expf(sv - mnew[qb]);
+            psum[qb] += p;
+            const bf16_t pbh = f2bf(p);
+            const bf16_t pbl = f2bf(p - bf2f(pbh));
+            ph[qb][4 * b + v] = __builtin_bit_cast(__bf16, pbh);
+            pl[qb][4 * b + v] = __builtin_bit_cast(__bf16, pbl);
+          }
+      }
+      // O^T += V^T P^T: A = V^T rows (dims 16 hb + lq), keys 32 s2 + 8 lg .. + 8
 #pragma unroll
       for (int hb = 0; hb < HB; ++hb) {
-        const bf16x8_t vf =
-            *(const bf16x8_t*)(&vs[(hb * 16 + (lane & 15)) * VROW + kk * 32 + (lane >> 4) * 8]);
-        oacc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, vf, oacc[hb], 0, 0, 0);
-        oacc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, vf, oacc[hb], 0, 0, 0);
+        const bf16x8_t vf = *(const bf16x8_t*)(vsb + (hb * 16 + lq) * VROW + 32 * s2 + 8 * lg);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          oacc[hb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph[qb], oacc[hb][qb], 0, 0, 0);
+          oacc[hb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[qb], oacc[hb][qb], 0, 0, 0);
+        }
       }
+    }
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      float sum = psum[qb];
+      sum += __shfl_xor(sum, 16, 64);
+      sum += __shfl_xor(sum, 32, 64);
+      lq_sum[qb] += sum;
+    }
+    // stage tile t + 1 into the other buffer (last read in iteration t - 1)
+    if (t + 1 < n_tiles) {
+      store_tile((t + 1) & 1);
+      if (t + 2 < n_tiles) load_tile(t + 2);
     }
     __syncthreads();
   }
 
+  // O^T: lane holds dims 16 hb + 4 lg + v of query column lq
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int row = r0 + (lane >> 4) * 4 + v;
+  for (int qb = 0; qb < 2; ++qb) {
+    const int row = q0 + qb * 16 + lq;
     if (row >= T) continue;
-    const float inv = 1.f / lrow[v];
-    bf16_t* op = out + ((size_t)n * T + row) * ldq + h * HD;
+    const float inv = 1.f / lq_sum[qb];
+    bf16_t* op = out + ((size_t)n * T + row) * ldq + h * HD + 4 * lg;
 #pragma unroll
-    for (int hb = 0; hb < HB; ++hb) op[hb * 16 + (lane & 15)] = f2bf(oacc[hb][v] * inv);
+    for (int hb = 0; hb < HB; ++hb) {
+      const uint32_t w0 = (uint32_t)f2bf(oacc[hb][qb][0] * inv) |
+                          ((uint32_t)f2bf(oacc[hb][qb][1] * inv) << 16);
+      const uint32_t w1 = (uint32_t)f2bf(oacc[hb][qb][2] * inv) |
+                          ((uint32_t)f2bf(oacc[hb][qb][3] * inv) << 16);
+      *(uint2*)(op + hb * 16) = make_uint2(w0, w1);
+    }
   }
+}
+
+template <int HD>
+hipError_t launch_flash(int gq, dim3 grid, hipStream_t st, const bf16_t* q, const bf16_t* k,
+                        const bf16_t* vt, int T, int H, int n_kv, int k_len, int k_seq_stride,
+                        int vt_len, float scale, bf16_t* out) {
+#define GRPO_FLASH(G)                                                                        \
+  case G:                                                                                   \
+    k_flash_bf16<HD, G><<<grid, 64 * G, 0, st>>>(q, k, vt, T, H, n_kv, k_len, k_seq_stride, \
+                                                 vt_len, scale, out);                       \
+    break;
+  switch (gq) {
+    GRPO_FLASH(1) GRPO_FLASH(2) GRPO_FLASH(3) GRPO_FLASH(4)
+    GRPO_FLASH(5) GRPO_FLASH(6) GRPO_FLASH(7) GRPO_FLASH(8)
+    default: return hipErrorInvalidValue;
+  }
+#undef GRPO_FLASH
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------- fp32 path
@@ -529,17 +629,15 @@ hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_o
     return hipGetLastError();
   }
   const int vt_len = (T + 7) / 8 * 8;
-  dim3 grid((T + 63) / 64, H, N);
+  dim3 grid((T + 31) / 32, n_kv, N);
   Prof pf("flash_attn", st);
+  const int gq = H / n_kv;
   if (hd == 128)
-    k_flash_bf16<128><<<grid, 256, 0, st>>>((const bf16_t*)q, (const bf16_t*)k,
-                                            (const bf16_t*)v_or_vt, T, H, n_kv, k_len,
-                                            k_seq_stride, vt_len, scale, (bf16_t*)out);
-  else
-    k_flash_bf16<64><<<grid, 256, 0, st>>>((const bf16_t*)q, (const bf16_t*)k,
-                                           (const bf16_t*)v_or_vt, T, H, n_kv, k_len, k_seq_stride,
-                                           vt_len, scale, (bf16_t*)out);
-  return hipGetLastError();
+    return launch_flash<128>(gq, grid, st, (const bf16_t*)q, (const bf16_t*)k,
+                             (const bf16_t*)v_or_vt, T, H, n_kv, k_len, k_seq_stride, vt_len,
+                             scale, (bf16_t*)out);
+  return launch_flash<64>(gq, grid, st, (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v_or_vt,
+                          T, H, n_kv, k_len, k_seq_stride, vt_len, scale, (bf16_t*)out);
 }
 
 }  // namespace grpo
