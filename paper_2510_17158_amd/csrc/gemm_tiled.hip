@@ -19,6 +19,7 @@ namespace grpo {
 namespace {
 
 constexpr int NT = 256, BM = 128, BN = 128, BK = 64, LROW = BK + 8;
+constexpr int kBigTileRows = 1024;   // rows from which the 256 x 256 tiles are used
 
 struct TArgs {
   const bf16_t* X; int ldx; int M;
@@ -160,6 +161,192 @@ __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Large tiles for large M (scoring, long prefill): a workgroup of 4 waves owns a
+// 256 x 256 output tile, each wave 128 x 128 as 4 x 4 blocks of
+// v_mfma_f32_32x32x16_bf16 (accumulators in the AGPR half of the register file),
+// so every 16-byte operand fragment read from LDS feeds 4 MFMAs.  With one wave
+// per SIMD only the 32 x 32 instruction keeps the matrix core busy (the 16 x 16
+// one issues at about half its peak rate from a single wave).  Operand tiles of 64 k-elements (256 rows x 128 B
+// each for X and W) move global -> LDS with direct-to-LDS loads
+// (global_load_lds_dwordx4: each lane names its own source, the 64 lanes fill
+// 1 KB of LDS in lane order), double-buffered so the next tile's copy overlaps
+// the current tile's MFMAs.  Rows are stored with
+// their eight 16-byte pieces XOR-swizzled by (row >> 1) & 7, which makes the
+// 16 rows of a fragment read hit 16 distinct bank groups.
+constexpr int GB = 256, GBK = 64;
+
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+
+template <int EPI>
+__device__ __forceinline__ const bf16_t* big_wrow(const TArgs& a, int tn, int r) {
+  if (EPI == EPI_SWIGLU) {
+    // B-tile row r: wave half wn = r / 128, within it 64 gate rows then 64 up rows
+    const int wn = r >> 7, q = r & 127;
+    const int n = min(tn * 128 + wn * 64 + (q & 63), a.n1 - 1);
+    return (q < 64 ? a.w0 + (size_t)n * a.K : a.w1 + (size_t)n * a.K);
+  }
+  const int n = min(tn * GB + r, a.N - 1);
+  if (n < a.n1) return a.w0 + (size_t)n * a.K;
+  if (n < a.n2) return a.w1 + (size_t)(n - a.n1) * a.K;
+  return a.w2 + (size_t)(n - a.n2) * a.K;
+}
+
+// One direct-to-LDS copy of 16 bytes per lane: the 64 lanes of the wave fill the
+// 1 KB at LDS byte address `lds` in lane order.  Issued as one asm statement that
+// also sets M0, so the compiler does not serialise consecutive copies (it cannot
+// prove they write disjoint LDS); the kernel waits on them itself (dma_wait)
+// before the barrier that publishes the tile.
+__device__ __forceinline__ void dma16(const bf16_t* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(g) : "memory");
+}
+__device__ __forceinline__ void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(256) void k_gemm_big(TArgs a) {
+  // [buffer][X tile, W tile]
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[2][2][GB * GBK];
+  const int tid = threadIdx.x, lane = tid % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // XCD-aware tile order: workgroups are dealt to the 8 XCDs round-robin
+  // (blockIdx % 8), each XCD with its own L2.  The tiles form super-tiles of
+  // 4 row tiles x 8 column tiles; the 32 workgroups an XCD runs at a time (one
+  // per compute unit) take one super-tile, so each X and W k-slice is fetched
+  // into that XCD's L2 once for 8 (X) or 4 (W) users.
+  const int xcd = blockIdx.x % 8, within = blockIdx.x / 8;
+  const int st = (within / 32) * 8 + xcd, loc = within % 32;
+  const int st_n = (a.tiles_n + 7) / 8;
+  const int tm = (st / st_n) * 4 + loc / 8;
+  const int tn = (st % st_n) * 8 + loc % 8;
+  if (tm >= a.tiles_m || tn >= a.tiles_n) return;
+
+  // Rows of copy instruction j advance by 8 per j: one base pointer per operand
+  // plus a uniform stride (the host guarantees that a W tile lies inside one
+  // matrix of the stack).  The last row tile is shifted back to end at M (M >= 256)
+  // and writes only the rows no earlier tile owns.
+  const int m0 = min(tm * GB, a.M - GB);
+  const int r0 = wave * 64 + lane / 8;                  // row of instruction 0
+  const int pbase = ((lane % 8) ^ swz(r0)) * 8;         // swz(r0 + 8 j) == swz(r0) ^ 4 j
+  const bf16_t* ab = a.X + (size_t)(m0 + r0) * a.ldx + pbase;
+  const bf16_t* bb = big_wrow<EPI>(a, tn, r0) + pbase;
+  const size_t astep = (size_t)8 * a.ldx, bstep = (size_t)8 * a.K;
+  auto copy = [&](int buf, int kt) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int off = (wave * 8 + j) * 8 * GBK;          // first LDS row of the instruction
+      const int flip = (j & 1) ? ((pbase ^ 32) - pbase) : 0;   // pieces XOR 4 j (mod 8)
+      dma16(ab + j * astep + kt * GBK + flip, lds_addr(&lds[buf][0][off]));
+      dma16(bb + j * bstep + kt * GBK + flip, lds_addr(&lds[buf][1][off]));
+    }
+  };
+
+
+  // Fragment rows of this lane: wm * 128 + 32 i + (lane & 31) for X, likewise for
+  // W; k-step s (16 elements) takes piece 2 s + (lane >> 5) of those rows.  The
+  // swizzle ((lane & 31) >> 1) & 7 is the same for all four blocks, so a k-step
+  // needs one LDS address per operand and the blocks sit 32 rows apart.
+  const int sw = ((lane & 31) >> 1) & 7;
+  const int g2 = lane >> 5;
+  int aoff[GBK / 16], boff[GBK / 16];
+#pragma unroll
+  for (int s = 0; s < GBK / 16; ++s) {
+    const int pc = ((s * 2 + g2) ^ sw) * 8;
+    aoff[s] = (wm * 128 + (lane & 31)) * GBK + pc;
+    boff[s] = (wn * 128 + (lane & 31)) * GBK + pc;
+  }
+  f32x16_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  // Software-pipelined over the 4 k-steps of a tile: the 8 fragment reads of
+  // step s + 1 are interleaved with the 16 MFMAs of step s (one read per two
+  // MFMAs), so the LDS latency hides under the matrix cores.
+#define GRPO_FRAGS(As, Bs, s, FA, FB)                                                 \
+  _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                     \
+    FA[i] = *(const bf16x8_t*)((As) + aoff[s] + i * 32 * GBK);                        \
+    FB[i] = *(const bf16x8_t*)((Bs) + boff[s] + i * 32 * GBK);                        \
+  }
+#define GRPO_MFMAS(FA, FB)                                                            \
+  _Pragma("unroll") for (int i = 0; i < 4; ++i)                                       \
+    _Pragma("unroll") for (int j = 0; j < 4; ++j)                                     \
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(FA[i], FB[j], acc[i][j], 0, 0, 0);
+#define GRPO_INTERLEAVE()                                                             \
+  _Pragma("unroll") for (int q = 0; q < 8; ++q) {                                     \
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                                \
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);                                \
+  }
+  auto mma_tile = [&](const bf16_t* As, const bf16_t* Bs) {
+    bf16x8_t a0[4], b0[4], a1[4], b1[4];
+    GRPO_FRAGS(As, Bs, 0, a0, b0)
+    GRPO_FRAGS(As, Bs, 1, a1, b1)
+    GRPO_MFMAS(a0, b0)
+    GRPO_INTERLEAVE()
+    GRPO_FRAGS(As, Bs, 2, a0, b0)
+    GRPO_MFMAS(a1, b1)
+    GRPO_INTERLEAVE()
+    GRPO_FRAGS(As, Bs, 3, a1, b1)
+    GRPO_MFMAS(a0, b0)
+    GRPO_INTERLEAVE()
+    GRPO_MFMAS(a1, b1)
+  };
+#undef GRPO_INTERLEAVE
+
+  const int nk = a.K / GBK;
+  copy(0, 0);
+  dma_wait();
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    // the other buffer was last read in iteration kt - 1, which ended at a barrier
+    if (kt + 1 < nk) copy(buf ^ 1, kt + 1);
+    mma_tile(&lds[buf][0][0], &lds[buf][1][0]);
+    __builtin_amdgcn_sched_barrier(0);   // every MFMA is issued before the copy is awaited
+    dma_wait();
+    __syncthreads();
+  }
+#undef GRPO_MFMAS
+#undef GRPO_FRAGS
+
+  // ---- epilogue: acc[i][j][r] is row 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4,
+  // column 32 j + (lane & 31) of the wave's 128 x 128 block ----
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = m0 + wm * 128 + i * 32 + (r / 4) * 8 + (lane >> 5) * 4 + (r % 4);
+      if (m < tm * GB) continue;
+      if (EPI == EPI_SWIGLU) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int n = tn * 128 + wn * 64 + j * 32 + (lane & 31);
+          if (n < a.n1) {
+            const float gt = acc[i][j][r], up = acc[i][j + 2][r];
+            a.out_act[(size_t)m * a.ld_out + n] = f2bf(gt / (1.f + __expf(-gt)) * up);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = tn * GB + wn * 128 + j * 32 + (lane & 31);
+          if (n < a.N) {
+            float* o = a.out_f32 + (size_t)m * a.ld_out + n;
+            if (EPI == EPI_RESID) *o += acc[i][j][r];
+            else *o = acc[i][j][r];
+          }
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // fp32 GEMM for fp32 models (VALU, 64x64 tiles, 4x4 outputs per thread).
 struct FArgs {
   const float* X; int ldx; int M;
@@ -244,11 +431,27 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
   a.X = X; a.ldx = ldx; a.M = M;
   a.w0 = (const bf16_t*)W.w[0]; a.w1 = (const bf16_t*)W.w[1]; a.w2 = (const bf16_t*)W.w[2];
   a.n1 = W.n1; a.n2 = W.n2; a.N = N; a.K = K;
+  a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;
+  Prof pf(epi == EPI_SWIGLU ? "gemm_tiled_swiglu" : "gemm_tiled", st);
+  const bool aligned = epi == EPI_SWIGLU
+                           ? W.n1 % 128 == 0
+                           : N % GB == 0 && (W.n1 >= N || W.n1 % GB == 0) && (W.n2 >= N || W.n2 % GB == 0);
+  if (M >= kBigTileRows && aligned) {
+    a.tiles_m = (M + GB - 1) / GB;
+    a.tiles_n = epi == EPI_SWIGLU ? (N + 127) / 128 : (N + GB - 1) / GB;
+    // super-tiles of 4 x 8 tiles, a whole number of rounds of 8 (one per XCD)
+    const int n_st = ((a.tiles_m + 3) / 4) * ((a.tiles_n + 7) / 8);
+    const int grid = (n_st + 7) / 8 * 8 * 32;
+    switch (epi) {
+      case EPI_STORE: k_gemm_big<EPI_STORE><<<grid, 256, 0, st>>>(a); break;
+      case EPI_RESID: k_gemm_big<EPI_RESID><<<grid, 256, 0, st>>>(a); break;
+      default: k_gemm_big<EPI_SWIGLU><<<grid, 256, 0, st>>>(a); break;
+    }
+    return hipGetLastError();
+  }
   a.tiles_m = (M + BM - 1) / BM;
   a.tiles_n = epi == EPI_SWIGLU ? (N + 63) / 64 : (N + BN - 1) / BN;
-  a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;
   const int grid = a.tiles_m * a.tiles_n;
-  Prof pf(epi == EPI_SWIGLU ? "gemm_tiled_swiglu" : "gemm_tiled", st);
   switch (epi) {
     case EPI_STORE: k_gemm_tiled<EPI_STORE><<<grid, NT, 0, st>>>(a); break;
     case EPI_RESID: k_gemm_tiled<EPI_RESID><<<grid, NT, 0, st>>>(a); break;
