@@ -24,6 +24,32 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 
+# HBM bytes of the decode attention kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE runs
+# (7B shape, contexts 3073..3104), each counter scaled by what it reads for a 1 GiB
+# device copy.  Valid only for the kernel source it was measured on.
+ATTN_TRAFFIC = {
+    "source": "paper_2510_17158_amd/csrc/attention.hip",
+    "sha256": "f4dbcab050a0481ad8798d5b20f1eb0f61eabda2cbdbdf15b1c281b4a4c0bcd7",
+    "fetch_kib": 396022.5, "fetch_scale": 2.0,
+    "write_kib": 512.0, "write_scale": 1.0,
+    "algorithmic_bytes": 64 * 3088.5 * 4096,
+}
+
+
+def attn_traffic(algorithmic_bytes_per_launch: float):
+    """Counter-measured HBM bytes per launch of the decode attention at this launch's
+    algorithmic size, or None when the kernel has changed since the counters."""
+    import hashlib
+    try:
+        with open(os.path.join(ROOT, ATTN_TRAFFIC["source"]), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != ATTN_TRAFFIC["sha256"]:
+                return None
+    except OSError:
+        return None
+    t = ATTN_TRAFFIC
+    measured = (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024
+    return measured / t["algorithmic_bytes"] * algorithmic_bytes_per_launch
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -126,6 +152,9 @@ def main():
                     help="override the workload's sampled tokens (profiling runs)")
     ap.add_argument("--prompt-len", type=int, default=None,
                     help="override the workload's prompt length (profiling runs)")
+    ap.add_argument("--no-kernel-timing", action="store_true",
+                    help="skip the replica of the step with per-launch HIP events (no roofline "
+                         "line); for hardware-counter runs")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy a 1 GiB device buffer 4 times (HBM counter calibration)")
     args = ap.parse_args()
@@ -235,6 +264,11 @@ def main():
     # per-kernel times from a profiled replica of the step (HIP events around
     # every launch, on the launch stream); the dominant decode kernel sets the
     # roofline line
+    if args.no_kernel_timing:
+        if not args.no_cpu_baseline:
+            out["cpu_baseline"] = cpu_baseline(w, host, args.cpu_budget)
+        print(json.dumps(out), flush=True)
+        return
     api.profile_begin()
     step()
     torch.cuda.synchronize()
@@ -246,7 +280,9 @@ def main():
     n, t = prof[dom]
     out["roofline"] = {"bound": "hbm", "achieved": kb[dom] / (t / 1e3) / 1e9,
                        "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                       "frac": kb[dom] / (t / 1e3) / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                       "frac": kb[dom] / (t / 1e3) / 1e9 / HBM_PEAK_GBS,
+                       "traffic": attn_traffic(kb[dom] / n) if dom == "attn_decode" else None,
+                       "traffic_unit": "bytes per launch",
                        "kernel": dom, "launches": n, "avg_us": 1e3 * t / n,
                        "algorithmic_bytes_per_launch": kb[dom] / n}
     out["decode_kernels_gbs"] = {k: kb[k] / (prof[k][1] / 1e3) / 1e9 for k in kb if k in prof}
