@@ -77,28 +77,24 @@ def score_flops(w) -> float:
 
 
 def kernel_bytes(w) -> dict:
-    """Algorithmic HBM bytes of one step, per decode-side kernel name.
-
-    gemm_decode: every QKV, O and down-projection weight once per decode step,
-    the LM head once per decode step and once for the prefill draw, plus the
-    activation rows read and the fp32 products written.
-    gemm_decode_swiglu: the gate and up weights once per decode step plus a.
-    attn_decode: the K and V of every context position of every sequence per
+    """Algorithmic HBM bytes of one step, per decode-side kernel name: every
+    weight byte of the projection once per decode step, plus its activation rows
+    read and its product written once (fp32 products, bf16 activations); for
+    attn_decode the K and V of every context position of every sequence per
     layer, context = position + 1."""
     c = w.model
     es = c.elem_bytes
     B, L, d, f, V = w.batch, c.n_layers, c.d_model, c.d_ffn, c.vocab
+    qd, kvd = c.q_dim, c.kv_dim
     n_dec = w.new_tokens - 1
-    qkv, o, down = (c.q_dim + 2 * c.kv_dim) * d, d * c.q_dim, d * f
-    gemm_w = L * (qkv + o + down) * es + V * d * es
-    gemm_act = L * B * ((d + c.q_dim + f) * es + (c.q_dim + 2 * c.kv_dim + 2 * d) * 4) \
-        + B * (d * es + V * 4)
-    swiglu = L * (2 * f * d * es + B * (d * es + f * es))
-    kv_layer_tok = 2 * c.kv_dim * es
+    kv_layer_tok = 2 * kvd * es
     ctx_sum = sum(w.prompt_len + s for s in range(1, n_dec + 1))   # context of decode step s
     return {
-        "gemm_decode": n_dec * (gemm_w + gemm_act) + V * d * es + w.n_prompts * (d * es + V * 4),
-        "gemm_decode_swiglu": n_dec * swiglu,
+        "gemm_decode_qkv": n_dec * L * ((qd + 2 * kvd) * d * es + B * d * es + B * (qd + 2 * kvd) * 4),
+        "gemm_decode_o": n_dec * L * (d * qd * es + B * qd * es + B * d * 4),
+        "gemm_decode_swiglu": n_dec * L * (2 * f * d * es + B * d * es + B * f * es),
+        "gemm_decode_down": n_dec * L * (d * f * es + B * f * es + B * d * 4),
+        "gemm_decode_lm_head": n_dec * (V * d * es + B * d * es + B * V * 4),
         "attn_decode": L * B * kv_layer_tok * ctx_sum,
     }
 
@@ -192,7 +188,7 @@ def main():
     ref = None
     if w.score:
         ref_host = synth.make_weights(c, w.master_seed, ref=True)
-        ref = api.Model(c, api.upload_weights(c, ref_host))
+        ref = api.Model(c, api.upload_weights(c, ref_host), decode=False)
         del ref_host
     it = GrpoIteration(w, pol, ref, synth.make_prompts(w), synth.make_rewards(w),
                        synth.make_seed(w))

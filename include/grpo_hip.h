@@ -68,7 +68,8 @@ enum grpo_op { GRPO_OP_PREFILL = 0, GRPO_OP_ROLLOUT = 1, GRPO_OP_SCORE = 2, GRPO
  * angle pos * rope_theta^(-2i/hd)), grouped-query attention (query head h reads
  * kv head floor(h*n_kv_heads/n_heads)), SwiGLU MLP, untied LM head, no biases.
  * Supported: head_dim in {64, 128}; n_heads a multiple of n_kv_heads; d_model,
- * n_heads*head_dim and d_ffn multiples of 128 (of 32 for fp32 models). */
+ * n_heads*head_dim and d_ffn multiples of 128 (of 32 for fp32 models); vocab
+ * a multiple of 16 for bf16 models. */
 typedef struct grpo_config {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
   float rms_eps, rope_theta;
@@ -111,6 +112,24 @@ typedef struct grpo_model grpo_model;
  * grpo_config).  Returns GRPO_INVALID_ARG / GRPO_UNSUPPORTED on bad input. */
 int grpo_model_create(const grpo_config* cfg, const grpo_weights* w, grpo_model** out);
 int grpo_model_destroy(grpo_model* m);
+
+/* Decode copy of the projections (bf16 models).  A decode step multiplies a
+ * few rows by every weight matrix (Alg. 1, sampling step), so it streams the
+ * weights from HBM once per step; the decode GEMM reads them from a copy stored
+ * in MFMA fragment order (16 rows x 32 columns as 1 KB in lane order, blocks of
+ * 16 rows consecutive along the columns; gate and up blocks alternate) so that
+ * every load is 1 KB of contiguous memory.
+ * grpo_decode_weights_bytes: bytes of that copy (0 for fp32 models or an
+ * invalid config).
+ * grpo_model_pack_decode: writes the copy of the handle's current weights into
+ * buf (device, caller-owned, 256-byte aligned, >= grpo_decode_weights_bytes)
+ * on `stream` and makes the handle's decode steps read it.  buf must outlive
+ * the handle's use; call again after the weights change.  Required before
+ * grpo_rollout_step on a bf16 model (GRPO_INVALID_ARG otherwise); a no-op for
+ * fp32 models.  Returns GRPO_INVALID_ARG for a NULL handle or buffer, or a
+ * buffer that is too small or misaligned. */
+size_t grpo_decode_weights_bytes(const grpo_config* cfg);
+int grpo_model_pack_decode(grpo_model* m, void* buf, size_t bytes, void* stream);
 
 /* Bytes of a KV cache for n_seqs sequences of max_len positions.  Layout:
  * [n_layers][2 (K, V)][n_seqs][n_kv_heads][max_len][head_dim], model dtype.

@@ -54,6 +54,8 @@ _VP, _I32, _F32, _SZ = C.c_void_p, C.c_int32, C.c_float, C.c_size_t
 _SIGS = {
     "grpo_model_create": (_I32, [C.POINTER(Config), C.POINTER(Weights), C.POINTER(_VP)]),
     "grpo_model_destroy": (_I32, [_VP]),
+    "grpo_decode_weights_bytes": (_SZ, [C.POINTER(Config)]),
+    "grpo_model_pack_decode": (_I32, [_VP, _VP, _SZ, _VP]),
     "grpo_kv_cache_bytes": (_SZ, [C.POINTER(Config), _I32, _I32]),
     "grpo_workspace_bytes": (_SZ, [_VP, _I32, _I32, _I32]),
     "grpo_last_error": (C.c_char_p, []),
@@ -126,9 +128,15 @@ def upload_weights(cfg: ModelConfig, host: dict, device="cuda") -> dict:
 
 
 class Model:
-    """A model handle over device weight tensors (which it keeps alive)."""
+    """A model handle over device weight tensors (which it keeps alive).
 
-    def __init__(self, cfg: ModelConfig, weights: dict):
+    ``decode=True`` (bf16 models) also allocates the decode copy of the
+    projections and has the library pack it (``grpo_model_pack_decode``), which
+    ``rollout_step`` needs; a model that is only scored can skip it.  Call
+    ``pack_decode()`` again after changing the weights in place.
+    """
+
+    def __init__(self, cfg: ModelConfig, weights: dict, decode: bool = True):
         self.cfg = cfg
         self.weights = weights
         L = cfg.n_layers
@@ -147,6 +155,17 @@ class Model:
         h = C.c_void_p()
         _check(lib().grpo_model_create(C.byref(self._cfg_s), C.byref(w), C.byref(h)))
         self.handle = h
+        self.decode_weights = None
+        if decode:
+            n = lib().grpo_decode_weights_bytes(C.byref(self._cfg_s))
+            if n:
+                self.decode_weights = torch.empty(n, dtype=torch.uint8, device="cuda")
+                self.pack_decode()
+
+    def pack_decode(self, stream=None):
+        t = self.decode_weights
+        if t is not None:
+            _check(lib().grpo_model_pack_decode(self.handle, _ptr(t), t.numel(), _stream(stream)))
 
     def close(self):
         if getattr(self, "handle", None):

@@ -18,7 +18,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libgrpo_hip.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "gemm_skinny.hip", "gemm_tiled.hip", "elementwise.hip", "attention.hip",
+SOURCES = ["api.cpp", "gemm_decode.hip", "gemm_tiled.hip", "elementwise.hip", "attention.hip",
            "sampler.hip", "grpo.hip"]
 
 COMMON_FLAGS = [

@@ -31,12 +31,21 @@ struct DecodeGraph {
   std::vector<uint64_t> key;
 };
 
+// Fragment-order copies of the projections for the decode GEMM (bf16 models),
+// in a caller-owned buffer written by grpo_model_pack_decode.
+struct DecodeWeights {
+  const void* base = nullptr;
+  std::vector<const uint16_t*> qkv, o, gate_up, down;
+  const uint16_t* lm_head = nullptr;
+};
+
 struct grpo_model {
   grpo_config cfg;
   const void* tok_emb;
   std::vector<const void*> attn_norm, wq, wk, wv, wo, mlp_norm, w_gate, w_up, w_down;
   const void* final_norm;
   const void* lm_head;
+  DecodeWeights dec;
   DecodeGraph graph;
 };
 
@@ -120,9 +129,8 @@ int fail(int code, const char* fmt, ...) {
     if (e_ != hipSuccess) return fail(GRPO_HIP_ERROR, "%s: %s", #expr, hipGetErrorString(e_)); \
   } while (0)
 
-constexpr int kSkinnyMax = 128;        // rows handled by the decode GEMM
 // split-K target grid of the decode GEMM (GRPO_DECODE_WGS overrides, for tuning)
-int skinny_target() {
+int decode_target() {
   static const int v = [] {
     const char* e = getenv("GRPO_DECODE_WGS");
     const int x = e ? atoi(e) : 0;
@@ -130,7 +138,6 @@ int skinny_target() {
   }();
   return v;
 }
-#define kSkinnyTargetWGs skinny_target()
 constexpr int kScoreTokens = 65536;    // rows per scoring chunk (sequences * T)
 constexpr size_t kLogitBytes = size_t(1) << 30;  // LM-head logits per scoring sub-chunk
 
@@ -170,6 +177,8 @@ int check_config(const grpo_config* c) {
   if (c->n_heads / c->n_kv_heads > 8)
     return fail(GRPO_UNSUPPORTED, "more than 8 query heads per kv head");
   if (c->d_model > 8192) return fail(GRPO_UNSUPPORTED, "d_model above 8192");
+  if (c->dtype == GRPO_BF16 && c->vocab % 16)
+    return fail(GRPO_UNSUPPORTED, "vocab %d of a bf16 model not a multiple of 16", c->vocab);
   const int mult = c->dtype == GRPO_F32 ? 32 : 128;
   if (c->d_model % mult || qdim(*c) % mult || c->d_ffn % mult)
     return fail(GRPO_UNSUPPORTED, "d_model, n_heads*head_dim and d_ffn must be multiples of %d",
@@ -188,9 +197,12 @@ Layer kv_layer(const grpo_model* m, void* kv, int l, int n_seqs, int max_len) {
   return Layer{base, base + per};
 }
 
-// ---- GEMMs: fp32 path, decode GEMM for few rows, tiled otherwise ----
-// The decode GEMM leaves split-K partial products for the consuming kernel
-// (RMSNorm adds residual partials, RoPE adds QKV partials).
+// ---- GEMMs ----
+// Many-row products (prefill, scoring) and every product of fp32 models read the
+// row-major weights: fp32 on the vector units, bf16 on the tiled MFMA kernels.
+// The decode steps of bf16 models run the decode GEMM on fragment-order operands
+// and leave split-K partial products for the consuming kernel (RMSNorm adds
+// residual partials, RoPE adds QKV partials).
 struct GemmScratch {
   float* part;   // decode-GEMM partial products
 };
@@ -199,78 +211,92 @@ int gemm_fail(hipError_t e) {
   return fail(GRPO_HIP_ERROR, "GEMM launch failed: %s", hipGetErrorString(e));
 }
 
-// x[M, N] += X W^T.  For the decode GEMM the product is left in *pend.
-int gemm_resid(const grpo_model* m, const void* X, int ldx, int M, WStack W, int N, int K,
-               float* x, GemmScratch s, Partials* pend, hipStream_t st, const char* name) {
-  hipError_t e;
-  *pend = Partials{nullptr, 0, 0, N};
-  if (m->cfg.dtype == GRPO_F32) {
-    e = gemm_f32((const float*)X, ldx, M, W, N, K, EPI_RESID, EpiArgs{x, nullptr, N}, st);
-  } else if (M <= kSkinnyMax) {
-    const SkinnyPlan p = skinny_plan(M, N, K, EPI_PARTIAL, kSkinnyTargetWGs);
-    e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, N, K, EPI_PARTIAL,
-                         EpiArgs{s.part, nullptr, N, name}, p, st);
-    *pend = Partials{s.part, p.splits, (size_t)M * N, N};
-  } else {
-    e = gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, N, K, EPI_RESID, EpiArgs{x, nullptr, N}, st);
-  }
+// out = X W^T (EPI_STORE), x += X W^T (EPI_RESID) or out_act = silu(gate) * up
+// (EPI_SWIGLU, W = (gate, up) stack), row-major everything
+int gemm_rows(const grpo_model* m, const void* X, int ldx, int M, WStack W, int N, int K, int epi,
+              EpiArgs ep, hipStream_t st) {
+  const hipError_t e =
+      m->cfg.dtype == GRPO_F32
+          ? gemm_f32((const float*)X, ldx, M, W, N, K, epi, ep, st)
+          : gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, N, K, epi, ep, st);
   return e == hipSuccess ? GRPO_OK : gemm_fail(e);
 }
 
-// out[M, N] = X W^T, possibly as *splits partial arrays *stride floats apart
-// (the first at `out` when there is one split, else in the scratch).
-int gemm_store(const grpo_model* m, const void* X, int ldx, int M, WStack W, int N, int K,
-               float* out, GemmScratch s, int max_splits, const float** res, int* splits,
-               size_t* stride, hipStream_t st, const char* name) {
-  hipError_t e;
-  *res = out;
-  *splits = 1;
-  *stride = 0;
-  if (m->cfg.dtype == GRPO_F32) {
-    e = gemm_f32((const float*)X, ldx, M, W, N, K, EPI_STORE, EpiArgs{out, nullptr, N}, st);
-  } else if (M <= kSkinnyMax) {
-    const SkinnyPlan p = skinny_plan(M, N, K, EPI_PARTIAL, kSkinnyTargetWGs, max_splits);
-    float* dst = p.splits == 1 ? out : s.part;
-    e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, N, K, EPI_PARTIAL,
-                         EpiArgs{dst, nullptr, N, name}, p, st);
-    *res = dst;
-    *splits = p.splits;
-    *stride = (size_t)M * N;
-  } else {
-    e = gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, N, K, EPI_STORE, EpiArgs{out, nullptr, N}, st);
-  }
+// Decode GEMM over fragment-order X [nb][K] and W: the product as *splits partial
+// arrays *stride floats apart, the first at `out` when there is one split, else
+// in the scratch.
+int gemm_dec(const void* Xf, int B, const uint16_t* Wf, int N, int K, float* out, GemmScratch s,
+             int max_splits, const float** res, int* splits, size_t* stride, hipStream_t st,
+             const char* name) {
+  const DecodePlan p = decode_plan(B, N, K, EPI_PARTIAL, decode_target(), max_splits);
+  float* dst = p.splits == 1 ? out : s.part;
+  const hipError_t e = gemm_decode_bf16((const uint16_t*)Xf, B, Wf, N, K, EPI_PARTIAL,
+                                        EpiArgs{dst, nullptr, N, name}, p, st);
+  *res = dst;
+  *splits = p.splits;
+  *stride = (size_t)B * N;
   return e == hipSuccess ? GRPO_OK : gemm_fail(e);
 }
 
-// a[M, f] = silu(X Wg^T) * (X Wu^T), rounded to the activation dtype
-int gemm_swiglu(const grpo_model* m, const void* X, int ldx, int M, WStack W, int f, int K,
-                void* a, hipStream_t st) {
-  hipError_t e;
-  if (m->cfg.dtype == GRPO_F32) {
-    e = gemm_f32((const float*)X, ldx, M, W, f, K, EPI_SWIGLU, EpiArgs{nullptr, a, f}, st);
-  } else if (M <= kSkinnyMax) {
-    const SkinnyPlan p = skinny_plan(M, f, K, EPI_SWIGLU, kSkinnyTargetWGs);
-    e = gemm_skinny_bf16((const uint16_t*)X, ldx, M, W, f, K, EPI_SWIGLU,
-                         EpiArgs{nullptr, a, f, "gemm_decode_swiglu"}, p, st);
-  } else {
-    e = gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, f, K, EPI_SWIGLU, EpiArgs{nullptr, a, f}, st);
-  }
+// residual projection: the product is left in *pend for the next RMSNorm to add
+int gemm_dec_resid(const void* Xf, int B, const uint16_t* Wf, int N, int K, GemmScratch s,
+                   Partials* pend, hipStream_t st, const char* name) {
+  const float* res;
+  int splits;
+  size_t stride;
+  if (int rc = gemm_dec(Xf, B, Wf, N, K, s.part, s, kMaxSplits, &res, &splits, &stride, st, name))
+    return rc;
+  *pend = Partials{res, splits, stride, N};
+  return GRPO_OK;
+}
+
+// a[nb][f] (fragment order) = silu(X Wg^T) * (X Wu^T)
+int gemm_dec_swiglu(const void* Xf, int B, const uint16_t* Wf, int f, int K, void* a,
+                    hipStream_t st) {
+  const DecodePlan p = decode_plan(B, 2 * f, K, EPI_SWIGLU, decode_target());
+  const hipError_t e = gemm_decode_bf16((const uint16_t*)Xf, B, Wf, 2 * f, K, EPI_SWIGLU,
+                                        EpiArgs{nullptr, a, f, "gemm_decode_swiglu"}, p, st);
   return e == hipSuccess ? GRPO_OK : gemm_fail(e);
 }
 
-// partial-product scratch of the decode GEMM for up to B rows, over the split
-// shapes of the model (QKV, O and down projections)
-size_t skinny_scratch(const grpo_config& c, int B) {
+// partial-product scratch of the decode GEMM for B rows, over the split shapes
+// of the model (QKV, O and down projections)
+size_t decode_scratch(const grpo_config& c, int B) {
   if (c.dtype == GRPO_F32) return 0;
-  const int rows = std::min(std::max(B, 1), kSkinnyMax);
   const int d = c.d_model, f = c.d_ffn;
   const int shapes[3][2] = {{qdim(c) + 2 * kvdim(c), d}, {d, qdim(c)}, {d, f}};
   size_t part = 0;
   for (auto& sh : shapes) {
-    const SkinnyPlan p = skinny_plan(rows, sh[0], sh[1], EPI_PARTIAL, kSkinnyTargetWGs);
-    part = std::max(part, (size_t)p.splits * rows * sh[0]);
+    const DecodePlan p = decode_plan(B, sh[0], sh[1], EPI_PARTIAL, decode_target());
+    part = std::max(part, (size_t)p.splits * B * sh[0]);
   }
   return part;
+}
+
+// Byte offsets of the decode copy: per layer QKV (rows q, k, v), O, gate/up
+// (16-row blocks interleaved), down; then the LM head.
+struct DecodeLayout {
+  std::vector<size_t> qkv, o, gate_up, down;
+  size_t lm_head = 0, total = 0;
+};
+DecodeLayout decode_layout(const grpo_config& c) {
+  DecodeLayout L;
+  const size_t d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
+  size_t off = 0;
+  auto take = [&](size_t rows, size_t cols) {
+    const size_t at = off;
+    off += (rows * cols * 2 + 255) & ~size_t(255);
+    return at;
+  };
+  for (int l = 0; l < c.n_layers; ++l) {
+    L.qkv.push_back(take(qd + 2 * kvd, d));
+    L.o.push_back(take(d, qd));
+    L.gate_up.push_back(take(2 * f, d));
+    L.down.push_back(take(d, f));
+  }
+  L.lm_head = take(c.vocab, d);
+  L.total = off;
+  return L;
 }
 
 // ---- workspace layouts ----
@@ -279,16 +305,17 @@ struct StepWS {   // activations of `rows` token rows
   GemmScratch g;
 };
 
-StepWS take_step(Bump& b, const grpo_config& c, int rows, int gemm_rows) {
+// act_rows: rows of the GEMM inputs h, o and a (the padded batch of a decode step)
+StepWS take_step(Bump& b, const grpo_config& c, int rows, int act_rows, size_t part_floats) {
   StepWS w;
   const int es = esize(c);
   w.x = b.take<float>((size_t)rows * c.d_model);
-  w.h = b.take<char>((size_t)rows * c.d_model * es);
+  w.h = b.take<char>((size_t)act_rows * c.d_model * es);
   w.qkv = b.take<float>((size_t)rows * (qdim(c) + 2 * kvdim(c)));
   w.q = b.take<char>((size_t)rows * qdim(c) * es);
-  w.o = b.take<char>((size_t)rows * qdim(c) * es);
-  w.a = b.take<char>((size_t)rows * c.d_ffn * es);
-  w.g.part = b.take<float>(skinny_scratch(c, gemm_rows));
+  w.o = b.take<char>((size_t)act_rows * qdim(c) * es);
+  w.a = b.take<char>((size_t)act_rows * c.d_ffn * es);
+  w.g.part = b.take<float>(part_floats);
   return w;
 }
 
@@ -300,7 +327,7 @@ struct RolloutWS {
 };
 RolloutWS take_rollout(Bump& b, const grpo_config& c, int B, int max_len) {
   RolloutWS w;
-  w.s = take_step(b, c, B, B);
+  w.s = take_step(b, c, B, c.dtype == GRPO_F32 ? B : decode_nb(B), decode_scratch(c, B));
   w.logits = b.take<float>((size_t)B * c.vocab);
   const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.n_kv_heads, c.head_dim, max_len);
   w.attn_part = b.take<float>(c.dtype == GRPO_F32 ? 0 : ap.part_floats);
@@ -318,7 +345,7 @@ int round8(int t) { return (t + 7) / 8 * 8; }
 PrefillWS take_prefill(Bump& b, const grpo_config& c, int P, int Tp) {
   PrefillWS w;
   const size_t M = (size_t)P * Tp;
-  w.s = take_step(b, c, (int)M, (int)std::max<size_t>(M, P));
+  w.s = take_step(b, c, (int)M, (int)M, 0);
   w.vt = b.take<uint16_t>(c.dtype == GRPO_F32 ? 0 : (size_t)P * kvdim(c) * round8(Tp));
   w.hl = b.take<char>((size_t)P * c.d_model * esize(c));
   w.logits = b.take<float>((size_t)P * c.vocab);
@@ -338,7 +365,7 @@ ScoreWS take_score(Bump& b, const grpo_config& c, int N, int T) {
   w.chunk = std::max(1, std::min(N, kScoreTokens / std::max(T, 1)));
   const size_t M = (size_t)w.chunk * T;
   w.sub_rows = (int)std::max<size_t>(64, std::min<size_t>(8192, kLogitBytes / ((size_t)c.vocab * 4)));
-  w.s = take_step(b, c, (int)M, (int)std::max<size_t>(M, w.sub_rows));
+  w.s = take_step(b, c, (int)M, (int)M, 0);
   const size_t kvn = (size_t)w.chunk * kvdim(c) * T;
   w.kbuf = b.take<char>(kvn * esize(c));
   w.vbuf = b.take<char>(c.dtype == GRPO_F32 ? kvn * 4 : 0);
@@ -371,7 +398,7 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
   const grpo_config& c = m->cfg;
   const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
   const int N = M / T;
-  Partials pend{nullptr, 0, 0, d};
+  const Partials none{nullptr, 0, 0, d};
   int rc;
   for (int l = 0; l < c.n_layers; ++l) {
     void *kl = kbuf, *vl = vbuf;
@@ -380,36 +407,34 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
       kl = L.k;
       vl = L.v;
     }
-    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), pend, m->attn_norm[l], M, d, c.rms_eps,
+    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), none, m->attn_norm[l], M, d, c.rms_eps,
                    w.h, d, st));
     if (hidden_dbg && (rc = copy_rows(hidden_dbg + (size_t)l * M * d, w.x, (size_t)M * d, st)))
       return rc;
-    const float* qsrc;
-    int qs;
-    size_t qstride;
-    if ((rc = gemm_store(m, w.h, d, M, qkv_stack(m, l), qd + 2 * kvd, d, w.qkv, w.g, kMaxSplits,
-                         &qsrc, &qs, &qstride, st, "gemm_decode_qkv")))
+    if ((rc = gemm_rows(m, w.h, d, M, qkv_stack(m, l), qd + 2 * kvd, d, EPI_STORE,
+                        EpiArgs{w.qkv, nullptr, qd + 2 * kvd}, st)))
       return rc;
     RopeArgs ra{};
     ra.mode = 1; ra.T = T; ra.G = G; ra.pos_arr = nullptr;
     ra.n_heads = c.n_heads; ra.n_kv = c.n_kv_heads; ra.hd = c.head_dim; ra.theta = c.rope_theta;
     ra.kcache = kl; ra.vcache = vl; ra.n_seqs = n_slots; ra.max_len = k_len;
     ra.vt = c.dtype == GRPO_F32 ? nullptr : vt; ra.vt_len = round8(T);
-    ra.splits = qs; ra.split_stride = qstride;
-    HIPCHK(rope_kv(c.dtype, qsrc, M, w.q, ra, st));
+    ra.splits = 1; ra.split_stride = 0;
+    HIPCHK(rope_kv(c.dtype, w.qkv, M, w.q, ra, st));
     HIPCHK(attn_prefill(c.dtype, w.q, kl, c.dtype == GRPO_F32 ? vl : (const void*)vt, N, T,
                         c.n_heads, c.n_kv_heads, c.head_dim, k_len, G, w.o, st));
-    if ((rc = gemm_resid(m, w.o, qd, M, one(m->wo[l]), d, qd, w.x, w.g, &pend, st,
-                          "gemm_decode_o"))) return rc;
-    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), pend, m->mlp_norm[l], M, d, c.rms_eps,
+    if ((rc = gemm_rows(m, w.o, qd, M, one(m->wo[l]), d, qd, EPI_RESID, EpiArgs{w.x, nullptr, d},
+                        st)))
+      return rc;
+    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), none, m->mlp_norm[l], M, d, c.rms_eps,
                    w.h, d, st));
-    if ((rc = gemm_swiglu(m, w.h, d, M, gate_up(m, l), f, d, w.a, st))) return rc;
-    if ((rc = gemm_resid(m, w.a, f, M, one(m->w_down[l]), d, f, w.x, w.g, &pend, st,
-                          "gemm_decode_down"))) return rc;
+    if ((rc = gemm_rows(m, w.h, d, M, gate_up(m, l), f, d, EPI_SWIGLU, EpiArgs{nullptr, w.a, f},
+                        st)))
+      return rc;
+    if ((rc = gemm_rows(m, w.a, f, M, one(m->w_down[l]), d, f, EPI_RESID, EpiArgs{w.x, nullptr, d},
+                        st)))
+      return rc;
   }
-  if (pend.splits)   // fold the last layer's partial products into the residual stream
-    HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), pend, nullptr, M, d, c.rms_eps, nullptr, 0,
-                   st));
   if (hidden_dbg && (rc = copy_rows(hidden_dbg + (size_t)c.n_layers * M * d, w.x, (size_t)M * d,
                                     st)))
     return rc;
@@ -465,6 +490,55 @@ int grpo_model_destroy(grpo_model* m) {
   }
   if (m->graph.capture) (void)hipStreamDestroy(m->graph.capture);
   delete m;
+  return GRPO_OK;
+}
+
+size_t grpo_decode_weights_bytes(const grpo_config* cfg) {
+  if (check_config(cfg) || cfg->dtype != GRPO_BF16) return 0;
+  return decode_layout(*cfg).total;
+}
+
+int grpo_model_pack_decode(grpo_model* m, void* buf, size_t bytes, void* stream) {
+  if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
+  const grpo_config& c = m->cfg;
+  if (c.dtype != GRPO_BF16) {
+    g_err.clear();
+    return GRPO_OK;   // fp32 models decode from the row-major weights
+  }
+  const DecodeLayout L = decode_layout(c);
+  if (!buf) return fail(GRPO_INVALID_ARG, "buf is NULL");
+  if (bytes < L.total)
+    return fail(GRPO_INVALID_ARG, "decode weight buffer %zu bytes, need %zu", bytes, L.total);
+  if ((uintptr_t)buf % 256) return fail(GRPO_INVALID_ARG, "buf must be 256-byte aligned");
+  hipStream_t st = (hipStream_t)stream;
+  const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
+  char* base = (char*)buf;
+  auto at = [&](size_t off) { return (uint16_t*)(base + off); };
+  for (int l = 0; l < c.n_layers; ++l) {
+    HIPCHK(pack_frag(PackSrc{{m->wq[l], m->wk[l], m->wv[l]}, qd, qd + kvd, 0}, qd + 2 * kvd, d,
+                     at(L.qkv[l]), st));
+    HIPCHK(pack_frag(PackSrc{{m->wo[l], m->wo[l], m->wo[l]}, d, d, 0}, d, qd, at(L.o[l]), st));
+    HIPCHK(pack_frag(PackSrc{{m->w_gate[l], m->w_up[l], m->w_up[l]}, 0, 0, 1}, 2 * f, d,
+                     at(L.gate_up[l]), st));
+    HIPCHK(pack_frag(PackSrc{{m->w_down[l], m->w_down[l], m->w_down[l]}, d, d, 0}, d, f,
+                     at(L.down[l]), st));
+  }
+  HIPCHK(pack_frag(PackSrc{{m->lm_head, m->lm_head, m->lm_head}, c.vocab, c.vocab, 0}, c.vocab, d,
+                   at(L.lm_head), st));
+  DecodeWeights& D = m->dec;
+  D.base = buf;
+  D.qkv.assign(c.n_layers, nullptr);
+  D.o.assign(c.n_layers, nullptr);
+  D.gate_up.assign(c.n_layers, nullptr);
+  D.down.assign(c.n_layers, nullptr);
+  for (int l = 0; l < c.n_layers; ++l) {
+    D.qkv[l] = at(L.qkv[l]);
+    D.o[l] = at(L.o[l]);
+    D.gate_up[l] = at(L.gate_up[l]);
+    D.down[l] = at(L.down[l]);
+  }
+  D.lm_head = at(L.lm_head);
+  g_err.clear();
   return GRPO_OK;
 }
 
@@ -548,14 +622,9 @@ int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
   const Partials none{nullptr, 0, 0, d};
   HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{0, 1, Tp, Tp - 1}, none, m->final_norm, P, d, c.rms_eps,
                  w.hl, d, st));
-  {
-    const float* res;
-    int ns;
-    size_t nst;
-    if (int rc = gemm_store(m, w.hl, d, P, one(m->lm_head), c.vocab, d, w.logits, w.s.g, 1, &res,
-                            &ns, &nst, st, "gemm_decode_lm_head"))
-      return rc;
-  }
+  if (int rc = gemm_rows(m, w.hl, d, P, one(m->lm_head), c.vocab, d, EPI_STORE,
+                         EpiArgs{w.logits, nullptr, c.vocab}, st))
+    return rc;
   SampleArgs sa{};
   sa.temperature = s->temperature; sa.top_k = s->top_k; sa.seed = s->seed; sa.step = 0;
   sa.G = G; sa.tok_out = tok_out; sa.logp_out = logp_out; sa.out_stride = 1;
@@ -586,10 +655,14 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
   const size_t need = grpo_workspace_bytes(m, GRPO_OP_ROLLOUT, B, max_len);
   if (ws_bytes < need)
     return fail(GRPO_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
+  if (c.dtype == GRPO_BF16 && !m->dec.base)
+    return fail(GRPO_INVALID_ARG, "bf16 model without decode weights (grpo_model_pack_decode)");
   hipStream_t st = (hipStream_t)stream;
   Bump b(ws);
   RolloutWS w = take_rollout(b, c, B, max_len);
   const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
+  const bool pk = c.dtype == GRPO_BF16;
+  const int nb = pk ? decode_nb(B) : 0;
   const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.n_kv_heads, c.head_dim, max_len);
   // One decode step on stream `ss`.  In graph mode the Philox step and the output
   // column come from the device step counter (advanced by the embedding kernel).
@@ -599,18 +672,26 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
     int rc;
     hipStream_t st = ss;
     HIPCHK(embed(c.dtype, m->tok_emb, tok, B, d, c.vocab, w.s.x, st, graph ? w.step_ctr : nullptr));
+    // bf16: GEMM inputs in fragment order, products as split-K partials;
+    // fp32: row-major, products straight into their destinations
     Partials pend{nullptr, 0, 0, d};
+    const DecodeWeights& D = m->dec;
     for (int l = 0; l < c.n_layers; ++l) {
       Layer L = kv_layer(m, kv, l, n_seqs, max_len);
       HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), pend, m->attn_norm[l], B, d,
-                     c.rms_eps, w.s.h, d, st));
+                     c.rms_eps, w.s.h, d, st, nb));
       if (hdbg && (rc = copy_rows(hdbg + (size_t)l * B * d, w.s.x, (size_t)B * d, st))) return rc;
-      const float* qsrc;
-      int qs;
-      size_t qstride;
-      if ((rc = gemm_store(m, w.s.h, d, B, qkv_stack(m, l), qd + 2 * kvd, d, w.s.qkv, w.s.g,
-                           kMaxSplits, &qsrc, &qs, &qstride, st, "gemm_decode_qkv")))
+      const float* qsrc = w.s.qkv;
+      int qs = 1;
+      size_t qstride = 0;
+      if (pk) {
+        if ((rc = gemm_dec(w.s.h, B, D.qkv[l], qd + 2 * kvd, d, w.s.qkv, w.s.g, kMaxSplits, &qsrc,
+                           &qs, &qstride, st, "gemm_decode_qkv")))
+          return rc;
+      } else if ((rc = gemm_rows(m, w.s.h, d, B, qkv_stack(m, l), qd + 2 * kvd, d, EPI_STORE,
+                                 EpiArgs{w.s.qkv, nullptr, qd + 2 * kvd}, st))) {
         return rc;
+      }
       RopeArgs ra{};
       ra.mode = 0; ra.T = 1; ra.G = 1; ra.pos_arr = pos;
       ra.n_heads = c.n_heads; ra.n_kv = c.n_kv_heads; ra.hd = c.head_dim; ra.theta = c.rope_theta;
@@ -619,28 +700,43 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
       ra.splits = qs; ra.split_stride = qstride;
       HIPCHK(rope_kv(c.dtype, qsrc, B, w.s.q, ra, st));
       HIPCHK(attn_decode(c.dtype, w.s.q, L.k, L.v, pos, B, c.n_heads, c.n_kv_heads, c.head_dim,
-                         n_seqs, max_len, ap, w.attn_part, w.s.o, st));
-      if ((rc = gemm_resid(m, w.s.o, qd, B, one(m->wo[l]), d, qd, w.s.x, w.s.g, &pend, st,
-                          "gemm_decode_o")))
+                         n_seqs, max_len, ap, w.attn_part, w.s.o, st, nb));
+      if (pk) {
+        if ((rc = gemm_dec_resid(w.s.o, B, D.o[l], d, qd, w.s.g, &pend, st, "gemm_decode_o")))
+          return rc;
+      } else if ((rc = gemm_rows(m, w.s.o, qd, B, one(m->wo[l]), d, qd, EPI_RESID,
+                                 EpiArgs{w.s.x, nullptr, d}, st))) {
         return rc;
+      }
       HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), pend, m->mlp_norm[l], B, d, c.rms_eps,
-                     w.s.h, d, st));
-      if ((rc = gemm_swiglu(m, w.s.h, d, B, gate_up(m, l), f, d, w.s.a, st))) return rc;
-      if ((rc = gemm_resid(m, w.s.a, f, B, one(m->w_down[l]), d, f, w.s.x, w.s.g, &pend, st,
-                          "gemm_decode_down")))
-        return rc;
+                     w.s.h, d, st, nb));
+      if (pk) {
+        if ((rc = gemm_dec_swiglu(w.s.h, B, D.gate_up[l], f, d, w.s.a, st))) return rc;
+        if ((rc = gemm_dec_resid(w.s.a, B, D.down[l], d, f, w.s.g, &pend, st, "gemm_decode_down")))
+          return rc;
+      } else {
+        if ((rc = gemm_rows(m, w.s.h, d, B, gate_up(m, l), f, d, EPI_SWIGLU,
+                            EpiArgs{nullptr, w.s.a, f}, st)))
+          return rc;
+        if ((rc = gemm_rows(m, w.s.a, f, B, one(m->w_down[l]), d, f, EPI_RESID,
+                            EpiArgs{w.s.x, nullptr, d}, st)))
+          return rc;
+      }
     }
     HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), pend, m->final_norm, B, d, c.rms_eps,
-                   w.s.h, d, st));
+                   w.s.h, d, st, nb));
     if (hdbg && (rc = copy_rows(hdbg + (size_t)c.n_layers * B * d, w.s.x, (size_t)B * d, st)))
       return rc;
-    {
+    if (pk) {
       const float* res;
       int ns;
       size_t nst;
-      if ((rc = gemm_store(m, w.s.h, d, B, one(m->lm_head), c.vocab, d, w.logits, w.s.g, 1, &res,
-                           &ns, &nst, st, "gemm_decode_lm_head")))
+      if ((rc = gemm_dec(w.s.h, B, D.lm_head, c.vocab, d, w.logits, w.s.g, 1, &res, &ns, &nst, st,
+                         "gemm_decode_lm_head")))
         return rc;
+    } else if ((rc = gemm_rows(m, w.s.h, d, B, one(m->lm_head), c.vocab, d, EPI_STORE,
+                               EpiArgs{w.logits, nullptr, c.vocab}, st))) {
+      return rc;
     }
     SampleArgs sa{};
     sa.temperature = s->temperature; sa.top_k = s->top_k; sa.seed = s->seed;
@@ -674,6 +770,7 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
       (uint64_t)(uintptr_t)kv, (uint64_t)n_seqs, (uint64_t)max_len, (uint64_t)B,
       (uint64_t)(uintptr_t)pos, (uint64_t)(uintptr_t)tok, (uint64_t)step0, (uint64_t)n_steps,
       (uint64_t)(uintptr_t)tok_out, (uint64_t)(uintptr_t)logp_out, (uint64_t)(uintptr_t)ws,
+      (uint64_t)(uintptr_t)m->dec.base,
       (uint64_t)*(const uint32_t*)&s->temperature, (uint64_t)(uint32_t)s->top_k, s->seed};
   HIPCHK(fill_i32(w.step_ctr, 1, -1, st));   // the first replay's embedding makes it 0
   if (!dg.exec || dg.key != key) {
@@ -739,11 +836,8 @@ int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, 
       const int rc_rows = std::min(w.sub_rows, R - i0);
       HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{i0, Ts, T, score_from - 1}, none, m->final_norm,
                      rc_rows, d, c.rms_eps, w.hs, d, st));
-      const float* res;
-      int ns;
-      size_t nst;
-      if (int rc = gemm_store(m, w.hs, d, rc_rows, one(m->lm_head), c.vocab, d, w.logits, w.s.g, 1,
-                              &res, &ns, &nst, st, "gemm_decode_lm_head"))
+      if (int rc = gemm_rows(m, w.hs, d, rc_rows, one(m->lm_head), c.vocab, d, EPI_STORE,
+                             EpiArgs{w.logits, nullptr, c.vocab}, st))
         return rc;
       HIPCHK(token_logprob(w.logits, rc_rows, c.vocab, c.vocab, tk, T, score_from, Ts, i0,
                            temperature, logp_out + (size_t)n0 * Ts + i0, st));

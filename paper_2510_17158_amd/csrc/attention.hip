@@ -44,7 +44,8 @@ template <int HD, int MAXG>
 __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const int32_t* __restrict__ pos, int H, int n_kv, int max_len, int S, int span, float scale,
-    float* __restrict__ part_o, float* __restrict__ part_ml, bf16_t* __restrict__ out) {
+    float* __restrict__ part_o, float* __restrict__ part_ml, bf16_t* __restrict__ out,
+    int pack_nb) {
   constexpr int QSTEPS = HD / 32;     // MFMA k-steps over the head dim
   constexpr int LPT = HD / 8;         // lanes per position in P.V
   constexpr int PPW = 64 / LPT;       // positions per V load instruction
@@ -227,7 +228,8 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
       L = fmaf(c, wl[w][h], L);
     }
     if (S == 1) {
-      out[((size_t)b * H + g * GQ + h) * HD + e] = f2bf(x / L);
+      const int k = (g * GQ + h) * HD + e;
+      out[pack_nb ? act_frag_index(b, k, pack_nb) : (size_t)b * H * HD + k] = f2bf(x / L);
     } else {
       const size_t row = ((size_t)b * H + g * GQ + h) * S + split;
       part_o[row * HD + e] = x;
@@ -241,7 +243,7 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const float* __restrict__ p
                                                      const float* __restrict__ part_ml,
                                                      const int32_t* __restrict__ pos, int H,
                                                      int max_len, int S, int span,
-                                                     bf16_t* __restrict__ out) {
+                                                     bf16_t* __restrict__ out, int pack_nb) {
   const int h = blockIdx.x, b = blockIdx.y, e = threadIdx.x;
   const int ctx = min(pos[b], max_len - 1) + 1;
   const int ns = min(S, (ctx + span - 1) / span);
@@ -254,7 +256,8 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const float* __restrict__ p
     L = fmaf(part_ml[(row0 + s) * 2 + 1], w, L);
     acc = fmaf(part_o[(row0 + s) * HD + e], w, acc);
   }
-  out[((size_t)b * H + h) * HD + e] = f2bf(acc / L);
+  const int k = h * HD + e;
+  out[pack_nb ? act_frag_index(b, k, pack_nb) : (size_t)b * H * HD + k] = f2bf(acc / L);
 }
 
 // ----------------------------------------------------------- flash attention, bf16
@@ -568,17 +571,19 @@ template <int HD, int MAXG>
 static void launch_decode(dim3 grid, hipStream_t st, const void* q, const void* kc,
                           const void* vc, const int32_t* pos, int H, int n_kv, int max_len,
                           const DecodeAttnPlan& p, float scale, float* part_o, float* part_ml,
-                          void* out) {
+                          void* out, int pack_nb) {
   k_attn_decode_bf16<HD, MAXG><<<grid, 256, 0, st>>>(
       (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, H, n_kv, max_len, p.splits,
-      p.tc, scale, part_o, part_ml, (bf16_t*)out);
+      p.tc, scale, part_o, part_ml, (bf16_t*)out, pack_nb);
 }
 
 hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
                        const int32_t* pos, int B, int H, int n_kv, int hd, int n_seqs, int max_len,
-                       const DecodeAttnPlan& p, float* part, void* out, hipStream_t st) {
+                       const DecodeAttnPlan& p, float* part, void* out, hipStream_t st,
+                       int pack_nb) {
   (void)n_seqs;
   if (B <= 0) return hipSuccess;
+  if (pack_nb && (dtype == 0 || B > pack_nb || pack_nb % 16)) return hipErrorInvalidValue;
   const float scale = 1.f / sqrtf((float)hd);
   if (dtype == 0) {
     dim3 grid(B, H);
@@ -595,11 +600,11 @@ hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
   {
     Prof pf("attn_decode", st);
     if (hd == 128) {
-      if (gq <= 4) launch_decode<128, 4>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out);
-      else launch_decode<128, 8>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out);
+      if (gq <= 4) launch_decode<128, 4>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
+      else launch_decode<128, 8>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
     } else {
-      if (gq <= 4) launch_decode<64, 4>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out);
-      else launch_decode<64, 8>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out);
+      if (gq <= 4) launch_decode<64, 4>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
+      else launch_decode<64, 8>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
     }
   }
   if (p.splits > 1) {
@@ -607,10 +612,10 @@ hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
     dim3 cgrid(H, B);
     if (hd == 128)
       k_attn_combine<128><<<cgrid, 128, 0, st>>>(part_o, part_ml, pos, H, max_len, p.splits,
-                                                 p.tc, (bf16_t*)out);
+                                                 p.tc, (bf16_t*)out, pack_nb);
     else
       k_attn_combine<64><<<cgrid, 64, 0, st>>>(part_o, part_ml, pos, H, max_len, p.splits,
-                                               p.tc, (bf16_t*)out);
+                                               p.tc, (bf16_t*)out, pack_nb);
   }
   return hipGetLastError();
 }

@@ -83,3 +83,13 @@ __device__ __forceinline__ float block_max(float v, float* sh) {
 }
 
 __device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+// ---- fragment order of the decode GEMM's activations ---------------------------
+// Element (b, k) of an activation [nb][K] (nb: the padded batch, a multiple of 16)
+// stored as MFMA B-operand fragments: fragment (k / 32, b / 16) is 1 KB, lane
+// (b % 16) + 16 ((k / 8) % 4) holding elements k % 8 = 0..7; fragments ordered by
+// k step, then batch block.
+__device__ __forceinline__ size_t act_frag_index(int b, int k, int nb) {
+  return ((size_t)(k >> 5) * (nb >> 4) + (b >> 4)) * 512 + ((b & 15) + 16 * ((k >> 3) & 3)) * 8 +
+         (k & 7);
+}

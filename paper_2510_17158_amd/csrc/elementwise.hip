@@ -54,7 +54,7 @@ __device__ __forceinline__ float4 load4<bf16_t>(const bf16_t* g, size_t i) {
 template <typename T>
 __global__ __launch_bounds__(NORM_NT) void k_rmsnorm(float* x, int ldx, RowMap rm, Partials pp,
                                                      const T* g, int d, float eps, T* out,
-                                                     int ldo) {
+                                                     int ldo, int pack_nb) {
   __shared__ float sh[NORM_NT / 64];
   const int m = blockIdx.x;
   const int gi = rm.i0 + m;
@@ -104,7 +104,7 @@ __global__ __launch_bounds__(NORM_NT) void k_rmsnorm(float* x, int ldx, RowMap r
     const int i4 = threadIdx.x + k * NORM_NT;
     if (i4 < n4) {
       const float4 gv = load4(g, 4 * (size_t)i4);
-      store4(out, (size_t)m * ldo + 4 * i4,
+      store4(out, pack_nb ? act_frag_index(m, 4 * i4, pack_nb) : (size_t)m * ldo + 4 * i4,
              make_float4(v[k].x * r * gv.x, v[k].y * r * gv.y, v[k].z * r * gv.z,
                          v[k].w * r * gv.w));
     }
@@ -209,16 +209,17 @@ hipError_t embed(int dtype, const void* emb, const int32_t* tok, int M, int d, i
 }
 
 hipError_t rmsnorm(int dtype, float* x, int ldx, RowMap rows, Partials p, const void* g, int M,
-                   int d, float eps, void* out, int ldo, hipStream_t st) {
+                   int d, float eps, void* out, int ldo, hipStream_t st, int pack_nb) {
   if (M <= 0) return hipSuccess;
+  if (pack_nb && (dtype == 0 || M > pack_nb || pack_nb % 16 || d % 32)) return hipErrorInvalidValue;
   Prof pf(M <= 128 ? "rmsnorm" : "rmsnorm_rows", st);
   if (d % 4 || d > 4 * NORM_NT * NORM_VPT) return hipErrorInvalidValue;
   if (dtype == 0)
     k_rmsnorm<float><<<M, NORM_NT, 0, st>>>(x, ldx, rows, p, (const float*)g, d, eps,
-                                            (float*)out, ldo);
+                                            (float*)out, ldo, 0);
   else
     k_rmsnorm<bf16_t><<<M, NORM_NT, 0, st>>>(x, ldx, rows, p, (const bf16_t*)g, d, eps,
-                                             (bf16_t*)out, ldo);
+                                             (bf16_t*)out, ldo, pack_nb);
   return hipGetLastError();
 }
 

@@ -1,0 +1,269 @@
+// Decode GEMM: Y[B, N] = X[B, K] . W[N, K]^T with few rows (B <= 128), on
+// operands stored in MFMA fragment order.
+//
+// Decode is bound by streaming the weights from HBM once per step; each weight
+// element is used B times, which at B = 64 is 64 flop per 2 bytes: more than the
+// fp32 vector units deliver at full HBM rate, so the products run on MFMA
+// (v_mfma_f32_16x16x32_bf16) with the weights as the A operand (16 output rows
+// per MFMA) and the activations as the B operand (16 batch columns per MFMA).
+//
+// Fragment order.  The A operand of one MFMA is 16 rows x 32 k, lane l holding
+// row l & 15, elements 8 (l >> 4) .. 8 (l >> 4) + 7: 64 lanes x 16 bytes.  The
+// decode copy of a weight matrix stores each such fragment as 1 KB in lane order,
+// fragments of a 16-row block consecutive along k ([N/16][K/32][64][8]), so every
+// weight load instruction of a wave reads 1 KB of contiguous memory (a row-major
+// matrix gives 64-byte pieces of 16 rows per instruction, measurably slower to
+// stream).  The activations entering a decode GEMM are written by their producer
+// (RMSNorm, attention, the SwiGLU epilogue below) in the same order with the
+// batch as the row ([K/32][nb/16][64][8], nb = padded batch), so they too arrive
+// in 1 KB contiguous loads.
+//
+// Work split: a workgroup of 4 waves owns RB fragment rows (16 RB weight rows;
+// for SwiGLU the gate and up rows of the same outputs alternate by 16-row block)
+// and one K range cut into 32-wide steps dealt round-robin to the waves.  Each
+// wave keeps D steps of weight and activation fragments in a register ring that
+// is unrolled at compile time, so loads run D - 1 steps ahead of the MFMAs and no
+// in-flight register is ever copied (a copy would make the wave wait for the
+// load).  Weight loads are non-temporal: each weight byte is used once per step,
+// and keeping it out of the way of the activations (read by every workgroup)
+// measured faster.  At the end the four waves' accumulators are added in a fixed
+// order ((w0 + w2) + (w1 + w3)) through LDS and written out: split-K partial
+// products [split][B][N] in fp32 for the consuming kernel (RMSNorm with the
+// residual add, or RoPE) to add in split order, or silu(gate) * up rounded to
+// bf16 in fragment order for the down projection.  No atomics; the result does
+// not depend on timing.
+#include "common.h"
+#include "kernels.h"
+
+namespace grpo {
+
+namespace {
+
+constexpr int NT = 256;
+constexpr int FRAG = 512;              // elements of one fragment (1 KB)
+constexpr int KGRAN = 128;             // k granularity of a split (4 waves x 32)
+
+struct DArgs {
+  const bf16_t* X;    // fragment order [K/32][NB/16]
+  const bf16_t* W;    // fragment order [N/16][K/32]
+  int B, N, K, kper, tiles;
+  float* out_f32; bf16_t* out_act; int ld_out;
+};
+
+// ring slot S <- step i (clamped to the last step: the repeat is never used)
+#define DG_LOAD(S, i)                                                           \
+  do {                                                                          \
+    const int i_ = min((i), nst - 1);                                           \
+    _Pragma("unroll") for (int rb = 0; rb < RB; ++rb)                           \
+        wr[S][rb] = __builtin_nontemporal_load(                                 \
+            (const u32x4_t*)(wp[rb] + (size_t)i_ * (4 * FRAG)));                \
+    _Pragma("unroll") for (int j = 0; j < NJ; ++j)                              \
+        xr[S][j] = *(const u32x4_t*)(xp + (size_t)i_ * (4 * NJ * FRAG) + j * FRAG); \
+  } while (0)
+
+#define DG_MMA(S)                                                               \
+  do {                                                                          \
+    _Pragma("unroll") for (int rb = 0; rb < RB; ++rb)                           \
+    _Pragma("unroll") for (int j = 0; j < NJ; ++j)                              \
+        acc[rb][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(                   \
+            __builtin_bit_cast(bf16x8_t, wr[S][rb]),                            \
+            __builtin_bit_cast(bf16x8_t, xr[S][j]), acc[rb][j], 0, 0, 0);       \
+  } while (0)
+
+template <int NB, int RB, int D, int EPI>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2)))
+void k_gemm_decode(DArgs a) {
+  constexpr int NJ = NB / 16;            // MFMA batch blocks
+  constexpr int ROWS = 16 * RB;          // weight rows of the tile
+  constexpr int CT = ROWS + 4;           // padded row of the [batch][row] LDS tile
+  __shared__ __attribute__((aligned(16))) float red[2 * NB * CT];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const int tile = blockIdx.x % a.tiles, ks = blockIdx.x / a.tiles;
+  const int KT = a.K / 32;
+  const int kt0 = ks * (a.kper / 32) + wave;           // this wave's first k step
+  const int nst = a.kper / KGRAN;                      // steps per wave
+
+  // fragment rows past the end repeat the last one (their outputs are never written)
+  const bf16_t* wp[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+    wp[rb] = a.W + ((size_t)min(tile * RB + rb, a.N / 16 - 1) * KT + kt0) * FRAG + lane * 8;
+  // batch rows past B hold whatever the producer left there: MFMA columns are
+  // independent and those columns are never written
+  const bf16_t* xp = a.X + (size_t)kt0 * NJ * FRAG + lane * 8;
+
+  f32x4_t acc[RB][NJ];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[rb][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+
+  u32x4_t wr[D][RB], xr[D][NJ];
+#pragma unroll
+  for (int p = 0; p < D - 1; ++p) DG_LOAD(p, p);
+  // whole ring turns without a branch, then the remaining nst % D steps
+  int i0 = 0;
+  for (; i0 + D <= nst; i0 += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      // fences keep the scheduler from sinking the loads below the MFMAs
+      DG_LOAD((u + D - 1) % D, i0 + u + D - 1);
+      __builtin_amdgcn_sched_barrier(0);
+      DG_MMA(u);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  const int rem = nst - i0;
+#pragma unroll
+  for (int u = 0; u < D - 1; ++u)
+    if (u < rem) DG_MMA(u);
+
+  // ---- fixed-order sum of the four waves' products in LDS [batch][row] ----
+  // C layout of the 16x16 MFMA: row 4 g + v, column r16.
+  float* r0 = red;
+  float* r1 = red + NB * CT;
+  auto put = [&](float* dst) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        *(f32x4_t*)(dst + (16 * j + r16) * CT + rb * 16 + 4 * g) = acc[rb][j];
+  };
+  auto add = [&](const float* src) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        acc[rb][j] += *(const f32x4_t*)(src + (16 * j + r16) * CT + rb * 16 + 4 * g);
+  };
+  if (wave >= 2) put(wave == 2 ? r0 : r1);
+  __syncthreads();
+  if (wave < 2) {
+    add(wave == 0 ? r0 : r1);
+    if (wave == 1) put(r1);
+  }
+  __syncthreads();
+  if (wave == 0) {
+    add(r1);
+    put(r0);
+  }
+  __syncthreads();
+
+  // ---- epilogue: consecutive threads take consecutive output columns ----
+  if (EPI == EPI_SWIGLU) {
+    // tile rows: gate block 2 o_b then up block 2 o_b + 1 for output block o_b
+    constexpr int HO = ROWS / 2;
+    for (int i = tid; i < HO * NB; i += NT) {
+      const int o = i % HO, b = i / HO;
+      const int n = tile * HO + o;
+      if (b < a.B && n < a.ld_out) {
+        const int rg = (o >> 4) * 32 + (o & 15);
+        const float gt = r0[b * CT + rg], up = r0[b * CT + rg + 16];
+        const float sg = gt / (1.f + __expf(-gt));
+        a.out_act[act_frag_index(b, n, NB)] = f2bf(sg * up);
+      }
+    }
+  } else {
+    float* out = a.out_f32 + (size_t)ks * a.B * a.ld_out;
+    for (int i = tid; i < ROWS * NB; i += NT) {
+      const int r = i % ROWS, b = i / ROWS;
+      const int n = tile * ROWS + r;
+      if (b < a.B && n < a.N) out[(size_t)b * a.ld_out + n] = r0[b * CT + r];
+    }
+  }
+}
+
+#undef DG_LOAD
+#undef DG_MMA
+
+template <int NB>
+hipError_t launch_nb(const DArgs& a, int epi, int grid, const char* name, hipStream_t st) {
+  constexpr int RB = decode_rb(NB);
+  constexpr int D = 3;
+  if (epi == EPI_SWIGLU) {
+    Prof pf(name ? name : "gemm_decode_swiglu", st);
+    k_gemm_decode<NB, RB, D, EPI_SWIGLU><<<grid, NT, 0, st>>>(a);
+  } else {
+    Prof pf(name ? name : "gemm_decode", st);
+    k_gemm_decode<NB, RB, D, EPI_PARTIAL><<<grid, NT, 0, st>>>(a);
+  }
+  return hipGetLastError();
+}
+
+// One thread per 16-byte piece of the fragment-order copy: piece u is lane
+// u % 64 of fragment (R, kt) = (u / 64 / KT, u / 64 % KT).
+__global__ __launch_bounds__(256) void k_pack_frag(PackSrc s, int N, int K, bf16_t* __restrict__ dst) {
+  const size_t u = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int KT = K / 32;
+  const size_t total = (size_t)N / 16 * KT * 64;
+  if (u >= total) return;
+  const int l = (int)(u % 64);
+  const size_t f = u / 64;
+  const int kt = (int)(f % KT), R = (int)(f / KT);
+  const int k = kt * 32 + 8 * (l >> 4);
+  const bf16_t* row;
+  if (s.interleave) {
+    // fragment rows alternate: even R = rows of s.w[0], odd R = the same rows of s.w[1]
+    const int n = (R >> 1) * 16 + (l & 15);
+    row = (const bf16_t*)s.w[R & 1] + (size_t)n * K;
+  } else {
+    const int n = R * 16 + (l & 15);
+    if (n < s.n1) row = (const bf16_t*)s.w[0] + (size_t)n * K;
+    else if (n < s.n2) row = (const bf16_t*)s.w[1] + (size_t)(n - s.n1) * K;
+    else row = (const bf16_t*)s.w[2] + (size_t)(n - s.n2) * K;
+  }
+  *(u32x4_t*)(dst + u * 8) = *(const u32x4_t*)(row + k);
+}
+
+}  // namespace
+
+int decode_nb(int B) { return B <= 16 ? 16 : B <= 32 ? 32 : B <= 64 ? 64 : 128; }
+
+DecodePlan decode_plan(int B, int N, int K, int epi, int target_wgs, int max_splits) {
+  DecodePlan p{};
+  p.nb = decode_nb(B);
+  const int rows = 16 * decode_rb(p.nb);
+  p.tiles = (N + rows - 1) / rows;
+  const int nchunk = K / KGRAN;
+  p.splits = 1;
+  if (target_wgs <= 0) target_wgs = 512;
+  // SwiGLU needs complete gate and up sums in one workgroup: never split
+  for (int d = 1; epi != EPI_SWIGLU && d <= nchunk && d <= max_splits; ++d) {
+    if (nchunk % d) continue;
+    p.splits = d;
+    if ((long)p.tiles * d >= target_wgs) break;
+  }
+  return p;
+}
+
+hipError_t gemm_decode_bf16(const uint16_t* Xf, int B, const uint16_t* Wf, int N, int K, int epi,
+                            EpiArgs ep, const DecodePlan& p, hipStream_t st) {
+  if (B < 1 || B > p.nb || p.nb != decode_nb(B) || N % 16 || K % KGRAN || p.splits < 1 ||
+      (K / p.splits) % KGRAN || (epi == EPI_SWIGLU && (N % 32 || ep.ld_out != N / 2)))
+    return hipErrorInvalidValue;
+  DArgs a;
+  a.X = (const bf16_t*)Xf; a.W = (const bf16_t*)Wf;
+  a.B = B; a.N = N; a.K = K; a.kper = K / p.splits; a.tiles = p.tiles;
+  a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;
+  const int grid = p.tiles * p.splits;
+  switch (p.nb) {
+    case 16: return launch_nb<16>(a, epi, grid, ep.name, st);
+    case 32: return launch_nb<32>(a, epi, grid, ep.name, st);
+    case 64: return launch_nb<64>(a, epi, grid, ep.name, st);
+    case 128: return launch_nb<128>(a, epi, grid, ep.name, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t pack_frag(const PackSrc& s, int N, int K, uint16_t* dst, hipStream_t st) {
+  if (N % 16 || K % 32 || N <= 0 || K <= 0) return hipErrorInvalidValue;
+  const size_t total = (size_t)N / 16 * (K / 32) * 64;
+  Prof pf("pack_frag", st);
+  k_pack_frag<<<(unsigned)((total + 255) / 256), 256, 0, st>>>(s, N, K, (bf16_t*)dst);
+  return hipGetLastError();
+}
+
+}  // namespace grpo

@@ -39,17 +39,30 @@ struct EpiArgs {
 };
 
 // ---- decode GEMM: Y[B, N] = X[B, K] . W[N, K]^T for B <= 128 (bf16 MFMA) ----
-// epi is EPI_PARTIAL (out_f32 [splits][B][ld_out]) or EPI_SWIGLU (N = d_ffn, W
-// stacks (gate, up) with n1 = N, out_act [B][ld_out], never split).
-struct SkinnyPlan {
-  int nb;        // padded batch (16, 32, 64, 128)
-  int kc;        // K chunk staged in LDS
-  int tiles;     // output tiles
+// Operands in fragment order: X [K/32][nb/16][64][8] (act_frag_index, nb =
+// decode_nb(B)), W [N/16][K/32][64][8] (pack_frag).  epi is EPI_PARTIAL
+// (out_f32 [splits][B][ld_out] row-major) or EPI_SWIGLU (W = pack_frag of
+// (gate, up) interleaved by 16-row blocks, N = 2 d_ffn, out_act = silu(gate) * up
+// in fragment order [nb][ld_out = d_ffn], never split).  N % 16 == 0, K % 128 == 0.
+constexpr int decode_rb(int nb) { return nb >= 128 ? 2 : 4; }   // 16-row blocks per tile
+int decode_nb(int B);                                           // 16, 32, 64 or 128
+struct DecodePlan {
+  int nb;        // padded batch
+  int tiles;     // output tiles of 16 * decode_rb(nb) weight rows
   int splits;    // split-K factor (partial products written)
 };
-SkinnyPlan skinny_plan(int B, int N, int K, int epi, int target_wgs, int max_splits = kMaxSplits);
-hipError_t gemm_skinny_bf16(const uint16_t* X, int ldx, int B, WStack W, int N, int K, int epi,
-                            EpiArgs ep, const SkinnyPlan& p, hipStream_t st);
+DecodePlan decode_plan(int B, int N, int K, int epi, int target_wgs, int max_splits = kMaxSplits);
+hipError_t gemm_decode_bf16(const uint16_t* Xf, int B, const uint16_t* Wf, int N, int K, int epi,
+                            EpiArgs ep, const DecodePlan& p, hipStream_t st);
+// Fragment-order copy [N/16][K/32][64][8] of N row-major bf16 rows of length K:
+// row n from w[0] (n < n1), w[1] (n1 <= n < n2) or w[2]; with interleave, the
+// 16-row blocks of w[0] and w[1] alternate (w[0] block i is fragment row 2i).
+struct PackSrc {
+  const void* w[3];
+  int n1, n2;
+  int interleave;
+};
+hipError_t pack_frag(const PackSrc& s, int N, int K, uint16_t* dst, hipStream_t st);
 
 // ---- tiled GEMM for many rows (prefill / scoring): bf16 MFMA -----------------
 hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, int K, int epi,
@@ -77,9 +90,10 @@ struct Partials {
   int ld;
 };
 // With p.splits > 0, first x[src(m)] += sum_s part (split order, written back).
-// Then, if g != NULL, out[m] = round(x[src(m)] / sqrt(mean(x^2) + eps) * g).
+// Then, if g != NULL, out[m] = round(x[src(m)] / sqrt(mean(x^2) + eps) * g), row-major
+// with row stride ldo, or (pack_nb > 0, bf16) in decode-GEMM fragment order [pack_nb][d].
 hipError_t rmsnorm(int dtype, float* x, int ldx, RowMap rows, Partials p, const void* g, int M,
-                   int d, float eps, void* out, int ldo, hipStream_t st);
+                   int d, float eps, void* out, int ldo, hipStream_t st, int pack_nb = 0);
 hipError_t fill_i32(int32_t* p, size_t n, int32_t v, hipStream_t st);
 // Rotary embedding + cache write.  qkv fp32 [M, q_dim + 2 kv_dim], or the sum
 // of `splits` such arrays split_stride floats apart (decode GEMM partials).  Row m is
@@ -102,14 +116,16 @@ hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeAr
 
 // ---- attention -------------------------------------------------------------------
 // Decode: q act [B, H, hd]; cache layer base K/V [n_seqs][n_kv][max_len][hd];
-// attends positions 0..pos[b].  out act [B, H*hd].
+// attends positions 0..pos[b].  out act [B, H*hd] row-major, or (pack_nb > 0) in
+// decode-GEMM fragment order [pack_nb][H*hd].
 // tc: context positions per span (a multiple of 128); splits: spans per (sequence,
 // kv head); part_floats: fp32 scratch for the span merge (0 with a single span).
 struct DecodeAttnPlan { int tc; int splits; size_t part_floats; };
 DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len);
 hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
                        const int32_t* pos, int B, int H, int n_kv, int hd, int n_seqs, int max_len,
-                       const DecodeAttnPlan& p, float* part, void* out, hipStream_t st);
+                       const DecodeAttnPlan& p, float* part, void* out, hipStream_t st,
+                       int pack_nb = 0);
 // Causal attention over N sequences of T rows: q act [N*T, H*hd]; K in cache
 // layout [n][n_kv][k_len][hd] (sequence n at slot n*k_stride_seq), Vt
 // [n][n_kv][hd][T] (bf16 path) or V in cache layout (fp32 path).  out act [N*T, H*hd].

@@ -48,7 +48,8 @@ def test_config_validation():
     for bad, code in [(dict(head_dim=96), api.UNSUPPORTED), (dict(n_kv_heads=5), api.UNSUPPORTED),
                       (dict(dtype=7), api.UNSUPPORTED), (dict(n_layers=0), api.INVALID_ARG),
                       (dict(d_model=800), api.UNSUPPORTED), (dict(n_heads=48, n_kv_heads=4),
-                                                             api.UNSUPPORTED)]:
+                                                             api.UNSUPPORTED),
+                      (dict(vocab=32001), api.UNSUPPORTED)]:
         import dataclasses
         rc, h, _ = _fake_model(dataclasses.replace(cfg, **bad))
         assert rc == code, (bad, rc)
@@ -68,6 +69,31 @@ def test_sizes():
     assert api.workspace_bytes(None, api.OP_LOSS, 64, 2048) >= 64 * 9 * 8
     assert api.workspace_bytes(m, api.OP_ROLLOUT, 0, 10) == 0
     api.lib().grpo_model_destroy(h)
+
+
+def test_decode_weights_size_and_errors():
+    L = api.lib()
+    c = get("small").model
+    d, qd, kvd, f = c.d_model, c.q_dim, c.kv_dim, c.d_ffn
+    per_layer = (qd + 2 * kvd) * d + d * qd + 2 * f * d + d * f
+    want = (c.n_layers * per_layer + c.vocab * d) * 2   # every piece is a multiple of 256 bytes
+    assert L.grpo_decode_weights_bytes(C.byref(api.config_struct(c))) == want
+    assert L.grpo_decode_weights_bytes(C.byref(api.config_struct(get("tiny").model))) == 0
+    rc, h, keep = _fake_model(c)
+    p = C.c_void_p(0x1000)
+    # no decode copy yet: a bf16 rollout step is refused before any device work
+    s = api.Sampling(1.0, 0, 1)
+    assert L.grpo_rollout_step(h, p, 64, 100, 64, p, p, 10, 1, 2, C.byref(s), p, p, None, None, p,
+                               1 << 40, None) == api.INVALID_ARG
+    assert b"decode weights" in L.grpo_last_error()
+    assert L.grpo_model_pack_decode(h, None, 1 << 40, None) == api.INVALID_ARG
+    assert L.grpo_model_pack_decode(h, C.c_void_p(0x100000), want - 1, None) == api.INVALID_ARG
+    assert L.grpo_model_pack_decode(h, C.c_void_p(0x100010), want, None) == api.INVALID_ARG
+    assert L.grpo_model_pack_decode(None, p, want, None) == api.INVALID_ARG
+    L.grpo_model_destroy(h)
+    rc, h, keep = _fake_model(get("tiny").model)   # fp32: nothing to pack
+    assert L.grpo_model_pack_decode(h, None, 0, None) == api.OK
+    L.grpo_model_destroy(h)
 
 
 def test_argument_errors_before_device_work():
