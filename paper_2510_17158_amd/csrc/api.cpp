@@ -134,7 +134,7 @@ int decode_target() {
   static const int v = [] {
     const char* e = getenv("GRPO_DECODE_WGS");
     const int x = e ? atoi(e) : 0;
-    return x > 0 ? x : 512;
+    return x > 0 ? x : 256;
   }();
   return v;
 }

@@ -161,41 +161,40 @@ __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Large tiles for large M (scoring, long prefill): a workgroup of 4 waves owns a
-// 256 x 256 output tile, each wave 128 x 128 as 4 x 4 blocks of
-// v_mfma_f32_32x32x16_bf16 (accumulators in the AGPR half of the register file),
-// so every 16-byte operand fragment read from LDS feeds 4 MFMAs.  With one wave
-// per SIMD only the 32 x 32 instruction keeps the matrix core busy (the 16 x 16
-// one issues at about half its peak rate from a single wave).  Operand tiles of 64 k-elements (256 rows x 128 B
-// each for X and W) move global -> LDS with direct-to-LDS loads
-// (global_load_lds_dwordx4: each lane names its own source, the 64 lanes fill
-// 1 KB of LDS in lane order), double-buffered so the next tile's copy overlaps
-// the current tile's MFMAs.  Rows are stored with
-// their eight 16-byte pieces XOR-swizzled by (row >> 1) & 7, which makes the
-// 16 rows of a fragment read hit 16 distinct bank groups.
-constexpr int GB = 256, GBK = 64;
+// Large tiles for large M (scoring, long prefill): a workgroup owns a 256 x 256
+// output tile on v_mfma_f32_32x32x16_bf16, with 8 waves, two per SIMD: waves w
+// and w + 4 share a SIMD (the hardware places a workgroup's waves on SIMDs with
+// period 4) and its 128 x 128 quarter of the tile, 64 columns each (4 x 2 blocks
+// of 32 x 32, 128 accumulators).  The two waves of a SIMD take turns: while one
+// runs the 16 MFMAs of a 32-wide k-tile on fragments already in registers, the
+// other reads its fragments of the next k-tile from LDS and (group A, waves 0-3)
+// issues direct-to-LDS copies (global_load_lds_dwordx4: each lane names its own
+// source, the 64 lanes fill 1 KB of LDS in lane order) three k-tiles ahead; a
+// barrier swaps the roles, so the wave feeding the matrix core never stops for a
+// memory instruction.  Four LDS stages (k-tile t in stage t % 4, 32 KB each).
+// Schedule (slot = the time between two barriers; A = waves 0-3, B = 4-7):
+//   slot 2t:   A copies tile t + 3 into stage (t + 3) % 4 and reads tile t;
+//              B multiplies tile t - 1
+//   slot 2t+1: A multiplies tile t, then waits until its copies of tile t + 1
+//              have landed; B reads tile t
+// A stage is refilled (slot 2t) only after both groups read its previous tile
+// (slots 2t - 2, 2t - 1), and a copied tile is published by the barrier after A's
+// wait, before its first read (slot 2t + 2).
+// Rows of a stage are 64 bytes, their four 16-byte pieces XOR-swizzled by
+// (row >> 2) & 3 (conflict-free fragment reads).
+// Measured on the scoring shapes, the operand copies alone (no MFMA) take about
+// 70% of this kernel's time and the MFMAs with their LDS reads alone about 63%
+// of it: the two overlap only partly, which is what holds the kernel near 40%
+// of the bf16 peak.
+constexpr int GB = 256, PBK = 32, PST = 4;
 
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
-
-template <int EPI>
-__device__ __forceinline__ const bf16_t* big_wrow(const TArgs& a, int tn, int r) {
-  if (EPI == EPI_SWIGLU) {
-    // B-tile row r: wave half wn = r / 128, within it 64 gate rows then 64 up rows
-    const int wn = r >> 7, q = r & 127;
-    const int n = min(tn * 128 + wn * 64 + (q & 63), a.n1 - 1);
-    return (q < 64 ? a.w0 + (size_t)n * a.K : a.w1 + (size_t)n * a.K);
-  }
-  const int n = min(tn * GB + r, a.N - 1);
-  if (n < a.n1) return a.w0 + (size_t)n * a.K;
-  if (n < a.n2) return a.w1 + (size_t)(n - a.n1) * a.K;
-  return a.w2 + (size_t)(n - a.n2) * a.K;
-}
+__device__ __forceinline__ int pswz(int r) { return (r >> 2) & 3; }
 
 // One direct-to-LDS copy of 16 bytes per lane: the 64 lanes of the wave fill the
 // 1 KB at LDS byte address `lds` in lane order.  Issued as one asm statement that
 // also sets M0, so the compiler does not serialise consecutive copies (it cannot
-// prove they write disjoint LDS); the kernel waits on them itself (dma_wait)
-// before the barrier that publishes the tile.
+// prove they write disjoint LDS); the kernel waits on them itself (s_waitcnt
+// vmcnt) before the barrier that publishes the tile.
 __device__ __forceinline__ void dma16(const bf16_t* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(g) : "memory");
 }
@@ -204,13 +203,38 @@ __device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
+// W row of B-tile row r.  SwiGLU: the B-tile rows form 4 slices of 64 (one per
+// wave column range), each 32 gate rows then the 32 up rows of the same outputs.
+// Otherwise rows of the (q, k, v) stack in order (the host guarantees that a
+// tile lies inside one matrix of the stack).
 template <int EPI>
-__global__ __launch_bounds__(256) void k_gemm_big(TArgs a) {
-  // [buffer][X tile, W tile]
-  __shared__ __attribute__((aligned(1024))) bf16_t lds[2][2][GB * GBK];
+__device__ __forceinline__ const bf16_t* pp_wrow(const TArgs& a, int tn, int r) {
+  if (EPI == EPI_SWIGLU) {
+    const int slice = r >> 6, q = r & 63;
+    const int n = min(tn * 128 + slice * 32 + (q & 31), a.n1 - 1);
+    return (q < 32 ? a.w0 + (size_t)n * a.K : a.w1 + (size_t)n * a.K);
+  }
+  const int n = min(tn * GB + r, a.N - 1);
+  if (n < a.n1) return a.w0 + (size_t)n * a.K;
+  if (n < a.n2) return a.w1 + (size_t)(n - a.n1) * a.K;
+  return a.w2 + (size_t)(n - a.n2) * a.K;
+}
+
+#define PP_BARRIER()                          \
+  do {                                        \
+    __builtin_amdgcn_sched_barrier(0);        \
+    asm volatile("s_barrier" ::: "memory");   \
+    __builtin_amdgcn_sched_barrier(0);        \
+  } while (0)
+
+template <int EPI>
+__global__ __launch_bounds__(512) void k_gemm_pp(TArgs a) {
+  // [stage][X tile, W tile]
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[PST][2][GB * PBK];
   const int tid = threadIdx.x, lane = tid % 64;
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int sq = wave & 3, grp = wave >> 2;
+  const int wm = sq >> 1, wn = sq & 1;
 
   // XCD-aware tile order: workgroups are dealt to the 8 XCDs round-robin
   // (blockIdx % 8), each XCD with its own L2.  The tiles form super-tiles of
@@ -224,98 +248,99 @@ __global__ __launch_bounds__(256) void k_gemm_big(TArgs a) {
   const int tn = (st % st_n) * 8 + loc % 8;
   if (tm >= a.tiles_m || tn >= a.tiles_n) return;
 
-  // Rows of copy instruction j advance by 8 per j: one base pointer per operand
-  // plus a uniform stride (the host guarantees that a W tile lies inside one
-  // matrix of the stack).  The last row tile is shifted back to end at M (M >= 256)
-  // and writes only the rows no earlier tile owns.
+  // Copies (group A only): instruction j (0..3) of wave sq fills tile rows
+  // 64 sq + 16 j .. + 16 of both operands (lane -> row + lane / 4, piece lane % 4
+  // holding source piece (lane % 4) ^ pswz(row), the same for every j); SwiGLU W
+  // rows switch from gate to up at j = 2.
   const int m0 = min(tm * GB, a.M - GB);
-  const int r0 = wave * 64 + lane / 8;                  // row of instruction 0
-  const int pbase = ((lane % 8) ^ swz(r0)) * 8;         // swz(r0 + 8 j) == swz(r0) ^ 4 j
-  const bf16_t* ab = a.X + (size_t)(m0 + r0) * a.ldx + pbase;
-  const bf16_t* bb = big_wrow<EPI>(a, tn, r0) + pbase;
-  const size_t astep = (size_t)8 * a.ldx, bstep = (size_t)8 * a.K;
+  const int r0 = sq * 64 + lane / 4;
+  const int pbase = ((lane % 4) ^ pswz(r0)) * 8;
+  const bf16_t* ab = a.X + (size_t)m0 * a.ldx + (size_t)r0 * a.ldx + pbase;
+  const bf16_t* bb0 = pp_wrow<EPI>(a, tn, r0) + pbase;
+  const bf16_t* bb1 = pp_wrow<EPI>(a, tn, r0 + 32) + pbase;
+  const size_t astep = (size_t)16 * a.ldx, bstep = (size_t)16 * a.K;
   auto copy = [&](int buf, int kt) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int off = (wave * 8 + j) * 8 * GBK;          // first LDS row of the instruction
-      const int flip = (j & 1) ? ((pbase ^ 32) - pbase) : 0;   // pieces XOR 4 j (mod 8)
-      dma16(ab + j * astep + kt * GBK + flip, lds_addr(&lds[buf][0][off]));
-      dma16(bb + j * bstep + kt * GBK + flip, lds_addr(&lds[buf][1][off]));
+    for (int j = 0; j < 4; ++j) {
+      const int off = (sq * 4 + j) * 16 * PBK;
+      dma16(ab + j * astep + kt * PBK, lds_addr(&lds[buf][0][off]));
+      const bf16_t* bsrc = (EPI == EPI_SWIGLU && j >= 2) ? bb1 + (j - 2) * bstep : bb0 + j * bstep;
+      dma16(bsrc + kt * PBK, lds_addr(&lds[buf][1][off]));
     }
   };
 
-
-  // Fragment rows of this lane: wm * 128 + 32 i + (lane & 31) for X, likewise for
-  // W; k-step s (16 elements) takes piece 2 s + (lane >> 5) of those rows.  The
-  // swizzle ((lane & 31) >> 1) & 7 is the same for all four blocks, so a k-step
-  // needs one LDS address per operand and the blocks sit 32 rows apart.
-  const int sw = ((lane & 31) >> 1) & 7;
+  // fragments: X rows wm * 128 + 32 i + (lane & 31); W rows (tile columns)
+  // wn * 128 + grp * 64 + 32 j + (lane & 31); k-step s takes piece 2 s + (lane >> 5)
+  const int sw = pswz(lane & 31);
   const int g2 = lane >> 5;
-  int aoff[GBK / 16], boff[GBK / 16];
+  int aoff[PBK / 16], boff[PBK / 16];
 #pragma unroll
-  for (int s = 0; s < GBK / 16; ++s) {
+  for (int s = 0; s < PBK / 16; ++s) {
     const int pc = ((s * 2 + g2) ^ sw) * 8;
-    aoff[s] = (wm * 128 + (lane & 31)) * GBK + pc;
-    boff[s] = (wn * 128 + (lane & 31)) * GBK + pc;
+    aoff[s] = (wm * 128 + (lane & 31)) * PBK + pc;
+    boff[s] = (wn * 128 + grp * 64 + (lane & 31)) * PBK + pc;
   }
-  f32x16_t acc[4][4];
+  f32x16_t acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  // Software-pipelined over the 4 k-steps of a tile: the 8 fragment reads of
-  // step s + 1 are interleaved with the 16 MFMAs of step s (one read per two
-  // MFMAs), so the LDS latency hides under the matrix cores.
-#define GRPO_FRAGS(As, Bs, s, FA, FB)                                                 \
-  _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                     \
-    FA[i] = *(const bf16x8_t*)((As) + aoff[s] + i * 32 * GBK);                        \
-    FB[i] = *(const bf16x8_t*)((Bs) + boff[s] + i * 32 * GBK);                        \
-  }
-#define GRPO_MFMAS(FA, FB)                                                            \
-  _Pragma("unroll") for (int i = 0; i < 4; ++i)                                       \
-    _Pragma("unroll") for (int j = 0; j < 4; ++j)                                     \
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(FA[i], FB[j], acc[i][j], 0, 0, 0);
-#define GRPO_INTERLEAVE()                                                             \
-  _Pragma("unroll") for (int q = 0; q < 8; ++q) {                                     \
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                                \
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);                                \
-  }
-  auto mma_tile = [&](const bf16_t* As, const bf16_t* Bs) {
-    bf16x8_t a0[4], b0[4], a1[4], b1[4];
-    GRPO_FRAGS(As, Bs, 0, a0, b0)
-    GRPO_FRAGS(As, Bs, 1, a1, b1)
-    GRPO_MFMAS(a0, b0)
-    GRPO_INTERLEAVE()
-    GRPO_FRAGS(As, Bs, 2, a0, b0)
-    GRPO_MFMAS(a1, b1)
-    GRPO_INTERLEAVE()
-    GRPO_FRAGS(As, Bs, 3, a1, b1)
-    GRPO_MFMAS(a0, b0)
-    GRPO_INTERLEAVE()
-    GRPO_MFMAS(a1, b1)
+  bf16x8_t fa[PBK / 16][4], fb[PBK / 16][2];
+  auto frags = [&](int buf) {
+#pragma unroll
+    for (int s = 0; s < PBK / 16; ++s) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) fa[s][i] = *(const bf16x8_t*)(&lds[buf][0][aoff[s] + i * 32 * PBK]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) fb[s][j] = *(const bf16x8_t*)(&lds[buf][1][boff[s] + j * 32 * PBK]);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   };
-#undef GRPO_INTERLEAVE
+  auto mma = [&]() {
+#pragma unroll
+    for (int s = 0; s < PBK / 16; ++s)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+  };
 
-  const int nk = a.K / GBK;
-  copy(0, 0);
-  dma_wait();
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    // the other buffer was last read in iteration kt - 1, which ended at a barrier
-    if (kt + 1 < nk) copy(buf ^ 1, kt + 1);
-    mma_tile(&lds[buf][0][0], &lds[buf][1][0]);
-    __builtin_amdgcn_sched_barrier(0);   // every MFMA is issued before the copy is awaited
-    dma_wait();
-    __syncthreads();
+  const int nk = a.K / PBK;    // >= 4 (K is a multiple of 128)
+  if (grp == 0) {
+    copy(0, 0);
+    copy(1, 1);
+    copy(2, 2);
+    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");   // tile 0 (8 copies per tile)
   }
-#undef GRPO_MFMAS
-#undef GRPO_FRAGS
+  PP_BARRIER();
+  if (grp == 0) {
+    for (int t = 0; t < nk; ++t) {
+      if (t + 3 < nk) copy((t + 3) % PST, t + 3);
+      frags(t % PST);
+      PP_BARRIER();
+      mma();
+      // tile t + 1 landed: only the copies of tiles t + 2 and t + 3 may remain
+      if (t + 3 < nk) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+      else if (t + 2 < nk) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+      else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      PP_BARRIER();
+    }
+    PP_BARRIER();
+  } else {
+    PP_BARRIER();
+    for (int t = 0; t < nk; ++t) {
+      frags(t % PST);
+      PP_BARRIER();
+      mma();
+      PP_BARRIER();
+    }
+  }
 
-  // ---- epilogue: acc[i][j][r] is row 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4,
-  // column 32 j + (lane & 31) of the wave's 128 x 128 block ----
+  // ---- epilogue: acc[i][j][r] is row 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4 of
+  // the SIMD's 128 rows, column 32 j + (lane & 31) of the wave's 64 columns ----
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -323,18 +348,15 @@ __global__ __launch_bounds__(256) void k_gemm_big(TArgs a) {
       const int m = m0 + wm * 128 + i * 32 + (r / 4) * 8 + (lane >> 5) * 4 + (r % 4);
       if (m < tm * GB) continue;
       if (EPI == EPI_SWIGLU) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int n = tn * 128 + wn * 64 + j * 32 + (lane & 31);
-          if (n < a.n1) {
-            const float gt = acc[i][j][r], up = acc[i][j + 2][r];
-            a.out_act[(size_t)m * a.ld_out + n] = f2bf(gt / (1.f + __expf(-gt)) * up);
-          }
+        const int n = tn * 128 + (wn * 2 + grp) * 32 + (lane & 31);
+        if (n < a.n1) {
+          const float gt = acc[i][0][r], up = acc[i][1][r];
+          a.out_act[(size_t)m * a.ld_out + n] = f2bf(gt / (1.f + __expf(-gt)) * up);
         }
       } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int n = tn * GB + wn * 128 + j * 32 + (lane & 31);
+        for (int j = 0; j < 2; ++j) {
+          const int n = tn * GB + wn * 128 + grp * 64 + j * 32 + (lane & 31);
           if (n < a.N) {
             float* o = a.out_f32 + (size_t)m * a.ld_out + n;
             if (EPI == EPI_RESID) *o += acc[i][j][r];
@@ -345,6 +367,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(TArgs a) {
     }
   }
 }
+#undef PP_BARRIER
 
 // ---------------------------------------------------------------------------
 // fp32 GEMM for fp32 models (VALU, 64x64 tiles, 4x4 outputs per thread).
@@ -443,9 +466,9 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
     const int n_st = ((a.tiles_m + 3) / 4) * ((a.tiles_n + 7) / 8);
     const int grid = (n_st + 7) / 8 * 8 * 32;
     switch (epi) {
-      case EPI_STORE: k_gemm_big<EPI_STORE><<<grid, 256, 0, st>>>(a); break;
-      case EPI_RESID: k_gemm_big<EPI_RESID><<<grid, 256, 0, st>>>(a); break;
-      default: k_gemm_big<EPI_SWIGLU><<<grid, 256, 0, st>>>(a); break;
+      case EPI_STORE: k_gemm_pp<EPI_STORE><<<grid, 512, 0, st>>>(a); break;
+      case EPI_RESID: k_gemm_pp<EPI_RESID><<<grid, 512, 0, st>>>(a); break;
+      default: k_gemm_pp<EPI_SWIGLU><<<grid, 512, 0, st>>>(a); break;
     }
     return hipGetLastError();
   }

@@ -194,9 +194,11 @@ def test_small_stage_local(small):
                    top_k=50)),
     ("7b", 1, dict(n_prompts=1, group=8, prompt_len=120, new_tokens=5)),
     ("32b", 1, dict(n_prompts=1, group=8, prompt_len=96, new_tokens=5)),
-    # >= 1024 prompt rows: the 256 x 256 GEMM tiles, last row tile shifted back
-    ("small", 2, dict(n_prompts=4, group=2, prompt_len=300, new_tokens=2)),
-    ("7b", 1, dict(n_prompts=2, group=2, prompt_len=520, new_tokens=2)),
+    # >= 1024 prompt rows: the 256 x 256 GEMM tiles, last row tile shifted back.
+    # 8 sequences x 2 decode steps: the decode floor check pools per-row rounding
+    # flip cascades, which a 4-row pool is too small to compare with the floor's
+    ("small", 2, dict(n_prompts=4, group=2, prompt_len=300, new_tokens=3)),
+    ("7b", 1, dict(n_prompts=2, group=4, prompt_len=520, new_tokens=3)),
 ])
 def test_full_width_stage_local(name, layers, kw):
     """Layer-truncated models at the 1B/7B/32B widths: every stage fed GPU inputs."""
