@@ -302,11 +302,14 @@ DecodeLayout decode_layout(const grpo_config& c) {
 // ---- workspace layouts ----
 struct StepWS {   // activations of `rows` token rows
   float* x; void* h; float* qkv; void* q; void* o; void* a;
+  float2* cs;      // rotary cos / sin table
   GemmScratch g;
 };
 
-// act_rows: rows of the GEMM inputs h, o and a (the padded batch of a decode step)
-StepWS take_step(Bump& b, const grpo_config& c, int rows, int act_rows, size_t part_floats) {
+// act_rows: rows of the GEMM inputs h, o and a (the padded batch of a decode step);
+// cs_rows: rows of the rotary table (decode: one per sequence; else one per position)
+StepWS take_step(Bump& b, const grpo_config& c, int rows, int act_rows, size_t part_floats,
+                 int cs_rows) {
   StepWS w;
   const int es = esize(c);
   w.x = b.take<float>((size_t)rows * c.d_model);
@@ -315,6 +318,7 @@ StepWS take_step(Bump& b, const grpo_config& c, int rows, int act_rows, size_t p
   w.q = b.take<char>((size_t)rows * qdim(c) * es);
   w.o = b.take<char>((size_t)act_rows * qdim(c) * es);
   w.a = b.take<char>((size_t)act_rows * c.d_ffn * es);
+  w.cs = b.take<float2>((size_t)cs_rows * (c.head_dim / 2));
   w.g.part = b.take<float>(part_floats);
   return w;
 }
@@ -327,7 +331,7 @@ struct RolloutWS {
 };
 RolloutWS take_rollout(Bump& b, const grpo_config& c, int B, int max_len) {
   RolloutWS w;
-  w.s = take_step(b, c, B, c.dtype == GRPO_F32 ? B : decode_nb(B), decode_scratch(c, B));
+  w.s = take_step(b, c, B, c.dtype == GRPO_F32 ? B : decode_nb(B), decode_scratch(c, B), B);
   w.logits = b.take<float>((size_t)B * c.vocab);
   const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.n_kv_heads, c.head_dim, max_len);
   w.attn_part = b.take<float>(c.dtype == GRPO_F32 ? 0 : ap.part_floats);
@@ -345,7 +349,7 @@ int round8(int t) { return (t + 7) / 8 * 8; }
 PrefillWS take_prefill(Bump& b, const grpo_config& c, int P, int Tp) {
   PrefillWS w;
   const size_t M = (size_t)P * Tp;
-  w.s = take_step(b, c, (int)M, (int)M, 0);
+  w.s = take_step(b, c, (int)M, (int)M, 0, Tp);
   w.vt = b.take<uint16_t>(c.dtype == GRPO_F32 ? 0 : (size_t)P * kvdim(c) * round8(Tp));
   w.hl = b.take<char>((size_t)P * c.d_model * esize(c));
   w.logits = b.take<float>((size_t)P * c.vocab);
@@ -365,7 +369,7 @@ ScoreWS take_score(Bump& b, const grpo_config& c, int N, int T) {
   w.chunk = std::max(1, std::min(N, kScoreTokens / std::max(T, 1)));
   const size_t M = (size_t)w.chunk * T;
   w.sub_rows = (int)std::max<size_t>(64, std::min<size_t>(8192, kLogitBytes / ((size_t)c.vocab * 4)));
-  w.s = take_step(b, c, (int)M, (int)M, 0);
+  w.s = take_step(b, c, (int)M, (int)M, 0, T);
   const size_t kvn = (size_t)w.chunk * kvdim(c) * T;
   w.kbuf = b.take<char>(kvn * esize(c));
   w.vbuf = b.take<char>(c.dtype == GRPO_F32 ? kvn * 4 : 0);
@@ -400,6 +404,7 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
   const int N = M / T;
   const Partials none{nullptr, 0, 0, d};
   int rc;
+  HIPCHK(rope_table(nullptr, T, c.head_dim, c.rope_theta, w.cs, st));
   for (int l = 0; l < c.n_layers; ++l) {
     void *kl = kbuf, *vl = vbuf;
     if (kv_or_null) {
@@ -420,6 +425,7 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
     ra.kcache = kl; ra.vcache = vl; ra.n_seqs = n_slots; ra.max_len = k_len;
     ra.vt = c.dtype == GRPO_F32 ? nullptr : vt; ra.vt_len = round8(T);
     ra.splits = 1; ra.split_stride = 0;
+    ra.cs = w.cs;
     HIPCHK(rope_kv(c.dtype, w.qkv, M, w.q, ra, st));
     HIPCHK(attn_prefill(c.dtype, w.q, kl, c.dtype == GRPO_F32 ? vl : (const void*)vt, N, T,
                         c.n_heads, c.n_kv_heads, c.head_dim, k_len, G, w.o, st));
@@ -672,6 +678,7 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
     int rc;
     hipStream_t st = ss;
     HIPCHK(embed(c.dtype, m->tok_emb, tok, B, d, c.vocab, w.s.x, st, graph ? w.step_ctr : nullptr));
+    HIPCHK(rope_table(pos, B, c.head_dim, c.rope_theta, w.s.cs, st));
     // bf16: GEMM inputs in fragment order, products as split-K partials;
     // fp32: row-major, products straight into their destinations
     Partials pend{nullptr, 0, 0, d};
@@ -698,6 +705,7 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
       ra.kcache = L.k; ra.vcache = L.v; ra.n_seqs = n_seqs; ra.max_len = max_len;
       ra.vt = nullptr; ra.vt_len = 0;
       ra.splits = qs; ra.split_stride = qstride;
+      ra.cs = w.s.cs;
       HIPCHK(rope_kv(c.dtype, qsrc, B, w.s.q, ra, st));
       HIPCHK(attn_decode(c.dtype, w.s.q, L.k, L.v, pos, B, c.n_heads, c.n_kv_heads, c.head_dim,
                          n_seqs, max_len, ap, w.attn_part, w.s.o, st, nb));

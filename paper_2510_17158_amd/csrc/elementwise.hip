@@ -68,18 +68,28 @@ __global__ __launch_bounds__(NORM_NT) void k_rmsnorm(float* x, int ldx, RowMap r
     v[k] = i4 < n4 ? *(const float4*)(xr + 4 * i4) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   if (pp.splits > 0) {
+    // four splits' loads in flight at a time (a split past the last re-reads the
+    // last one and is not added), then added in split order
     const float* pr = pp.part + src * pp.ld;
-    for (int sp = 0; sp < pp.splits; ++sp) {
-      float4 t[NORM_VPT];
+    for (int sp0 = 0; sp0 < pp.splits; sp0 += 4) {
+      float4 t[4][NORM_VPT];
 #pragma unroll
-      for (int k = 0; k < NORM_VPT; ++k) {
-        const int i4 = threadIdx.x + k * NORM_NT;
-        t[k] = i4 < n4 ? *(const float4*)(pr + sp * pp.split_stride + 4 * i4)
-                       : make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int u = 0; u < 4; ++u) {
+        const size_t so = (size_t)min(sp0 + u, pp.splits - 1) * pp.split_stride;
+#pragma unroll
+        for (int k = 0; k < NORM_VPT; ++k) {
+          const int i4 = threadIdx.x + k * NORM_NT;
+          t[u][k] = i4 < n4 ? *(const float4*)(pr + so + 4 * i4) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
       }
 #pragma unroll
-      for (int k = 0; k < NORM_VPT; ++k) {
-        v[k].x += t[k].x; v[k].y += t[k].y; v[k].z += t[k].z; v[k].w += t[k].w;
+      for (int u = 0; u < 4; ++u) {
+        if (sp0 + u < pp.splits) {
+#pragma unroll
+          for (int k = 0; k < NORM_VPT; ++k) {
+            v[k].x += t[u][k].x; v[k].y += t[u][k].y; v[k].z += t[u][k].z; v[k].w += t[u][k].w;
+          }
+        }
       }
     }
 #pragma unroll
@@ -133,15 +143,8 @@ __global__ void k_rope_kv(const float* qkv, int M, T* q_out, RopeArgs a) {
     hi += src[sp * a.split_stride + i + half];
   }
   if (h < a.n_heads + a.n_kv) {
-    // angle pos * theta^(-2i/hd) in fp64, reduced to [-pi, pi] in fp64 (keeps
-    // sincos on its short path), cos/sin rounded to fp32
-    const double inv = pow((double)a.theta, -2.0 * (double)i / (double)a.hd);
-    const double two_pi = 6.283185307179586476925286766559;
-    double ang = (double)pos * inv;
-    ang -= rint(ang / two_pi) * two_pi;
-    double sd, cd;
-    sincos(ang, &sd, &cd);
-    const float c = (float)cd, s = (float)sd;
+    const float2 cs = a.cs[(size_t)(a.mode == 0 ? m : pos) * half + i];
+    const float c = cs.x, s = cs.y;
     const float l2 = lo * c - hi * s;
     const float h2 = hi * c + lo * s;
     lo = l2; hi = h2;
@@ -163,10 +166,51 @@ __global__ void k_rope_kv(const float* qkv, int M, T* q_out, RopeArgs a) {
     stf(dst, i, lo);
     stf(dst, i + half, hi);
   }
-  if (is_v && a.vt && pos < a.vt_len) {
-    bf16_t* vt = a.vt + ((size_t)seq * a.n_kv + g) * a.hd * a.vt_len;
-    vt[(size_t)i * a.vt_len + pos] = f2bf(lo);
-    vt[(size_t)(i + half) * a.vt_len + pos] = f2bf(hi);
+}
+
+// cos / sin of the rotary angles: row r of the table is position pos_arr[r]
+// (pos_arr != NULL) or position r.  Angle pos * theta^(-2i/hd) in fp64, reduced
+// to [-pi, pi] in fp64 (keeps sincos on its short path), cos/sin rounded to fp32.
+__global__ void k_rope_table(const int32_t* pos_arr, int rows, int half, float theta,
+                             float2* cs) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= rows * half) return;
+  const int r = idx / half, i = idx % half;
+  const int pos = pos_arr ? pos_arr[r] : r;
+  const double inv = pow((double)theta, -2.0 * (double)i / (double)(2 * half));
+  const double two_pi = 6.283185307179586476925286766559;
+  double ang = (double)pos * inv;
+  ang -= rint(ang / two_pi) * two_pi;
+  double sd, cd;
+  sincos(ang, &sd, &cd);
+  cs[idx] = make_float2((float)cd, (float)sd);
+}
+
+// V^T for the prefill/scoring attention: vt[seq][g][d][pos] = bf16 of the V part
+// of qkv (sum of its splits) for row seq * T + pos.  A workgroup moves a 64-position
+// x hd tile through LDS, reading rows along d and writing along positions.
+__global__ __launch_bounds__(256) void k_v_transpose(const float* qkv, int T, RopeArgs a,
+                                                     bf16_t* vt) {
+  __shared__ float tile[64][129];
+  const int p0 = blockIdx.x * 64, g = blockIdx.y, seq = blockIdx.z;
+  const int hd = a.hd;
+  const int ldq = (a.n_heads + 2 * a.n_kv) * hd;
+  const float* src = qkv + (size_t)seq * T * ldq + (size_t)(a.n_heads + a.n_kv + g) * hd;
+  for (int e = threadIdx.x; e < 64 * hd; e += 256) {
+    const int p = e / hd, d = e % hd;
+    float v = 0.f;
+    if (p0 + p < T) {
+      const float* r = src + (size_t)(p0 + p) * ldq + d;
+      v = r[0];
+      for (int sp = 1; sp < a.splits; ++sp) v += r[sp * a.split_stride];
+    }
+    tile[p][d] = v;
+  }
+  __syncthreads();
+  bf16_t* dst = vt + ((size_t)seq * a.n_kv + g) * hd * a.vt_len;
+  for (int e = threadIdx.x; e < 64 * hd; e += 256) {
+    const int d = e / 64, p = e % 64;
+    if (p0 + p < a.vt_len) dst[(size_t)d * a.vt_len + p0 + p] = p0 + p < T ? f2bf(tile[p][d]) : 0;
   }
 }
 
@@ -230,14 +274,31 @@ hipError_t fill_i32(int32_t* p, size_t n, int32_t v, hipStream_t st) {
   return hipGetLastError();
 }
 
+hipError_t rope_table(const int32_t* pos_arr, int rows, int hd, float theta, float2* cs,
+                      hipStream_t st) {
+  const int n = rows * (hd / 2);
+  if (n <= 0) return hipSuccess;
+  Prof pf("rope_table", st);
+  k_rope_table<<<(n + 255) / 256, 256, 0, st>>>(pos_arr, rows, hd / 2, theta, cs);
+  return hipGetLastError();
+}
+
 hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeArgs& a,
                    hipStream_t st) {
   const size_t total = (size_t)M * (a.n_heads + 2 * a.n_kv) * (a.hd / 2);
   if (total == 0) return hipSuccess;
+  if (!a.cs || a.hd > 128) return hipErrorInvalidValue;
   const int grid = (int)((total + 255) / 256);
-  Prof pf(a.mode == 0 ? "rope_kv" : "rope_kv_rows", st);
-  if (dtype == 0) k_rope_kv<float><<<grid, 256, 0, st>>>(qkv, M, (float*)q_out, a);
-  else k_rope_kv<bf16_t><<<grid, 256, 0, st>>>(qkv, M, (bf16_t*)q_out, a);
+  {
+    Prof pf(a.mode == 0 ? "rope_kv" : "rope_kv_rows", st);
+    if (dtype == 0) k_rope_kv<float><<<grid, 256, 0, st>>>(qkv, M, (float*)q_out, a);
+    else k_rope_kv<bf16_t><<<grid, 256, 0, st>>>(qkv, M, (bf16_t*)q_out, a);
+  }
+  if (a.vt && a.mode == 1 && a.T > 0) {
+    Prof pf("v_transpose", st);
+    dim3 grid_t((a.T + 63) / 64, a.n_kv, M / a.T);
+    k_v_transpose<<<grid_t, 256, 0, st>>>(qkv, a.T, a, a.vt);
+  }
   return hipGetLastError();
 }
 

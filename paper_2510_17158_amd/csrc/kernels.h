@@ -95,12 +95,18 @@ struct Partials {
 hipError_t rmsnorm(int dtype, float* x, int ldx, RowMap rows, Partials p, const void* g, int M,
                    int d, float eps, void* out, int ldo, hipStream_t st, int pack_nb = 0);
 hipError_t fill_i32(int32_t* p, size_t n, int32_t v, hipStream_t st);
+// cos / sin table of the rotary angles, [rows][hd / 2] float2: row r is position
+// pos_arr[r] (device array) or, with pos_arr NULL, position r.
+hipError_t rope_table(const int32_t* pos_arr, int rows, int hd, float theta, float2* cs,
+                      hipStream_t st);
 // Rotary embedding + cache write.  qkv fp32 [M, q_dim + 2 kv_dim], or the sum
 // of `splits` such arrays split_stride floats apart (decode GEMM partials).  Row m is
 // (seq, pos): mode 0: seq = m, pos = pos_arr[m];  mode 1: seq = m / T, pos = m % T.
+// cs: rope_table rows of pos_arr (mode 0) or of positions 0..T-1 (mode 1).
 // q_out: [M, q_dim] act.  K/V written to cache slots seq*G + g (g < G) at pos
-// (positions >= max_len skipped).  vt (optional) gets V transposed:
-// [seq][n_kv][hd][vt_len] for the prefill/scoring attention.
+// (positions >= max_len skipped).  vt (optional, mode 1, M a multiple of T) gets
+// V transposed: [seq][n_kv][hd][vt_len] for the prefill/scoring attention,
+// positions T..vt_len-1 zero.
 struct RopeArgs {
   int mode, T, G;
   const int32_t* pos_arr;
@@ -110,6 +116,7 @@ struct RopeArgs {
   int n_seqs, max_len;
   uint16_t* vt; int vt_len;
   int splits; size_t split_stride;
+  const float2* cs;
 };
 hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeArgs& a,
                    hipStream_t st);
