@@ -364,6 +364,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
     for (int qb = 0; qb < 2; ++qb) oacc[hb][qb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
   float mq[2] = {-1e30f, -1e30f}, lq_sum[2] = {0.f, 0.f};
 
+  const float scale2 = scale * 1.4426950408889634f;   // log2(e)
   const int qlast = min(q0 + 31, T - 1);
   const int n_tiles = qlast / 64 + 1;
   load_tile(0);
@@ -394,10 +395,14 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
                 __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][st], sacc[s2][b][qb], 0, 0, 0);
         }
       }
-    // online softmax per query column: tile maximum and rescale first, then per
-    // 32-key step the P^T operands (hi, lo) and their products with V^T
+    // online softmax per query column in base 2 (scores scaled by scale * log2 e,
+    // P = 2^(s - m)): tile maximum and rescale first, then per 32-key step the P^T
+    // operands (hi, lo: hardware round-to-nearest-even conversions) and their
+    // products with V^T.  A masked score is -inf and gives P = 0; the running
+    // maximum starts finite, so s - m is never inf - inf.
     const bool full = k0 + 63 <= q0 && k0 + 63 < T;   // no key of the tile is masked
     float mnew[2], psum[2] = {0.f, 0.f};
+    bool moved = false;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       const int qrow = q0 + qb * 16 + lq;
@@ -409,7 +414,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const int key = k0 + 32 * s2 + 8 * lg + 4 * b + v;
-            float sc = sacc[s2][b][qb][v] * scale;
+            float sc = sacc[s2][b][qb][v] * scale2;
             if (!full) sc = (key <= qrow && key < T) ? sc : -INFINITY;
             sacc[s2][b][qb][v] = sc;
             mx = fmaxf(mx, sc);
@@ -417,14 +422,22 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       mnew[qb] = fmaxf(mq[qb], mx);
-      const float alpha = __expf(mq[qb] - mnew[qb]);
-      mq[qb] = mnew[qb];
-      lq_sum[qb] *= alpha;
-#pragma unroll
-      for (int hb = 0; hb < HB; ++hb)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) oacc[hb][qb][v] *= alpha;
+      moved |= mnew[qb] != mq[qb];
     }
+    // rescale only when some column's maximum moved (a factor of exactly 1 otherwise)
+    if (__builtin_amdgcn_ballot_w64(moved)) {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        const float alpha = __builtin_amdgcn_exp2f(mq[qb] - mnew[qb]);
+        lq_sum[qb] *= alpha;
+#pragma unroll
+        for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) oacc[hb][qb][v] *= alpha;
+      }
+    }
+    mq[0] = mnew[0];
+    mq[1] = mnew[1];
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       bf16x8_t ph[2], pl[2];
@@ -433,14 +446,18 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const float sv = sacc[s2][b][qb][v];
-            const float p = (sv == -INFINITY) ? 0.f : __expf(sv - mnew[qb]);
-            psum[qb] += p;
-            const bf16_t pbh = f2bf(p);
-            const bf16_t pbl = f2bf(p - bf2f(pbh));
-            ph[qb][4 * b + v] = __builtin_bit_cast(__bf16, pbh);
-            pl[qb][4 * b + v] = __builtin_bit_cast(__bf16, pbl);
+          for (int v = 0; v < 4; v += 2) {
+            const float p0 = __builtin_amdgcn_exp2f(sacc[s2][b][qb][v] - mnew[qb]);
+            const float p1 = __builtin_amdgcn_exp2f(sacc[s2][b][qb][v + 1] - mnew[qb]);
+            psum[qb] += p0;
+            psum[qb] += p1;
+            const bf16x2_t h = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
+            const bf16x2_t l = __builtin_convertvector(
+                (f32x2_t){p0 - (float)h[0], p1 - (float)h[1]}, bf16x2_t);
+            ph[qb][4 * b + v] = h[0];
+            ph[qb][4 * b + v + 1] = h[1];
+            pl[qb][4 * b + v] = l[0];
+            pl[qb][4 * b + v + 1] = l[1];
           }
       }
       // O^T += V^T P^T: A = V^T rows (dims 16 hb + lq), keys 32 s2 + 8 lg .. + 8
