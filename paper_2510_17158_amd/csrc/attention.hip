@@ -271,19 +271,29 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const float* __restrict__ p
 // 8 g .. 8 g + 7: exactly the B operand of O^T += V^T P^T, which therefore never
 // leaves registers.  P enters that product as two bf16 terms (hi + lo), so no
 // rounding point is added.  K and V^T tiles of 64 keys are double-buffered in
-// LDS and prefetched into registers one tile ahead; one barrier per tile.  The
+// LDS (K rows swizzled, V^T rows padded: conflict-free fragment reads) and
+// prefetched into registers one tile ahead; one barrier per tile.  The
 // latest query blocks (the most key tiles under the causal mask) start first.
+// K tile rows in LDS are unpadded, their 16-byte pieces XOR-swizzled so that the
+// 16 key rows one fragment read touches (8 (i >> 2) + (i & 3) plus a multiple of 4)
+// fall in 16 distinct bank groups (HD 128: 256-byte rows, the swizzle takes row
+// bits 0-1 and 3-4; HD 64: 128-byte rows, bits 1 and 3-4).
+template <int HD>
+__device__ __forceinline__ int kswz(int r) {
+  return HD == 128 ? ((r & 3) | (((r >> 3) & 3) << 2)) : (((r >> 1) & 1) | (((r >> 3) & 3) << 1));
+}
+
 template <int HD, int GQ>
 __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) void k_flash_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ vt,
     int T, int H, int n_kv, int k_len, int k_seq_stride, int vt_len, float scale,
     bf16_t* __restrict__ out) {
   constexpr int NT = 64 * GQ;
-  constexpr int KROW = HD + 8, VROW = 64 + 8;
+  constexpr int VROW = 64 + 8;
   constexpr int QSTEPS = HD / 32, HB = HD / 16;
   constexpr int KP = 64 * HD / 8, VP = HD * 8;          // 16-byte pieces of a K / V^T tile
   constexpr int KPT = (KP + NT - 1) / NT, VPT = (VP + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) bf16_t ks[2][64 * KROW];
+  __shared__ __attribute__((aligned(16))) bf16_t ks[2][64 * HD];
   __shared__ __attribute__((aligned(16))) bf16_t vs[2][HD * VROW];
 
   const int qblk = gridDim.x - 1 - blockIdx.x;
@@ -344,7 +354,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
       const int pi = tid + i * NT;
       if (pi < KP) {
         const int r = pi / (HD / 8), c = (pi % (HD / 8)) * 8;
-        *(u32x4_t*)(&ks[buf][r * KROW + c]) = kr[i];
+        *(u32x4_t*)(&ks[buf][r * HD + ((c / 8) ^ kswz<HD>(r)) * 8]) = kr[i];
       }
     }
 #pragma unroll
@@ -388,7 +398,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
         for (int qb = 0; qb < 2; ++qb) sacc[s2][b][qb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int st = 0; st < QSTEPS; ++st) {
-          const bf16x8_t kf = *(const bf16x8_t*)(ksb + kr_ * KROW + (st * 4 + lg) * 8);
+          const bf16x8_t kf = *(const bf16x8_t*)(ksb + kr_ * HD + ((st * 4 + lg) ^ kswz<HD>(kr_)) * 8);
 #pragma unroll
           for (int qb = 0; qb < 2; ++qb)
             sacc[s2][b][qb] =
