@@ -271,34 +271,36 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const float* __restrict__ p
 // 8 g .. 8 g + 7: exactly the B operand of O^T += V^T P^T, which therefore never
 // leaves registers.  P enters that product as two bf16 terms (hi + lo), so no
 // rounding point is added.  K and V^T tiles of 64 keys are double-buffered in
-// LDS (K rows swizzled, V^T rows padded: conflict-free fragment reads) and
-// prefetched into registers one tile ahead; one barrier per tile.  The
-// latest query blocks (the most key tiles under the causal mask) start first.
-// K tile rows in LDS are unpadded, their 16-byte pieces XOR-swizzled so that the
-// 16 key rows one fragment read touches (8 (i >> 2) + (i & 3) plus a multiple of 4)
+// LDS and filled by direct-to-LDS copies one tile ahead (no staging registers);
+// one barrier per tile.  The latest query blocks (the most key tiles under the
+// causal mask) start first.
+// Tile rows in LDS are unpadded, their 16-byte pieces XOR-swizzled.  K: the 16
+// key rows one fragment read touches (8 (i >> 2) + (i & 3) plus a multiple of 4)
 // fall in 16 distinct bank groups (HD 128: 256-byte rows, the swizzle takes row
 // bits 0-1 and 3-4; HD 64: 128-byte rows, bits 1 and 3-4).
 template <int HD>
 __device__ __forceinline__ int kswz(int r) {
   return HD == 128 ? ((r & 3) | (((r >> 3) & 3) << 2)) : (((r >> 1) & 1) | (((r >> 3) & 3) << 1));
 }
+// V^T tile rows (one head dimension, 64 keys = 128 bytes): the 16 consecutive rows
+// one fragment read touches, all at the same piece, fall in 16 distinct bank groups
+// (row bit 0 selects the half of the 256-byte bank line, bits 1-3 the piece).
+__device__ __forceinline__ int vswz(int r) { return (r >> 1) & 7; }
 
 template <int HD, int GQ>
 __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) void k_flash_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ vt,
     int T, int H, int n_kv, int k_len, int k_seq_stride, int vt_len, float scale,
     bf16_t* __restrict__ out) {
-  constexpr int NT = 64 * GQ;
-  constexpr int VROW = 64 + 8;
   constexpr int QSTEPS = HD / 32, HB = HD / 16;
-  constexpr int KP = 64 * HD / 8, VP = HD * 8;          // 16-byte pieces of a K / V^T tile
-  constexpr int KPT = (KP + NT - 1) / NT, VPT = (VP + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) bf16_t ks[2][64 * HD];
-  __shared__ __attribute__((aligned(16))) bf16_t vs[2][HD * VROW];
+  constexpr int NCP = HD / 8;   // 1 KB copies per K tile (and per V^T tile)
+  __shared__ __attribute__((aligned(1024))) bf16_t ks[2][64 * HD];
+  __shared__ __attribute__((aligned(1024))) bf16_t vs[2][HD * 64];
 
   const int qblk = gridDim.x - 1 - blockIdx.x;
   const int g = blockIdx.y, n = blockIdx.z;
-  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
+  const int tid = threadIdx.x, lane = tid % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
   const int h = g * GQ + wave;
   const int ldq = H * HD;
   const int q0 = qblk * 32;
@@ -317,52 +319,34 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
   const bf16_t* kbase = k + ((size_t)n * k_seq_stride * n_kv + g) * (size_t)k_len * HD;
   const bf16_t* vbase = vt + ((size_t)n * n_kv + g) * (size_t)HD * vt_len;
 
-  u32x4_t kr[KPT], vr[VPT];
-  auto load_tile = [&](int t) {
+  // Tile t of 64 keys into stage buf by direct-to-LDS copies, NCP of K and NCP of
+  // V^T dealt round-robin to the waves.  Copy i, lane l fills the 16-byte LDS
+  // piece o = 64 i + l: for K, row o / (HD / 8) (a key), piece o % (HD / 8) holding
+  // source piece (o % (HD / 8)) ^ kswz(row); for V^T, row o / 8 (a head dimension),
+  // piece o % 8 holding keys 8 ((o % 8) ^ vswz(row)) .. + 8.  A tile inside the
+  // sequence is addressed as a wave-uniform base plus a 32-bit lane offset; in the
+  // last tile of a sequence whose length is not a multiple of 64, keys past T - 1
+  // read clamped positions: their scores are masked (P = 0) and the V^T values
+  // they read are finite.
+  constexpr int KRPC = 512 / HD;   // K rows per copy
+  auto copy_tile = [&](int t, int buf) {
+    const bool edge = (t + 1) * 64 > T;
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int pi = tid + i * NT;
-      if (pi < KP) {
-        const int r = pi / (HD / 8), c = (pi % (HD / 8)) * 8;
-        const int key = min(t * 64 + r, T - 1);
-        kr[i] = *(const u32x4_t*)(kbase + (size_t)key * HD + c);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int pi = tid + i * NT;
-      if (pi < VP) {
-        const int r = pi / 8, c = (pi % 8) * 8;
-        const int key0 = t * 64 + c;
-        u32x4_t v = (u32x4_t){0u, 0u, 0u, 0u};
-        if (key0 < T) {
-          v = *(const u32x4_t*)(vbase + (size_t)r * vt_len + key0);
-          const int nv = T - key0;   // keys past T are zeroed (their P is 0, V must be finite)
-          if (nv < 8) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (e >= nv) v[e / 2] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-          }
-        }
-        vr[i] = v;
-      }
-    }
-  };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int pi = tid + i * NT;
-      if (pi < KP) {
-        const int r = pi / (HD / 8), c = (pi % (HD / 8)) * 8;
-        *(u32x4_t*)(&ks[buf][r * HD + ((c / 8) ^ kswz<HD>(r)) * 8]) = kr[i];
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int pi = tid + i * NT;
-      if (pi < VP) {
-        const int r = pi / 8, c = (pi % 8) * 8;
-        *(u32x4_t*)(&vs[buf][r * VROW + c]) = vr[i];
+    for (int i0 = 0; i0 < NCP; i0 += GQ) {
+      const int i = i0 + wave;
+      if (NCP % GQ != 0 && i >= NCP) break;
+      const int o = i * 64 + lane;
+      const int kr_ = o / (HD / 8), kp = (o % (HD / 8)) ^ kswz<HD>(kr_);
+      const int vr_ = o / 8, vp = (o % 8) ^ vswz(vr_);
+      const uint32_t kl = lds_addr(&ks[buf][i * 512]), vl = lds_addr(&vs[buf][i * 512]);
+      if (!edge) {
+        dma16s(kbase + (size_t)(t * 64 + i * KRPC) * HD, ((kr_ - i * KRPC) * HD + kp * 8) * 2, kl);
+        dma16s(vbase + (size_t)(i * 8) * vt_len + t * 64, ((vr_ - i * 8) * vt_len + vp * 8) * 2, vl);
+      } else {
+        const int key = min(t * 64 + kr_, T - 1);
+        dma16(kbase + (size_t)key * HD + kp * 8, kl);
+        const int key0 = min(t * 64 + vp * 8, vt_len - 8);
+        dma16(vbase + (size_t)vr_ * vt_len + key0, vl);
       }
     }
   };
@@ -377,12 +361,14 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
   const float scale2 = scale * 1.4426950408889634f;   // log2(e)
   const int qlast = min(q0 + 31, T - 1);
   const int n_tiles = qlast / 64 + 1;
-  load_tile(0);
-  store_tile(0);
-  if (n_tiles > 1) load_tile(1);
+  copy_tile(0, 0);
+  dma_wait();
   __syncthreads();
 
   for (int t = 0; t < n_tiles; ++t) {
+    // copy tile t + 1 into the other stage (last read in iteration t - 1, which
+    // every wave has left); it lands while tile t is used
+    if (t + 1 < n_tiles) copy_tile(t + 1, (t + 1) & 1);
     const bf16_t* ksb = &ks[t & 1][0];
     const bf16_t* vsb = &vs[t & 1][0];
     const int k0 = t * 64;
@@ -405,17 +391,19 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
                 __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][st], sacc[s2][b][qb], 0, 0, 0);
         }
       }
-    // online softmax per query column in base 2 (scores scaled by scale * log2 e,
-    // P = 2^(s - m)): tile maximum and rescale first, then per 32-key step the P^T
-    // operands (hi, lo: hardware round-to-nearest-even conversions) and their
-    // products with V^T.  A masked score is -inf and gives P = 0; the running
-    // maximum starts finite, so s - m is never inf - inf.
-    const bool full = k0 + 63 <= q0 && k0 + 63 < T;   // no key of the tile is masked
+    // online softmax per query column in base 2 (P = 2^(s scale log2 e - m), the
+    // scaling folded into one fused multiply-add; the maximum is taken over the raw
+    // scores, which commutes with the positive scaling): tile maximum and rescale
+    // first, then per 32-key step the P^T operands (hi, lo: hardware
+    // round-to-nearest-even conversions) and their products with V^T.  A masked
+    // score is -inf and gives P = 0; the running maximum starts finite, so the
+    // exponent is never inf - inf.
     float mnew[2], psum[2] = {0.f, 0.f};
     bool moved = false;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-      const int qrow = q0 + qb * 16 + lq;
+      // key k0 + 32 s2 + 8 lg + 4 b + v is visible iff 32 s2 + 4 b + v <= lim
+      const int lim = min(q0 + qb * 16 + lq, T - 1) - k0 - 8 * lg;
       float mx = -INFINITY;
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2)
@@ -423,15 +411,12 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
         for (int b = 0; b < 2; ++b)
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            const int key = k0 + 32 * s2 + 8 * lg + 4 * b + v;
-            float sc = sacc[s2][b][qb][v] * scale2;
-            if (!full) sc = (key <= qrow && key < T) ? sc : -INFINITY;
-            sacc[s2][b][qb][v] = sc;
-            mx = fmaxf(mx, sc);
+            if (32 * s2 + 4 * b + v > lim) sacc[s2][b][qb][v] = -INFINITY;
+            mx = fmaxf(mx, sacc[s2][b][qb][v]);
           }
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      mnew[qb] = fmaxf(mq[qb], mx);
+      mnew[qb] = fmaxf(mq[qb], mx * scale2);
       moved |= mnew[qb] != mq[qb];
     }
     // rescale only when some column's maximum moved (a factor of exactly 1 otherwise)
@@ -457,23 +442,26 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
         for (int b = 0; b < 2; ++b)
 #pragma unroll
           for (int v = 0; v < 4; v += 2) {
-            const float p0 = __builtin_amdgcn_exp2f(sacc[s2][b][qb][v] - mnew[qb]);
-            const float p1 = __builtin_amdgcn_exp2f(sacc[s2][b][qb][v + 1] - mnew[qb]);
+            const float p0 =
+                __builtin_amdgcn_exp2f(fmaf(sacc[s2][b][qb][v], scale2, -mnew[qb]));
+            const float p1 =
+                __builtin_amdgcn_exp2f(fmaf(sacc[s2][b][qb][v + 1], scale2, -mnew[qb]));
             psum[qb] += p0;
             psum[qb] += p1;
-            const bf16x2_t h = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
-            const bf16x2_t l = __builtin_convertvector(
-                (f32x2_t){p0 - (float)h[0], p1 - (float)h[1]}, bf16x2_t);
-            ph[qb][4 * b + v] = h[0];
-            ph[qb][4 * b + v + 1] = h[1];
-            pl[qb][4 * b + v] = l[0];
-            pl[qb][4 * b + v + 1] = l[1];
+            const bf16x2_t hi = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
+            const bf16x2_t lo = __builtin_convertvector(
+                (f32x2_t){p0 - (float)hi[0], p1 - (float)hi[1]}, bf16x2_t);
+            ph[qb][4 * b + v] = hi[0];
+            ph[qb][4 * b + v + 1] = hi[1];
+            pl[qb][4 * b + v] = lo[0];
+            pl[qb][4 * b + v + 1] = lo[1];
           }
       }
       // O^T += V^T P^T: A = V^T rows (dims 16 hb + lq), keys 32 s2 + 8 lg .. + 8
 #pragma unroll
       for (int hb = 0; hb < HB; ++hb) {
-        const bf16x8_t vf = *(const bf16x8_t*)(vsb + (hb * 16 + lq) * VROW + 32 * s2 + 8 * lg);
+        const int vr_ = hb * 16 + lq;
+        const bf16x8_t vf = *(const bf16x8_t*)(vsb + vr_ * 64 + ((4 * s2 + lg) ^ vswz(vr_)) * 8);
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
           oacc[hb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph[qb], oacc[hb][qb], 0, 0, 0);
@@ -488,11 +476,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
       sum += __shfl_xor(sum, 32, 64);
       lq_sum[qb] += sum;
     }
-    // stage tile t + 1 into the other buffer (last read in iteration t - 1)
-    if (t + 1 < n_tiles) {
-      store_tile((t + 1) & 1);
-      if (t + 2 < n_tiles) load_tile(t + 2);
-    }
+    dma_wait();
     __syncthreads();
   }
 

@@ -95,3 +95,23 @@ __device__ __forceinline__ size_t act_frag_index(int b, int k, int nb) {
   return ((size_t)(k >> 5) * (nb >> 4) + (b >> 4)) * 512 + ((b & 15) + 16 * ((k >> 3) & 3)) * 8 +
          (k & 7);
 }
+
+// ---- direct-to-LDS copies ---------------------------------------------------------
+// One copy of 16 bytes per lane (global_load_lds_dwordx4): the 64 lanes of the wave
+// fill the 1 KB at LDS byte address `lds` (wave-uniform) in lane order, each lane
+// naming its own source.  Issued as one asm statement that also sets M0, so the
+// compiler does not serialise consecutive copies (it cannot prove they write
+// disjoint LDS); the kernel waits for them itself (s_waitcnt vmcnt) before the
+// barrier that publishes the data.
+__device__ __forceinline__ void dma16(const bf16_t* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(g) : "memory");
+}
+// The same with a wave-uniform base address and a 32-bit byte offset per lane.
+__device__ __forceinline__ void dma16s(const bf16_t* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(off), "s"(base)
+               : "memory");
+}
+__device__ __forceinline__ void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}

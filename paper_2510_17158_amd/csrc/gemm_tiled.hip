@@ -190,19 +190,6 @@ constexpr int GB = 256, PBK = 32, PST = 4;
 
 __device__ __forceinline__ int pswz(int r) { return (r >> 2) & 3; }
 
-// One direct-to-LDS copy of 16 bytes per lane: the 64 lanes of the wave fill the
-// 1 KB at LDS byte address `lds` in lane order.  Issued as one asm statement that
-// also sets M0, so the compiler does not serialise consecutive copies (it cannot
-// prove they write disjoint LDS); the kernel waits on them itself (s_waitcnt
-// vmcnt) before the barrier that publishes the tile.
-__device__ __forceinline__ void dma16(const bf16_t* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(g) : "memory");
-}
-__device__ __forceinline__ void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-__device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
 // W row of B-tile row r.  SwiGLU: the B-tile rows form 4 slices of 64 (one per
 // wave column range), each 32 gate rows then the 32 up rows of the same outputs.
 // Otherwise rows of the (q, k, v) stack in order (the host guarantees that a
