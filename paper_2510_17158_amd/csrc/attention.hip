@@ -22,6 +22,7 @@
 //
 // fp32 models use a plain vector kernel (one workgroup per query row and head).
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -329,24 +330,32 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
   // read clamped positions: their scores are masked (P = 0) and the V^T values
   // they read are finite.
   constexpr int KRPC = 512 / HD;   // K rows per copy
-  auto copy_tile = [&](int t, int buf) {
-    const bool edge = (t + 1) * 64 > T;
+  auto copy_tile = [&](int t, int buf) __attribute__((always_inline)) {
+    if ((t + 1) * 64 <= T) {
 #pragma unroll
-    for (int i0 = 0; i0 < NCP; i0 += GQ) {
-      const int i = i0 + wave;
-      if (NCP % GQ != 0 && i >= NCP) break;
-      const int o = i * 64 + lane;
-      const int kr_ = o / (HD / 8), kp = (o % (HD / 8)) ^ kswz<HD>(kr_);
-      const int vr_ = o / 8, vp = (o % 8) ^ vswz(vr_);
-      const uint32_t kl = lds_addr(&ks[buf][i * 512]), vl = lds_addr(&vs[buf][i * 512]);
-      if (!edge) {
-        dma16s(kbase + (size_t)(t * 64 + i * KRPC) * HD, ((kr_ - i * KRPC) * HD + kp * 8) * 2, kl);
-        dma16s(vbase + (size_t)(i * 8) * vt_len + t * 64, ((vr_ - i * 8) * vt_len + vp * 8) * 2, vl);
-      } else {
+      for (int i0 = 0; i0 < NCP; i0 += GQ) {
+        const int i = i0 + wave;
+        if (NCP % GQ != 0 && i >= NCP) break;
+        const int o = i * 64 + lane;
+        const int kr_ = o / (HD / 8), kp = (o % (HD / 8)) ^ kswz<HD>(kr_);
+        const int vr_ = o / 8, vp = (o % 8) ^ vswz(vr_);
+        dma16s(kbase + (size_t)(t * 64 + i * KRPC) * HD, ((kr_ - i * KRPC) * HD + kp * 8) * 2,
+               lds_addr(&ks[buf][i * 512]));
+        dma16s(vbase + (size_t)(i * 8) * vt_len + t * 64, ((vr_ - i * 8) * vt_len + vp * 8) * 2,
+               lds_addr(&vs[buf][i * 512]));
+      }
+    } else {
+#pragma unroll
+      for (int i0 = 0; i0 < NCP; i0 += GQ) {
+        const int i = i0 + wave;
+        if (NCP % GQ != 0 && i >= NCP) break;
+        const int o = i * 64 + lane;
+        const int kr_ = o / (HD / 8), kp = (o % (HD / 8)) ^ kswz<HD>(kr_);
+        const int vr_ = o / 8, vp = (o % 8) ^ vswz(vr_);
         const int key = min(t * 64 + kr_, T - 1);
-        dma16(kbase + (size_t)key * HD + kp * 8, kl);
+        dma16(kbase + (size_t)key * HD + kp * 8, lds_addr(&ks[buf][i * 512]));
         const int key0 = min(t * 64 + vp * 8, vt_len - 8);
-        dma16(vbase + (size_t)vr_ * vt_len + key0, vl);
+        dma16(vbase + (size_t)vr_ * vt_len + key0, lds_addr(&vs[buf][i * 512]));
       }
     }
   };
@@ -365,7 +374,11 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
   dma_wait();
   __syncthreads();
 
-  for (int t = 0; t < n_tiles; ++t) {
+  // One key tile: scores, online softmax and P.V.  Only the last tile holds
+  // masked keys (the causal diagonal and keys past T - 1): every key of an
+  // earlier tile is below q0, so MASK is set for the last tile only.
+  auto tile_step = [&](int t, auto mask_c) __attribute__((always_inline)) {
+    constexpr bool MASK = decltype(mask_c)::value;
     // copy tile t + 1 into the other stage (last read in iteration t - 1, which
     // every wave has left); it lands while tile t is used
     if (t + 1 < n_tiles) copy_tile(t + 1, (t + 1) & 1);
@@ -391,10 +404,10 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
                 __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][st], sacc[s2][b][qb], 0, 0, 0);
         }
       }
-    // online softmax per query column in base 2 (P = 2^(s scale log2 e - m), the
-    // scaling folded into one fused multiply-add; the maximum is taken over the raw
-    // scores, which commutes with the positive scaling): tile maximum and rescale
-    // first, then per 32-key step the P^T operands (hi, lo: hardware
+    // online softmax per query column in base 2 (P = 2^(s scale log2 e - m) for a
+    // reference maximum m of the column, the scaling folded into one fused
+    // multiply-add; the tile maximum is taken over the raw scores, which commutes
+    // with the positive scaling): tile maximum and rescale first, then per 32-key step the P^T operands (hi, lo: hardware
     // round-to-nearest-even conversions) and their products with V^T.  A masked
     // score is -inf and gives P = 0; the running maximum starts finite, so the
     // exponent is never inf - inf.
@@ -402,7 +415,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
     bool moved = false;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-      // key k0 + 32 s2 + 8 lg + 4 b + v is visible iff 32 s2 + 4 b + v <= lim
+      // (last tile) key k0 + 32 s2 + 8 lg + 4 b + v is visible iff 32 s2 + 4 b + v <= lim
       const int lim = min(q0 + qb * 16 + lq, T - 1) - k0 - 8 * lg;
       float mx = -INFINITY;
 #pragma unroll
@@ -411,15 +424,19 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
         for (int b = 0; b < 2; ++b)
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            if (32 * s2 + 4 * b + v > lim) sacc[s2][b][qb][v] = -INFINITY;
+            if (MASK && 32 * s2 + 4 * b + v > lim) sacc[s2][b][qb][v] = -INFINITY;
             mx = fmaxf(mx, sacc[s2][b][qb][v]);
           }
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      mnew[qb] = fmaxf(mq[qb], mx * scale2);
+      // the reference maximum moves only when the column maximum exceeds it by
+      // more than 8 (so P <= 2^8; the hi + lo terms keep their relative precision
+      // and the fp32 sums their range), which makes the rescale rare
+      mnew[qb] = mx * scale2 > mq[qb] + 8.f ? mx * scale2 : mq[qb];
       moved |= mnew[qb] != mq[qb];
     }
-    // rescale only when some column's maximum moved (a factor of exactly 1 otherwise)
+    // rescale only when some column's reference maximum moved (a factor of exactly
+    // 1 otherwise)
     if (__builtin_amdgcn_ballot_w64(moved)) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
@@ -478,7 +495,9 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
     }
     dma_wait();
     __syncthreads();
-  }
+  };
+  for (int t = 0; t + 1 < n_tiles; ++t) tile_step(t, std::false_type{});
+  tile_step(n_tiles - 1, std::true_type{});
 
   // O^T: lane holds dims 16 hb + 4 lg + v of query column lq
 #pragma unroll
