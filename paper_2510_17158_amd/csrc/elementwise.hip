@@ -61,11 +61,13 @@ __global__ __launch_bounds__(NORM_NT) void k_rmsnorm(float* x, int ldx, RowMap r
   const size_t src = (size_t)(gi / rm.per) * rm.stride + rm.off + gi % rm.per;
   float* xr = x + src * ldx;
   const int n4 = d / 4;
-  float4 v[NORM_VPT];
+  float4 v[NORM_VPT], gv[NORM_VPT];
 #pragma unroll
   for (int k = 0; k < NORM_VPT; ++k) {
     const int i4 = threadIdx.x + k * NORM_NT;
     v[k] = i4 < n4 ? *(const float4*)(xr + 4 * i4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    // the gain is loaded up front with the row (no second memory round trip)
+    gv[k] = g && i4 < n4 ? load4(g, 4 * (size_t)i4) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   if (pp.splits > 0) {
     // four splits' loads in flight at a time (a split past the last re-reads the
@@ -112,12 +114,10 @@ __global__ __launch_bounds__(NORM_NT) void k_rmsnorm(float* x, int ldx, RowMap r
 #pragma unroll
   for (int k = 0; k < NORM_VPT; ++k) {
     const int i4 = threadIdx.x + k * NORM_NT;
-    if (i4 < n4) {
-      const float4 gv = load4(g, 4 * (size_t)i4);
+    if (i4 < n4)
       store4(out, pack_nb ? act_frag_index(m, 4 * i4, pack_nb) : (size_t)m * ldo + 4 * i4,
-             make_float4(v[k].x * r * gv.x, v[k].y * r * gv.y, v[k].z * r * gv.z,
-                         v[k].w * r * gv.w));
-    }
+             make_float4(v[k].x * r * gv[k].x, v[k].y * r * gv[k].y, v[k].z * r * gv[k].z,
+                         v[k].w * r * gv[k].w));
   }
 }
 
@@ -137,13 +137,24 @@ __global__ void k_rope_kv(const float* qkv, int M, T* q_out, RopeArgs a) {
   else { seq = m / a.T; pos = m % a.T; }
   const int ldq = heads * a.hd;
   const float* src = qkv + (size_t)m * ldq + h * a.hd;
+  const bool rotate = h < a.n_heads + a.n_kv;
+  // the cos/sin pair and up to four splits' values are loaded together, then the
+  // splits are added in split order
+  const float2 cs = rotate ? a.cs[(size_t)(a.mode == 0 ? m : pos) * half + i] : make_float2(1.f, 0.f);
   float lo = src[i], hi = src[i + half];
-  for (int sp = 1; sp < a.splits; ++sp) {
-    lo += src[sp * a.split_stride + i];
-    hi += src[sp * a.split_stride + i + half];
+  for (int sp0 = 1; sp0 < a.splits; sp0 += 4) {
+    float tl[4], th[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const size_t so = (size_t)min(sp0 + u, a.splits - 1) * a.split_stride;
+      tl[u] = src[so + i];
+      th[u] = src[so + i + half];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (sp0 + u < a.splits) { lo += tl[u]; hi += th[u]; }
   }
-  if (h < a.n_heads + a.n_kv) {
-    const float2 cs = a.cs[(size_t)(a.mode == 0 ? m : pos) * half + i];
+  if (rotate) {
     const float c = cs.x, s = cs.y;
     const float l2 = lo * c - hi * s;
     const float h2 = hi * c + lo * s;

@@ -167,19 +167,20 @@ __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
 // period 4) and its 128 x 128 quarter of the tile, 64 columns each (4 x 2 blocks
 // of 32 x 32, 128 accumulators).  The two waves of a SIMD take turns: while one
 // runs the 16 MFMAs of a 32-wide k-tile on fragments already in registers, the
-// other reads its fragments of the next k-tile from LDS and (group A, waves 0-3)
-// issues direct-to-LDS copies (global_load_lds_dwordx4: each lane names its own
+// other reads its fragments of the next k-tile from LDS and issues its half of
+// the direct-to-LDS copies (global_load_lds_dwordx4: each lane names its own
 // source, the 64 lanes fill 1 KB of LDS in lane order) three k-tiles ahead; a
 // barrier swaps the roles, so the wave feeding the matrix core never stops for a
 // memory instruction.  Four LDS stages (k-tile t in stage t % 4, 32 KB each).
 // Schedule (slot = the time between two barriers; A = waves 0-3, B = 4-7):
-//   slot 2t:   A copies tile t + 3 into stage (t + 3) % 4 and reads tile t;
-//              B multiplies tile t - 1
+//   slot 2t:   A copies its half of tile t + 3 into stage (t + 3) % 4 and reads
+//              tile t; B multiplies tile t - 1
 //   slot 2t+1: A multiplies tile t, then waits until its copies of tile t + 1
-//              have landed; B reads tile t
-// A stage is refilled (slot 2t) only after both groups read its previous tile
-// (slots 2t - 2, 2t - 1), and a copied tile is published by the barrier after A's
-// wait, before its first read (slot 2t + 2).
+//              have landed; B copies its half of tile t + 3, reads tile t and
+//              waits for its copies of tile t + 1
+// A stage is refilled (slots 2t, 2t + 1) only after both groups read its previous
+// tile (slots 2t - 2, 2t - 1), and a copied tile is published by the barrier after
+// both groups' waits, before its first read (slot 2t + 2).
 // Rows of a stage are 64 bytes, their four 16-byte pieces XOR-swizzled by
 // (row >> 2) & 3 (conflict-free fragment reads).
 // Measured on the scoring shapes, the operand copies alone (no MFMA) take about
@@ -235,10 +236,10 @@ __global__ __launch_bounds__(512) void k_gemm_pp(TArgs a) {
   const int tn = (st % st_n) * 8 + loc % 8;
   if (tm >= a.tiles_m || tn >= a.tiles_n) return;
 
-  // Copies (group A only): instruction j (0..3) of wave sq fills tile rows
-  // 64 sq + 16 j .. + 16 of both operands (lane -> row + lane / 4, piece lane % 4
-  // holding source piece (lane % 4) ^ pswz(row), the same for every j); SwiGLU W
-  // rows switch from gate to up at j = 2.
+  // Copies: instruction j (0..3) of wave sq fills tile rows 64 sq + 16 j .. + 16
+  // of both operands, group A issuing j = 0, 1 and group B j = 2, 3 (lane -> row
+  // + lane / 4, piece lane % 4 holding source piece (lane % 4) ^ pswz(row), the
+  // same for every j); SwiGLU W rows switch from gate to up at j = 2.
   const int m0 = min(tm * GB, a.M - GB);
   const int r0 = sq * 64 + lane / 4;
   const int pbase = ((lane % 4) ^ pswz(r0)) * 8;
@@ -248,7 +249,7 @@ __global__ __launch_bounds__(512) void k_gemm_pp(TArgs a) {
   const size_t astep = (size_t)16 * a.ldx, bstep = (size_t)16 * a.K;
   auto copy = [&](int buf, int kt) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 2 * grp; j < 2 * grp + 2; ++j) {
       const int off = (sq * 4 + j) * 16 * PBK;
       dma16(ab + j * astep + kt * PBK, lds_addr(&lds[buf][0][off]));
       const bf16_t* bsrc = (EPI == EPI_SWIGLU && j >= 2) ? bb1 + (j - 2) * bstep : bb0 + j * bstep;
@@ -296,30 +297,33 @@ __global__ __launch_bounds__(512) void k_gemm_pp(TArgs a) {
   };
 
   const int nk = a.K / PBK;    // >= 4 (K is a multiple of 128)
-  if (grp == 0) {
-    copy(0, 0);
-    copy(1, 1);
-    copy(2, 2);
-    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");   // tile 0 (8 copies per tile)
-  }
+  copy(0, 0);
+  copy(1, 1);
+  copy(2, 2);
+  asm volatile("s_waitcnt vmcnt(8)" ::: "memory");   // tile 0 (4 copies per wave per tile)
   PP_BARRIER();
+  auto wait_next = [&](int t) {
+    // tile t + 1 landed: only the copies of tiles t + 2 and t + 3 may remain
+    if (t + 3 < nk) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else if (t + 2 < nk) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  };
   if (grp == 0) {
     for (int t = 0; t < nk; ++t) {
       if (t + 3 < nk) copy((t + 3) % PST, t + 3);
       frags(t % PST);
       PP_BARRIER();
       mma();
-      // tile t + 1 landed: only the copies of tiles t + 2 and t + 3 may remain
-      if (t + 3 < nk) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-      else if (t + 2 < nk) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-      else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      wait_next(t);
       PP_BARRIER();
     }
     PP_BARRIER();
   } else {
     PP_BARRIER();
     for (int t = 0; t < nk; ++t) {
+      if (t + 3 < nk) copy((t + 3) % PST, t + 3);
       frags(t % PST);
+      wait_next(t);
       PP_BARRIER();
       mma();
       PP_BARRIER();
