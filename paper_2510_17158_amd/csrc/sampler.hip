@@ -1,6 +1,7 @@
 // Next-token sampling over the LM-head logits and its log-probability.
 //
-// One workgroup per (row, draw).  The row is read from L2 a few times:
+// One workgroup per (row, draw).  Vocabularies up to 32768 ids are read once into
+// registers (1024 threads x 32 logits); larger ones are read from L2 per pass:
 //   1. max and arg-max of z = l / T (lowest id among equal maxima),
 //   2. sum of exp(z - max) -> log-sum-exp (full vocabulary),
 //   3. with top_k > 0: radix select (four 8-bit passes, LDS histograms with
@@ -41,6 +42,7 @@ __device__ __forceinline__ void better(float& bv, int& bi, float v, int i) {
   if (v > bv || (v == bv && i < bi)) { bv = v; bi = i; }
 }
 
+template <int NTH = NT>
 __device__ __forceinline__ void block_argmax(float& bv, int& bi, float* shv, int* shi) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -53,7 +55,7 @@ __device__ __forceinline__ void block_argmax(float& bv, int& bi, float* shv, int
   if ((threadIdx.x & 63) == 0) { shv[w] = bv; shi[w] = bi; }
   __syncthreads();
   bv = shv[0]; bi = shi[0];
-  for (int i = 1; i < NT / 64; ++i) better(bv, bi, shv[i], shi[i]);
+  for (int i = 1; i < NTH / 64; ++i) better(bv, bi, shv[i], shi[i]);
 }
 
 __global__ __launch_bounds__(NT) void k_sample(const float* __restrict__ logits, int V, int ld,
@@ -166,13 +168,158 @@ __global__ __launch_bounds__(NT) void k_sample(const float* __restrict__ logits,
   }
 }
 
+// The same for a vocabulary of at most NTR * 4 * R4 ids, read from memory once:
+// NTR threads each hold R4 groups of 4 consecutive logits (group c = thread + NTR j,
+// which is also its Philox block) in registers for every pass.
+constexpr int NTR = 1024, R4 = 8;
+
+__global__ __launch_bounds__(NTR) void k_sample_reg(const float* __restrict__ logits, int V,
+                                                    int ld, SampleArgs a) {
+  __shared__ float sh[NTR / 64];
+  __shared__ float shv[NTR / 64];
+  __shared__ int shi[NTR / 64];
+  __shared__ int hist[256];
+  __shared__ uint32_t s_prefix;
+  __shared__ int s_krem, s_eq, s_cut;
+  const int r = blockIdx.x, gdraw = blockIdx.y;
+  const int seq = r * a.G + gdraw;
+  const int col = a.step_ctr ? *a.step_ctr : 0;
+  const int step = a.step + col;
+  const float* l = logits + (size_t)r * ld;
+  const int tid = threadIdx.x;
+  const bool greedy = !(a.temperature > 0.f);
+  const float T = greedy ? 1.f : a.temperature;
+
+  // ids past V hold -inf (never the maximum, exp gives 0, excluded below)
+  float x[R4][4];
+#pragma unroll
+  for (int j = 0; j < R4; ++j) {
+    const int i0 = 4 * (tid + NTR * j);
+    if (i0 + 3 < V && (ld & 3) == 0) {
+      const float4 v = *(const float4*)(l + i0);
+      x[j][0] = v.x; x[j][1] = v.y; x[j][2] = v.z; x[j][3] = v.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[j][e] = i0 + e < V ? l[i0 + e] : -INFINITY;
+    }
+  }
+
+  // 1-2: max / arg-max and log-sum-exp of z
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+#pragma unroll
+  for (int j = 0; j < R4; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) better(bv, bi, x[j][e], 4 * (tid + NTR * j) + e);
+  block_argmax<NTR>(bv, bi, shv, shi);
+  const float zmax = bv / T;
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < R4; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s += __expf(x[j][e] / T - zmax);
+  s = block_sum<NTR>(s, sh);
+  const float lse = zmax + logf(s);
+
+  int tok = bi;
+  if (!greedy) {
+    // 3: top-k cut
+    uint32_t thr = 0;
+    int cut = 0x7fffffff;
+    const bool use_k = a.top_k > 0 && a.top_k < V;
+    if (use_k) {
+      uint32_t prefix = 0, pmask = 0;
+      int krem = a.top_k;
+      for (int shift = 24; shift >= 0; shift -= 8) {
+        for (int i = tid; i < 256; i += NTR) hist[i] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < R4; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t u = order_key(x[j][e]);
+            if (4 * (tid + NTR * j) + e < V && (u & pmask) == prefix)
+              atomicAdd(&hist[(u >> shift) & 255], 1);
+          }
+        __syncthreads();
+        if (tid == 0) {
+          int cum = 0, sel = 0;
+          for (int bin = 255; bin >= 0; --bin) {
+            if (cum + hist[bin] >= krem) { sel = bin; break; }
+            cum += hist[bin];
+          }
+          s_krem = krem - cum;
+          s_eq = hist[sel];
+          s_prefix = prefix | ((uint32_t)sel << shift);
+        }
+        __syncthreads();
+        krem = s_krem;
+        prefix = s_prefix;
+        pmask |= 255u << shift;
+        __syncthreads();
+      }
+      thr = prefix;
+      // ids equal to the cut value: keep the lowest krem of them
+      if (tid == 0) {
+        int c = 0x7fffffff;
+        if (s_eq > krem) {
+          int seen = 0;
+          for (int i = 0; i < V; ++i)
+            if (order_key(l[i]) == thr && ++seen == krem) { c = i; break; }
+        }
+        s_cut = c;
+      }
+      __syncthreads();
+      cut = s_cut;
+    }
+    // 4: Gumbel-max over the allowed ids
+    const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
+    float gv = -INFINITY;
+    int gi = 0x7fffffff;
+#pragma unroll
+    for (int j = 0; j < R4; ++j) {
+      const int c = tid + NTR * j;
+      if (4 * c < V) {
+        const uint4 w = philox4x32_10(make_uint4((uint32_t)c, (uint32_t)step, (uint32_t)seq, 0u),
+                                      k0, k1);
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int i = 4 * c + e;
+          const float li = x[j][e];
+          bool ok = i < V;
+          if (use_k) {
+            const uint32_t u = order_key(li);
+            ok = ok && (u > thr || (u == thr && i <= cut));
+          }
+          const float uu = (float)(2u * (ws[e] >> 9) + 1u) * 5.9604644775390625e-8f;  // 2^-24
+          const float key = li / T - logf(-logf(uu));
+          if (ok) better(gv, gi, key, i);
+        }
+      }
+    }
+    block_argmax<NTR>(gv, gi, shv, shi);
+    tok = gi;
+  }
+  if (tid == 0) {
+    tok = clampi(tok, 0, V - 1);
+    a.tok_out[(size_t)seq * a.out_stride + col] = tok;
+    a.logp_out[(size_t)seq * a.out_stride + col] = l[tok] / T - lse;
+    if (a.tok_state) a.tok_state[seq] = tok;
+    if (a.pos_state) a.pos_state[seq] += 1;
+  }
+}
+
 }  // namespace
 
 hipError_t sample(const float* logits, int R, int V, int ld, const SampleArgs& a, hipStream_t st) {
   if (R <= 0) return hipSuccess;
   dim3 grid(R, a.G);
   Prof pf("sample", st);
-  k_sample<<<grid, NT, 0, st>>>(logits, V, ld, a);
+  if (V <= NTR * 4 * R4)
+    k_sample_reg<<<grid, NTR, 0, st>>>(logits, V, ld, a);
+  else
+    k_sample<<<grid, NT, 0, st>>>(logits, V, ld, a);
   return hipGetLastError();
 }
 
