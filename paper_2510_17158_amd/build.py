@@ -19,6 +19,7 @@ LIB = os.path.join(HERE, "libgrpo_hip.so")
 ARCH = "gfx950"
 
 SOURCES = ["api.cpp", "gemm_decode.hip", "gemm_tiled.hip", "elementwise.hip", "attention.hip",
+           "attn_decode.hip",
            "sampler.hip", "grpo.hip"]
 
 COMMON_FLAGS = [

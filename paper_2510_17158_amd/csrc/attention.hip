@@ -1,26 +1,11 @@
-// Attention of the decoder: decode against the per-sequence KV cache
-// (split-K over the context) and causal attention for prompt prefill and
-// teacher-forced scoring.
+// Causal attention of the decoder for prompt prefill and teacher-forced scoring.
 //
-// Decode (bf16): one workgroup per (context span, kv head, sequence); the span
-// is the whole context unless there are too few (sequence, kv head) pairs to
-// fill the chip.  Each of the 4 waves streams tiles of 32 positions (tiles
-// w, w+4, ...) with the next tile's K and V loads in flight while the current
-// tile is computed, and keeps an online softmax (running max, sum and
-// unnormalised output per query head).  QK^T runs on MFMA with the K tile as
-// the A operand (16 positions x head_dim) and the group's query heads as the
-// B columns; P.V runs on the vector units (each lane owns 8 head-dim elements of
-// one position, 16-byte coalesced V loads).  The waves are merged through LDS at
-// the end; a single-span launch writes the normalised bf16 output directly,
-// otherwise each span writes (max, sum, unnormalised o) and a second kernel
-// merges the spans in span order.
+// bf16: flash attention, one workgroup per (32 queries, kv head, sequence) with
+// one wave per query head of the group sharing the K and V^T tiles (V^T is
+// written transposed by the rotary kernel); details at the kernel.
 //
-// Prefill / scoring (bf16): flash attention, one workgroup per (32 queries, kv
-// head, sequence) with one wave per query head of the group sharing the K and
-// V^T tiles (V^T is written transposed by the rotary kernel); details at the
-// kernel.
-//
-// fp32 models use a plain vector kernel (one workgroup per query row and head).
+// fp32 models use a plain vector kernel (one workgroup per query row and head),
+// also for decode.
 #include <algorithm>
 #include <type_traits>
 
@@ -30,236 +15,6 @@
 namespace grpo {
 
 namespace {
-
-constexpr int DT = 32;            // decode positions per wave tile
-constexpr int SPAN_Q = 4 * DT;    // span granularity: one tile per wave
-
-template <int HD, int NG, int NVT>
-struct KVTile {
-  u32x4_t k[NG][HD / 32];
-  u32x4_t v[NVT];
-};
-
-// ---------------------------------------------------------------- decode, bf16
-template <int HD, int MAXG>
-__global__ __launch_bounds__(256) void k_attn_decode_bf16(
-    const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
-    const int32_t* __restrict__ pos, int H, int n_kv, int max_len, int S, int span, float scale,
-    float* __restrict__ part_o, float* __restrict__ part_ml, bf16_t* __restrict__ out,
-    int pack_nb) {
-  constexpr int QSTEPS = HD / 32;     // MFMA k-steps over the head dim
-  constexpr int LPT = HD / 8;         // lanes per position in P.V
-  constexpr int PPW = 64 / LPT;       // positions per V load instruction
-  constexpr int NVT = DT / PPW;       // V load instructions per tile
-  constexpr int NG = DT / 16;         // MFMA position groups per tile
-  using Tile = KVTile<HD, NG, NVT>;
-  __shared__ __attribute__((aligned(16))) float pw[4][DT][MAXG];
-  __shared__ __attribute__((aligned(16))) float pa[4][MAXG];
-  __shared__ float red[4][MAXG * HD];
-  __shared__ float wm[4][MAXG], wl[4][MAXG];
-
-  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-  const int GQ = H / n_kv;
-  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
-  const int ctx = min(pos[b], max_len - 1) + 1;
-  const int t0 = split * span;
-  if (t0 >= ctx) return;
-  const int t1 = min(t0 + span, ctx);
-  const int ntiles = (t1 - t0 + DT - 1) / DT;
-  const int nmine = ntiles > wave ? (ntiles - wave + 3) / 4 : 0;
-  const size_t head_base = ((size_t)b * n_kv + g) * max_len;
-  const bf16_t* kb = kc + head_base * HD;
-  const bf16_t* vb = vc + head_base * HD;
-  const int lg = lane >> 4;           // MFMA k-group of this lane
-  const int j = lane & 15;            // MFMA row (position) / column (query head)
-  const int ts = lane / LPT, hg = lane % LPT;
-
-  // query fragments; head-dim chunk (st * 4 + lg) of 8 elements feeds MFMA step st,
-  // so each K load instruction reads 64 contiguous bytes per position
-  bf16x8_t qf[QSTEPS];
-  {
-    const bf16_t* qp = q + ((size_t)b * H + g * GQ + min(j, GQ - 1)) * HD + lg * 8;
-#pragma unroll
-    for (int st = 0; st < QSTEPS; ++st) {
-      u32x4_t v = *(const u32x4_t*)(qp + st * 32);
-      if (j >= GQ) v = (u32x4_t){0u, 0u, 0u, 0u};
-      qf[st] = __builtin_bit_cast(bf16x8_t, v);
-    }
-  }
-
-  auto load = [&](Tile& tl, int i) {
-    const int tb = t0 + (wave + 4 * i) * DT;
-#pragma unroll
-    for (int grp = 0; grp < NG; ++grp) {
-      const int t = min(tb + grp * 16 + j, ctx - 1);
-      const bf16_t* kp = kb + (size_t)t * HD + lg * 8;
-#pragma unroll
-      for (int st = 0; st < QSTEPS; ++st) tl.k[grp][st] = *(const u32x4_t*)(kp + st * 32);
-    }
-#pragma unroll
-    for (int iv = 0; iv < NVT; ++iv) {
-      const int t = min(tb + iv * PPW + ts, ctx - 1);
-      tl.v[iv] = *(const u32x4_t*)(vb + (size_t)t * HD + hg * 8);
-    }
-  };
-
-  float m = -1e30f, l = 0.f;          // running max / partial sum of head j (this lane's rows)
-  float o[MAXG][8];
-#pragma unroll
-  for (int h = 0; h < MAXG; ++h)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
-
-  auto compute = [&](const Tile& tl, int i) {
-    const int tb = t0 + (wave + 4 * i) * DT;
-    float sv[NG][4];
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int grp = 0; grp < NG; ++grp) {
-      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int st = 0; st < QSTEPS; ++st)
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, tl.k[grp][st]),
-                                                      qf[st], acc, 0, 0, 0);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float sc = (tb + grp * 16 + lg * 4 + v < t1) ? acc[v] * scale : -INFINITY;
-        sv[grp][v] = sc;
-        tmax = fmaxf(tmax, sc);
-      }
-    }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mnew = fmaxf(m, tmax);
-    const float alpha = __expf(m - mnew);
-    m = mnew;
-    float ps = 0.f;
-#pragma unroll
-    for (int grp = 0; grp < NG; ++grp)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float p = __expf(sv[grp][v] - mnew);
-        ps += p;
-        if (j < MAXG) pw[wave][grp * 16 + lg * 4 + v][j] = p;
-      }
-    l = l * alpha + ps;
-    if (lg == 0 && j < MAXG) pa[wave][j] = alpha;
-    __builtin_amdgcn_wave_barrier();
-    float al[MAXG];
-#pragma unroll
-    for (int h = 0; h < MAXG; h += 4) {
-      const float4 a4 = *(const float4*)&pa[wave][h];
-      al[h] = a4.x; al[h + 1] = a4.y; al[h + 2] = a4.z; al[h + 3] = a4.w;
-    }
-    // all MAXG columns are updated (no per-head branches in the loop); columns
-    // past GQ hold products of a zero query and are never written out
-#pragma unroll
-    for (int h = 0; h < MAXG; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[h][e] *= al[h];
-#pragma unroll
-    for (int iv = 0; iv < NVT; ++iv) {
-      const u32x4_t raw = tl.v[iv];
-      float vv[8];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vv[2 * e] = __uint_as_float(raw[e] << 16);
-        vv[2 * e + 1] = __uint_as_float(raw[e] & 0xffff0000u);
-      }
-      float pp[MAXG];
-#pragma unroll
-      for (int h = 0; h < MAXG; h += 4) {
-        const float4 p4 = *(const float4*)&pw[wave][iv * PPW + ts][h];
-        pp[h] = p4.x; pp[h + 1] = p4.y; pp[h + 2] = p4.z; pp[h + 3] = p4.w;
-      }
-#pragma unroll
-      for (int h = 0; h < MAXG; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[h][e] = fmaf(pp[h], vv[e], o[h][e]);
-    }
-    __builtin_amdgcn_wave_barrier();
-  };
-
-  // two tiles in registers: the next one loads while the current one is used;
-  // past the wave's last tile the loads repeat that tile (in bounds, results unused)
-  if (nmine > 0) {
-    Tile ta, tb;
-    load(ta, 0);
-    for (int i = 0; i < nmine; i += 2) {
-      load(tb, min(i + 1, nmine - 1));
-      compute(ta, i);
-      load(ta, min(i + 2, nmine - 1));
-      if (i + 1 < nmine) compute(tb, i + 1);
-    }
-  }
-
-  // wave totals: o over the positions of a load instruction, l over the k-groups
-#pragma unroll
-  for (int h = 0; h < MAXG; ++h)
-    if (h < GQ) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float x = o[h][e];
-#pragma unroll
-        for (int off = LPT; off < 64; off <<= 1) x += __shfl_xor(x, off, 64);
-        o[h][e] = x;
-      }
-    }
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
-  if (lg == 0 && j < MAXG) { wm[wave][j] = m; wl[wave][j] = l; }
-  if (ts == 0) {
-#pragma unroll
-    for (int h = 0; h < MAXG; ++h)
-      if (h < GQ) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) red[wave][h * HD + hg * 8 + e] = o[h][e];
-      }
-  }
-  __syncthreads();
-  // merge the 4 waves (fixed order)
-  for (int i = tid; i < GQ * HD; i += 256) {
-    const int h = i / HD, e = i % HD;
-    const float M = fmaxf(fmaxf(wm[0][h], wm[1][h]), fmaxf(wm[2][h], wm[3][h]));
-    float x = 0.f, L = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float c = __expf(wm[w][h] - M);
-      x = fmaf(c, red[w][i], x);
-      L = fmaf(c, wl[w][h], L);
-    }
-    if (S == 1) {
-      const int k = (g * GQ + h) * HD + e;
-      out[pack_nb ? act_frag_index(b, k, pack_nb) : (size_t)b * H * HD + k] = f2bf(x / L);
-    } else {
-      const size_t row = ((size_t)b * H + g * GQ + h) * S + split;
-      part_o[row * HD + e] = x;
-      if (e == 0) { part_ml[row * 2] = M; part_ml[row * 2 + 1] = L; }
-    }
-  }
-}
-
-template <int HD>
-__global__ __launch_bounds__(HD) void k_attn_combine(const float* __restrict__ part_o,
-                                                     const float* __restrict__ part_ml,
-                                                     const int32_t* __restrict__ pos, int H,
-                                                     int max_len, int S, int span,
-                                                     bf16_t* __restrict__ out, int pack_nb) {
-  const int h = blockIdx.x, b = blockIdx.y, e = threadIdx.x;
-  const int ctx = min(pos[b], max_len - 1) + 1;
-  const int ns = min(S, (ctx + span - 1) / span);
-  const size_t row0 = ((size_t)b * H + h) * S;
-  float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, part_ml[(row0 + s) * 2]);
-  float L = 0.f, acc = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const float w = __expf(part_ml[(row0 + s) * 2] - M);
-    L = fmaf(part_ml[(row0 + s) * 2 + 1], w, L);
-    acc = fmaf(part_o[(row0 + s) * HD + e], w, acc);
-  }
-  const int k = h * HD + e;
-  out[pack_nb ? act_frag_index(b, k, pack_nb) : (size_t)b * H * HD + k] = f2bf(acc / L);
-}
 
 // ----------------------------------------------------------- flash attention, bf16
 // One workgroup per (32 query rows, kv head, sequence) with one wave per query
@@ -583,70 +338,15 @@ __global__ __launch_bounds__(256) void k_attn_rows_f32(const float* __restrict__
 
 }  // namespace
 
-DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len) {
-  // enough spans for about two workgroups per compute unit; one span (and no
-  // merge kernel) whenever the (sequence, kv head) pairs alone reach that
-  constexpr int kTargetWGs = 512;
-  const int pairs = std::max(1, B * n_kv);
-  const int max_spans = (max_len + SPAN_Q - 1) / SPAN_Q;
-  const int want = std::min(std::max(1, (kTargetWGs + pairs / 2) / pairs), max_spans);
-  DecodeAttnPlan p;
-  p.tc = ((max_len + want - 1) / want + SPAN_Q - 1) / SPAN_Q * SPAN_Q;
-  p.splits = (max_len + p.tc - 1) / p.tc;
-  p.part_floats = p.splits > 1 ? (size_t)B * H * p.splits * (hd + 2) : 0;
-  return p;
-}
-
-template <int HD, int MAXG>
-static void launch_decode(dim3 grid, hipStream_t st, const void* q, const void* kc,
-                          const void* vc, const int32_t* pos, int H, int n_kv, int max_len,
-                          const DecodeAttnPlan& p, float scale, float* part_o, float* part_ml,
-                          void* out, int pack_nb) {
-  k_attn_decode_bf16<HD, MAXG><<<grid, 256, 0, st>>>(
-      (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, H, n_kv, max_len, p.splits,
-      p.tc, scale, part_o, part_ml, (bf16_t*)out, pack_nb);
-}
-
-hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
-                       const int32_t* pos, int B, int H, int n_kv, int hd, int n_seqs, int max_len,
-                       const DecodeAttnPlan& p, float* part, void* out, hipStream_t st,
-                       int pack_nb) {
-  (void)n_seqs;
-  if (B <= 0) return hipSuccess;
-  if (pack_nb && (dtype == 0 || B > pack_nb || pack_nb % 16)) return hipErrorInvalidValue;
+hipError_t attn_rows_f32(const float* q, const float* kc, const float* vc, const int32_t* pos,
+                         int rows, int T, int slot_mul, int H, int n_kv, int hd, int k_len,
+                         float* out, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
   const float scale = 1.f / sqrtf((float)hd);
-  if (dtype == 0) {
-    dim3 grid(B, H);
-    Prof pf("attn_f32", st);
-    k_attn_rows_f32<<<grid, 256, max_len * sizeof(float), st>>>(
-        (const float*)q, H * hd, (const float*)kc, (const float*)vc, pos, 1, 1, H, n_kv, hd,
-        max_len, scale, (float*)out);
-    return hipGetLastError();
-  }
-  float* part_o = p.splits > 1 ? part : nullptr;
-  float* part_ml = p.splits > 1 ? part + (size_t)B * H * p.splits * hd : nullptr;
-  dim3 grid(p.splits, n_kv, B);
-  const int gq = H / n_kv;
-  {
-    Prof pf("attn_decode", st);
-    if (hd == 128) {
-      if (gq <= 4) launch_decode<128, 4>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
-      else launch_decode<128, 8>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
-    } else {
-      if (gq <= 4) launch_decode<64, 4>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
-      else launch_decode<64, 8>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
-    }
-  }
-  if (p.splits > 1) {
-    Prof pf("attn_combine", st);
-    dim3 cgrid(H, B);
-    if (hd == 128)
-      k_attn_combine<128><<<cgrid, 128, 0, st>>>(part_o, part_ml, pos, H, max_len, p.splits,
-                                                 p.tc, (bf16_t*)out, pack_nb);
-    else
-      k_attn_combine<64><<<cgrid, 64, 0, st>>>(part_o, part_ml, pos, H, max_len, p.splits,
-                                               p.tc, (bf16_t*)out, pack_nb);
-  }
+  dim3 grid(rows, H);
+  Prof pf("attn_f32", st);
+  k_attn_rows_f32<<<grid, 256, k_len * sizeof(float), st>>>(q, H * hd, kc, vc, pos, T, slot_mul,
+                                                            H, n_kv, hd, k_len, scale, out);
   return hipGetLastError();
 }
 

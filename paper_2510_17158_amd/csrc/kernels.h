@@ -133,6 +133,12 @@ hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
                        const int32_t* pos, int B, int H, int n_kv, int hd, int n_seqs, int max_len,
                        const DecodeAttnPlan& p, float* part, void* out, hipStream_t st,
                        int pack_nb = 0);
+// fp32 attention rows (decode rows when pos != NULL: row m is sequence m at
+// position pos[m]; else row m is position m % T of sequence m / T at cache slot
+// (m / T) * slot_mul); k_len positions of cache per sequence and kv head.
+hipError_t attn_rows_f32(const float* q, const float* kc, const float* vc, const int32_t* pos,
+                         int rows, int T, int slot_mul, int H, int n_kv, int hd, int k_len,
+                         float* out, hipStream_t st);
 // Causal attention over N sequences of T rows: q act [N*T, H*hd]; K in cache
 // layout [n][n_kv][k_len][hd] (sequence n at slot n*k_stride_seq), Vt
 // [n][n_kv][hd][T] (bf16 path) or V in cache layout (fp32 path).  out act [N*T, H*hd].
