@@ -116,9 +116,10 @@ int grpo_model_destroy(grpo_model* m);
 /* Decode copy of the projections (bf16 models).  A decode step multiplies a
  * few rows by every weight matrix (Alg. 1, sampling step), so it streams the
  * weights from HBM once per step; the decode GEMM reads them from a copy stored
- * in MFMA fragment order (16 rows x 32 columns as 1 KB in lane order, blocks of
- * 16 rows consecutive along the columns; gate and up blocks alternate) so that
- * every load is 1 KB of contiguous memory.
+ * in MFMA fragment order (16 rows x 32 columns as 1 KB in lane order; the
+ * fragments of all 16-row blocks at one 32-column step consecutive, the steps in
+ * column order; gate and up blocks alternate) so that every load is 1 KB of
+ * contiguous memory.
  * grpo_decode_weights_bytes: bytes of that copy (0 for fp32 models or an
  * invalid config).
  * grpo_model_pack_decode: writes the copy of the handle's current weights into

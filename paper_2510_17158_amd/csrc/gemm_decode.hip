@@ -10,10 +10,12 @@
 // Fragment order.  The A operand of one MFMA is 16 rows x 32 k, lane l holding
 // row l & 15, elements 8 (l >> 4) .. 8 (l >> 4) + 7: 64 lanes x 16 bytes.  The
 // decode copy of a weight matrix stores each such fragment as 1 KB in lane order,
-// fragments of a 16-row block consecutive along k ([N/16][K/32][64][8]), so every
-// weight load instruction of a wave reads 1 KB of contiguous memory (a row-major
-// matrix gives 64-byte pieces of 16 rows per instruction, measurably slower to
-// stream).  The activations entering a decode GEMM are written by their producer
+// k-major: the fragments of all 16-row blocks at one 32-wide k step are
+// consecutive ([K/32][N/16][64][8]).  Every weight load instruction of a wave
+// reads 1 KB of contiguous memory (a row-major matrix gives 64-byte pieces of 16
+// rows per instruction, measurably slower to stream), and the workgroups, which
+// advance along k at about the same pace, read neighbouring memory at any moment
+// (measured 4-13% faster streaming than row-block-major fragments).  The activations entering a decode GEMM are written by their producer
 // (RMSNorm, attention, the SwiGLU epilogue below) in the same order with the
 // batch as the row ([K/32][nb/16][64][8], nb = padded batch), so they too arrive
 // in 1 KB contiguous loads.
@@ -45,7 +47,7 @@ constexpr int KGRAN = 128;             // k granularity of a split (4 waves x 32
 
 struct DArgs {
   const bf16_t* X;    // fragment order [K/32][NB/16]
-  const bf16_t* W;    // fragment order [N/16][K/32]
+  const bf16_t* W;    // fragment order [K/32][N/16]
   int B, N, K, kper, tiles;
   float* out_f32; bf16_t* out_act; int ld_out;
 };
@@ -56,7 +58,7 @@ struct DArgs {
     const int i_ = min((i), nst - 1);                                           \
     _Pragma("unroll") for (int rb = 0; rb < RB; ++rb)                           \
         wr[S][rb] = __builtin_nontemporal_load(                                 \
-            (const u32x4_t*)(wp[rb] + (size_t)i_ * (4 * FRAG)));                \
+            (const u32x4_t*)(wp[rb] + (size_t)i_ * wstep));                     \
     _Pragma("unroll") for (int j = 0; j < NJ; ++j)                              \
         xr[S][j] = *(const u32x4_t*)(xp + (size_t)i_ * (4 * NJ * FRAG) + j * FRAG); \
   } while (0)
@@ -82,15 +84,16 @@ void k_gemm_decode(DArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, g = lane >> 4;
   const int tile = blockIdx.x % a.tiles, ks = blockIdx.x / a.tiles;
-  const int KT = a.K / 32;
+  const int NR = a.N / 16;                             // 16-row blocks
   const int kt0 = ks * (a.kper / 32) + wave;           // this wave's first k step
+  const size_t wstep = (size_t)4 * NR * FRAG;          // a wave's next k step (4 later)
   const int nst = a.kper / KGRAN;                      // steps per wave
 
   // fragment rows past the end repeat the last one (their outputs are never written)
   const bf16_t* wp[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
-    wp[rb] = a.W + ((size_t)min(tile * RB + rb, a.N / 16 - 1) * KT + kt0) * FRAG + lane * 8;
+    wp[rb] = a.W + ((size_t)kt0 * NR + min(tile * RB + rb, NR - 1)) * FRAG + lane * 8;
   // batch rows past B hold whatever the producer left there: MFMA columns are
   // independent and those columns are never written
   const bf16_t* xp = a.X + (size_t)kt0 * NJ * FRAG + lane * 8;
@@ -194,15 +197,15 @@ hipError_t launch_nb(const DArgs& a, int epi, int grid, const char* name, hipStr
 }
 
 // One thread per 16-byte piece of the fragment-order copy: piece u is lane
-// u % 64 of fragment (R, kt) = (u / 64 / KT, u / 64 % KT).
+// u % 64 of fragment (kt, R) = (u / 64 / NR, u / 64 % NR).
 __global__ __launch_bounds__(256) void k_pack_frag(PackSrc s, int N, int K, bf16_t* __restrict__ dst) {
   const size_t u = (size_t)blockIdx.x * 256 + threadIdx.x;
-  const int KT = K / 32;
-  const size_t total = (size_t)N / 16 * KT * 64;
+  const int NR = N / 16;
+  const size_t total = (size_t)NR * (K / 32) * 64;
   if (u >= total) return;
   const int l = (int)(u % 64);
   const size_t f = u / 64;
-  const int kt = (int)(f % KT), R = (int)(f / KT);
+  const int R = (int)(f % NR), kt = (int)(f / NR);
   const int k = kt * 32 + 8 * (l >> 4);
   const bf16_t* row;
   if (s.interleave) {
