@@ -28,10 +28,10 @@ BF16_PEAK_TFLOPS = 2500.0
 # (7B shape, contexts 3073..3104), each counter scaled by what it reads for a 1 GiB
 # device copy.  Valid only for the kernel source it was measured on.
 ATTN_TRAFFIC = {
-    "source": "paper_2510_17158_amd/csrc/attention.hip",
-    "sha256": "903fde8dfb7e2ae82f5f47b4e1f0ed5accb5fabb24702de93b0d8b4d3f5a98e7",
-    "fetch_kib": 395998.8, "fetch_scale": 2.0,
-    "write_kib": 570.0, "write_scale": 1.0,
+    "source": "paper_2510_17158_amd/csrc/attn_decode.hip",
+    "sha256": "455d42e51d54f2a0a5b9c2743986dd0e777444b1f89bc3b3da6c564653318035",
+    "fetch_kib": 409178.6, "fetch_scale": 2.0,
+    "write_kib": 512.5, "write_scale": 1.0,
     "algorithmic_bytes": 64 * 3088.5 * 4096,
 }
 
