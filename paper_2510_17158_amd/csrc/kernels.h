@@ -40,7 +40,7 @@ struct EpiArgs {
 
 // ---- decode GEMM: Y[B, N] = X[B, K] . W[N, K]^T for B <= 128 (bf16 MFMA) ----
 // Operands in fragment order: X [K/32][nb/16][64][8] (act_frag_index, nb =
-// decode_nb(B)), W [N/16][K/32][64][8] (pack_frag).  epi is EPI_PARTIAL
+// decode_nb(B)), W [K/32][N/16][64][8] (pack_frag).  epi is EPI_PARTIAL
 // (out_f32 [splits][B][ld_out] row-major) or EPI_SWIGLU (W = pack_frag of
 // (gate, up) interleaved by 16-row blocks, N = 2 d_ffn, out_act = silu(gate) * up
 // in fragment order [nb][ld_out = d_ffn], never split).  N % 16 == 0, K % 128 == 0.
@@ -54,7 +54,7 @@ struct DecodePlan {
 DecodePlan decode_plan(int B, int N, int K, int epi, int target_wgs, int max_splits = kMaxSplits);
 hipError_t gemm_decode_bf16(const uint16_t* Xf, int B, const uint16_t* Wf, int N, int K, int epi,
                             EpiArgs ep, const DecodePlan& p, hipStream_t st);
-// Fragment-order copy [N/16][K/32][64][8] of N row-major bf16 rows of length K:
+// Fragment-order copy [K/32][N/16][64][8] of N row-major bf16 rows of length K:
 // row n from w[0] (n < n1), w[1] (n1 <= n < n2) or w[2]; with interleave, the
 // 16-row blocks of w[0] and w[1] alternate (w[0] block i is fragment row 2i).
 struct PackSrc {
