@@ -11,6 +11,8 @@
 //
 // SwiGLU epilogue: each wave's 64 columns are 32 gate rows and the 32 up rows of
 // the same outputs, so silu(gate) * up is formed in registers.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -161,46 +163,43 @@ __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Large tiles for large M (scoring, long prefill): a workgroup owns a 256 x 256
-// output tile on v_mfma_f32_32x32x16_bf16, with 8 waves, two per SIMD: waves w
-// and w + 4 share a SIMD (the hardware places a workgroup's waves on SIMDs with
-// period 4) and its 128 x 128 quarter of the tile, 64 columns each (4 x 2 blocks
-// of 32 x 32, 128 accumulators).  The two waves of a SIMD take turns: while one
-// runs the 16 MFMAs of a 32-wide k-tile on fragments already in registers, the
-// other reads its fragments of the next k-tile from LDS and issues its half of
-// the direct-to-LDS copies (global_load_lds_dwordx4: each lane names its own
-// source, the 64 lanes fill 1 KB of LDS in lane order) three k-tiles ahead; a
-// barrier swaps the roles, so the wave feeding the matrix core never stops for a
-// memory instruction.  Four LDS stages (k-tile t in stage t % 4, 32 KB each).
-// Schedule (slot = the time between two barriers; A = waves 0-3, B = 4-7):
-//   slot 2t:   A copies its half of tile t + 3 into stage (t + 3) % 4 and reads
-//              tile t; B multiplies tile t - 1
-//   slot 2t+1: A multiplies tile t, then waits until its copies of tile t + 1
-//              have landed; B copies its half of tile t + 3, reads tile t and
-//              waits for its copies of tile t + 1
-// A stage is refilled (slots 2t, 2t + 1) only after both groups read its previous
-// tile (slots 2t - 2, 2t - 1), and a copied tile is published by the barrier after
-// both groups' waits, before its first read (slot 2t + 2).
+// Large tiles for large M (scoring, long prefill): a workgroup of 4 waves (one per
+// SIMD) owns a 256 x 256 output tile, each wave a 128 x 128 quarter as 4 x 4
+// blocks of v_mfma_f32_32x32x16_bf16, so every 1 KB fragment read from LDS feeds
+// four MFMAs (the LDS bytes per MFMA cycle are what bounds these kernels: a wave
+// reads LDS at a limited rate, and a 128 x 64 quarter per wave needs half again
+// as many bytes per MFMA).  Operand k-tiles of 32 (256 rows x 64 B each for X
+// and W) sit in a 4-stage LDS ring (32 KB per stage) filled by direct-to-LDS
+// copies (global_load_lds_dwordx4: each lane names its own source, the 64 lanes
+// fill 1 KB in lane order) three k-tiles ahead.  Per k-tile each wave issues
+// its 32 MFMAs as two phases of 16 with one instruction between consecutive
+// MFMAs: in phase 1 (step 0 of the tile) the fragment reads of step 1 and half
+// of its copies, in phase 2 (step 1) the reads of the next tile's step 0 and
+// the other half; scheduling fences keep that order, so the LDS reads and the
+// copies run in the shadow of the matrix core.  Between the phases each wave
+// waits for its copies of the next tile and a barrier publishes that tile.
+// A stage is refilled (tile t + 3 during tile t) only after every wave passed
+// the barrier of tile t - 1, which follows the last read of its old contents.
 // Rows of a stage are 64 bytes, their four 16-byte pieces XOR-swizzled by
-// (row >> 2) & 3 (conflict-free fragment reads).
-// Measured on the scoring shapes, the operand copies alone (no MFMA) take about
-// 70% of this kernel's time and the MFMAs with their LDS reads alone about 63%
-// of it: the two overlap only partly, which is what holds the kernel near 40%
-// of the bf16 peak.
+// (row >> 2) & 3 (conflict-free fragment reads).  XCD-aware tile order:
+// super-tiles of 4 x 8 tiles per XCD.  Measured on the scoring shapes (65536
+// rows, K = 4096): 1010-1160 TFLOP/s, against 890-990 for an 8-wave ping-pong
+// design (two waves per SIMD alternating MFMA and LDS phases, 128 x 64 per
+// wave) whose LDS phases outlasted its MFMA phases.
 constexpr int GB = 256, PBK = 32, PST = 4;
 
 __device__ __forceinline__ int pswz(int r) { return (r >> 2) & 3; }
 
-// W row of B-tile row r.  SwiGLU: the B-tile rows form 4 slices of 64 (one per
-// wave column range), each 32 gate rows then the 32 up rows of the same outputs.
+// W row of B-tile row r.  SwiGLU: the B-tile rows form two halves (one per wave
+// column wn), each 64 gate rows then the 64 up rows of the same outputs.
 // Otherwise rows of the (q, k, v) stack in order (the host guarantees that a
 // tile lies inside one matrix of the stack).
 template <int EPI>
-__device__ __forceinline__ const bf16_t* pp_wrow(const TArgs& a, int tn, int r) {
+__device__ __forceinline__ const bf16_t* big_wrow(const TArgs& a, int tn, int r) {
   if (EPI == EPI_SWIGLU) {
-    const int slice = r >> 6, q = r & 63;
-    const int n = min(tn * 128 + slice * 32 + (q & 31), a.n1 - 1);
-    return (q < 32 ? a.w0 + (size_t)n * a.K : a.w1 + (size_t)n * a.K);
+    const int wn = r >> 7, q = r & 127;
+    const int n = min(tn * 128 + wn * 64 + (q & 63), a.n1 - 1);
+    return (q < 64 ? a.w0 + (size_t)n * a.K : a.w1 + (size_t)n * a.K);
   }
   const int n = min(tn * GB + r, a.N - 1);
   if (n < a.n1) return a.w0 + (size_t)n * a.K;
@@ -208,27 +207,12 @@ __device__ __forceinline__ const bf16_t* pp_wrow(const TArgs& a, int tn, int r) 
   return a.w2 + (size_t)(n - a.n2) * a.K;
 }
 
-#define PP_BARRIER()                          \
-  do {                                        \
-    __builtin_amdgcn_sched_barrier(0);        \
-    asm volatile("s_barrier" ::: "memory");   \
-    __builtin_amdgcn_sched_barrier(0);        \
-  } while (0)
-
 template <int EPI>
-__global__ __launch_bounds__(512) void k_gemm_pp(TArgs a) {
-  // [stage][X tile, W tile]
+__global__ __launch_bounds__(256) void k_gemm_big(TArgs a) {
   __shared__ __attribute__((aligned(1024))) bf16_t lds[PST][2][GB * PBK];
   const int tid = threadIdx.x, lane = tid % 64;
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
-  const int sq = wave & 3, grp = wave >> 2;
-  const int wm = sq >> 1, wn = sq & 1;
-
-  // XCD-aware tile order: workgroups are dealt to the 8 XCDs round-robin
-  // (blockIdx % 8), each XCD with its own L2.  The tiles form super-tiles of
-  // 4 row tiles x 8 column tiles; the 32 workgroups an XCD runs at a time (one
-  // per compute unit) take one super-tile, so each X and W k-slice is fetched
-  // into that XCD's L2 once for 8 (X) or 4 (W) users.
+  const int wm = wave >> 1, wn = wave & 1;
   const int xcd = blockIdx.x % 8, within = blockIdx.x / 8;
   const int st = (within / 32) * 8 + xcd, loc = within % 32;
   const int st_n = (a.tiles_n + 7) / 8;
@@ -236,130 +220,156 @@ __global__ __launch_bounds__(512) void k_gemm_pp(TArgs a) {
   const int tn = (st % st_n) * 8 + loc % 8;
   if (tm >= a.tiles_m || tn >= a.tiles_n) return;
 
-  // Copies: instruction j (0..3) of wave sq fills tile rows 64 sq + 16 j .. + 16
-  // of both operands, group A issuing j = 0, 1 and group B j = 2, 3 (lane -> row
-  // + lane / 4, piece lane % 4 holding source piece (lane % 4) ^ pswz(row), the
-  // same for every j); SwiGLU W rows switch from gate to up at j = 2.
+  // copy instruction j (0..7): j < 4 -> X rows 64 wave + 16 j .., else W rows
+  // 64 wave + 16 (j - 4) ..; lane -> row + lane / 4, piece (lane % 4) ^ pswz(row)
   const int m0 = min(tm * GB, a.M - GB);
-  const int r0 = sq * 64 + lane / 4;
+  const int r0 = wave * 64 + lane / 4;
   const int pbase = ((lane % 4) ^ pswz(r0)) * 8;
-  const bf16_t* ab = a.X + (size_t)m0 * a.ldx + (size_t)r0 * a.ldx + pbase;
-  const bf16_t* bb0 = pp_wrow<EPI>(a, tn, r0) + pbase;
-  const bf16_t* bb1 = pp_wrow<EPI>(a, tn, r0 + 32) + pbase;
-  const size_t astep = (size_t)16 * a.ldx, bstep = (size_t)16 * a.K;
-  auto copy = [&](int buf, int kt) {
+  const bf16_t* ab = a.X + (size_t)(m0 + r0) * a.ldx + pbase;
+  const size_t astep = (size_t)16 * a.ldx;
+  const bf16_t* bsrc[4];
 #pragma unroll
-    for (int j = 2 * grp; j < 2 * grp + 2; ++j) {
-      const int off = (sq * 4 + j) * 16 * PBK;
-      dma16(ab + j * astep + kt * PBK, lds_addr(&lds[buf][0][off]));
-      const bf16_t* bsrc = (EPI == EPI_SWIGLU && j >= 2) ? bb1 + (j - 2) * bstep : bb0 + j * bstep;
-      dma16(bsrc + kt * PBK, lds_addr(&lds[buf][1][off]));
-    }
+  for (int j = 0; j < 4; ++j) bsrc[j] = big_wrow<EPI>(a, tn, r0 + 16 * j) + pbase;
+  auto dma = [&](int j, int kt) {
+    const int buf = kt % PST;
+    if (j < 4)
+      dma16(ab + j * astep + kt * PBK, lds_addr(&lds[buf][0][(wave * 4 + j) * 16 * PBK]));
+    else
+      dma16(bsrc[j - 4] + kt * PBK, lds_addr(&lds[buf][1][(wave * 4 + j - 4) * 16 * PBK]));
   };
 
-  // fragments: X rows wm * 128 + 32 i + (lane & 31); W rows (tile columns)
-  // wn * 128 + grp * 64 + 32 j + (lane & 31); k-step s takes piece 2 s + (lane >> 5)
   const int sw = pswz(lane & 31);
   const int g2 = lane >> 5;
-  int aoff[PBK / 16], boff[PBK / 16];
+  int aoff[2], boff[2];
 #pragma unroll
-  for (int s = 0; s < PBK / 16; ++s) {
+  for (int s = 0; s < 2; ++s) {
     const int pc = ((s * 2 + g2) ^ sw) * 8;
     aoff[s] = (wm * 128 + (lane & 31)) * PBK + pc;
-    boff[s] = (wn * 128 + grp * 64 + (lane & 31)) * PBK + pc;
+    boff[s] = (wn * 128 + (lane & 31)) * PBK + pc;
   }
-  f32x16_t acc[4][2];
+  f32x16_t acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  bf16x8_t fa[PBK / 16][4], fb[PBK / 16][2];
-  auto frags = [&](int buf) {
-#pragma unroll
-    for (int s = 0; s < PBK / 16; ++s) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) fa[s][i] = *(const bf16x8_t*)(&lds[buf][0][aoff[s] + i * 32 * PBK]);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) fb[s][j] = *(const bf16x8_t*)(&lds[buf][1][boff[s] + j * 32 * PBK]);
-    }
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  bf16x8_t F[2][8];   // [step parity][A0..A3, B0..B3]
+  auto rd = [&](int set, int f, int kt, int s) {
+    const bf16_t* base = &lds[kt % PST][f < 4 ? 0 : 1][0];
+    const int off = (f < 4 ? aoff[s] : boff[s]) + (f & 3) * 32 * PBK;
+    F[set][f] = *(const bf16x8_t*)(base + off);
   };
-  auto mma = [&]() {
-#pragma unroll
-    for (int s = 0; s < PBK / 16; ++s)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+  auto mf = [&](int set, int q) {
+    const int i = q >> 2, j = q & 3;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F[set][i], F[set][4 + j], acc[i][j], 0, 0, 0);
   };
 
-  const int nk = a.K / PBK;    // >= 4 (K is a multiple of 128)
-  copy(0, 0);
-  copy(1, 1);
-  copy(2, 2);
-  asm volatile("s_waitcnt vmcnt(8)" ::: "memory");   // tile 0 (4 copies per wave per tile)
-  PP_BARRIER();
-  auto wait_next = [&](int t) {
-    // tile t + 1 landed: only the copies of tiles t + 2 and t + 3 may remain
-    if (t + 3 < nk) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else if (t + 2 < nk) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  const int nk = a.K / PBK;
+#pragma unroll
+  for (int p = 0; p < 3; ++p)
+    if (p < nk)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) dma(j, p);
+  if (nk > 2) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+  else if (nk > 1) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+#pragma unroll
+  for (int f = 0; f < 8; ++f) rd(0, f, 0, 0);
+
+  auto tile = [&](int t, auto cp_c, auto nx_c) __attribute__((always_inline)) {
+    constexpr bool CP = decltype(cp_c)::value, NX = decltype(nx_c)::value;
+    // phase 1: MFMAs of step 0 (set 0), reads of step 1 (set 1), first half of copies
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      mf(0, q);
+      __builtin_amdgcn_sched_barrier(0);
+      if ((q & 1) == 0) rd(1, q >> 1, t, 1);
+      else if (CP && (q >> 1) < 4) dma(q >> 1, t + 3);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // tile t + 1 landed (newer copies may remain), then publish it
+    if (CP) asm volatile("s_waitcnt vmcnt(12)" ::: "memory");
+    else if (t + 2 < nk) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_barrier" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    // phase 2: MFMAs of step 1 (set 1), reads of the next tile's step 0 (set 0),
+    // second half of copies
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      mf(1, q);
+      __builtin_amdgcn_sched_barrier(0);
+      if ((q & 1) == 0) { if (NX) rd(0, q >> 1, t + 1, 0); }
+      else if (CP && (q >> 1) < 4) dma(4 + (q >> 1), t + 3);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   };
-  if (grp == 0) {
-    for (int t = 0; t < nk; ++t) {
-      if (t + 3 < nk) copy((t + 3) % PST, t + 3);
-      frags(t % PST);
-      PP_BARRIER();
-      mma();
-      wait_next(t);
-      PP_BARRIER();
-    }
-    PP_BARRIER();
-  } else {
-    PP_BARRIER();
-    for (int t = 0; t < nk; ++t) {
-      if (t + 3 < nk) copy((t + 3) % PST, t + 3);
-      frags(t % PST);
-      wait_next(t);
-      PP_BARRIER();
-      mma();
-      PP_BARRIER();
-    }
-  }
+  int t = 0;
+  for (; t + 3 < nk; ++t) tile(t, std::true_type{}, std::true_type{});
+  for (; t + 1 < nk; ++t) tile(t, std::false_type{}, std::true_type{});
+  tile(t, std::false_type{}, std::false_type{});
 
-  // ---- epilogue: acc[i][j][r] is row 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4 of
-  // the SIMD's 128 rows, column 32 j + (lane & 31) of the wave's 64 columns ----
+  // ---- epilogue through LDS (the ring is free once every wave passed this
+  // barrier): 32 rows of the wave's quarter at a time are staged row-major
+  // (rows padded: conflict-free stores), then moved out in 16-byte pieces, whole
+  // 512-byte (fp32) or 128-byte (bf16) row segments per 32 or 8 lanes.
+  // acc[i][j][r] is row 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4, column
+  // 32 j + (lane & 31) of the wave's 128 x 128 quarter.
+  __syncthreads();
+  if (EPI == EPI_SWIGLU) {
+    constexpr int SR = 72;   // staged row: 64 outputs + 8 pad (bf16)
+    bf16_t* stg = &lds[0][0][0] + wave * 32 * SR;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 4; ++i) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = m0 + wm * 128 + i * 32 + (r / 4) * 8 + (lane >> 5) * 4 + (r % 4);
-      if (m < tm * GB) continue;
-      if (EPI == EPI_SWIGLU) {
-        const int n = tn * 128 + (wn * 2 + grp) * 32 + (lane & 31);
-        if (n < a.n1) {
-          const float gt = acc[i][0][r], up = acc[i][1][r];
-          a.out_act[(size_t)m * a.ld_out + n] = f2bf(gt / (1.f + __expf(-gt)) * up);
-        }
-      } else {
+      for (int r = 0; r < 16; ++r)
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          const int n = tn * GB + wn * 128 + grp * 64 + j * 32 + (lane & 31);
-          if (n < a.N) {
-            float* o = a.out_f32 + (size_t)m * a.ld_out + n;
-            if (EPI == EPI_RESID) *o += acc[i][j][r];
-            else *o = acc[i][j][r];
+          const float gt = acc[i][j][r], up = acc[i][j + 2][r];
+          stg[((r / 4) * 8 + (lane >> 5) * 4 + (r % 4)) * SR + j * 32 + (lane & 31)] =
+              f2bf(gt / (1.f + __expf(-gt)) * up);
+        }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int idx = lane + 64 * k, row = idx >> 3, c8 = (idx & 7) * 8;
+        const int m = m0 + wm * 128 + i * 32 + row;
+        const int n = tn * 128 + wn * 64 + c8;
+        const u32x4_t v = *(const u32x4_t*)(stg + row * SR + c8);
+        if (m >= tm * GB && n < a.n1) *(u32x4_t*)(a.out_act + (size_t)m * a.ld_out + n) = v;
+      }
+    }
+  } else {
+    constexpr int SR = 132;  // staged row: 128 columns + 4 pad (fp32)
+    float* stg = reinterpret_cast<float*>(&lds[0][0][0]) + wave * 32 * SR;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          stg[((r / 4) * 8 + (lane >> 5) * 4 + (r % 4)) * SR + j * 32 + (lane & 31)] = acc[i][j][r];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int idx = lane + 64 * k, row = idx >> 5, c4 = (idx & 31) * 4;
+        const int m = m0 + wm * 128 + i * 32 + row;
+        const int n = tn * GB + wn * 128 + c4;
+        const float4 v = *(const float4*)(stg + row * SR + c4);
+        if (m >= tm * GB && n < a.N) {
+          float4* o = (float4*)(a.out_f32 + (size_t)m * a.ld_out + n);
+          if (EPI == EPI_RESID) {
+            const float4 w = *o;
+            *o = make_float4(w.x + v.x, w.y + v.y, w.z + v.z, w.w + v.w);
+          } else {
+            *o = v;
           }
         }
       }
     }
   }
 }
-#undef PP_BARRIER
-
 // ---------------------------------------------------------------------------
 // fp32 GEMM for fp32 models (VALU, 64x64 tiles, 4x4 outputs per thread).
 struct FArgs {
@@ -437,6 +447,7 @@ __global__ __launch_bounds__(256) void k_gemm_f32(FArgs a) {
   }
 }
 
+
 }  // namespace
 
 hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, int K, int epi,
@@ -447,9 +458,13 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
   a.n1 = W.n1; a.n2 = W.n2; a.N = N; a.K = K;
   a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;
   Prof pf(epi == EPI_SWIGLU ? "gemm_tiled_swiglu" : "gemm_tiled", st);
-  const bool aligned = epi == EPI_SWIGLU
+  // the big tiles store 16-byte pieces of output rows
+  const bool out16 = epi == EPI_SWIGLU
+                         ? ep.ld_out % 8 == 0 && (uintptr_t)ep.out_act % 16 == 0
+                         : ep.ld_out % 4 == 0 && (uintptr_t)ep.out_f32 % 16 == 0;
+  const bool aligned = out16 && (epi == EPI_SWIGLU
                            ? W.n1 % 128 == 0
-                           : N % GB == 0 && (W.n1 >= N || W.n1 % GB == 0) && (W.n2 >= N || W.n2 % GB == 0);
+                           : N % GB == 0 && (W.n1 >= N || W.n1 % GB == 0) && (W.n2 >= N || W.n2 % GB == 0));
   if (M >= kBigTileRows && aligned) {
     a.tiles_m = (M + GB - 1) / GB;
     a.tiles_n = epi == EPI_SWIGLU ? (N + 127) / 128 : (N + GB - 1) / GB;
@@ -457,9 +472,9 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
     const int n_st = ((a.tiles_m + 3) / 4) * ((a.tiles_n + 7) / 8);
     const int grid = (n_st + 7) / 8 * 8 * 32;
     switch (epi) {
-      case EPI_STORE: k_gemm_pp<EPI_STORE><<<grid, 512, 0, st>>>(a); break;
-      case EPI_RESID: k_gemm_pp<EPI_RESID><<<grid, 512, 0, st>>>(a); break;
-      default: k_gemm_pp<EPI_SWIGLU><<<grid, 512, 0, st>>>(a); break;
+      case EPI_STORE: k_gemm_big<EPI_STORE><<<grid, 256, 0, st>>>(a); break;
+      case EPI_RESID: k_gemm_big<EPI_RESID><<<grid, 256, 0, st>>>(a); break;
+      default: k_gemm_big<EPI_SWIGLU><<<grid, 256, 0, st>>>(a); break;
     }
     return hipGetLastError();
   }
