@@ -28,12 +28,12 @@
 // in-flight register is ever copied (a copy would make the wave wait for the
 // load).  Weight loads are non-temporal: each weight byte is used once per step,
 // and keeping it out of the way of the activations (read by every workgroup)
-// measured faster.  At the end the four waves' accumulators are added in a fixed
-// order ((w0 + w2) + (w1 + w3)) through LDS and written out: split-K partial
-// products [split][B][N] in fp32 for the consuming kernel (RMSNorm with the
-// residual add, or RoPE) to add in split order, or silu(gate) * up rounded to
-// bf16 in fragment order for the down projection.  No atomics; the result does
-// not depend on timing.
+// measured faster.  At the end the four waves' accumulators go to LDS (one
+// barrier) and are added in a fixed order ((w0 + w2) + (w1 + w3)) as they are
+// written out: split-K partial products [split][B][N] in fp32 for the
+// consuming kernel (RMSNorm with the residual add, or RoPE) to add in split
+// order, or silu(gate) * up rounded to bf16 in fragment order for the down
+// projection.  No atomics; the result does not depend on timing.
 #include "common.h"
 #include "kernels.h"
 
@@ -78,7 +78,7 @@ void k_gemm_decode(DArgs a) {
   constexpr int NJ = NB / 16;            // MFMA batch blocks
   constexpr int ROWS = 16 * RB;          // weight rows of the tile
   constexpr int CT = ROWS + 4;           // padded row of the [batch][row] LDS tile
-  __shared__ __attribute__((aligned(16))) float red[2 * NB * CT];
+  __shared__ __attribute__((aligned(16))) float red[4 * NB * CT];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -124,36 +124,22 @@ void k_gemm_decode(DArgs a) {
   for (int u = 0; u < D - 1; ++u)
     if (u < rem) DG_MMA(u);
 
-  // ---- fixed-order sum of the four waves' products in LDS [batch][row] ----
+  // ---- the four waves' products in LDS [wave][batch][row], one barrier; the
+  // epilogue adds them in a fixed order ((w0 + w2) + (w1 + w3)) ----
   // C layout of the 16x16 MFMA: row 4 g + v, column r16.
-  float* r0 = red;
-  float* r1 = red + NB * CT;
-  auto put = [&](float* dst) {
+  {
+    float* dst = red + wave * NB * CT;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
         *(f32x4_t*)(dst + (16 * j + r16) * CT + rb * 16 + 4 * g) = acc[rb][j];
-  };
-  auto add = [&](const float* src) {
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int j = 0; j < NJ; ++j)
-        acc[rb][j] += *(const f32x4_t*)(src + (16 * j + r16) * CT + rb * 16 + 4 * g);
-  };
-  if (wave >= 2) put(wave == 2 ? r0 : r1);
-  __syncthreads();
-  if (wave < 2) {
-    add(wave == 0 ? r0 : r1);
-    if (wave == 1) put(r1);
   }
   __syncthreads();
-  if (wave == 0) {
-    add(r1);
-    put(r0);
-  }
-  __syncthreads();
+  auto val = [&](int b, int r) {
+    const int o = b * CT + r;
+    return (red[o] + red[2 * NB * CT + o]) + (red[NB * CT + o] + red[3 * NB * CT + o]);
+  };
 
   // ---- epilogue: consecutive threads take consecutive output columns ----
   if (EPI == EPI_SWIGLU) {
@@ -164,7 +150,7 @@ void k_gemm_decode(DArgs a) {
       const int n = tile * HO + o;
       if (b < a.B && n < a.ld_out) {
         const int rg = (o >> 4) * 32 + (o & 15);
-        const float gt = r0[b * CT + rg], up = r0[b * CT + rg + 16];
+        const float gt = val(b, rg), up = val(b, rg + 16);
         const float sg = gt / (1.f + __expf(-gt));
         a.out_act[act_frag_index(b, n, NB)] = f2bf(sg * up);
       }
@@ -174,7 +160,7 @@ void k_gemm_decode(DArgs a) {
     for (int i = tid; i < ROWS * NB; i += NT) {
       const int r = i % ROWS, b = i / ROWS;
       const int n = tile * ROWS + r;
-      if (b < a.B && n < a.N) out[(size_t)b * a.ld_out + n] = r0[b * CT + r];
+      if (b < a.B && n < a.N) out[(size_t)b * a.ld_out + n] = val(b, r);
     }
   }
 }
