@@ -136,31 +136,44 @@ void k_gemm_decode(DArgs a) {
         *(f32x4_t*)(dst + (16 * j + r16) * CT + rb * 16 + 4 * g) = acc[rb][j];
   }
   __syncthreads();
-  auto val = [&](int b, int r) {
+  // four consecutive rows r .. r + 3 of batch row b (r a multiple of 4)
+  auto val4 = [&](int b, int r) {
     const int o = b * CT + r;
-    return (red[o] + red[2 * NB * CT + o]) + (red[NB * CT + o] + red[3 * NB * CT + o]);
+    const f32x4_t p0 = *(const f32x4_t*)(red + o), p1 = *(const f32x4_t*)(red + NB * CT + o);
+    const f32x4_t p2 = *(const f32x4_t*)(red + 2 * NB * CT + o);
+    const f32x4_t p3 = *(const f32x4_t*)(red + 3 * NB * CT + o);
+    return (p0 + p2) + (p1 + p3);
   };
 
-  // ---- epilogue: consecutive threads take consecutive output columns ----
+  // ---- epilogue: 16-byte stores, consecutive threads on consecutive columns ----
   if (EPI == EPI_SWIGLU) {
-    // tile rows: gate block 2 o_b then up block 2 o_b + 1 for output block o_b
+    // tile rows: gate block 2 o_b then up block 2 o_b + 1 for output block o_b;
+    // a thread makes 8 consecutive outputs (one 16-byte piece of a fragment row)
     constexpr int HO = ROWS / 2;
-    for (int i = tid; i < HO * NB; i += NT) {
-      const int o = i % HO, b = i / HO;
+    for (int i = tid; i < HO / 8 * NB; i += NT) {
+      const int o = i % (HO / 8) * 8, b = i / (HO / 8);
       const int n = tile * HO + o;
       if (b < a.B && n < a.ld_out) {
         const int rg = (o >> 4) * 32 + (o & 15);
-        const float gt = val(b, rg), up = val(b, rg + 16);
-        const float sg = gt / (1.f + __expf(-gt));
-        a.out_act[act_frag_index(b, n, NB)] = f2bf(sg * up);
+        float y[8];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const f32x4_t gt = val4(b, rg + 4 * h), up = val4(b, rg + 16 + 4 * h);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[4 * h + e] = gt[e] / (1.f + __expf(-gt[e])) * up[e];
+        }
+        u32x4_t w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = (uint32_t)f2bf(y[2 * e]) | ((uint32_t)f2bf(y[2 * e + 1]) << 16);
+        *(u32x4_t*)(a.out_act + act_frag_index(b, n, NB)) = w;
       }
     }
   } else {
     float* out = a.out_f32 + (size_t)ks * a.B * a.ld_out;
-    for (int i = tid; i < ROWS * NB; i += NT) {
-      const int r = i % ROWS, b = i / ROWS;
+    for (int i = tid; i < ROWS / 4 * NB; i += NT) {
+      const int r = i % (ROWS / 4) * 4, b = i / (ROWS / 4);
       const int n = tile * ROWS + r;
-      if (b < a.B && n < a.N) out[(size_t)b * a.ld_out + n] = val(b, r);
+      if (b < a.B && n < a.N) *(f32x4_t*)(out + (size_t)b * a.ld_out + n) = val4(b, r);
     }
   }
 }
