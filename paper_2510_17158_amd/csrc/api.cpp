@@ -274,7 +274,7 @@ size_t decode_scratch(const grpo_config& c, int B) {
 }
 
 // Byte offsets of the decode copy: per layer QKV (rows q, k, v), O, gate/up
-// (16-row blocks interleaved), down; then the LM head.
+// (8 gate rows then the same 8 up rows per 16-row block), down; then the LM head.
 struct DecodeLayout {
   std::vector<size_t> qkv, o, gate_up, down;
   size_t lm_head = 0, total = 0;

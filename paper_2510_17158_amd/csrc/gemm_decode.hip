@@ -21,7 +21,8 @@
 // in 1 KB contiguous loads.
 //
 // Work split: a workgroup of 4 waves owns RB fragment rows (16 RB weight rows;
-// for SwiGLU the gate and up rows of the same outputs alternate by 16-row block)
+// for SwiGLU each 16-row block holds 8 gate rows and the up rows of the same
+// outputs; RB per projection shape evens out the grid over the compute units)
 // and one K range cut into 32-wide steps dealt round-robin to the waves.  Each
 // wave keeps D steps of weight and activation fragments in a register ring that
 // is unrolled at compile time, so loads run D - 1 steps ahead of the MFMAs and no
@@ -73,7 +74,7 @@ struct DArgs {
   } while (0)
 
 template <int NB, int RB, int D, int EPI>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(RB > 4 ? 1 : 2)))
 void k_gemm_decode(DArgs a) {
   constexpr int NJ = NB / 16;            // MFMA batch blocks
   constexpr int ROWS = 16 * RB;          // weight rows of the tile
@@ -147,18 +148,19 @@ void k_gemm_decode(DArgs a) {
 
   // ---- epilogue: 16-byte stores, consecutive threads on consecutive columns ----
   if (EPI == EPI_SWIGLU) {
-    // tile rows: gate block 2 o_b then up block 2 o_b + 1 for output block o_b;
-    // a thread makes 8 consecutive outputs (one 16-byte piece of a fragment row)
+    // 16-row block o_b of the tile: gate rows of outputs 8 o_b .. 8 o_b + 7, then
+    // their up rows; a thread makes those 8 consecutive outputs (one 16-byte
+    // piece of a fragment row)
     constexpr int HO = ROWS / 2;
     for (int i = tid; i < HO / 8 * NB; i += NT) {
       const int o = i % (HO / 8) * 8, b = i / (HO / 8);
       const int n = tile * HO + o;
       if (b < a.B && n < a.ld_out) {
-        const int rg = (o >> 4) * 32 + (o & 15);
+        const int rg = (o >> 3) * 16;
         float y[8];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const f32x4_t gt = val4(b, rg + 4 * h), up = val4(b, rg + 16 + 4 * h);
+          const f32x4_t gt = val4(b, rg + 4 * h), up = val4(b, rg + 8 + 4 * h);
 #pragma unroll
           for (int e = 0; e < 4; ++e) y[4 * h + e] = gt[e] / (1.f + __expf(-gt[e])) * up[e];
         }
@@ -181,9 +183,8 @@ void k_gemm_decode(DArgs a) {
 #undef DG_LOAD
 #undef DG_MMA
 
-template <int NB>
-hipError_t launch_nb(const DArgs& a, int epi, int grid, const char* name, hipStream_t st) {
-  constexpr int RB = decode_rb(NB);
+template <int NB, int RB>
+hipError_t launch_rb(const DArgs& a, int epi, int grid, const char* name, hipStream_t st) {
   constexpr int D = 3;
   if (epi == EPI_SWIGLU) {
     Prof pf(name ? name : "gemm_decode_swiglu", st);
@@ -193,6 +194,20 @@ hipError_t launch_nb(const DArgs& a, int epi, int grid, const char* name, hipStr
     k_gemm_decode<NB, RB, D, EPI_PARTIAL><<<grid, NT, 0, st>>>(a);
   }
   return hipGetLastError();
+}
+
+template <int NB>
+hipError_t launch_nb(const DArgs& a, int epi, int grid, int rb, const char* name, hipStream_t st) {
+  if constexpr (NB >= 128) {
+    return rb == 2 ? launch_rb<NB, 2>(a, epi, grid, name, st) : hipErrorInvalidValue;
+  } else {
+    switch (rb) {
+      case 4: return launch_rb<NB, 4>(a, epi, grid, name, st);
+      case 6: return launch_rb<NB, 6>(a, epi, grid, name, st);
+      case 7: return launch_rb<NB, 7>(a, epi, grid, name, st);
+    }
+    return hipErrorInvalidValue;
+  }
 }
 
 // One thread per 16-byte piece of the fragment-order copy: piece u is lane
@@ -208,9 +223,9 @@ __global__ __launch_bounds__(256) void k_pack_frag(PackSrc s, int N, int K, bf16
   const int k = kt * 32 + 8 * (l >> 4);
   const bf16_t* row;
   if (s.interleave) {
-    // fragment rows alternate: even R = rows of s.w[0], odd R = the same rows of s.w[1]
-    const int n = (R >> 1) * 16 + (l & 15);
-    row = (const bf16_t*)s.w[R & 1] + (size_t)n * K;
+    // fragment row R: rows 8 R .. 8 R + 7 of s.w[0], then the same rows of s.w[1]
+    const int n = R * 8 + (l & 7);
+    row = (const bf16_t*)s.w[(l & 15) >> 3] + (size_t)n * K;
   } else {
     const int n = R * 16 + (l & 15);
     if (n < s.n1) row = (const bf16_t*)s.w[0] + (size_t)n * K;
@@ -224,19 +239,40 @@ __global__ __launch_bounds__(256) void k_pack_frag(PackSrc s, int N, int K, bf16
 
 int decode_nb(int B) { return B <= 16 ? 16 : B <= 32 ? 32 : B <= 64 ? 64 : 128; }
 
+// Split-K factor of a plan: the first divisor of K / KGRAN reaching the target
+// grid (SwiGLU needs complete gate and up sums in one workgroup: never split).
+static int decode_splits(int tiles, int K, int epi, int target_wgs, int max_splits) {
+  const int nchunk = K / KGRAN;
+  int splits = 1;
+  for (int d = 1; epi != EPI_SWIGLU && d <= nchunk && d <= max_splits; ++d) {
+    if (nchunk % d) continue;
+    splits = d;
+    if ((long)tiles * d >= target_wgs) break;
+  }
+  return splits;
+}
+
+// Tile height: of 4, 6 and 7 blocks of 16 rows (2 at nb = 128, for registers),
+// the one whose grid fills the compute units most evenly (workgroups over the
+// next multiple of 256; 4 on ties): QKV at the 7B shape takes 6 (64 tiles x 4
+// splits), the SwiGLU projection 7 (256 tiles), O, down and the LM head 4.
 DecodePlan decode_plan(int B, int N, int K, int epi, int target_wgs, int max_splits) {
   DecodePlan p{};
   p.nb = decode_nb(B);
-  const int rows = 16 * decode_rb(p.nb);
-  p.tiles = (N + rows - 1) / rows;
-  const int nchunk = K / KGRAN;
-  p.splits = 1;
   if (target_wgs <= 0) target_wgs = 512;
-  // SwiGLU needs complete gate and up sums in one workgroup: never split
-  for (int d = 1; epi != EPI_SWIGLU && d <= nchunk && d <= max_splits; ++d) {
-    if (nchunk % d) continue;
-    p.splits = d;
-    if ((long)p.tiles * d >= target_wgs) break;
+  const int blocks = N / 16;
+  const int cands[3] = {4, 6, 7};
+  double best = -1.0;
+  for (int c = 0; c < (p.nb >= 128 ? 1 : 3); ++c) {
+    const int rb = p.nb >= 128 ? 2 : cands[c];
+    const int tiles = (blocks + rb - 1) / rb;
+    const int splits = decode_splits(tiles, K, epi, target_wgs, max_splits);
+    const long wgs = (long)tiles * splits;
+    const double fill = (double)wgs / (double)(((wgs + 255) / 256) * 256);
+    if (fill > best + 1e-9) {
+      best = fill;
+      p.rb = rb; p.tiles = tiles; p.splits = splits;
+    }
   }
   return p;
 }
@@ -244,6 +280,7 @@ DecodePlan decode_plan(int B, int N, int K, int epi, int target_wgs, int max_spl
 hipError_t gemm_decode_bf16(const uint16_t* Xf, int B, const uint16_t* Wf, int N, int K, int epi,
                             EpiArgs ep, const DecodePlan& p, hipStream_t st) {
   if (B < 1 || B > p.nb || p.nb != decode_nb(B) || N % 16 || K % KGRAN || p.splits < 1 ||
+      p.tiles * 16 * p.rb < N ||
       (K / p.splits) % KGRAN || (epi == EPI_SWIGLU && (N % 32 || ep.ld_out != N / 2)))
     return hipErrorInvalidValue;
   DArgs a;
@@ -252,10 +289,10 @@ hipError_t gemm_decode_bf16(const uint16_t* Xf, int B, const uint16_t* Wf, int N
   a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;
   const int grid = p.tiles * p.splits;
   switch (p.nb) {
-    case 16: return launch_nb<16>(a, epi, grid, ep.name, st);
-    case 32: return launch_nb<32>(a, epi, grid, ep.name, st);
-    case 64: return launch_nb<64>(a, epi, grid, ep.name, st);
-    case 128: return launch_nb<128>(a, epi, grid, ep.name, st);
+    case 16: return launch_nb<16>(a, epi, grid, p.rb, ep.name, st);
+    case 32: return launch_nb<32>(a, epi, grid, p.rb, ep.name, st);
+    case 64: return launch_nb<64>(a, epi, grid, p.rb, ep.name, st);
+    case 128: return launch_nb<128>(a, epi, grid, p.rb, ep.name, st);
   }
   return hipErrorInvalidValue;
 }

@@ -42,21 +42,21 @@ struct EpiArgs {
 // Operands in fragment order: X [K/32][nb/16][64][8] (act_frag_index, nb =
 // decode_nb(B)), W [K/32][N/16][64][8] (pack_frag).  epi is EPI_PARTIAL
 // (out_f32 [splits][B][ld_out] row-major) or EPI_SWIGLU (W = pack_frag of
-// (gate, up) interleaved by 16-row blocks, N = 2 d_ffn, out_act = silu(gate) * up
+// (gate, up) interleaved, N = 2 d_ffn, out_act = silu(gate) * up
 // in fragment order [nb][ld_out = d_ffn], never split).  N % 16 == 0, K % 128 == 0.
-constexpr int decode_rb(int nb) { return nb >= 128 ? 2 : 4; }   // 16-row blocks per tile
 int decode_nb(int B);                                           // 16, 32, 64 or 128
 struct DecodePlan {
   int nb;        // padded batch
-  int tiles;     // output tiles of 16 * decode_rb(nb) weight rows
+  int rb;        // 16-row blocks per output tile (2 for nb = 128; else 4, 6 or 7)
+  int tiles;     // output tiles of 16 * rb weight rows
   int splits;    // split-K factor (partial products written)
 };
 DecodePlan decode_plan(int B, int N, int K, int epi, int target_wgs, int max_splits = kMaxSplits);
 hipError_t gemm_decode_bf16(const uint16_t* Xf, int B, const uint16_t* Wf, int N, int K, int epi,
                             EpiArgs ep, const DecodePlan& p, hipStream_t st);
 // Fragment-order copy [K/32][N/16][64][8] of N row-major bf16 rows of length K:
-// row n from w[0] (n < n1), w[1] (n1 <= n < n2) or w[2]; with interleave, the
-// 16-row blocks of w[0] and w[1] alternate (w[0] block i is fragment row 2i).
+// row n from w[0] (n < n1), w[1] (n1 <= n < n2) or w[2]; with interleave, 16-row
+// block i holds rows 8 i .. 8 i + 7 of w[0] and then the same rows of w[1].
 struct PackSrc {
   const void* w[3];
   int n1, n2;
