@@ -205,6 +205,7 @@ hipError_t launch_nb(const DArgs& a, int epi, int grid, int rb, const char* name
       case 4: return launch_rb<NB, 4>(a, epi, grid, name, st);
       case 6: return launch_rb<NB, 6>(a, epi, grid, name, st);
       case 7: return launch_rb<NB, 7>(a, epi, grid, name, st);
+      case 8: return launch_rb<NB, 8>(a, epi, grid, name, st);
     }
     return hipErrorInvalidValue;
   }
@@ -252,24 +253,26 @@ static int decode_splits(int tiles, int K, int epi, int target_wgs, int max_spli
   return splits;
 }
 
-// Tile height: of 4, 6 and 7 blocks of 16 rows (2 at nb = 128, for registers),
-// the one whose grid fills the compute units most evenly (workgroups over the
-// next multiple of 256; 4 on ties): QKV at the 7B shape takes 6 (64 tiles x 4
-// splits), the SwiGLU projection 7 (256 tiles), O, down and the LM head 4.
+// Tile height: of 4, 6, 7 and 8 blocks of 16 rows (2 at nb = 128, for
+// registers), the one whose grid fills the compute units most evenly (workgroups
+// over the next multiple of 256); on ties fewer splits (less partial traffic),
+// then the taller tile (fewer activation reloads).  At the 7B shape: QKV 6 (64
+// tiles x 4 splits), SwiGLU 7 (256 tiles), O and down 4 (64 x 4), LM head 8.
 DecodePlan decode_plan(int B, int N, int K, int epi, int target_wgs, int max_splits) {
   DecodePlan p{};
   p.nb = decode_nb(B);
   if (target_wgs <= 0) target_wgs = 512;
   const int blocks = N / 16;
-  const int cands[3] = {4, 6, 7};
+  const int cands[4] = {4, 6, 7, 8};
   double best = -1.0;
-  for (int c = 0; c < (p.nb >= 128 ? 1 : 3); ++c) {
+  for (int c = 0; c < (p.nb >= 128 ? 1 : 4); ++c) {
     const int rb = p.nb >= 128 ? 2 : cands[c];
     const int tiles = (blocks + rb - 1) / rb;
     const int splits = decode_splits(tiles, K, epi, target_wgs, max_splits);
     const long wgs = (long)tiles * splits;
     const double fill = (double)wgs / (double)(((wgs + 255) / 256) * 256);
-    if (fill > best + 1e-9) {
+    const bool tie = fill > best - 1e-9 && fill < best + 1e-9;
+    if (fill > best + 1e-9 || (tie && (splits < p.splits || (splits == p.splits && rb > p.rb)))) {
       best = fill;
       p.rb = rb; p.tiles = tiles; p.splits = splits;
     }

@@ -47,7 +47,7 @@ struct EpiArgs {
 int decode_nb(int B);                                           // 16, 32, 64 or 128
 struct DecodePlan {
   int nb;        // padded batch
-  int rb;        // 16-row blocks per output tile (2 for nb = 128; else 4, 6 or 7)
+  int rb;        // 16-row blocks per output tile (2 for nb = 128; else 4, 6, 7 or 8)
   int tiles;     // output tiles of 16 * rb weight rows
   int splits;    // split-K factor (partial products written)
 };
