@@ -273,3 +273,37 @@ def test_decode_span_count_does_not_change_results(small):
     err = np.abs(outs[0][0] - outs[1][0]).max()
     say("max |dlogit| between capacities", err)
     assert err <= 1e-3
+
+
+def test_bench_launch_configuration():
+    """The 7B workload's own launch configuration on a 1-layer model of the 7B
+    width: 8 prompts x G 8 = 64 sequences, 2048-token prompts, 2048 sampled tokens
+    (temperature 1), scoring over 4096 positions.  One decode step at context 2049
+    is checked stage-locally against the oracle (the decode GEMM plans at batch 64,
+    single-span attention over 8 kv heads x 64 sequences, the LM head and the
+    sampler over 32000 logits); then the whole rollout runs, and teacher-forced
+    scoring of its sequences (flash attention over 4096 positions, the 256 x 256
+    GEMM tiles over chunks of 16 x 4096 rows) must reproduce every rollout log-prob:
+    both are log_softmax(logits / T) at the sampled token (Eq. (1)), computed by
+    different kernels."""
+    require_gpu()
+    w = truncated(get("7b"), 1)
+    assert (w.n_prompts * w.group, w.prompt_len, w.new_tokens) == (64, 2048, 2048)
+    say("bench launch configuration, 1 layer of the 7B width")
+    host, model = build_model(w.model, w.master_seed, gain_noise=0.1)
+    it = GrpoIteration(w, model, None, synth.make_prompts(w), synth.make_rewards(w),
+                       synth.make_seed(w))
+    it.prefill()
+    _stage_local(w, host, model, it, 1)
+    say("full rollout and scoring")
+    it.decode()
+    it.assemble()
+    it.score()
+    torch.cuda.synchronize()
+    old = it.logp_old.cpu().numpy()
+    new = it.lp_pol.cpu().numpy()
+    assert np.isfinite(old).all() and np.isfinite(new).all()
+    err = float(np.abs(new - old).max())
+    say("rollout vs scoring log-prob err", err, "mean logp", float(old.mean()))
+    assert err <= LOGIT_TOL
+    model.close()
