@@ -57,12 +57,17 @@ def log(*a):
 
 def decode_bytes_per_step(w, ctx_avg: float) -> float:
     """Algorithmic HBM bytes of one decode step: every weight once (embedding rows
-    aside), the KV of every context position once, the new K/V written."""
+    aside), the KV of every context position once, the new K/V written.  With the
+    prompt shared within groups the prompt's KV counts once per group."""
     c = w.model
     es = c.elem_bytes
     weights = (c.n_params() - c.vocab * c.d_model) * es + w.batch * c.d_model * es
     kv_tok = c.kv_bytes_per_token()
-    return weights + w.batch * ctx_avg * kv_tok + w.batch * kv_tok
+    if w.shared_prompt:
+        kv = (w.n_prompts * w.prompt_len + w.batch * (ctx_avg - w.prompt_len)) * kv_tok
+    else:
+        kv = w.batch * ctx_avg * kv_tok
+    return weights + kv + w.batch * kv_tok
 
 
 def score_flops(w) -> float:
@@ -81,7 +86,9 @@ def kernel_bytes(w) -> dict:
     weight byte of the projection once per decode step, plus its activation rows
     read and its product written once (fp32 products, bf16 activations); for
     attn_decode the K and V of every context position of every sequence per
-    layer, context = position + 1."""
+    layer, context = position + 1, or, with the prompt shared within groups,
+    attn_prefix the prompt's K and V once per group and attn_decode every
+    sequence's generated positions."""
     c = w.model
     es = c.elem_bytes
     B, L, d, f, V = w.batch, c.n_layers, c.d_model, c.d_ffn, c.vocab
@@ -89,14 +96,19 @@ def kernel_bytes(w) -> dict:
     n_dec = w.new_tokens - 1
     kv_layer_tok = 2 * kvd * es
     ctx_sum = sum(w.prompt_len + s for s in range(1, n_dec + 1))   # context of decode step s
-    return {
+    out = {
         "gemm_decode_qkv": n_dec * L * ((qd + 2 * kvd) * d * es + B * d * es + B * (qd + 2 * kvd) * 4),
         "gemm_decode_o": n_dec * L * (d * qd * es + B * qd * es + B * d * 4),
         "gemm_decode_swiglu": n_dec * L * (2 * f * d * es + B * d * es + B * f * es),
         "gemm_decode_down": n_dec * L * (d * f * es + B * f * es + B * d * 4),
         "gemm_decode_lm_head": n_dec * (V * d * es + B * d * es + B * V * 4),
-        "attn_decode": L * B * kv_layer_tok * ctx_sum,
     }
+    if w.shared_prompt:
+        out["attn_prefix"] = n_dec * L * w.n_prompts * w.prompt_len * kv_layer_tok
+        out["attn_decode"] = L * B * kv_layer_tok * (ctx_sum - n_dec * w.prompt_len)
+    else:
+        out["attn_decode"] = L * B * kv_layer_tok * ctx_sum
+    return out
 
 
 def cpu_baseline(w, host, budget_s: float = 15.0) -> dict:

@@ -12,6 +12,8 @@
  *   grpo_prefill          prompt forward + first sampled token of each group
  *                         member (Alg. 1, sampling step, generation step 0)
  *   grpo_rollout_step     n_steps batched decode steps (Alg. 1, sampling step)
+ *   grpo_rollout_step_grouped  the same, reading each group's shared prompt
+ *                         K/V once per group
  *   grpo_score_sequences  teacher-forced log pi(x_t | c, x_<t) (Eq. 1, KL term)
  *   grpo_advantages       group-normalised rewards w(x) (Alg. 1, normalisation)
  *   grpo_token_loss       clipped-ratio + KL per-token loss, its gradient with
@@ -185,6 +187,31 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
                       const grpo_sampling* s, int32_t* tok_out, float* logp_out,
                       float* logits_dbg, float* hidden_dbg, void* ws, size_t ws_bytes,
                       void* stream);
+
+/* grpo_rollout_step for a batch of groups: rows g*G .. g*G+G-1 are the G
+ * samples of one prompt (Alg. 1 samples G completions per prompt; grpo_prefill
+ * lays them out so), and their cache positions 0 .. prefix_len-1 hold the same
+ * K/V (the prompt, written once per prompt by grpo_prefill into every member's
+ * slot).  Attention reads those positions once per group, from the slot of row
+ * g*G, instead of once per row; each row's later positions come from its own
+ * slot.  Every row must be at pos[b] >= prefix_len on entry (true after
+ * grpo_prefill with prefix_len = Tp), so that no step writes a shared
+ * position; the kernels cut the shared length to min(prefix_len, pos[b] + 1)
+ * over a group's rows, so they never read past a row's own context.  Under
+ * these conditions the results are those of grpo_rollout_step except for the
+ * order of floating-point additions in attention.  Arguments as
+ * grpo_rollout_step, plus
+ *   G           group size, >= 1, dividing B
+ *   prefix_len  shared positions, 0 <= prefix_len <= max_len (0: no sharing)
+ * fp32 models read every row's own cache (same results).  The workspace is the
+ * one grpo_workspace_bytes(GRPO_OP_ROLLOUT) gives.  GRPO_INVALID_ARG for a G or
+ * prefix_len outside these ranges. */
+int grpo_rollout_step_grouped(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
+                              int32_t B, int32_t G, int32_t prefix_len, int32_t* pos, int32_t* tok,
+                              int32_t max_pos, int32_t step0, int32_t n_steps,
+                              const grpo_sampling* s, int32_t* tok_out, float* logp_out,
+                              float* logits_dbg, float* hidden_dbg, void* ws, size_t ws_bytes,
+                              void* stream);
 
 /* Teacher-forced scoring (Eq. 1's log pi and the KL term's reference): for
  * j in [score_from, T): logp_out[n, j - score_from] =

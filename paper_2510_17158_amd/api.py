@@ -63,6 +63,9 @@ _SIGS = {
                             _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "grpo_rollout_step": (_I32, [_VP, _VP, _I32, _I32, _I32, _VP, _VP, _I32, _I32, _I32,
                                  C.POINTER(Sampling), _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
+    "grpo_rollout_step_grouped": (_I32, [_VP, _VP, _I32, _I32, _I32, _I32, _I32, _VP, _VP, _I32,
+                                         _I32, _I32, C.POINTER(Sampling), _VP, _VP, _VP, _VP, _VP,
+                                         _SZ, _VP]),
     "grpo_score_sequences": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _VP, _VP, _SZ, _VP]),
     "grpo_advantages": (_I32, [_VP, _I32, _I32, _F32, _VP, _VP]),
     "grpo_token_loss": (_I32, [_VP, _VP, _VP, _VP, _VP, _I32, _I32, _F32, _F32, _I32, _VP, _VP,
@@ -216,13 +219,21 @@ def prefill(model: Model, kv, n_seqs: int, max_len: int, prompts, G: int, sampli
 
 def rollout_step(model: Model, kv, n_seqs: int, max_len: int, pos, tok, max_pos: int, step0: int,
                  n_steps: int, sampling: Sampling, tok_out, logp_out, logits_dbg=None,
-                 hidden_dbg=None, ws=None, stream=None):
+                 hidden_dbg=None, ws=None, stream=None, group: int = 0, prefix_len: int = 0):
+    """grpo_rollout_step, or grpo_rollout_step_grouped when group > 0 (rows in
+    groups of `group` sharing cache positions below prefix_len)."""
     B = pos.numel()
+    nws = ws.numel() if ws is not None else 0
+    if group > 0:
+        _check(lib().grpo_rollout_step_grouped(
+            model.handle, _ptr(kv), n_seqs, max_len, B, group, prefix_len, _ptr(pos), _ptr(tok),
+            max_pos, step0, n_steps, C.byref(sampling), _ptr(tok_out), _ptr(logp_out),
+            _ptr(logits_dbg), _ptr(hidden_dbg), _ptr(ws), nws, _stream(stream)))
+        return
     _check(lib().grpo_rollout_step(model.handle, _ptr(kv), n_seqs, max_len, B, _ptr(pos),
                                    _ptr(tok), max_pos, step0, n_steps, C.byref(sampling),
                                    _ptr(tok_out), _ptr(logp_out), _ptr(logits_dbg),
-                                   _ptr(hidden_dbg), _ptr(ws), ws.numel() if ws is not None else 0,
-                                   _stream(stream)))
+                                   _ptr(hidden_dbg), _ptr(ws), nws, _stream(stream)))
 
 
 def score_sequences(model: Model, tokens, score_from: int, temperature: float, logp_out, ws=None,

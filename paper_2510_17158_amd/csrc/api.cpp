@@ -333,8 +333,10 @@ RolloutWS take_rollout(Bump& b, const grpo_config& c, int B, int max_len) {
   RolloutWS w;
   w.s = take_step(b, c, B, c.dtype == GRPO_F32 ? B : decode_nb(B), decode_scratch(c, B), B);
   w.logits = b.take<float>((size_t)B * c.vocab);
-  const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.n_kv_heads, c.head_dim, max_len);
-  w.attn_part = b.take<float>(c.dtype == GRPO_F32 ? 0 : ap.part_floats);
+  w.attn_part = b.take<float>(
+      c.dtype == GRPO_F32 ? 0
+                          : decode_attn_part_floats_max(B, c.n_heads, c.n_kv_heads, c.head_dim,
+                                                        max_len));
   w.step_ctr = b.take<int32_t>(1);
   return w;
 }
@@ -641,11 +643,12 @@ int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
   return GRPO_OK;
 }
 
-int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len, int32_t B,
-                      int32_t* pos, int32_t* tok, int32_t max_pos, int32_t step0, int32_t n_steps,
-                      const grpo_sampling* s, int32_t* tok_out, float* logp_out,
-                      float* logits_dbg, float* hidden_dbg, void* ws, size_t ws_bytes,
-                      void* stream) {
+// Decode steps; G > 0: rows in groups of G sharing the cache below prefix_len.
+static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len, int32_t B,
+                   int32_t* pos, int32_t* tok, int32_t max_pos, int32_t step0, int32_t n_steps,
+                   const grpo_sampling* s, int32_t* tok_out, float* logp_out, float* logits_dbg,
+                   float* hidden_dbg, int32_t G, int32_t prefix_len, void* ws, size_t ws_bytes,
+                   void* stream) {
   if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
   const grpo_config& c = m->cfg;
   if (!kv || !pos || !tok || !tok_out || !logp_out || !ws)
@@ -669,7 +672,11 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
   const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
   const bool pk = c.dtype == GRPO_BF16;
   const int nb = pk ? decode_nb(B) : 0;
-  const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.n_kv_heads, c.head_dim, max_len);
+  // fp32 attention reads every row's own cache (the shared positions hold the
+  // same values, so the results are those of a grouped step)
+  const bool grouped = pk && G > 0 && prefix_len > 0;
+  const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.n_kv_heads, c.head_dim, max_len,
+                                             grouped ? G : 0, grouped ? prefix_len : 0);
   // One decode step on stream `ss`.  In graph mode the Philox step and the output
   // column come from the device step counter (advanced by the embedding kernel).
   auto enqueue_step = [&](hipStream_t ss, bool graph, int step) -> int {
@@ -779,7 +786,8 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
       (uint64_t)(uintptr_t)pos, (uint64_t)(uintptr_t)tok, (uint64_t)step0, (uint64_t)n_steps,
       (uint64_t)(uintptr_t)tok_out, (uint64_t)(uintptr_t)logp_out, (uint64_t)(uintptr_t)ws,
       (uint64_t)(uintptr_t)m->dec.base,
-      (uint64_t)*(const uint32_t*)&s->temperature, (uint64_t)(uint32_t)s->top_k, s->seed};
+      (uint64_t)*(const uint32_t*)&s->temperature, (uint64_t)(uint32_t)s->top_k, s->seed,
+      (uint64_t)(uint32_t)ap.G, (uint64_t)(uint32_t)ap.prefix_len};
   HIPCHK(fill_i32(w.step_ctr, 1, -1, st));   // the first replay's embedding makes it 0
   if (!dg.exec || dg.key != key) {
     if (dg.exec) {
@@ -808,6 +816,30 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
   for (int step = 0; step < n_steps; ++step) HIPCHK(hipGraphLaunch(dg.exec, st));
   g_err.clear();
   return GRPO_OK;
+}
+
+int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len, int32_t B,
+                      int32_t* pos, int32_t* tok, int32_t max_pos, int32_t step0, int32_t n_steps,
+                      const grpo_sampling* s, int32_t* tok_out, float* logp_out,
+                      float* logits_dbg, float* hidden_dbg, void* ws, size_t ws_bytes,
+                      void* stream) {
+  return rollout(m, kv, n_seqs, max_len, B, pos, tok, max_pos, step0, n_steps, s, tok_out,
+                 logp_out, logits_dbg, hidden_dbg, 0, 0, ws, ws_bytes, stream);
+}
+
+int grpo_rollout_step_grouped(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
+                              int32_t B, int32_t G, int32_t prefix_len, int32_t* pos, int32_t* tok,
+                              int32_t max_pos, int32_t step0, int32_t n_steps,
+                              const grpo_sampling* s, int32_t* tok_out, float* logp_out,
+                              float* logits_dbg, float* hidden_dbg, void* ws, size_t ws_bytes,
+                              void* stream) {
+  if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
+  if (G < 1 || B < 1 || B % G)
+    return fail(GRPO_INVALID_ARG, "G %d must be >= 1 and divide B %d", G, B);
+  if (prefix_len < 0 || prefix_len > max_len)
+    return fail(GRPO_INVALID_ARG, "prefix_len %d outside [0, max_len %d]", prefix_len, max_len);
+  return rollout(m, kv, n_seqs, max_len, B, pos, tok, max_pos, step0, n_steps, s, tok_out,
+                 logp_out, logits_dbg, hidden_dbg, G, prefix_len, ws, ws_bytes, stream);
 }
 
 int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, int32_t T,

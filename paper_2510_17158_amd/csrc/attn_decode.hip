@@ -14,6 +14,15 @@
 // span writes (max, sum, unnormalised o) and a second kernel merges the spans in
 // span order.
 //
+// Grouped rollouts (the G samples of a prompt in consecutive batch rows, their
+// prompt K/V identical): the prompt positions are read once per group.  A
+// prefix launch, one workgroup per (prompt chunk, kv head, group), stages the
+// group leader's K and V and gives each wave the query heads of its own samples
+// (8 MFMA columns: two samples of 4 heads at the 7B shape); each wave runs all
+// tiles of the chunk and writes its columns' (max, sum, o) as one span.  The
+// per-sequence launch then covers the generated positions only, and the merge
+// takes the prompt chunks first, then the generated spans.
+//
 // fp32 models use the plain vector kernel of the prefill path.
 #include <algorithm>
 
@@ -26,6 +35,21 @@ namespace {
 
 constexpr int DT = 32;            // decode positions per wave tile
 constexpr int SPAN_Q = 4 * DT;    // span granularity: one tile per wave
+constexpr int MAX_CHUNKS = 16;    // prompt chunks of a grouped step, at most
+
+// Grouped rollout: G samples per group (0 = every row on its own), prompt
+// positions shared below prefix_len, n_sub workgroups per group and chunk (each
+// holding 4 waves x 8 / GQ samples).
+struct DecodeGroup { int G, prefix_len, n_sub; };
+
+// Positions the group of batch row b shares: prefix_len, cut to the context
+// every member has reached (so a shared position exists for all of them).
+__device__ __forceinline__ int group_shared(const int32_t* __restrict__ pos, int grp,
+                                            const DecodeGroup& ga, int max_len) {
+  int pl = ga.prefix_len;
+  for (int i = 0; i < ga.G; ++i) pl = min(pl, min(pos[grp * ga.G + i], max_len - 1) + 1);
+  return pl;
+}
 
 template <int HD, int NG, int NVT>
 struct KVTile {
@@ -34,12 +58,16 @@ struct KVTile {
 };
 
 // ---------------------------------------------------------------- decode, bf16
-template <int HD, int MAXG>
+// GRP: the prefix launch of a grouped step (blockIdx = (chunk, kv head, group x
+// n_sub)); otherwise blockIdx = (span, kv head, batch row), the spans starting at
+// the group's shared length when ga.G > 0.  Spans write partial row
+// split_base + span of S.
+template <int HD, int MAXG, bool GRP>
 __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const int32_t* __restrict__ pos, int H, int n_kv, int max_len, int S, int span, float scale,
     float* __restrict__ part_o, float* __restrict__ part_ml, bf16_t* __restrict__ out,
-    int pack_nb) {
+    int pack_nb, DecodeGroup ga, int split_base) {
   constexpr int QSTEPS = HD / 32;     // MFMA k-steps over the head dim
   constexpr int LPT = HD / 8;         // lanes per position in P.V
   constexpr int PPW = 64 / LPT;       // positions per V load instruction
@@ -51,40 +79,62 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   __shared__ float red[4][MAXG * HD];
   __shared__ float wm[4][MAXG], wl[4][MAXG];
 
-  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int split = blockIdx.x, g = blockIdx.y;
   const int GQ = H / n_kv;
   const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
-  const int ctx = min(pos[b], max_len - 1) + 1;
-  const int t0 = split * span;
-  if (t0 >= ctx) return;
-  const int t1 = min(t0 + span, ctx);
-  const int ntiles = (t1 - t0 + DT - 1) / DT;
-  const int nmine = ntiles > wave ? (ntiles - wave + 3) / 4 : 0;
-  const size_t head_base = ((size_t)b * n_kv + g) * max_len;
-  const bf16_t* kb = kc + head_base * HD;
-  const bf16_t* vb = vc + head_base * HD;
   const int lg = lane >> 4;           // MFMA k-group of this lane
   const int j = lane & 15;            // MFMA row (position) / column (query head)
   const int ts = lane / LPT, hg = lane % LPT;
+  // positions [t0, t1) of this workgroup; the cache rows of batch row `src`
+  int t0, t1, src, sbase = 0;
+  if constexpr (GRP) {
+    const int group = blockIdx.z / ga.n_sub;
+    sbase = (blockIdx.z % ga.n_sub * 4 + wave) * (MAXG / GQ);   // this wave's first sample
+    t0 = split * span;
+    t1 = min(t0 + span, group_shared(pos, group, ga, max_len));
+    src = group * ga.G;
+  } else {
+    src = blockIdx.z;
+    const int ctx = min(pos[src], max_len - 1) + 1;
+    t0 = (ga.G > 0 ? group_shared(pos, src / ga.G, ga, max_len) : 0) + split * span;
+    t1 = min(t0 + span, ctx);
+  }
+  if (t0 >= t1) return;
+  const int ntiles = (t1 - t0 + DT - 1) / DT;
+  // grouped: every wave runs every tile (its own query columns); else the tiles
+  // are dealt round-robin to the waves
+  const int nmine = GRP ? ntiles : ntiles > wave ? (ntiles - wave + 3) / 4 : 0;
+  const size_t head_base = ((size_t)src * n_kv + g) * max_len;
+  const bf16_t* kb = kc + head_base * HD;
+  const bf16_t* vb = vc + head_base * HD;
+  // valid query columns: the GQ heads of the row, or (grouped) GQ heads of each of
+  // the wave's MAXG / GQ samples that exist
+  const int ncols = GRP ? min(MAXG / GQ, max(ga.G - sbase, 0)) * GQ : GQ;
+  // a grouped wave past the group's last sample has nothing to do (the grouped
+  // path has no workgroup barrier)
+  if (GRP && ncols == 0) return;
 
   // query fragments; head-dim chunk (st * 4 + lg) of 8 elements feeds MFMA step st,
   // so each K load instruction reads 64 contiguous bytes per position
   bf16x8_t qf[QSTEPS];
   {
-    const bf16_t* qp = q + ((size_t)b * H + g * GQ + min(j, GQ - 1)) * HD + lg * 8;
+    const int jc = min(j, max(ncols, 1) - 1);
+    const int qrow = GRP ? (src + min(sbase + jc / GQ, ga.G - 1)) * H + g * GQ + jc % GQ
+                         : src * H + g * GQ + jc;
+    const bf16_t* qp = q + (size_t)qrow * HD + lg * 8;
 #pragma unroll
     for (int st = 0; st < QSTEPS; ++st) {
       u32x4_t v = *(const u32x4_t*)(qp + st * 32);
-      if (j >= GQ) v = (u32x4_t){0u, 0u, 0u, 0u};
+      if (j >= ncols) v = (u32x4_t){0u, 0u, 0u, 0u};
       qf[st] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
 
   auto load = [&](Tile& tl, int i) {
-    const int tb = t0 + (wave + 4 * i) * DT;
+    const int tb = t0 + (GRP ? i : wave + 4 * i) * DT;
 #pragma unroll
     for (int grp = 0; grp < NG; ++grp) {
-      const int t = min(tb + grp * 16 + j, ctx - 1);
+      const int t = min(tb + grp * 16 + j, t1 - 1);
       const bf16_t* kp = kb + (size_t)t * HD + lg * 8;
 #pragma unroll
       for (int st = 0; st < QSTEPS; ++st)
@@ -92,7 +142,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     }
 #pragma unroll
     for (int iv = 0; iv < NVT; ++iv) {
-      const int t = min(tb + iv * PPW + ts, ctx - 1);
+      const int t = min(tb + iv * PPW + ts, t1 - 1);
       tl.v[iv] = __builtin_nontemporal_load((const u32x4_t*)(vb + (size_t)t * HD + hg * 8));
     }
   };
@@ -105,7 +155,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
 
   auto compute = [&](const Tile& tl, int i) {
-    const int tb = t0 + (wave + 4 * i) * DT;
+    const int tb = t0 + (GRP ? i : wave + 4 * i) * DT;
     float sv[NG][4];
     float tmax = -INFINITY;
 #pragma unroll
@@ -190,7 +240,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   // wave totals: o over the positions of a load instruction, l over the k-groups
 #pragma unroll
   for (int h = 0; h < MAXG; ++h)
-    if (h < GQ) {
+    if (h < ncols) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float x = o[h][e];
@@ -201,11 +251,33 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     }
   l += __shfl_xor(l, 16, 64);
   l += __shfl_xor(l, 32, 64);
+  if constexpr (GRP) {
+    // the wave's columns are whole: column h is head g*GQ + h % GQ of batch row
+    // src + sbase + h / GQ
+    auto row_of = [&](int h) {
+      return ((size_t)(src + sbase + h / GQ) * H + g * GQ + h % GQ) * S + split_base + split;
+    };
+    if (ts == 0) {
+#pragma unroll
+      for (int h = 0; h < MAXG; ++h)
+        if (h < ncols) {
+          float* po = part_o + row_of(h) * HD + hg * 8;
+          *(float4*)po = make_float4(o[h][0], o[h][1], o[h][2], o[h][3]);
+          *(float4*)(po + 4) = make_float4(o[h][4], o[h][5], o[h][6], o[h][7]);
+        }
+    }
+    if (lg == 0 && j < ncols) {
+      const size_t row = row_of(j);
+      part_ml[row * 2] = m;
+      part_ml[row * 2 + 1] = l;
+    }
+    return;
+  }
   if (lg == 0 && j < MAXG) { wm[wave][j] = m; wl[wave][j] = l; }
   if (ts == 0) {
 #pragma unroll
     for (int h = 0; h < MAXG; ++h)
-      if (h < GQ) {
+      if (h < ncols) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) red[wave][h * HD + hg * 8 + e] = o[h][e];
       }
@@ -224,29 +296,36 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     }
     if (S == 1) {
       const int k = (g * GQ + h) * HD + e;
-      out[pack_nb ? act_frag_index(b, k, pack_nb) : (size_t)b * H * HD + k] = f2bf(x / L);
+      out[pack_nb ? act_frag_index(src, k, pack_nb) : (size_t)src * H * HD + k] = f2bf(x / L);
     } else {
-      const size_t row = ((size_t)b * H + g * GQ + h) * S + split;
+      const size_t row = ((size_t)src * H + g * GQ + h) * S + split_base + split;
       part_o[row * HD + e] = x;
       if (e == 0) { part_ml[row * 2] = M; part_ml[row * 2 + 1] = L; }
     }
   }
 }
 
+// Merge of the spans of (row b, head h) in partial-row order.  Grouped: rows
+// 0 .. chunks-1 are the prompt chunks of span_p positions below the group's
+// shared length, then the spans of the generated positions from there.
 template <int HD>
 __global__ __launch_bounds__(HD) void k_attn_combine(const float* __restrict__ part_o,
                                                      const float* __restrict__ part_ml,
                                                      const int32_t* __restrict__ pos, int H,
                                                      int max_len, int S, int span,
-                                                     bf16_t* __restrict__ out, int pack_nb) {
+                                                     bf16_t* __restrict__ out, int pack_nb,
+                                                     DecodeGroup ga, int chunks, int span_p) {
   const int h = blockIdx.x, b = blockIdx.y, e = threadIdx.x;
   const int ctx = min(pos[b], max_len - 1) + 1;
-  const int ns = min(S, (ctx + span - 1) / span);
+  const int base = ga.G > 0 ? group_shared(pos, b / ga.G, ga, max_len) : 0;
+  auto used = [&](int s) { return s < chunks ? s * span_p < base : base + (s - chunks) * span < ctx; };
   const size_t row0 = ((size_t)b * H + h) * S;
   float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, part_ml[(row0 + s) * 2]);
+  for (int s = 0; s < S; ++s)
+    if (used(s)) M = fmaxf(M, part_ml[(row0 + s) * 2]);
   float L = 0.f, acc = 0.f;
-  for (int s = 0; s < ns; ++s) {
+  for (int s = 0; s < S; ++s) {
+    if (!used(s)) continue;
     const float w = __expf(part_ml[(row0 + s) * 2] - M);
     L = fmaf(part_ml[(row0 + s) * 2 + 1], w, L);
     acc = fmaf(part_o[(row0 + s) * HD + e], w, acc);
@@ -257,28 +336,84 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const float* __restrict__ p
 
 }  // namespace
 
-DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len) {
+DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len, int G,
+                                int prefix_len) {
   // enough spans for about two workgroups per compute unit; one span (and no
   // merge kernel) whenever the (sequence, kv head) pairs alone reach that
   constexpr int kTargetWGs = 512;
   const int pairs = std::max(1, B * n_kv);
   const int max_spans = (max_len + SPAN_Q - 1) / SPAN_Q;
   const int want = std::min(std::max(1, (kTargetWGs + pairs / 2) / pairs), max_spans);
-  DecodeAttnPlan p;
+  DecodeAttnPlan p{};
   p.tc = ((max_len + want - 1) / want + SPAN_Q - 1) / SPAN_Q * SPAN_Q;
   p.splits = (max_len + p.tc - 1) / p.tc;
   p.part_floats = p.splits > 1 ? (size_t)B * H * p.splits * (hd + 2) : 0;
+  if (G <= 0 || prefix_len <= 0) return p;
+  // grouped: the generated positions keep the spans above (they start at the
+  // shared length, so they cover at most max_len positions); the prompt is cut
+  // into chunks of whole tiles, about kTargetWGs prefix workgroups in all
+  const int spw = std::max(1, 8 / std::max(1, H / n_kv));
+  p.G = G;
+  p.prefix_len = std::min(prefix_len, max_len);
+  p.n_sub = (G + 4 * spw - 1) / (4 * spw);
+  const int gpairs = std::max(1, B / G * n_kv * p.n_sub);
+  const int max_chunks = std::min(MAX_CHUNKS, (p.prefix_len + DT - 1) / DT);
+  const int wc = std::min(std::max(1, (kTargetWGs + gpairs / 2) / gpairs), max_chunks);
+  p.span_p = ((p.prefix_len + wc - 1) / wc + DT - 1) / DT * DT;
+  p.chunks = (p.prefix_len + p.span_p - 1) / p.span_p;
+  p.part_floats = (size_t)B * H * (p.chunks + p.splits) * (hd + 2);
   return p;
 }
 
-template <int HD, int MAXG>
+size_t decode_attn_part_floats_max(int B, int H, int n_kv, int hd, int max_len) {
+  const DecodeAttnPlan p = decode_attn_plan(B, H, n_kv, hd, max_len);
+  return (size_t)B * H * (MAX_CHUNKS + p.splits) * (hd + 2);
+}
+
+template <int HD, int MAXG, bool GRP>
 static void launch_decode(dim3 grid, hipStream_t st, const void* q, const void* kc,
-                          const void* vc, const int32_t* pos, int H, int n_kv, int max_len,
-                          const DecodeAttnPlan& p, float scale, float* part_o, float* part_ml,
-                          void* out, int pack_nb) {
-  k_attn_decode_bf16<HD, MAXG><<<grid, 256, 0, st>>>(
-      (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, H, n_kv, max_len, p.splits,
-      p.tc, scale, part_o, part_ml, (bf16_t*)out, pack_nb);
+                          const void* vc, const int32_t* pos, int H, int n_kv, int max_len, int S,
+                          int span, float scale, float* part_o, float* part_ml, void* out,
+                          int pack_nb, DecodeGroup ga, int split_base) {
+  k_attn_decode_bf16<HD, MAXG, GRP><<<grid, 256, 0, st>>>(
+      (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, H, n_kv, max_len, S, span,
+      scale, part_o, part_ml, (bf16_t*)out, pack_nb, ga, split_base);
+}
+
+template <int HD>
+static hipError_t attn_decode_hd(const void* q, const void* kc, const void* vc,
+                                 const int32_t* pos, int B, int H, int n_kv, int max_len,
+                                 const DecodeAttnPlan& p, float* part, void* out, hipStream_t st,
+                                 int pack_nb) {
+  const float scale = 1.f / sqrtf((float)HD);
+  const int gq = H / n_kv;
+  const bool grouped = p.G > 0;
+  const int S = p.chunks + p.splits;      // partial rows per (row, head)
+  float* part_o = S > 1 ? part : nullptr;
+  float* part_ml = S > 1 ? part + (size_t)B * H * S * HD : nullptr;
+  const DecodeGroup ga{p.G, p.prefix_len, p.n_sub};
+  if (grouped) {
+    Prof pf("attn_prefix", st);
+    dim3 grid(p.chunks, n_kv, B / p.G * p.n_sub);
+    launch_decode<HD, 8, true>(grid, st, q, kc, vc, pos, H, n_kv, max_len, S, p.span_p, scale,
+                               part_o, part_ml, out, pack_nb, ga, 0);
+  }
+  {
+    Prof pf("attn_decode", st);
+    dim3 grid(p.splits, n_kv, B);
+    if (gq <= 4)
+      launch_decode<HD, 4, false>(grid, st, q, kc, vc, pos, H, n_kv, max_len, S, p.tc, scale,
+                                  part_o, part_ml, out, pack_nb, ga, p.chunks);
+    else
+      launch_decode<HD, 8, false>(grid, st, q, kc, vc, pos, H, n_kv, max_len, S, p.tc, scale,
+                                  part_o, part_ml, out, pack_nb, ga, p.chunks);
+  }
+  if (S > 1) {
+    Prof pf("attn_combine", st);
+    k_attn_combine<HD><<<dim3(H, B), HD, 0, st>>>(part_o, part_ml, pos, H, max_len, S, p.tc,
+                                                  (bf16_t*)out, pack_nb, ga, p.chunks, p.span_p);
+  }
+  return hipGetLastError();
 }
 
 hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
@@ -288,35 +423,16 @@ hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
   (void)n_seqs;
   if (B <= 0) return hipSuccess;
   if (pack_nb && (dtype == 0 || B > pack_nb || pack_nb % 16)) return hipErrorInvalidValue;
-  const float scale = 1.f / sqrtf((float)hd);
   if (dtype == 0)
     return attn_rows_f32((const float*)q, (const float*)kc, (const float*)vc, pos, B, 1, 1, H,
                          n_kv, hd, max_len, (float*)out, st);
-  float* part_o = p.splits > 1 ? part : nullptr;
-  float* part_ml = p.splits > 1 ? part + (size_t)B * H * p.splits * hd : nullptr;
-  dim3 grid(p.splits, n_kv, B);
-  const int gq = H / n_kv;
-  {
-    Prof pf("attn_decode", st);
-    if (hd == 128) {
-      if (gq <= 4) launch_decode<128, 4>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
-      else launch_decode<128, 8>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
-    } else {
-      if (gq <= 4) launch_decode<64, 4>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
-      else launch_decode<64, 8>(grid, st, q, kc, vc, pos, H, n_kv, max_len, p, scale, part_o, part_ml, out, pack_nb);
-    }
-  }
-  if (p.splits > 1) {
-    Prof pf("attn_combine", st);
-    dim3 cgrid(H, B);
-    if (hd == 128)
-      k_attn_combine<128><<<cgrid, 128, 0, st>>>(part_o, part_ml, pos, H, max_len, p.splits,
-                                                 p.tc, (bf16_t*)out, pack_nb);
-    else
-      k_attn_combine<64><<<cgrid, 64, 0, st>>>(part_o, part_ml, pos, H, max_len, p.splits,
-                                               p.tc, (bf16_t*)out, pack_nb);
-  }
-  return hipGetLastError();
+  if (H % n_kv || H / n_kv > 8 || (hd != 64 && hd != 128)) return hipErrorInvalidValue;
+  if (p.G > 0 && (B % p.G || p.chunks < 1 || p.chunks > MAX_CHUNKS || p.n_sub < 1 ||
+                  (long)p.n_sub * 4 * (8 / (H / n_kv)) < p.G || p.prefix_len > max_len ||
+                  (long)p.chunks * p.span_p < p.prefix_len))
+    return hipErrorInvalidValue;
+  return hd == 128 ? attn_decode_hd<128>(q, kc, vc, pos, B, H, n_kv, max_len, p, part, out, st, pack_nb)
+                   : attn_decode_hd<64>(q, kc, vc, pos, B, H, n_kv, max_len, p, part, out, st, pack_nb);
 }
 
 }  // namespace grpo

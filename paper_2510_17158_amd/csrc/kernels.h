@@ -127,8 +127,19 @@ hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeAr
 // decode-GEMM fragment order [pack_nb][H*hd].
 // tc: context positions per span (a multiple of 128); splits: spans per (sequence,
 // kv head); part_floats: fp32 scratch for the span merge (0 with a single span).
-struct DecodeAttnPlan { int tc; int splits; size_t part_floats; };
-DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len);
+// tc positions per span, splits spans per row; grouped steps (G > 0) add
+// `chunks` prompt chunks of span_p positions below prefix_len per group of G
+// rows, n_sub prefix workgroups per group and chunk.  part_floats: the partial
+// buffer the plan needs.
+struct DecodeAttnPlan {
+  int tc, splits;
+  int G, prefix_len, chunks, span_p, n_sub;
+  size_t part_floats;
+};
+DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len, int G = 0,
+                                int prefix_len = 0);
+// partial floats of any plan for these shapes, grouped or not
+size_t decode_attn_part_floats_max(int B, int H, int n_kv, int hd, int max_len);
 hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
                        const int32_t* pos, int B, int H, int n_kv, int hd, int n_seqs, int max_len,
                        const DecodeAttnPlan& p, float* part, void* out, hipStream_t st,

@@ -78,7 +78,9 @@ class GrpoIteration:
         self.pos.fill_(w.prompt_len)
         api.rollout_step(self.policy, self.kv, self.B, self.max_len, self.pos, self.tok,
                          w.prompt_len, 1, n, self.sampling, self.tok_dec, self.logp_dec,
-                         logits_dbg=logits_dbg, hidden_dbg=hidden_dbg, ws=self.ws_roll)
+                         logits_dbg=logits_dbg, hidden_dbg=hidden_dbg, ws=self.ws_roll,
+                         group=w.group if w.shared_prompt else 0,
+                         prefix_len=w.prompt_len if w.shared_prompt else 0)
 
     def assemble(self):
         """Sequences [B, Tp + Tn] and rollout log-probs [B, Tn] from the phase outputs."""

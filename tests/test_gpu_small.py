@@ -33,8 +33,9 @@ def _small_workload(**kw):
     return w.with_(**kw)
 
 
-def _stage_local(w, host, model, it, n_steps):
-    """Decode n_steps one at a time; check every layer, the head and the sampler."""
+def _stage_local(w, host, model, it, n_steps, group=0, prefix_len=0):
+    """Decode n_steps one at a time; check every layer, the head and the sampler
+    (group > 0: grouped steps sharing the cache below prefix_len)."""
     cfg = w.model
     B, L, d, V = it.B, cfg.n_layers, cfg.d_model, cfg.vocab
     om = oracle.OracleModel(cfg, host)
@@ -52,7 +53,8 @@ def _stage_local(w, host, model, it, n_steps):
         lg = torch.empty(B, V, device="cuda")
         hid = torch.empty(L + 1, B, d, device="cuda")
         api.rollout_step(model, it.kv, B, it.max_len, it.pos, it.tok, pos, 1 + s, 1, it.sampling,
-                         to, lo, logits_dbg=lg, hidden_dbg=hid, ws=it.ws_roll)
+                         to, lo, logits_dbg=lg, hidden_dbg=hid, ws=it.ws_roll, group=group,
+                         prefix_len=prefix_len)
         torch.cuda.synchronize()
         hid = hid.double().cpu().numpy()
         lg = lg.cpu().numpy()
@@ -278,10 +280,11 @@ def test_decode_span_count_does_not_change_results(small):
 def test_bench_launch_configuration():
     """The 7B workload's own launch configuration on a 1-layer model of the 7B
     width: 8 prompts x G 8 = 64 sequences, 2048-token prompts, 2048 sampled tokens
-    (temperature 1), scoring over 4096 positions.  One decode step at context 2049
-    is checked stage-locally against the oracle (the decode GEMM plans at batch 64,
-    single-span attention over 8 kv heads x 64 sequences, the LM head and the
-    sampler over 32000 logits); then the whole rollout runs, and teacher-forced
+    (temperature 1), scoring over 4096 positions.  One grouped decode step at
+    context 2049 is checked stage-locally against the oracle (the decode GEMM plans
+    at batch 64, the prompt attention once per group in 8 chunks, the generated
+    positions per sequence and their merge, the LM head and the sampler over 32000
+    logits); then the whole rollout runs (grouped, as the workload does), and teacher-forced
     scoring of its sequences (flash attention over 4096 positions, the 256 x 256
     GEMM tiles over chunks of 16 x 4096 rows) must reproduce every rollout log-prob:
     both are log_softmax(logits / T) at the sampled token (Eq. (1)), computed by
@@ -293,8 +296,9 @@ def test_bench_launch_configuration():
     host, model = build_model(w.model, w.master_seed, gain_noise=0.1)
     it = GrpoIteration(w, model, None, synth.make_prompts(w), synth.make_rewards(w),
                        synth.make_seed(w))
+    assert w.shared_prompt
     it.prefill()
-    _stage_local(w, host, model, it, 1)
+    _stage_local(w, host, model, it, 1, group=w.group, prefix_len=w.prompt_len)
     say("full rollout and scoring")
     it.decode()
     it.assemble()
@@ -306,4 +310,60 @@ def test_bench_launch_configuration():
     err = float(np.abs(new - old).max())
     say("rollout vs scoring log-prob err", err, "mean logp", float(old.mean()))
     assert err <= LOGIT_TOL
+    model.close()
+
+
+@pytest.mark.parametrize("name,P,G,Tp,prefix,steps", [
+    ("small", 2, 4, 300, 300, 3),      # GQ 3: two samples (6 of 8 columns) per wave
+    ("small", 2, 4, 300, 100, 2),      # only part of the prompt shared
+    ("small", 1, 3, 33, 33, 2),        # G not a multiple of the samples per wave
+    ("7b", 2, 16, 70, 70, 2),          # GQ 4, G 16: two prefix workgroups per group
+    ("7b", 4, 8, 520, 520, 2),         # several prompt chunks, ragged last tile
+])
+def test_grouped_decode_matches_per_row(name, P, G, Tp, prefix, steps):
+    """Grouped decode (each group's prompt K/V read once) against per-row decode,
+    step by step from the same state (both write the same K/V: same token, same
+    projections): logits within the bf16 tolerance (attention differs only in
+    the order of its additions; measured far below it), log-probs likewise,
+    identical tokens except near-ties of the per-row logits."""
+    require_gpu()
+    base = get(name)
+    layers = 2 if name == "small" else 1
+    w = truncated(base, layers, n_prompts=P, group=G, prompt_len=Tp, new_tokens=steps + 1,
+                  temperature=1.0, top_k=0)
+    say("grouped vs per-row decode", name, P, G, Tp, prefix)
+    host, model = build_model(w.model, w.master_seed, gain_noise=0.1)
+    it = GrpoIteration(w, model, None, synth.make_prompts(w), synth.make_rewards(w),
+                       synth.make_seed(w))
+    it.prefill()
+    B, V = it.B, w.model.vocab
+    it.tok.copy_(it.tok0)
+    it.pos.fill_(Tp)
+    worst, near = 0.0, 0
+    for s in range(steps):
+        tok_in, pos_in = it.tok.clone(), it.pos.clone()
+        res = []
+        for grouped in (False, True):
+            it.tok.copy_(tok_in)
+            it.pos.copy_(pos_in)
+            to = torch.empty(B, 1, dtype=torch.int32, device="cuda")
+            lo = torch.empty(B, 1, device="cuda")
+            lg = torch.empty(B, V, device="cuda")
+            api.rollout_step(model, it.kv, B, it.max_len, it.pos, it.tok, Tp + s, 1 + s, 1,
+                             it.sampling, to, lo, logits_dbg=lg, ws=it.ws_roll,
+                             group=G if grouped else 0, prefix_len=prefix if grouped else 0)
+            torch.cuda.synchronize()
+            res.append((to.cpu().numpy()[:, 0], lo.cpu().numpy()[:, 0], lg.cpu().numpy()))
+        (t0, l0, g0), (t1, l1, g1) = res
+        worst = max(worst, float(np.abs(g1 - g0).max()))
+        assert np.abs(g1 - g0).max() <= LOGIT_TOL
+        for b in np.flatnonzero(t0 != t1):
+            _, _, margin = oracle.sample_token(g0[b].astype(np.float64), w.temperature, w.top_k,
+                                               it.sampling.seed, 1 + s, b)
+            assert margin < 1e-4, (s, b)
+            near += 1
+        keep = t0 == t1
+        assert np.abs(l1 - l0)[keep].max() <= LOGIT_TOL
+        it.tok.copy_(torch.from_numpy(t0).to("cuda"))   # both continue from the per-row token
+    say("grouped vs per-row: logit err", worst, "near ties", near)
     model.close()
