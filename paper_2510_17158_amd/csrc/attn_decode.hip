@@ -16,12 +16,14 @@
 //
 // Grouped rollouts (the G samples of a prompt in consecutive batch rows, their
 // prompt K/V identical): the prompt positions are read once per group.  A
-// prefix launch, one workgroup per (prompt chunk, kv head, group), stages the
-// group leader's K and V and gives each wave the query heads of its own samples
-// (8 MFMA columns: two samples of 4 heads at the 7B shape); each wave runs all
-// tiles of the chunk and writes its columns' (max, sum, o) as one span.  The
-// per-sequence launch then covers the generated positions only, and the merge
-// takes the prompt chunks first, then the generated spans.
+// prefix launch, one workgroup per (prompt chunk, kv head, group), copies the
+// group leader's K and V tiles straight into a 4-stage LDS ring (one copy per
+// workgroup, three tiles ahead, one barrier per tile) and gives each wave the
+// query heads of its own samples (8 MFMA columns: two samples of 4 heads at the
+// 7B shape); each wave runs every tile of the chunk with the same scores,
+// softmax and P.V as above and writes its columns' (max, sum, o) as one span.
+// The per-sequence launch then covers the generated positions only, and the
+// merge takes the prompt chunks first, then the generated spans.
 //
 // fp32 models use the plain vector kernel of the prefill path.
 #include <algorithm>
@@ -58,11 +60,9 @@ struct KVTile {
 };
 
 // ---------------------------------------------------------------- decode, bf16
-// GRP: the prefix launch of a grouped step (blockIdx = (chunk, kv head, group x
-// n_sub)); otherwise blockIdx = (span, kv head, batch row), the spans starting at
-// the group's shared length when ga.G > 0.  Spans write partial row
-// split_base + span of S.
-template <int HD, int MAXG, bool GRP>
+// blockIdx = (span, kv head, batch row); the spans start at the group's shared
+// length when ga.G > 0 and write partial row split_base + span of S.
+template <int HD, int MAXG>
 __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const int32_t* __restrict__ pos, int H, int n_kv, int max_len, int S, int span, float scale,
@@ -85,53 +85,33 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   const int lg = lane >> 4;           // MFMA k-group of this lane
   const int j = lane & 15;            // MFMA row (position) / column (query head)
   const int ts = lane / LPT, hg = lane % LPT;
-  // positions [t0, t1) of this workgroup; the cache rows of batch row `src`
-  int t0, t1, src, sbase = 0;
-  if constexpr (GRP) {
-    const int group = blockIdx.z / ga.n_sub;
-    sbase = (blockIdx.z % ga.n_sub * 4 + wave) * (MAXG / GQ);   // this wave's first sample
-    t0 = split * span;
-    t1 = min(t0 + span, group_shared(pos, group, ga, max_len));
-    src = group * ga.G;
-  } else {
-    src = blockIdx.z;
-    const int ctx = min(pos[src], max_len - 1) + 1;
-    t0 = (ga.G > 0 ? group_shared(pos, src / ga.G, ga, max_len) : 0) + split * span;
-    t1 = min(t0 + span, ctx);
-  }
-  if (t0 >= t1) return;
+  // positions [t0, t1) of this workgroup
+  const int src = blockIdx.z;
+  const int ctx = min(pos[src], max_len - 1) + 1;
+  const int t0 = (ga.G > 0 ? group_shared(pos, src / ga.G, ga, max_len) : 0) + split * span;
+  if (t0 >= ctx) return;
+  const int t1 = min(t0 + span, ctx);
   const int ntiles = (t1 - t0 + DT - 1) / DT;
-  // grouped: every wave runs every tile (its own query columns); else the tiles
-  // are dealt round-robin to the waves
-  const int nmine = GRP ? ntiles : ntiles > wave ? (ntiles - wave + 3) / 4 : 0;
+  const int nmine = ntiles > wave ? (ntiles - wave + 3) / 4 : 0;
   const size_t head_base = ((size_t)src * n_kv + g) * max_len;
   const bf16_t* kb = kc + head_base * HD;
   const bf16_t* vb = vc + head_base * HD;
-  // valid query columns: the GQ heads of the row, or (grouped) GQ heads of each of
-  // the wave's MAXG / GQ samples that exist
-  const int ncols = GRP ? min(MAXG / GQ, max(ga.G - sbase, 0)) * GQ : GQ;
-  // a grouped wave past the group's last sample has nothing to do (the grouped
-  // path has no workgroup barrier)
-  if (GRP && ncols == 0) return;
 
   // query fragments; head-dim chunk (st * 4 + lg) of 8 elements feeds MFMA step st,
   // so each K load instruction reads 64 contiguous bytes per position
   bf16x8_t qf[QSTEPS];
   {
-    const int jc = min(j, max(ncols, 1) - 1);
-    const int qrow = GRP ? (src + min(sbase + jc / GQ, ga.G - 1)) * H + g * GQ + jc % GQ
-                         : src * H + g * GQ + jc;
-    const bf16_t* qp = q + (size_t)qrow * HD + lg * 8;
+    const bf16_t* qp = q + ((size_t)src * H + g * GQ + min(j, GQ - 1)) * HD + lg * 8;
 #pragma unroll
     for (int st = 0; st < QSTEPS; ++st) {
       u32x4_t v = *(const u32x4_t*)(qp + st * 32);
-      if (j >= ncols) v = (u32x4_t){0u, 0u, 0u, 0u};
+      if (j >= GQ) v = (u32x4_t){0u, 0u, 0u, 0u};
       qf[st] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
 
   auto load = [&](Tile& tl, int i) {
-    const int tb = t0 + (GRP ? i : wave + 4 * i) * DT;
+    const int tb = t0 + (wave + 4 * i) * DT;
 #pragma unroll
     for (int grp = 0; grp < NG; ++grp) {
       const int t = min(tb + grp * 16 + j, t1 - 1);
@@ -155,7 +135,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
 
   auto compute = [&](const Tile& tl, int i) {
-    const int tb = t0 + (GRP ? i : wave + 4 * i) * DT;
+    const int tb = t0 + (wave + 4 * i) * DT;
     float sv[NG][4];
     float tmax = -INFINITY;
 #pragma unroll
@@ -240,7 +220,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   // wave totals: o over the positions of a load instruction, l over the k-groups
 #pragma unroll
   for (int h = 0; h < MAXG; ++h)
-    if (h < ncols) {
+    if (h < GQ) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float x = o[h][e];
@@ -251,33 +231,11 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     }
   l += __shfl_xor(l, 16, 64);
   l += __shfl_xor(l, 32, 64);
-  if constexpr (GRP) {
-    // the wave's columns are whole: column h is head g*GQ + h % GQ of batch row
-    // src + sbase + h / GQ
-    auto row_of = [&](int h) {
-      return ((size_t)(src + sbase + h / GQ) * H + g * GQ + h % GQ) * S + split_base + split;
-    };
-    if (ts == 0) {
-#pragma unroll
-      for (int h = 0; h < MAXG; ++h)
-        if (h < ncols) {
-          float* po = part_o + row_of(h) * HD + hg * 8;
-          *(float4*)po = make_float4(o[h][0], o[h][1], o[h][2], o[h][3]);
-          *(float4*)(po + 4) = make_float4(o[h][4], o[h][5], o[h][6], o[h][7]);
-        }
-    }
-    if (lg == 0 && j < ncols) {
-      const size_t row = row_of(j);
-      part_ml[row * 2] = m;
-      part_ml[row * 2 + 1] = l;
-    }
-    return;
-  }
   if (lg == 0 && j < MAXG) { wm[wave][j] = m; wl[wave][j] = l; }
   if (ts == 0) {
 #pragma unroll
     for (int h = 0; h < MAXG; ++h)
-      if (h < ncols) {
+      if (h < GQ) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) red[wave][h * HD + hg * 8 + e] = o[h][e];
       }
@@ -302,6 +260,218 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
       part_o[row * HD + e] = x;
       if (e == 0) { part_ml[row * 2] = M; part_ml[row * 2 + 1] = L; }
     }
+  }
+}
+
+// ------------------------------------------------- grouped prompt chunks, bf16
+// 16 bytes per lane global -> LDS (lds + 16 lane), non-temporal.
+__device__ __forceinline__ void dma16_nt(const bf16_t* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off nt" ::"s"(lds), "v"(g)
+               : "memory");
+}
+// K stage rows: the 16 rows one fragment read touches at one 16-byte piece fall
+// in 16 distinct bank groups (hd 128: 256-byte rows, piece ^ row % 16; hd 64:
+// 128-byte rows, piece ^ (row / 2) % 8, rows 2i and 2i + 1 in the two halves).
+template <int HD>
+__device__ __forceinline__ int kstage_swz(int r) { return HD == 128 ? (r & 15) : ((r >> 1) & 7); }
+
+// blockIdx = (chunk, kv head, group x n_sub).  Wave w of sub-block u takes the
+// samples (4 u + w) * 8 / GQ .. + 8 / GQ of the group (MFMA columns: GQ heads of
+// each); a wave without samples still shares the copies and barriers.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_prefix_bf16(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
+    const int32_t* __restrict__ pos, int H, int n_kv, int max_len, int S, int span, float scale,
+    float* __restrict__ part_o, float* __restrict__ part_ml, DecodeGroup ga) {
+  constexpr int MAXG = 8;             // MFMA columns per wave
+  constexpr int QSTEPS = HD / 32;
+  constexpr int LPT = HD / 8;         // lanes per position in P.V (16-byte pieces per row)
+  constexpr int PPW = 64 / LPT;       // positions per 1 KB of a tile
+  constexpr int NVT = DT / PPW;       // V reads per tile and lane
+  constexpr int NG = DT / 16;
+  constexpr int NCP = DT / PPW;       // 1 KB copies per K (and per V) tile
+  constexpr int NSTG = 4;             // LDS ring stages
+  constexpr int CPW = 2 * NCP / 4;    // copies per wave and tile
+  static_assert(NCP % 4 == 0, "copies dealt evenly to the 4 waves");
+  __shared__ __attribute__((aligned(1024))) bf16_t ks[NSTG][DT * HD];
+  __shared__ __attribute__((aligned(1024))) bf16_t vs[NSTG][DT * HD];
+  __shared__ __attribute__((aligned(16))) float pw[4][DT][MAXG];
+  __shared__ __attribute__((aligned(16))) float pa[4][MAXG];
+
+  const int split = blockIdx.x, g = blockIdx.y;
+  const int GQ = H / n_kv;
+  const int tid = threadIdx.x, lane = tid % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
+  const int lg = lane >> 4, j = lane & 15;
+  const int ts = lane / LPT, hg = lane % LPT;
+  const int group = blockIdx.z / ga.n_sub;
+  const int sbase = (blockIdx.z % ga.n_sub * 4 + wave) * (MAXG / GQ);
+  const int t0 = split * span;
+  const int t1 = min(t0 + span, group_shared(pos, group, ga, max_len));
+  if (t0 >= t1) return;                       // the whole workgroup
+  const int ntiles = (t1 - t0 + DT - 1) / DT;
+  const int src = group * ga.G;               // the group leader's cache rows
+  const size_t head_base = ((size_t)src * n_kv + g) * max_len;
+  const bf16_t* kb = kc + head_base * HD;
+  const bf16_t* vb = vc + head_base * HD;
+  const int ncols = min(MAXG / GQ, max(ga.G - sbase, 0)) * GQ;
+
+  bf16x8_t qf[QSTEPS];
+  {
+    const int jc = min(j, max(ncols, 1) - 1);
+    const int qrow = (src + min(sbase + jc / GQ, ga.G - 1)) * H + g * GQ + jc % GQ;
+    const bf16_t* qp = q + (size_t)qrow * HD + lg * 8;
+#pragma unroll
+    for (int st = 0; st < QSTEPS; ++st) {
+      u32x4_t v = *(const u32x4_t*)(qp + st * 32);
+      if (j >= ncols) v = (u32x4_t){0u, 0u, 0u, 0u};
+      qf[st] = __builtin_bit_cast(bf16x8_t, v);
+    }
+  }
+  // the query loads complete before the copies start (the copies are counted by
+  // hand below): an empty use of the fragments holds them here
+#pragma unroll
+  for (int st = 0; st < QSTEPS; ++st) asm volatile("" ::"v"(qf[st]));
+
+  // Tile t (clamped to the last) into stage t % NSTG: copy c of K fills rows
+  // PPW c .. PPW c + PPW - 1, lane l the 16-byte slot l % LPT of row PPW c + l / LPT
+  // with source piece slot ^ swizzle; V rows are copied as they are.  Positions
+  // past t1 - 1 read position t1 - 1 (masked scores, finite values).
+  auto copy_tile = [&](int t) __attribute__((always_inline)) {
+    const int stg = t % NSTG, tb = t0 + t * DT;
+#pragma unroll
+    for (int c0 = 0; c0 < NCP; c0 += 4) {
+      const int c = c0 + wave;
+      const int row = c * PPW + lane / LPT, slot = lane % LPT;
+      const size_t p = (size_t)min(tb + row, t1 - 1) * HD;
+      dma16_nt(kb + p + (slot ^ kstage_swz<HD>(row)) * 8, lds_addr(&ks[stg][c * 512]));
+      dma16_nt(vb + p + slot * 8, lds_addr(&vs[stg][c * 512]));
+    }
+  };
+
+  float m = -1e30f, l = 0.f;
+  float o[MAXG][8];
+#pragma unroll
+  for (int h = 0; h < MAXG; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
+
+  auto compute = [&](int stg, int t) __attribute__((always_inline)) {
+    const int tb = t0 + t * DT;
+    const bf16_t* ksb = &ks[stg][0];
+    const bf16_t* vsb = &vs[stg][0];
+    float sv[NG][4];
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int grp = 0; grp < NG; ++grp) {
+      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+      const int row = grp * 16 + j;
+#pragma unroll
+      for (int st = 0; st < QSTEPS; ++st) {
+        const bf16x8_t kf =
+            *(const bf16x8_t*)(ksb + row * HD + ((st * 4 + lg) ^ kstage_swz<HD>(row)) * 8);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[st], acc, 0, 0, 0);
+      }
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const float sc = (tb + grp * 16 + lg * 4 + v < t1) ? acc[v] * scale : -INFINITY;
+        sv[grp][v] = sc;
+        tmax = fmaxf(tmax, sc);
+      }
+    }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float mnew = fmaxf(m, tmax);
+    const float alpha = __expf(m - mnew);
+    m = mnew;
+    float ps = 0.f;
+#pragma unroll
+    for (int grp = 0; grp < NG; ++grp)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const float pv = __expf(sv[grp][v] - mnew);
+        ps += pv;
+        if (j < MAXG) pw[wave][grp * 16 + lg * 4 + v][j] = pv;
+      }
+    l = l * alpha + ps;
+    if (lg == 0 && j < MAXG) pa[wave][j] = alpha;
+    __builtin_amdgcn_wave_barrier();
+    float al[MAXG];
+#pragma unroll
+    for (int h = 0; h < MAXG; h += 4) {
+      const float4 a4 = *(const float4*)&pa[wave][h];
+      al[h] = a4.x; al[h + 1] = a4.y; al[h + 2] = a4.z; al[h + 3] = a4.w;
+    }
+#pragma unroll
+    for (int h = 0; h < MAXG; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[h][e] *= al[h];
+#pragma unroll
+    for (int iv = 0; iv < NVT; ++iv) {
+      const u32x4_t raw = *(const u32x4_t*)(vsb + (iv * PPW + ts) * HD + hg * 8);
+      float vv[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        vv[2 * e] = __uint_as_float(raw[e] << 16);
+        vv[2 * e + 1] = __uint_as_float(raw[e] & 0xffff0000u);
+      }
+      float pp[MAXG];
+#pragma unroll
+      for (int h = 0; h < MAXG; h += 4) {
+        const float4 p4 = *(const float4*)&pw[wave][iv * PPW + ts][h];
+        pp[h] = p4.x; pp[h + 1] = p4.y; pp[h + 2] = p4.z; pp[h + 3] = p4.w;
+      }
+#pragma unroll
+      for (int h = 0; h < MAXG; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[h][e] = fmaf(pp[h], vv[e], o[h][e]);
+    }
+    __builtin_amdgcn_wave_barrier();
+  };
+
+  // ring: tiles t .. t + NSTG - 2 in flight when tile t is awaited
+#pragma unroll
+  for (int t = 0; t < NSTG - 1; ++t) copy_tile(min(t, ntiles - 1));
+  for (int t = 0; t < ntiles; ++t) {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NSTG - 2) * CPW) : "memory");   // this wave's copies of t
+    __syncthreads();   // every wave's copies of t landed; every wave is done with tile t - 1
+    copy_tile(min(t + NSTG - 1, ntiles - 1));                      // into tile t - 1's stage
+    if (ncols > 0) compute(t % NSTG, t);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the repeated tail copies land before exit
+  if (ncols == 0) return;
+
+  // wave totals: o over the positions of a 1 KB row group, l over the k-groups;
+  // column h is head g * GQ + h % GQ of batch row src + sbase + h / GQ
+#pragma unroll
+  for (int h = 0; h < MAXG; ++h)
+    if (h < ncols) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float x = o[h][e];
+#pragma unroll
+        for (int off = LPT; off < 64; off <<= 1) x += __shfl_xor(x, off, 64);
+        o[h][e] = x;
+      }
+    }
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  auto row_of = [&](int h) {
+    return ((size_t)(src + sbase + h / GQ) * H + g * GQ + h % GQ) * S + split;
+  };
+  if (ts == 0) {
+#pragma unroll
+    for (int h = 0; h < MAXG; ++h)
+      if (h < ncols) {
+        float* po = part_o + row_of(h) * HD + hg * 8;
+        *(float4*)po = make_float4(o[h][0], o[h][1], o[h][2], o[h][3]);
+        *(float4*)(po + 4) = make_float4(o[h][4], o[h][5], o[h][6], o[h][7]);
+      }
+  }
+  if (lg == 0 && j < ncols) {
+    const size_t row = row_of(j);
+    part_ml[row * 2] = m;
+    part_ml[row * 2 + 1] = l;
   }
 }
 
@@ -370,12 +540,12 @@ size_t decode_attn_part_floats_max(int B, int H, int n_kv, int hd, int max_len) 
   return (size_t)B * H * (MAX_CHUNKS + p.splits) * (hd + 2);
 }
 
-template <int HD, int MAXG, bool GRP>
+template <int HD, int MAXG>
 static void launch_decode(dim3 grid, hipStream_t st, const void* q, const void* kc,
                           const void* vc, const int32_t* pos, int H, int n_kv, int max_len, int S,
                           int span, float scale, float* part_o, float* part_ml, void* out,
                           int pack_nb, DecodeGroup ga, int split_base) {
-  k_attn_decode_bf16<HD, MAXG, GRP><<<grid, 256, 0, st>>>(
+  k_attn_decode_bf16<HD, MAXG><<<grid, 256, 0, st>>>(
       (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, H, n_kv, max_len, S, span,
       scale, part_o, part_ml, (bf16_t*)out, pack_nb, ga, split_base);
 }
@@ -395,17 +565,18 @@ static hipError_t attn_decode_hd(const void* q, const void* kc, const void* vc,
   if (grouped) {
     Prof pf("attn_prefix", st);
     dim3 grid(p.chunks, n_kv, B / p.G * p.n_sub);
-    launch_decode<HD, 8, true>(grid, st, q, kc, vc, pos, H, n_kv, max_len, S, p.span_p, scale,
-                               part_o, part_ml, out, pack_nb, ga, 0);
+    k_attn_prefix_bf16<HD><<<grid, 256, 0, st>>>(
+        (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, H, n_kv, max_len, S,
+        p.span_p, scale, part_o, part_ml, ga);
   }
   {
     Prof pf("attn_decode", st);
     dim3 grid(p.splits, n_kv, B);
     if (gq <= 4)
-      launch_decode<HD, 4, false>(grid, st, q, kc, vc, pos, H, n_kv, max_len, S, p.tc, scale,
+      launch_decode<HD, 4>(grid, st, q, kc, vc, pos, H, n_kv, max_len, S, p.tc, scale,
                                   part_o, part_ml, out, pack_nb, ga, p.chunks);
     else
-      launch_decode<HD, 8, false>(grid, st, q, kc, vc, pos, H, n_kv, max_len, S, p.tc, scale,
+      launch_decode<HD, 8>(grid, st, q, kc, vc, pos, H, n_kv, max_len, S, p.tc, scale,
                                   part_o, part_ml, out, pack_nb, ga, p.chunks);
   }
   if (S > 1) {
