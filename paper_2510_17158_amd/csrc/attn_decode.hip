@@ -41,8 +41,8 @@ constexpr int MAX_CHUNKS = 16;    // prompt chunks of a grouped step, at most
 
 // Grouped rollout: G samples per group (0 = every row on its own), prompt
 // positions shared below prefix_len, n_sub workgroups per group and chunk (each
-// holding 4 waves x 8 / GQ samples).
-struct DecodeGroup { int G, prefix_len, n_sub; };
+// holding 4 waves x 8 / GQ samples), `chunks` prompt chunks of span_p positions.
+struct DecodeGroup { int G, prefix_len, n_sub, chunks, span_p; };
 
 // Positions the group of batch row b shares: prefix_len, cut to the context
 // every member has reached (so a shared position exists for all of them).
@@ -61,7 +61,9 @@ struct KVTile {
 
 // ---------------------------------------------------------------- decode, bf16
 // blockIdx = (span, kv head, batch row); the spans start at the group's shared
-// length when ga.G > 0 and write partial row split_base + span of S.
+// length when ga.G > 0 and write partial row split_base + span of S.  A grouped
+// step whose generated positions are one span (S = chunks + 1) merges the prompt
+// chunks' partials here and writes the output (no merge kernel).
 template <int HD, int MAXG>
 __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
@@ -88,10 +90,12 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   // positions [t0, t1) of this workgroup
   const int src = blockIdx.z;
   const int ctx = min(pos[src], max_len - 1) + 1;
-  const int t0 = (ga.G > 0 ? group_shared(pos, src / ga.G, ga, max_len) : 0) + split * span;
-  if (t0 >= ctx) return;
+  const int base = ga.G > 0 ? group_shared(pos, src / ga.G, ga, max_len) : 0;
+  const bool fold = ga.G > 0 && S == ga.chunks + 1;
+  const int t0 = base + split * span;
+  if (t0 >= ctx && !fold) return;             // (folding still merges the prompt part)
   const int t1 = min(t0 + span, ctx);
-  const int ntiles = (t1 - t0 + DT - 1) / DT;
+  const int ntiles = t1 > t0 ? (t1 - t0 + DT - 1) / DT : 0;
   const int nmine = ntiles > wave ? (ntiles - wave + 3) / 4 : 0;
   const size_t head_base = ((size_t)src * n_kv + g) * max_len;
   const bf16_t* kb = kc + head_base * HD;
@@ -242,6 +246,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   }
   __syncthreads();
   // merge the 4 waves (fixed order)
+#pragma unroll 2
   for (int i = tid; i < GQ * HD; i += 256) {
     const int h = i / HD, e = i % HD;
     const float M = fmaxf(fmaxf(wm[0][h], wm[1][h]), fmaxf(wm[2][h], wm[3][h]));
@@ -252,7 +257,32 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
       x = fmaf(c, red[w][i], x);
       L = fmaf(c, wl[w][h], L);
     }
-    if (S == 1) {
+    if (fold) {
+      // the prompt chunks below the shared length (partial rows 0 .. chunks-1),
+      // all loads issued before any is used
+      const size_t r0 = ((size_t)src * H + g * GQ + h) * S;
+      float cm[MAX_CHUNKS], cl[MAX_CHUNKS], co[MAX_CHUNKS];
+#pragma unroll
+      for (int c = 0; c < MAX_CHUNKS; ++c) {
+        const bool u = c < ga.chunks && c * ga.span_p < base;
+        cm[c] = u ? part_ml[(r0 + c) * 2] : -INFINITY;
+        cl[c] = u ? part_ml[(r0 + c) * 2 + 1] : 0.f;
+        co[c] = u ? part_o[(r0 + c) * HD + e] : 0.f;
+      }
+      float Mt = M;
+#pragma unroll
+      for (int c = 0; c < MAX_CHUNKS; ++c) Mt = fmaxf(Mt, cm[c]);
+      const float sc = __expf(M - Mt);
+      x *= sc;
+      L *= sc;
+#pragma unroll
+      for (int c = 0; c < MAX_CHUNKS; ++c) {
+        const float w = __expf(cm[c] - Mt);   // 0 for unused chunks
+        x = fmaf(co[c], w, x);
+        L = fmaf(cl[c], w, L);
+      }
+    }
+    if (S == 1 || fold) {
       const int k = (g * GQ + h) * HD + e;
       out[pack_nb ? act_frag_index(src, k, pack_nb) : (size_t)src * H * HD + k] = f2bf(x / L);
     } else {
@@ -269,41 +299,47 @@ __device__ __forceinline__ void dma16_nt(const bf16_t* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off nt" ::"s"(lds), "v"(g)
                : "memory");
 }
-// K stage rows: the 16 rows one fragment read touches at one 16-byte piece fall
-// in 16 distinct bank groups (hd 128: 256-byte rows, piece ^ row % 16; hd 64:
-// 128-byte rows, piece ^ (row / 2) % 8, rows 2i and 2i + 1 in the two halves).
+// Stage swizzles (16-byte pieces XOR-ed per row).  K: the 16 rows one fragment
+// read touches, 8 (i >> 2) + 4 b + (i & 3) for lane row i, fall in 16 distinct
+// bank groups (hd 128: 256-byte rows, the swizzle takes row bits 0-1 and 3-4;
+// hd 64: 128-byte rows, bits 1 and 3-4).  V: the four position groups 8 g + e
+// one transposed read touches sit 2 pieces apart (row bits 3-4).
 template <int HD>
-__device__ __forceinline__ int kstage_swz(int r) { return HD == 128 ? (r & 15) : ((r >> 1) & 7); }
+__device__ __forceinline__ int kstage_swz(int r) {
+  return HD == 128 ? ((r & 3) | (((r >> 3) & 3) << 2)) : (((r >> 1) & 1) | (((r >> 3) & 3) << 1));
+}
+__device__ __forceinline__ int vstage_swz(int r) { return ((r >> 3) & 3) << 1; }
 
 // blockIdx = (chunk, kv head, group x n_sub).  Wave w of sub-block u takes the
 // samples (4 u + w) * 8 / GQ .. + 8 / GQ of the group (MFMA columns: GQ heads of
 // each); a wave without samples still shares the copies and barriers.
+// Per 32-position tile and wave: S^T = K Q^T on MFMA with the K rows of each
+// 16-row block permuted (block b, row i -> position 8 (i >> 2) + 4 b + (i & 3)),
+// so a lane's eight scores of its column are positions 8 g .. 8 g + 7: exactly
+// the B operand of O^T += V^T P^T, which takes P as two bf16 terms (hi + lo: no
+// rounding point added) and V^T fragments read transposed from the stage.
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const int32_t* __restrict__ pos, int H, int n_kv, int max_len, int S, int span, float scale,
     float* __restrict__ part_o, float* __restrict__ part_ml, DecodeGroup ga) {
-  constexpr int MAXG = 8;             // MFMA columns per wave
+  constexpr int MAXG = 8;             // query columns per wave (of the 16 MFMA columns)
   constexpr int QSTEPS = HD / 32;
-  constexpr int LPT = HD / 8;         // lanes per position in P.V (16-byte pieces per row)
-  constexpr int PPW = 64 / LPT;       // positions per 1 KB of a tile
-  constexpr int NVT = DT / PPW;       // V reads per tile and lane
-  constexpr int NG = DT / 16;
-  constexpr int NCP = DT / PPW;       // 1 KB copies per K (and per V) tile
+  constexpr int HB = HD / 16;         // 16-row head-dim blocks of O^T
+  constexpr int PPR = HD / 8;         // 16-byte pieces per row
+  constexpr int RPC = 64 / PPR;       // rows per 1 KB copy
+  constexpr int NCP = DT / RPC;       // copies per K (and per V) tile
   constexpr int NSTG = 4;             // LDS ring stages
   constexpr int CPW = 2 * NCP / 4;    // copies per wave and tile
-  static_assert(NCP % 4 == 0, "copies dealt evenly to the 4 waves");
+  static_assert(DT == 32 && NCP % 4 == 0, "one 32-deep MFMA step per tile; copies dealt evenly");
   __shared__ __attribute__((aligned(1024))) bf16_t ks[NSTG][DT * HD];
   __shared__ __attribute__((aligned(1024))) bf16_t vs[NSTG][DT * HD];
-  __shared__ __attribute__((aligned(16))) float pw[4][DT][MAXG];
-  __shared__ __attribute__((aligned(16))) float pa[4][MAXG];
 
   const int split = blockIdx.x, g = blockIdx.y;
   const int GQ = H / n_kv;
   const int tid = threadIdx.x, lane = tid % 64;
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
   const int lg = lane >> 4, j = lane & 15;
-  const int ts = lane / LPT, hg = lane % LPT;
   const int group = blockIdx.z / ga.n_sub;
   const int sbase = (blockIdx.z % ga.n_sub * 4 + wave) * (MAXG / GQ);
   const int t0 = split * span;
@@ -316,6 +352,8 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
   const bf16_t* vb = vc + head_base * HD;
   const int ncols = min(MAXG / GQ, max(ga.G - sbase, 0)) * GQ;
 
+  // Q as the B operand: column j = head g * GQ + j % GQ of batch row
+  // src + sbase + j / GQ (zero past ncols); MFMA step st takes piece 4 st + lg
   bf16x8_t qf[QSTEPS];
   {
     const int jc = min(j, max(ncols, 1) - 1);
@@ -333,100 +371,96 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
 #pragma unroll
   for (int st = 0; st < QSTEPS; ++st) asm volatile("" ::"v"(qf[st]));
 
-  // Tile t (clamped to the last) into stage t % NSTG: copy c of K fills rows
-  // PPW c .. PPW c + PPW - 1, lane l the 16-byte slot l % LPT of row PPW c + l / LPT
-  // with source piece slot ^ swizzle; V rows are copied as they are.  Positions
-  // past t1 - 1 read position t1 - 1 (masked scores, finite values).
+  // Tile t (clamped to the last) into stage t % NSTG: copy c fills rows
+  // RPC c .. RPC c + RPC - 1, lane l the 16-byte slot l % PPR of row RPC c + l / PPR
+  // with source piece slot ^ swizzle.  Positions past t1 - 1 read position t1 - 1
+  // (masked scores, finite values).
   auto copy_tile = [&](int t) __attribute__((always_inline)) {
     const int stg = t % NSTG, tb = t0 + t * DT;
 #pragma unroll
     for (int c0 = 0; c0 < NCP; c0 += 4) {
       const int c = c0 + wave;
-      const int row = c * PPW + lane / LPT, slot = lane % LPT;
+      const int row = c * RPC + lane / PPR, slot = lane % PPR;
       const size_t p = (size_t)min(tb + row, t1 - 1) * HD;
       dma16_nt(kb + p + (slot ^ kstage_swz<HD>(row)) * 8, lds_addr(&ks[stg][c * 512]));
-      dma16_nt(vb + p + slot * 8, lds_addr(&vs[stg][c * 512]));
+      dma16_nt(vb + p + (slot ^ vstage_swz(row)) * 8, lds_addr(&vs[stg][c * 512]));
     }
   };
 
-  float m = -1e30f, l = 0.f;
-  float o[MAXG][8];
+  float m = -1e30f, l = 0.f;          // column j's reference maximum, this lane's partial sum
+  f32x4_t oacc[HB];                   // O^T: rows 16 hb + 4 lg + v of column j
 #pragma unroll
-  for (int h = 0; h < MAXG; ++h)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
+  for (int hb = 0; hb < HB; ++hb) oacc[hb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
   auto compute = [&](int stg, int t) __attribute__((always_inline)) {
     const int tb = t0 + t * DT;
     const bf16_t* ksb = &ks[stg][0];
-    const bf16_t* vsb = &vs[stg][0];
-    float sv[NG][4];
-    float tmax = -INFINITY;
+    const uint16_t* vsb = (const uint16_t*)&vs[stg][0];
+    f32x4_t sacc[2];
 #pragma unroll
-    for (int grp = 0; grp < NG; ++grp) {
-      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-      const int row = grp * 16 + j;
+    for (int b = 0; b < 2; ++b) {
+      const int row = 8 * (j >> 2) + 4 * b + (j & 3);      // this lane's A row
+      sacc[b] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < QSTEPS; ++st) {
         const bf16x8_t kf =
             *(const bf16x8_t*)(ksb + row * HD + ((st * 4 + lg) ^ kstage_swz<HD>(row)) * 8);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[st], acc, 0, 0, 0);
-      }
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float sc = (tb + grp * 16 + lg * 4 + v < t1) ? acc[v] * scale : -INFINITY;
-        sv[grp][v] = sc;
-        tmax = fmaxf(tmax, sc);
+        sacc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[st], sacc[b], 0, 0, 0);
       }
     }
+    // lane (j, lg): sacc[b][v] is position 8 lg + 4 b + v of the tile
+    float sv[8];
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const float sc = (tb + 8 * lg + 4 * b + v < t1) ? sacc[b][v] * scale : -INFINITY;
+        sv[4 * b + v] = sc;
+        tmax = fmaxf(tmax, sc);
+      }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
     const float mnew = fmaxf(m, tmax);
-    const float alpha = __expf(m - mnew);
+    // rescale only when some column's maximum moved (otherwise the factor is 1)
+    if (__builtin_amdgcn_ballot_w64(mnew != m)) {
+      const float alpha = __expf(m - mnew);
+      l *= alpha;
+#pragma unroll
+      for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) oacc[hb][v] *= alpha;
+    }
     m = mnew;
-    float ps = 0.f;
+    bf16x8_t ph, pl;
 #pragma unroll
-    for (int grp = 0; grp < NG; ++grp)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float pv = __expf(sv[grp][v] - mnew);
-        ps += pv;
-        if (j < MAXG) pw[wave][grp * 16 + lg * 4 + v][j] = pv;
-      }
-    l = l * alpha + ps;
-    if (lg == 0 && j < MAXG) pa[wave][j] = alpha;
-    __builtin_amdgcn_wave_barrier();
-    float al[MAXG];
-#pragma unroll
-    for (int h = 0; h < MAXG; h += 4) {
-      const float4 a4 = *(const float4*)&pa[wave][h];
-      al[h] = a4.x; al[h + 1] = a4.y; al[h + 2] = a4.z; al[h + 3] = a4.w;
+    for (int e = 0; e < 8; e += 2) {
+      const float p0 = __expf(sv[e] - mnew), p1 = __expf(sv[e + 1] - mnew);
+      l += p0;
+      l += p1;
+      const bf16x2_t hi = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
+      const bf16x2_t lo =
+          __builtin_convertvector((f32x2_t){p0 - (float)hi[0], p1 - (float)hi[1]}, bf16x2_t);
+      ph[e] = hi[0]; ph[e + 1] = hi[1];
+      pl[e] = lo[0]; pl[e + 1] = lo[1];
     }
+    // V^T fragment of block hb: row 16 hb + j (a head dimension), positions
+    // 8 lg .. 8 lg + 7, read as 2-byte elements from the row-major stage
 #pragma unroll
-    for (int h = 0; h < MAXG; ++h)
+    for (int hb = 0; hb < HB; ++hb) {
+      const int d = hb * 16 + j;
+      u32x4_t w;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[h][e] *= al[h];
-#pragma unroll
-    for (int iv = 0; iv < NVT; ++iv) {
-      const u32x4_t raw = *(const u32x4_t*)(vsb + (iv * PPW + ts) * HD + hg * 8);
-      float vv[8];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vv[2 * e] = __uint_as_float(raw[e] << 16);
-        vv[2 * e + 1] = __uint_as_float(raw[e] & 0xffff0000u);
+      for (int e = 0; e < 8; e += 2) {
+        const int r0 = 8 * lg + e, r1 = r0 + 1;
+        const uint32_t a = vsb[r0 * HD + (((d >> 3) ^ vstage_swz(r0)) << 3) + (d & 7)];
+        const uint32_t c = vsb[r1 * HD + (((d >> 3) ^ vstage_swz(r1)) << 3) + (d & 7)];
+        w[e / 2] = a | (c << 16);
       }
-      float pp[MAXG];
-#pragma unroll
-      for (int h = 0; h < MAXG; h += 4) {
-        const float4 p4 = *(const float4*)&pw[wave][iv * PPW + ts][h];
-        pp[h] = p4.x; pp[h + 1] = p4.y; pp[h + 2] = p4.z; pp[h + 3] = p4.w;
-      }
-#pragma unroll
-      for (int h = 0; h < MAXG; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[h][e] = fmaf(pp[h], vv[e], o[h][e]);
+      const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, w);
+      oacc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph, oacc[hb], 0, 0, 0);
+      oacc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, oacc[hb], 0, 0, 0);
     }
-    __builtin_amdgcn_wave_barrier();
   };
 
   // ring: tiles t .. t + NSTG - 2 in flight when tile t is awaited
@@ -441,37 +475,18 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the repeated tail copies land before exit
   if (ncols == 0) return;
 
-  // wave totals: o over the positions of a 1 KB row group, l over the k-groups;
-  // column h is head g * GQ + h % GQ of batch row src + sbase + h / GQ
-#pragma unroll
-  for (int h = 0; h < MAXG; ++h)
-    if (h < ncols) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float x = o[h][e];
-#pragma unroll
-        for (int off = LPT; off < 64; off <<= 1) x += __shfl_xor(x, off, 64);
-        o[h][e] = x;
-      }
-    }
+  // column j is head g * GQ + j % GQ of batch row src + sbase + j / GQ
   l += __shfl_xor(l, 16, 64);
   l += __shfl_xor(l, 32, 64);
-  auto row_of = [&](int h) {
-    return ((size_t)(src + sbase + h / GQ) * H + g * GQ + h % GQ) * S + split;
-  };
-  if (ts == 0) {
+  if (j < ncols) {
+    const size_t row = ((size_t)(src + sbase + j / GQ) * H + g * GQ + j % GQ) * S + split;
 #pragma unroll
-    for (int h = 0; h < MAXG; ++h)
-      if (h < ncols) {
-        float* po = part_o + row_of(h) * HD + hg * 8;
-        *(float4*)po = make_float4(o[h][0], o[h][1], o[h][2], o[h][3]);
-        *(float4*)(po + 4) = make_float4(o[h][4], o[h][5], o[h][6], o[h][7]);
-      }
-  }
-  if (lg == 0 && j < ncols) {
-    const size_t row = row_of(j);
-    part_ml[row * 2] = m;
-    part_ml[row * 2 + 1] = l;
+    for (int hb = 0; hb < HB; ++hb)
+      *(f32x4_t*)(part_o + row * HD + hb * 16 + 4 * lg) = oacc[hb];
+    if (lg == 0) {
+      part_ml[row * 2] = m;
+      part_ml[row * 2 + 1] = l;
+    }
   }
 }
 
@@ -561,7 +576,7 @@ static hipError_t attn_decode_hd(const void* q, const void* kc, const void* vc,
   const int S = p.chunks + p.splits;      // partial rows per (row, head)
   float* part_o = S > 1 ? part : nullptr;
   float* part_ml = S > 1 ? part + (size_t)B * H * S * HD : nullptr;
-  const DecodeGroup ga{p.G, p.prefix_len, p.n_sub};
+  const DecodeGroup ga{p.G, p.prefix_len, p.n_sub, p.chunks, p.span_p};
   if (grouped) {
     Prof pf("attn_prefix", st);
     dim3 grid(p.chunks, n_kv, B / p.G * p.n_sub);
@@ -579,7 +594,8 @@ static hipError_t attn_decode_hd(const void* q, const void* kc, const void* vc,
       launch_decode<HD, 8>(grid, st, q, kc, vc, pos, H, n_kv, max_len, S, p.tc, scale,
                                   part_o, part_ml, out, pack_nb, ga, p.chunks);
   }
-  if (S > 1) {
+  // grouped with one span of generated positions: merged by the per-row kernel
+  if (S > 1 && !(grouped && p.splits == 1)) {
     Prof pf("attn_combine", st);
     k_attn_combine<HD><<<dim3(H, B), HD, 0, st>>>(part_o, part_ml, pos, H, max_len, S, p.tc,
                                                   (bf16_t*)out, pack_nb, ga, p.chunks, p.span_p);
