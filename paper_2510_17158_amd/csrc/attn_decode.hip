@@ -18,12 +18,14 @@
 // prompt K/V identical): the prompt positions are read once per group.  A
 // prefix launch, one workgroup per (prompt chunk, kv head, group), copies the
 // group leader's K and V tiles straight into a 4-stage LDS ring (one copy per
-// workgroup, three tiles ahead, one barrier per tile) and gives each wave the
-// query heads of its own samples (8 MFMA columns: two samples of 4 heads at the
-// 7B shape); each wave runs every tile of the chunk with the same scores,
-// softmax and P.V as above and writes its columns' (max, sum, o) as one span.
-// The per-sequence launch then covers the generated positions only, and the
-// merge takes the prompt chunks first, then the generated spans.
+// workgroup, three tiles ahead, one barrier per tile).  Its query columns are
+// the heads of up to 32 / GQ samples (all 8 samples x 4 heads at the 7B shape),
+// and both products run on MFMA: every wave computes the scores and softmax of
+// all the columns and P.V for a quarter of the head dimension; the (max, sum,
+// o) of each column form one span.  The per-sequence launch then covers the
+// generated positions only and merges the prompt chunks into its result when
+// those are a single span (else a merge kernel takes the prompt chunks first,
+// then the generated spans).
 //
 // fp32 models use the plain vector kernel of the prefill path.
 #include <algorithm>
@@ -41,7 +43,7 @@ constexpr int MAX_CHUNKS = 16;    // prompt chunks of a grouped step, at most
 
 // Grouped rollout: G samples per group (0 = every row on its own), prompt
 // positions shared below prefix_len, n_sub workgroups per group and chunk (each
-// holding 4 waves x 8 / GQ samples), `chunks` prompt chunks of span_p positions.
+// holding 32 / GQ samples), `chunks` prompt chunks of span_p positions.
 struct DecodeGroup { int G, prefix_len, n_sub, chunks, span_p; };
 
 // Positions the group of batch row b shares: prefix_len, cut to the context
@@ -310,28 +312,30 @@ __device__ __forceinline__ int kstage_swz(int r) {
 }
 __device__ __forceinline__ int vstage_swz(int r) { return ((r >> 3) & 3) << 1; }
 
-// blockIdx = (chunk, kv head, group x n_sub).  Wave w of sub-block u takes the
-// samples (4 u + w) * 8 / GQ .. + 8 / GQ of the group (MFMA columns: GQ heads of
-// each); a wave without samples still shares the copies and barriers.
-// Per 32-position tile and wave: S^T = K Q^T on MFMA with the K rows of each
-// 16-row block permuted (block b, row i -> position 8 (i >> 2) + 4 b + (i & 3)),
-// so a lane's eight scores of its column are positions 8 g .. 8 g + 7: exactly
-// the B operand of O^T += V^T P^T, which takes P as two bf16 terms (hi + lo: no
-// rounding point added) and V^T fragments read transposed from the stage.
+// blockIdx = (chunk, kv head, group x n_sub).  Sub-block u takes the 32 / GQ
+// samples u * (32 / GQ) .. of the group: query column c (two MFMA blocks of 16)
+// is head g * GQ + c % GQ of sample c / GQ.  Every wave computes the scores and
+// softmax of all the columns (the same values in each wave) and O^T for its
+// quarter of the head dimension, so a wave reads a quarter of the V^T fragments.
+// Per 32-position tile: S^T = K Q^T on MFMA with the K rows of each 16-row block
+// permuted (block b, row i -> position 8 (i >> 2) + 4 b + (i & 3)), so a lane's
+// eight scores of its column are positions 8 g .. 8 g + 7: exactly the B operand
+// of O^T += V^T P^T, which takes P as two bf16 terms (hi + lo: no rounding point
+// added) and V^T fragments read transposed from the stage.
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const int32_t* __restrict__ pos, int H, int n_kv, int max_len, int S, int span, float scale,
     float* __restrict__ part_o, float* __restrict__ part_ml, DecodeGroup ga) {
-  constexpr int MAXG = 8;             // query columns per wave (of the 16 MFMA columns)
   constexpr int QSTEPS = HD / 32;
   constexpr int HB = HD / 16;         // 16-row head-dim blocks of O^T
+  constexpr int HBW = HB / 4;         // blocks per wave
   constexpr int PPR = HD / 8;         // 16-byte pieces per row
   constexpr int RPC = 64 / PPR;       // rows per 1 KB copy
   constexpr int NCP = DT / RPC;       // copies per K (and per V) tile
   constexpr int NSTG = 4;             // LDS ring stages
   constexpr int CPW = 2 * NCP / 4;    // copies per wave and tile
-  static_assert(DT == 32 && NCP % 4 == 0, "one 32-deep MFMA step per tile; copies dealt evenly");
+  static_assert(DT == 32 && NCP % 4 == 0 && HB % 4 == 0, "tile, copy and block split");
   __shared__ __attribute__((aligned(1024))) bf16_t ks[NSTG][DT * HD];
   __shared__ __attribute__((aligned(1024))) bf16_t vs[NSTG][DT * HD];
 
@@ -341,7 +345,9 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
   const int lg = lane >> 4, j = lane & 15;
   const int group = blockIdx.z / ga.n_sub;
-  const int sbase = (blockIdx.z % ga.n_sub * 4 + wave) * (MAXG / GQ);
+  const int spb = 32 / GQ;                                   // samples per sub-block
+  const int s0 = blockIdx.z % ga.n_sub * spb;                // its first sample
+  const int ncols = min(spb, ga.G - s0) * GQ;                // valid columns (> 0)
   const int t0 = split * span;
   const int t1 = min(t0 + span, group_shared(pos, group, ga, max_len));
   if (t0 >= t1) return;                       // the whole workgroup
@@ -350,26 +356,28 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
   const size_t head_base = ((size_t)src * n_kv + g) * max_len;
   const bf16_t* kb = kc + head_base * HD;
   const bf16_t* vb = vc + head_base * HD;
-  const int ncols = min(MAXG / GQ, max(ga.G - sbase, 0)) * GQ;
 
-  // Q as the B operand: column j = head g * GQ + j % GQ of batch row
-  // src + sbase + j / GQ (zero past ncols); MFMA step st takes piece 4 st + lg
-  bf16x8_t qf[QSTEPS];
-  {
-    const int jc = min(j, max(ncols, 1) - 1);
-    const int qrow = (src + min(sbase + jc / GQ, ga.G - 1)) * H + g * GQ + jc % GQ;
-    const bf16_t* qp = q + (size_t)qrow * HD + lg * 8;
+  // Q as the B operand of column block cb: column j -> c = 16 cb + j (zero past
+  // ncols); MFMA step st takes piece 4 st + lg
+  bf16x8_t qf[2][QSTEPS];
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) {
+    const int c = min(16 * cb + j, ncols - 1);
+    const bf16_t* qp =
+        q + ((size_t)(src + s0 + c / GQ) * H + g * GQ + c % GQ) * HD + lg * 8;
 #pragma unroll
     for (int st = 0; st < QSTEPS; ++st) {
       u32x4_t v = *(const u32x4_t*)(qp + st * 32);
-      if (j >= ncols) v = (u32x4_t){0u, 0u, 0u, 0u};
-      qf[st] = __builtin_bit_cast(bf16x8_t, v);
+      if (16 * cb + j >= ncols) v = (u32x4_t){0u, 0u, 0u, 0u};
+      qf[cb][st] = __builtin_bit_cast(bf16x8_t, v);
     }
   }
   // the query loads complete before the copies start (the copies are counted by
   // hand below): an empty use of the fragments holds them here
 #pragma unroll
-  for (int st = 0; st < QSTEPS; ++st) asm volatile("" ::"v"(qf[st]));
+  for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+    for (int st = 0; st < QSTEPS; ++st) asm volatile("" ::"v"(qf[cb][st]));
 
   // Tile t (clamped to the last) into stage t % NSTG: copy c fills rows
   // RPC c .. RPC c + RPC - 1, lane l the 16-byte slot l % PPR of row RPC c + l / PPR
@@ -387,68 +395,84 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
     }
   };
 
-  float m = -1e30f, l = 0.f;          // column j's reference maximum, this lane's partial sum
-  f32x4_t oacc[HB];                   // O^T: rows 16 hb + 4 lg + v of column j
+  float m[2] = {-1e30f, -1e30f}, l[2] = {0.f, 0.f};   // per column block: column j
+  f32x4_t oacc[HBW][2];   // O^T rows 16 (HBW wave + hb) + 4 lg + v of column j of block cb
 #pragma unroll
-  for (int hb = 0; hb < HB; ++hb) oacc[hb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  for (int hb = 0; hb < HBW; ++hb)
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) oacc[hb][cb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
   auto compute = [&](int stg, int t) __attribute__((always_inline)) {
     const int tb = t0 + t * DT;
     const bf16_t* ksb = &ks[stg][0];
     const uint16_t* vsb = (const uint16_t*)&vs[stg][0];
-    f32x4_t sacc[2];
+    f32x4_t sacc[2][2];   // [b][cb]
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const int row = 8 * (j >> 2) + 4 * b + (j & 3);      // this lane's A row
-      sacc[b] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) sacc[b][cb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < QSTEPS; ++st) {
         const bf16x8_t kf =
             *(const bf16x8_t*)(ksb + row * HD + ((st * 4 + lg) ^ kstage_swz<HD>(row)) * 8);
-        sacc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[st], sacc[b], 0, 0, 0);
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+          sacc[b][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[cb][st], sacc[b][cb], 0, 0, 0);
       }
     }
-    // lane (j, lg): sacc[b][v] is position 8 lg + 4 b + v of the tile
-    float sv[8];
-    float tmax = -INFINITY;
+    // lane (j, lg): sacc[b][cb][v] is position 8 lg + 4 b + v of the tile
+    float sv[2][8], mnew[2];
+    bool moved = false;
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int cb = 0; cb < 2; ++cb) {
+      float tmax = -INFINITY;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float sc = (tb + 8 * lg + 4 * b + v < t1) ? sacc[b][v] * scale : -INFINITY;
-        sv[4 * b + v] = sc;
-        tmax = fmaxf(tmax, sc);
-      }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mnew = fmaxf(m, tmax);
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float sc = (tb + 8 * lg + 4 * b + v < t1) ? sacc[b][cb][v] * scale : -INFINITY;
+          sv[cb][4 * b + v] = sc;
+          tmax = fmaxf(tmax, sc);
+        }
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      mnew[cb] = fmaxf(m[cb], tmax);
+      moved |= mnew[cb] != m[cb];
+    }
     // rescale only when some column's maximum moved (otherwise the factor is 1)
-    if (__builtin_amdgcn_ballot_w64(mnew != m)) {
-      const float alpha = __expf(m - mnew);
-      l *= alpha;
+    if (__builtin_amdgcn_ballot_w64(moved)) {
 #pragma unroll
-      for (int hb = 0; hb < HB; ++hb)
+      for (int cb = 0; cb < 2; ++cb) {
+        const float alpha = __expf(m[cb] - mnew[cb]);
+        l[cb] *= alpha;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) oacc[hb][v] *= alpha;
+        for (int hb = 0; hb < HBW; ++hb)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) oacc[hb][cb][v] *= alpha;
+      }
     }
-    m = mnew;
-    bf16x8_t ph, pl;
+    bf16x8_t ph[2], pl[2];
 #pragma unroll
-    for (int e = 0; e < 8; e += 2) {
-      const float p0 = __expf(sv[e] - mnew), p1 = __expf(sv[e + 1] - mnew);
-      l += p0;
-      l += p1;
-      const bf16x2_t hi = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
-      const bf16x2_t lo =
-          __builtin_convertvector((f32x2_t){p0 - (float)hi[0], p1 - (float)hi[1]}, bf16x2_t);
-      ph[e] = hi[0]; ph[e + 1] = hi[1];
-      pl[e] = lo[0]; pl[e + 1] = lo[1];
+    for (int cb = 0; cb < 2; ++cb) {
+      m[cb] = mnew[cb];
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const float p0 = __expf(sv[cb][e] - mnew[cb]), p1 = __expf(sv[cb][e + 1] - mnew[cb]);
+        l[cb] += p0;
+        l[cb] += p1;
+        const bf16x2_t hi = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
+        const bf16x2_t lo =
+            __builtin_convertvector((f32x2_t){p0 - (float)hi[0], p1 - (float)hi[1]}, bf16x2_t);
+        ph[cb][e] = hi[0]; ph[cb][e + 1] = hi[1];
+        pl[cb][e] = lo[0]; pl[cb][e + 1] = lo[1];
+      }
     }
-    // V^T fragment of block hb: row 16 hb + j (a head dimension), positions
-    // 8 lg .. 8 lg + 7, read as 2-byte elements from the row-major stage
+    // V^T fragment of block HBW wave + hb: row 16 (HBW wave + hb) + j (a head
+    // dimension), positions 8 lg .. 8 lg + 7, read as 2-byte elements
 #pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-      const int d = hb * 16 + j;
+    for (int hb = 0; hb < HBW; ++hb) {
+      const int d = (HBW * wave + hb) * 16 + j;
       u32x4_t w;
 #pragma unroll
       for (int e = 0; e < 8; e += 2) {
@@ -458,8 +482,11 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
         w[e / 2] = a | (c << 16);
       }
       const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, w);
-      oacc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph, oacc[hb], 0, 0, 0);
-      oacc[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, oacc[hb], 0, 0, 0);
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) {
+        oacc[hb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph[cb], oacc[hb][cb], 0, 0, 0);
+        oacc[hb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[cb], oacc[hb][cb], 0, 0, 0);
+      }
     }
   };
 
@@ -470,22 +497,26 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NSTG - 2) * CPW) : "memory");   // this wave's copies of t
     __syncthreads();   // every wave's copies of t landed; every wave is done with tile t - 1
     copy_tile(min(t + NSTG - 1, ntiles - 1));                      // into tile t - 1's stage
-    if (ncols > 0) compute(t % NSTG, t);
+    compute(t % NSTG, t);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the repeated tail copies land before exit
-  if (ncols == 0) return;
 
-  // column j is head g * GQ + j % GQ of batch row src + sbase + j / GQ
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
-  if (j < ncols) {
-    const size_t row = ((size_t)(src + sbase + j / GQ) * H + g * GQ + j % GQ) * S + split;
+  // column c = 16 cb + j: head g * GQ + c % GQ of batch row src + s0 + c / GQ
 #pragma unroll
-    for (int hb = 0; hb < HB; ++hb)
-      *(f32x4_t*)(part_o + row * HD + hb * 16 + 4 * lg) = oacc[hb];
-    if (lg == 0) {
-      part_ml[row * 2] = m;
-      part_ml[row * 2 + 1] = l;
+  for (int cb = 0; cb < 2; ++cb) {
+    float lt = l[cb];
+    lt += __shfl_xor(lt, 16, 64);
+    lt += __shfl_xor(lt, 32, 64);
+    const int c = 16 * cb + j;
+    if (c < ncols) {
+      const size_t row = ((size_t)(src + s0 + c / GQ) * H + g * GQ + c % GQ) * S + split;
+#pragma unroll
+      for (int hb = 0; hb < HBW; ++hb)
+        *(f32x4_t*)(part_o + row * HD + (HBW * wave + hb) * 16 + 4 * lg) = oacc[hb][cb];
+      if (wave == 0 && lg == 0) {
+        part_ml[row * 2] = m[cb];
+        part_ml[row * 2 + 1] = lt;
+      }
     }
   }
 }
@@ -537,10 +568,10 @@ DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len, int
   // grouped: the generated positions keep the spans above (they start at the
   // shared length, so they cover at most max_len positions); the prompt is cut
   // into chunks of whole tiles, about kTargetWGs prefix workgroups in all
-  const int spw = std::max(1, 8 / std::max(1, H / n_kv));
+  const int spb = 32 / std::max(1, H / n_kv);   // samples per prefix workgroup
   p.G = G;
   p.prefix_len = std::min(prefix_len, max_len);
-  p.n_sub = (G + 4 * spw - 1) / (4 * spw);
+  p.n_sub = (G + spb - 1) / spb;
   const int gpairs = std::max(1, B / G * n_kv * p.n_sub);
   const int max_chunks = std::min(MAX_CHUNKS, (p.prefix_len + DT - 1) / DT);
   const int wc = std::min(std::max(1, (kTargetWGs + gpairs / 2) / gpairs), max_chunks);
@@ -615,7 +646,7 @@ hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
                          n_kv, hd, max_len, (float*)out, st);
   if (H % n_kv || H / n_kv > 8 || (hd != 64 && hd != 128)) return hipErrorInvalidValue;
   if (p.G > 0 && (B % p.G || p.chunks < 1 || p.chunks > MAX_CHUNKS || p.n_sub < 1 ||
-                  (long)p.n_sub * 4 * (8 / (H / n_kv)) < p.G || p.prefix_len > max_len ||
+                  (long)p.n_sub * (32 / (H / n_kv)) < p.G || p.prefix_len > max_len ||
                   (long)p.chunks * p.span_p < p.prefix_len))
     return hipErrorInvalidValue;
   return hd == 128 ? attn_decode_hd<128>(q, kc, vc, pos, B, H, n_kv, max_len, p, part, out, st, pack_nb)
