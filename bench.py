@@ -24,15 +24,21 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 
-# HBM bytes of the decode attention kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE runs
-# (7B shape, contexts 3073..3104), each counter scaled by what it reads for a 1 GiB
-# device copy.  Valid only for the kernel source it was measured on.
+# HBM bytes of the per-row decode attention kernel of a grouped step (the generated
+# positions of every sequence, the prompt chunks' partials merged in) from rocprofv3
+# FETCH_SIZE / WRITE_SIZE runs at the 7B shape (64 sequences, 2048-token prompt shared
+# per group of 8, 1 .. 48 generated positions; 32 launches per position count), each
+# counter scaled by what it reads for a 1 GiB device copy.  The fetch per launch fits
+# fixed + per_position x (generated positions): the fixed part is mostly the prompt
+# chunks' partial rows.  Valid only for the kernel source it was measured on and
+# for that shape (position_bytes: algorithmic K + V bytes of one position of all
+# 64 sequences).
 ATTN_TRAFFIC = {
     "source": "paper_2510_17158_amd/csrc/attn_decode.hip",
-    "sha256": "455d42e51d54f2a0a5b9c2743986dd0e777444b1f89bc3b3da6c564653318035",
-    "fetch_kib": 409178.6, "fetch_scale": 2.0,
-    "write_kib": 512.5, "write_scale": 1.0,
-    "algorithmic_bytes": 64 * 3088.5 * 4096,
+    "sha256": "3035248a273ad777715056aedf518f0fd3c09527947fdc947ae5955717643d59",
+    "fixed_fetch_kib": 4586.2, "per_position_fetch_kib": 128.297, "fetch_scale": 2.0,
+    "write_kib": 512.0, "write_scale": 1.0,
+    "position_bytes": 64 * 4096,
 }
 
 
@@ -47,8 +53,9 @@ def attn_traffic(algorithmic_bytes_per_launch: float):
     except OSError:
         return None
     t = ATTN_TRAFFIC
-    measured = (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024
-    return measured / t["algorithmic_bytes"] * algorithmic_bytes_per_launch
+    positions = algorithmic_bytes_per_launch / t["position_bytes"]
+    fetch = (t["fixed_fetch_kib"] + t["per_position_fetch_kib"] * positions) * t["fetch_scale"]
+    return (fetch + t["write_kib"] * t["write_scale"]) * 1024
 
 
 def log(*a):

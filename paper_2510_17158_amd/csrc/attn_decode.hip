@@ -379,7 +379,7 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
 #pragma unroll
     for (int st = 0; st < QSTEPS; ++st) asm volatile("" ::"v"(qf[cb][st]));
 
-  // Tile t (clamped to the last) into stage t % NSTG: copy c fills rows
+  // Tile t into stage t % NSTG: copy c fills rows
   // RPC c .. RPC c + RPC - 1, lane l the 16-byte slot l % PPR of row RPC c + l / PPR
   // with source piece slot ^ swizzle.  Positions past t1 - 1 read position t1 - 1
   // (masked scores, finite values).
@@ -490,16 +490,21 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
     }
   };
 
-  // ring: tiles t .. t + NSTG - 2 in flight when tile t is awaited
+  // ring: tiles t + 1 .. min(t + NSTG - 2, ntiles - 1) stay in flight while this
+  // wave waits for its copies of tile t (copies complete in issue order)
 #pragma unroll
-  for (int t = 0; t < NSTG - 1; ++t) copy_tile(min(t, ntiles - 1));
+  for (int t = 0; t < NSTG - 1; ++t)
+    if (t < ntiles) copy_tile(t);
+  static_assert(NSTG == 4, "the waits below count two tiles ahead");
   for (int t = 0; t < ntiles; ++t) {
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NSTG - 2) * CPW) : "memory");   // this wave's copies of t
+    const int ahead = ntiles - 1 - t;
+    if (ahead >= 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * CPW) : "memory");
+    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CPW) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();   // every wave's copies of t landed; every wave is done with tile t - 1
-    copy_tile(min(t + NSTG - 1, ntiles - 1));                      // into tile t - 1's stage
+    if (t + NSTG - 1 < ntiles) copy_tile(t + NSTG - 1);           // into tile t - 1's stage
     compute(t % NSTG, t);
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the repeated tail copies land before exit
 
   // column c = 16 cb + j: head g * GQ + c % GQ of batch row src + s0 + c / GQ
 #pragma unroll
