@@ -109,6 +109,16 @@ def test_argument_errors_before_device_work():
     r = L.grpo_rollout_step(h, p, 64, 100, 64, p, p, 10, 1, 2, C.byref(s), p, p, None, None, p, 16,
                             None)
     assert r == api.WORKSPACE_TOO_SMALL
+    # grouped steps: G must divide B, 0 <= prefix_len <= max_len; the per-row
+    # checks still apply
+    def grouped(G, prefix, max_pos=10):
+        return L.grpo_rollout_step_grouped(h, p, 64, 100, 64, G, prefix, p, p, max_pos, 1, 2,
+                                           C.byref(s), p, p, None, None, p, 1 << 40, None)
+    assert grouped(0, 50) == api.INVALID_ARG
+    assert grouped(3, 50) == api.INVALID_ARG
+    assert grouped(8, 101) == api.INVALID_ARG
+    assert grouped(8, -1) == api.INVALID_ARG
+    assert grouped(8, 50, max_pos=99) == api.KV_CAPACITY
     # B above n_seqs, bad temperature, bad top_k
     assert L.grpo_rollout_step(h, p, 8, 100, 64, p, p, 10, 1, 2, C.byref(s), p, p, None, None, p,
                                1 << 40, None) == api.INVALID_ARG
