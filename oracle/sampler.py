@@ -1,7 +1,7 @@
 """Next-token sampling and its log-probability.
 
 One draw of Alg. 1's rollout step for one sequence.  Definitions (the paper
-leaves the sampler unspecified; these are the readings this build fixes):
+leaves the sampler unspecified; these are the readings taken here):
 
 * z = l / T (T = 0 means greedy and uses T = 1 for the log-probability).
 * S = the top-k vocabulary ids of l ordered by (value desc, id asc); all ids
