@@ -78,14 +78,22 @@ def decode_bytes_per_step(w, ctx_avg: float) -> float:
 
 
 def score_flops(w) -> float:
-    """Algorithmic flops of scoring one model over the batch."""
+    """Algorithmic flops of scoring one model over the batch.  With the prompt
+    shared within groups its positions count once per group (projections and
+    causal attention), every sequence's later positions once each."""
     c = w.model
-    T, N = w.total_len, w.batch
+    T, N, Tp = w.total_len, w.batch, w.prompt_len
     per_tok = 2 * (c.d_model * (c.q_dim + 2 * c.kv_dim) + c.q_dim * c.d_model
                    + 3 * c.d_model * c.d_ffn)
-    attn = 2 * 2 * c.n_layers * c.n_heads * c.head_dim * (T * (T + 1) / 2)
-    head = 2 * c.vocab * c.d_model * (T - w.prompt_len)
-    return c.n_layers * per_tok * N * T + attn * N + head * N
+    attn_pos = 2 * 2 * c.n_layers * c.n_heads * c.head_dim   # per (query, key) pair
+    head = 2 * c.vocab * c.d_model * (T - Tp) * N
+    if w.shared_prompt:
+        rows = w.n_prompts * Tp + N * (T - Tp)
+        pairs = w.n_prompts * Tp * (Tp + 1) / 2 + N * (T * (T + 1) / 2 - Tp * (Tp + 1) / 2)
+    else:
+        rows = N * T
+        pairs = N * T * (T + 1) / 2
+    return c.n_layers * per_tok * rows + attn_pos * pairs + head
 
 
 def kernel_bytes(w) -> dict:

@@ -15,6 +15,7 @@
  *   grpo_rollout_step_grouped  the same, reading each group's shared prompt
  *                         K/V once per group
  *   grpo_score_sequences  teacher-forced log pi(x_t | c, x_<t) (Eq. 1, KL term)
+ *   grpo_score_sequences_grouped  the same, the group's shared prompt run once
  *   grpo_advantages       group-normalised rewards w(x) (Alg. 1, normalisation)
  *   grpo_token_loss       clipped-ratio + KL per-token loss, its gradient with
  *                         respect to logp, and statistics (Eq. 1, GRPO form)
@@ -220,6 +221,24 @@ int grpo_rollout_step_grouped(const grpo_model* m, void* kv, int32_t n_seqs, int
 int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, int32_t T,
                          int32_t score_from, float temperature, float* logp_out, void* ws,
                          size_t ws_bytes, void* stream);
+
+/* grpo_score_sequences for groups that share a prefix: rows g*G .. g*G+G-1 of
+ * tokens are the G samples of one prompt (Alg. 1) and hold the same tokens at
+ * positions 0 .. prefix_len-1.  Under causal attention those positions' states
+ * are the same for all G rows, so the forward runs them once per group (their
+ * K/V shared by the group) and runs each row only from the multiple of 32 at or
+ * below prefix_len-1 on.  The results are those of grpo_score_sequences except
+ * for the order of floating-point additions; rows that do not share the prefix
+ * are scored as if they did.  Arguments as grpo_score_sequences, plus
+ *   G           group size, >= 1, dividing N
+ *   prefix_len  shared positions, 0 <= prefix_len <= score_from
+ * Same workspace as grpo_score_sequences.  fp32 models, G = 1 and short prefixes
+ * (below 33 positions) take the per-row path.  GRPO_INVALID_ARG for a G or
+ * prefix_len outside these ranges. */
+int grpo_score_sequences_grouped(const grpo_model* m, const int32_t* tokens, int32_t N,
+                                 int32_t T, int32_t score_from, float temperature, int32_t G,
+                                 int32_t prefix_len, float* logp_out, void* ws, size_t ws_bytes,
+                                 void* stream);
 
 /* Group advantages (Alg. 1, normalisation step): for each of the P groups of
  * G >= 2 rewards, A = (r - mean) / (sample std (divisor G-1) + eps); a group

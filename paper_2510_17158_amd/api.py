@@ -67,6 +67,8 @@ _SIGS = {
                                          _I32, _I32, C.POINTER(Sampling), _VP, _VP, _VP, _VP, _VP,
                                          _SZ, _VP]),
     "grpo_score_sequences": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _VP, _VP, _SZ, _VP]),
+    "grpo_score_sequences_grouped": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _I32, _I32, _VP,
+                                            _VP, _SZ, _VP]),
     "grpo_advantages": (_I32, [_VP, _I32, _I32, _F32, _VP, _VP]),
     "grpo_token_loss": (_I32, [_VP, _VP, _VP, _VP, _VP, _I32, _I32, _F32, _F32, _I32, _VP, _VP,
                                _VP, _VP, _VP, _SZ, _VP]),
@@ -237,11 +239,18 @@ def rollout_step(model: Model, kv, n_seqs: int, max_len: int, pos, tok, max_pos:
 
 
 def score_sequences(model: Model, tokens, score_from: int, temperature: float, logp_out, ws=None,
-                    stream=None):
+                    stream=None, group: int = 0, prefix_len: int = 0):
+    """grpo_score_sequences, or grpo_score_sequences_grouped when group > 0 (rows in
+    groups of `group` sharing their first prefix_len tokens)."""
     N, T = tokens.shape
+    nws = ws.numel() if ws is not None else 0
+    if group > 0:
+        _check(lib().grpo_score_sequences_grouped(model.handle, _ptr(tokens), N, T, score_from,
+                                                  temperature, group, prefix_len, _ptr(logp_out),
+                                                  _ptr(ws), nws, _stream(stream)))
+        return
     _check(lib().grpo_score_sequences(model.handle, _ptr(tokens), N, T, score_from, temperature,
-                                      _ptr(logp_out), _ptr(ws),
-                                      ws.numel() if ws is not None else 0, _stream(stream)))
+                                      _ptr(logp_out), _ptr(ws), nws, _stream(stream)))
 
 
 def advantages(rewards, P: int, G: int, eps: float, adv_out, stream=None):

@@ -887,6 +887,103 @@ int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, 
   return GRPO_OK;
 }
 
+int grpo_score_sequences_grouped(const grpo_model* m, const int32_t* tokens, int32_t N,
+                                 int32_t T, int32_t score_from, float temperature, int32_t G,
+                                 int32_t prefix_len, float* logp_out, void* ws, size_t ws_bytes,
+                                 void* stream) {
+  if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
+  if (G < 1 || N < 1 || N % G) return fail(GRPO_INVALID_ARG, "G %d must be >= 1 and divide N %d", G, N);
+  if (prefix_len < 0 || prefix_len > score_from)
+    return fail(GRPO_INVALID_ARG, "prefix_len %d outside [0, score_from %d]", prefix_len, score_from);
+  const grpo_config& c = m->cfg;
+  // every sequence's own rows start at the multiple of 32 at or below the last
+  // shared position (its K/V recomputed per sequence: the same values)
+  const int P0 = prefix_len > 0 ? (prefix_len - 1) / 32 * 32 : 0;
+  const int chunk_seqs = std::max(1, std::min(N, kScoreTokens / std::max(T, 1)));
+  const int C = chunk_seqs / G * G;
+  if (c.dtype == GRPO_F32 || G == 1 || P0 == 0 || C == 0 || score_from < 1 || score_from >= T)
+    return grpo_score_sequences(m, tokens, N, T, score_from, temperature, logp_out, ws, ws_bytes,
+                                stream);
+  if (!tokens || !logp_out || !ws) return fail(GRPO_INVALID_ARG, "tokens, logp_out and ws must be set");
+  if (!(temperature >= 0.f) || temperature == INFINITY)
+    return fail(GRPO_INVALID_ARG, "temperature must be finite and >= 0");
+  if ((long)T > kScoreTokens) return fail(GRPO_UNSUPPORTED, "T above %d", kScoreTokens);
+  const size_t need = grpo_workspace_bytes(m, GRPO_OP_SCORE, N, T);
+  if (ws_bytes < need)
+    return fail(GRPO_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
+  hipStream_t st = (hipStream_t)stream;
+  Bump b(ws);
+  ScoreWS w = take_score(b, c, N, T);
+  const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn, Ts = T - score_from;
+  const int Tb = T - 1 - P0;          // own rows per sequence: positions P0 .. T - 2
+  const int ldqkv = qd + 2 * kvd, es = esize(c);
+  const Partials none{nullptr, 0, 0, d};
+  HIPCHK(rope_table(nullptr, T, c.head_dim, c.rope_theta, w.s.cs, st));
+  for (int n0 = 0; n0 < N; n0 += C) {
+    const int Cc = std::min(C, N - n0), Pc = Cc / G;
+    // rows: the Pc groups' shared positions 0 .. prefix_len - 1 once each, then
+    // every sequence's own rows
+    const int M1 = Pc * prefix_len, M = M1 + Cc * Tb;
+    const int32_t* tk = tokens + (size_t)n0 * T;
+    for (int p = 0; p < Pc; ++p)
+      HIPCHK(embed(c.dtype, m->tok_emb, tk + (size_t)p * G * T, prefix_len, d, c.vocab,
+                   w.s.x + (size_t)p * prefix_len * d, st));
+    for (int n = 0; n < Cc; ++n)
+      HIPCHK(embed(c.dtype, m->tok_emb, tk + (size_t)n * T + P0, Tb, d, c.vocab,
+                   w.s.x + ((size_t)M1 + (size_t)n * Tb) * d, st));
+    char* q1 = (char*)w.s.q + (size_t)M1 * qd * es;
+    char* o1 = (char*)w.s.o + (size_t)M1 * qd * es;
+    int rc;
+    for (int l = 0; l < c.n_layers; ++l) {
+      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), none, m->attn_norm[l], M, d,
+                     c.rms_eps, w.s.h, d, st));
+      if ((rc = gemm_rows(m, w.s.h, d, M, qkv_stack(m, l), ldqkv, d, EPI_STORE,
+                          EpiArgs{w.s.qkv, nullptr, ldqkv}, st)))
+        return rc;
+      // shared rows: K and V^T into all G slots of the group; own rows from P0
+      RopeArgs ra{};
+      ra.mode = 1; ra.T = prefix_len; ra.G = G; ra.pos_arr = nullptr;
+      ra.n_heads = c.n_heads; ra.n_kv = c.n_kv_heads; ra.hd = c.head_dim; ra.theta = c.rope_theta;
+      ra.kcache = w.kbuf; ra.vcache = nullptr; ra.n_seqs = Cc; ra.max_len = T;
+      ra.vt = w.vt; ra.vt_len = round8(T); ra.vt_G = G;
+      ra.splits = 1; ra.split_stride = 0; ra.cs = w.s.cs; ra.pos0 = 0;
+      HIPCHK(rope_kv(c.dtype, w.s.qkv, M1, w.s.q, ra, st));
+      RopeArgs rb = ra;
+      rb.T = Tb; rb.G = 1; rb.vt_G = 1; rb.pos0 = P0;
+      HIPCHK(rope_kv(c.dtype, w.s.qkv + (size_t)M1 * ldqkv, Cc * Tb, q1, rb, st));
+      HIPCHK(attn_prefill(c.dtype, w.s.q, w.kbuf, w.vt, Pc, prefix_len, c.n_heads, c.n_kv_heads,
+                          c.head_dim, T, G, w.s.o, st, 0, G, round8(T)));
+      HIPCHK(attn_prefill(c.dtype, q1, w.kbuf, w.vt, Cc, Tb, c.n_heads, c.n_kv_heads,
+                          c.head_dim, T, 1, o1, st, P0, 1, round8(T)));
+      if ((rc = gemm_rows(m, w.s.o, qd, M, one(m->wo[l]), d, qd, EPI_RESID,
+                          EpiArgs{w.s.x, nullptr, d}, st)))
+        return rc;
+      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), none, m->mlp_norm[l], M, d,
+                     c.rms_eps, w.s.h, d, st));
+      if ((rc = gemm_rows(m, w.s.h, d, M, gate_up(m, l), f, d, EPI_SWIGLU,
+                          EpiArgs{nullptr, w.s.a, f}, st)))
+        return rc;
+      if ((rc = gemm_rows(m, w.s.a, f, M, one(m->w_down[l]), d, f, EPI_RESID,
+                          EpiArgs{w.s.x, nullptr, d}, st)))
+        return rc;
+    }
+    // logits of positions score_from - 1 .. T - 2: own rows of each sequence
+    const int R = Cc * Ts;
+    for (int i0 = 0; i0 < R; i0 += w.sub_rows) {
+      const int rc_rows = std::min(w.sub_rows, R - i0);
+      HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{i0, Ts, Tb, M1 + score_from - 1 - P0}, none,
+                     m->final_norm, rc_rows, d, c.rms_eps, w.hs, d, st));
+      if ((rc = gemm_rows(m, w.hs, d, rc_rows, one(m->lm_head), c.vocab, d, EPI_STORE,
+                          EpiArgs{w.logits, nullptr, c.vocab}, st)))
+        return rc;
+      HIPCHK(token_logprob(w.logits, rc_rows, c.vocab, c.vocab, tk, T, score_from, Ts, i0,
+                           temperature, logp_out + (size_t)n0 * Ts + i0, st));
+    }
+  }
+  g_err.clear();
+  return GRPO_OK;
+}
+
 int grpo_advantages(const float* rewards, int32_t P, int32_t G, float eps, float* adv_out,
                     void* stream) {
   if (!rewards || !adv_out) return fail(GRPO_INVALID_ARG, "rewards and adv_out must be set");

@@ -47,7 +47,7 @@ template <int HD, int GQ>
 __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) void k_flash_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ vt,
     int T, int H, int n_kv, int k_len, int k_seq_stride, int vt_len, float scale,
-    bf16_t* __restrict__ out) {
+    bf16_t* __restrict__ out, int q_pos0, int vt_seq_stride) {
   constexpr int QSTEPS = HD / 32, HB = HD / 16;
   constexpr int NCP = HD / 8;   // 1 KB copies per K tile (and per V^T tile)
   __shared__ __attribute__((aligned(1024))) bf16_t ks[2][64 * HD];
@@ -73,7 +73,9 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
     for (int st = 0; st < QSTEPS; ++st) qf[qb][st] = *(const bf16x8_t*)(qp + st * 32);
   }
   const bf16_t* kbase = k + ((size_t)n * k_seq_stride * n_kv + g) * (size_t)k_len * HD;
-  const bf16_t* vbase = vt + ((size_t)n * n_kv + g) * (size_t)HD * vt_len;
+  const bf16_t* vbase = vt + ((size_t)n * vt_seq_stride * n_kv + g) * (size_t)HD * vt_len;
+  // query rows are positions q_pos0 + row; keys run to position Tk - 1
+  const int Tk = q_pos0 + T;
 
   // Tile t of 64 keys into stage buf by direct-to-LDS copies, NCP of K and NCP of
   // V^T dealt round-robin to the waves.  Copy i, lane l fills the 16-byte LDS
@@ -86,7 +88,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
   // they read are finite.
   constexpr int KRPC = 512 / HD;   // K rows per copy
   auto copy_tile = [&](int t, int buf) __attribute__((always_inline)) {
-    if ((t + 1) * 64 <= T) {
+    if ((t + 1) * 64 <= Tk) {
 #pragma unroll
       for (int i0 = 0; i0 < NCP; i0 += GQ) {
         const int i = i0 + wave;
@@ -107,7 +109,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
         const int o = i * 64 + lane;
         const int kr_ = o / (HD / 8), kp = (o % (HD / 8)) ^ kswz<HD>(kr_);
         const int vr_ = o / 8, vp = (o % 8) ^ vswz(vr_);
-        const int key = min(t * 64 + kr_, T - 1);
+        const int key = min(t * 64 + kr_, Tk - 1);
         dma16(kbase + (size_t)key * HD + kp * 8, lds_addr(&ks[buf][i * 512]));
         const int key0 = min(t * 64 + vp * 8, vt_len - 8);
         dma16(vbase + (size_t)vr_ * vt_len + key0, lds_addr(&vs[buf][i * 512]));
@@ -123,7 +125,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
   float mq[2] = {-1e30f, -1e30f}, lq_sum[2] = {0.f, 0.f};
 
   const float scale2 = scale * 1.4426950408889634f;   // log2(e)
-  const int qlast = min(q0 + 31, T - 1);
+  const int qlast = q_pos0 + min(q0 + 31, T - 1);
   const int n_tiles = qlast / 64 + 1;
   copy_tile(0, 0);
   dma_wait();
@@ -171,7 +173,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       // (last tile) key k0 + 32 s2 + 8 lg + 4 b + v is visible iff 32 s2 + 4 b + v <= lim
-      const int lim = min(q0 + qb * 16 + lq, T - 1) - k0 - 8 * lg;
+      const int lim = q_pos0 + min(q0 + qb * 16 + lq, T - 1) - k0 - 8 * lg;
       float mx = -INFINITY;
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2)
@@ -275,11 +277,11 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
 template <int HD>
 hipError_t launch_flash(int gq, dim3 grid, hipStream_t st, const bf16_t* q, const bf16_t* k,
                         const bf16_t* vt, int T, int H, int n_kv, int k_len, int k_seq_stride,
-                        int vt_len, float scale, bf16_t* out) {
+                        int vt_len, float scale, bf16_t* out, int q_pos0, int vt_seq_stride) {
 #define GRPO_FLASH(G)                                                                        \
   case G:                                                                                   \
     k_flash_bf16<HD, G><<<grid, 64 * G, 0, st>>>(q, k, vt, T, H, n_kv, k_len, k_seq_stride, \
-                                                 vt_len, scale, out);                       \
+                                                 vt_len, scale, out, q_pos0, vt_seq_stride); \
     break;
   switch (gq) {
     GRPO_FLASH(1) GRPO_FLASH(2) GRPO_FLASH(3) GRPO_FLASH(4)
@@ -352,9 +354,14 @@ hipError_t attn_rows_f32(const float* q, const float* kc, const float* vc, const
 
 hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_or_vt, int N,
                         int T, int H, int n_kv, int hd, int k_len, int k_seq_stride, void* out,
-                        hipStream_t st) {
+                        hipStream_t st, int q_pos0, int vt_seq_stride, int vt_len_in) {
   if (N <= 0 || T <= 0) return hipSuccess;
   const float scale = 1.f / sqrtf((float)hd);
+  // the flash kernel masks only the last key tile of a query block, which needs
+  // query blocks to start at multiples of 32
+  if (q_pos0 < 0 || q_pos0 % 32 || q_pos0 + T > k_len || vt_seq_stride < 1 ||
+      (dtype == 0 && (q_pos0 || vt_seq_stride != 1)))
+    return hipErrorInvalidValue;
   if (dtype == 0) {
     dim3 grid(N * T, H);
     Prof pf("attn_f32", st);
@@ -363,16 +370,18 @@ hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_o
         H, n_kv, hd, k_len, scale, (float*)out);
     return hipGetLastError();
   }
-  const int vt_len = (T + 7) / 8 * 8;
+  const int vt_len = vt_len_in > 0 ? vt_len_in : (q_pos0 + T + 7) / 8 * 8;
+  if (vt_len < q_pos0 + T) return hipErrorInvalidValue;
   dim3 grid((T + 31) / 32, n_kv, N);
   Prof pf("flash_attn", st);
   const int gq = H / n_kv;
   if (hd == 128)
     return launch_flash<128>(gq, grid, st, (const bf16_t*)q, (const bf16_t*)k,
                              (const bf16_t*)v_or_vt, T, H, n_kv, k_len, k_seq_stride, vt_len,
-                             scale, (bf16_t*)out);
+                             scale, (bf16_t*)out, q_pos0, vt_seq_stride);
   return launch_flash<64>(gq, grid, st, (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v_or_vt,
-                          T, H, n_kv, k_len, k_seq_stride, vt_len, scale, (bf16_t*)out);
+                          T, H, n_kv, k_len, k_seq_stride, vt_len, scale, (bf16_t*)out, q_pos0,
+                          vt_seq_stride);
 }
 
 }  // namespace grpo

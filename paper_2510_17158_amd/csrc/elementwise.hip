@@ -134,7 +134,7 @@ __global__ void k_rope_kv(const float* qkv, int M, T* q_out, RopeArgs a) {
   const int m = (int)(idx / ((size_t)half * heads));
   int seq, pos;
   if (a.mode == 0) { seq = m; pos = a.pos_arr[m]; }
-  else { seq = m / a.T; pos = m % a.T; }
+  else { seq = m / a.T; pos = a.pos0 + m % a.T; }
   const int ldq = heads * a.hd;
   const float* src = qkv + (size_t)m * ldq + h * a.hd;
   const bool rotate = h < a.n_heads + a.n_kv;
@@ -197,9 +197,10 @@ __global__ void k_rope_table(const int32_t* pos_arr, int rows, int half, float t
   cs[idx] = make_float2((float)cd, (float)sd);
 }
 
-// V^T for the prefill/scoring attention: vt[seq][g][d][pos] = bf16 of the V part
-// of qkv (sum of its splits) for row seq * T + pos.  A workgroup moves a 64-position
-// x hd tile through LDS, reading rows along d and writing along positions.
+// V^T for the prefill/scoring attention: vt[slot][g][d][pos0 + p] = bf16 of the V
+// part of qkv (sum of its splits) for row seq * T + p, for slots seq * vt_G ..
+// seq * vt_G + vt_G - 1 (one when vt_G <= 1).  A workgroup moves a 64-position x hd
+// tile through LDS, reading rows along d and writing along positions.
 __global__ __launch_bounds__(256) void k_v_transpose(const float* qkv, int T, RopeArgs a,
                                                      bf16_t* vt) {
   __shared__ float tile[64][129];
@@ -218,10 +219,13 @@ __global__ __launch_bounds__(256) void k_v_transpose(const float* qkv, int T, Ro
     tile[p][d] = v;
   }
   __syncthreads();
-  bf16_t* dst = vt + ((size_t)seq * a.n_kv + g) * hd * a.vt_len;
-  for (int e = threadIdx.x; e < 64 * hd; e += 256) {
-    const int d = e / 64, p = e % 64;
-    if (p0 + p < a.vt_len) dst[(size_t)d * a.vt_len + p0 + p] = p0 + p < T ? f2bf(tile[p][d]) : 0;
+  const int vg = max(a.vt_G, 1);
+  for (int r = 0; r < vg; ++r) {
+    bf16_t* dst = vt + (((size_t)seq * vg + r) * a.n_kv + g) * hd * a.vt_len;
+    for (int e = threadIdx.x; e < 64 * hd; e += 256) {
+      const int d = e / 64, p = e % 64, t = a.pos0 + p0 + p;
+      if (t < a.vt_len) dst[(size_t)d * a.vt_len + t] = p0 + p < T ? f2bf(tile[p][d]) : 0;
+    }
   }
 }
 

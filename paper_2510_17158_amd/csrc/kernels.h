@@ -117,6 +117,8 @@ struct RopeArgs {
   uint16_t* vt; int vt_len;
   int splits; size_t split_stride;
   const float2* cs;
+  int pos0;    // mode 1: position of each sequence's first row (0: rows start at 0)
+  int vt_G;    // V^T written to vt_G consecutive sequence slots per sequence (0 or 1: one)
 };
 hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeArgs& a,
                    hipStream_t st);
@@ -153,9 +155,13 @@ hipError_t attn_rows_f32(const float* q, const float* kc, const float* vc, const
 // Causal attention over N sequences of T rows: q act [N*T, H*hd]; K in cache
 // layout [n][n_kv][k_len][hd] (sequence n at slot n*k_stride_seq), Vt
 // [n][n_kv][hd][T] (bf16 path) or V in cache layout (fp32 path).  out act [N*T, H*hd].
+// bf16 only: q_pos0 (a multiple of 32) is the position of each sequence's first
+// query row (keys 0 .. q_pos0 + T - 1 are attended), V^T of sequence n at slot
+// n * vt_seq_stride with rows of vt_len positions (0: (q_pos0 + T) rounded up to 8).
 hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_or_vt, int N,
                         int T, int H, int n_kv, int hd, int k_len, int k_seq_stride,
-                        void* out, hipStream_t st);
+                        void* out, hipStream_t st, int q_pos0 = 0, int vt_seq_stride = 1,
+                        int vt_len = 0);
 
 // ---- sampling / log-probs ---------------------------------------------------------
 // logits fp32 [R, V] (row stride ld).  Row r makes G draws; draw g uses Philox

@@ -95,11 +95,12 @@ class GrpoIteration:
 
     def score(self):
         w = self.w
+        grp = dict(group=w.group, prefix_len=w.prompt_len) if w.shared_prompt else {}
         api.score_sequences(self.policy, self.seqs, w.prompt_len, w.temperature, self.lp_pol,
-                            ws=self.ws_score)
+                            ws=self.ws_score, **grp)
         if self.ref is not None:
             api.score_sequences(self.ref, self.seqs, w.prompt_len, w.temperature, self.lp_ref,
-                                ws=self.ws_score)
+                                ws=self.ws_score, **grp)
 
     def grpo(self):
         w = self.w

@@ -74,7 +74,7 @@ class Workload:
     prompt_kind: str = "uniform"   # "uniform" or "code" (code-like stream + tool spans)
     tool_spans: int = 0        # number of 256-token tool-output spans in a prompt
     score: bool = True         # teacher-forced scoring of policy + reference
-    shared_prompt: bool = True  # decode reads each group's prompt K/V once per group
+    shared_prompt: bool = True  # decode and scoring run each group's shared prompt once
     clip_eps: float = 0.2
     beta: float = 0.04
     adv_eps: float = 1e-6

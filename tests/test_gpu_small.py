@@ -373,3 +373,41 @@ def test_grouped_decode_matches_per_row(name, P, G, Tp, prefix, steps):
         it.tok.copy_(torch.from_numpy(t0).to("cuda"))   # both continue from the per-row token
     say("grouped vs per-row: logit err", worst, "tokens changed within the margin bound", near)
     model.close()
+
+
+@pytest.mark.parametrize("name,P,G,Tp,Tn,prefix", [
+    ("small", 2, 4, 300, 100, 300),    # GQ 3; own rows from position 288
+    ("small", 2, 4, 300, 100, 200),    # part of the prompt shared (prefix below score_from)
+    ("7b", 2, 8, 70, 60, 70),          # GQ 4; own rows from 64
+    ("7b", 1, 8, 520, 40, 520),        # several 64-key tiles shared
+])
+def test_grouped_scoring_matches_per_row(name, P, G, Tp, Tn, prefix):
+    """Teacher-forced scoring with each group's shared prompt run once against
+    per-row scoring of the same sequences: under causal attention the shared
+    positions' states are the same for every member, so the log-probs agree up
+    to the order of additions (bf16 tolerance; bf16 roundings may flip)."""
+    require_gpu()
+    base = get(name)
+    layers = 2 if name == "small" else 1
+    w = truncated(base, layers, n_prompts=P, group=G, prompt_len=Tp, new_tokens=Tn)
+    say("grouped vs per-row scoring", name, P, G, Tp, Tn, prefix)
+    host, model = build_model(w.model, w.master_seed, gain_noise=0.1)
+    V = w.model.vocab
+    rng = np.random.default_rng(P * 1000 + Tp)
+    prompts = rng.integers(0, V, (P, Tp))
+    gen = rng.integers(0, V, (P * G, Tn))
+    seqs = np.concatenate([np.repeat(prompts, G, 0), gen], 1).astype(np.int32)
+    tok = torch.from_numpy(seqs).to("cuda")
+    N, T = seqs.shape
+    ws = api.alloc_workspace(model, api.OP_SCORE, N, T, "cuda")
+    out = []
+    for group in (0, G):
+        lp = torch.empty(N, Tn, device="cuda")
+        api.score_sequences(model, tok, Tp, 1.0, lp, ws=ws, group=group, prefix_len=prefix)
+        torch.cuda.synchronize()
+        out.append(lp.cpu().numpy())
+    assert np.isfinite(out[1]).all()
+    err = float(np.abs(out[1] - out[0]).max())
+    say("grouped vs per-row scoring: log-prob err", err)
+    assert err <= LOGIT_TOL
+    model.close()
