@@ -133,6 +133,13 @@ def test_argument_errors_before_device_work():
                           None) == api.INVALID_ARG
     assert L.grpo_prefill(h, p, 64, 100, p, 8, 200, 8, C.byref(s), p, p, None, None, p, 1 << 40,
                           None) == api.KV_CAPACITY
+    # grouped scoring: G must divide N, 0 <= prefix_len <= score_from
+    assert L.grpo_score_sequences_grouped(h, p, 8, 100, 50, 1.0, 3, 50, p, p, 1 << 40,
+                                          None) == api.INVALID_ARG
+    assert L.grpo_score_sequences_grouped(h, p, 8, 100, 50, 1.0, 4, 51, p, p, 1 << 40,
+                                          None) == api.INVALID_ARG
+    assert L.grpo_score_sequences_grouped(h, p, 8, 100, 50, 1.0, 0, 50, p, p, 1 << 40,
+                                          None) == api.INVALID_ARG
     # scoring range
     assert L.grpo_score_sequences(h, p, 4, 10, 0, 1.0, p, p, 1 << 40, None) == api.INVALID_ARG
     assert L.grpo_score_sequences(h, p, 4, 10, 10, 1.0, p, p, 1 << 40, None) == api.INVALID_ARG
