@@ -62,6 +62,25 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def copy_ceiling_gbs(torch) -> float:
+    """HBM rate of a plain 1 GiB device-to-device copy (bytes read + written per
+    second), the best of 5 timed copies after one untimed."""
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    best = float("inf")
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * (1 << 30) / (best / 1e3) / 1e9
+
+
 def decode_bytes_per_step(w, ctx_avg: float) -> float:
     """Algorithmic HBM bytes of one decode step: every weight once (embedding rows
     aside), the KV of every context position once, the new K/V written.  With the
@@ -278,12 +297,17 @@ def main():
         "decode_step_ms": dec_ms,
         "decode_step_gbs": dec_bytes / (dec_ms / 1e3) / 1e9,
         "decode_step_hbm_frac": dec_bytes / (dec_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+        "decode_tokens_per_s": w.batch / (dec_ms / 1e3),
     }
     if w.score:
         sf = score_flops(w)
         out["scored_tokens_per_s"] = n_models * w.batch * w.total_len / (phases[2] / 1e3)
         out["score_tflops"] = n_models * sf / (phases[2] / 1e3) / 1e12
         out["score_mfma_frac"] = out["score_tflops"] / BF16_PEAK_TFLOPS
+    # the decode step against a measured stream-copy ceiling as well as the spec peak
+    cc = copy_ceiling_gbs(torch)
+    out["copy_ceiling_gbs"] = cc
+    out["decode_step_copy_frac"] = out["decode_step_gbs"] / cc
     # per-kernel times from a profiled replica of the step (HIP events around
     # every launch, on the launch stream); the dominant decode kernel sets the
     # roofline line
