@@ -138,7 +138,7 @@ int decode_target() {
   }();
   return v;
 }
-constexpr int kScoreTokens = 65536;    // rows per scoring chunk (sequences * T)
+constexpr int kScoreTokens = 131072;   // rows per scoring chunk (sequences * T)
 constexpr size_t kLogitBytes = size_t(1) << 30;  // LM-head logits per scoring sub-chunk
 
 // bump allocator over the caller's workspace; base == nullptr only measures
