@@ -33,21 +33,24 @@ def _small_workload(**kw):
     return w.with_(**kw)
 
 
-def _stage_local(w, host, model, it, n_steps, group=0, prefix_len=0):
+def _stage_local(w, host, model, it, n_steps, group=0, prefix_len=0, back=None):
     """Decode n_steps one at a time; check every layer, the head and the sampler
-    (group > 0: grouped steps sharing the cache below prefix_len)."""
+    (group > 0: grouped steps sharing the cache below prefix_len; back: per-row
+    steps back from the prompt's end, so the rows decode at ragged positions)."""
     cfg = w.model
     B, L, d, V = it.B, cfg.n_layers, cfg.d_model, cfg.vocab
     om = oracle.OracleModel(cfg, host)
     om32 = oracle.OracleModel(cfg, host, precision="fp32")
     om32s = oracle.OracleModel(cfg, host, precision="fp32-seq")
     it.tok.copy_(it.tok0)
-    it.pos.fill_(w.prompt_len)
+    back = np.zeros(B, np.int64) if back is None else np.asarray(back, np.int64)
+    it.pos.copy_(torch.from_numpy((w.prompt_len - back).astype(np.int32)).to("cuda"))
     pool = FloorPool()
     worst_logit, near = 0.0, 0
     toks = []
     for s in range(n_steps):
         pos = w.prompt_len + s
+        posv = pos - back
         to = torch.empty(B, 1, dtype=torch.int32, device="cuda")
         lo = torch.empty(B, 1, device="cuda")
         lg = torch.empty(B, V, device="cuda")
@@ -62,15 +65,15 @@ def _stage_local(w, host, model, it, n_steps, group=0, prefix_len=0):
         lo = lo.cpu().numpy()[:, 0]
         toks.append(to)
         kv = kv_view(cfg, it.kv, B, it.max_len)
-        posv = np.full(B, pos)
+        rows = np.arange(B)
         for l in range(L):
             x64, k64, v64 = om.decode_layer(l, hid[l], posv, kv[l, 0].copy(), kv[l, 1].copy())
             f32 = [m.decode_layer(l, hid[l], posv, kv[l, 0].astype(np.float32),
                                   kv[l, 1].astype(np.float32)) for m in (om32, om32s)]
             ak, av = h_flip_allowance(om, cfg, l, hid[l])
             pool.add("x", hid[l + 1], x64, [r[0] for r in f32])
-            pool.add("k", kv[l, 0, :, :, pos], k64, [r[1] for r in f32], bf16=True, allow=ak)
-            pool.add("v", kv[l, 1, :, :, pos], v64, [r[2] for r in f32], bf16=True, allow=av)
+            pool.add("k", kv[l, 0, rows, :, posv], k64, [r[1] for r in f32], bf16=True, allow=ak)
+            pool.add("v", kv[l, 1, rows, :, posv], v64, [r[2] for r in f32], bf16=True, allow=av)
         worst_logit = max(worst_logit, float(np.abs(om.head(hid[L]) - lg).max()))
         for b in range(B):
             t, lp, margin = oracle.sample_token(lg[b].astype(np.float64), w.temperature, w.top_k,
@@ -411,3 +414,20 @@ def test_grouped_scoring_matches_per_row(name, P, G, Tp, Tn, prefix):
     say("grouped vs per-row scoring: log-prob err", err)
     assert err <= LOGIT_TOL
     model.close()
+
+
+@pytest.mark.parametrize("group", [0, 4])
+def test_ragged_positions_stage_local(small, group):
+    """One batch whose rows decode at different positions (1 .. 9 steps back from
+    the prompt's end, re-entering the prompt: each row attends its own context
+    0 .. pos[b]), stage-local against the oracle; grouped with the shared length
+    below every row's position."""
+    require_gpu()
+    w, host, model = small
+    say("ragged positions stage-local, group", group)
+    it = GrpoIteration(w, model, None, synth.make_prompts(w), synth.make_rewards(w),
+                       synth.make_seed(w))
+    it.prefill()
+    back = 1 + (np.arange(it.B) * 5) % 9
+    prefix = w.prompt_len - int(back.max()) if group else 0
+    _stage_local(w, host, model, it, 2, group=group, prefix_len=prefix, back=back)
