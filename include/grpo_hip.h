@@ -109,6 +109,43 @@ typedef struct grpo_sampling {
   uint64_t seed;
 } grpo_sampling;
 
+/* Intermediate values of a forward pass, for parity tests that check each
+ * rounding point of the precision contract against the plain definition fed
+ * the same inputs.  Every member is NULL (not captured) or a DEVICE fp32
+ * buffer, row-major; values stored in bf16 by the forward are written exactly
+ * (as fp32).  "rows" is the entry point's row set:
+ *   grpo_prefill:          R = P * Tp prompt rows (prompt-major); head rows = P
+ *                          (the last position of each prompt)
+ *   grpo_rollout_step[_grouped]: R = B batch rows, the call's last step
+ *   grpo_score_sequences[_grouped]: R = N * T rows (sequence-major; rows a call
+ *                          does not compute are left unwritten: the grouped call
+ *                          computes no row T-1); head rows = N * (T - score_from),
+ *                          the scored positions score_from-1 .. T-2
+ * A call with a trace runs without graph replay.
+ *   x        [n_layers + 1][R][d]   residual entering each layer, then leaving the last
+ *   x_attn   [n_layers][R][d]       residual after the attention block (x + o Wo^T)
+ *   h_attn   [n_layers][R][d]       normed input of the QKV projection
+ *   q        [n_layers][R][H*hd]    queries after RoPE
+ *   k, v     [n_layers][R][Hkv*hd]  keys after RoPE and values, as cached
+ *   o        [n_layers][R][H*hd]    attention output
+ *   h_mlp    [n_layers][R][d]       normed input of the gate/up projection
+ *   act      [n_layers][R][d_ffn]   SwiGLU output
+ *   h_final  [head rows][d]         normed input of the LM head
+ *   logits   [head rows][vocab]     fp32 logits (decode: the sampler's input) */
+typedef struct grpo_trace {
+  float* x;
+  float* x_attn;
+  float* h_attn;
+  float* q;
+  float* k;
+  float* v;
+  float* o;
+  float* h_mlp;
+  float* act;
+  float* h_final;
+  float* logits;
+} grpo_trace;
+
 typedef struct grpo_model grpo_model;
 
 /* Creates a handle over caller-owned weights.  Validates the shape (see
@@ -157,36 +194,38 @@ const char* grpo_last_error(void);
  *   prompts   int32 [P, Tp] token ids in [0, vocab)
  *   kv        cache of n_seqs >= P*G sequences, max_len >= Tp
  *   tok_out   int32 [P*G] sampled tokens;  logp_out  fp32 [P*G]
- *   logits_dbg NULL or fp32 [P, vocab]: the last-position logits
- *   hidden_dbg NULL or fp32 [n_layers+1, P*Tp, d]: residual stream entering
- *              each layer and leaving the last one, every prompt position
+ *   trace     NULL or the intermediates to capture (see grpo_trace)
  * Ids outside [0, vocab) are clamped by the kernels (memory safety only). */
 int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
                  const int32_t* prompts, int32_t P, int32_t Tp, int32_t G,
-                 const grpo_sampling* s, int32_t* tok_out, float* logp_out, float* logits_dbg,
-                 float* hidden_dbg, void* ws, size_t ws_bytes, void* stream);
+                 const grpo_sampling* s, int32_t* tok_out, float* logp_out,
+                 const grpo_trace* trace, void* ws, size_t ws_bytes, void* stream);
 
-/* n_steps decode steps for batch rows 0..B-1 (cache slots 0..B-1, Philox
- * sequence id = row).  Per step: token tok[b] enters at position pos[b] (its
- * K/V written there), attention over positions 0..pos[b], the next token is
- * drawn with Philox step step0+s and written to tok[b] and tok_out[b, s], its
- * log-prob to logp_out[b, s]; pos[b] += 1.
+/* n_steps decode steps for batch rows 0..B-1 (Alg. 1, sampling step).  Row b
+ * is sequence seq_ids[b]: its K/V live in cache slot seq_ids[b] and its draws
+ * use Philox sequence id seq_ids[b], so a row set that changes between calls
+ * (sequences paused for a tool call, finished ones replaced) continues every
+ * sequence exactly where it stopped.  Per step: token tok[b] enters at position
+ * pos[b] (its K/V written there), attention over positions 0..pos[b], the next
+ * token is drawn with Philox step step0+s and written to tok[b] and
+ * tok_out[b, s], its log-prob to logp_out[b, s]; pos[b] += 1.
+ *   seq_ids    HOST int32 [B], distinct, each in [0, n_seqs); NULL means
+ *              seq_ids[b] = b.  Read before the call returns.
  *   pos, tok   int32 [B] device, in/out
  *   max_pos    host hint: the largest pos[b] on entry.  The call is rejected
  *              with GRPO_KV_CAPACITY unless max_pos + n_steps <= max_len; the
  *              kernels additionally never touch positions >= max_len.
  *   tok_out    int32 [B, n_steps];  logp_out  fp32 [B, n_steps]
- * With n_steps >= 2 and no debug output the step is captured once as a HIP
- * graph and replayed n_steps times; the graph is kept in the model handle and
- * recaptured when an argument changes, so a handle must not be used from two
- * threads at once.
- *   logits_dbg NULL or fp32 [B, vocab]: logits of the last step
- *   hidden_dbg NULL or fp32 [n_layers+1, B, d]: residual stream entering each
- *              layer and leaving the last one, for the last step */
+ *   trace      NULL or the intermediates of the last step (see grpo_trace)
+ * B <= 128 for bf16 models.  With n_steps >= 2 and no trace the step is
+ * captured once as a HIP graph and replayed n_steps times; the graph is kept in
+ * the model handle and recaptured when an argument changes, so a handle must
+ * not be used from two threads at once.  GRPO_INVALID_ARG for seq_ids out of
+ * range or repeated. */
 int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len, int32_t B,
-                      int32_t* pos, int32_t* tok, int32_t max_pos, int32_t step0, int32_t n_steps,
-                      const grpo_sampling* s, int32_t* tok_out, float* logp_out,
-                      float* logits_dbg, float* hidden_dbg, void* ws, size_t ws_bytes,
+                      const int32_t* seq_ids, int32_t* pos, int32_t* tok, int32_t max_pos,
+                      int32_t step0, int32_t n_steps, const grpo_sampling* s, int32_t* tok_out,
+                      float* logp_out, const grpo_trace* trace, void* ws, size_t ws_bytes,
                       void* stream);
 
 /* grpo_rollout_step for a batch of groups: rows g*G .. g*G+G-1 are the G
@@ -194,9 +233,9 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
  * lays them out so), and their cache positions 0 .. prefix_len-1 hold the same
  * K/V (the prompt, written once per prompt by grpo_prefill into every member's
  * slot).  Attention reads those positions once per group, from the slot of row
- * g*G, instead of once per row; each row's later positions come from its own
- * slot.  Every row must be at pos[b] >= prefix_len on entry (true after
- * grpo_prefill with prefix_len = Tp), so that no step writes a shared
+ * g*G (seq_ids[g*G]), instead of once per row; each row's later positions come
+ * from its own slot.  Every row must be at pos[b] >= prefix_len on entry (true
+ * after grpo_prefill with prefix_len = Tp), so that no step writes a shared
  * position; the kernels cut the shared length to min(prefix_len, pos[b] + 1)
  * over a group's rows, so they never read past a row's own context.  Under
  * these conditions the results are those of grpo_rollout_step except for the
@@ -208,19 +247,20 @@ int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max
  * one grpo_workspace_bytes(GRPO_OP_ROLLOUT) gives.  GRPO_INVALID_ARG for a G or
  * prefix_len outside these ranges. */
 int grpo_rollout_step_grouped(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
-                              int32_t B, int32_t G, int32_t prefix_len, int32_t* pos, int32_t* tok,
-                              int32_t max_pos, int32_t step0, int32_t n_steps,
-                              const grpo_sampling* s, int32_t* tok_out, float* logp_out,
-                              float* logits_dbg, float* hidden_dbg, void* ws, size_t ws_bytes,
-                              void* stream);
+                              int32_t B, int32_t G, int32_t prefix_len, const int32_t* seq_ids,
+                              int32_t* pos, int32_t* tok, int32_t max_pos, int32_t step0,
+                              int32_t n_steps, const grpo_sampling* s, int32_t* tok_out,
+                              float* logp_out, const grpo_trace* trace, void* ws,
+                              size_t ws_bytes, void* stream);
 
 /* Teacher-forced scoring (Eq. 1's log pi and the KL term's reference): for
  * j in [score_from, T): logp_out[n, j - score_from] =
  * log_softmax(logits at position j-1 / temperature)[tokens[n, j]]
- * (temperature 0 is read as 1).  tokens int32 [N, T]; 1 <= score_from < T. */
+ * (temperature 0 is read as 1).  tokens int32 [N, T]; 1 <= score_from < T.
+ * trace: NULL or the intermediates to capture (see grpo_trace). */
 int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, int32_t T,
-                         int32_t score_from, float temperature, float* logp_out, void* ws,
-                         size_t ws_bytes, void* stream);
+                         int32_t score_from, float temperature, float* logp_out,
+                         const grpo_trace* trace, void* ws, size_t ws_bytes, void* stream);
 
 /* grpo_score_sequences for groups that share a prefix: rows g*G .. g*G+G-1 of
  * tokens are the G samples of one prompt (Alg. 1) and hold the same tokens at
@@ -237,8 +277,8 @@ int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, 
  * prefix_len outside these ranges. */
 int grpo_score_sequences_grouped(const grpo_model* m, const int32_t* tokens, int32_t N,
                                  int32_t T, int32_t score_from, float temperature, int32_t G,
-                                 int32_t prefix_len, float* logp_out, void* ws, size_t ws_bytes,
-                                 void* stream);
+                                 int32_t prefix_len, float* logp_out, const grpo_trace* trace,
+                                 void* ws, size_t ws_bytes, void* stream);
 
 /* Group advantages (Alg. 1, normalisation step): for each of the P groups of
  * G >= 2 rewards, A = (r - mean) / (sample std (divisor G-1) + eps); a group
@@ -263,6 +303,19 @@ int grpo_token_loss(const float* logp, const float* logp_old, const float* logp_
                     const uint8_t* mask, const float* adv, int32_t N, int32_t Tr, float clip_eps,
                     float beta, int32_t agg, float* loss_out, float* tok_loss, float* dloss_dlogp,
                     float* stats, void* ws, size_t ws_bytes, void* stream);
+
+/* Reduction structure of a decode step, for error analysis of its results
+ * (the order in which partial sums meet decides the rounding).  For a model, a
+ * batch of B rows, a KV capacity max_len and a grouping (G, prefix_len as
+ * grpo_rollout_step_grouped; G = 0 for grpo_rollout_step) it writes
+ *   out[0..3] split-K factors of the QKV, O, down and LM-head projections
+ *   out[4]    context positions per decode-attention span; out[5] spans
+ *   out[6]    positions per prompt chunk of a grouped step; out[7] chunks
+ *             (both 0 without grouping or for fp32 models)
+ * fp32 models: out[0..7] = 0 (they use one fma chain per output).
+ * GRPO_INVALID_ARG for a NULL pointer or sizes outside the call's ranges. */
+int grpo_decode_structure(const grpo_model* m, int32_t B, int32_t max_len, int32_t G,
+                          int32_t prefix_len, int32_t* out);
 
 /* Kernel timing for benchmarks.  Between grpo_profile_begin and
  * grpo_profile_end every kernel launch of the library is bracketed by HIP

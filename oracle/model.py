@@ -56,27 +56,16 @@ def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
 class OracleModel:
     """cfg: any object with the decoder shape attributes (n_layers, d_model, ...).
 
-    precision "fp64" is the oracle.  "fp32" and "fp32-seq" evaluate the same
-    definition with float32 arithmetic; they are not references but measuring
-    sticks: their distance from the fp64 result is the noise floor that an
-    fp32-accumulating implementation of the same rounding contract shows.
-    "fp32" takes BLAS's summation order for the weight products; "fp32-seq"
-    adds 32-term float32 partial products one after the other along the
-    contraction, the order in which matrix-core instructions accumulate.
-    """
+    Everything is evaluated in fp64; for bf16 models (weights stored as bf16 bit
+    patterns) the rounding points R1..R5 are applied unless round_points is
+    False."""
 
-    MM_CHUNK = 32
-
-    def __init__(self, cfg, weights: dict, round_points: bool = True, precision: str = "fp64"):
+    def __init__(self, cfg, weights: dict, round_points: bool = True):
         self.cfg = cfg
         self.w = weights
         self.bf16 = np.asarray(weights["tok_emb"]).dtype == np.uint16
-        self.dt = {"fp64": np.float64, "fp32": np.float32, "fp32-seq": np.float32}[precision]
-        self.seq_mm = precision == "fp32-seq"
-        if self.bf16 and round_points:
-            self.R = lambda x: round_bf16(x).astype(self.dt)
-        else:
-            self.R = _ident
+        self.dt = np.float64
+        self.R = round_bf16 if (self.bf16 and round_points) else _ident
         self._f64 = {}
 
     # -- weights --------------------------------------------------------------
@@ -92,14 +81,7 @@ class OracleModel:
 
     def mm(self, h: np.ndarray, name: str) -> np.ndarray:
         """h @ W^T for the weight matrix `name` ([out, in])."""
-        W = self.mat(name)
-        if not self.seq_mm:
-            return h @ W.T
-        K = W.shape[1]
-        acc = np.zeros(h.shape[:-1] + (W.shape[0],), np.float32)
-        for k0 in range(0, K, self.MM_CHUNK):
-            acc += h[..., k0:k0 + self.MM_CHUNK] @ W[:, k0:k0 + self.MM_CHUNK].T
-        return acc
+        return h @ self.mat(name).T
 
     def embed(self, tokens) -> np.ndarray:
         a = np.asarray(self.w["tok_emb"])[np.asarray(tokens)]

@@ -33,9 +33,7 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
 
 
 def _float(x) -> np.ndarray:
-    """float32 arrays stay float32 (the noise-floor variant); all else is float64."""
-    x = np.asarray(x)
-    return x if x.dtype == np.float32 else x.astype(np.float64)
+    return np.asarray(x, np.float64)
 
 
 def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
@@ -59,7 +57,7 @@ def rope_angles(pos: np.ndarray, head_dim: int, theta: float) -> np.ndarray:
 def rope(v: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
     """Rotate [T, n_heads, hd] vectors at positions pos[T], half-split pairing.
 
-    Angles, cos and sin are fp64; float32 input is rotated in float32."""
+    Angles, cos, sin and the rotation are fp64."""
     v = _float(v)
     hd = v.shape[-1]
     a = rope_angles(pos, hd, theta)[:, None, :]

@@ -48,9 +48,72 @@ class Sampling(C.Structure):
     _fields_ = [("temperature", C.c_float), ("top_k", C.c_int32), ("seed", C.c_uint64)]
 
 
+TRACE_FIELDS = ("x", "x_attn", "h_attn", "q", "k", "v", "o", "h_mlp", "act", "h_final", "logits")
+
+
+class TraceStruct(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in TRACE_FIELDS]
+
+
+class Trace:
+    """Device buffers of a grpo_trace for a call with `rows` forward rows and
+    `head_rows` LM-head rows (see include/grpo_hip.h), filled with NaN so that
+    rows a call leaves unwritten stay recognisable."""
+
+    def __init__(self, cfg: ModelConfig, rows: int, head_rows: int, fields=TRACE_FIELDS,
+                 device="cuda"):
+        L, d, f = cfg.n_layers, cfg.d_model, cfg.d_ffn
+        shapes = dict(x=(L + 1, rows, d), x_attn=(L, rows, d), h_attn=(L, rows, d),
+                      q=(L, rows, cfg.q_dim), k=(L, rows, cfg.kv_dim), v=(L, rows, cfg.kv_dim),
+                      o=(L, rows, cfg.q_dim), h_mlp=(L, rows, d), act=(L, rows, f),
+                      h_final=(head_rows, d), logits=(head_rows, cfg.vocab))
+        self.t = {n: torch.full(shapes[n], float("nan"), dtype=torch.float32, device=device)
+                  for n in fields}
+        self._s = TraceStruct(*[_ptr(self.t.get(n)) for n in TRACE_FIELDS])
+
+    def struct(self):
+        return C.byref(self._s)
+
+    def numpy(self) -> dict:
+        return {n: t.cpu().numpy().astype(np.float64) for n, t in self.t.items()}
+
+    def lazy(self) -> dict:
+        """Members that copy only the rows they are indexed with to the host:
+        lazy()["x"][layer][rows] -> float64 array."""
+        return {n: _LazyMember(t) for n, t in self.t.items()}
+
+
+class _LazyMember:
+    def __init__(self, t):
+        self.t = t
+
+    def __getitem__(self, i):
+        if self.t.dim() == 3 and isinstance(i, (int, np.integer)):
+            return _LazyMember(self.t[int(i)])
+        if isinstance(i, slice):
+            return self.t[i].cpu().numpy().astype(np.float64)
+        idx = torch.as_tensor(np.asarray(i), device=self.t.device, dtype=torch.long)
+        return self.t[idx].cpu().numpy().astype(np.float64)
+
+
+def _trace(tr):
+    return tr.struct() if tr is not None else None
+
+
+def _ids(seq_ids, B):
+    if seq_ids is None:
+        return None
+    a = np.ascontiguousarray(np.asarray(seq_ids, np.int32).ravel())
+    if a.size != B:
+        raise ValueError(f"seq_ids has {a.size} entries, the batch {B}")
+    return (C.c_int32 * B)(*a.tolist())
+
+
 _lib = None
 
 _VP, _I32, _F32, _SZ = C.c_void_p, C.c_int32, C.c_float, C.c_size_t
+_IP = C.POINTER(C.c_int32)
+_TP = C.POINTER(TraceStruct)
 _SIGS = {
     "grpo_model_create": (_I32, [C.POINTER(Config), C.POINTER(Weights), C.POINTER(_VP)]),
     "grpo_model_destroy": (_I32, [_VP]),
@@ -60,18 +123,19 @@ _SIGS = {
     "grpo_workspace_bytes": (_SZ, [_VP, _I32, _I32, _I32]),
     "grpo_last_error": (C.c_char_p, []),
     "grpo_prefill": (_I32, [_VP, _VP, _I32, _I32, _VP, _I32, _I32, _I32, C.POINTER(Sampling),
-                            _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
-    "grpo_rollout_step": (_I32, [_VP, _VP, _I32, _I32, _I32, _VP, _VP, _I32, _I32, _I32,
-                                 C.POINTER(Sampling), _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
-    "grpo_rollout_step_grouped": (_I32, [_VP, _VP, _I32, _I32, _I32, _I32, _I32, _VP, _VP, _I32,
-                                         _I32, _I32, C.POINTER(Sampling), _VP, _VP, _VP, _VP, _VP,
-                                         _SZ, _VP]),
-    "grpo_score_sequences": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _VP, _VP, _SZ, _VP]),
+                            _VP, _VP, _TP, _VP, _SZ, _VP]),
+    "grpo_rollout_step": (_I32, [_VP, _VP, _I32, _I32, _I32, _IP, _VP, _VP, _I32, _I32, _I32,
+                                 C.POINTER(Sampling), _VP, _VP, _TP, _VP, _SZ, _VP]),
+    "grpo_rollout_step_grouped": (_I32, [_VP, _VP, _I32, _I32, _I32, _I32, _I32, _IP, _VP, _VP,
+                                         _I32, _I32, _I32, C.POINTER(Sampling), _VP, _VP, _TP,
+                                         _VP, _SZ, _VP]),
+    "grpo_score_sequences": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _VP, _TP, _VP, _SZ, _VP]),
     "grpo_score_sequences_grouped": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _I32, _I32, _VP,
-                                            _VP, _SZ, _VP]),
+                                            _TP, _VP, _SZ, _VP]),
     "grpo_advantages": (_I32, [_VP, _I32, _I32, _F32, _VP, _VP]),
     "grpo_token_loss": (_I32, [_VP, _VP, _VP, _VP, _VP, _I32, _I32, _F32, _F32, _I32, _VP, _VP,
                                _VP, _VP, _VP, _SZ, _VP]),
+    "grpo_decode_structure": (_I32, [_VP, _I32, _I32, _I32, _I32, _IP]),
     "grpo_profile_begin": (_I32, []),
     "grpo_profile_end": (_I32, [C.c_char_p, _SZ]),
 }
@@ -211,35 +275,38 @@ def alloc_kv(cfg: ModelConfig, n_seqs: int, max_len: int, device="cuda"):
 
 
 def prefill(model: Model, kv, n_seqs: int, max_len: int, prompts, G: int, sampling: Sampling,
-            tok_out, logp_out, logits_dbg=None, hidden_dbg=None, ws=None, stream=None):
+            tok_out, logp_out, trace: Trace | None = None, ws=None, stream=None):
     P, Tp = prompts.shape
     _check(lib().grpo_prefill(model.handle, _ptr(kv), n_seqs, max_len, _ptr(prompts), P, Tp, G,
-                              C.byref(sampling), _ptr(tok_out), _ptr(logp_out), _ptr(logits_dbg),
-                              _ptr(hidden_dbg), _ptr(ws), ws.numel() if ws is not None else 0,
-                              _stream(stream)))
+                              C.byref(sampling), _ptr(tok_out), _ptr(logp_out), _trace(trace),
+                              _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)))
 
 
 def rollout_step(model: Model, kv, n_seqs: int, max_len: int, pos, tok, max_pos: int, step0: int,
-                 n_steps: int, sampling: Sampling, tok_out, logp_out, logits_dbg=None,
-                 hidden_dbg=None, ws=None, stream=None, group: int = 0, prefix_len: int = 0):
+                 n_steps: int, sampling: Sampling, tok_out, logp_out, seq_ids=None,
+                 trace: Trace | None = None, ws=None, stream=None, group: int = 0,
+                 prefix_len: int = 0):
     """grpo_rollout_step, or grpo_rollout_step_grouped when group > 0 (rows in
-    groups of `group` sharing cache positions below prefix_len)."""
+    groups of `group` sharing cache positions below prefix_len).  seq_ids: host
+    sequence of B ints (cache slot and Philox sequence id of each row) or None."""
     B = pos.numel()
     nws = ws.numel() if ws is not None else 0
+    ids = _ids(seq_ids, B)
     if group > 0:
         _check(lib().grpo_rollout_step_grouped(
-            model.handle, _ptr(kv), n_seqs, max_len, B, group, prefix_len, _ptr(pos), _ptr(tok),
-            max_pos, step0, n_steps, C.byref(sampling), _ptr(tok_out), _ptr(logp_out),
-            _ptr(logits_dbg), _ptr(hidden_dbg), _ptr(ws), nws, _stream(stream)))
+            model.handle, _ptr(kv), n_seqs, max_len, B, group, prefix_len, ids, _ptr(pos),
+            _ptr(tok), max_pos, step0, n_steps, C.byref(sampling), _ptr(tok_out), _ptr(logp_out),
+            _trace(trace), _ptr(ws), nws, _stream(stream)))
         return
-    _check(lib().grpo_rollout_step(model.handle, _ptr(kv), n_seqs, max_len, B, _ptr(pos),
+    _check(lib().grpo_rollout_step(model.handle, _ptr(kv), n_seqs, max_len, B, ids, _ptr(pos),
                                    _ptr(tok), max_pos, step0, n_steps, C.byref(sampling),
-                                   _ptr(tok_out), _ptr(logp_out), _ptr(logits_dbg),
-                                   _ptr(hidden_dbg), _ptr(ws), nws, _stream(stream)))
+                                   _ptr(tok_out), _ptr(logp_out), _trace(trace), _ptr(ws), nws,
+                                   _stream(stream)))
 
 
-def score_sequences(model: Model, tokens, score_from: int, temperature: float, logp_out, ws=None,
-                    stream=None, group: int = 0, prefix_len: int = 0):
+def score_sequences(model: Model, tokens, score_from: int, temperature: float, logp_out,
+                    trace: Trace | None = None, ws=None, stream=None, group: int = 0,
+                    prefix_len: int = 0):
     """grpo_score_sequences, or grpo_score_sequences_grouped when group > 0 (rows in
     groups of `group` sharing their first prefix_len tokens)."""
     N, T = tokens.shape
@@ -247,10 +314,11 @@ def score_sequences(model: Model, tokens, score_from: int, temperature: float, l
     if group > 0:
         _check(lib().grpo_score_sequences_grouped(model.handle, _ptr(tokens), N, T, score_from,
                                                   temperature, group, prefix_len, _ptr(logp_out),
-                                                  _ptr(ws), nws, _stream(stream)))
+                                                  _trace(trace), _ptr(ws), nws, _stream(stream)))
         return
     _check(lib().grpo_score_sequences(model.handle, _ptr(tokens), N, T, score_from, temperature,
-                                      _ptr(logp_out), _ptr(ws), nws, _stream(stream)))
+                                      _ptr(logp_out), _trace(trace), _ptr(ws), nws,
+                                      _stream(stream)))
 
 
 def advantages(rewards, P: int, G: int, eps: float, adv_out, stream=None):
@@ -264,6 +332,15 @@ def token_loss(logp, logp_old, logp_ref, mask, adv, clip_eps: float, beta: float
                                  N, Tr, clip_eps, beta, agg, _ptr(loss_out), _ptr(tok_loss),
                                  _ptr(dloss_dlogp), _ptr(stats), _ptr(ws),
                                  ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def decode_structure(model: Model, B: int, max_len: int, G: int = 0, prefix_len: int = 0) -> dict:
+    """grpo_decode_structure as a dict."""
+    out = (C.c_int32 * 8)()
+    _check(lib().grpo_decode_structure(model.handle, B, max_len, G, prefix_len, out))
+    v = list(out)
+    return dict(splits_qkv=v[0], splits_o=v[1], splits_down=v[2], splits_head=v[3], span=v[4],
+                spans=v[5], chunk=v[6], chunks=v[7])
 
 
 def profile_begin():

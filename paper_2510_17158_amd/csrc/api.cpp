@@ -328,6 +328,7 @@ struct RolloutWS {
   float* logits;
   float* attn_part;
   int32_t* step_ctr;   // decode steps done by the replayed graph
+  int32_t* slots;      // [B] cache slot / Philox sequence id of each row (seq_ids)
 };
 RolloutWS take_rollout(Bump& b, const grpo_config& c, int B, int max_len) {
   RolloutWS w;
@@ -338,6 +339,7 @@ RolloutWS take_rollout(Bump& b, const grpo_config& c, int B, int max_len) {
                           : decode_attn_part_floats_max(B, c.n_heads, c.n_kv_heads, c.head_dim,
                                                         max_len));
   w.step_ctr = b.take<int32_t>(1);
+  w.slots = b.take<int32_t>(B);
   return w;
 }
 
@@ -390,21 +392,29 @@ WStack gate_up(const grpo_model* m, int l) {
   return WStack{{m->w_gate[l], m->w_up[l], m->w_up[l]}, m->cfg.d_ffn, 2 * m->cfg.d_ffn};
 }
 
-int copy_rows(float* dst, const float* x, size_t n, hipStream_t st) {
-  HIPCHK(hipMemcpyAsync(dst, x, n * 4, hipMemcpyDeviceToDevice, st));
+// Trace capture: rows of a forward buffer into layer l of a trace member
+// ([layers][R][width] fp32); a NULL member is skipped.
+int trace(float* member, int l, size_t R, int width, const void* src, int layout, int ld, int M,
+          TraceMap map, hipStream_t st) {
+  if (!member || M <= 0) return GRPO_OK;
+  HIPCHK(trace_rows(src, layout, ld, M, width, map, member + (size_t)l * R * width, st));
   return GRPO_OK;
 }
+// trace member pointer or NULL
+#define TRM(tr, f) ((tr) ? (tr)->f : nullptr)
 
 // Layers of a many-row forward (prefill or scoring).  Rows are sequence-major
 // (row = seq * T + t).  K/V go to kc/vc (cache layout with n_slots slots of
 // k_len positions; sequence s at slot s * G) and V also transposed to vt.
+// tr: trace of R rows, these rows at tmap.
 int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slots, int k_len,
-                 void* kv_or_null, void* kbuf, void* vbuf, uint16_t* vt, float* hidden_dbg,
-                 hipStream_t st) {
+                 void* kv_or_null, void* kbuf, void* vbuf, uint16_t* vt, const grpo_trace* tr,
+                 size_t R, TraceMap tmap, hipStream_t st) {
   const grpo_config& c = m->cfg;
   const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
   const int N = M / T;
   const Partials none{nullptr, 0, 0, d};
+  const int act = c.dtype == GRPO_F32 ? TR_F32 : TR_BF16;
   int rc;
   HIPCHK(rope_table(nullptr, T, c.head_dim, c.rope_theta, w.cs, st));
   for (int l = 0; l < c.n_layers; ++l) {
@@ -416,7 +426,8 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
     }
     HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), none, m->attn_norm[l], M, d, c.rms_eps,
                    w.h, d, st));
-    if (hidden_dbg && (rc = copy_rows(hidden_dbg + (size_t)l * M * d, w.x, (size_t)M * d, st)))
+    if ((rc = trace(TRM(tr, x), l, R, d, w.x, TR_F32, d, M, tmap, st)) ||
+        (rc = trace(TRM(tr, h_attn), l, R, d, w.h, act, d, M, tmap, st)))
       return rc;
     if ((rc = gemm_rows(m, w.h, d, M, qkv_stack(m, l), qd + 2 * kvd, d, EPI_STORE,
                         EpiArgs{w.qkv, nullptr, qd + 2 * kvd}, st)))
@@ -428,25 +439,43 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
     ra.vt = c.dtype == GRPO_F32 ? nullptr : vt; ra.vt_len = round8(T);
     ra.splits = 1; ra.split_stride = 0;
     ra.cs = w.cs;
+    if (tr) {
+      ra.tq = tr->q ? tr->q + (size_t)l * R * qd : nullptr;
+      ra.tk = tr->k ? tr->k + (size_t)l * R * kvd : nullptr;
+      ra.tv = tr->v ? tr->v + (size_t)l * R * kvd : nullptr;
+      ra.tmap = tmap;
+    }
     HIPCHK(rope_kv(c.dtype, w.qkv, M, w.q, ra, st));
     HIPCHK(attn_prefill(c.dtype, w.q, kl, c.dtype == GRPO_F32 ? vl : (const void*)vt, N, T,
                         c.n_heads, c.n_kv_heads, c.head_dim, k_len, G, w.o, st));
+    if ((rc = trace(TRM(tr, o), l, R, qd, w.o, act, qd, M, tmap, st))) return rc;
     if ((rc = gemm_rows(m, w.o, qd, M, one(m->wo[l]), d, qd, EPI_RESID, EpiArgs{w.x, nullptr, d},
                         st)))
       return rc;
     HIPCHK(rmsnorm(c.dtype, w.x, d, RowMap::identity(), none, m->mlp_norm[l], M, d, c.rms_eps,
                    w.h, d, st));
+    if ((rc = trace(TRM(tr, x_attn), l, R, d, w.x, TR_F32, d, M, tmap, st)) ||
+        (rc = trace(TRM(tr, h_mlp), l, R, d, w.h, act, d, M, tmap, st)))
+      return rc;
     if ((rc = gemm_rows(m, w.h, d, M, gate_up(m, l), f, d, EPI_SWIGLU, EpiArgs{nullptr, w.a, f},
                         st)))
       return rc;
+    if ((rc = trace(TRM(tr, act), l, R, f, w.a, act, f, M, tmap, st))) return rc;
     if ((rc = gemm_rows(m, w.a, f, M, one(m->w_down[l]), d, f, EPI_RESID, EpiArgs{w.x, nullptr, d},
                         st)))
       return rc;
   }
-  if (hidden_dbg && (rc = copy_rows(hidden_dbg + (size_t)c.n_layers * M * d, w.x, (size_t)M * d,
-                                    st)))
+  return trace(TRM(tr, x), c.n_layers, R, d, w.x, TR_F32, d, M, tmap, st);
+}
+
+// head rows [off, off + M) of a scoring trace: normed input and logits
+int score_head_trace(const grpo_config& c, const grpo_trace* tr, size_t R, const void* hs,
+                     const float* logits, int M, int off, hipStream_t st) {
+  if (!tr) return GRPO_OK;
+  if (int rc = trace(tr->h_final, 0, R, c.d_model, hs, c.dtype == GRPO_F32 ? TR_F32 : TR_BF16,
+                     c.d_model, M, TraceMap::rows(off), st))
     return rc;
-  return GRPO_OK;
+  return trace(tr->logits, 0, R, c.vocab, logits, TR_F32, c.vocab, M, TraceMap::rows(off), st);
 }
 
 int check_sampling(const grpo_sampling* s, int vocab) {
@@ -550,6 +579,34 @@ int grpo_model_pack_decode(grpo_model* m, void* buf, size_t bytes, void* stream)
   return GRPO_OK;
 }
 
+int grpo_decode_structure(const grpo_model* m, int32_t B, int32_t max_len, int32_t G,
+                          int32_t prefix_len, int32_t* out) {
+  if (!m || !out) return fail(GRPO_INVALID_ARG, "model and out must be set");
+  if (B < 1 || B > 128 || max_len < 1 || G < 0 || (G > 0 && B % G) || prefix_len < 0 ||
+      prefix_len > max_len)
+    return fail(GRPO_INVALID_ARG, "sizes outside the decode step's ranges");
+  for (int i = 0; i < 8; ++i) out[i] = 0;
+  const grpo_config& c = m->cfg;
+  if (c.dtype == GRPO_F32) {
+    g_err.clear();
+    return GRPO_OK;
+  }
+  const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
+  out[0] = decode_plan(B, qd + 2 * kvd, d, EPI_PARTIAL, decode_target()).splits;
+  out[1] = decode_plan(B, d, qd, EPI_PARTIAL, decode_target()).splits;
+  out[2] = decode_plan(B, d, f, EPI_PARTIAL, decode_target()).splits;
+  out[3] = decode_plan(B, c.vocab, d, EPI_PARTIAL, decode_target(), 1).splits;
+  const bool grouped = G > 0 && prefix_len > 0;
+  const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.n_kv_heads, c.head_dim, max_len,
+                                             grouped ? G : 0, grouped ? prefix_len : 0);
+  out[4] = ap.tc;
+  out[5] = ap.splits;
+  out[6] = grouped ? ap.span_p : 0;
+  out[7] = grouped ? ap.chunks : 0;
+  g_err.clear();
+  return GRPO_OK;
+}
+
 int grpo_profile_begin(void) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   g_prof_acc.clear();
@@ -604,7 +661,7 @@ size_t grpo_workspace_bytes(const grpo_model* m, int32_t op, int32_t n_rows, int
 
 int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
                  const int32_t* prompts, int32_t P, int32_t Tp, int32_t G, const grpo_sampling* s,
-                 int32_t* tok_out, float* logp_out, float* logits_dbg, float* hidden_dbg, void* ws,
+                 int32_t* tok_out, float* logp_out, const grpo_trace* trace_out, void* ws,
                  size_t ws_bytes, void* stream) {
   if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
   const grpo_config& c = m->cfg;
@@ -625,7 +682,7 @@ int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
   const int M = P * Tp, d = c.d_model;
   HIPCHK(embed(c.dtype, m->tok_emb, prompts, M, d, c.vocab, w.s.x, st));
   if (int rc = forward_rows(m, w.s, M, Tp, G, n_seqs, max_len, kv, nullptr, nullptr, w.vt,
-                            hidden_dbg, st))
+                            trace_out, (size_t)M, TraceMap::rows(), st))
     return rc;
   const Partials none{nullptr, 0, 0, d};
   HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{0, 1, Tp, Tp - 1}, none, m->final_norm, P, d, c.rms_eps,
@@ -633,34 +690,49 @@ int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
   if (int rc = gemm_rows(m, w.hl, d, P, one(m->lm_head), c.vocab, d, EPI_STORE,
                          EpiArgs{w.logits, nullptr, c.vocab}, st))
     return rc;
+  if (int rc = trace(TRM(trace_out, h_final), 0, P, d, w.hl,
+                     c.dtype == GRPO_F32 ? TR_F32 : TR_BF16, d, P, TraceMap::rows(), st))
+    return rc;
+  if (int rc = trace(TRM(trace_out, logits), 0, P, c.vocab, w.logits, TR_F32, c.vocab, P,
+                     TraceMap::rows(), st))
+    return rc;
   SampleArgs sa{};
   sa.temperature = s->temperature; sa.top_k = s->top_k; sa.seed = s->seed; sa.step = 0;
   sa.G = G; sa.tok_out = tok_out; sa.logp_out = logp_out; sa.out_stride = 1;
   HIPCHK(sample(w.logits, P, c.vocab, c.vocab, sa, st));
-  if (logits_dbg)
-    HIPCHK(hipMemcpyAsync(logits_dbg, w.logits, (size_t)P * c.vocab * 4, hipMemcpyDeviceToDevice, st));
   g_err.clear();
   return GRPO_OK;
 }
 
 // Decode steps; G > 0: rows in groups of G sharing the cache below prefix_len.
 static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len, int32_t B,
-                   int32_t* pos, int32_t* tok, int32_t max_pos, int32_t step0, int32_t n_steps,
-                   const grpo_sampling* s, int32_t* tok_out, float* logp_out, float* logits_dbg,
-                   float* hidden_dbg, int32_t G, int32_t prefix_len, void* ws, size_t ws_bytes,
-                   void* stream) {
+                   const int32_t* seq_ids, int32_t* pos, int32_t* tok, int32_t max_pos,
+                   int32_t step0, int32_t n_steps, const grpo_sampling* s, int32_t* tok_out,
+                   float* logp_out, const grpo_trace* trace_out, int32_t G, int32_t prefix_len,
+                   void* ws, size_t ws_bytes, void* stream) {
   if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
   const grpo_config& c = m->cfg;
   if (!kv || !pos || !tok || !tok_out || !logp_out || !ws)
     return fail(GRPO_INVALID_ARG, "kv, pos, tok, tok_out, logp_out and ws must be set");
   if (B < 1 || n_steps < 1 || max_len < 1) return fail(GRPO_INVALID_ARG, "B, n_steps, max_len must be >= 1");
   if (B > n_seqs) return fail(GRPO_INVALID_ARG, "B %d exceeds n_seqs %d", B, n_seqs);
+  if (c.dtype == GRPO_BF16 && B > 128) return fail(GRPO_UNSUPPORTED, "B %d above 128 for a bf16 model", B);
   if (max_pos < 0 || step0 < 0) return fail(GRPO_INVALID_ARG, "max_pos and step0 must be >= 0");
   if ((long)max_pos + n_steps > max_len)
     return fail(GRPO_KV_CAPACITY, "max_pos %d + n_steps %d exceeds max_len %d", max_pos, n_steps,
                 max_len);
   if (c.dtype == GRPO_F32 && max_len > 16384) return fail(GRPO_UNSUPPORTED, "fp32 caches above 16384");
   if (int rc = check_sampling(s, c.vocab)) return rc;
+  if (seq_ids) {
+    std::vector<int32_t> sorted(seq_ids, seq_ids + B);
+    for (int b = 0; b < B; ++b)
+      if (sorted[b] < 0 || sorted[b] >= n_seqs)
+        return fail(GRPO_INVALID_ARG, "seq_ids[%d] = %d outside [0, n_seqs %d)", b, sorted[b], n_seqs);
+    std::sort(sorted.begin(), sorted.end());
+    for (int b = 1; b < B; ++b)
+      if (sorted[b] == sorted[b - 1])
+        return fail(GRPO_INVALID_ARG, "seq_ids repeats sequence %d", sorted[b]);
+  }
   const size_t need = grpo_workspace_bytes(m, GRPO_OP_ROLLOUT, B, max_len);
   if (ws_bytes < need)
     return fail(GRPO_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
@@ -672,16 +744,25 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
   const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
   const bool pk = c.dtype == GRPO_BF16;
   const int nb = pk ? decode_nb(B) : 0;
+  // GEMM inputs of bf16 decode sit in fragment order over the padded batch
+  const int act = pk ? TR_FRAG : TR_F32;
+  const int act_ld = pk ? nb : 0;
   // fp32 attention reads every row's own cache (the shared positions hold the
   // same values, so the results are those of a grouped step)
   const bool grouped = pk && G > 0 && prefix_len > 0;
   const DecodeAttnPlan ap = decode_attn_plan(B, c.n_heads, c.n_kv_heads, c.head_dim, max_len,
                                              grouped ? G : 0, grouped ? prefix_len : 0);
+  // the rows' cache slots / Philox sequence ids, once per call
+  const int32_t* slots = nullptr;
+  if (seq_ids) {
+    HIPCHK(set_i32(w.slots, seq_ids, B, st));
+    slots = w.slots;
+  }
+  const TraceMap rows = TraceMap::rows();
   // One decode step on stream `ss`.  In graph mode the Philox step and the output
   // column come from the device step counter (advanced by the embedding kernel).
   auto enqueue_step = [&](hipStream_t ss, bool graph, int step) -> int {
-    const bool last = step == n_steps - 1;
-    float* hdbg = last ? hidden_dbg : nullptr;
+    const grpo_trace* tr = step == n_steps - 1 ? trace_out : nullptr;
     int rc;
     hipStream_t st = ss;
     HIPCHK(embed(c.dtype, m->tok_emb, tok, B, d, c.vocab, w.s.x, st, graph ? w.step_ctr : nullptr));
@@ -694,7 +775,9 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
       Layer L = kv_layer(m, kv, l, n_seqs, max_len);
       HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), pend, m->attn_norm[l], B, d,
                      c.rms_eps, w.s.h, d, st, nb));
-      if (hdbg && (rc = copy_rows(hdbg + (size_t)l * B * d, w.s.x, (size_t)B * d, st))) return rc;
+      if ((rc = trace(TRM(tr, x), l, B, d, w.s.x, TR_F32, d, B, rows, st)) ||
+          (rc = trace(TRM(tr, h_attn), l, B, d, w.s.h, act, pk ? act_ld : d, B, rows, st)))
+        return rc;
       const float* qsrc = w.s.qkv;
       int qs = 1;
       size_t qstride = 0;
@@ -707,15 +790,22 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
         return rc;
       }
       RopeArgs ra{};
-      ra.mode = 0; ra.T = 1; ra.G = 1; ra.pos_arr = pos;
+      ra.mode = 0; ra.T = 1; ra.G = 1; ra.pos_arr = pos; ra.slots = slots;
       ra.n_heads = c.n_heads; ra.n_kv = c.n_kv_heads; ra.hd = c.head_dim; ra.theta = c.rope_theta;
       ra.kcache = L.k; ra.vcache = L.v; ra.n_seqs = n_seqs; ra.max_len = max_len;
       ra.vt = nullptr; ra.vt_len = 0;
       ra.splits = qs; ra.split_stride = qstride;
       ra.cs = w.s.cs;
+      if (tr) {
+        ra.tq = tr->q ? tr->q + (size_t)l * B * qd : nullptr;
+        ra.tk = tr->k ? tr->k + (size_t)l * B * kvd : nullptr;
+        ra.tv = tr->v ? tr->v + (size_t)l * B * kvd : nullptr;
+        ra.tmap = rows;
+      }
       HIPCHK(rope_kv(c.dtype, qsrc, B, w.s.q, ra, st));
-      HIPCHK(attn_decode(c.dtype, w.s.q, L.k, L.v, pos, B, c.n_heads, c.n_kv_heads, c.head_dim,
-                         n_seqs, max_len, ap, w.attn_part, w.s.o, st, nb));
+      HIPCHK(attn_decode(c.dtype, w.s.q, L.k, L.v, pos, slots, B, c.n_heads, c.n_kv_heads,
+                         c.head_dim, n_seqs, max_len, ap, w.attn_part, w.s.o, st, nb));
+      if ((rc = trace(TRM(tr, o), l, B, qd, w.s.o, act, pk ? act_ld : qd, B, rows, st))) return rc;
       if (pk) {
         if ((rc = gemm_dec_resid(w.s.o, B, D.o[l], d, qd, w.s.g, &pend, st, "gemm_decode_o")))
           return rc;
@@ -725,14 +815,19 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
       }
       HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), pend, m->mlp_norm[l], B, d, c.rms_eps,
                      w.s.h, d, st, nb));
+      if ((rc = trace(TRM(tr, x_attn), l, B, d, w.s.x, TR_F32, d, B, rows, st)) ||
+          (rc = trace(TRM(tr, h_mlp), l, B, d, w.s.h, act, pk ? act_ld : d, B, rows, st)))
+        return rc;
       if (pk) {
         if ((rc = gemm_dec_swiglu(w.s.h, B, D.gate_up[l], f, d, w.s.a, st))) return rc;
+        if ((rc = trace(TRM(tr, act), l, B, f, w.s.a, act, act_ld, B, rows, st))) return rc;
         if ((rc = gemm_dec_resid(w.s.a, B, D.down[l], d, f, w.s.g, &pend, st, "gemm_decode_down")))
           return rc;
       } else {
         if ((rc = gemm_rows(m, w.s.h, d, B, gate_up(m, l), f, d, EPI_SWIGLU,
                             EpiArgs{nullptr, w.s.a, f}, st)))
           return rc;
+        if ((rc = trace(TRM(tr, act), l, B, f, w.s.a, TR_F32, f, B, rows, st))) return rc;
         if ((rc = gemm_rows(m, w.s.a, f, B, one(m->w_down[l]), d, f, EPI_RESID,
                             EpiArgs{w.s.x, nullptr, d}, st)))
           return rc;
@@ -740,7 +835,8 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
     }
     HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), pend, m->final_norm, B, d, c.rms_eps,
                    w.s.h, d, st, nb));
-    if (hdbg && (rc = copy_rows(hdbg + (size_t)c.n_layers * B * d, w.s.x, (size_t)B * d, st)))
+    if ((rc = trace(TRM(tr, x), c.n_layers, B, d, w.s.x, TR_F32, d, B, rows, st)) ||
+        (rc = trace(TRM(tr, h_final), 0, B, d, w.s.h, act, pk ? act_ld : d, B, rows, st)))
       return rc;
     if (pk) {
       const float* res;
@@ -753,10 +849,12 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
                                EpiArgs{w.logits, nullptr, c.vocab}, st))) {
       return rc;
     }
+    if ((rc = trace(TRM(tr, logits), 0, B, c.vocab, w.logits, TR_F32, c.vocab, B, rows, st)))
+      return rc;
     SampleArgs sa{};
     sa.temperature = s->temperature; sa.top_k = s->top_k; sa.seed = s->seed;
     sa.G = 1; sa.out_stride = n_steps;
-    sa.tok_state = tok; sa.pos_state = pos;
+    sa.tok_state = tok; sa.pos_state = pos; sa.seq_ids = slots;
     if (graph) {
       sa.step = step0; sa.step_ctr = w.step_ctr;
       sa.tok_out = tok_out; sa.logp_out = logp_out;
@@ -765,14 +863,10 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
       sa.tok_out = tok_out + step; sa.logp_out = logp_out + step;
     }
     HIPCHK(sample(w.logits, B, c.vocab, c.vocab, sa, st));
-    if (last && logits_dbg)
-      HIPCHK(hipMemcpyAsync(logits_dbg, w.logits, (size_t)B * c.vocab * 4,
-                            hipMemcpyDeviceToDevice, st));
     return GRPO_OK;
   };
 
-  const bool use_graph = n_steps >= 2 && !hidden_dbg && !logits_dbg && !profiling() &&
-                         !getenv("GRPO_NO_GRAPH");
+  const bool use_graph = n_steps >= 2 && !trace_out && !profiling() && !getenv("GRPO_NO_GRAPH");
   if (!use_graph) {
     for (int step = 0; step < n_steps; ++step)
       if (int rc = enqueue_step(st, false, step)) return rc;
@@ -785,7 +879,7 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
       (uint64_t)(uintptr_t)kv, (uint64_t)n_seqs, (uint64_t)max_len, (uint64_t)B,
       (uint64_t)(uintptr_t)pos, (uint64_t)(uintptr_t)tok, (uint64_t)step0, (uint64_t)n_steps,
       (uint64_t)(uintptr_t)tok_out, (uint64_t)(uintptr_t)logp_out, (uint64_t)(uintptr_t)ws,
-      (uint64_t)(uintptr_t)m->dec.base,
+      (uint64_t)(uintptr_t)m->dec.base, (uint64_t)(slots != nullptr),
       (uint64_t)*(const uint32_t*)&s->temperature, (uint64_t)(uint32_t)s->top_k, s->seed,
       (uint64_t)(uint32_t)ap.G, (uint64_t)(uint32_t)ap.prefix_len};
   HIPCHK(fill_i32(w.step_ctr, 1, -1, st));   // the first replay's embedding makes it 0
@@ -819,32 +913,32 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
 }
 
 int grpo_rollout_step(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len, int32_t B,
-                      int32_t* pos, int32_t* tok, int32_t max_pos, int32_t step0, int32_t n_steps,
-                      const grpo_sampling* s, int32_t* tok_out, float* logp_out,
-                      float* logits_dbg, float* hidden_dbg, void* ws, size_t ws_bytes,
+                      const int32_t* seq_ids, int32_t* pos, int32_t* tok, int32_t max_pos,
+                      int32_t step0, int32_t n_steps, const grpo_sampling* s, int32_t* tok_out,
+                      float* logp_out, const grpo_trace* trace, void* ws, size_t ws_bytes,
                       void* stream) {
-  return rollout(m, kv, n_seqs, max_len, B, pos, tok, max_pos, step0, n_steps, s, tok_out,
-                 logp_out, logits_dbg, hidden_dbg, 0, 0, ws, ws_bytes, stream);
+  return rollout(m, kv, n_seqs, max_len, B, seq_ids, pos, tok, max_pos, step0, n_steps, s,
+                 tok_out, logp_out, trace, 0, 0, ws, ws_bytes, stream);
 }
 
 int grpo_rollout_step_grouped(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
-                              int32_t B, int32_t G, int32_t prefix_len, int32_t* pos, int32_t* tok,
-                              int32_t max_pos, int32_t step0, int32_t n_steps,
-                              const grpo_sampling* s, int32_t* tok_out, float* logp_out,
-                              float* logits_dbg, float* hidden_dbg, void* ws, size_t ws_bytes,
-                              void* stream) {
+                              int32_t B, int32_t G, int32_t prefix_len, const int32_t* seq_ids,
+                              int32_t* pos, int32_t* tok, int32_t max_pos, int32_t step0,
+                              int32_t n_steps, const grpo_sampling* s, int32_t* tok_out,
+                              float* logp_out, const grpo_trace* trace, void* ws,
+                              size_t ws_bytes, void* stream) {
   if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
   if (G < 1 || B < 1 || B % G)
     return fail(GRPO_INVALID_ARG, "G %d must be >= 1 and divide B %d", G, B);
   if (prefix_len < 0 || prefix_len > max_len)
     return fail(GRPO_INVALID_ARG, "prefix_len %d outside [0, max_len %d]", prefix_len, max_len);
-  return rollout(m, kv, n_seqs, max_len, B, pos, tok, max_pos, step0, n_steps, s, tok_out,
-                 logp_out, logits_dbg, hidden_dbg, G, prefix_len, ws, ws_bytes, stream);
+  return rollout(m, kv, n_seqs, max_len, B, seq_ids, pos, tok, max_pos, step0, n_steps, s,
+                 tok_out, logp_out, trace, G, prefix_len, ws, ws_bytes, stream);
 }
 
 int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, int32_t T,
-                         int32_t score_from, float temperature, float* logp_out, void* ws,
-                         size_t ws_bytes, void* stream) {
+                         int32_t score_from, float temperature, float* logp_out,
+                         const grpo_trace* trace_out, void* ws, size_t ws_bytes, void* stream) {
   if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
   const grpo_config& c = m->cfg;
   if (!tokens || !logp_out || !ws) return fail(GRPO_INVALID_ARG, "tokens, logp_out and ws must be set");
@@ -869,7 +963,8 @@ int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, 
     const int32_t* tk = tokens + (size_t)n0 * T;
     HIPCHK(embed(c.dtype, m->tok_emb, tk, M, d, c.vocab, w.s.x, st));
     if (int rc = forward_rows(m, w.s, M, T, 1, C, T, nullptr, w.kbuf,
-                              c.dtype == GRPO_F32 ? w.vbuf : nullptr, w.vt, nullptr, st))
+                              c.dtype == GRPO_F32 ? w.vbuf : nullptr, w.vt, trace_out,
+                              (size_t)N * T, TraceMap::rows(n0 * T), st))
       return rc;
     const int R = C * Ts;
     for (int i0 = 0; i0 < R; i0 += w.sub_rows) {
@@ -878,6 +973,9 @@ int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, 
                      rc_rows, d, c.rms_eps, w.hs, d, st));
       if (int rc = gemm_rows(m, w.hs, d, rc_rows, one(m->lm_head), c.vocab, d, EPI_STORE,
                              EpiArgs{w.logits, nullptr, c.vocab}, st))
+        return rc;
+      if (int rc = score_head_trace(c, trace_out, (size_t)N * Ts, w.hs, w.logits, rc_rows,
+                                    n0 * Ts + i0, st))
         return rc;
       HIPCHK(token_logprob(w.logits, rc_rows, c.vocab, c.vocab, tk, T, score_from, Ts, i0,
                            temperature, logp_out + (size_t)n0 * Ts + i0, st));
@@ -889,8 +987,8 @@ int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, 
 
 int grpo_score_sequences_grouped(const grpo_model* m, const int32_t* tokens, int32_t N,
                                  int32_t T, int32_t score_from, float temperature, int32_t G,
-                                 int32_t prefix_len, float* logp_out, void* ws, size_t ws_bytes,
-                                 void* stream) {
+                                 int32_t prefix_len, float* logp_out, const grpo_trace* trace_out,
+                                 void* ws, size_t ws_bytes, void* stream) {
   if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
   if (G < 1 || N < 1 || N % G) return fail(GRPO_INVALID_ARG, "G %d must be >= 1 and divide N %d", G, N);
   if (prefix_len < 0 || prefix_len > score_from)
@@ -902,8 +1000,8 @@ int grpo_score_sequences_grouped(const grpo_model* m, const int32_t* tokens, int
   const int chunk_seqs = std::max(1, std::min(N, kScoreTokens / std::max(T, 1)));
   const int C = chunk_seqs / G * G;
   if (c.dtype == GRPO_F32 || G == 1 || P0 == 0 || C == 0 || score_from < 1 || score_from >= T)
-    return grpo_score_sequences(m, tokens, N, T, score_from, temperature, logp_out, ws, ws_bytes,
-                                stream);
+    return grpo_score_sequences(m, tokens, N, T, score_from, temperature, logp_out, trace_out,
+                                ws, ws_bytes, stream);
   if (!tokens || !logp_out || !ws) return fail(GRPO_INVALID_ARG, "tokens, logp_out and ws must be set");
   if (!(temperature >= 0.f) || temperature == INFINITY)
     return fail(GRPO_INVALID_ARG, "temperature must be finite and >= 0");
@@ -934,9 +1032,23 @@ int grpo_score_sequences_grouped(const grpo_model* m, const int32_t* tokens, int
     char* q1 = (char*)w.s.q + (size_t)M1 * qd * es;
     char* o1 = (char*)w.s.o + (size_t)M1 * qd * es;
     int rc;
+    // trace rows: each shared row to all G members' rows, own rows from P0
+    const size_t RT = (size_t)N * T;
+    const TraceMap tm_shared{prefix_len, G * T, n0 * T, G, T};
+    const TraceMap tm_own{Tb, T, n0 * T + P0, 1, 0};
+    auto tr2 = [&](float* member, int l, int width, const void* src, int layout, int ld,
+                   int ebytes) -> int {
+      if (int r = trace(member, l, RT, width, src, layout, ld, M1, tm_shared, st)) return r;
+      return trace(member, l, RT, width, (const char*)src + (size_t)M1 * ld * ebytes, layout, ld,
+                   Cc * Tb, tm_own, st);
+    };
+    const int act = c.dtype == GRPO_F32 ? TR_F32 : TR_BF16;
     for (int l = 0; l < c.n_layers; ++l) {
       HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), none, m->attn_norm[l], M, d,
                      c.rms_eps, w.s.h, d, st));
+      if ((rc = tr2(TRM(trace_out, x), l, d, w.s.x, TR_F32, d, 4)) ||
+          (rc = tr2(TRM(trace_out, h_attn), l, d, w.s.h, act, d, es)))
+        return rc;
       if ((rc = gemm_rows(m, w.s.h, d, M, qkv_stack(m, l), ldqkv, d, EPI_STORE,
                           EpiArgs{w.s.qkv, nullptr, ldqkv}, st)))
         return rc;
@@ -947,26 +1059,39 @@ int grpo_score_sequences_grouped(const grpo_model* m, const int32_t* tokens, int
       ra.kcache = w.kbuf; ra.vcache = nullptr; ra.n_seqs = Cc; ra.max_len = T;
       ra.vt = w.vt; ra.vt_len = round8(T); ra.vt_G = G;
       ra.splits = 1; ra.split_stride = 0; ra.cs = w.s.cs; ra.pos0 = 0;
+      if (trace_out) {
+        const grpo_trace* t = trace_out;
+        ra.tq = t->q ? t->q + (size_t)l * RT * qd : nullptr;
+        ra.tk = t->k ? t->k + (size_t)l * RT * kvd : nullptr;
+        ra.tv = t->v ? t->v + (size_t)l * RT * kvd : nullptr;
+        ra.tmap = tm_shared;
+      }
       HIPCHK(rope_kv(c.dtype, w.s.qkv, M1, w.s.q, ra, st));
       RopeArgs rb = ra;
-      rb.T = Tb; rb.G = 1; rb.vt_G = 1; rb.pos0 = P0;
+      rb.T = Tb; rb.G = 1; rb.vt_G = 1; rb.pos0 = P0; rb.tmap = tm_own;
       HIPCHK(rope_kv(c.dtype, w.s.qkv + (size_t)M1 * ldqkv, Cc * Tb, q1, rb, st));
       HIPCHK(attn_prefill(c.dtype, w.s.q, w.kbuf, w.vt, Pc, prefix_len, c.n_heads, c.n_kv_heads,
                           c.head_dim, T, G, w.s.o, st, 0, G, round8(T)));
       HIPCHK(attn_prefill(c.dtype, q1, w.kbuf, w.vt, Cc, Tb, c.n_heads, c.n_kv_heads,
                           c.head_dim, T, 1, o1, st, P0, 1, round8(T)));
+      if ((rc = tr2(TRM(trace_out, o), l, qd, w.s.o, act, qd, es))) return rc;
       if ((rc = gemm_rows(m, w.s.o, qd, M, one(m->wo[l]), d, qd, EPI_RESID,
                           EpiArgs{w.s.x, nullptr, d}, st)))
         return rc;
       HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), none, m->mlp_norm[l], M, d,
                      c.rms_eps, w.s.h, d, st));
+      if ((rc = tr2(TRM(trace_out, x_attn), l, d, w.s.x, TR_F32, d, 4)) ||
+          (rc = tr2(TRM(trace_out, h_mlp), l, d, w.s.h, act, d, es)))
+        return rc;
       if ((rc = gemm_rows(m, w.s.h, d, M, gate_up(m, l), f, d, EPI_SWIGLU,
                           EpiArgs{nullptr, w.s.a, f}, st)))
         return rc;
+      if ((rc = tr2(TRM(trace_out, act), l, f, w.s.a, act, f, es))) return rc;
       if ((rc = gemm_rows(m, w.s.a, f, M, one(m->w_down[l]), d, f, EPI_RESID,
                           EpiArgs{w.s.x, nullptr, d}, st)))
         return rc;
     }
+    if ((rc = tr2(TRM(trace_out, x), c.n_layers, d, w.s.x, TR_F32, d, 4))) return rc;
     // logits of positions score_from - 1 .. T - 2: own rows of each sequence
     const int R = Cc * Ts;
     for (int i0 = 0; i0 < R; i0 += w.sub_rows) {
@@ -975,6 +1100,9 @@ int grpo_score_sequences_grouped(const grpo_model* m, const int32_t* tokens, int
                      m->final_norm, rc_rows, d, c.rms_eps, w.hs, d, st));
       if ((rc = gemm_rows(m, w.hs, d, rc_rows, one(m->lm_head), c.vocab, d, EPI_STORE,
                           EpiArgs{w.logits, nullptr, c.vocab}, st)))
+        return rc;
+      if ((rc = score_head_trace(c, trace_out, (size_t)N * Ts, w.hs, w.logits, rc_rows,
+                                 n0 * Ts + i0, st)))
         return rc;
       HIPCHK(token_logprob(w.logits, rc_rows, c.vocab, c.vocab, tk, T, score_from, Ts, i0,
                            temperature, logp_out + (size_t)n0 * Ts + i0, st));

@@ -299,14 +299,15 @@ hipError_t launch_flash(int gq, dim3 grid, hipStream_t st, const bf16_t* q, cons
 __global__ __launch_bounds__(256) void k_attn_rows_f32(const float* __restrict__ q, int ldq,
                                                        const float* __restrict__ kc,
                                                        const float* __restrict__ vc,
-                                                       const int32_t* pos_arr, int T, int slot_mul,
+                                                       const int32_t* pos_arr,
+                                                       const int32_t* slots, int T, int slot_mul,
                                                        int H, int n_kv, int hd, int k_len,
                                                        float scale, float* __restrict__ out) {
   extern __shared__ float sc[];
   __shared__ float sh[4];
   const int m = blockIdx.x, h = blockIdx.y;
   int seq, p;
-  if (pos_arr) { seq = m; p = pos_arr[m]; }
+  if (pos_arr) { seq = slots ? slots[m] : m; p = pos_arr[m]; }
   else { seq = m / T; p = m % T; }
   p = min(p, k_len - 1);
   const int ctx = p + 1;
@@ -341,13 +342,13 @@ __global__ __launch_bounds__(256) void k_attn_rows_f32(const float* __restrict__
 }  // namespace
 
 hipError_t attn_rows_f32(const float* q, const float* kc, const float* vc, const int32_t* pos,
-                         int rows, int T, int slot_mul, int H, int n_kv, int hd, int k_len,
+                         const int32_t* slots, int rows, int T, int slot_mul, int H, int n_kv, int hd, int k_len,
                          float* out, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   const float scale = 1.f / sqrtf((float)hd);
   dim3 grid(rows, H);
   Prof pf("attn_f32", st);
-  k_attn_rows_f32<<<grid, 256, k_len * sizeof(float), st>>>(q, H * hd, kc, vc, pos, T, slot_mul,
+  k_attn_rows_f32<<<grid, 256, k_len * sizeof(float), st>>>(q, H * hd, kc, vc, pos, slots, T, slot_mul,
                                                             H, n_kv, hd, k_len, scale, out);
   return hipGetLastError();
 }
@@ -366,7 +367,8 @@ hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_o
     dim3 grid(N * T, H);
     Prof pf("attn_f32", st);
     k_attn_rows_f32<<<grid, 256, T * sizeof(float), st>>>(
-        (const float*)q, H * hd, (const float*)k, (const float*)v_or_vt, nullptr, T, k_seq_stride,
+        (const float*)q, H * hd, (const float*)k, (const float*)v_or_vt, nullptr, nullptr, T,
+        k_seq_stride,
         H, n_kv, hd, k_len, scale, (float*)out);
     return hipGetLastError();
   }

@@ -69,9 +69,10 @@ struct KVTile {
 template <int HD, int MAXG>
 __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
-    const int32_t* __restrict__ pos, int H, int n_kv, int max_len, int S, int span, float scale,
-    float* __restrict__ part_o, float* __restrict__ part_ml, bf16_t* __restrict__ out,
-    int pack_nb, DecodeGroup ga, int split_base) {
+    const int32_t* __restrict__ pos, const int32_t* __restrict__ slots, int H, int n_kv,
+    int max_len, int S, int span, float scale, float* __restrict__ part_o,
+    float* __restrict__ part_ml, bf16_t* __restrict__ out, int pack_nb, DecodeGroup ga,
+    int split_base) {
   constexpr int QSTEPS = HD / 32;     // MFMA k-steps over the head dim
   constexpr int LPT = HD / 8;         // lanes per position in P.V
   constexpr int PPW = 64 / LPT;       // positions per V load instruction
@@ -99,7 +100,8 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   const int t1 = min(t0 + span, ctx);
   const int ntiles = t1 > t0 ? (t1 - t0 + DT - 1) / DT : 0;
   const int nmine = ntiles > wave ? (ntiles - wave + 3) / 4 : 0;
-  const size_t head_base = ((size_t)src * n_kv + g) * max_len;
+  const int slot = slots ? slots[src] : src;          // the row's cache slot
+  const size_t head_base = ((size_t)slot * n_kv + g) * max_len;
   const bf16_t* kb = kc + head_base * HD;
   const bf16_t* vb = vc + head_base * HD;
 
@@ -325,8 +327,9 @@ __device__ __forceinline__ int vstage_swz(int r) { return ((r >> 3) & 3) << 1; }
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
-    const int32_t* __restrict__ pos, int H, int n_kv, int max_len, int S, int span, float scale,
-    float* __restrict__ part_o, float* __restrict__ part_ml, DecodeGroup ga) {
+    const int32_t* __restrict__ pos, const int32_t* __restrict__ slots, int H, int n_kv,
+    int max_len, int S, int span, float scale, float* __restrict__ part_o,
+    float* __restrict__ part_ml, DecodeGroup ga) {
   constexpr int QSTEPS = HD / 32;
   constexpr int HB = HD / 16;         // 16-row head-dim blocks of O^T
   constexpr int HBW = HB / 4;         // blocks per wave
@@ -352,8 +355,8 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
   const int t1 = min(t0 + span, group_shared(pos, group, ga, max_len));
   if (t0 >= t1) return;                       // the whole workgroup
   const int ntiles = (t1 - t0 + DT - 1) / DT;
-  const int src = group * ga.G;               // the group leader's cache rows
-  const size_t head_base = ((size_t)src * n_kv + g) * max_len;
+  const int src = group * ga.G;               // the group leader's batch row
+  const size_t head_base = ((size_t)(slots ? slots[src] : src) * n_kv + g) * max_len;
   const bf16_t* kb = kc + head_base * HD;
   const bf16_t* vb = vc + head_base * HD;
 
@@ -593,17 +596,18 @@ size_t decode_attn_part_floats_max(int B, int H, int n_kv, int hd, int max_len) 
 
 template <int HD, int MAXG>
 static void launch_decode(dim3 grid, hipStream_t st, const void* q, const void* kc,
-                          const void* vc, const int32_t* pos, int H, int n_kv, int max_len, int S,
-                          int span, float scale, float* part_o, float* part_ml, void* out,
-                          int pack_nb, DecodeGroup ga, int split_base) {
+                          const void* vc, const int32_t* pos, const int32_t* slots, int H,
+                          int n_kv, int max_len, int S, int span, float scale, float* part_o,
+                          float* part_ml, void* out, int pack_nb, DecodeGroup ga,
+                          int split_base) {
   k_attn_decode_bf16<HD, MAXG><<<grid, 256, 0, st>>>(
-      (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, H, n_kv, max_len, S, span,
-      scale, part_o, part_ml, (bf16_t*)out, pack_nb, ga, split_base);
+      (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, slots, H, n_kv, max_len, S,
+      span, scale, part_o, part_ml, (bf16_t*)out, pack_nb, ga, split_base);
 }
 
 template <int HD>
 static hipError_t attn_decode_hd(const void* q, const void* kc, const void* vc,
-                                 const int32_t* pos, int B, int H, int n_kv, int max_len,
+                                 const int32_t* pos, const int32_t* slots, int B, int H, int n_kv, int max_len,
                                  const DecodeAttnPlan& p, float* part, void* out, hipStream_t st,
                                  int pack_nb) {
   const float scale = 1.f / sqrtf((float)HD);
@@ -617,18 +621,18 @@ static hipError_t attn_decode_hd(const void* q, const void* kc, const void* vc,
     Prof pf("attn_prefix", st);
     dim3 grid(p.chunks, n_kv, B / p.G * p.n_sub);
     k_attn_prefix_bf16<HD><<<grid, 256, 0, st>>>(
-        (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, H, n_kv, max_len, S,
+        (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, slots, H, n_kv, max_len, S,
         p.span_p, scale, part_o, part_ml, ga);
   }
   {
     Prof pf("attn_decode", st);
     dim3 grid(p.splits, n_kv, B);
     if (gq <= 4)
-      launch_decode<HD, 4>(grid, st, q, kc, vc, pos, H, n_kv, max_len, S, p.tc, scale,
-                                  part_o, part_ml, out, pack_nb, ga, p.chunks);
+      launch_decode<HD, 4>(grid, st, q, kc, vc, pos, slots, H, n_kv, max_len, S, p.tc, scale,
+                           part_o, part_ml, out, pack_nb, ga, p.chunks);
     else
-      launch_decode<HD, 8>(grid, st, q, kc, vc, pos, H, n_kv, max_len, S, p.tc, scale,
-                                  part_o, part_ml, out, pack_nb, ga, p.chunks);
+      launch_decode<HD, 8>(grid, st, q, kc, vc, pos, slots, H, n_kv, max_len, S, p.tc, scale,
+                           part_o, part_ml, out, pack_nb, ga, p.chunks);
   }
   // grouped with one span of generated positions: merged by the per-row kernel
   if (S > 1 && !(grouped && p.splits == 1)) {
@@ -640,22 +644,24 @@ static hipError_t attn_decode_hd(const void* q, const void* kc, const void* vc,
 }
 
 hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
-                       const int32_t* pos, int B, int H, int n_kv, int hd, int n_seqs, int max_len,
+                       const int32_t* pos, const int32_t* slots, int B, int H, int n_kv, int hd, int n_seqs, int max_len,
                        const DecodeAttnPlan& p, float* part, void* out, hipStream_t st,
                        int pack_nb) {
   (void)n_seqs;
   if (B <= 0) return hipSuccess;
   if (pack_nb && (dtype == 0 || B > pack_nb || pack_nb % 16)) return hipErrorInvalidValue;
   if (dtype == 0)
-    return attn_rows_f32((const float*)q, (const float*)kc, (const float*)vc, pos, B, 1, 1, H,
-                         n_kv, hd, max_len, (float*)out, st);
+    return attn_rows_f32((const float*)q, (const float*)kc, (const float*)vc, pos, slots, B, 1, 1,
+                         H, n_kv, hd, max_len, (float*)out, st);
   if (H % n_kv || H / n_kv > 8 || (hd != 64 && hd != 128)) return hipErrorInvalidValue;
   if (p.G > 0 && (B % p.G || p.chunks < 1 || p.chunks > MAX_CHUNKS || p.n_sub < 1 ||
                   (long)p.n_sub * (32 / (H / n_kv)) < p.G || p.prefix_len > max_len ||
                   (long)p.chunks * p.span_p < p.prefix_len))
     return hipErrorInvalidValue;
-  return hd == 128 ? attn_decode_hd<128>(q, kc, vc, pos, B, H, n_kv, max_len, p, part, out, st, pack_nb)
-                   : attn_decode_hd<64>(q, kc, vc, pos, B, H, n_kv, max_len, p, part, out, st, pack_nb);
+  return hd == 128 ? attn_decode_hd<128>(q, kc, vc, pos, slots, B, H, n_kv, max_len, p, part, out,
+                                         st, pack_nb)
+                   : attn_decode_hd<64>(q, kc, vc, pos, slots, B, H, n_kv, max_len, p, part, out,
+                                        st, pack_nb);
 }
 
 }  // namespace grpo

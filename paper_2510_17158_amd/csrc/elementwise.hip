@@ -160,6 +160,22 @@ __global__ void k_rope_kv(const float* qkv, int M, T* q_out, RopeArgs a) {
     const float h2 = hi * c + lo * s;
     lo = l2; hi = h2;
   }
+  if (a.tq || a.tk || a.tv) {
+    // trace: the values as stored, fp32 rows at tmap(m) (and its copies)
+    const bool is_q = h < a.n_heads, is_k = !is_q && h < a.n_heads + a.n_kv;
+    float* tb = is_q ? a.tq : (is_k ? a.tk : a.tv);
+    const int width = (is_q ? a.n_heads : a.n_kv) * a.hd;
+    const int col = (is_q ? h : (is_k ? h - a.n_heads : h - a.n_heads - a.n_kv)) * a.hd;
+    if (tb) {
+      const TraceMap& tm = a.tmap;
+      const size_t r0 = (size_t)(m / tm.per) * tm.stride + tm.off + m % tm.per;
+      for (int r = 0; r < tm.dup; ++r) {
+        float* d = tb + (r0 + (size_t)r * tm.dup_stride) * width + col;
+        d[i] = rnd<T>(lo);
+        d[i + half] = rnd<T>(hi);
+      }
+    }
+  }
   if (h < a.n_heads) {
     T* qo = q_out + (size_t)m * a.n_heads * a.hd + h * a.hd;
     stf(qo, i, lo);
@@ -170,9 +186,11 @@ __global__ void k_rope_kv(const float* qkv, int M, T* q_out, RopeArgs a) {
   const bool is_v = h >= a.n_heads + a.n_kv;
   const int g = is_v ? h - a.n_heads - a.n_kv : h - a.n_heads;
   T* base = (T*)(is_v ? a.vcache : a.kcache);
+  // mode 0 with a slot map: the row's own cache slot; else slots seq*G .. seq*G+G-1
+  const int slot0 = (a.mode == 0 && a.slots) ? a.slots[m] : seq * a.G;
   for (int r = 0; base && r < a.G; ++r) {
-    const int slot = seq * a.G + r;
-    if (slot >= a.n_seqs) break;
+    const int slot = slot0 + r;
+    if (slot < 0 || slot >= a.n_seqs) break;
     T* dst = base + (((size_t)slot * a.n_kv + g) * a.max_len + pos) * a.hd;
     stf(dst, i, lo);
     stf(dst, i + half, hi);
@@ -227,6 +245,28 @@ __global__ __launch_bounds__(256) void k_v_transpose(const float* qkv, int T, Ro
       if (t < a.vt_len) dst[(size_t)d * a.vt_len + t] = p0 + p < T ? f2bf(tile[p][d]) : 0;
     }
   }
+}
+
+// Trace copy (debug path): element (m, i) of a source laid out as `layout`
+// into fp32 row map(m) of dst; one thread per element.
+__global__ void k_trace_rows(const void* src, int layout, int ld, int M, int width, TraceMap tm,
+                             float* dst) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (size_t)M * width) return;
+  const int m = (int)(idx / width), i = (int)(idx % width);
+  float v;
+  if (layout == TR_F32) v = ((const float*)src)[(size_t)m * ld + i];
+  else if (layout == TR_BF16) v = bf2f(((const bf16_t*)src)[(size_t)m * ld + i]);
+  else v = bf2f(((const bf16_t*)src)[act_frag_index(m, i, ld)]);
+  const size_t r0 = (size_t)(m / tm.per) * tm.stride + tm.off + m % tm.per;
+  for (int r = 0; r < tm.dup; ++r) dst[(r0 + (size_t)r * tm.dup_stride) * width + i] = v;
+}
+
+struct I32Block {
+  int32_t v[128];
+};
+__global__ void k_set_i32(int32_t* dst, I32Block b, int n) {
+  if ((int)threadIdx.x < n) dst[threadIdx.x] = b.v[threadIdx.x];
 }
 
 __global__ void k_fill_i32(int32_t* p, size_t n, int32_t v) {
@@ -286,6 +326,30 @@ hipError_t fill_i32(int32_t* p, size_t n, int32_t v, hipStream_t st) {
   if (n == 0) return hipSuccess;
   Prof pf("fill", st);
   k_fill_i32<<<(int)((n + 255) / 256), 256, 0, st>>>(p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t set_i32(int32_t* dst, const int32_t* host_vals, int n, hipStream_t st) {
+  for (int i0 = 0; i0 < n; i0 += 128) {
+    const int k = n - i0 < 128 ? n - i0 : 128;
+    I32Block b{};
+    for (int i = 0; i < k; ++i) b.v[i] = host_vals[i0 + i];
+    Prof pf("set", st);
+    k_set_i32<<<1, 128, 0, st>>>(dst + i0, b, k);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t trace_rows(const void* src, int layout, int ld, int M, int width, TraceMap map,
+                      float* dst, hipStream_t st) {
+  const size_t n = (size_t)M * width;
+  if (n == 0 || !dst) return hipSuccess;
+  if (map.per <= 0 || map.dup < 1 || (layout == TR_FRAG && (ld % 16 || width % 32 || M > ld)))
+    return hipErrorInvalidValue;
+  Prof pf("trace", st);
+  k_trace_rows<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(src, layout, ld, M, width, map, dst);
   return hipGetLastError();
 }
 

@@ -95,6 +95,22 @@ struct Partials {
 hipError_t rmsnorm(int dtype, float* x, int ldx, RowMap rows, Partials p, const void* g, int M,
                    int d, float eps, void* out, int ldo, hipStream_t st, int pack_nb = 0);
 hipError_t fill_i32(int32_t* p, size_t n, int32_t v, hipStream_t st);
+// dst[i] = vals[i] for i < n (host values passed as launch arguments, 128 per launch)
+hipError_t set_i32(int32_t* dst, const int32_t* host_vals, int n, hipStream_t st);
+
+// Destination row of a traced row m (and copy r < dup of it):
+// (m / per) * stride + off + m % per + r * dup_stride.
+struct TraceMap {
+  int per, stride, off, dup, dup_stride;
+  static TraceMap rows(int off = 0) { return TraceMap{0x7fffffff, 0, off, 1, 0}; }
+};
+// Trace copy: dst[map(m) * width + i] = element (m, i) of src as fp32, for
+// m < M, i < width.  src layout: TR_F32 fp32 row-major (row stride ld),
+// TR_BF16 bf16 row-major (ld), TR_FRAG bf16 in decode-GEMM fragment order
+// [width/32][ld/16][64][8] (ld = the padded batch).
+enum TraceSrc { TR_F32 = 0, TR_BF16 = 1, TR_FRAG = 2 };
+hipError_t trace_rows(const void* src, int layout, int ld, int M, int width, TraceMap map,
+                      float* dst, hipStream_t st);
 // cos / sin table of the rotary angles, [rows][hd / 2] float2: row r is position
 // pos_arr[r] (device array) or, with pos_arr NULL, position r.
 hipError_t rope_table(const int32_t* pos_arr, int rows, int hd, float theta, float2* cs,
@@ -110,6 +126,7 @@ hipError_t rope_table(const int32_t* pos_arr, int rows, int hd, float theta, flo
 struct RopeArgs {
   int mode, T, G;
   const int32_t* pos_arr;
+  const int32_t* slots;         // mode 0: cache slot of row m (NULL: m)
   int n_heads, n_kv, hd;
   float theta;
   void* kcache; void* vcache;   // layer base of K and V: [n_seqs][n_kv][max_len][hd]; V may be NULL
@@ -119,13 +136,16 @@ struct RopeArgs {
   const float2* cs;
   int pos0;    // mode 1: position of each sequence's first row (0: rows start at 0)
   int vt_G;    // V^T written to vt_G consecutive sequence slots per sequence (0 or 1: one)
+  // trace (each optional): q [.][q_dim], k and v [.][kv_dim] fp32 rows at tmap(m)
+  float* tq; float* tk; float* tv;
+  TraceMap tmap;
 };
 hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeArgs& a,
                    hipStream_t st);
 
 // ---- attention -------------------------------------------------------------------
 // Decode: q act [B, H, hd]; cache layer base K/V [n_seqs][n_kv][max_len][hd];
-// attends positions 0..pos[b].  out act [B, H*hd] row-major, or (pack_nb > 0) in
+// row b reads cache slot slots[b] (NULL: b) and attends positions 0..pos[b].  out act [B, H*hd] row-major, or (pack_nb > 0) in
 // decode-GEMM fragment order [pack_nb][H*hd].
 // tc: context positions per span (a multiple of 128); splits: spans per (sequence,
 // kv head); part_floats: fp32 scratch for the span merge (0 with a single span).
@@ -143,14 +163,14 @@ DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len, int
 // partial floats of any plan for these shapes, grouped or not
 size_t decode_attn_part_floats_max(int B, int H, int n_kv, int hd, int max_len);
 hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
-                       const int32_t* pos, int B, int H, int n_kv, int hd, int n_seqs, int max_len,
+                       const int32_t* pos, const int32_t* slots, int B, int H, int n_kv, int hd, int n_seqs, int max_len,
                        const DecodeAttnPlan& p, float* part, void* out, hipStream_t st,
                        int pack_nb = 0);
 // fp32 attention rows (decode rows when pos != NULL: row m is sequence m at
 // position pos[m]; else row m is position m % T of sequence m / T at cache slot
 // (m / T) * slot_mul); k_len positions of cache per sequence and kv head.
 hipError_t attn_rows_f32(const float* q, const float* kc, const float* vc, const int32_t* pos,
-                         int rows, int T, int slot_mul, int H, int n_kv, int hd, int k_len,
+                         const int32_t* slots, int rows, int T, int slot_mul, int H, int n_kv, int hd, int k_len,
                          float* out, hipStream_t st);
 // Causal attention over N sequences of T rows: q act [N*T, H*hd]; K in cache
 // layout [n][n_kv][k_len][hd] (sequence n at slot n*k_stride_seq), Vt
@@ -164,8 +184,9 @@ hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_o
                         int vt_len = 0);
 
 // ---- sampling / log-probs ---------------------------------------------------------
-// logits fp32 [R, V] (row stride ld).  Row r makes G draws; draw g uses Philox
-// sequence id q = r*G + g and writes tok_out[q*out_stride], logp_out[q*out_stride].
+// logits fp32 [R, V] (row stride ld).  Row r makes G draws; draw g writes
+// tok_out[q*out_stride], logp_out[q*out_stride] for q = r*G + g and uses Philox
+// sequence id seq_ids[q] (NULL: q).
 struct SampleArgs {
   float temperature; int top_k; uint64_t seed;
   int step;               // Philox step word
@@ -175,6 +196,7 @@ struct SampleArgs {
   int32_t* tok_state;     // optional [R*G]: also store token here
   int32_t* pos_state;     // optional [R*G]: pos += 1
   const int32_t* step_ctr;  // optional: Philox step = step + *step_ctr, outputs at column *step_ctr
+  const int32_t* seq_ids;   // optional [R*G]: Philox sequence id of draw q
 };
 hipError_t sample(const float* logits, int R, int V, int ld, const SampleArgs& a, hipStream_t st);
 // Teacher-forced log-prob of scored row m (global index gi = i0 + m over

@@ -68,6 +68,7 @@ __global__ __launch_bounds__(NT) void k_sample(const float* __restrict__ logits,
   __shared__ int s_krem, s_eq, s_cut;
   const int r = blockIdx.x, gdraw = blockIdx.y;
   const int seq = r * a.G + gdraw;
+  const int pid = a.seq_ids ? a.seq_ids[seq] : seq;   // Philox sequence id
   const int col = a.step_ctr ? *a.step_ctr : 0;
   const int step = a.step + col;
   const float* l = logits + (size_t)r * ld;
@@ -139,7 +140,7 @@ __global__ __launch_bounds__(NT) void k_sample(const float* __restrict__ logits,
     int gi = 0x7fffffff;
     const int nblk = (V + 3) / 4;
     for (int c = tid; c < nblk; c += NT) {
-      const uint4 w = philox4x32_10(make_uint4((uint32_t)c, (uint32_t)step, (uint32_t)seq, 0u),
+      const uint4 w = philox4x32_10(make_uint4((uint32_t)c, (uint32_t)step, (uint32_t)pid, 0u),
                                     k0, k1);
       const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
@@ -183,6 +184,7 @@ __global__ __launch_bounds__(NTR) void k_sample_reg(const float* __restrict__ lo
   __shared__ int s_krem, s_eq, s_cut;
   const int r = blockIdx.x, gdraw = blockIdx.y;
   const int seq = r * a.G + gdraw;
+  const int pid = a.seq_ids ? a.seq_ids[seq] : seq;   // Philox sequence id
   const int col = a.step_ctr ? *a.step_ctr : 0;
   const int step = a.step + col;
   const float* l = logits + (size_t)r * ld;
@@ -280,7 +282,7 @@ __global__ __launch_bounds__(NTR) void k_sample_reg(const float* __restrict__ lo
     for (int j = 0; j < R4; ++j) {
       const int c = tid + NTR * j;
       if (4 * c < V) {
-        const uint4 w = philox4x32_10(make_uint4((uint32_t)c, (uint32_t)step, (uint32_t)seq, 0u),
+        const uint4 w = philox4x32_10(make_uint4((uint32_t)c, (uint32_t)step, (uint32_t)pid, 0u),
                                       k0, k1);
         const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll

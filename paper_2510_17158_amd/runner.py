@@ -62,13 +62,12 @@ class GrpoIteration:
         self.stats = torch.empty(4, **f32)
 
     # --- phases -----------------------------------------------------------------------
-    def prefill(self, logits_dbg=None, hidden_dbg=None):
+    def prefill(self, trace=None):
         w = self.w
         api.prefill(self.policy, self.kv, self.B, self.max_len, self.prompts, w.group,
-                    self.sampling, self.tok0, self.logp0, logits_dbg=logits_dbg,
-                    hidden_dbg=hidden_dbg, ws=self.ws_prefill)
+                    self.sampling, self.tok0, self.logp0, trace=trace, ws=self.ws_prefill)
 
-    def decode(self, logits_dbg=None, hidden_dbg=None):
+    def decode(self, trace=None):
         """Generation steps 1 .. new_tokens-1 for the whole batch."""
         w = self.w
         n = w.new_tokens - 1
@@ -78,7 +77,7 @@ class GrpoIteration:
         self.pos.fill_(w.prompt_len)
         api.rollout_step(self.policy, self.kv, self.B, self.max_len, self.pos, self.tok,
                          w.prompt_len, 1, n, self.sampling, self.tok_dec, self.logp_dec,
-                         logits_dbg=logits_dbg, hidden_dbg=hidden_dbg, ws=self.ws_roll,
+                         trace=trace, ws=self.ws_roll,
                          group=w.group if w.shared_prompt else 0,
                          prefix_len=w.prompt_len if w.shared_prompt else 0)
 

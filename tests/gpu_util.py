@@ -7,8 +7,17 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
+from bounds import Report
 from paper_2510_17158_amd import api, synth
 from paper_2510_17158_amd.workloads import DTYPE_F32, ModelConfig
+from stagecheck import (StageChecker, decode_segments, f32_segments, flash_segments,
+                        gemms_decode, gemms_rows, sampler_check)
+from bounds import F32_GEMM, decode_gemm, rows_gemm
+
+LOGIT_TOL = 2e-2       # bf16 logits / log-probs (stated tolerance)
+LOGIT_TOL_F32 = 1e-4   # fp32 logits / log-probs (stated tolerance)
+NEAR_TIE = 1e-5        # sampler decisions closer than this are logged, not compared
 
 
 def require_gpu():
@@ -37,114 +46,128 @@ def kv_view(cfg: ModelConfig, kv: torch.Tensor, n_seqs: int, max_len: int) -> np
     return kv.view(torch.bfloat16).view(shape).double().cpu().numpy()
 
 
-def bf16_ulps(a: np.ndarray, b: np.ndarray) -> np.ndarray:
-    """Distance in bf16 units in the last place between bf16-representable values."""
-    def key(x):
-        u = (np.asarray(x, np.float32).view(np.uint32) >> 16).astype(np.int64)
-        return np.where(u & 0x8000, -(u & 0x7FFF), u)
-    return np.abs(key(a) - key(b))
+def logit_tol(cfg) -> float:
+    return LOGIT_TOL_F32 if cfg.dtype == DTYPE_F32 else LOGIT_TOL
 
 
-BF16_ABS = 1e-5
+def head_cols(V: int, logits: np.ndarray, n: int = 4096, seed: int = 0) -> np.ndarray | None:
+    """Vocabulary columns on which the LM-head bound is evaluated: all of a small
+    vocabulary, else n random ones plus every row's largest logits."""
+    if V <= n:
+        return None
+    rng = np.random.default_rng(seed)
+    top = np.argsort(-logits, axis=1)[:, :4].ravel()
+    return np.unique(np.concatenate([rng.choice(V, n, replace=False), top]))
 
 
-def bf16_bad(gpu: np.ndarray, ref: np.ndarray) -> np.ndarray:
-    """Elements of a bf16-stored GPU output outside the contract: more than one
-    bf16 ulp from the oracle's bf16 value AND more than BF16_ABS away (near zero
-    the fp32 accumulation error alone exceeds an ulp)."""
-    return (bf16_ulps(gpu, ref) > 1) & (np.abs(np.asarray(gpu) - np.asarray(ref)) > BF16_ABS)
+# ------------------------------------------------------------- decode step
+def decode_traced(model: api.Model, kv, n_seqs, max_len, pos_host, tok_dev, step: int,
+                  sampling, ws, group: int = 0, prefix_len: int = 0, seq_ids=None):
+    """One traced decode step for the rows of pos_host (host positions, written to a
+    fresh device pos array).  Returns (trace numpy dict, tokens, log-probs)."""
+    cfg = model.cfg
+    B = len(pos_host)
+    pos = torch.from_numpy(np.asarray(pos_host, np.int32)).to("cuda")
+    tr = api.Trace(cfg, B, B)
+    to = torch.empty(B, 1, dtype=torch.int32, device="cuda")
+    lo = torch.empty(B, 1, device="cuda")
+    api.rollout_step(model, kv, n_seqs, max_len, pos, tok_dev, int(np.max(pos_host)), step, 1,
+                     sampling, to, lo, seq_ids=seq_ids, trace=tr, ws=ws, group=group,
+                     prefix_len=prefix_len)
+    torch.cuda.synchronize()
+    return tr.numpy(), to.cpu().numpy()[:, 0], lo.cpu().numpy()[:, 0]
 
 
-def ulp_bf16(r):
-    a = np.abs(np.asarray(r, np.float64))
-    e = np.floor(np.log2(np.maximum(a, 2.0 ** -126)))
-    return 2.0 ** (e - 7)
+def check_decode(cfg, host, model, tr: dict, kvnp: np.ndarray, pos, max_len: int, rows=None,
+                 group: int = 0, prefix_len: int = 0, slots=None, rep: Report | None = None):
+    """Rounding-point-local check of a traced decode step.  kvnp: the cache after
+    the step ([L, 2, n_seqs, n_kv, max_len, hd]); pos: each row's position; slots:
+    each row's cache slot (seq_ids)."""
+    pos = np.asarray(pos)
+    B = len(pos)
+    rows = np.arange(B) if rows is None else np.asarray(rows)
+    slots = np.arange(B) if slots is None else np.asarray(slots)
+    chk = StageChecker(cfg, host, rep)
+    if cfg.dtype == DTYPE_F32:
+        gem = gemms_rows(cfg, B)
+        seg = lambda i: f32_segments(int(pos[rows[i]]) + 1)   # noqa: E731
+        ghead = F32_GEMM
+    else:
+        st = api.decode_structure(model, B, max_len, group, prefix_len)
+        gem = gemms_decode(st)
+        ghead = decode_gemm(st["splits_head"])
+        grouped = group > 0 and prefix_len > 0
+
+        def seg(i):
+            b = rows[i]
+            ctx = int(pos[b]) + 1
+            base = 0
+            if grouped:
+                g0 = b // group * group
+                base = min(prefix_len, int((pos[g0:g0 + group] + 1).min()))
+            return decode_segments(ctx, st, base)
+    for l in range(cfg.n_layers):
+        def context(i, l=l):
+            b = rows[i]
+            ctx = int(pos[b]) + 1
+            K = kvnp[l, 0, slots[b], :, :ctx].transpose(1, 0, 2)
+            V = kvnp[l, 1, slots[b], :, :ctx].transpose(1, 0, 2)
+            return K, V
+        chk.layer(l, tr, rows, pos[rows], context, seg, gem)
+    cols = head_cols(cfg.vocab, tr["logits"][rows])
+    worst = chk.head(tr, rows, rows, ghead, cols=cols, logit_tol=logit_tol(cfg))
+    return chk.rep, worst
 
 
-def floor_check(gpu, ref64, refs32, bf16: bool = False, kmax: float = 3.0, kmean: float = 2.5,
-                allow=None):
-    """GPU vs the fp64 oracle, judged against the noise floor of the same rounding
-    contract: the larger elementwise distance from fp64 of the fp32 evaluations
-    in `refs32` (BLAS order and matrix-core order).  fp32 outputs: max and mean
-    within kmax / kmean of the floor.  bf16-stored outputs: every element within
-    kmax floor maxima plus one ulp, and no more than kmax times the floor's
-    fraction of differing elements (at least 2e-3).  `allow` (bf16 outputs) adds a
-    per-element allowance, e.g. the reach of rounding flips of an input that the
-    rounding contract leaves open (see h_flip_allowance)."""
-    gpu, ref64 = (np.asarray(a, np.float64) for a in (gpu, ref64))
-    if not isinstance(refs32, (list, tuple)):
-        refs32 = [refs32]
-    e = np.abs(gpu - ref64)
-    f = np.max([np.abs(np.asarray(r, np.float64) - ref64) for r in refs32], axis=0)
-    st = dict(err_max=float(e.max()), floor_max=float(f.max()), err_mean=float(e.mean()),
-              floor_mean=float(f.mean()))
-    if bf16:
-        ulp = ulp_bf16(ref64)
-        extra = 0.0 if allow is None else np.asarray(allow, np.float64)
-        bad = e > kmax * f.max() + ulp + extra
-        ok = not bool(bad.any())
-        frac, ffrac = float((e > 0).mean()), float((f > 0).mean())
-        st.update(flip_frac=frac, floor_flip_frac=ffrac)
-        if not ok:
-            idx = np.argsort(-(e - ulp))[:4]
-            st["worst"] = [dict(i=int(i), gpu=float(gpu[i]), ref=float(ref64[i]), err=float(e[i]),
-                                ulp=float(ulp[i]), floor=float(f[i])) for i in idx]
-        return ok and frac <= max(kmax * ffrac, 2e-3), st
-    slack = 1e-6 * float(np.abs(ref64).max())
-    ok = bool(e.max() <= kmax * f.max() + slack) and bool(e.mean() <= kmean * f.mean() + 1e-7)
-    return ok, st
+# ------------------------------------------------------- many-row forwards
+def check_rows(cfg, host, tr: dict, T: int, M_call: int, rows, rep: Report | None = None,
+               head=None):
+    """Rounding-point-local check of a traced prefill or scoring forward on the
+    trace rows `rows` (row = seq * T + t).  M_call: rows of the call's GEMMs.
+    head: None, or (head_rows, x_rows, M_head) for the LM-head check."""
+    rows = np.asarray(rows)
+    chk = StageChecker(cfg, host, rep)
+    gem = gemms_rows(cfg, M_call)
+    pos = rows % T
+    for l in range(cfg.n_layers):
+        seq_kv = {}
+
+        def context(i, l=l):
+            r = rows[i]
+            s0 = r - r % T
+            if s0 not in seq_kv:
+                seq_kv.clear()
+                last = int(rows[rows < s0 + T].max())      # the sequence's last checked row
+                seq_kv[s0] = (tr["k"][l][s0:last + 1].reshape(-1, cfg.n_kv_heads, cfg.head_dim),
+                              tr["v"][l][s0:last + 1].reshape(-1, cfg.n_kv_heads, cfg.head_dim))
+            K, V = seq_kv[s0]
+            return K[:r - s0 + 1], V[:r - s0 + 1]
+        segf = f32_segments if cfg.dtype == DTYPE_F32 else flash_segments
+        chk.layer(l, tr, rows, pos, context, lambda i: segf(int(pos[i]) + 1), gem)
+    worst = None
+    if head is not None:
+        hrows, xrows, M_head = head
+        g = F32_GEMM if cfg.dtype == DTYPE_F32 else rows_gemm(M_head)
+        cols = head_cols(cfg.vocab, tr["logits"][np.asarray(hrows)])
+        worst = chk.head(tr, hrows, xrows, g, cols=cols, logit_tol=logit_tol(cfg))
+    return chk.rep, worst
 
 
-class FloorPool:
-    """Pools GPU and noise-floor errors of one output kind over layers, steps and
-    sequences, then applies the floor criterion once: a single rounding flip more
-    or less in one small instance is chance, a systematic excess is not."""
-
-    def __init__(self):
-        self.g, self.r64, self.r32, self.bf, self.al = {}, {}, {}, {}, {}
-
-    def add(self, name, gpu, ref64, refs32, bf16=False, allow=None):
-        if not isinstance(refs32, (list, tuple)):
-            refs32 = [refs32]
-        a = np.zeros(np.size(gpu)) if allow is None else np.asarray(allow, np.float64).ravel()
-        self.al.setdefault(name, []).append(a)
-        self.g.setdefault(name, []).append(np.asarray(gpu, np.float64).ravel())
-        self.r64.setdefault(name, []).append(np.asarray(ref64, np.float64).ravel())
-        self.r32.setdefault(name, []).append([np.asarray(r, np.float64).ravel() for r in refs32])
-        self.bf[name] = bf16
-
-    def check(self):
-        out, ok = {}, True
-        for n in self.g:
-            refs = [np.concatenate([r[i] for r in self.r32[n]]) for i in range(len(self.r32[n][0]))]
-            o, st = floor_check(np.concatenate(self.g[n]), np.concatenate(self.r64[n]), refs,
-                                bf16=self.bf[n], allow=np.concatenate(self.al[n]))
-            out[n] = st
-            ok &= o
-        return ok, out
+def sample_rows(T: int, n_seqs: int, k: int, seed: int = 0, lo: int = 0, hi: int | None = None):
+    """Rows to check: per sequence the first and last rows, rows around 32/64-row
+    tile edges, and k random rows from [lo, hi)."""
+    hi = T if hi is None else hi
+    rng = np.random.default_rng(seed)
+    edges = [t for e in (31, 32, 63, 64, 127, 128, 255, 256, 1023, 1024, 2047, 2048, 4095)
+             for t in (e,) if lo <= t < hi]
+    out = []
+    for s in range(n_seqs):
+        r = set([lo, hi - 1] + edges)
+        r.update(rng.integers(lo, hi, k).tolist())
+        out.extend(s * T + t for t in sorted(r))
+    return np.array(sorted(out))
 
 
-def h_flip_allowance(om, cfg, l, x, rel=4e-6):
-    """Per-element reach of rounding flips of the normed attention input of layer l
-    on its K and V outputs.  h = R1(rms(x) g) is rounded to bf16; where the fp64
-    value of an element lies within `rel` (relative) of a rounding midpoint, an
-    fp32 evaluation of the norm (relative error below 1e-6 at these widths) may
-    round it either way, moving every K/V output j by up to sum_i |W[j, i]| ulp(h_i)
-    over those elements (K: also its RoPE partner dimension).
-    x: [..., d] residual fed to the layer; returns (allow_k, allow_v) [..., n_kv, hd]."""
-    import oracle
-    x = np.asarray(x, np.float64)
-    h = oracle.rmsnorm(x, om.mat(f"l{l}.attn_norm"), cfg.rms_eps)
-    r = oracle.round_bf16(h)
-    a, ar = np.abs(h), np.abs(r)
-    u = ulp_bf16(r)
-    pow2 = ar == 2.0 ** np.floor(np.log2(np.maximum(ar, 2.0 ** -126)))
-    half = np.where(a >= ar, u / 2, np.where(pow2, u / 4, u / 2))   # to the midpoint beyond h
-    near = (half - np.abs(a - ar)) <= rel * a
-    dh = np.where(near, u, 0.0)
-    hd, hk = cfg.head_dim, cfg.n_kv_heads
-    lead = x.shape[:-1]
-    ak = (dh @ np.abs(om.mat(f"l{l}.wk")).T).reshape(*lead, hk, hd)
-    ak = ak + np.roll(ak, hd // 2, axis=-1)
-    av = (dh @ np.abs(om.mat(f"l{l}.wv")).T).reshape(*lead, hk, hd)
-    return ak, av
+def assert_report(rep: Report, label: str):
+    say(label, rep.summary())
+    assert rep.ok(), rep.summary()

@@ -83,7 +83,7 @@ def test_decode_weights_size_and_errors():
     p = C.c_void_p(0x1000)
     # no decode copy yet: a bf16 rollout step is refused before any device work
     s = api.Sampling(1.0, 0, 1)
-    assert L.grpo_rollout_step(h, p, 64, 100, 64, p, p, 10, 1, 2, C.byref(s), p, p, None, None, p,
+    assert L.grpo_rollout_step(h, p, 64, 100, 64, None, p, p, 10, 1, 2, C.byref(s), p, p, None, p,
                                1 << 40, None) == api.INVALID_ARG
     assert b"decode weights" in L.grpo_last_error()
     assert L.grpo_model_pack_decode(h, None, 1 << 40, None) == api.INVALID_ARG
@@ -101,48 +101,58 @@ def test_argument_errors_before_device_work():
     rc, h, keep = _fake_model(get("small").model)
     s = api.Sampling(1.0, 0, 1)
     p = C.c_void_p(0x1000)
+    BIG = 1 << 40
+
+    def roll(n_seqs=64, B=64, max_pos=10, ids=None, ws_bytes=BIG, samp=s):
+        return L.grpo_rollout_step(h, p, n_seqs, 100, B, ids, p, p, max_pos, 1, 2, C.byref(samp),
+                                   p, p, None, p, ws_bytes, None)
     # KV capacity: max_pos + n_steps > max_len
-    r = L.grpo_rollout_step(h, p, 64, 100, 64, p, p, 99, 1, 2, C.byref(s), p, p, None, None, p,
-                            1 << 40, None)
-    assert r == api.KV_CAPACITY
+    assert roll(max_pos=99) == api.KV_CAPACITY
     # workspace too small
-    r = L.grpo_rollout_step(h, p, 64, 100, 64, p, p, 10, 1, 2, C.byref(s), p, p, None, None, p, 16,
-                            None)
-    assert r == api.WORKSPACE_TOO_SMALL
+    assert roll(ws_bytes=16) == api.WORKSPACE_TOO_SMALL
     # grouped steps: G must divide B, 0 <= prefix_len <= max_len; the per-row
     # checks still apply
-    def grouped(G, prefix, max_pos=10):
-        return L.grpo_rollout_step_grouped(h, p, 64, 100, 64, G, prefix, p, p, max_pos, 1, 2,
-                                           C.byref(s), p, p, None, None, p, 1 << 40, None)
+    def grouped(G, prefix, max_pos=10, ids=None):
+        return L.grpo_rollout_step_grouped(h, p, 64, 100, 64, G, prefix, ids, p, p, max_pos, 1, 2,
+                                           C.byref(s), p, p, None, p, BIG, None)
     assert grouped(0, 50) == api.INVALID_ARG
     assert grouped(3, 50) == api.INVALID_ARG
     assert grouped(8, 101) == api.INVALID_ARG
     assert grouped(8, -1) == api.INVALID_ARG
     assert grouped(8, 50, max_pos=99) == api.KV_CAPACITY
-    # B above n_seqs, bad temperature, bad top_k
-    assert L.grpo_rollout_step(h, p, 8, 100, 64, p, p, 10, 1, 2, C.byref(s), p, p, None, None, p,
-                               1 << 40, None) == api.INVALID_ARG
-    bad = api.Sampling(-1.0, 0, 1)
-    assert L.grpo_rollout_step(h, p, 64, 100, 64, p, p, 10, 1, 2, C.byref(bad), p, p, None, None,
-                               p, 1 << 40, None) == api.INVALID_ARG
+    # B above n_seqs or above 128 for a bf16 model, bad temperature, bad top_k
+    assert roll(n_seqs=8) == api.INVALID_ARG
+    assert roll(n_seqs=200, B=130) == api.UNSUPPORTED
+    assert roll(samp=api.Sampling(-1.0, 0, 1)) == api.INVALID_ARG
+    # seq_ids: each in [0, n_seqs), no repeats (host array, checked before any work)
+    ids = lambda v: (C.c_int32 * len(v))(*v)  # noqa: E731
+    good = list(range(63, -1, -1))
+    assert roll(ids=ids(good), ws_bytes=16) == api.WORKSPACE_TOO_SMALL   # ids accepted
+    assert roll(ids=ids(good[:-1] + [64])) == api.INVALID_ARG
+    assert b"seq_ids" in L.grpo_last_error()
+    assert roll(ids=ids(good[:-1] + [-1])) == api.INVALID_ARG
+    assert roll(ids=ids(good[:-1] + [5])) == api.INVALID_ARG
+    assert b"repeats" in L.grpo_last_error()
+    assert roll(n_seqs=100, B=4, ids=ids([99, 0, 50, 7]), ws_bytes=16) == api.WORKSPACE_TOO_SMALL
+    assert grouped(8, 50, ids=ids(good[:-1] + [70])) == api.INVALID_ARG
     bad = api.Sampling(1.0, 40000, 1)
-    assert L.grpo_prefill(h, p, 64, 100, p, 8, 10, 8, C.byref(bad), p, p, None, None, p, 1 << 40,
+    assert L.grpo_prefill(h, p, 64, 100, p, 8, 10, 8, C.byref(bad), p, p, None, p, BIG,
                           None) == api.INVALID_ARG
     # prefill: P*G > n_seqs, prompt longer than the cache
-    assert L.grpo_prefill(h, p, 8, 100, p, 8, 10, 8, C.byref(s), p, p, None, None, p, 1 << 40,
+    assert L.grpo_prefill(h, p, 8, 100, p, 8, 10, 8, C.byref(s), p, p, None, p, BIG,
                           None) == api.INVALID_ARG
-    assert L.grpo_prefill(h, p, 64, 100, p, 8, 200, 8, C.byref(s), p, p, None, None, p, 1 << 40,
+    assert L.grpo_prefill(h, p, 64, 100, p, 8, 200, 8, C.byref(s), p, p, None, p, BIG,
                           None) == api.KV_CAPACITY
     # grouped scoring: G must divide N, 0 <= prefix_len <= score_from
-    assert L.grpo_score_sequences_grouped(h, p, 8, 100, 50, 1.0, 3, 50, p, p, 1 << 40,
+    assert L.grpo_score_sequences_grouped(h, p, 8, 100, 50, 1.0, 3, 50, p, None, p, BIG,
                                           None) == api.INVALID_ARG
-    assert L.grpo_score_sequences_grouped(h, p, 8, 100, 50, 1.0, 4, 51, p, p, 1 << 40,
+    assert L.grpo_score_sequences_grouped(h, p, 8, 100, 50, 1.0, 4, 51, p, None, p, BIG,
                                           None) == api.INVALID_ARG
-    assert L.grpo_score_sequences_grouped(h, p, 8, 100, 50, 1.0, 0, 50, p, p, 1 << 40,
+    assert L.grpo_score_sequences_grouped(h, p, 8, 100, 50, 1.0, 0, 50, p, None, p, BIG,
                                           None) == api.INVALID_ARG
     # scoring range
-    assert L.grpo_score_sequences(h, p, 4, 10, 0, 1.0, p, p, 1 << 40, None) == api.INVALID_ARG
-    assert L.grpo_score_sequences(h, p, 4, 10, 10, 1.0, p, p, 1 << 40, None) == api.INVALID_ARG
+    assert L.grpo_score_sequences(h, p, 4, 10, 0, 1.0, p, None, p, BIG, None) == api.INVALID_ARG
+    assert L.grpo_score_sequences(h, p, 4, 10, 10, 1.0, p, None, p, BIG, None) == api.INVALID_ARG
     # advantages and loss
     assert L.grpo_advantages(p, 4, 1, 1e-6, p, None) == api.INVALID_ARG
     assert L.grpo_advantages(None, 4, 2, 1e-6, p, None) == api.INVALID_ARG
@@ -153,6 +163,23 @@ def test_argument_errors_before_device_work():
     assert L.grpo_token_loss(p, p, p, p, p, 4, 8, 0.2, 0.04, 0, p, None, None, None, p, 8,
                              None) == api.WORKSPACE_TOO_SMALL
     assert b"workspace" in L.grpo_last_error()
+    L.grpo_model_destroy(h)
+
+
+def test_decode_structure_query():
+    """The reduction structure the tests' error bounds use comes from the library's
+    own planner; its arguments are checked."""
+    L = api.lib()
+    rc, h, keep = _fake_model(get("7b").model)
+    out = (C.c_int32 * 8)()
+    assert L.grpo_decode_structure(h, 64, 4095, 8, 2048, out) == api.OK
+    v = list(out)
+    assert all(x >= 1 for x in v[:6]) and v[3] == 1       # the LM head is never split
+    assert v[6] > 0 and v[7] >= 1 and v[6] * v[7] >= 2048
+    assert L.grpo_decode_structure(h, 64, 4095, 0, 0, out) == api.OK and list(out)[6:] == [0, 0]
+    assert L.grpo_decode_structure(h, 129, 4095, 0, 0, out) == api.INVALID_ARG
+    assert L.grpo_decode_structure(h, 64, 4095, 3, 100, out) == api.INVALID_ARG
+    assert L.grpo_decode_structure(None, 64, 4095, 0, 0, out) == api.INVALID_ARG
     L.grpo_model_destroy(h)
 
 
