@@ -304,6 +304,21 @@ int grpo_token_loss(const float* logp, const float* logp_old, const float* logp_
                     float beta, int32_t agg, float* loss_out, float* tok_loss, float* dloss_dlogp,
                     float* stats, void* ws, size_t ws_bytes, void* stream);
 
+/* grpo_token_loss for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops, harnesses that forbid hipMalloc): the same
+ * kernels and results, with the per-sequence scratch in a static device array
+ * of the library (one per GPU, GRPO_LOSS_STATIC_ROWS sequences x 72 bytes =
+ * 1.2 MB, held until the process ends) instead of a workspace argument.  The
+ * call allocates nothing.  All calls on one GPU share that array: calls that
+ * overlap on one GPU (different streams or threads without ordering) race and
+ * must be serialised by the caller.  Arguments and outputs as grpo_token_loss;
+ * GRPO_INVALID_ARG for N above GRPO_LOSS_STATIC_ROWS. */
+#define GRPO_LOSS_STATIC_ROWS 16384
+int grpo_token_loss_noalloc(const float* logp, const float* logp_old, const float* logp_ref,
+                            const uint8_t* mask, const float* adv, int32_t N, int32_t Tr,
+                            float clip_eps, float beta, int32_t agg, float* loss_out,
+                            float* tok_loss, float* dloss_dlogp, float* stats, void* stream);
+
 /* Reduction structure of a decode step, for error analysis of its results
  * (the order in which partial sums meet decides the rounding).  For a model, a
  * batch of B rows, a KV capacity max_len and a grouping (G, prefix_len as

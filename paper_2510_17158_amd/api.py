@@ -136,6 +136,8 @@ _SIGS = {
     "grpo_token_loss": (_I32, [_VP, _VP, _VP, _VP, _VP, _I32, _I32, _F32, _F32, _I32, _VP, _VP,
                                _VP, _VP, _VP, _SZ, _VP]),
     "grpo_decode_structure": (_I32, [_VP, _I32, _I32, _I32, _I32, _IP]),
+    "grpo_token_loss_noalloc": (_I32, [_VP, _VP, _VP, _VP, _VP, _I32, _I32, _F32, _F32, _I32, _VP,
+                                       _VP, _VP, _VP, _VP]),
     "grpo_profile_begin": (_I32, []),
     "grpo_profile_end": (_I32, [C.c_char_p, _SZ]),
 }
@@ -341,6 +343,17 @@ def decode_structure(model: Model, B: int, max_len: int, G: int = 0, prefix_len:
     v = list(out)
     return dict(splits_qkv=v[0], splits_o=v[1], splits_down=v[2], splits_head=v[3], span=v[4],
                 spans=v[5], chunk=v[6], chunks=v[7])
+
+
+def token_loss_noalloc(logp, logp_old, logp_ref, mask, adv, clip_eps: float, beta: float,
+                       agg: int, loss_out, tok_loss=None, dloss_dlogp=None, stats=None,
+                       stream=None):
+    """grpo_token_loss_noalloc: grpo_token_loss with the library's static scratch."""
+    N, Tr = logp.shape
+    _check(lib().grpo_token_loss_noalloc(_ptr(logp), _ptr(logp_old), _ptr(logp_ref), _ptr(mask),
+                                         _ptr(adv), N, Tr, clip_eps, beta, agg, _ptr(loss_out),
+                                         _ptr(tok_loss), _ptr(dloss_dlogp), _ptr(stats),
+                                         _stream(stream)))
 
 
 def profile_begin():

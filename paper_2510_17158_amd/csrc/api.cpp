@@ -1143,3 +1143,27 @@ int grpo_token_loss(const float* logp, const float* logp_old, const float* logp_
 }
 
 }  // extern "C"
+
+static_assert(GRPO_LOSS_STATIC_ROWS == kLossStaticRows, "static loss scratch size");
+
+extern "C" int grpo_token_loss_noalloc(const float* logp, const float* logp_old,
+                                       const float* logp_ref, const uint8_t* mask,
+                                       const float* adv, int32_t N, int32_t Tr, float clip_eps,
+                                       float beta, int32_t agg, float* loss_out, float* tok_loss,
+                                       float* dloss_dlogp, float* stats, void* stream) {
+  if (!logp || !logp_old || !logp_ref || !mask || !adv || !loss_out)
+    return fail(GRPO_INVALID_ARG, "logp, logp_old, logp_ref, mask, adv and loss_out must be set");
+  if (N < 1 || Tr < 1) return fail(GRPO_INVALID_ARG, "N and Tr must be >= 1");
+  if (N > kLossStaticRows)
+    return fail(GRPO_INVALID_ARG, "N %d exceeds the %d sequences of the static scratch", N,
+                kLossStaticRows);
+  if (!(clip_eps >= 0.f && clip_eps < 1.f)) return fail(GRPO_INVALID_ARG, "clip_eps outside [0, 1)");
+  if (!(beta >= 0.f)) return fail(GRPO_INVALID_ARG, "beta must be >= 0");
+  if (agg != 0 && agg != 1) return fail(GRPO_INVALID_ARG, "agg must be 0 or 1");
+  double* scr = nullptr;
+  HIPCHK(loss_static_scratch(&scr));
+  HIPCHK(token_loss(logp, logp_old, logp_ref, mask, adv, N, Tr, clip_eps, beta, agg, loss_out,
+                    tok_loss, dloss_dlogp, stats, scr, (hipStream_t)stream));
+  g_err.clear();
+  return GRPO_OK;
+}

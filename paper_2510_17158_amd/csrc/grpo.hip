@@ -4,8 +4,18 @@
 // internally so the per-token KL estimator exp(d) - d - 1 (a difference of
 // nearly equal numbers when d is small) keeps its relative accuracy, and every
 // reduction is a fixed-order tree: per-row sums, then one workgroup over rows.
+#include <mutex>
+#include <vector>
+
 #include "common.h"
 #include "kernels.h"
+
+// Scratch of the allocation-free loss entry point: per sequence 8 partial sums
+// and 1 gradient weight (fp64) for up to kLossStaticRows sequences.  Each GPU
+// holds its own copy from the library's load until the process ends.  In host
+// code the name stands for the host-side shadow, never the device memory:
+// kernels get the address from loss_static_scratch().
+static __device__ __align__(256) double scratch[(size_t)grpo::kLossStaticRows * 9];
 
 namespace grpo {
 
@@ -156,6 +166,25 @@ hipError_t advantages(const float* r, int P, int G, float eps, float* adv, hipSt
   Prof pf("advantages", st);
   k_advantages<<<(P + 63) / 64, 64, 0, st>>>(r, P, G, eps, adv);
   return hipGetLastError();
+}
+
+hipError_t loss_static_scratch(double** out) {
+  static std::mutex mu;
+  static std::vector<double*> by_device;   // device address of `scratch` per device
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  if ((int)by_device.size() <= dev) by_device.resize(dev + 1, nullptr);
+  if (!by_device[dev]) {
+    // the current device is `dev`: the address of its copy
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    by_device[dev] = (double*)p;
+  }
+  *out = by_device[dev];
+  return hipSuccess;
 }
 
 hipError_t token_loss(const float* lp, const float* lo, const float* lr, const uint8_t* mask,

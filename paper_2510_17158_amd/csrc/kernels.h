@@ -208,6 +208,10 @@ hipError_t token_logprob(const float* logits, int R, int V, int ld, const int32_
 
 // ---- GRPO ---------------------------------------------------------------------------
 hipError_t advantages(const float* r, int P, int G, float eps, float* adv, hipStream_t st);
+// Device address, on the current device, of the loss's static scratch
+// (kLossStaticRows sequences x 9 doubles); looked up once per device.
+constexpr int kLossStaticRows = 16384;
+hipError_t loss_static_scratch(double** out);
 hipError_t token_loss(const float* lp, const float* lo, const float* lr, const uint8_t* mask,
                       const float* adv, int N, int Tr, float clip_eps, float beta, int agg,
                       float* loss, float* tok_loss, float* dl, float* stats, double* row_ws,
