@@ -335,6 +335,8 @@ int grpo_decode_structure(const grpo_model* m, int32_t B, int32_t max_len, int32
 /* Kernel timing for benchmarks.  Between grpo_profile_begin and
  * grpo_profile_end every kernel launch of the library is bracketed by HIP
  * events on its stream (decode steps run without graph replay meanwhile).
+ * GRPO_UNSUPPORTED while rocprofv3 collects hardware counters in the process
+ * (ROCPROF_COUNTER_COLLECTION set), which also turns decode graph replay off.
  * grpo_profile_end synchronises those events and writes NUL-terminated JSON
  * {"kernel": [launches, total_ms], ...} into json (len bytes); it returns
  * GRPO_INVALID_ARG if the text does not fit.  Process-wide; not for use while

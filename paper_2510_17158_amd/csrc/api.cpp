@@ -129,6 +129,17 @@ int fail(int code, const char* fmt, ...) {
     if (e_ != hipSuccess) return fail(GRPO_HIP_ERROR, "%s: %s", #expr, hipGetErrorString(e_)); \
   } while (0)
 
+// True while rocprofv3 collects hardware counters in this process (it exports
+// ROCPROF_COUNTER_COLLECTION).  Counter collection rewrites every kernel dispatch
+// on the intercepted queue; two combinations aborted under it (graph replay:
+// "invalid AQL packet"; HIP-event bracketing of every launch: the process died
+// on the host), so during such runs decode steps launch eagerly and kernel
+// timing is refused.  Results are identical either way.
+bool counter_collection() {
+  static const bool on = getenv("ROCPROF_COUNTER_COLLECTION") != nullptr;
+  return on;
+}
+
 // split-K target grid of the decode GEMM (GRPO_DECODE_WGS overrides, for tuning)
 int decode_target() {
   static const int v = [] {
@@ -608,6 +619,8 @@ int grpo_decode_structure(const grpo_model* m, int32_t B, int32_t max_len, int32
 }
 
 int grpo_profile_begin(void) {
+  if (counter_collection())
+    return fail(GRPO_UNSUPPORTED, "kernel timing is off while hardware counters are collected");
   std::lock_guard<std::mutex> lk(g_prof_mu);
   g_prof_acc.clear();
   g_prof.store(true);
@@ -866,7 +879,8 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
     return GRPO_OK;
   };
 
-  const bool use_graph = n_steps >= 2 && !trace_out && !profiling() && !getenv("GRPO_NO_GRAPH");
+  const bool use_graph = n_steps >= 2 && !trace_out && !profiling() && !getenv("GRPO_NO_GRAPH") &&
+                         !counter_collection();
   if (!use_graph) {
     for (int step = 0; step < n_steps; ++step)
       if (int rc = enqueue_step(st, false, step)) return rc;
