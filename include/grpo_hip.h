@@ -304,6 +304,38 @@ int grpo_token_loss(const float* logp, const float* logp_old, const float* logp_
                     float beta, int32_t agg, float* loss_out, float* tok_loss, float* dloss_dlogp,
                     float* stats, void* ws, size_t ws_bytes, void* stream);
 
+/* Reward of one completion (Sec. VI-A, Eq. 2-4), on the host:
+ *   r = r_perf + r_tools
+ *   r_perf  = -2 if the final code is incorrect; -1 if correct but slower than
+ *             the baseline (t > t_base); else min(10, t_base / t - 1)
+ *   r_tools = 0.5 * tools_used / tools_avail (unique available tools used)
+ * so r lies in [-2, 10.5].  All arguments are HOST arrays of n entries;
+ * correct is 0/1, times in any common unit.  GRPO_INVALID_ARG for
+ * non-positive or infinite times or tools_used outside [0, tools_avail]
+ * (checked for every entry before any output is written). */
+int grpo_reward(const uint8_t* correct, const double* t_base, const double* t,
+                const int32_t* tools_used, const int32_t* tools_avail, int32_t n, float* r_out);
+
+/* Distillation loss (Sec. VI-B: supervised fine-tuning of the small model on
+ * the large model's reasoning traces, tool-call tokens and arguments kept in
+ * the targets): the teacher-forced cross-entropy over the target tokens,
+ *   agg 1: -sum(mask * logp) / max(1, sum(mask))   (token mean)
+ *   agg 0: mean over sequences of each one's token mean (0 without targets)
+ * logp fp32 [N, Tr] (as grpo_score_sequences returns it), mask uint8 [N, Tr];
+ * loss_out fp32 [1]; dloss_dlogp NULL or fp32 [N, Tr].  fp64 inside.  The
+ * workspace is grpo_workspace_bytes(GRPO_OP_LOSS, N, Tr). */
+int grpo_sft_loss(const float* logp, const uint8_t* mask, int32_t N, int32_t Tr, int32_t agg,
+                  float* loss_out, float* dloss_dlogp, void* ws, size_t ws_bytes, void* stream);
+
+/* Exact full-vocabulary KL of the policy to the frozen reference (Alg. 1, KL
+ * step; the GRPO loss uses its per-token estimator): for each of R rows,
+ * kl_out[r] = sum_v p(v) (log p(v) - log p_ref(v)), p = softmax(logits[r] / T),
+ * p_ref = softmax(logits_ref[r] / T) (temperature 0 read as 1).  logits,
+ * logits_ref fp32 [R, ld] device rows of V entries; kl_out fp32 [R].  fp64
+ * inside. */
+int grpo_exact_kl(const float* logits, const float* logits_ref, int32_t R, int32_t V, int32_t ld,
+                  float temperature, float* kl_out, void* stream);
+
 /* grpo_token_loss for callers that cannot allocate device memory (code under
  * HIP graph capture, serving loops, harnesses that forbid hipMalloc): the same
  * kernels and results, with the per-sequence scratch in a static device array

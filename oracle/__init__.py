@@ -23,10 +23,11 @@ from .philox import philox4x32_10, philox_uniform24, gumbel_keys
 from .sampler import sample_token, topk_set, log_softmax
 from .model import OracleModel
 from .grpo import advantages, token_loss
+from .distill import exact_kl, reward, sft_loss
 
 __all__ = [
     "bf16_bits_to_f64", "round_bf16", "rmsnorm", "silu", "rope",
     "philox4x32_10", "philox_uniform24", "gumbel_keys",
     "sample_token", "topk_set", "log_softmax",
-    "OracleModel", "advantages", "token_loss",
+    "OracleModel", "advantages", "token_loss", "reward", "sft_loss", "exact_kl",
 ]

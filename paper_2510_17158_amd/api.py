@@ -138,6 +138,9 @@ _SIGS = {
     "grpo_decode_structure": (_I32, [_VP, _I32, _I32, _I32, _I32, _IP]),
     "grpo_token_loss_noalloc": (_I32, [_VP, _VP, _VP, _VP, _VP, _I32, _I32, _F32, _F32, _I32, _VP,
                                        _VP, _VP, _VP, _VP]),
+    "grpo_reward": (_I32, [_VP, _VP, _VP, _VP, _VP, _I32, _VP]),
+    "grpo_sft_loss": (_I32, [_VP, _VP, _I32, _I32, _I32, _VP, _VP, _VP, _SZ, _VP]),
+    "grpo_exact_kl": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _VP, _VP]),
     "grpo_profile_begin": (_I32, []),
     "grpo_profile_end": (_I32, [C.c_char_p, _SZ]),
 }
@@ -354,6 +357,32 @@ def token_loss_noalloc(logp, logp_old, logp_ref, mask, adv, clip_eps: float, bet
                                          _ptr(adv), N, Tr, clip_eps, beta, agg, _ptr(loss_out),
                                          _ptr(tok_loss), _ptr(dloss_dlogp), _ptr(stats),
                                          _stream(stream)))
+
+
+def reward(correct, t_base, t, tools_used, tools_avail) -> np.ndarray:
+    """grpo_reward on host arrays; returns fp32 rewards."""
+    c = np.ascontiguousarray(np.asarray(correct, np.uint8))
+    tb = np.ascontiguousarray(np.asarray(t_base, np.float64))
+    tt = np.ascontiguousarray(np.asarray(t, np.float64))
+    u = np.ascontiguousarray(np.asarray(tools_used, np.int32))
+    a = np.ascontiguousarray(np.asarray(tools_avail, np.int32))
+    out = np.empty(c.size, np.float32)
+    _check(lib().grpo_reward(c.ctypes.data, tb.ctypes.data, tt.ctypes.data, u.ctypes.data,
+                             a.ctypes.data, c.size, out.ctypes.data))
+    return out
+
+
+def sft_loss(logp, mask, agg: int, loss_out, dloss_dlogp=None, ws=None, stream=None):
+    N, Tr = logp.shape
+    _check(lib().grpo_sft_loss(_ptr(logp), _ptr(mask), N, Tr, agg, _ptr(loss_out),
+                               _ptr(dloss_dlogp), _ptr(ws), ws.numel() if ws is not None else 0,
+                               _stream(stream)))
+
+
+def exact_kl(logits, logits_ref, temperature: float, kl_out, stream=None):
+    R, V = logits.shape
+    _check(lib().grpo_exact_kl(_ptr(logits), _ptr(logits_ref), R, V, V, temperature,
+                               _ptr(kl_out), _stream(stream)))
 
 
 def profile_begin():

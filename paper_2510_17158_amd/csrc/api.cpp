@@ -1137,6 +1137,55 @@ int grpo_advantages(const float* rewards, int32_t P, int32_t G, float eps, float
   return GRPO_OK;
 }
 
+int grpo_reward(const uint8_t* correct, const double* t_base, const double* t,
+                const int32_t* tools_used, const int32_t* tools_avail, int32_t n, float* r_out) {
+  if (!correct || !t_base || !t || !tools_used || !tools_avail || !r_out)
+    return fail(GRPO_INVALID_ARG, "every array must be set");
+  if (n < 1) return fail(GRPO_INVALID_ARG, "n must be >= 1");
+  for (int i = 0; i < n; ++i) {
+    if (!(t_base[i] > 0.0) || !(t[i] > 0.0) || t_base[i] == INFINITY || t[i] == INFINITY)
+      return fail(GRPO_INVALID_ARG, "times of entry %d must be positive and finite", i);
+    if (tools_avail[i] < 1 || tools_used[i] < 0 || tools_used[i] > tools_avail[i])
+      return fail(GRPO_INVALID_ARG, "entry %d: need 0 <= tools_used <= tools_avail, avail >= 1", i);
+  }
+  for (int i = 0; i < n; ++i) {
+    double perf;
+    if (!correct[i]) perf = -2.0;
+    else if (t[i] > t_base[i]) perf = -1.0;
+    else perf = std::min(10.0, t_base[i] / t[i] - 1.0);
+    r_out[i] = (float)(perf + 0.5 * (double)tools_used[i] / (double)tools_avail[i]);
+  }
+  g_err.clear();
+  return GRPO_OK;
+}
+
+int grpo_sft_loss(const float* logp, const uint8_t* mask, int32_t N, int32_t Tr, int32_t agg,
+                  float* loss_out, float* dloss_dlogp, void* ws, size_t ws_bytes, void* stream) {
+  if (!logp || !mask || !loss_out || !ws)
+    return fail(GRPO_INVALID_ARG, "logp, mask, loss_out and ws must be set");
+  if (N < 1 || Tr < 1) return fail(GRPO_INVALID_ARG, "N and Tr must be >= 1");
+  if (agg != 0 && agg != 1) return fail(GRPO_INVALID_ARG, "agg must be 0 or 1");
+  const size_t need = grpo_workspace_bytes(nullptr, GRPO_OP_LOSS, N, Tr);
+  if (ws_bytes < need)
+    return fail(GRPO_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
+  HIPCHK(sft_loss(logp, mask, N, Tr, agg, loss_out, dloss_dlogp, (double*)ws,
+                  (hipStream_t)stream));
+  g_err.clear();
+  return GRPO_OK;
+}
+
+int grpo_exact_kl(const float* logits, const float* logits_ref, int32_t R, int32_t V, int32_t ld,
+                  float temperature, float* kl_out, void* stream) {
+  if (!logits || !logits_ref || !kl_out)
+    return fail(GRPO_INVALID_ARG, "logits, logits_ref and kl_out must be set");
+  if (R < 1 || V < 1 || ld < V) return fail(GRPO_INVALID_ARG, "need R, V >= 1 and ld >= V");
+  if (!(temperature >= 0.f) || temperature == INFINITY)
+    return fail(GRPO_INVALID_ARG, "temperature must be finite and >= 0");
+  HIPCHK(exact_kl(logits, logits_ref, R, V, ld, temperature, kl_out, (hipStream_t)stream));
+  g_err.clear();
+  return GRPO_OK;
+}
+
 int grpo_token_loss(const float* logp, const float* logp_old, const float* logp_ref,
                     const uint8_t* mask, const float* adv, int32_t N, int32_t Tr, float clip_eps,
                     float beta, int32_t agg, float* loss_out, float* tok_loss, float* dloss_dlogp,

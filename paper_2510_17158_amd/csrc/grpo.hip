@@ -159,7 +159,136 @@ __global__ __launch_bounds__(256) void k_loss_grad(const float* lp, const float*
   }
 }
 
+// distillation loss, row sums: [sum m*logp, count]
+__global__ __launch_bounds__(256) void k_sft_rows(const float* lp, const uint8_t* mask, int Tr,
+                                                  double* row_ws) {
+  __shared__ double sh[2][4];
+  const int n = blockIdx.x;
+  double acc[2] = {0, 0};
+  for (int t = threadIdx.x; t < Tr; t += 256) {
+    const size_t i = (size_t)n * Tr + t;
+    if (mask[i]) {
+      acc[0] += lp[i];
+      acc[1] += 1.0;
+    }
+  }
+  const int w = threadIdx.x / 64, l = threadIdx.x % 64;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const double v = wave_sum_d(acc[k]);
+    if (l == 0) sh[k][w] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < 2) {
+    const int k = threadIdx.x;
+    row_ws[(size_t)n * 2 + k] = ((sh[k][0] + sh[k][1]) + sh[k][2]) + sh[k][3];
+  }
+}
+
+// one workgroup: the loss and the per-row gradient weights
+__global__ __launch_bounds__(256) void k_sft_final(const double* row_ws, int N, int agg,
+                                                   float* loss, double* wts) {
+  __shared__ double sh[2][4];
+  __shared__ double s_tot[2];
+  double acc[2] = {0, 0};
+  for (int n = threadIdx.x; n < N; n += 256) {
+    const double* r = row_ws + (size_t)n * 2;
+    acc[0] += agg == 0 ? r[0] / fmax(1.0, r[1]) : r[0];
+    acc[1] += r[1];
+  }
+  const int w = threadIdx.x / 64, l = threadIdx.x % 64;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const double v = wave_sum_d(acc[k]);
+    if (l == 0) sh[k][w] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < 2) {
+    const int k = threadIdx.x;
+    s_tot[k] = ((sh[k][0] + sh[k][1]) + sh[k][2]) + sh[k][3];
+  }
+  __syncthreads();
+  const double ntok = fmax(1.0, s_tot[1]);
+  if (threadIdx.x == 0) loss[0] = (float)(agg == 0 ? -s_tot[0] / (double)N : -s_tot[0] / ntok);
+  for (int n = threadIdx.x; n < N; n += 256)
+    wts[n] = agg == 0 ? 1.0 / ((double)N * fmax(1.0, row_ws[(size_t)n * 2 + 1])) : 1.0 / ntok;
+}
+
+__global__ __launch_bounds__(256) void k_sft_grad(const uint8_t* mask, int Tr, const double* wts,
+                                                  float* dl) {
+  const int n = blockIdx.x;
+  const float g = (float)(-wts[n]);
+  for (int t = threadIdx.x; t < Tr; t += 256) {
+    const size_t i = (size_t)n * Tr + t;
+    dl[i] = mask[i] ? g : 0.f;
+  }
+}
+
+// Exact KL(softmax(a) || softmax(b)) of one row, a = z / T, b = z_ref / T, in fp64:
+// KL = sum e^(a - ma) (a - b) / Sa - (ma + ln Sa) + (mb + ln Sb).
+__global__ __launch_bounds__(256) void k_exact_kl(const float* z, const float* zr, int V, int ld,
+                                                  double inv_t, float* kl) {
+  __shared__ double sh[4];
+  const int r = blockIdx.x;
+  const float* a = z + (size_t)r * ld;
+  const float* b = zr + (size_t)r * ld;
+  double ma = -INFINITY, mb = -INFINITY;
+  for (int i = threadIdx.x; i < V; i += 256) {
+    ma = fmax(ma, (double)a[i] * inv_t);
+    mb = fmax(mb, (double)b[i] * inv_t);
+  }
+  auto bmax = [&](double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
+    __syncthreads();
+    if (threadIdx.x % 64 == 0) sh[threadIdx.x / 64] = v;
+    __syncthreads();
+    return fmax(fmax(sh[0], sh[1]), fmax(sh[2], sh[3]));
+  };
+  auto bsum = [&](double v) {
+    v = wave_sum_d(v);
+    __syncthreads();
+    if (threadIdx.x % 64 == 0) sh[threadIdx.x / 64] = v;
+    __syncthreads();
+    return ((sh[0] + sh[1]) + sh[2]) + sh[3];
+  };
+  ma = bmax(ma);
+  mb = bmax(mb);
+  double sa = 0.0, sb = 0.0, d = 0.0;
+  for (int i = threadIdx.x; i < V; i += 256) {
+    const double ai = (double)a[i] * inv_t, bi = (double)b[i] * inv_t;
+    const double ea = exp(ai - ma);
+    sa += ea;
+    sb += exp(bi - mb);
+    d += ea * (ai - bi);
+  }
+  sa = bsum(sa);
+  sb = bsum(sb);
+  d = bsum(d);
+  if (threadIdx.x == 0) kl[r] = (float)(d / sa - (ma + log(sa)) + (mb + log(sb)));
+}
+
 }  // namespace
+
+hipError_t sft_loss(const float* lp, const uint8_t* mask, int N, int Tr, int agg, float* loss,
+                    float* dl, double* row_ws, hipStream_t st) {
+  if (N <= 0) return hipSuccess;
+  double* wts = row_ws + (size_t)N * 2;
+  Prof pf("sft_loss", st);
+  k_sft_rows<<<N, 256, 0, st>>>(lp, mask, Tr, row_ws);
+  k_sft_final<<<1, 256, 0, st>>>(row_ws, N, agg, loss, wts);
+  if (dl) k_sft_grad<<<N, 256, 0, st>>>(mask, Tr, wts, dl);
+  return hipGetLastError();
+}
+
+hipError_t exact_kl(const float* z, const float* zr, int R, int V, int ld, float temperature,
+                    float* kl, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  const double inv_t = 1.0 / (double)(temperature > 0.f ? temperature : 1.f);
+  Prof pf("exact_kl", st);
+  k_exact_kl<<<R, 256, 0, st>>>(z, zr, V, ld, inv_t, kl);
+  return hipGetLastError();
+}
 
 hipError_t advantages(const float* r, int P, int G, float eps, float* adv, hipStream_t st) {
   if (P <= 0) return hipSuccess;

@@ -208,6 +208,13 @@ hipError_t token_logprob(const float* logits, int R, int V, int ld, const int32_
 
 // ---- GRPO ---------------------------------------------------------------------------
 hipError_t advantages(const float* r, int P, int G, float eps, float* adv, hipStream_t st);
+// Distillation loss -mean(logp) over the masked tokens (agg as token_loss) and its
+// gradient; row_ws: 3 N doubles.
+hipError_t sft_loss(const float* lp, const uint8_t* mask, int N, int Tr, int agg, float* loss,
+                    float* dl, double* row_ws, hipStream_t st);
+// kl[r] = KL(softmax(z[r] / T) || softmax(zr[r] / T)) over V entries, fp64 inside.
+hipError_t exact_kl(const float* z, const float* zr, int R, int V, int ld, float temperature,
+                    float* kl, hipStream_t st);
 // Device address, on the current device, of the loss's static scratch
 // (kLossStaticRows sequences x 9 doubles); looked up once per device.
 constexpr int kLossStaticRows = 16384;

@@ -189,3 +189,30 @@ def test_product_path_has_no_cpu_fallback():
     for mod in (a, r):
         src = open(mod.__file__).read()
         assert "import oracle" not in src and "from oracle" not in src
+
+
+def test_reward_host_call_matches_the_oracle_and_checks_arguments():
+    """grpo_reward computes on the host (no GPU): every branch of Eq. 2-4 against
+    the oracle, and bad times / tool counts rejected before any output."""
+    import numpy as np
+    import oracle
+    rng = np.random.default_rng(3)
+    n = 2000
+    c = rng.random(n) < 0.7
+    tb = rng.lognormal(0, 1, n)
+    t = tb * rng.lognormal(0, 1.2, n)
+    t[:5] = tb[:5]                          # exactly as fast: r_perf 0
+    avail = rng.integers(4, 7, n)
+    used = (rng.random(n) * (avail + 1)).astype(np.int32)
+    got = api.reward(c, tb, t, used, avail)
+    want = oracle.reward(c, tb, t, used, avail)
+    # fp32 output of an fp64 evaluation
+    np.testing.assert_allclose(got, want, rtol=2.0 ** -24, atol=0)
+    assert got.min() >= -2.0 and got.max() <= 10.5
+    for bad in (dict(t=-1.0), dict(t_base=0.0), dict(used=5, avail=4), dict(avail=0)):
+        args = dict(c=1, t_base=1.0, t=0.5, used=1, avail=4)
+        args.update(bad)
+        with pytest.raises(api.GrpoError) as e:
+            api.reward([args["c"]], [args["t_base"]], [args["t"]], [args["used"]],
+                       [args["avail"]])
+        assert e.value.code == api.INVALID_ARG

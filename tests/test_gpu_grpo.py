@@ -93,3 +93,46 @@ def test_token_loss_ratio_one_and_nonfinite():
     inp["logp"][1, 3] = np.inf
     loss, tl, dl, st = _loss(inp, 0.2, 0.04, 0)
     assert st[3] == 1.0 and not np.isfinite(loss)
+
+
+@pytest.mark.parametrize("agg", [0, 1])
+def test_sft_loss_matches_oracle(agg):
+    """Distillation cross-entropy (Sec. VI-B) over target tokens: loss within 1e-5
+    relative, gradient within fp32 rounding of the oracle's."""
+    require_gpu()
+    rng = np.random.default_rng(11 + agg)
+    N, Tr = 33, 1500
+    lp = (-rng.random((N, Tr)) * 6).astype(np.float32)
+    m = (rng.random((N, Tr)) < 0.6).astype(np.uint8)
+    m[3] = 0
+    d_lp, d_m = torch.from_numpy(lp).cuda(), torch.from_numpy(m).cuda()
+    loss = torch.empty(1, device="cuda")
+    g = torch.full((N, Tr), float("nan"), device="cuda")
+    ws = api.alloc_workspace(None, api.OP_LOSS, N, Tr)
+    api.sft_loss(d_lp, d_m, agg, loss, g, ws=ws)
+    torch.cuda.synchronize()
+    ref = oracle.sft_loss(lp, m, agg)
+    assert abs(loss.item() - ref["loss"]) <= 1e-5 * abs(ref["loss"]) + 1e-7
+    np.testing.assert_allclose(g.cpu().numpy(), ref["grad"], rtol=2.0 ** -23, atol=0)
+
+
+def test_exact_kl_matches_oracle():
+    """Full-vocabulary KL of two logit rows (fp64 inside, fp32 out): within fp32
+    rounding of the oracle plus 1e-10 (fp64 sums over 32000 terms), at two
+    temperatures, equal logits giving 0."""
+    require_gpu()
+    rng = np.random.default_rng(5)
+    R, V = 40, 32000
+    z = (rng.standard_normal((R, V)) * 1.3).astype(np.float32)
+    zr = (z + rng.standard_normal((R, V)) * rng.choice([1e-3, 0.05, 0.5], (R, 1))).astype(
+        np.float32)
+    zr[0] = z[0]
+    dz, dzr = torch.from_numpy(z).cuda(), torch.from_numpy(zr).cuda()
+    for T in (1.0, 0.8):
+        kl = torch.empty(R, device="cuda")
+        api.exact_kl(dz, dzr, T, kl)
+        torch.cuda.synchronize()
+        ref = oracle.exact_kl(z.astype(np.float64), zr.astype(np.float64), T)
+        got = kl.cpu().numpy()
+        np.testing.assert_allclose(got, ref, rtol=2.0 ** -23, atol=1e-10)
+        assert abs(got[0]) <= 1e-10
