@@ -65,7 +65,10 @@ enum grpo_status {
 enum grpo_dtype { GRPO_F32 = 0, GRPO_BF16 = 1 };
 
 /* Workspace kinds for grpo_workspace_bytes. */
-enum grpo_op { GRPO_OP_PREFILL = 0, GRPO_OP_ROLLOUT = 1, GRPO_OP_SCORE = 2, GRPO_OP_LOSS = 3 };
+enum grpo_op {
+  GRPO_OP_PREFILL = 0, GRPO_OP_ROLLOUT = 1, GRPO_OP_SCORE = 2, GRPO_OP_LOSS = 3,
+  GRPO_OP_EXTEND = 4
+};
 
 /* Decoder shape.  Llama family: RMSNorm, RoPE (half-split pairs (i, i+hd/2),
  * angle pos * rope_theta^(-2i/hd)), grouped-query attention (query head h reads
@@ -181,6 +184,7 @@ size_t grpo_kv_cache_bytes(const grpo_config* cfg, int32_t n_seqs, int32_t max_l
  *   GRPO_OP_PREFILL: n_rows = prompts P, seq_len = prompt length Tp
  *   GRPO_OP_ROLLOUT: n_rows = batch B,   seq_len = KV capacity max_len
  *   GRPO_OP_SCORE:   n_rows = sequences N, seq_len = T
+ *   GRPO_OP_EXTEND:  n_rows = batch B,   seq_len = KV capacity max_len
  *   GRPO_OP_LOSS:    n_rows = sequences N, seq_len = Tr (model may be NULL) */
 size_t grpo_workspace_bytes(const grpo_model* m, int32_t op, int32_t n_rows, int32_t seq_len);
 
@@ -252,6 +256,33 @@ int grpo_rollout_step_grouped(const grpo_model* m, void* kv, int32_t n_seqs, int
                               int32_t n_steps, const grpo_sampling* s, int32_t* tok_out,
                               float* logp_out, const grpo_trace* trace, void* ws,
                               size_t ws_bytes, void* stream);
+
+/* Tool-output injection into live sequences (Sec. V-B: the model emits a tool
+ * call, the tool's output is placed into its context and generation resumes;
+ * Sec. VI-C: group members not waiting on a tool keep decoding).  For each row
+ * b, sequence seq_ids[b] (cache slot and Philox sequence id, as in
+ * grpo_rollout_step) receives the Te tokens tokens[b, :] at positions
+ * pos0[b] .. pos0[b] + Te - 1: a causal forward of those rows over the
+ * sequence's cached positions 0 .. pos0[b] - 1 and the span itself, their K/V
+ * written into the cache; then the next token is drawn from the span's last
+ * position with Philox step `step` (tok_out[b], logp_out[b] as in
+ * grpo_rollout_step).  The injected tokens are context, not samples: they get no
+ * log-probability (their loss mask is 0).  Rows may sit at different positions;
+ * rows not in the call keep their cache untouched (a paused or finished
+ * sequence simply is not listed).  Generation continues with grpo_rollout_step
+ * from pos = pos0[b] + Te, tok = tok_out[b].
+ *   seq_ids  HOST int32 [B] (NULL: b), distinct, in [0, n_seqs)
+ *   pos0     HOST int32 [B], pos0[b] >= 0, pos0[b] + Te <= max_len
+ *            (GRPO_KV_CAPACITY otherwise)
+ *   tokens   DEVICE int32 [B, Te]; 1 <= Te <= GRPO_EXTEND_CHUNK (a longer
+ *            output is injected by consecutive calls, pos0 advancing by Te)
+ *   trace    NULL or the intermediates (rows R = B * Te; head rows = B)
+ * Workspace: grpo_workspace_bytes(GRPO_OP_EXTEND, B, max_len). */
+#define GRPO_EXTEND_CHUNK 512
+int grpo_extend(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len, int32_t B,
+                const int32_t* seq_ids, const int32_t* pos0, const int32_t* tokens, int32_t Te,
+                int32_t step, const grpo_sampling* s, int32_t* tok_out, float* logp_out,
+                const grpo_trace* trace, void* ws, size_t ws_bytes, void* stream);
 
 /* Teacher-forced scoring (Eq. 1's log pi and the KL term's reference): for
  * j in [score_from, T): logp_out[n, j - score_from] =

@@ -174,6 +174,46 @@ class OracleModel:
         x = x + self.mm(a, p + "w_down")
         return x, k_new, v_new
 
+    # -- a span of tokens appended to a cached sequence -----------------------
+    def extend_layer(self, l: int, x: np.ndarray, pos0: int, K: np.ndarray, V: np.ndarray):
+        """x [Te, d] residual of a span at positions pos0 .. pos0 + Te - 1 of one
+        sequence whose K/V [Hkv, >= pos0 + Te, hd] hold positions 0 .. pos0 - 1;
+        the span's k, v are written there and every row attends positions
+        0 .. its own.  Returns the new residual (tool output injected into a live
+        sequence, Sec. V-B)."""
+        c, R = self.cfg, self.R
+        x = np.asarray(x, np.float64)
+        Te = x.shape[0]
+        H, Hk, hd = c.n_heads, c.n_kv_heads, c.head_dim
+        p = f"l{l}."
+        pos = pos0 + np.arange(Te)
+        h = R(rmsnorm(x, self.mat(p + "attn_norm"), c.rms_eps))
+        q = R(rope(self.mm(h, p + "wq").reshape(Te, H, hd), pos, c.rope_theta))
+        k = R(rope(self.mm(h, p + "wk").reshape(Te, Hk, hd), pos, c.rope_theta))
+        v = R(self.mm(h, p + "wv").reshape(Te, Hk, hd))
+        K[:, pos0:pos0 + Te] = k.transpose(1, 0, 2)
+        V[:, pos0:pos0 + Te] = v.transpose(1, 0, 2)
+        o = np.empty((Te, H, hd))
+        for t in range(Te):
+            n = pos0 + t + 1
+            for hh in range(H):
+                g = hh * Hk // H
+                sc = K[g, :n] @ q[t, hh] / float(np.sqrt(hd))
+                pr = np.exp(sc - sc.max())
+                o[t, hh] = (pr / pr.sum()) @ V[g, :n]
+        x = x + self.mm(R(o.reshape(Te, H * hd)), p + "wo")
+        h = R(rmsnorm(x, self.mat(p + "mlp_norm"), c.rms_eps))
+        a = R(silu(self.mm(h, p + "w_gate")) * self.mm(h, p + "w_up"))
+        return x + self.mm(a, p + "w_down")
+
+    def extend(self, tokens, pos0: int, K: np.ndarray, V: np.ndarray) -> np.ndarray:
+        """Span tokens [Te] at positions pos0.. of one sequence with caches K/V
+        [L, Hkv, Tmax, hd] (updated in place) -> logits of every span row [Te, V]."""
+        x = self.embed(tokens)
+        for l in range(self.cfg.n_layers):
+            x = self.extend_layer(l, x, pos0, K[l], V[l])
+        return self.head(x)
+
     def decode(self, tokens, pos, K: np.ndarray, V: np.ndarray, return_hidden: bool = False):
         """One decode step for B sequences; K/V [L, B, Hkv, Tmax, hd] updated in place."""
         x = self.embed(tokens)

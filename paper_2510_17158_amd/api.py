@@ -19,7 +19,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgrpo_hip.so")
 
 OK, INVALID_ARG, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP_ERROR, KV_CAPACITY = 0, -1, -2, -3, -4, -5
-OP_PREFILL, OP_ROLLOUT, OP_SCORE, OP_LOSS = 0, 1, 2, 3
+OP_PREFILL, OP_ROLLOUT, OP_SCORE, OP_LOSS, OP_EXTEND = 0, 1, 2, 3, 4
+EXTEND_CHUNK = 512
 
 
 class GrpoError(RuntimeError):
@@ -129,6 +130,8 @@ _SIGS = {
     "grpo_rollout_step_grouped": (_I32, [_VP, _VP, _I32, _I32, _I32, _I32, _I32, _IP, _VP, _VP,
                                          _I32, _I32, _I32, C.POINTER(Sampling), _VP, _VP, _TP,
                                          _VP, _SZ, _VP]),
+    "grpo_extend": (_I32, [_VP, _VP, _I32, _I32, _I32, _IP, _IP, _VP, _I32, _I32,
+                           C.POINTER(Sampling), _VP, _VP, _TP, _VP, _SZ, _VP]),
     "grpo_score_sequences": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _VP, _TP, _VP, _SZ, _VP]),
     "grpo_score_sequences_grouped": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _I32, _I32, _VP,
                                             _TP, _VP, _SZ, _VP]),
@@ -307,6 +310,18 @@ def rollout_step(model: Model, kv, n_seqs: int, max_len: int, pos, tok, max_pos:
                                    _ptr(tok), max_pos, step0, n_steps, C.byref(sampling),
                                    _ptr(tok_out), _ptr(logp_out), _trace(trace), _ptr(ws), nws,
                                    _stream(stream)))
+
+
+def extend(model: Model, kv, n_seqs: int, max_len: int, pos0, tokens, step: int,
+           sampling: Sampling, tok_out, logp_out, seq_ids=None, trace: Trace | None = None,
+           ws=None, stream=None):
+    """grpo_extend: tokens [B, Te] (device) injected at host positions pos0[b] of
+    sequences seq_ids[b] (host, None: b); the next token of each row drawn at `step`."""
+    B, Te = tokens.shape
+    _check(lib().grpo_extend(model.handle, _ptr(kv), n_seqs, max_len, B, _ids(seq_ids, B),
+                             _ids(pos0, B), _ptr(tokens), Te, step, C.byref(sampling),
+                             _ptr(tok_out), _ptr(logp_out), _trace(trace), _ptr(ws),
+                             ws.numel() if ws is not None else 0, _stream(stream)))
 
 
 def score_sequences(model: Model, tokens, score_from: int, temperature: float, logp_out,

@@ -371,6 +371,29 @@ PrefillWS take_prefill(Bump& b, const grpo_config& c, int P, int Tp) {
   return w;
 }
 
+constexpr int kExtendChunk = GRPO_EXTEND_CHUNK;   // span rows per sequence and call
+
+struct ExtendWS {
+  StepWS s;
+  uint16_t* vt;         // V^T of every sequence up to max_len (bf16)
+  void* hl;
+  float* logits;
+  int32_t *slots, *pos0, *row_pos, *row_slot;
+};
+ExtendWS take_extend(Bump& b, const grpo_config& c, int B, int max_len) {
+  ExtendWS w;
+  const size_t M = (size_t)B * kExtendChunk;
+  w.s = take_step(b, c, (int)M, (int)M, 0, max_len);
+  w.vt = b.take<uint16_t>(c.dtype == GRPO_F32 ? 0 : (size_t)B * kvdim(c) * round8(max_len));
+  w.hl = b.take<char>((size_t)B * c.d_model * esize(c));
+  w.logits = b.take<float>((size_t)B * c.vocab);
+  w.slots = b.take<int32_t>(B);
+  w.pos0 = b.take<int32_t>(B);
+  w.row_pos = b.take<int32_t>(M);
+  w.row_slot = b.take<int32_t>(M);
+  return w;
+}
+
 struct ScoreWS {
   int chunk;         // sequences per chunk
   int sub_rows;      // LM-head rows per logits sub-chunk
@@ -667,6 +690,7 @@ size_t grpo_workspace_bytes(const grpo_model* m, int32_t op, int32_t n_rows, int
     case GRPO_OP_PREFILL: take_prefill(b, m->cfg, n_rows, seq_len); break;
     case GRPO_OP_ROLLOUT: take_rollout(b, m->cfg, n_rows, seq_len); break;
     case GRPO_OP_SCORE: take_score(b, m->cfg, n_rows, seq_len); break;
+    case GRPO_OP_EXTEND: take_extend(b, m->cfg, n_rows, seq_len); break;
     default: return 0;
   }
   return b.off;
@@ -1122,6 +1146,126 @@ int grpo_score_sequences_grouped(const grpo_model* m, const int32_t* tokens, int
                            temperature, logp_out + (size_t)n0 * Ts + i0, st));
     }
   }
+  g_err.clear();
+  return GRPO_OK;
+}
+
+int grpo_extend(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len, int32_t B,
+                const int32_t* seq_ids, const int32_t* pos0, const int32_t* tokens, int32_t Te,
+                int32_t step, const grpo_sampling* s, int32_t* tok_out, float* logp_out,
+                const grpo_trace* trace_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
+  const grpo_config& c = m->cfg;
+  if (!kv || !pos0 || !tokens || !tok_out || !logp_out || !ws)
+    return fail(GRPO_INVALID_ARG, "kv, pos0, tokens, tok_out, logp_out and ws must be set");
+  if (B < 1 || max_len < 1 || step < 0) return fail(GRPO_INVALID_ARG, "B, max_len >= 1, step >= 0");
+  if (Te < 1 || Te > kExtendChunk)
+    return fail(GRPO_INVALID_ARG, "span length %d outside [1, %d]: inject longer spans in chunks",
+                Te, kExtendChunk);
+  if (!seq_ids && B > n_seqs) return fail(GRPO_INVALID_ARG, "B %d exceeds n_seqs %d", B, n_seqs);
+  if (c.dtype == GRPO_F32 && max_len > 16384) return fail(GRPO_UNSUPPORTED, "fp32 caches above 16384");
+  if (int rc = check_sampling(s, c.vocab)) return rc;
+  std::vector<int32_t> ids(B);
+  for (int b = 0; b < B; ++b) ids[b] = seq_ids ? seq_ids[b] : b;
+  {
+    std::vector<int32_t> sorted(ids);
+    for (int b = 0; b < B; ++b)
+      if (sorted[b] < 0 || sorted[b] >= n_seqs)
+        return fail(GRPO_INVALID_ARG, "seq_ids[%d] = %d outside [0, n_seqs %d)", b, sorted[b], n_seqs);
+    std::sort(sorted.begin(), sorted.end());
+    for (int b = 1; b < B; ++b)
+      if (sorted[b] == sorted[b - 1]) return fail(GRPO_INVALID_ARG, "seq_ids repeats sequence %d", sorted[b]);
+  }
+  for (int b = 0; b < B; ++b) {
+    if (pos0[b] < 0) return fail(GRPO_INVALID_ARG, "pos0[%d] = %d is negative", b, pos0[b]);
+    if ((long)pos0[b] + Te > max_len)
+      return fail(GRPO_KV_CAPACITY, "pos0[%d] %d + span %d exceeds max_len %d", b, pos0[b], Te,
+                  max_len);
+  }
+  const size_t need = grpo_workspace_bytes(m, GRPO_OP_EXTEND, B, max_len);
+  if (ws_bytes < need)
+    return fail(GRPO_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
+  hipStream_t st = (hipStream_t)stream;
+  Bump bump(ws);
+  ExtendWS w = take_extend(bump, c, B, max_len);
+  const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn, M = B * Te;
+  const Partials none{nullptr, 0, 0, d};
+  const int act = c.dtype == GRPO_F32 ? TR_F32 : TR_BF16;
+  const TraceMap rows = TraceMap::rows();
+  const grpo_trace* tr = trace_out;
+  int rc;
+  HIPCHK(set_i32(w.slots, ids.data(), B, st));
+  HIPCHK(set_i32(w.pos0, pos0, B, st));
+  if (c.dtype == GRPO_F32) HIPCHK(row_positions(w.pos0, w.slots, B, Te, w.row_pos, w.row_slot, st));
+  HIPCHK(embed(c.dtype, m->tok_emb, tokens, M, d, c.vocab, w.s.x, st));
+  HIPCHK(rope_table(nullptr, max_len, c.head_dim, c.rope_theta, w.s.cs, st));
+  const int vt_len = round8(max_len);
+  for (int l = 0; l < c.n_layers; ++l) {
+    Layer L = kv_layer(m, kv, l, n_seqs, max_len);
+    HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), none, m->attn_norm[l], M, d, c.rms_eps,
+                   w.s.h, d, st));
+    if ((rc = trace(TRM(tr, x), l, M, d, w.s.x, TR_F32, d, M, rows, st)) ||
+        (rc = trace(TRM(tr, h_attn), l, M, d, w.s.h, act, d, M, rows, st)))
+      return rc;
+    if ((rc = gemm_rows(m, w.s.h, d, M, qkv_stack(m, l), qd + 2 * kvd, d, EPI_STORE,
+                        EpiArgs{w.s.qkv, nullptr, qd + 2 * kvd}, st)))
+      return rc;
+    // the span's K/V into each sequence's slot at pos0[b] + t
+    RopeArgs ra{};
+    ra.mode = 1; ra.T = Te; ra.G = 1; ra.pos_arr = w.pos0; ra.slots = w.slots;
+    ra.n_heads = c.n_heads; ra.n_kv = c.n_kv_heads; ra.hd = c.head_dim; ra.theta = c.rope_theta;
+    ra.kcache = L.k; ra.vcache = L.v; ra.n_seqs = n_seqs; ra.max_len = max_len;
+    ra.vt = nullptr; ra.vt_len = 0; ra.splits = 1; ra.split_stride = 0; ra.cs = w.s.cs;
+    if (tr) {
+      ra.tq = tr->q ? tr->q + (size_t)l * M * qd : nullptr;
+      ra.tk = tr->k ? tr->k + (size_t)l * M * kvd : nullptr;
+      ra.tv = tr->v ? tr->v + (size_t)l * M * kvd : nullptr;
+      ra.tmap = rows;
+    }
+    HIPCHK(rope_kv(c.dtype, w.s.qkv, M, w.s.q, ra, st));
+    // causal attention of the span rows over each sequence's cache 0 .. pos0[b] + t
+    if (c.dtype == GRPO_F32) {
+      HIPCHK(attn_rows_f32((const float*)w.s.q, (const float*)L.k, (const float*)L.v, w.row_pos,
+                           w.row_slot, M, 1, 1, c.n_heads, c.n_kv_heads, c.head_dim, max_len,
+                           (float*)w.s.o, st));
+    } else {
+      HIPCHK(cache_vt(L.v, w.slots, w.pos0, B, Te, c.n_kv_heads, max_len, c.head_dim, vt_len,
+                      w.vt, st));
+      HIPCHK(attn_prefill(c.dtype, w.s.q, L.k, w.vt, B, Te, c.n_heads, c.n_kv_heads, c.head_dim,
+                          max_len, 1, w.s.o, st, 0, 1, vt_len, w.pos0, w.slots));
+    }
+    if ((rc = trace(TRM(tr, o), l, M, qd, w.s.o, act, qd, M, rows, st))) return rc;
+    if ((rc = gemm_rows(m, w.s.o, qd, M, one(m->wo[l]), d, qd, EPI_RESID,
+                        EpiArgs{w.s.x, nullptr, d}, st)))
+      return rc;
+    HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap::identity(), none, m->mlp_norm[l], M, d, c.rms_eps,
+                   w.s.h, d, st));
+    if ((rc = trace(TRM(tr, x_attn), l, M, d, w.s.x, TR_F32, d, M, rows, st)) ||
+        (rc = trace(TRM(tr, h_mlp), l, M, d, w.s.h, act, d, M, rows, st)))
+      return rc;
+    if ((rc = gemm_rows(m, w.s.h, d, M, gate_up(m, l), f, d, EPI_SWIGLU,
+                        EpiArgs{nullptr, w.s.a, f}, st)))
+      return rc;
+    if ((rc = trace(TRM(tr, act), l, M, f, w.s.a, act, f, M, rows, st))) return rc;
+    if ((rc = gemm_rows(m, w.s.a, f, M, one(m->w_down[l]), d, f, EPI_RESID,
+                        EpiArgs{w.s.x, nullptr, d}, st)))
+      return rc;
+  }
+  if ((rc = trace(TRM(tr, x), c.n_layers, M, d, w.s.x, TR_F32, d, M, rows, st))) return rc;
+  // the next token of each sequence, from the span's last row
+  HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{0, 1, Te, Te - 1}, none, m->final_norm, B, d, c.rms_eps,
+                 w.hl, d, st));
+  if ((rc = gemm_rows(m, w.hl, d, B, one(m->lm_head), c.vocab, d, EPI_STORE,
+                      EpiArgs{w.logits, nullptr, c.vocab}, st)))
+    return rc;
+  if ((rc = trace(TRM(tr, h_final), 0, B, d, w.hl, act, d, B, rows, st)) ||
+      (rc = trace(TRM(tr, logits), 0, B, c.vocab, w.logits, TR_F32, c.vocab, B, rows, st)))
+    return rc;
+  SampleArgs sa{};
+  sa.temperature = s->temperature; sa.top_k = s->top_k; sa.seed = s->seed; sa.step = step;
+  sa.G = 1; sa.tok_out = tok_out; sa.logp_out = logp_out; sa.out_stride = 1;
+  sa.seq_ids = w.slots;
+  HIPCHK(sample(w.logits, B, c.vocab, c.vocab, sa, st));
   g_err.clear();
   return GRPO_OK;
 }

@@ -47,7 +47,8 @@ template <int HD, int GQ>
 __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) void k_flash_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ vt,
     int T, int H, int n_kv, int k_len, int k_seq_stride, int vt_len, float scale,
-    bf16_t* __restrict__ out, int q_pos0, int vt_seq_stride) {
+    bf16_t* __restrict__ out, int q_pos0, int vt_seq_stride, const int32_t* __restrict__ qpos,
+    const int32_t* __restrict__ kslots) {
   constexpr int QSTEPS = HD / 32, HB = HD / 16;
   constexpr int NCP = HD / 8;   // 1 KB copies per K tile (and per V^T tile)
   __shared__ __attribute__((aligned(1024))) bf16_t ks[2][64 * HD];
@@ -72,10 +73,14 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
     for (int st = 0; st < QSTEPS; ++st) qf[qb][st] = *(const bf16x8_t*)(qp + st * 32);
   }
-  const bf16_t* kbase = k + ((size_t)n * k_seq_stride * n_kv + g) * (size_t)k_len * HD;
+  // sequence n's first query position (per sequence when qpos is given) and
+  // its K slot (kslots, else n * k_seq_stride)
+  const int qp0 = qpos ? qpos[n] : q_pos0;
+  const size_t kslot = kslots ? (size_t)kslots[n] : (size_t)n * k_seq_stride;
+  const bf16_t* kbase = k + (kslot * n_kv + g) * (size_t)k_len * HD;
   const bf16_t* vbase = vt + ((size_t)n * vt_seq_stride * n_kv + g) * (size_t)HD * vt_len;
-  // query rows are positions q_pos0 + row; keys run to position Tk - 1
-  const int Tk = q_pos0 + T;
+  // query rows are positions qp0 + row; keys run to position Tk - 1
+  const int Tk = qp0 + T;
 
   // Tile t of 64 keys into stage buf by direct-to-LDS copies, NCP of K and NCP of
   // V^T dealt round-robin to the waves.  Copy i, lane l fills the 16-byte LDS
@@ -125,7 +130,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
   float mq[2] = {-1e30f, -1e30f}, lq_sum[2] = {0.f, 0.f};
 
   const float scale2 = scale * 1.4426950408889634f;   // log2(e)
-  const int qlast = q_pos0 + min(q0 + 31, T - 1);
+  const int qlast = qp0 + min(q0 + 31, T - 1);
   const int n_tiles = qlast / 64 + 1;
   copy_tile(0, 0);
   dma_wait();
@@ -173,7 +178,7 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       // (last tile) key k0 + 32 s2 + 8 lg + 4 b + v is visible iff 32 s2 + 4 b + v <= lim
-      const int lim = q_pos0 + min(q0 + qb * 16 + lq, T - 1) - k0 - 8 * lg;
+      const int lim = qp0 + min(q0 + qb * 16 + lq, T - 1) - k0 - 8 * lg;
       float mx = -INFINITY;
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2)
@@ -253,8 +258,12 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
     dma_wait();
     __syncthreads();
   };
-  for (int t = 0; t + 1 < n_tiles; ++t) tile_step(t, std::false_type{});
-  tile_step(n_tiles - 1, std::true_type{});
+  // key tiles from the one holding the block's first query position on hold
+  // keys past some query of the block (only the last one when qp0 is a
+  // multiple of 32)
+  const int tm = min((qp0 + q0) / 64, n_tiles - 1);
+  for (int t = 0; t < tm; ++t) tile_step(t, std::false_type{});
+  for (int t = tm; t < n_tiles; ++t) tile_step(t, std::true_type{});
 
   // O^T: lane holds dims 16 hb + 4 lg + v of query column lq
 #pragma unroll
@@ -277,11 +286,13 @@ __global__ __launch_bounds__(64 * GQ) __attribute__((amdgpu_waves_per_eu(2))) vo
 template <int HD>
 hipError_t launch_flash(int gq, dim3 grid, hipStream_t st, const bf16_t* q, const bf16_t* k,
                         const bf16_t* vt, int T, int H, int n_kv, int k_len, int k_seq_stride,
-                        int vt_len, float scale, bf16_t* out, int q_pos0, int vt_seq_stride) {
+                        int vt_len, float scale, bf16_t* out, int q_pos0, int vt_seq_stride,
+                        const int32_t* qpos, const int32_t* kslots) {
 #define GRPO_FLASH(G)                                                                        \
   case G:                                                                                   \
     k_flash_bf16<HD, G><<<grid, 64 * G, 0, st>>>(q, k, vt, T, H, n_kv, k_len, k_seq_stride, \
-                                                 vt_len, scale, out, q_pos0, vt_seq_stride); \
+                                                 vt_len, scale, out, q_pos0, vt_seq_stride, \
+                                                 qpos, kslots);                             \
     break;
   switch (gq) {
     GRPO_FLASH(1) GRPO_FLASH(2) GRPO_FLASH(3) GRPO_FLASH(4)
@@ -355,13 +366,14 @@ hipError_t attn_rows_f32(const float* q, const float* kc, const float* vc, const
 
 hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_or_vt, int N,
                         int T, int H, int n_kv, int hd, int k_len, int k_seq_stride, void* out,
-                        hipStream_t st, int q_pos0, int vt_seq_stride, int vt_len_in) {
+                        hipStream_t st, int q_pos0, int vt_seq_stride, int vt_len_in,
+                        const int32_t* qpos, const int32_t* kslots) {
   if (N <= 0 || T <= 0) return hipSuccess;
   const float scale = 1.f / sqrtf((float)hd);
-  // the flash kernel masks only the last key tile of a query block, which needs
-  // query blocks to start at multiples of 32
-  if (q_pos0 < 0 || q_pos0 % 32 || q_pos0 + T > k_len || vt_seq_stride < 1 ||
-      (dtype == 0 && (q_pos0 || vt_seq_stride != 1)))
+  // (per-sequence offsets qpos: the caller guarantees qpos[n] + T <= k_len and
+  // <= vt_len)
+  if (q_pos0 < 0 || q_pos0 + T > k_len || vt_seq_stride < 1 ||
+      (dtype == 0 && (q_pos0 || vt_seq_stride != 1 || qpos || kslots)))
     return hipErrorInvalidValue;
   if (dtype == 0) {
     dim3 grid(N * T, H);
@@ -380,10 +392,10 @@ hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_o
   if (hd == 128)
     return launch_flash<128>(gq, grid, st, (const bf16_t*)q, (const bf16_t*)k,
                              (const bf16_t*)v_or_vt, T, H, n_kv, k_len, k_seq_stride, vt_len,
-                             scale, (bf16_t*)out, q_pos0, vt_seq_stride);
+                             scale, (bf16_t*)out, q_pos0, vt_seq_stride, qpos, kslots);
   return launch_flash<64>(gq, grid, st, (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v_or_vt,
                           T, H, n_kv, k_len, k_seq_stride, vt_len, scale, (bf16_t*)out, q_pos0,
-                          vt_seq_stride);
+                          vt_seq_stride, qpos, kslots);
 }
 
 }  // namespace grpo

@@ -134,7 +134,7 @@ __global__ void k_rope_kv(const float* qkv, int M, T* q_out, RopeArgs a) {
   const int m = (int)(idx / ((size_t)half * heads));
   int seq, pos;
   if (a.mode == 0) { seq = m; pos = a.pos_arr[m]; }
-  else { seq = m / a.T; pos = a.pos0 + m % a.T; }
+  else { seq = m / a.T; pos = (a.pos_arr ? a.pos_arr[seq] : a.pos0) + m % a.T; }
   const int ldq = heads * a.hd;
   const float* src = qkv + (size_t)m * ldq + h * a.hd;
   const bool rotate = h < a.n_heads + a.n_kv;
@@ -186,8 +186,8 @@ __global__ void k_rope_kv(const float* qkv, int M, T* q_out, RopeArgs a) {
   const bool is_v = h >= a.n_heads + a.n_kv;
   const int g = is_v ? h - a.n_heads - a.n_kv : h - a.n_heads;
   T* base = (T*)(is_v ? a.vcache : a.kcache);
-  // mode 0 with a slot map: the row's own cache slot; else slots seq*G .. seq*G+G-1
-  const int slot0 = (a.mode == 0 && a.slots) ? a.slots[m] : seq * a.G;
+  // with a slot map: the sequence's own cache slot; else slots seq*G .. seq*G+G-1
+  const int slot0 = a.slots ? a.slots[seq] : seq * a.G;
   for (int r = 0; base && r < a.G; ++r) {
     const int slot = slot0 + r;
     if (slot < 0 || slot >= a.n_seqs) break;
@@ -267,6 +267,38 @@ struct I32Block {
 };
 __global__ void k_set_i32(int32_t* dst, I32Block b, int n) {
   if ((int)threadIdx.x < n) dst[threadIdx.x] = b.v[threadIdx.x];
+}
+
+// V^T of cached sequences for the prefill/scoring attention: vt[b][g][d][t] =
+// V[slots[b]][g][t][d] for t < pos0[b] + T, 0 up to vt_len.  A workgroup moves a
+// 64-position x hd tile through LDS.
+__global__ __launch_bounds__(256) void k_cache_vt(const bf16_t* vc, const int32_t* slots,
+                                                  const int32_t* pos0, int T, int n_kv,
+                                                  int max_len, int hd, int vt_len, bf16_t* vt) {
+  __shared__ bf16_t tile[64][130];
+  const int p0 = blockIdx.x * 64, g = blockIdx.y, b = blockIdx.z;
+  const int len = pos0[b] + T;
+  const bf16_t* src = vc + ((size_t)slots[b] * n_kv + g) * max_len * hd;
+  for (int e = threadIdx.x; e < 64 * hd; e += 256) {
+    const int p = e / hd, d = e % hd;
+    tile[p][d] = p0 + p < len ? src[(size_t)(p0 + p) * hd + d] : (bf16_t)0;
+  }
+  __syncthreads();
+  bf16_t* dst = vt + ((size_t)b * n_kv + g) * hd * vt_len;
+  for (int e = threadIdx.x; e < 64 * hd; e += 256) {
+    const int d = e / 64, p = e % 64;
+    if (p0 + p < vt_len) dst[(size_t)d * vt_len + p0 + p] = tile[p][d];
+  }
+}
+
+// per-row position and cache slot of B sequences x T rows: row m of sequence b
+// is position pos0[b] + m % T of slot slots[b]
+__global__ void k_row_positions(const int32_t* pos0, const int32_t* slots, int B, int T,
+                                int32_t* row_pos, int32_t* row_slot) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= B * T) return;
+  row_pos[m] = pos0[m / T] + m % T;
+  row_slot[m] = slots[m / T];
 }
 
 __global__ void k_fill_i32(int32_t* p, size_t n, int32_t v) {
@@ -350,6 +382,24 @@ hipError_t trace_rows(const void* src, int layout, int ld, int M, int width, Tra
     return hipErrorInvalidValue;
   Prof pf("trace", st);
   k_trace_rows<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(src, layout, ld, M, width, map, dst);
+  return hipGetLastError();
+}
+
+hipError_t cache_vt(const void* vc, const int32_t* slots, const int32_t* pos0, int B, int T,
+                    int n_kv, int max_len, int hd, int vt_len, uint16_t* vt, hipStream_t st) {
+  if (B <= 0) return hipSuccess;
+  Prof pf("cache_vt", st);
+  k_cache_vt<<<dim3((vt_len + 63) / 64, n_kv, B), 256, 0, st>>>(
+      (const bf16_t*)vc, slots, pos0, T, n_kv, max_len, hd, vt_len, (bf16_t*)vt);
+  return hipGetLastError();
+}
+
+hipError_t row_positions(const int32_t* pos0, const int32_t* slots, int B, int T,
+                         int32_t* row_pos, int32_t* row_slot, hipStream_t st) {
+  const int n = B * T;
+  if (n <= 0) return hipSuccess;
+  Prof pf("row_positions", st);
+  k_row_positions<<<(n + 255) / 256, 256, 0, st>>>(pos0, slots, B, T, row_pos, row_slot);
   return hipGetLastError();
 }
 

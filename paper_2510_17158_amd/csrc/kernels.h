@@ -115,9 +115,17 @@ hipError_t trace_rows(const void* src, int layout, int ld, int M, int width, Tra
 // pos_arr[r] (device array) or, with pos_arr NULL, position r.
 hipError_t rope_table(const int32_t* pos_arr, int rows, int hd, float theta, float2* cs,
                       hipStream_t st);
+// V^T [b][n_kv][hd][vt_len] of cached sequences (slot slots[b]) for positions
+// 0 .. pos0[b] + T - 1, zero beyond (device arrays slots, pos0 of B entries).
+hipError_t cache_vt(const void* vc, const int32_t* slots, const int32_t* pos0, int B, int T,
+                    int n_kv, int max_len, int hd, int vt_len, uint16_t* vt, hipStream_t st);
+// row_pos[m] = pos0[m / T] + m % T, row_slot[m] = slots[m / T] for m < B * T.
+hipError_t row_positions(const int32_t* pos0, const int32_t* slots, int B, int T,
+                         int32_t* row_pos, int32_t* row_slot, hipStream_t st);
 // Rotary embedding + cache write.  qkv fp32 [M, q_dim + 2 kv_dim], or the sum
 // of `splits` such arrays split_stride floats apart (decode GEMM partials).  Row m is
-// (seq, pos): mode 0: seq = m, pos = pos_arr[m];  mode 1: seq = m / T, pos = m % T.
+// (seq, pos): mode 0: seq = m, pos = pos_arr[m];  mode 1: seq = m / T, pos =
+// (pos_arr ? pos_arr[seq] : pos0) + m % T.  slots (optional): cache slot of seq.
 // cs: rope_table rows of pos_arr (mode 0) or of positions 0..T-1 (mode 1).
 // q_out: [M, q_dim] act.  K/V written to cache slots seq*G + g (g < G) at pos
 // (positions >= max_len skipped).  vt (optional, mode 1, M a multiple of T) gets
@@ -126,7 +134,7 @@ hipError_t rope_table(const int32_t* pos_arr, int rows, int hd, float theta, flo
 struct RopeArgs {
   int mode, T, G;
   const int32_t* pos_arr;
-  const int32_t* slots;         // mode 0: cache slot of row m (NULL: m)
+  const int32_t* slots;         // cache slot of sequence seq (NULL: seq * G + g)
   int n_heads, n_kv, hd;
   float theta;
   void* kcache; void* vcache;   // layer base of K and V: [n_seqs][n_kv][max_len][hd]; V may be NULL
@@ -175,13 +183,16 @@ hipError_t attn_rows_f32(const float* q, const float* kc, const float* vc, const
 // Causal attention over N sequences of T rows: q act [N*T, H*hd]; K in cache
 // layout [n][n_kv][k_len][hd] (sequence n at slot n*k_stride_seq), Vt
 // [n][n_kv][hd][T] (bf16 path) or V in cache layout (fp32 path).  out act [N*T, H*hd].
-// bf16 only: q_pos0 (a multiple of 32) is the position of each sequence's first
+// bf16 only: q_pos0 is the position of each sequence's first
 // query row (keys 0 .. q_pos0 + T - 1 are attended), V^T of sequence n at slot
 // n * vt_seq_stride with rows of vt_len positions (0: (q_pos0 + T) rounded up to 8).
+// qpos (optional, bf16): per-sequence first query position (replaces q_pos0);
+// kslots (optional, bf16): cache slot of sequence n's K (replaces n * k_seq_stride).
 hipError_t attn_prefill(int dtype, const void* q, const void* k, const void* v_or_vt, int N,
                         int T, int H, int n_kv, int hd, int k_len, int k_seq_stride,
                         void* out, hipStream_t st, int q_pos0 = 0, int vt_seq_stride = 1,
-                        int vt_len = 0);
+                        int vt_len = 0, const int32_t* qpos = nullptr,
+                        const int32_t* kslots = nullptr);
 
 // ---- sampling / log-probs ---------------------------------------------------------
 // logits fp32 [R, V] (row stride ld).  Row r makes G draws; draw g writes

@@ -171,3 +171,32 @@ def sample_rows(T: int, n_seqs: int, k: int, seed: int = 0, lo: int = 0, hi: int
 def assert_report(rep: Report, label: str):
     say(label, rep.summary())
     assert rep.ok(), rep.summary()
+
+
+def check_extend(cfg, host, tr: dict, kvnp: np.ndarray, pos0, Te: int, slots,
+                 rows=None, rep: Report | None = None):
+    """Rounding-point-local check of a traced grpo_extend: span row r of sequence
+    b = r // Te sits at position pos0[b] + r % Te of cache slot slots[b] and
+    attends that slot's positions 0 .. its own (one matrix-core chain over the
+    keys on bf16 models); the head on each sequence's last span row."""
+    pos0 = np.asarray(pos0)
+    slots = np.asarray(slots)
+    B = len(pos0)
+    M = B * Te
+    rows = np.arange(M) if rows is None else np.asarray(rows)
+    pos = pos0[rows // Te] + rows % Te
+    chk = StageChecker(cfg, host, rep)
+    gem = gemms_rows(cfg, M)
+    segf = f32_segments if cfg.dtype == DTYPE_F32 else flash_segments
+    for l in range(cfg.n_layers):
+        def context(i, l=l):
+            b = rows[i] // Te
+            ctx = int(pos[i]) + 1
+            return (kvnp[l, 0, slots[b], :, :ctx].transpose(1, 0, 2),
+                    kvnp[l, 1, slots[b], :, :ctx].transpose(1, 0, 2))
+        chk.layer(l, tr, rows, pos, context, lambda i: segf(int(pos[i]) + 1), gem)
+    g = F32_GEMM if cfg.dtype == DTYPE_F32 else rows_gemm(B)
+    hrows = np.arange(B)
+    cols = head_cols(cfg.vocab, tr["logits"][hrows])
+    worst = chk.head(tr, hrows, hrows * Te + Te - 1, g, cols=cols, logit_tol=logit_tol(cfg))
+    return chk.rep, worst

@@ -166,6 +166,38 @@ def test_argument_errors_before_device_work():
     L.grpo_model_destroy(h)
 
 
+def test_extend_argument_errors_before_device_work():
+    """grpo_extend checks its host arrays (positions, sequence ids) and the span
+    length before any device work."""
+    L = api.lib()
+    rc, h, keep = _fake_model(get("small").model)
+    s = api.Sampling(1.0, 0, 1)
+    p = C.c_void_p(0x1000)
+    BIG = 1 << 40
+    arr = lambda v: (C.c_int32 * len(v))(*v)  # noqa: E731
+
+    def ext(pos0, ids=None, n_seqs=8, B=4, Te=16, ws_bytes=16, max_len=100):
+        return L.grpo_extend(h, p, n_seqs, max_len, B, ids, arr(pos0), p, Te, 3, C.byref(s), p, p,
+                             None, p, ws_bytes, None)
+    ok = [10, 84, 0, 50]
+    assert ext(ok) == api.WORKSPACE_TOO_SMALL                 # arguments accepted
+    assert ext([10, 85, 0, 50]) == api.KV_CAPACITY             # 85 + 16 > 100
+    assert ext([10, -1, 0, 50]) == api.INVALID_ARG
+    assert b"negative" in L.grpo_last_error()
+    assert ext(ok, Te=0) == api.INVALID_ARG
+    assert ext(ok, Te=api.EXTEND_CHUNK + 1, max_len=2000) == api.INVALID_ARG
+    assert ext(ok, n_seqs=3) == api.INVALID_ARG                # B > n_seqs without ids
+    assert ext(ok, ids=arr([7, 0, 3, 5])) == api.WORKSPACE_TOO_SMALL
+    assert ext(ok, ids=arr([7, 0, 3, 7])) == api.INVALID_ARG
+    assert b"repeats" in L.grpo_last_error()
+    assert ext(ok, ids=arr([7, 0, 3, 8])) == api.INVALID_ARG
+    assert L.grpo_extend(h, p, 8, 100, 4, None, None, p, 16, 3, C.byref(s), p, p, None, p, BIG,
+                         None) == api.INVALID_ARG
+    need = L.grpo_workspace_bytes(h, api.OP_EXTEND, 4, 100)
+    assert need > 0 and ext(ok, ws_bytes=need - 1) == api.WORKSPACE_TOO_SMALL
+    L.grpo_model_destroy(h)
+
+
 def test_decode_structure_query():
     """The reduction structure the tests' error bounds use comes from the library's
     own planner; its arguments are checked."""

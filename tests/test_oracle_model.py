@@ -169,3 +169,45 @@ def test_layer_truncation_and_hidden_states():
     logits, _, hidden = om.forward(tokens, return_hidden=True)
     assert len(hidden) == cfg.n_layers + 1
     np.testing.assert_allclose(om.head(hidden[-1]), logits, rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("dtype", [DTYPE_F32, DTYPE_BF16])
+def test_extend_then_decode_equals_full_forward(dtype):
+    """A tool-output span appended to a cached sequence, then decode steps after
+    it, give the logits and K/V of one full forward over the concatenated
+    tokens (fp64, 1e-12): prompt prefill, 3 decode steps, a 7-token injected
+    span, 2 more decode steps."""
+    cfg = dataclasses.replace(MICRO, dtype=dtype)
+    w = synth.make_weights(cfg, 21, gain_noise=0.1, std=0.2)
+    om = OracleModel(cfg, w, round_points=(dtype == DTYPE_BF16))
+    rng = np.random.default_rng(4)
+    prompt = rng.integers(0, cfg.vocab, 6)
+    gen1 = rng.integers(0, cfg.vocab, 3)
+    span = rng.integers(0, cfg.vocab, 7)
+    gen2 = rng.integers(0, cfg.vocab, 2)
+    seq = np.concatenate([prompt, gen1, span, gen2])
+    full, kv_full = om.forward(seq)
+    L, Hk, hd = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim
+    Tmax = len(seq)
+    K = np.zeros((L, 1, Hk, Tmax, hd))
+    V = np.zeros_like(K)
+    lg, kvp = om.forward(prompt)
+    for l in range(L):
+        K[l, 0, :, :6], V[l, 0, :, :6] = kvp[l]
+    logits = [lg[-1]]
+    pos = 6
+    for t in gen1:
+        logits.append(om.decode(np.array([t]), np.array([pos]), K, V)[0])
+        pos += 1
+    # the span: its own rows' logits; the last row's is the next-token logit
+    ls = om.extend(span, pos, K[:, 0], V[:, 0])
+    np.testing.assert_allclose(ls, full[pos:pos + len(span)], rtol=0, atol=1e-12)
+    pos += len(span)
+    for t in gen2:
+        logits.append(om.decode(np.array([t]), np.array([pos]), K, V)[0])
+        pos += 1
+    want = np.concatenate([full[5:9], full[len(prompt) + 3 + len(span):]])
+    np.testing.assert_allclose(np.stack(logits), want, rtol=0, atol=1e-12)
+    for l in range(L):
+        np.testing.assert_allclose(K[l, 0], kv_full[l][0], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(V[l, 0], kv_full[l][1], rtol=0, atol=1e-12)
