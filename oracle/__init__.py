@@ -5,8 +5,9 @@ HIP path computes: the Llama-family decoder forward the paper fine-tunes
 (Sec. VI-C), counter-based sampling of a group of K rollouts per prompt
 (Alg. 1, sampling step), teacher-forced scoring of the sampled completions
 (log pi(x|c) in Eq. 1), group-normalised advantages (Alg. 1, normalisation
-step) and the clipped-ratio + KL token loss (Eq. 1 in the clipped GRPO form the
-paper keeps, Sec. VI-A).
+step), the clipped-ratio + KL token loss (Eq. 1 in the clipped GRPO form the
+paper keeps, Sec. VI-A), and the gradient step that closes each iteration
+(Alg. 1: the weight gradient of the scored log-probs, AdamW).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  It imports nothing from the HIP
@@ -24,10 +25,12 @@ from .sampler import sample_token, topk_set, log_softmax
 from .model import OracleModel
 from .grpo import advantages, token_loss
 from .distill import exact_kl, reward, sft_loss
+from .backward import adamw, policy_gradient
 
 __all__ = [
     "bf16_bits_to_f64", "round_bf16", "rmsnorm", "silu", "rope",
     "philox4x32_10", "philox_uniform24", "gumbel_keys",
     "sample_token", "topk_set", "log_softmax",
     "OracleModel", "advantages", "token_loss", "reward", "sft_loss", "exact_kl",
+    "policy_gradient", "adamw",
 ]
