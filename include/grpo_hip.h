@@ -67,7 +67,7 @@ enum grpo_dtype { GRPO_F32 = 0, GRPO_BF16 = 1 };
 /* Workspace kinds for grpo_workspace_bytes. */
 enum grpo_op {
   GRPO_OP_PREFILL = 0, GRPO_OP_ROLLOUT = 1, GRPO_OP_SCORE = 2, GRPO_OP_LOSS = 3,
-  GRPO_OP_EXTEND = 4
+  GRPO_OP_EXTEND = 4, GRPO_OP_BACKWARD = 5
 };
 
 /* Decoder shape.  Llama family: RMSNorm, RoPE (half-split pairs (i, i+hd/2),
@@ -185,7 +185,8 @@ size_t grpo_kv_cache_bytes(const grpo_config* cfg, int32_t n_seqs, int32_t max_l
  *   GRPO_OP_ROLLOUT: n_rows = batch B,   seq_len = KV capacity max_len
  *   GRPO_OP_SCORE:   n_rows = sequences N, seq_len = T
  *   GRPO_OP_EXTEND:  n_rows = batch B,   seq_len = KV capacity max_len
- *   GRPO_OP_LOSS:    n_rows = sequences N, seq_len = Tr (model may be NULL) */
+ *   GRPO_OP_LOSS:    n_rows = sequences N, seq_len = Tr (model may be NULL)
+ *   GRPO_OP_BACKWARD: n_rows = sequences N, seq_len = T (at most 16384) */
 size_t grpo_workspace_bytes(const grpo_model* m, int32_t op, int32_t n_rows, int32_t seq_len);
 
 /* Thread-local message of the last failed call on this thread ("" if none). */
@@ -357,6 +358,55 @@ int grpo_reward(const uint8_t* correct, const double* t_base, const double* t,
  * workspace is grpo_workspace_bytes(GRPO_OP_LOSS, N, Tr). */
 int grpo_sft_loss(const float* logp, const uint8_t* mask, int32_t N, int32_t Tr, int32_t agg,
                   float* loss_out, float* dloss_dlogp, void* ws, size_t ws_bytes, void* stream);
+
+/* fp32 gradient accumulators, one per weight of grpo_weights with the same
+ * shape (row-major).  The backward ADDS into them; the caller zeroes them at
+ * the start of an accumulation. */
+typedef struct grpo_grads {
+  float* tok_emb;
+  float* const* attn_norm; float* const* wq; float* const* wk; float* const* wv;
+  float* const* wo; float* const* mlp_norm; float* const* w_gate; float* const* w_up;
+  float* const* w_down;
+  float* final_norm;
+  float* lm_head;
+} grpo_grads;
+
+/* Gradient step of Alg. 1, first half: the weight gradient of the GRPO
+ * objective (Eq. 1, clipped form of Sec. VI-A).  The objective reaches the
+ * weights only through the scored log-probs, so given g = dL/dlogp (the
+ * dloss_dlogp output of grpo_token_loss, fp32 [N, T - score_from] device) this
+ * accumulates into `grads` the gradient of sum_{n,j} g[n, j] logp[n, j], with
+ * logp as grpo_score_sequences defines it (tokens int32 [N, T] device, the
+ * same score_from and temperature):
+ *   dz_t = g_t / T (onehot(x_{t+1}) - softmax(z_t / T)) on each scored row,
+ * then back through the LM head, the final RMSNorm, every layer in reverse and
+ * the embedding gather.  Each sequence's forward is recomputed (its layer
+ * inputs kept), the rounding points of the bf16 forward pass gradients
+ * straight through.  Gradients accumulate in fp32; data-gradient operands are
+ * the model dtype (bf16 products on the matrix cores).  The embedding rows are
+ * added with fp32 atomics (order not fixed); every other sum has a fixed order.
+ * Workspace: grpo_workspace_bytes(GRPO_OP_BACKWARD, N, T) (it holds transposed
+ * copies of every weight matrix).  GRPO_INVALID_ARG for a NULL gradient buffer
+ * or score_from outside [1, T); GRPO_UNSUPPORTED for T above 16384. */
+int grpo_policy_backward(const grpo_model* m, const int32_t* tokens, int32_t N, int32_t T,
+                         int32_t score_from, float temperature, const float* dlogp,
+                         const grpo_grads* grads, void* ws, size_t ws_bytes, void* stream);
+
+/* AdamW hyper-parameters (decoupled weight decay). */
+typedef struct grpo_adamw {
+  float lr, beta1, beta2, eps, weight_decay;
+} grpo_adamw;
+
+/* Gradient step of Alg. 1, second half (the paper names no optimizer; AdamW
+ * with bias correction): over n elements of one parameter tensor,
+ *   m = b1 m + (1 - b1) g,  v = b2 v + (1 - b2) g^2,
+ *   p = p - lr wd p - lr (m / (1 - b1^step)) / (sqrt(v / (1 - b2^step)) + eps)
+ * step counts from 1.  dtype GRPO_F32: param is the fp32 tensor itself and
+ * master may be NULL; GRPO_BF16: master (fp32) is updated and param receives
+ * its bf16 rounding.  m, v, grad fp32 device arrays of n entries. */
+int grpo_adamw_step(int32_t dtype, void* param, float* master, float* m, float* v,
+                    const float* grad, size_t n, const grpo_adamw* hp, int32_t step,
+                    void* stream);
 
 /* Exact full-vocabulary KL of the policy to the frozen reference (Alg. 1, KL
  * step; the GRPO loss uses its per-token estimator): for each of R rows,

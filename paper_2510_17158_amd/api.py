@@ -19,7 +19,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgrpo_hip.so")
 
 OK, INVALID_ARG, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP_ERROR, KV_CAPACITY = 0, -1, -2, -3, -4, -5
-OP_PREFILL, OP_ROLLOUT, OP_SCORE, OP_LOSS, OP_EXTEND = 0, 1, 2, 3, 4
+OP_PREFILL, OP_ROLLOUT, OP_SCORE, OP_LOSS, OP_EXTEND, OP_BACKWARD = 0, 1, 2, 3, 4, 5
 EXTEND_CHUNK = 512
 
 
@@ -43,6 +43,15 @@ class Weights(C.Structure):
     _fields_ = [("tok_emb", C.c_void_p), ("attn_norm", _PP), ("wq", _PP), ("wk", _PP),
                 ("wv", _PP), ("wo", _PP), ("mlp_norm", _PP), ("w_gate", _PP), ("w_up", _PP),
                 ("w_down", _PP), ("final_norm", C.c_void_p), ("lm_head", C.c_void_p)]
+
+
+class GradsStruct(C.Structure):
+    _fields_ = Weights._fields_
+
+
+class AdamW(C.Structure):
+    _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
+                ("weight_decay", C.c_float)]
 
 
 class Sampling(C.Structure):
@@ -144,6 +153,9 @@ _SIGS = {
     "grpo_reward": (_I32, [_VP, _VP, _VP, _VP, _VP, _I32, _VP]),
     "grpo_sft_loss": (_I32, [_VP, _VP, _I32, _I32, _I32, _VP, _VP, _VP, _SZ, _VP]),
     "grpo_exact_kl": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _VP, _VP]),
+    "grpo_policy_backward": (_I32, [_VP, _VP, _I32, _I32, _I32, _F32, _VP, C.POINTER(GradsStruct),
+                                     _VP, _SZ, _VP]),
+    "grpo_adamw_step": (_I32, [_I32, _VP, _VP, _VP, _VP, _VP, _SZ, C.POINTER(AdamW), _I32, _VP]),
     "grpo_profile_begin": (_I32, []),
     "grpo_profile_end": (_I32, [C.c_char_p, _SZ]),
 }
@@ -410,3 +422,45 @@ def profile_end() -> dict:
     buf = C.create_string_buffer(1 << 16)
     _check(lib().grpo_profile_end(buf, len(buf)))
     return {k: tuple(v) for k, v in json.loads(buf.value.decode()).items()}
+
+
+# ---- gradient step ------------------------------------------------------------------
+WEIGHT_NAMES_LAYER = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down")
+
+
+class Grads:
+    """fp32 gradient accumulators shaped like a model's weights (zeroed)."""
+
+    def __init__(self, model: "Model"):
+        self.t = {k: torch.zeros(v.shape, dtype=torch.float32, device=v.device)
+                  for k, v in model.weights.items()}
+        L = model.cfg.n_layers
+        self._arrays = {n: (C.c_void_p * L)(*[_ptr(self.t[f"l{i}.{n}"]) for i in range(L)])
+                        for n in WEIGHT_NAMES_LAYER}
+        self.struct = GradsStruct(_ptr(self.t["tok_emb"]),
+                                  *[C.cast(self._arrays[n], _PP) for n in WEIGHT_NAMES_LAYER],
+                                  _ptr(self.t["final_norm"]), _ptr(self.t["lm_head"]))
+
+    def zero_(self):
+        for v in self.t.values():
+            v.zero_()
+
+
+def policy_backward(model: "Model", tokens, score_from: int, temperature: float, dlogp,
+                    grads: Grads, ws=None, stream=None):
+    """grpo_policy_backward: tokens int32 [N, T], dlogp fp32 [N, T - score_from] (device)."""
+    N, T = tokens.shape
+    if ws is None:
+        ws = alloc_workspace(model, OP_BACKWARD, N, T)
+    _check(lib().grpo_policy_backward(model.handle, _ptr(tokens), N, T, score_from, temperature,
+                                      _ptr(dlogp), C.byref(grads.struct), _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+
+
+def adamw_step(dtype: int, param, master, m, v, grad, lr: float, beta1: float, beta2: float,
+               eps: float, weight_decay: float, step: int, stream=None):
+    """grpo_adamw_step over one tensor (master None for fp32 parameters)."""
+    hp = AdamW(lr, beta1, beta2, eps, weight_decay)
+    _check(lib().grpo_adamw_step(dtype, _ptr(param), _ptr(master) if master is not None else None,
+                                 _ptr(m), _ptr(v), _ptr(grad), grad.numel(), C.byref(hp), step,
+                                 _stream(stream)))

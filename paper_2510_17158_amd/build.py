@@ -20,7 +20,7 @@ ARCH = "gfx950"
 
 SOURCES = ["api.cpp", "gemm_decode.hip", "gemm_tiled.hip", "elementwise.hip", "attention.hip",
            "attn_decode.hip",
-           "sampler.hip", "grpo.hip"]
+           "sampler.hip", "grpo.hip", "backward.hip"]
 
 COMMON_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

@@ -150,6 +150,7 @@ int decode_target() {
   return v;
 }
 constexpr int kScoreTokens = 131072;   // rows per scoring chunk (sequences * T)
+constexpr int kBackwardTokens = 16384; // longest sequence of the backward pass
 constexpr size_t kLogitBytes = size_t(1) << 30;  // LM-head logits per scoring sub-chunk
 
 // bump allocator over the caller's workspace; base == nullptr only measures
@@ -520,6 +521,214 @@ int check_sampling(const grpo_sampling* s, int vocab) {
   return GRPO_OK;
 }
 
+// ---- backward pass (grpo_policy_backward) ----------------------------------------
+constexpr size_t kAttnBwdBytes = size_t(2) << 30;   // per-head attention scratch per batch
+constexpr size_t kHeadBwdBytes = size_t(1) << 30;   // LM-head logits per row chunk
+int round64(int t) { return (t + 63) / 64 * 64; }
+
+struct BackwardWS {
+  int Tp, hb, head_rows;
+  float* X;                       // (L + 1) x [T, d] residual stream checkpoints
+  void* h; float* qkv; void* q; void* kb; void* vb; uint16_t* vt; void* o;
+  float* xa; void* h2; float* gu; void* a; float2* cs;
+  float* dx; float* dxa; void* dxe; float* da; void* dgu; float* dh; float* dof; void* doe;
+  float* dqkv; void* dqkve; float* rr; float* part;
+  void* tA; void* tB;             // transposed gradient / activation operands [rows][Tp]
+  float* S; float* dP; void* P; void* dS; void* PT; void* dST; void* qT; void* doT; void* kT;
+  float* tk; float* tv;           // per-head dk, dv before the sum over each group
+  void* hf; float* z; void* dz; void* dzT; void* hfT; float* dhf;
+  std::vector<void*> WdT, WguT, WoT, WqkvT;
+  void* WheadT;
+};
+
+BackwardWS take_backward(Bump& b, const grpo_config& c, int T) {
+  BackwardWS w;
+  const int es = esize(c), d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn;
+  const int ldqkv = qd + 2 * kvd, hd = c.head_dim, V = c.vocab, L = c.n_layers;
+  const int gq = c.n_heads / c.n_kv_heads;
+  const int Tp = round64(T);
+  w.Tp = Tp;
+  const size_t TT = (size_t)T * Tp, PP = (size_t)Tp * Tp;
+  const size_t per_head = TT * (8 + 2 * es) + PP * 2 * es + (size_t)hd * Tp * 2 * es +
+                          (size_t)T * hd * 8;
+  int groups = (int)std::max<size_t>(1, kAttnBwdBytes / (per_head * gq));
+  groups = std::min(groups, c.n_kv_heads);
+  while (c.n_kv_heads % groups) --groups;
+  w.hb = groups * gq;
+  w.head_rows = (int)std::max<size_t>(64, std::min<size_t>((size_t)T, kHeadBwdBytes / ((size_t)V * (4 + 2 * es))));
+  w.head_rows = std::max(64, w.head_rows / 64 * 64);
+  const int R = w.head_rows, Rp = round64(R);
+  w.X = b.take<float>((size_t)(L + 1) * T * d);
+  w.h = b.take<char>((size_t)T * d * es);
+  w.qkv = b.take<float>((size_t)T * ldqkv);
+  w.q = b.take<char>((size_t)T * qd * es);
+  w.kb = b.take<char>((size_t)kvd * Tp * es);
+  w.vb = b.take<char>((size_t)kvd * Tp * es);
+  w.vt = b.take<uint16_t>(c.dtype == GRPO_F32 ? 0 : (size_t)kvd * round8(T));
+  w.o = b.take<char>((size_t)T * qd * es);
+  w.xa = b.take<float>((size_t)T * d);
+  w.h2 = b.take<char>((size_t)T * d * es);
+  w.gu = b.take<float>((size_t)T * 2 * f);
+  w.a = b.take<char>((size_t)T * f * es);
+  w.cs = b.take<float2>((size_t)T * (hd / 2));
+  w.dx = b.take<float>((size_t)T * d);
+  w.dxa = b.take<float>((size_t)T * d);
+  w.dxe = b.take<char>((size_t)T * d * es);
+  w.da = b.take<float>((size_t)T * f);
+  w.dgu = b.take<char>((size_t)T * 2 * f * es);
+  w.dh = b.take<float>((size_t)T * std::max(d, R > 0 ? d : d));
+  w.dof = b.take<float>((size_t)T * qd);
+  w.doe = b.take<char>((size_t)T * qd * es);
+  w.dqkv = b.take<float>((size_t)T * ldqkv);
+  w.dqkve = b.take<char>((size_t)T * ldqkv * es);
+  w.rr = b.take<float>((size_t)std::max(T, R));
+  w.part = b.take<float>((size_t)((std::max(T, R) + 63) / 64) * d);
+  const int rowsA = std::max(std::max(2 * f, ldqkv), d);
+  const int rowsB = std::max(std::max(f, d), qd);
+  w.tA = b.take<char>((size_t)rowsA * Tp * es);
+  w.tB = b.take<char>((size_t)rowsB * Tp * es);
+  const int hb = w.hb;
+  w.S = b.take<float>(hb * TT);
+  w.dP = b.take<float>(hb * TT);
+  w.P = b.take<char>(hb * TT * es);
+  w.dS = b.take<char>(hb * TT * es);
+  w.PT = b.take<char>(hb * PP * es);
+  w.dST = b.take<char>(hb * PP * es);
+  w.qT = b.take<char>((size_t)hb * hd * Tp * es);
+  w.doT = b.take<char>((size_t)hb * hd * Tp * es);
+  w.kT = b.take<char>((size_t)c.n_kv_heads * hd * Tp * es);
+  w.tk = b.take<float>((size_t)hb * T * hd);
+  w.tv = b.take<float>((size_t)hb * T * hd);
+  w.hf = b.take<char>((size_t)R * d * es);
+  w.z = b.take<float>((size_t)R * V);
+  w.dz = b.take<char>((size_t)R * V * es);
+  w.dzT = b.take<char>((size_t)V * Rp * es);
+  w.hfT = b.take<char>((size_t)d * Rp * es);
+  w.dhf = b.take<float>((size_t)R * d);
+  for (int l = 0; l < L; ++l) {
+    w.WdT.push_back(b.take<char>((size_t)f * d * es));
+    w.WguT.push_back(b.take<char>((size_t)d * 2 * f * es));
+    w.WoT.push_back(b.take<char>((size_t)qd * d * es));
+    w.WqkvT.push_back(b.take<char>((size_t)d * ldqkv * es));
+  }
+  w.WheadT = b.take<char>((size_t)d * V * es);
+  return w;
+}
+
+int gemm_bt(const grpo_model* m, const void* X, int ldx, int M, WStack W, int N, int K, int epi,
+            EpiArgs ep, GemmBatch bt, hipStream_t st) {
+  const hipError_t e =
+      m->cfg.dtype == GRPO_F32
+          ? gemm_f32((const float*)X, ldx, M, W, N, K, epi, ep, st, bt)
+          : gemm_tiled_bf16((const uint16_t*)X, ldx, M, W, N, K, epi, ep, st, bt);
+  return e == hipSuccess ? GRPO_OK : gemm_fail(e);
+}
+
+// transposed copy of rows [N, K] (the model dtype) as [K, N]
+hipError_t transpose_w(const grpo_config& c, const void* w, int N, int K, void* out, int ldo,
+                       hipStream_t st) {
+  const int t = c.dtype == GRPO_F32 ? 0 : 1;
+  return transpose(t, t, w, K, 0, N, K, out, ldo, 0, 0, 1, N, 1, st);
+}
+
+// one layer's forward over a sequence from its input x [T, d]: h, q, K/V (kb, vb
+// [n_kv][Tp][hd]), o, xa, h2, gate|up (gu) and a; x_out (optional) = xa + a Wd^T
+int layer_fwd(const grpo_model* m, BackwardWS& w, int l, const float* x, int T, float* x_out,
+              hipStream_t st) {
+  const grpo_config& c = m->cfg;
+  const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn, ldqkv = qd + 2 * kvd;
+  const Partials none{nullptr, 0, 0, d};
+  int rc;
+  HIPCHK(rmsnorm(c.dtype, const_cast<float*>(x), d, RowMap::identity(), none, m->attn_norm[l], T,
+                 d, c.rms_eps, w.h, d, st));
+  if ((rc = gemm_rows(m, w.h, d, T, qkv_stack(m, l), ldqkv, d, EPI_STORE,
+                      EpiArgs{w.qkv, nullptr, ldqkv}, st)))
+    return rc;
+  RopeArgs ra{};
+  ra.mode = 1; ra.T = T; ra.G = 1; ra.pos_arr = nullptr; ra.pos0 = 0;
+  ra.n_heads = c.n_heads; ra.n_kv = c.n_kv_heads; ra.hd = c.head_dim; ra.theta = c.rope_theta;
+  ra.kcache = w.kb; ra.vcache = w.vb; ra.n_seqs = 1; ra.max_len = w.Tp;
+  ra.vt = c.dtype == GRPO_F32 ? nullptr : w.vt; ra.vt_len = round8(T);
+  ra.splits = 1; ra.split_stride = 0; ra.cs = w.cs;
+  HIPCHK(rope_kv(c.dtype, w.qkv, T, w.q, ra, st));
+  HIPCHK(attn_prefill(c.dtype, w.q, w.kb, c.dtype == GRPO_F32 ? w.vb : (const void*)w.vt, 1, T,
+                      c.n_heads, c.n_kv_heads, c.head_dim, w.Tp, 1, w.o, st, 0, 1, round8(T)));
+  HIPCHK(hipMemcpyAsync(w.xa, x, (size_t)T * d * 4, hipMemcpyDeviceToDevice, st));
+  if ((rc = gemm_rows(m, w.o, qd, T, one(m->wo[l]), d, qd, EPI_RESID, EpiArgs{w.xa, nullptr, d},
+                      st)))
+    return rc;
+  HIPCHK(rmsnorm(c.dtype, w.xa, d, RowMap::identity(), none, m->mlp_norm[l], T, d, c.rms_eps,
+                 w.h2, d, st));
+  if ((rc = gemm_rows(m, w.h2, d, T, gate_up(m, l), 2 * f, d, EPI_STORE,
+                      EpiArgs{w.gu, nullptr, 2 * f}, st)))
+    return rc;
+  HIPCHK(swiglu_fwd(c.dtype, w.gu, T, f, w.a, st));
+  if (!x_out) return GRPO_OK;
+  HIPCHK(hipMemcpyAsync(x_out, w.xa, (size_t)T * d * 4, hipMemcpyDeviceToDevice, st));
+  return gemm_rows(m, w.a, f, T, one(m->w_down[l]), d, f, EPI_RESID, EpiArgs{x_out, nullptr, d}, st);
+}
+
+// dW[N, K] += dY^T X over T token rows: dY [T, N] (fp32 or the model dtype, ld
+// ldy), X [T, K] (the model dtype, ld ldx); both transposed into [.][Tp] first
+int wgrad(const grpo_model* m, BackwardWS& w, const void* dY, int dy_f32, int ldy, int N,
+          const void* X, int ldx, int K, int T, float* dW, hipStream_t st) {
+  const grpo_config& c = m->cfg;
+  const int e = c.dtype == GRPO_F32 ? 0 : 1;
+  HIPCHK(transpose(dy_f32 ? 0 : e, e, dY, ldy, 0, T, N, w.tA, w.Tp, 0, 0, 1, w.Tp, 1, st));
+  HIPCHK(transpose(e, e, X, ldx, 0, T, K, w.tB, w.Tp, 0, 0, 1, w.Tp, 1, st));
+  return gemm_rows(m, w.tA, w.Tp, N, one(w.tB), K, w.Tp, EPI_RESID, EpiArgs{dW, nullptr, K}, st);
+}
+
+// attention backward of one sequence: do (w.doe) -> dq, dk, dv in w.dqkv
+int attn_bwd(const grpo_model* m, BackwardWS& w, int T, hipStream_t st) {
+  const grpo_config& c = m->cfg;
+  const int H = c.n_heads, Hk = c.n_kv_heads, hd = c.head_dim, gq = H / Hk;
+  const int qd = qdim(c), kvd = kvdim(c), ldqkv = qd + 2 * kvd, Tp = w.Tp, es = esize(c);
+  const int e = c.dtype == GRPO_F32 ? 0 : 1;
+  const size_t TT = (size_t)T * Tp, PP = (size_t)Tp * Tp, hT = (size_t)hd * Tp;
+  const float scale = 1.f / sqrtf((float)hd);
+  char* kb = (char*)w.kb;
+  char* vb = (char*)w.vb;
+  int rc;
+  // K^T of every kv head [n_kv][hd][Tp]
+  HIPCHK(transpose(e, e, w.kb, hd, (size_t)Tp * hd, T, hd, w.kT, Tp, hT, 0, 1, Tp, Hk, st));
+  for (int h0 = 0; h0 < H; h0 += w.hb) {
+    const int nb = std::min(w.hb, H - h0), g0 = h0 / gq;
+    // S = q_h k_g^T, dP = do_h v_g^T (raw products, fp32)
+    GemmBatch sb{nb, (size_t)hd, (size_t)Tp * hd, TT, gq};
+    if ((rc = gemm_bt(m, (char*)w.q + (size_t)h0 * hd * es, qd, T,
+                      one(kb + (size_t)g0 * Tp * hd * es), T, hd, EPI_STORE,
+                      EpiArgs{w.S, nullptr, Tp}, sb, st)))
+      return rc;
+    if ((rc = gemm_bt(m, (char*)w.doe + (size_t)h0 * hd * es, qd, T,
+                      one(vb + (size_t)g0 * Tp * hd * es), T, hd, EPI_STORE,
+                      EpiArgs{w.dP, nullptr, Tp}, sb, st)))
+      return rc;
+    HIPCHK(attn_softmax_bwd(c.dtype, w.S, w.dP, T, Tp, nb, scale, w.P, w.dS, st));
+    // dq_h = dS'_h k_g (K = key positions)
+    GemmBatch qb{nb, TT, hT, (size_t)hd, gq};
+    if ((rc = gemm_bt(m, w.dS, Tp, T, one((char*)w.kT + (size_t)g0 * hT * es), hd, Tp, EPI_STORE,
+                      EpiArgs{w.dqkv + (size_t)h0 * hd, nullptr, ldqkv}, qb, st)))
+      return rc;
+    // per head: dk_h = dS'_h^T q_h, dv_h = P_h^T do_h (K = query positions)
+    HIPCHK(transpose(e, e, w.dS, Tp, TT, T, Tp, w.dST, Tp, PP, 0, 1, Tp, nb, st));
+    HIPCHK(transpose(e, e, w.P, Tp, TT, T, Tp, w.PT, Tp, PP, 0, 1, Tp, nb, st));
+    HIPCHK(transpose(e, e, (char*)w.q + (size_t)h0 * hd * es, qd, hd, T, hd, w.qT, Tp, hT, 0, 1,
+                     Tp, nb, st));
+    HIPCHK(transpose(e, e, (char*)w.doe + (size_t)h0 * hd * es, qd, hd, T, hd, w.doT, Tp, hT, 0,
+                     1, Tp, nb, st));
+    GemmBatch kb2{nb, PP, hT, (size_t)T * hd, 1};
+    if ((rc = gemm_bt(m, w.dST, Tp, T, one(w.qT), hd, Tp, EPI_STORE, EpiArgs{w.tk, nullptr, hd},
+                      kb2, st)) ||
+        (rc = gemm_bt(m, w.PT, Tp, T, one(w.doT), hd, Tp, EPI_STORE, EpiArgs{w.tv, nullptr, hd},
+                      kb2, st)))
+      return rc;
+    HIPCHK(sum_heads(w.tk, T, hd, gq, nb / gq, w.dqkv + qd + (size_t)g0 * hd, ldqkv, st));
+    HIPCHK(sum_heads(w.tv, T, hd, gq, nb / gq, w.dqkv + qd + kvd + (size_t)g0 * hd, ldqkv, st));
+  }
+  return GRPO_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -691,6 +900,10 @@ size_t grpo_workspace_bytes(const grpo_model* m, int32_t op, int32_t n_rows, int
     case GRPO_OP_ROLLOUT: take_rollout(b, m->cfg, n_rows, seq_len); break;
     case GRPO_OP_SCORE: take_score(b, m->cfg, n_rows, seq_len); break;
     case GRPO_OP_EXTEND: take_extend(b, m->cfg, n_rows, seq_len); break;
+    case GRPO_OP_BACKWARD:
+      if (seq_len < 2 || seq_len > kBackwardTokens) return 0;
+      take_backward(b, m->cfg, seq_len);
+      break;
     default: return 0;
   }
   return b.off;
@@ -1345,6 +1558,152 @@ int grpo_token_loss(const float* logp, const float* logp_old, const float* logp_
     return fail(GRPO_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
   HIPCHK(token_loss(logp, logp_old, logp_ref, mask, adv, N, Tr, clip_eps, beta, agg, loss_out,
                     tok_loss, dloss_dlogp, stats, (double*)ws, (hipStream_t)stream));
+  g_err.clear();
+  return GRPO_OK;
+}
+
+int grpo_policy_backward(const grpo_model* m, const int32_t* tokens, int32_t N, int32_t T,
+                         int32_t score_from, float temperature, const float* dlogp,
+                         const grpo_grads* g, void* ws, size_t ws_bytes, void* stream) {
+  if (!m) return fail(GRPO_INVALID_ARG, "model is NULL");
+  const grpo_config& c = m->cfg;
+  if (!tokens || !dlogp || !g || !ws) return fail(GRPO_INVALID_ARG, "tokens, dlogp, g and ws must be set");
+  if (N < 1 || T < 2) return fail(GRPO_INVALID_ARG, "N must be >= 1 and T >= 2");
+  if (score_from < 1 || score_from >= T)
+    return fail(GRPO_INVALID_ARG, "score_from %d outside [1, T)", score_from);
+  if (!(temperature >= 0.f) || temperature == INFINITY)
+    return fail(GRPO_INVALID_ARG, "temperature must be finite and >= 0");
+  if (T > kBackwardTokens) return fail(GRPO_UNSUPPORTED, "T above %d", kBackwardTokens);
+  if (c.n_heads % c.n_kv_heads) return fail(GRPO_UNSUPPORTED, "n_heads not a multiple of n_kv_heads");
+  if (!g->tok_emb || !g->final_norm || !g->lm_head || !g->attn_norm || !g->wq || !g->wk ||
+      !g->wv || !g->wo || !g->mlp_norm || !g->w_gate || !g->w_up || !g->w_down)
+    return fail(GRPO_INVALID_ARG, "every gradient buffer must be set");
+  for (int l = 0; l < c.n_layers; ++l)
+    if (!g->attn_norm[l] || !g->wq[l] || !g->wk[l] || !g->wv[l] || !g->wo[l] || !g->mlp_norm[l] ||
+        !g->w_gate[l] || !g->w_up[l] || !g->w_down[l])
+      return fail(GRPO_INVALID_ARG, "gradient buffers of layer %d must be set", l);
+  const size_t need = grpo_workspace_bytes(m, GRPO_OP_BACKWARD, N, T);
+  if (ws_bytes < need)
+    return fail(GRPO_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
+  hipStream_t st = (hipStream_t)stream;
+  Bump b(ws);
+  BackwardWS w = take_backward(b, c, T);
+  const int d = c.d_model, qd = qdim(c), kvd = kvdim(c), f = c.d_ffn, ldqkv = qd + 2 * kvd;
+  const int V = c.vocab, L = c.n_layers, Ts = T - score_from, Tp = w.Tp, es = esize(c);
+  const int e = c.dtype == GRPO_F32 ? 0 : 1;
+  const Partials none{nullptr, 0, 0, d};
+  int rc;
+  // transposed weights, once per call: the data gradients' W operands
+  for (int l = 0; l < L; ++l) {
+    HIPCHK(transpose_w(c, m->w_down[l], d, f, w.WdT[l], d, st));
+    HIPCHK(transpose_w(c, m->w_gate[l], f, d, w.WguT[l], 2 * f, st));
+    HIPCHK(transpose_w(c, m->w_up[l], f, d, (char*)w.WguT[l] + (size_t)f * es, 2 * f, st));
+    HIPCHK(transpose_w(c, m->wo[l], d, qd, w.WoT[l], d, st));
+    HIPCHK(transpose_w(c, m->wq[l], qd, d, w.WqkvT[l], ldqkv, st));
+    HIPCHK(transpose_w(c, m->wk[l], kvd, d, (char*)w.WqkvT[l] + (size_t)qd * es, ldqkv, st));
+    HIPCHK(transpose_w(c, m->wv[l], kvd, d, (char*)w.WqkvT[l] + (size_t)(qd + kvd) * es, ldqkv, st));
+  }
+  HIPCHK(transpose_w(c, m->lm_head, V, d, w.WheadT, V, st));
+  HIPCHK(rope_table(nullptr, T, c.head_dim, c.rope_theta, w.cs, st));
+  const size_t Td = (size_t)T * d;
+  for (int n = 0; n < N; ++n) {
+    const int32_t* tk = tokens + (size_t)n * T;
+    const float* gn = dlogp + (size_t)n * Ts;
+    // forward, keeping every layer's input
+    HIPCHK(embed(c.dtype, m->tok_emb, tk, T, d, V, w.X, st));
+    for (int l = 0; l < L; ++l)
+      if ((rc = layer_fwd(m, w, l, w.X + l * Td, T, w.X + (l + 1) * Td, st))) return rc;
+    // head: scored rows score_from - 1 .. T - 2 in chunks
+    const float* xL = w.X + L * Td;
+    HIPCHK(fill_f32(w.dx, Td, 0.f, st));
+    for (int i0 = 0; i0 < Ts; i0 += w.head_rows) {
+      const int R = std::min(w.head_rows, Ts - i0), Rp = round64(R), r0 = score_from - 1 + i0;
+      HIPCHK(rmsnorm(c.dtype, const_cast<float*>(xL), d, RowMap{r0, 1, 1, 0}, none, m->final_norm,
+                     R, d, c.rms_eps, w.hf, d, st));
+      if ((rc = gemm_rows(m, w.hf, d, R, one(m->lm_head), V, d, EPI_STORE,
+                          EpiArgs{w.z, nullptr, V}, st)))
+        return rc;
+      HIPCHK(dlogits(c.dtype, w.z, R, V, V, tk + score_from + i0, 1, gn + i0, temperature, w.dz,
+                     V, st));
+      HIPCHK(transpose(e, e, w.dz, V, 0, R, V, w.dzT, Rp, 0, 0, 1, Rp, 1, st));
+      HIPCHK(transpose(e, e, w.hf, d, 0, R, d, w.hfT, Rp, 0, 0, 1, Rp, 1, st));
+      if ((rc = gemm_rows(m, w.dzT, Rp, V, one(w.hfT), d, Rp, EPI_RESID,
+                          EpiArgs{g->lm_head, nullptr, d}, st)))
+        return rc;
+      if ((rc = gemm_rows(m, w.dz, V, R, one(w.WheadT), d, V, EPI_STORE,
+                          EpiArgs{w.dhf, nullptr, d}, st)))
+        return rc;
+      HIPCHK(rmsnorm_bwd(c.dtype, xL + (size_t)r0 * d, d, m->final_norm, w.dhf, d, R, d, c.rms_eps,
+                         w.dx + (size_t)r0 * d, nullptr, w.rr, w.part, g->final_norm, st));
+    }
+    // layers in reverse; w.dx holds the gradient of the layer's output
+    for (int l = L - 1; l >= 0; --l) {
+      const float* x = w.X + l * Td;
+      if ((rc = layer_fwd(m, w, l, x, T, nullptr, st))) return rc;
+      // down projection: x_out = xa + a Wd^T
+      if ((rc = wgrad(m, w, w.dx, 1, d, d, w.a, f, f, T, g->w_down[l], st))) return rc;
+      HIPCHK(cast_f32(w.dx, Td, c.dtype, w.dxe, st));
+      if ((rc = gemm_rows(m, w.dxe, d, T, one(w.WdT[l]), f, d, EPI_STORE,
+                          EpiArgs{w.da, nullptr, f}, st)))
+        return rc;
+      HIPCHK(swiglu_bwd(c.dtype, w.gu, w.da, T, f, w.dgu, st));
+      // gate / up: dgu^T h2 for each half, dh2 = dgu [Wg; Wu]
+      HIPCHK(transpose(e, e, w.dgu, 2 * f, 0, T, 2 * f, w.tA, Tp, 0, 0, 1, Tp, 1, st));
+      HIPCHK(transpose(e, e, w.h2, d, 0, T, d, w.tB, Tp, 0, 0, 1, Tp, 1, st));
+      if ((rc = gemm_rows(m, w.tA, Tp, f, one(w.tB), d, Tp, EPI_RESID,
+                          EpiArgs{g->w_gate[l], nullptr, d}, st)) ||
+          (rc = gemm_rows(m, (char*)w.tA + (size_t)f * Tp * es, Tp, f, one(w.tB), d, Tp, EPI_RESID,
+                          EpiArgs{g->w_up[l], nullptr, d}, st)))
+        return rc;
+      if ((rc = gemm_rows(m, w.dgu, 2 * f, T, one(w.WguT[l]), d, 2 * f, EPI_STORE,
+                          EpiArgs{w.dh, nullptr, d}, st)))
+        return rc;
+      HIPCHK(hipMemcpyAsync(w.dxa, w.dx, Td * 4, hipMemcpyDeviceToDevice, st));
+      HIPCHK(rmsnorm_bwd(c.dtype, w.xa, d, m->mlp_norm[l], w.dh, d, T, d, c.rms_eps, w.dxa, w.dxe,
+                         w.rr, w.part, g->mlp_norm[l], st));
+      // output projection: xa = x + o Wo^T
+      if ((rc = wgrad(m, w, w.dxa, 1, d, d, w.o, qd, qd, T, g->wo[l], st))) return rc;
+      if ((rc = gemm_rows(m, w.dxe, d, T, one(w.WoT[l]), qd, d, EPI_STORE,
+                          EpiArgs{w.dof, nullptr, qd}, st)))
+        return rc;
+      HIPCHK(cast_f32(w.dof, (size_t)T * qd, c.dtype, w.doe, st));
+      if ((rc = attn_bwd(m, w, T, st))) return rc;
+      HIPCHK(rope_bwd(c.dtype, w.dqkv, T, c.n_heads + 2 * c.n_kv_heads, c.n_heads + c.n_kv_heads,
+                      c.head_dim, w.cs, w.dqkve, st));
+      // q, k, v projections: dqkv^T h into the three gradients, dh = dqkv [Wq; Wk; Wv]
+      HIPCHK(transpose(e, e, w.dqkve, ldqkv, 0, T, ldqkv, w.tA, Tp, 0, 0, 1, Tp, 1, st));
+      HIPCHK(transpose(e, e, w.h, d, 0, T, d, w.tB, Tp, 0, 0, 1, Tp, 1, st));
+      if ((rc = gemm_rows(m, w.tA, Tp, qd, one(w.tB), d, Tp, EPI_RESID,
+                          EpiArgs{g->wq[l], nullptr, d}, st)) ||
+          (rc = gemm_rows(m, (char*)w.tA + (size_t)qd * Tp * es, Tp, kvd, one(w.tB), d, Tp,
+                          EPI_RESID, EpiArgs{g->wk[l], nullptr, d}, st)) ||
+          (rc = gemm_rows(m, (char*)w.tA + (size_t)(qd + kvd) * Tp * es, Tp, kvd, one(w.tB), d, Tp,
+                          EPI_RESID, EpiArgs{g->wv[l], nullptr, d}, st)))
+        return rc;
+      if ((rc = gemm_rows(m, w.dqkve, ldqkv, T, one(w.WqkvT[l]), d, ldqkv, EPI_STORE,
+                          EpiArgs{w.dh, nullptr, d}, st)))
+        return rc;
+      HIPCHK(rmsnorm_bwd(c.dtype, x, d, m->attn_norm[l], w.dh, d, T, d, c.rms_eps, w.dxa, nullptr,
+                         w.rr, w.part, g->attn_norm[l], st));
+      std::swap(w.dx, w.dxa);
+    }
+    HIPCHK(embed_bwd(tk, w.dx, T, d, g->tok_emb, st));
+  }
+  g_err.clear();
+  return GRPO_OK;
+}
+
+int grpo_adamw_step(int32_t dtype, void* param, float* master, float* m1, float* m2,
+                    const float* grad, size_t n, const grpo_adamw* hp, int32_t step, void* stream) {
+  if (dtype != GRPO_F32 && dtype != GRPO_BF16) return fail(GRPO_INVALID_ARG, "dtype must be 0 or 1");
+  if (!param || !m1 || !m2 || !grad || !hp) return fail(GRPO_INVALID_ARG, "param, m, v, grad and hp must be set");
+  if (dtype == GRPO_BF16 && !master) return fail(GRPO_INVALID_ARG, "bf16 parameters need an fp32 master copy");
+  if (step < 1) return fail(GRPO_INVALID_ARG, "step counts from 1");
+  if (!(hp->lr >= 0.f) || !(hp->beta1 >= 0.f && hp->beta1 < 1.f) ||
+      !(hp->beta2 >= 0.f && hp->beta2 < 1.f) || !(hp->eps > 0.f) || !(hp->weight_decay >= 0.f))
+    return fail(GRPO_INVALID_ARG, "AdamW hyper-parameters out of range");
+  HIPCHK(adamw(dtype, param, master, m1, m2, grad, n, hp->lr, hp->beta1, hp->beta2, hp->eps,
+               hp->weight_decay, step, (hipStream_t)stream));
   g_err.clear();
   return GRPO_OK;
 }

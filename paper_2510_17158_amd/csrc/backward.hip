@@ -1,0 +1,407 @@
+// Backward pass of the teacher-forced policy log-probs and the AdamW step.
+//
+// The weight gradient of sum_t g_t logp_t (g = dL/dlogp from the GRPO token
+// loss) runs as matrix products on the tiled MFMA GEMMs plus the element-wise
+// and row-wise kernels here.  Every product is cast as Y[M, N] = X[M, K] W[N, K]^T
+// with both operands K-contiguous (the layout the matrix cores read); the
+// operands that are not stored that way are transposed first (k_transpose):
+//   data gradient   dX = dY W      -> X operand dY, W operand W^T
+//   weight gradient dW += dY^T X   -> X operand dY^T, W operand X^T (K = tokens)
+// Attention's backward materialises, per head, the T x T scores S = q k^T and
+// dP = do v^T (fp32), turns them into P and dS' = P (dP - rowsum(P dP)) / sqrt(hd)
+// (k_attn_softmax_bwd), and finishes with three products per head, batched over
+// a block of heads: dq_h = dS'_h k, dk_h = dS'_h^T q_h, dv_h = P_h^T do_h, the
+// last two summed over each kv group's heads in a fixed order (k_sum_heads).
+// The causal upper triangle is computed and zeroed.
+//
+// Gradients accumulate in fp32; GEMM operands are the model's dtype (bf16
+// products on MFMA, fp32 on the vector units for fp32 models).  The embedding
+// gradient is a scatter-add with fp32 atomics (its summation order is not
+// fixed); every other reduction runs in a fixed order.
+#include "common.h"
+#include "kernels.h"
+
+namespace grpo {
+
+namespace {
+
+constexpr int BT = 64;    // transpose tile
+
+// out[c][r] = in[r][c] (r < R, c < C); out columns R .. Rpad-1 are zero.
+// Batch element b: in + b * in_bs, out + (b / div) * s1 + (b % div) * s2.
+template <typename TI, typename TO>
+__global__ __launch_bounds__(256) void k_transpose(const TI* __restrict__ in, int ldi, size_t in_bs,
+                                                   int R, int C, TO* __restrict__ out, int ldo,
+                                                   size_t s1, size_t s2, int div, int Rpad) {
+  __shared__ float tile[BT][BT + 1];
+  const int b = blockIdx.z, r0 = blockIdx.x * BT, c0 = blockIdx.y * BT;
+  in += (size_t)b * in_bs;
+  out += (size_t)(b / div) * s1 + (size_t)(b % div) * s2;
+  for (int i = threadIdx.x; i < BT * BT; i += 256) {
+    const int r = i / BT, c = i % BT;
+    tile[r][c] = (r0 + r < R && c0 + c < C) ? ldf(in, (size_t)(r0 + r) * ldi + c0 + c) : 0.f;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < BT * BT; i += 256) {
+    const int c = i / BT, r = i % BT;
+    if (c0 + c < C && r0 + r < Rpad) stf(out, (size_t)(c0 + c) * ldo + r0 + r, tile[r][c]);
+  }
+}
+
+// dz[r, v] = g_r / T (onehot(tgt_r) - softmax(z_r / T)); one workgroup per row.
+template <typename TO>
+__global__ __launch_bounds__(256) void k_dlogits(const float* __restrict__ z, int V, int ldz,
+                                                 const int32_t* __restrict__ tgt, int tstride,
+                                                 const float* __restrict__ g, float inv_t,
+                                                 TO* __restrict__ dz, int ldo) {
+  __shared__ float sh[4];
+  const int r = blockIdx.x;
+  const float* zr = z + (size_t)r * ldz;
+  float m = -INFINITY;
+  for (int v = threadIdx.x; v < V; v += 256) m = fmaxf(m, zr[v] * inv_t);
+  m = block_max<256>(m, sh);
+  float s = 0.f;
+  for (int v = threadIdx.x; v < V; v += 256) s += __expf(zr[v] * inv_t - m);
+  s = block_sum<256>(s, sh);
+  const float c = g[r] * inv_t, rs = 1.f / s;
+  const int t = tgt[(size_t)r * tstride];
+  TO* o = dz + (size_t)r * ldo;
+  for (int v = threadIdx.x; v < V; v += 256) {
+    const float p = __expf(zr[v] * inv_t - m) * rs;
+    stf(o, v, c * ((v == t ? 1.f : 0.f) - p));
+  }
+}
+
+// RMSNorm backward of one row: y = x r g, r = (mean x^2 + eps)^-1/2.
+// dres[t] += r (g dy) - x r^3 sum(g dy x) / d; dres_e = dres in the GEMM dtype
+// (optional); rr[t] = r for the gain gradient.
+template <typename TG>
+__global__ __launch_bounds__(256) void k_rmsnorm_bwd(const float* __restrict__ x, int ldx,
+                                                     const TG* __restrict__ g,
+                                                     const float* __restrict__ dy, int ldy, int d,
+                                                     float eps, float* __restrict__ dres,
+                                                     TG* __restrict__ dres_e, float* __restrict__ rr) {
+  __shared__ float sh[4];
+  const int t = blockIdx.x;
+  const float* xr = x + (size_t)t * ldx;
+  const float* dr = dy + (size_t)t * ldy;
+  float ss = 0.f, sd = 0.f;
+  for (int k = threadIdx.x; k < d; k += 256) {
+    const float xv = xr[k];
+    ss = fmaf(xv, xv, ss);
+    sd = fmaf(ldf(g, k) * dr[k], xv, sd);
+  }
+  ss = block_sum<256>(ss, sh);
+  sd = block_sum<256>(sd, sh);
+  const float r = 1.f / sqrtf(ss / (float)d + eps);
+  const float c = r * r * r * sd / (float)d;
+  float* o = dres + (size_t)t * d;
+  for (int k = threadIdx.x; k < d; k += 256) {
+    const float v = o[k] + r * ldf(g, k) * dr[k] - xr[k] * c;
+    o[k] = v;
+    if (dres_e) stf(dres_e, (size_t)t * d + k, v);
+  }
+  if (threadIdx.x == 0) rr[t] = r;
+}
+
+// Gain gradient partials: part[chunk][k] = sum over the chunk's 64 rows of
+// dy[t, k] x[t, k] rr[t]; then dg[k] += sum over chunks in order.
+__global__ __launch_bounds__(256) void k_norm_dg_part(const float* __restrict__ x, int ldx,
+                                                      const float* __restrict__ dy, int ldy,
+                                                      const float* __restrict__ rr, int T, int d,
+                                                      float* __restrict__ part) {
+  const int k = blockIdx.x * 256 + threadIdx.x, c = blockIdx.y;
+  if (k >= d) return;
+  float s = 0.f;
+  const int t1 = min(T, (c + 1) * 64);
+  for (int t = c * 64; t < t1; ++t) s = fmaf(dy[(size_t)t * ldy + k] * x[(size_t)t * ldx + k], rr[t], s);
+  part[(size_t)c * d + k] = s;
+}
+__global__ __launch_bounds__(256) void k_norm_dg_sum(const float* __restrict__ part, int chunks,
+                                                     int d, float* __restrict__ dg) {
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  if (k >= d) return;
+  float s = 0.f;
+  for (int c = 0; c < chunks; ++c) s += part[(size_t)c * d + k];
+  dg[k] += s;
+}
+
+// SwiGLU: gu = [gate | up] fp32 [T, 2F].  Forward a = silu(gate) up (activation
+// dtype); backward dgate = da up silu'(gate), dup = da silu(gate) into dgu [T, 2F].
+template <typename TO>
+__global__ __launch_bounds__(256) void k_swiglu_fwd(const float* __restrict__ gu, int T, int F,
+                                                    TO* __restrict__ a) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)T * F) return;
+  const size_t t = i / F, n = i % F;
+  const float gt = gu[t * 2 * F + n], up = gu[t * 2 * F + F + n];
+  stf(a, i, gt / (1.f + __expf(-gt)) * up);
+}
+template <typename TO>
+__global__ __launch_bounds__(256) void k_swiglu_bwd(const float* __restrict__ gu,
+                                                    const float* __restrict__ da, int T, int F,
+                                                    TO* __restrict__ dgu) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)T * F) return;
+  const size_t t = i / F, n = i % F;
+  const float gt = gu[t * 2 * F + n], up = gu[t * 2 * F + F + n], d = da[i];
+  const float sg = 1.f / (1.f + __expf(-gt));
+  stf(dgu, t * 2 * F + n, d * up * sg * (1.f + gt * (1.f - sg)));
+  stf(dgu, t * 2 * F + F + n, d * gt * sg);
+}
+
+// RoPE adjoint on the q and k heads of dqkv [T, (H + 2 Hkv) hd] (fp32, in place:
+// lo' = lo c + hi s, hi' = hi c - lo s), and the whole row in the GEMM dtype.
+template <typename TO>
+__global__ __launch_bounds__(256) void k_rope_bwd(float* __restrict__ dqkv, int T, int heads,
+                                                  int n_rot, int hd, const float2* __restrict__ cs,
+                                                  TO* __restrict__ out) {
+  const int half = hd / 2;
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)T * heads * half) return;
+  const int e = (int)(i % half);
+  const int h = (int)((i / half) % heads);
+  const size_t t = i / ((size_t)half * heads);
+  float* p = dqkv + (t * heads + h) * hd;
+  float lo = p[e], hi = p[e + half];
+  if (h < n_rot) {
+    const float2 c = cs[t * half + e];
+    const float l2 = lo * c.x + hi * c.y, h2 = hi * c.x - lo * c.y;
+    lo = l2; hi = h2;
+    p[e] = lo; p[e + half] = hi;
+  }
+  stf(out, (t * heads + h) * hd + e, lo);
+  stf(out, (t * heads + h) * hd + e + half, hi);
+}
+
+// Attention softmax backward of one query row i of head-batch element b:
+// S [T, ldS] raw scores q.k (fp32), dP [T, ldS]; P = causal softmax(S s),
+// dS' = P (dP - sum_j P dP) s.  Writes P and dS' rows of length Tp (zeros past i).
+template <typename TO>
+__global__ __launch_bounds__(256) void k_attn_softmax_bwd(const float* __restrict__ S,
+                                                          const float* __restrict__ dP, int T,
+                                                          int Tp, float s, TO* __restrict__ P,
+                                                          TO* __restrict__ dS) {
+  __shared__ float sh[4];
+  const int i = blockIdx.x, b = blockIdx.y;
+  const size_t row = ((size_t)b * T + i) * Tp;
+  const float* sr = S + row;
+  const float* dr = dP + row;
+  float m = -INFINITY;
+  for (int j = threadIdx.x; j <= i; j += 256) m = fmaxf(m, sr[j] * s);
+  m = block_max<256>(m, sh);
+  float l = 0.f, dd = 0.f;
+  for (int j = threadIdx.x; j <= i; j += 256) {
+    const float e = __expf(sr[j] * s - m);
+    l += e;
+    dd = fmaf(e, dr[j], dd);
+  }
+  l = block_sum<256>(l, sh);
+  dd = block_sum<256>(dd, sh);
+  const float rl = 1.f / l, D = dd * rl;
+  for (int j = threadIdx.x; j < Tp; j += 256) {
+    float p = 0.f, ds = 0.f;
+    if (j <= i) {
+      p = __expf(sr[j] * s - m) * rl;
+      ds = p * (dr[j] - D) * s;
+    }
+    stf(P, row + j, p);
+    stf(dS, row + j, ds);
+  }
+}
+
+// Sum over each kv group's heads: out[t][g hd + e] = sum_j tmp[g gq + j][t][e].
+__global__ __launch_bounds__(256) void k_sum_heads(const float* __restrict__ tmp, int T, int hd,
+                                                   int gq, int groups, float* __restrict__ out,
+                                                   int ldo) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)groups * T * hd) return;
+  const int e = (int)(i % hd);
+  const size_t t = (i / hd) % T;
+  const int g = (int)(i / ((size_t)hd * T));
+  float s = 0.f;
+  for (int j = 0; j < gq; ++j) s += tmp[(((size_t)g * gq + j) * T + t) * hd + e];
+  out[t * ldo + (size_t)g * hd + e] = s;
+}
+
+// Embedding gradient: demb[tok[t]] += dx[t] (fp32 atomics).
+__global__ __launch_bounds__(256) void k_embed_bwd(const int32_t* __restrict__ tok,
+                                                   const float* __restrict__ dx, int d,
+                                                   float* __restrict__ demb) {
+  const int t = blockIdx.x;
+  const size_t row = (size_t)tok[t] * d;
+  for (int k = threadIdx.x; k < d; k += 256) atomicAdd(demb + row + k, dx[(size_t)t * d + k]);
+}
+
+__global__ __launch_bounds__(256) void k_fill_f32(float* p, size_t n, float v) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+template <typename TI, typename TO>
+__global__ __launch_bounds__(256) void k_cast(const TI* __restrict__ in, size_t n, TO* __restrict__ out) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) stf(out, i, ldf(in, i));
+}
+
+// AdamW: m = b1 m + (1 - b1) g, v = b2 v + (1 - b2) g^2, p -= lr wd p + lr mhat /
+// (sqrt(vhat) + eps) on the fp32 master; the model copy gets the rounded value.
+template <typename TP>
+__global__ __launch_bounds__(256) void k_adamw(TP* __restrict__ param, float* __restrict__ master,
+                                               float* __restrict__ m, float* __restrict__ v,
+                                               const float* __restrict__ grad, size_t n, float lr,
+                                               float b1, float b2, float eps, float wd, float bc1,
+                                               float bc2) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const float g = grad[i];
+  const float mi = b1 * m[i] + (1.f - b1) * g;
+  const float vi = b2 * v[i] + (1.f - b2) * g * g;
+  m[i] = mi;
+  v[i] = vi;
+  float p = master ? master[i] : ldf(param, i);
+  p = p - lr * wd * p - lr * (mi / bc1) / (sqrtf(vi / bc2) + eps);
+  if (master) master[i] = p;
+  stf(param, i, p);
+}
+
+inline unsigned blocks(size_t n) { return (unsigned)((n + 255) / 256); }
+
+}  // namespace
+
+hipError_t transpose(int tin, int tout, const void* in, int ldi, size_t in_bs, int R, int C,
+                     void* out, int ldo, size_t s1, size_t s2, int div, int Rpad, int batch,
+                     hipStream_t st) {
+  if (R <= 0 || C <= 0 || batch <= 0) return hipSuccess;
+  if (Rpad < R || div < 1) return hipErrorInvalidValue;
+  dim3 grid((Rpad + BT - 1) / BT, (C + BT - 1) / BT, batch);
+  Prof pf("transpose", st);
+  if (tin == 0 && tout == 0)
+    k_transpose<float, float><<<grid, 256, 0, st>>>((const float*)in, ldi, in_bs, R, C, (float*)out,
+                                                    ldo, s1, s2, div, Rpad);
+  else if (tin == 0)
+    k_transpose<float, bf16_t><<<grid, 256, 0, st>>>((const float*)in, ldi, in_bs, R, C,
+                                                     (bf16_t*)out, ldo, s1, s2, div, Rpad);
+  else if (tout == 1)
+    k_transpose<bf16_t, bf16_t><<<grid, 256, 0, st>>>((const bf16_t*)in, ldi, in_bs, R, C,
+                                                      (bf16_t*)out, ldo, s1, s2, div, Rpad);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t dlogits(int dtype, const float* z, int R, int V, int ldz, const int32_t* tgt,
+                   int tstride, const float* g, float temperature, void* dz, int ldo,
+                   hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  const float inv_t = 1.f / (temperature > 0.f ? temperature : 1.f);
+  Prof pf("dlogits", st);
+  if (dtype == 0) k_dlogits<float><<<R, 256, 0, st>>>(z, V, ldz, tgt, tstride, g, inv_t, (float*)dz, ldo);
+  else k_dlogits<bf16_t><<<R, 256, 0, st>>>(z, V, ldz, tgt, tstride, g, inv_t, (bf16_t*)dz, ldo);
+  return hipGetLastError();
+}
+
+hipError_t rmsnorm_bwd(int dtype, const float* x, int ldx, const void* g, const float* dy, int ldy,
+                       int T, int d, float eps, float* dres, void* dres_e, float* rr, float* part,
+                       float* dg, hipStream_t st) {
+  if (T <= 0) return hipSuccess;
+  Prof pf("rmsnorm_bwd", st);
+  if (dtype == 0)
+    k_rmsnorm_bwd<float><<<T, 256, 0, st>>>(x, ldx, (const float*)g, dy, ldy, d, eps, dres,
+                                            (float*)dres_e, rr);
+  else
+    k_rmsnorm_bwd<bf16_t><<<T, 256, 0, st>>>(x, ldx, (const bf16_t*)g, dy, ldy, d, eps, dres,
+                                             (bf16_t*)dres_e, rr);
+  const int chunks = (T + 63) / 64;
+  k_norm_dg_part<<<dim3((d + 255) / 256, chunks), 256, 0, st>>>(x, ldx, dy, ldy, rr, T, d, part);
+  k_norm_dg_sum<<<(d + 255) / 256, 256, 0, st>>>(part, chunks, d, dg);
+  return hipGetLastError();
+}
+
+hipError_t swiglu_fwd(int dtype, const float* gu, int T, int F, void* a, hipStream_t st) {
+  const size_t n = (size_t)T * F;
+  if (n == 0) return hipSuccess;
+  Prof pf("swiglu_fwd", st);
+  if (dtype == 0) k_swiglu_fwd<float><<<blocks(n), 256, 0, st>>>(gu, T, F, (float*)a);
+  else k_swiglu_fwd<bf16_t><<<blocks(n), 256, 0, st>>>(gu, T, F, (bf16_t*)a);
+  return hipGetLastError();
+}
+
+hipError_t swiglu_bwd(int dtype, const float* gu, const float* da, int T, int F, void* dgu,
+                      hipStream_t st) {
+  const size_t n = (size_t)T * F;
+  if (n == 0) return hipSuccess;
+  Prof pf("swiglu_bwd", st);
+  if (dtype == 0) k_swiglu_bwd<float><<<blocks(n), 256, 0, st>>>(gu, da, T, F, (float*)dgu);
+  else k_swiglu_bwd<bf16_t><<<blocks(n), 256, 0, st>>>(gu, da, T, F, (bf16_t*)dgu);
+  return hipGetLastError();
+}
+
+hipError_t rope_bwd(int dtype, float* dqkv, int T, int heads, int n_rot, int hd, const float2* cs,
+                    void* out, hipStream_t st) {
+  const size_t n = (size_t)T * heads * (hd / 2);
+  if (n == 0) return hipSuccess;
+  Prof pf("rope_bwd", st);
+  if (dtype == 0) k_rope_bwd<float><<<blocks(n), 256, 0, st>>>(dqkv, T, heads, n_rot, hd, cs, (float*)out);
+  else k_rope_bwd<bf16_t><<<blocks(n), 256, 0, st>>>(dqkv, T, heads, n_rot, hd, cs, (bf16_t*)out);
+  return hipGetLastError();
+}
+
+hipError_t attn_softmax_bwd(int dtype, const float* S, const float* dP, int T, int Tp, int batch,
+                            float scale, void* P, void* dS, hipStream_t st) {
+  if (T <= 0 || batch <= 0) return hipSuccess;
+  Prof pf("attn_softmax_bwd", st);
+  dim3 grid(T, batch);
+  if (dtype == 0)
+    k_attn_softmax_bwd<float><<<grid, 256, 0, st>>>(S, dP, T, Tp, scale, (float*)P, (float*)dS);
+  else
+    k_attn_softmax_bwd<bf16_t><<<grid, 256, 0, st>>>(S, dP, T, Tp, scale, (bf16_t*)P, (bf16_t*)dS);
+  return hipGetLastError();
+}
+
+hipError_t sum_heads(const float* tmp, int T, int hd, int gq, int groups, float* out, int ldo,
+                     hipStream_t st) {
+  const size_t n = (size_t)groups * T * hd;
+  if (n == 0) return hipSuccess;
+  Prof pf("sum_heads", st);
+  k_sum_heads<<<blocks(n), 256, 0, st>>>(tmp, T, hd, gq, groups, out, ldo);
+  return hipGetLastError();
+}
+
+hipError_t embed_bwd(const int32_t* tok, const float* dx, int T, int d, float* demb, hipStream_t st) {
+  if (T <= 0) return hipSuccess;
+  Prof pf("embed_bwd", st);
+  k_embed_bwd<<<T, 256, 0, st>>>(tok, dx, d, demb);
+  return hipGetLastError();
+}
+
+hipError_t fill_f32(float* p, size_t n, float v, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  k_fill_f32<<<blocks(n), 256, 0, st>>>(p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t cast_f32(const float* in, size_t n, int dtype, void* out, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  if (dtype == 0) k_cast<float, float><<<blocks(n), 256, 0, st>>>(in, n, (float*)out);
+  else k_cast<float, bf16_t><<<blocks(n), 256, 0, st>>>(in, n, (bf16_t*)out);
+  return hipGetLastError();
+}
+
+hipError_t adamw(int dtype, void* param, float* master, float* m, float* v, const float* grad,
+                 size_t n, float lr, float b1, float b2, float eps, float wd, int step,
+                 hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  const float bc1 = (float)(1.0 - pow((double)b1, (double)step));
+  const float bc2 = (float)(1.0 - pow((double)b2, (double)step));
+  Prof pf("adamw", st);
+  if (dtype == 0)
+    k_adamw<float><<<blocks(n), 256, 0, st>>>((float*)param, master, m, v, grad, n, lr, b1, b2, eps,
+                                              wd, bc1, bc2);
+  else
+    k_adamw<bf16_t><<<blocks(n), 256, 0, st>>>((bf16_t*)param, master, m, v, grad, n, lr, b1, b2,
+                                               eps, wd, bc1, bc2);
+  return hipGetLastError();
+}
+
+}  // namespace grpo

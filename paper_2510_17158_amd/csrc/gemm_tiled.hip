@@ -28,7 +28,16 @@ struct TArgs {
   const bf16_t* w0; const bf16_t* w1; const bf16_t* w2; int n1, n2;
   int N, K, tiles_m, tiles_n;
   float* out_f32; bf16_t* out_act; int ld_out;
+  GemmBatch bt;     // product b of a batch: blockIdx.y of the tiled kernel
 };
+
+// operands and output of batch product b
+__device__ __forceinline__ void batch_offset(TArgs& a, int b) {
+  const size_t wo = (size_t)(b / a.bt.wdiv) * a.bt.sw;
+  a.X += (size_t)b * a.bt.sx;
+  a.w0 += wo; a.w1 += wo; a.w2 += wo;
+  a.out_f32 += (size_t)b * a.bt.so;
+}
 
 template <int EPI>
 __device__ __forceinline__ const bf16_t* tile_wrow(const TArgs& a, int tn, int r) {
@@ -48,6 +57,7 @@ template <int EPI>
 __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LROW];
   __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * LROW];
+  if (gridDim.y > 1) batch_offset(a, blockIdx.y);
   const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
   const int wm = wave >> 1, wn = wave & 1;
 
@@ -377,6 +387,7 @@ struct FArgs {
   const float* w0; const float* w1; const float* w2; int n1, n2;
   int N, K, epi;
   float* out_f32; float* out_act; int ld_out;
+  GemmBatch bt;     // product b of a batch: blockIdx.z
 };
 
 __device__ __forceinline__ const float* frow(const FArgs& a, int n) {
@@ -388,6 +399,13 @@ __device__ __forceinline__ const float* frow(const FArgs& a, int n) {
 __global__ __launch_bounds__(256) void k_gemm_f32(FArgs a) {
   __shared__ float xs[16][65];
   __shared__ float ws[16][65];
+  if (gridDim.z > 1) {
+    const int b = blockIdx.z;
+    const size_t wo = (size_t)(b / a.bt.wdiv) * a.bt.sw;
+    a.X += (size_t)b * a.bt.sx;
+    a.w0 += wo; a.w1 += wo; a.w2 += wo;
+    a.out_f32 += (size_t)b * a.bt.so;
+  }
   const int tid = threadIdx.x;
   const int tx = tid % 16, ty = tid / 16;
   const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
@@ -451,8 +469,12 @@ __global__ __launch_bounds__(256) void k_gemm_f32(FArgs a) {
 }  // namespace
 
 hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, int K, int epi,
-                           EpiArgs ep, hipStream_t st) {
+                           EpiArgs ep, hipStream_t st, GemmBatch bt) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (K % BK || bt.count < 1 || bt.wdiv < 1 || (bt.count > 1 && epi == EPI_SWIGLU))
+    return hipErrorInvalidValue;
   TArgs a;
+  a.bt = bt;
   a.X = X; a.ldx = ldx; a.M = M;
   a.w0 = (const bf16_t*)W.w[0]; a.w1 = (const bf16_t*)W.w[1]; a.w2 = (const bf16_t*)W.w[2];
   a.n1 = W.n1; a.n2 = W.n2; a.N = N; a.K = K;
@@ -465,7 +487,7 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
   const bool aligned = out16 && (epi == EPI_SWIGLU
                            ? W.n1 % 128 == 0
                            : N % GB == 0 && (W.n1 >= N || W.n1 % GB == 0) && (W.n2 >= N || W.n2 % GB == 0));
-  if (M >= kBigTileRows && aligned) {
+  if (M >= kBigTileRows && aligned && bt.count == 1) {
     a.tiles_m = (M + GB - 1) / GB;
     a.tiles_n = epi == EPI_SWIGLU ? (N + 127) / 128 : (N + GB - 1) / GB;
     // super-tiles of 4 x 8 tiles, a whole number of rounds of 8 (one per XCD)
@@ -480,7 +502,7 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
   }
   a.tiles_m = (M + BM - 1) / BM;
   a.tiles_n = epi == EPI_SWIGLU ? (N + 63) / 64 : (N + BN - 1) / BN;
-  const int grid = a.tiles_m * a.tiles_n;
+  const dim3 grid(a.tiles_m * a.tiles_n, bt.count);
   switch (epi) {
     case EPI_STORE: k_gemm_tiled<EPI_STORE><<<grid, NT, 0, st>>>(a); break;
     case EPI_RESID: k_gemm_tiled<EPI_RESID><<<grid, NT, 0, st>>>(a); break;
@@ -490,13 +512,16 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
 }
 
 hipError_t gemm_f32(const float* X, int ldx, int M, WStack W, int N, int K, int epi, EpiArgs ep,
-                    hipStream_t st) {
+                    hipStream_t st, GemmBatch bt) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (K % 16 || bt.count < 1 || bt.wdiv < 1) return hipErrorInvalidValue;
   FArgs a;
+  a.bt = bt;
   a.X = X; a.ldx = ldx; a.M = M;
   a.w0 = (const float*)W.w[0]; a.w1 = (const float*)W.w[1]; a.w2 = (const float*)W.w[2];
   a.n1 = W.n1; a.n2 = W.n2; a.N = N; a.K = K; a.epi = epi;
   a.out_f32 = ep.out_f32; a.out_act = (float*)ep.out_act; a.ld_out = ep.ld_out;
-  dim3 grid((N + 63) / 64, (M + 63) / 64);
+  dim3 grid((N + 63) / 64, (M + 63) / 64, bt.count);
   Prof pf("gemm_f32", st);
   k_gemm_f32<<<grid, 256, 0, st>>>(a);
   return hipGetLastError();

@@ -31,6 +31,14 @@ struct WStack {
   int n1, n2;
 };
 
+// A batch of products with the same shape: product b reads X + b sx, the
+// weights + (b / wdiv) sw and writes out + b so (elements).
+struct GemmBatch {
+  int count = 1;
+  size_t sx = 0, sw = 0, so = 0;
+  int wdiv = 1;
+};
+
 struct EpiArgs {
   float* out_f32;       // EPI_STORE: [rows, ld_out] fp32;  EPI_RESID: residual [rows, ld_out]
   void* out_act;        // EPI_SWIGLU: [rows, ld_out] activation dtype
@@ -66,11 +74,11 @@ hipError_t pack_frag(const PackSrc& s, int N, int K, uint16_t* dst, hipStream_t 
 
 // ---- tiled GEMM for many rows (prefill / scoring): bf16 MFMA -----------------
 hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, int K, int epi,
-                           EpiArgs ep, hipStream_t st);
+                           EpiArgs ep, hipStream_t st, GemmBatch bt = GemmBatch{});
 
 // ---- fp32 GEMM (fp32 models; VALU) -------------------------------------------
 hipError_t gemm_f32(const float* X, int ldx, int M, WStack W, int N, int K, int epi, EpiArgs ep,
-                    hipStream_t st);
+                    hipStream_t st, GemmBatch bt = GemmBatch{});
 
 // ---- elementwise ---------------------------------------------------------------
 // x[m, :] = emb[tok[m]] (fp32).  tok ids clamped to [0, vocab).
@@ -234,5 +242,34 @@ hipError_t token_loss(const float* lp, const float* lo, const float* lr, const u
                       const float* adv, int N, int Tr, float clip_eps, float beta, int agg,
                       float* loss, float* tok_loss, float* dl, float* stats, double* row_ws,
                       hipStream_t st);
+
+// ---- backward pass and optimizer (backward.hip) ---------------------------------
+// dtype / tin / tout: 0 fp32, 1 bf16.  Transpose: out[c][r] = in[r][c] for r < R,
+// c < C, out columns R .. Rpad-1 zero; batch element b reads in + b in_bs and
+// writes out + (b / div) s1 + (b % div) s2.
+hipError_t transpose(int tin, int tout, const void* in, int ldi, size_t in_bs, int R, int C,
+                     void* out, int ldo, size_t s1, size_t s2, int div, int Rpad, int batch,
+                     hipStream_t st);
+hipError_t dlogits(int dtype, const float* z, int R, int V, int ldz, const int32_t* tgt,
+                   int tstride, const float* g, float temperature, void* dz, int ldo,
+                   hipStream_t st);
+hipError_t rmsnorm_bwd(int dtype, const float* x, int ldx, const void* g, const float* dy, int ldy,
+                       int T, int d, float eps, float* dres, void* dres_e, float* rr, float* part,
+                       float* dg, hipStream_t st);
+hipError_t swiglu_fwd(int dtype, const float* gu, int T, int F, void* a, hipStream_t st);
+hipError_t swiglu_bwd(int dtype, const float* gu, const float* da, int T, int F, void* dgu,
+                      hipStream_t st);
+hipError_t rope_bwd(int dtype, float* dqkv, int T, int heads, int n_rot, int hd, const float2* cs,
+                    void* out, hipStream_t st);
+hipError_t attn_softmax_bwd(int dtype, const float* S, const float* dP, int T, int Tp, int batch,
+                            float scale, void* P, void* dS, hipStream_t st);
+hipError_t sum_heads(const float* tmp, int T, int hd, int gq, int groups, float* out, int ldo,
+                     hipStream_t st);
+hipError_t embed_bwd(const int32_t* tok, const float* dx, int T, int d, float* demb, hipStream_t st);
+hipError_t fill_f32(float* p, size_t n, float v, hipStream_t st);
+hipError_t cast_f32(const float* in, size_t n, int dtype, void* out, hipStream_t st);
+hipError_t adamw(int dtype, void* param, float* master, float* m, float* v, const float* grad,
+                 size_t n, float lr, float b1, float b2, float eps, float wd, int step,
+                 hipStream_t st);
 
 }  // namespace grpo

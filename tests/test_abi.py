@@ -198,6 +198,45 @@ def test_extend_argument_errors_before_device_work():
     L.grpo_model_destroy(h)
 
 
+def test_backward_and_adamw_argument_errors():
+    """grpo_policy_backward and grpo_adamw_step reject bad arguments before any
+    device work."""
+    L = api.lib()
+    cfg = get("small").model
+    rc, h, keep = _fake_model(cfg)
+    p = C.c_void_p(0x1000)
+    BIG = 1 << 44
+    Lc = cfg.n_layers
+    arrs = [(C.c_void_p * Lc)(*([0x2000] * Lc)) for _ in range(9)]
+    g = api.GradsStruct(p, *[C.cast(a, api._PP) for a in arrs], p, p)
+
+    def bwd(N=2, T=100, sf=10, temp=1.0, grads=g, ws_bytes=BIG):
+        return L.grpo_policy_backward(h, p, N, T, sf, temp, p, C.byref(grads) if grads else None,
+                                      p, ws_bytes, None)
+    assert bwd(ws_bytes=16) == api.WORKSPACE_TOO_SMALL          # arguments accepted
+    assert bwd(sf=0) == api.INVALID_ARG
+    assert bwd(sf=100) == api.INVALID_ARG
+    assert bwd(T=1, sf=1) == api.INVALID_ARG
+    assert bwd(temp=-1.0) == api.INVALID_ARG
+    assert bwd(T=20000) == api.UNSUPPORTED
+    assert bwd(grads=None) == api.INVALID_ARG
+    holes = (C.c_void_p * Lc)(*([0x2000] * (Lc - 1) + [0]))
+    g2 = api.GradsStruct(p, *[C.cast(a, api._PP) for a in arrs[:4]], C.cast(holes, api._PP),
+                         *[C.cast(a, api._PP) for a in arrs[5:]], p, p)
+    assert bwd(grads=g2) == api.INVALID_ARG
+    assert b"layer" in L.grpo_last_error()
+    need = L.grpo_workspace_bytes(h, api.OP_BACKWARD, 2, 100)
+    assert need > 0 and bwd(ws_bytes=need - 1) == api.WORKSPACE_TOO_SMALL
+    assert L.grpo_workspace_bytes(h, api.OP_BACKWARD, 2, 20000) == 0
+    hp = api.AdamW(1e-3, 0.9, 0.95, 1e-8, 0.1)
+    assert L.grpo_adamw_step(1, p, None, p, p, p, 10, C.byref(hp), 1, None) == api.INVALID_ARG
+    assert L.grpo_adamw_step(0, p, None, p, p, p, 10, C.byref(hp), 0, None) == api.INVALID_ARG
+    assert L.grpo_adamw_step(2, p, p, p, p, p, 10, C.byref(hp), 1, None) == api.INVALID_ARG
+    bad = api.AdamW(1e-3, 1.0, 0.95, 1e-8, 0.1)
+    assert L.grpo_adamw_step(0, p, None, p, p, p, 10, C.byref(bad), 1, None) == api.INVALID_ARG
+    L.grpo_model_destroy(h)
+
+
 def test_decode_structure_query():
     """The reduction structure the tests' error bounds use comes from the library's
     own planner; its arguments are checked."""
