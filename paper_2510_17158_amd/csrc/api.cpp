@@ -522,7 +522,7 @@ int check_sampling(const grpo_sampling* s, int vocab) {
 }
 
 // ---- backward pass (grpo_policy_backward) ----------------------------------------
-constexpr size_t kAttnBwdBytes = size_t(2) << 30;   // per-head attention scratch per batch
+constexpr size_t kAttnBwdBytes = size_t(8) << 30;   // per-head attention scratch per batch
 constexpr size_t kHeadBwdBytes = size_t(1) << 30;   // LM-head logits per row chunk
 int round64(int t) { return (t + 63) / 64 * 64; }
 
@@ -534,7 +534,7 @@ struct BackwardWS {
   float* dx; float* dxa; void* dxe; float* da; void* dgu; float* dh; float* dof; void* doe;
   float* dqkv; void* dqkve; float* rr; float* part;
   void* tA; void* tB;             // transposed gradient / activation operands [rows][Tp]
-  float* S; float* dP; void* P; void* dS; void* PT; void* dST; void* qT; void* doT; void* kT;
+  float* S; float* dP; float* stats; void* dS; void* PT; void* dST; void* qT; void* doT; void* kT;
   float* tk; float* tv;           // per-head dk, dv before the sum over each group
   void* hf; float* z; void* dz; void* dzT; void* hfT; float* dhf;
   std::vector<void*> WdT, WguT, WoT, WqkvT;
@@ -549,8 +549,8 @@ BackwardWS take_backward(Bump& b, const grpo_config& c, int T) {
   const int Tp = round64(T);
   w.Tp = Tp;
   const size_t TT = (size_t)T * Tp, PP = (size_t)Tp * Tp;
-  const size_t per_head = TT * (8 + 2 * es) + PP * 2 * es + (size_t)hd * Tp * 2 * es +
-                          (size_t)T * hd * 8;
+  const size_t per_head = TT * (8 + es) + PP * 2 * es + (size_t)hd * Tp * 2 * es +
+                          (size_t)T * hd * 8 + (size_t)T * 12;
   int groups = (int)std::max<size_t>(1, kAttnBwdBytes / (per_head * gq));
   groups = std::min(groups, c.n_kv_heads);
   while (c.n_kv_heads % groups) --groups;
@@ -590,7 +590,7 @@ BackwardWS take_backward(Bump& b, const grpo_config& c, int T) {
   const int hb = w.hb;
   w.S = b.take<float>(hb * TT);
   w.dP = b.take<float>(hb * TT);
-  w.P = b.take<char>(hb * TT * es);
+  w.stats = b.take<float>((size_t)hb * T * 3);
   w.dS = b.take<char>(hb * TT * es);
   w.PT = b.take<char>(hb * PP * es);
   w.dST = b.take<char>(hb * PP * es);
@@ -704,15 +704,13 @@ int attn_bwd(const grpo_model* m, BackwardWS& w, int T, hipStream_t st) {
                       one(vb + (size_t)g0 * Tp * hd * es), T, hd, EPI_STORE,
                       EpiArgs{w.dP, nullptr, Tp}, sb, st)))
       return rc;
-    HIPCHK(attn_softmax_bwd(c.dtype, w.S, w.dP, T, Tp, nb, scale, w.P, w.dS, st));
+    HIPCHK(attn_softmax_bwd(c.dtype, w.S, w.dP, T, Tp, nb, scale, w.stats, w.dS, w.dST, w.PT, st));
     // dq_h = dS'_h k_g (K = key positions)
     GemmBatch qb{nb, TT, hT, (size_t)hd, gq};
     if ((rc = gemm_bt(m, w.dS, Tp, T, one((char*)w.kT + (size_t)g0 * hT * es), hd, Tp, EPI_STORE,
                       EpiArgs{w.dqkv + (size_t)h0 * hd, nullptr, ldqkv}, qb, st)))
       return rc;
     // per head: dk_h = dS'_h^T q_h, dv_h = P_h^T do_h (K = query positions)
-    HIPCHK(transpose(e, e, w.dS, Tp, TT, T, Tp, w.dST, Tp, PP, 0, 1, Tp, nb, st));
-    HIPCHK(transpose(e, e, w.P, Tp, TT, T, Tp, w.PT, Tp, PP, 0, 1, Tp, nb, st));
     HIPCHK(transpose(e, e, (char*)w.q + (size_t)h0 * hd * es, qd, hd, T, hd, w.qT, Tp, hT, 0, 1,
                      Tp, nb, st));
     HIPCHK(transpose(e, e, (char*)w.doe + (size_t)h0 * hd * es, qd, hd, T, hd, w.doT, Tp, hT, 0,

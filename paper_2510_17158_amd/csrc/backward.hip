@@ -9,7 +9,7 @@
 //   weight gradient dW += dY^T X   -> X operand dY^T, W operand X^T (K = tokens)
 // Attention's backward materialises, per head, the T x T scores S = q k^T and
 // dP = do v^T (fp32), turns them into P and dS' = P (dP - rowsum(P dP)) / sqrt(hd)
-// (k_attn_softmax_bwd), and finishes with three products per head, batched over
+// (row statistics, then 64 x 64 tiles that also write P^T and dS'^T), and finishes with three products per head, batched over
 // a block of heads: dq_h = dS'_h k, dk_h = dS'_h^T q_h, dv_h = P_h^T do_h, the
 // last two summed over each kv group's heads in a fixed order (k_sum_heads).
 // The causal upper triangle is computed and zeroed.
@@ -174,14 +174,12 @@ __global__ __launch_bounds__(256) void k_rope_bwd(float* __restrict__ dqkv, int 
   stf(out, (t * heads + h) * hd + e + half, hi);
 }
 
-// Attention softmax backward of one query row i of head-batch element b:
-// S [T, ldS] raw scores q.k (fp32), dP [T, ldS]; P = causal softmax(S s),
-// dS' = P (dP - sum_j P dP) s.  Writes P and dS' rows of length Tp (zeros past i).
-template <typename TO>
-__global__ __launch_bounds__(256) void k_attn_softmax_bwd(const float* __restrict__ S,
-                                                          const float* __restrict__ dP, int T,
-                                                          int Tp, float s, TO* __restrict__ P,
-                                                          TO* __restrict__ dS) {
+// Attention softmax backward, pass 1: per query row i of head-batch element b,
+// from the raw scores S [T, ldS = Tp] (q.k, fp32) and dP = do.v: the row maximum
+// m of S s over j <= i, l = sum_j e^(S s - m) and D = sum_j P dP (P = e^(..) / l).
+__global__ __launch_bounds__(256) void k_attn_row_stats(const float* __restrict__ S,
+                                                        const float* __restrict__ dP, int T, int Tp,
+                                                        float s, float* __restrict__ stats) {
   __shared__ float sh[4];
   const int i = blockIdx.x, b = blockIdx.y;
   const size_t row = ((size_t)b * T + i) * Tp;
@@ -198,15 +196,46 @@ __global__ __launch_bounds__(256) void k_attn_softmax_bwd(const float* __restric
   }
   l = block_sum<256>(l, sh);
   dd = block_sum<256>(dd, sh);
-  const float rl = 1.f / l, D = dd * rl;
-  for (int j = threadIdx.x; j < Tp; j += 256) {
+  if (threadIdx.x == 0) {
+    float* o = stats + ((size_t)b * T + i) * 3;
+    o[0] = m; o[1] = 1.f / l; o[2] = dd / l;
+  }
+}
+
+// Pass 2, one 64 x 64 tile (query rows i0.., key columns j0..) per workgroup:
+// P = e^(S s - m) / l and dS' = P (dP - D) s on j <= i < T (zero elsewhere),
+// written as dS' [T][Tp] (rows i) and, through LDS, as P^T and dS'^T [Tp][Tp]
+// (rows j, columns i; zero for i >= T).
+template <typename TO>
+__global__ __launch_bounds__(256) void k_attn_tiles(const float* __restrict__ S,
+                                                    const float* __restrict__ dP,
+                                                    const float* __restrict__ stats, int T, int Tp,
+                                                    float s, TO* __restrict__ dS,
+                                                    TO* __restrict__ dST, TO* __restrict__ PT) {
+  __shared__ float tp[BT][BT + 1], td[BT][BT + 1];
+  const int j0 = blockIdx.x * BT, i0 = blockIdx.y * BT, b = blockIdx.z;
+  const size_t base = (size_t)b * T * Tp;
+  const bool live = j0 <= i0 + BT - 1 && i0 < T;     // some (i, j) with j <= i < T
+  for (int e = threadIdx.x; e < BT * BT; e += 256) {
+    const int r = e / BT, c = e % BT, i = i0 + r, j = j0 + c;
     float p = 0.f, ds = 0.f;
-    if (j <= i) {
-      p = __expf(sr[j] * s - m) * rl;
-      ds = p * (dr[j] - D) * s;
+    if (live && i < T && j <= i) {
+      const float* st = stats + ((size_t)b * T + i) * 3;
+      const size_t o = base + (size_t)i * Tp + j;
+      p = __expf(S[o] * s - st[0]) * st[1];
+      ds = p * (dP[o] - st[2]) * s;
     }
-    stf(P, row + j, p);
-    stf(dS, row + j, ds);
+    if (i < T) stf(dS, base + (size_t)i * Tp + j, ds);
+    tp[r][c] = p;
+    td[r][c] = ds;
+  }
+  __syncthreads();
+  const size_t tb = (size_t)b * Tp * Tp;
+  for (int e = threadIdx.x; e < BT * BT; e += 256) {
+    const int c = e / BT, r = e % BT;
+    const size_t o = tb + (size_t)(j0 + c) * Tp + i0 + r;
+    stf(PT, o, tp[r][c]);
+    stf(dST, o, td[r][c]);
   }
 }
 
@@ -348,14 +377,19 @@ hipError_t rope_bwd(int dtype, float* dqkv, int T, int heads, int n_rot, int hd,
 }
 
 hipError_t attn_softmax_bwd(int dtype, const float* S, const float* dP, int T, int Tp, int batch,
-                            float scale, void* P, void* dS, hipStream_t st) {
+                            float scale, float* stats, void* dS, void* dST, void* PT,
+                            hipStream_t st) {
   if (T <= 0 || batch <= 0) return hipSuccess;
+  if (Tp % BT || Tp < T) return hipErrorInvalidValue;
   Prof pf("attn_softmax_bwd", st);
-  dim3 grid(T, batch);
+  k_attn_row_stats<<<dim3(T, batch), 256, 0, st>>>(S, dP, T, Tp, scale, stats);
+  const dim3 grid(Tp / BT, Tp / BT, batch);
   if (dtype == 0)
-    k_attn_softmax_bwd<float><<<grid, 256, 0, st>>>(S, dP, T, Tp, scale, (float*)P, (float*)dS);
+    k_attn_tiles<float><<<grid, 256, 0, st>>>(S, dP, stats, T, Tp, scale, (float*)dS, (float*)dST,
+                                              (float*)PT);
   else
-    k_attn_softmax_bwd<bf16_t><<<grid, 256, 0, st>>>(S, dP, T, Tp, scale, (bf16_t*)P, (bf16_t*)dS);
+    k_attn_tiles<bf16_t><<<grid, 256, 0, st>>>(S, dP, stats, T, Tp, scale, (bf16_t*)dS,
+                                               (bf16_t*)dST, (bf16_t*)PT);
   return hipGetLastError();
 }
 

@@ -262,7 +262,8 @@ hipError_t swiglu_bwd(int dtype, const float* gu, const float* da, int T, int F,
 hipError_t rope_bwd(int dtype, float* dqkv, int T, int heads, int n_rot, int hd, const float2* cs,
                     void* out, hipStream_t st);
 hipError_t attn_softmax_bwd(int dtype, const float* S, const float* dP, int T, int Tp, int batch,
-                            float scale, void* P, void* dS, hipStream_t st);
+                            float scale, float* stats, void* dS, void* dST, void* PT,
+                            hipStream_t st);
 hipError_t sum_heads(const float* tmp, int T, int hd, int gq, int groups, float* out, int ldo,
                      hipStream_t st);
 hipError_t embed_bwd(const int32_t* tok, const float* dx, int T, int d, float* demb, hipStream_t st);
