@@ -115,6 +115,70 @@ def score_flops(w) -> float:
     return c.n_layers * per_tok * rows + attn_pos * pairs + head
 
 
+def update_flops_per_seq(w) -> float:
+    """Algorithmic flops of the gradient of one sequence's scored log-probs:
+    three times its forward (the forward, then the data and the weight
+    gradients of every product): the projections over all T positions, causal
+    attention, and the LM head on the scored positions."""
+    c = w.model
+    T, Tn = w.total_len, w.new_tokens
+    per_tok = 2 * (c.d_model * (c.q_dim + 2 * c.kv_dim) + c.q_dim * c.d_model
+                   + 3 * c.d_model * c.d_ffn)
+    attn = 2 * 2 * c.n_layers * c.n_heads * c.head_dim * T * (T + 1) / 2
+    head = 2 * c.vocab * c.d_model * Tn
+    return 3 * (c.n_layers * per_tok * T + attn + head)
+
+
+def update_measure(w, it, pol, api, torch, n_seqs: int = 2) -> dict:
+    """The iteration's gradient step on a slice, outside the timed step: the
+    policy backward of the first n_seqs sequences of the step's batch with the
+    token loss's dL/dlogp (grpo_policy_backward), then AdamW over every
+    parameter (grpo_adamw_step, fp32 master weights)."""
+    c = w.model
+    T, sf = w.total_len, w.prompt_len
+    n = min(n_seqs, w.batch)
+    try:
+        grads = api.Grads(pol)
+        ws = api.alloc_workspace(pol, api.OP_BACKWARD, n, T)
+        toks = it.seqs[:n].contiguous()
+        dl = it.dloss[:n].contiguous()
+        api.policy_backward(pol, toks, sf, w.temperature, dl, grads, ws=ws)    # untimed
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        api.policy_backward(pol, toks, sf, w.temperature, dl, grads, ws=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        bwd_ms = e0.elapsed_time(e1)
+        del ws
+        # a copy of the weights (the model itself stays as it is), fp32 masters, moments
+        state = {k: (v.clone(), v.float() if c.dtype == 1 else None,
+                     torch.zeros_like(v, dtype=torch.float32),
+                     torch.zeros_like(v, dtype=torch.float32)) for k, v in pol.weights.items()}
+        hp = dict(lr=1e-6, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.0)
+        torch.cuda.synchronize()
+        e0.record()
+        for k, (prm, mst, m1, m2) in state.items():
+            api.adamw_step(c.dtype, prm, mst, m1, m2, grads.t[k], step=1, **hp)
+        e1.record()
+        torch.cuda.synchronize()
+        opt_ms = e0.elapsed_time(e1)
+        nparam = sum(v.numel() for v in pol.weights.values())
+        del state, grads
+        torch.cuda.empty_cache()
+    except torch.cuda.OutOfMemoryError as ex:
+        torch.cuda.empty_cache()
+        return {"error": f"out of memory: {ex}"[:200]}
+    fl = update_flops_per_seq(w) * n
+    per_seq = bwd_ms / n
+    return {"sequences": n, "tokens_per_seq": T, "backward_ms_per_seq": per_seq,
+            "alg_tflops": fl / (bwd_ms / 1e3) / 1e12,
+            "mfma_frac": fl / (bwd_ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS,
+            "adamw_ms": opt_ms, "params": nparam,
+            "est_batch_update_ms": per_seq * w.batch + opt_ms,
+            "note": "outside the timed step; a slice of the step's batch"}
+
+
 def kernel_bytes(w) -> dict:
     """Algorithmic HBM bytes of one step, per decode-side kernel name: every
     weight byte of the projection once per decode step, plus its activation rows
@@ -380,6 +444,9 @@ def main():
                        "kernel": dom, "launches": n, "avg_us": 1e3 * t / n,
                        "algorithmic_bytes_per_launch": kb[dom] / n}
     out["decode_kernels_gbs"] = {k: kb[k] / (prof[k][1] / 1e3) / 1e9 for k in kb if k in prof}
+    if w.score:
+        out["update"] = update_measure(w, it, pol, api, torch)
+        log("[bench] update measured")
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, host, args.cpu_budget)
     print(json.dumps(out), flush=True)

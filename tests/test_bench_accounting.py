@@ -69,6 +69,18 @@ def test_score_flops():
     assert shared / 1e15 == pytest.approx(2.3126, rel=1e-3)
 
 
+def test_update_flops_per_sequence():
+    """Gradient of one sequence's scored log-probs: three forwards' worth of the
+    projections over all T rows, causal attention and the head on the Tn scored
+    rows (186.3 TFLOP at the 7B shape)."""
+    b = _bench()
+    w = get("7b")
+    proj = 2 * (d * (Hq + 2 * Hk) * hd + Hq * hd * d + 3 * d * f)
+    fwd = L * proj * T + 4 * L * Hq * hd * T * (T + 1) / 2 + 2 * V * d * Tn
+    assert b.update_flops_per_seq(w) == pytest.approx(3 * fwd)
+    assert 3 * fwd / 1e12 == pytest.approx(186.33, rel=1e-3)
+
+
 def test_attention_traffic_fit():
     """The counter fit (fixed + per generated position) at the mean of 1024
     generated positions; null when the kernel source changed."""
