@@ -149,7 +149,7 @@ int decode_target() {
   }();
   return v;
 }
-constexpr int kScoreTokens = 131072;   // rows per scoring chunk (sequences * T)
+constexpr int kScoreTokens = 262144;   // rows per scoring chunk (sequences * T)
 constexpr int kBackwardTokens = 16384; // longest sequence of the backward pass
 constexpr size_t kLogitBytes = size_t(1) << 30;  // LM-head logits per scoring sub-chunk
 
