@@ -151,6 +151,7 @@ def update_measure(w, it, pol, api, torch, n_seqs: int = 2) -> dict:
         torch.cuda.synchronize()
         bwd_ms = e0.elapsed_time(e1)
         del ws
+        torch.cuda.empty_cache()
         # a copy of the weights (the model itself stays as it is), fp32 masters, moments
         state = {k: (v.clone(), v.float() if c.dtype == 1 else None,
                      torch.zeros_like(v, dtype=torch.float32),

@@ -109,6 +109,35 @@ class GrpoIteration:
                        w.beta, 0, self.loss, self.tok_loss, self.dloss, self.stats,
                        ws=self.ws_loss)
 
+    def update(self, lr: float = 1e-5, beta1: float = 0.9, beta2: float = 0.95,
+               eps: float = 1e-8, weight_decay: float = 0.0, micro_batch: int = 1):
+        """The gradient step that closes the iteration (Alg. 1): the policy's
+        weight gradient of the token loss (grpo_policy_backward over the batch,
+        micro_batch sequences per call, dL/dlogp from grpo()), then AdamW on fp32
+        master weights (created on the first call) and a repack of the decode
+        copy.  Returns the step number."""
+        w, pol = self.w, self.policy
+        if not hasattr(self, "_opt"):
+            self._opt = {k: (v.float() if w.model.dtype == 1 else None,
+                             torch.zeros(v.shape, dtype=torch.float32, device=v.device),
+                             torch.zeros(v.shape, dtype=torch.float32, device=v.device))
+                         for k, v in pol.weights.items()}
+            self._grads = api.Grads(pol)
+            self._ws_bwd = api.alloc_workspace(pol, api.OP_BACKWARD, micro_batch, self.T)
+            self._step = 0
+        self._grads.zero_()
+        for n0 in range(0, self.B, micro_batch):
+            n1 = min(self.B, n0 + micro_batch)
+            api.policy_backward(pol, self.seqs[n0:n1], w.prompt_len, w.temperature,
+                                self.dloss[n0:n1], self._grads, ws=self._ws_bwd)
+        self._step += 1
+        for k, v in pol.weights.items():
+            mst, m1, m2 = self._opt[k]
+            api.adamw_step(w.model.dtype, v, mst, m1, m2, self._grads.t[k], lr=lr, beta1=beta1,
+                           beta2=beta2, eps=eps, weight_decay=weight_decay, step=self._step)
+        pol.pack_decode()
+        return self._step
+
     def run(self):
         """One full pass of the hot path."""
         self.prefill()

@@ -119,3 +119,48 @@ def test_adamw_matches_oracle(dtype):
         np.testing.assert_allclose(v.double().cpu().numpy(), v_ref, rtol=1e-5, atol=1e-7)
         if dtype == 1:   # the model copy is the master rounded to bf16
             assert torch.equal(param, master.to(torch.bfloat16))
+
+
+@pytest.mark.parametrize("name,layers", [("tiny", 2), ("small", 2)])
+def test_grpo_iteration_with_update_lowers_its_loss(name, layers):
+    """A whole Alg. 1 iteration: rollout, scoring, advantages and loss, then the
+    gradient step (backward over the batch + AdamW, decode copy repacked).  On the
+    same sampled batch the loss after the step is lower.  On the fp32 model its
+    change also matches the first-order prediction sum(g * dw) from the GPU's own
+    gradient and the weights' actual change (5e-2 relative).  bf16 weights only
+    move in steps of their rounding, so the first AdamW step (every weight moved
+    by about lr) has to be large enough to change them, which puts it outside
+    the first-order regime; there only the decrease is asserted."""
+    require_gpu()
+    from paper_2510_17158_amd import synth
+    from paper_2510_17158_amd.runner import GrpoIteration
+    from paper_2510_17158_amd.workloads import get, truncated
+    w = truncated(get(name), layers, n_prompts=2, group=4, prompt_len=48, new_tokens=24,
+                  temperature=1.0, top_k=0)
+    cfg = w.model
+    host, model = build_model(cfg, w.master_seed, gain_noise=0.1)
+    ref_host = synth.make_weights(cfg, w.master_seed, ref=True)
+    ref = api.Model(cfg, api.upload_weights(cfg, ref_host), decode=False)
+    it = GrpoIteration(w, model, ref, synth.make_prompts(w), synth.make_rewards(w), 11)
+    it.run()
+    torch.cuda.synchronize()
+    l0 = it.loss.item()
+    before = {k: v.double().clone() for k, v in model.weights.items()}
+    it.update(lr=1e-5 if cfg.dtype == DTYPE_F32 else 2e-4)
+    torch.cuda.synchronize()
+    pred = sum(float((it._grads.t[k].double() * (v.double() - before[k])).sum())
+               for k, v in model.weights.items())
+    it.score()
+    it.grpo()
+    torch.cuda.synchronize()
+    l1 = it.loss.item()
+    say(name, "loss", l0, "->", l1, "first-order", pred)
+    assert l1 < l0 and pred < 0
+    if cfg.dtype == DTYPE_F32:
+        assert abs((l1 - l0) - pred) <= 5e-2 * abs(pred) + 1e-7
+    # the next rollout decodes with the updated weights (decode copy repacked)
+    it.run()
+    torch.cuda.synchronize()
+    assert np.isfinite(it.loss.item())
+    model.close()
+    ref.close()
