@@ -288,8 +288,11 @@ int grpo_extend(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len, 
 /* Teacher-forced scoring (Eq. 1's log pi and the KL term's reference): for
  * j in [score_from, T): logp_out[n, j - score_from] =
  * log_softmax(logits at position j-1 / temperature)[tokens[n, j]]
- * (temperature 0 is read as 1).  tokens int32 [N, T]; 1 <= score_from < T.
- * trace: NULL or the intermediates to capture (see grpo_trace). */
+ * (temperature 0 is read as 1; a token outside [0, vocab) is read as the
+ * nearest id).  tokens int32 [N, T]; 1 <= score_from < T.  The log-softmax is
+ * fused into the LM-head product: the [rows, vocab] logits are not stored.
+ * trace: NULL or the intermediates to capture (see grpo_trace; its logits are
+ * then computed by a second product). */
 int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, int32_t T,
                          int32_t score_from, float temperature, float* logp_out,
                          const grpo_trace* trace, void* ws, size_t ws_bytes, void* stream);

@@ -151,7 +151,7 @@ int decode_target() {
 }
 constexpr int kScoreTokens = 262144;   // rows per scoring chunk (sequences * T)
 constexpr int kBackwardTokens = 16384; // longest sequence of the backward pass
-constexpr size_t kLogitBytes = size_t(1) << 30;  // LM-head logits per scoring sub-chunk
+constexpr size_t kHeadBytes = size_t(1) << 30;   // LM-head working set per scoring sub-chunk
 
 // bump allocator over the caller's workspace; base == nullptr only measures
 struct Bump {
@@ -397,25 +397,34 @@ ExtendWS take_extend(Bump& b, const grpo_config& c, int B, int max_len) {
 
 struct ScoreWS {
   int chunk;         // sequences per chunk
-  int sub_rows;      // LM-head rows per logits sub-chunk
+  int sub_rows;      // LM-head rows per sub-chunk, at most
   StepWS s;
   void* kbuf; void* vbuf; uint16_t* vt;
-  void* hs;
-  float* logits;
+  void* hs;          // the sub-chunk's normed final hidden rows
+  float* lse;        // its LM-head log-sum-exp pieces: [rows][lse_slots(V)] (max, sum)
+  float* tgt_z;      // its target logits
 };
 ScoreWS take_score(Bump& b, const grpo_config& c, int N, int T) {
   ScoreWS w;
   w.chunk = std::max(1, std::min(N, kScoreTokens / std::max(T, 1)));
   const size_t M = (size_t)w.chunk * T;
-  w.sub_rows = (int)std::max<size_t>(64, std::min<size_t>(8192, kLogitBytes / ((size_t)c.vocab * 4)));
+  const size_t per_row = (size_t)c.d_model * esize(c) + (size_t)lse_slots(c.vocab) * 8 + 4;
+  w.sub_rows = (int)std::min<size_t>(M, std::max<size_t>(256, kHeadBytes / per_row / 256 * 256));
   w.s = take_step(b, c, (int)M, (int)M, 0, T);
   const size_t kvn = (size_t)w.chunk * kvdim(c) * T;
   w.kbuf = b.take<char>(kvn * esize(c));
   w.vbuf = b.take<char>(c.dtype == GRPO_F32 ? kvn * 4 : 0);
   w.vt = b.take<uint16_t>(c.dtype == GRPO_F32 ? 0 : (size_t)w.chunk * kvdim(c) * round8(T));
   w.hs = b.take<char>((size_t)w.sub_rows * c.d_model * esize(c));
-  w.logits = b.take<float>((size_t)w.sub_rows * c.vocab);
+  w.lse = b.take<float>((size_t)w.sub_rows * lse_slots(c.vocab) * 2);
+  w.tgt_z = b.take<float>((size_t)w.sub_rows);
   return w;
+}
+// Rows per LM-head sub-chunk for R scored rows: the fewest sub-chunks of at most
+// sub_rows rows, of equal size in multiples of 256 (the last one shorter).
+int head_step(const ScoreWS& w, int R) {
+  const int n = (R + w.sub_rows - 1) / w.sub_rows;
+  return std::min(w.sub_rows, ((R + n - 1) / n + 255) / 256 * 256);
 }
 
 WStack qkv_stack(const grpo_model* m, int l) {
@@ -504,13 +513,30 @@ int forward_rows(const grpo_model* m, StepWS& w, int M, int T, int G, int n_slot
 }
 
 // head rows [off, off + M) of a scoring trace: normed input and logits
-int score_head_trace(const grpo_config& c, const grpo_trace* tr, size_t R, const void* hs,
-                     const float* logits, int M, int off, hipStream_t st) {
+// LM head of `rows` normed rows (w.hs) with the log-softmax at each row's
+// target fused into the product (Alg. 1 scoring, log pi of the sampled token):
+// the product's epilogue leaves per-row log-sum-exp pieces and the target
+// logit, lse_combine turns them into logp; the [rows, V] logits are never
+// stored.  Row r is scored row i0 + r of the chunk's tokens tk.  With a trace,
+// the normed rows and (by a second product into the trace itself) the logits
+// are recorded at trace rows off ...; R = the trace's rows.
+int score_head(const grpo_model* m, const ScoreWS& w, int rows, const int32_t* tk, int T,
+               int score_from, int Ts, int i0, float temperature, float* logp,
+               const grpo_trace* tr, size_t R, int off, hipStream_t st) {
+  const grpo_config& c = m->cfg;
+  const int d = c.d_model, slots = lse_slots(c.vocab);
+  const float t = temperature > 0.f ? temperature : 1.f;
+  EpiArgs ep{w.lse, nullptr, slots};
+  ep.lse = LseArgs{tk, T, Ts, score_from, i0, 1.44269504088896341f / t, w.tgt_z};
+  if (int rc = gemm_rows(m, w.hs, d, rows, one(m->lm_head), c.vocab, d, EPI_LSE, ep, st)) return rc;
+  HIPCHK(lse_combine(w.lse, slots, w.tgt_z, rows, t, logp, st));
   if (!tr) return GRPO_OK;
-  if (int rc = trace(tr->h_final, 0, R, c.d_model, hs, c.dtype == GRPO_F32 ? TR_F32 : TR_BF16,
-                     c.d_model, M, TraceMap::rows(off), st))
+  if (int rc = trace(tr->h_final, 0, R, d, w.hs, c.dtype == GRPO_F32 ? TR_F32 : TR_BF16, d, rows,
+                     TraceMap::rows(off), st))
     return rc;
-  return trace(tr->logits, 0, R, c.vocab, logits, TR_F32, c.vocab, M, TraceMap::rows(off), st);
+  if (!tr->logits) return GRPO_OK;
+  return gemm_rows(m, w.hs, d, rows, one(m->lm_head), c.vocab, d, EPI_STORE,
+                   EpiArgs{tr->logits + (size_t)off * c.vocab, nullptr, c.vocab}, st);
 }
 
 int check_sampling(const grpo_sampling* s, int vocab) {
@@ -1215,19 +1241,15 @@ int grpo_score_sequences(const grpo_model* m, const int32_t* tokens, int32_t N, 
                               c.dtype == GRPO_F32 ? w.vbuf : nullptr, w.vt, trace_out,
                               (size_t)N * T, TraceMap::rows(n0 * T), st))
       return rc;
-    const int R = C * Ts;
-    for (int i0 = 0; i0 < R; i0 += w.sub_rows) {
-      const int rc_rows = std::min(w.sub_rows, R - i0);
+    const int R = C * Ts, step = head_step(w, R);
+    for (int i0 = 0; i0 < R; i0 += step) {
+      const int rc_rows = std::min(step, R - i0);
       HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{i0, Ts, T, score_from - 1}, none, m->final_norm,
                      rc_rows, d, c.rms_eps, w.hs, d, st));
-      if (int rc = gemm_rows(m, w.hs, d, rc_rows, one(m->lm_head), c.vocab, d, EPI_STORE,
-                             EpiArgs{w.logits, nullptr, c.vocab}, st))
+      if (int rc = score_head(m, w, rc_rows, tk, T, score_from, Ts, i0, temperature,
+                              logp_out + (size_t)n0 * Ts + i0, trace_out, (size_t)N * Ts,
+                              n0 * Ts + i0, st))
         return rc;
-      if (int rc = score_head_trace(c, trace_out, (size_t)N * Ts, w.hs, w.logits, rc_rows,
-                                    n0 * Ts + i0, st))
-        return rc;
-      HIPCHK(token_logprob(w.logits, rc_rows, c.vocab, c.vocab, tk, T, score_from, Ts, i0,
-                           temperature, logp_out + (size_t)n0 * Ts + i0, st));
     }
   }
   g_err.clear();
@@ -1342,19 +1364,15 @@ int grpo_score_sequences_grouped(const grpo_model* m, const int32_t* tokens, int
     }
     if ((rc = tr2(TRM(trace_out, x), c.n_layers, d, w.s.x, TR_F32, d, 4))) return rc;
     // logits of positions score_from - 1 .. T - 2: own rows of each sequence
-    const int R = Cc * Ts;
-    for (int i0 = 0; i0 < R; i0 += w.sub_rows) {
-      const int rc_rows = std::min(w.sub_rows, R - i0);
+    const int R = Cc * Ts, step = head_step(w, R);
+    for (int i0 = 0; i0 < R; i0 += step) {
+      const int rc_rows = std::min(step, R - i0);
       HIPCHK(rmsnorm(c.dtype, w.s.x, d, RowMap{i0, Ts, Tb, M1 + score_from - 1 - P0}, none,
                      m->final_norm, rc_rows, d, c.rms_eps, w.hs, d, st));
-      if ((rc = gemm_rows(m, w.hs, d, rc_rows, one(m->lm_head), c.vocab, d, EPI_STORE,
-                          EpiArgs{w.logits, nullptr, c.vocab}, st)))
+      if ((rc = score_head(m, w, rc_rows, tk, T, score_from, Ts, i0, temperature,
+                           logp_out + (size_t)n0 * Ts + i0, trace_out, (size_t)N * Ts,
+                           n0 * Ts + i0, st)))
         return rc;
-      if ((rc = score_head_trace(c, trace_out, (size_t)N * Ts, w.hs, w.logits, rc_rows,
-                                 n0 * Ts + i0, st)))
-        return rc;
-      HIPCHK(token_logprob(w.logits, rc_rows, c.vocab, c.vocab, tk, T, score_from, Ts, i0,
-                           temperature, logp_out + (size_t)n0 * Ts + i0, st));
     }
   }
   g_err.clear();

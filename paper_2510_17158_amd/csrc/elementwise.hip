@@ -306,26 +306,24 @@ __global__ void k_fill_i32(int32_t* p, size_t n, int32_t v) {
   if (i < n) p[i] = v;
 }
 
-// logp[r] = z[r, target] - LSE(z[r, :]), one workgroup per row, fp32
-__global__ __launch_bounds__(256) void k_token_logprob(const float* logits, int V, int ld,
-                                                       const int32_t* tokens, int T,
-                                                       int score_from, int Ts, int i0, float temp,
-                                                       float* logp) {
-  __shared__ float sh[4];
-  const int r = blockIdx.x;
-  const int gi = i0 + r;
-  const int tgt = tokens[(size_t)(gi / Ts) * T + score_from + gi % Ts];
-  const float* l = logits + (size_t)r * ld;
+// logp[r] from the LM head's log-sum-exp pieces: one wave per row, slots read
+// lane-strided (fixed order), then the wave's max and sum.
+__global__ __launch_bounds__(256) void k_lse_combine(const float2* __restrict__ part, int slots,
+                                                     const float* __restrict__ tgt_z, int R,
+                                                     float temp, float* __restrict__ logp) {
+  const int r = blockIdx.x * 4 + threadIdx.x / 64, lane = threadIdx.x % 64;
+  if (r >= R) return;                       // whole waves
+  const float2* p = part + (size_t)r * slots;
   float mx = -INFINITY;
-  for (int i = threadIdx.x; i < V; i += 256) mx = fmaxf(mx, l[i] / temp);
-  mx = block_max<256>(mx, sh);
-  float s = 0.f;
-  for (int i = threadIdx.x; i < V; i += 256) s += __expf(l[i] / temp - mx);
-  s = block_sum<256>(s, sh);
-  if (threadIdx.x == 0) {
-    const int t = clampi(tgt, 0, V - 1);
-    logp[r] = l[t] / temp - (mx + logf(s));
+  for (int s = lane; s < slots; s += 64) mx = fmaxf(mx, p[s].x);
+  mx = wave_max(mx);
+  float sum = 0.f;
+  for (int s = lane; s < slots; s += 64) {
+    const float2 v = p[s];
+    sum = fmaf(v.y, __builtin_amdgcn_exp2f(v.x - mx), sum);
   }
+  sum = wave_sum(sum);
+  if (lane == 0) logp[r] = tgt_z[r] / temp - 0.693147180559945309f * (mx + __log2f(sum));
 }
 
 }  // namespace
@@ -431,13 +429,13 @@ hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeAr
   return hipGetLastError();
 }
 
-hipError_t token_logprob(const float* logits, int R, int V, int ld, const int32_t* tokens, int T,
-                         int score_from, int Ts, int i0, float temperature, float* logp,
-                         hipStream_t st) {
+hipError_t lse_combine(const float* part, int slots, const float* tgt_z, int R,
+                       float temperature, float* logp, hipStream_t st) {
   if (R <= 0) return hipSuccess;
+  if (slots < 1) return hipErrorInvalidValue;
   const float t = temperature > 0.f ? temperature : 1.f;
-  Prof pf("token_logprob", st);
-  k_token_logprob<<<R, 256, 0, st>>>(logits, V, ld, tokens, T, score_from, Ts, i0, t, logp);
+  Prof pf("lse_combine", st);
+  k_lse_combine<<<(R + 3) / 4, 256, 0, st>>>((const float2*)part, slots, tgt_z, R, t, logp);
   return hipGetLastError();
 }
 

@@ -29,7 +29,15 @@ struct TArgs {
   int N, K, tiles_m, tiles_n;
   float* out_f32; bf16_t* out_act; int ld_out;
   GemmBatch bt;     // product b of a batch: blockIdx.y of the tiled kernel
+  LseArgs lse;      // EPI_LSE
 };
+
+// EPI_LSE: the target column of product row m (clamped to the columns)
+__device__ __forceinline__ int lse_target(const LseArgs& l, int m, int N) {
+  const int g = l.i0 + m;
+  const int t = l.tokens[(size_t)(g / l.Ts) * l.T + l.score_from + g % l.Ts];
+  return min(max(t, 0), N - 1);
+}
 
 // operands and output of batch product b
 __device__ __forceinline__ void batch_offset(TArgs& a, int b) {
@@ -142,6 +150,42 @@ __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
   }
 
   // ---- epilogue ----
+  if (EPI == EPI_LSE) {
+    // slot tn * 2 + wn = the wave's 64 columns; a row's 64 values sit in the 16
+    // lanes of its lane group (4 columns each): in-lane, then across the group
+    const int slot = tn * 2 + wn;
+    if (slot >= a.ld_out) return;            // (tile half past the last column)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = tm * BM + wm * 64 + i * 16 + (lane >> 4) * 4 + v;
+        float x[4], mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = tn * BN + wn * 64 + j * 16 + (lane & 15);
+          x[j] = n < a.N ? acc[i][j][v] * a.lse.c : -INFINITY;
+          mx = fmaxf(mx, x[j]);
+        }
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+        float s = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s += __builtin_amdgcn_exp2f(x[j] - mx);
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o, 64);
+        if (m < a.M) {
+          if ((lane & 15) == 0)
+            *(float2*)(a.out_f32 + ((size_t)m * a.ld_out + slot) * 2) = make_float2(mx, s);
+          const int t = lse_target(a.lse, m, a.N);
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (tn * BN + wn * 64 + j * 16 + (lane & 15) == t) a.lse.tgt_z[m] = acc[i][j][v];
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -329,7 +373,41 @@ __global__ __launch_bounds__(256) void k_gemm_big(TArgs a) {
   // acc[i][j][r] is row 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4, column
   // 32 j + (lane & 31) of the wave's 128 x 128 quarter.
   __syncthreads();
-  if (EPI == EPI_SWIGLU) {
+  if (EPI == EPI_LSE) {
+    // 32 rows of the wave's quarter staged as for the store; lane (row, half)
+    // then reduces that row's 64 columns of slot half (its 16-byte pieces read
+    // back in order) and, when the row's target lies there, passes its logit on
+    constexpr int SR = 132;
+    float* stg = reinterpret_cast<float*>(&lds[0][0][0]) + wave * 32 * SR;
+    const int row = lane & 31, half = lane >> 5;
+    const int c0 = tn * GB + wn * 128 + half * 64;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          stg[((r / 4) * 8 + (lane >> 5) * 4 + (r % 4)) * SR + j * 32 + (lane & 31)] = acc[i][j][r];
+      float x[64], mx = -INFINITY;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const float4 v = *(const float4*)(stg + row * SR + half * 64 + 4 * k);
+        x[4 * k] = v.x * a.lse.c; x[4 * k + 1] = v.y * a.lse.c;
+        x[4 * k + 2] = v.z * a.lse.c; x[4 * k + 3] = v.w * a.lse.c;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, x[4 * k + e]);
+      }
+      float s = 0.f;
+#pragma unroll
+      for (int k = 0; k < 64; ++k) s += __builtin_amdgcn_exp2f(x[k] - mx);
+      const int m = m0 + wm * 128 + i * 32 + row;
+      if (m >= tm * GB) {
+        *(float2*)(a.out_f32 + ((size_t)m * a.ld_out + c0 / 64) * 2) = make_float2(mx, s);
+        const int t = lse_target(a.lse, m, a.N);
+        if (t >= c0 && t < c0 + 64) a.lse.tgt_z[m] = stg[row * SR + half * 64 + (t - c0)];
+      }
+    }
+  } else if (EPI == EPI_SWIGLU) {
     constexpr int SR = 72;   // staged row: 64 outputs + 8 pad (bf16)
     bf16_t* stg = &lds[0][0][0] + wave * 32 * SR;
 #pragma unroll
@@ -388,6 +466,7 @@ struct FArgs {
   int N, K, epi;
   float* out_f32; float* out_act; int ld_out;
   GemmBatch bt;     // product b of a batch: blockIdx.z
+  LseArgs lse;      // EPI_LSE
 };
 
 __device__ __forceinline__ const float* frow(const FArgs& a, int n) {
@@ -444,6 +523,36 @@ __global__ __launch_bounds__(256) void k_gemm_f32(FArgs a) {
       __syncthreads();
     }
   }
+  if (a.epi == EPI_LSE) {
+    // slot blockIdx.x = the tile's 64 columns; a row's values sit in the 16
+    // lanes tx of its lane group (4 columns each)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + ty * 4 + i;
+      float x[4], mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[j] = n0 + tx * 4 + j < a.N ? acc[i][j] * a.lse.c : -INFINITY;
+        mx = fmaxf(mx, x[j]);
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+      float s = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) s += __builtin_amdgcn_exp2f(x[j] - mx);
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o, 64);
+      if (m < a.M) {
+        if (tx == 0)
+          *(float2*)(a.out_f32 + ((size_t)m * a.ld_out + blockIdx.x) * 2) = make_float2(mx, s);
+        const int t = lse_target(a.lse, m, a.N);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (n0 + tx * 4 + j == t) a.lse.tgt_z[m] = acc[i][j];
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = m0 + ty * 4 + i;
@@ -471,19 +580,24 @@ __global__ __launch_bounds__(256) void k_gemm_f32(FArgs a) {
 hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, int K, int epi,
                            EpiArgs ep, hipStream_t st, GemmBatch bt) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  if (K % BK || bt.count < 1 || bt.wdiv < 1 || (bt.count > 1 && epi == EPI_SWIGLU))
+  if (K % BK || bt.count < 1 || bt.wdiv < 1 ||
+      (bt.count > 1 && (epi == EPI_SWIGLU || epi == EPI_LSE)) ||
+      (epi == EPI_LSE && (ep.ld_out != lse_slots(N) || !ep.lse.tokens || !ep.lse.tgt_z ||
+                          ep.lse.Ts < 1)))
     return hipErrorInvalidValue;
   TArgs a;
   a.bt = bt;
+  a.lse = ep.lse;
   a.X = X; a.ldx = ldx; a.M = M;
   a.w0 = (const bf16_t*)W.w[0]; a.w1 = (const bf16_t*)W.w[1]; a.w2 = (const bf16_t*)W.w[2];
   a.n1 = W.n1; a.n2 = W.n2; a.N = N; a.K = K;
   a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;
-  Prof pf(epi == EPI_SWIGLU ? "gemm_tiled_swiglu" : "gemm_tiled", st);
-  // the big tiles store 16-byte pieces of output rows
-  const bool out16 = epi == EPI_SWIGLU
-                         ? ep.ld_out % 8 == 0 && (uintptr_t)ep.out_act % 16 == 0
-                         : ep.ld_out % 4 == 0 && (uintptr_t)ep.out_f32 % 16 == 0;
+  Prof pf(epi == EPI_SWIGLU ? "gemm_tiled_swiglu" : epi == EPI_LSE ? "gemm_tiled_lse" : "gemm_tiled",
+          st);
+  // the big tiles store 16-byte pieces of output rows (LSE: 8-byte pairs)
+  const bool out16 = epi == EPI_SWIGLU ? ep.ld_out % 8 == 0 && (uintptr_t)ep.out_act % 16 == 0
+                     : epi == EPI_LSE  ? (uintptr_t)ep.out_f32 % 8 == 0
+                                       : ep.ld_out % 4 == 0 && (uintptr_t)ep.out_f32 % 16 == 0;
   const bool aligned = out16 && (epi == EPI_SWIGLU
                            ? W.n1 % 128 == 0
                            : N % GB == 0 && (W.n1 >= N || W.n1 % GB == 0) && (W.n2 >= N || W.n2 % GB == 0));
@@ -496,6 +610,7 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
     switch (epi) {
       case EPI_STORE: k_gemm_big<EPI_STORE><<<grid, 256, 0, st>>>(a); break;
       case EPI_RESID: k_gemm_big<EPI_RESID><<<grid, 256, 0, st>>>(a); break;
+      case EPI_LSE: k_gemm_big<EPI_LSE><<<grid, 256, 0, st>>>(a); break;
       default: k_gemm_big<EPI_SWIGLU><<<grid, 256, 0, st>>>(a); break;
     }
     return hipGetLastError();
@@ -506,6 +621,7 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
   switch (epi) {
     case EPI_STORE: k_gemm_tiled<EPI_STORE><<<grid, NT, 0, st>>>(a); break;
     case EPI_RESID: k_gemm_tiled<EPI_RESID><<<grid, NT, 0, st>>>(a); break;
+    case EPI_LSE: k_gemm_tiled<EPI_LSE><<<grid, NT, 0, st>>>(a); break;
     default: k_gemm_tiled<EPI_SWIGLU><<<grid, NT, 0, st>>>(a); break;
   }
   return hipGetLastError();
@@ -514,9 +630,13 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
 hipError_t gemm_f32(const float* X, int ldx, int M, WStack W, int N, int K, int epi, EpiArgs ep,
                     hipStream_t st, GemmBatch bt) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  if (K % 16 || bt.count < 1 || bt.wdiv < 1) return hipErrorInvalidValue;
+  if (K % 16 || bt.count < 1 || bt.wdiv < 1 ||
+      (epi == EPI_LSE && (bt.count > 1 || ep.ld_out != lse_slots(N) || !ep.lse.tokens ||
+                          !ep.lse.tgt_z || ep.lse.Ts < 1)))
+    return hipErrorInvalidValue;
   FArgs a;
   a.bt = bt;
+  a.lse = ep.lse;
   a.X = X; a.ldx = ldx; a.M = M;
   a.w0 = (const float*)W.w[0]; a.w1 = (const float*)W.w[1]; a.w2 = (const float*)W.w[2];
   a.n1 = W.n1; a.n2 = W.n2; a.N = N; a.K = K; a.epi = epi;

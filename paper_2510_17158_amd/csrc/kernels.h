@@ -20,8 +20,9 @@ bool profiling();
 
 // STORE: out = X W^T;  RESID: out += X W^T;  SWIGLU: out = silu(gate) * up;
 // PARTIAL (decode GEMM only): out[split] = this split's share of X W^T, the
-// consumer adds the splits.
-enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_PARTIAL = 3 };
+// consumer adds the splits;  LSE (row-tile GEMMs, the scoring LM head): the
+// product's log-sum-exp pieces per row instead of the product (LseArgs).
+enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_PARTIAL = 3, EPI_LSE = 4 };
 constexpr int kMaxSplits = 16;
 
 // Up to three weight matrices stacked along the output dimension: output row r
@@ -39,11 +40,27 @@ struct GemmBatch {
   int wdiv = 1;
 };
 
+// EPI_LSE: for product row r (logits z = X W^T of the row, scaled x = c z with
+// c = log2(e) / temperature) and each 64-column slot s (columns 64 s .. 64 s + 63
+// below N), the pair (max_n x_n, sum_n 2^(x_n - max)) at out_f32[(r ld_out + s) 2]
+// (ld_out = lse_slots(N)); the row's target logit z_t at tgt_z[r], the target
+// being tokens[(g / Ts) T + score_from + g % Ts] for g = i0 + r, clamped to
+// [0, N) (the token that follows the row's position).
+struct LseArgs {
+  const int32_t* tokens = nullptr;
+  int T = 0, Ts = 1, score_from = 0, i0 = 0;
+  float c = 0.f;
+  float* tgt_z = nullptr;
+};
+inline int lse_slots(int N) { return (N + 63) / 64; }
+
 struct EpiArgs {
   float* out_f32;       // EPI_STORE: [rows, ld_out] fp32;  EPI_RESID: residual [rows, ld_out]
+                        // EPI_LSE: [rows, ld_out slots] (max, sum) pairs
   void* out_act;        // EPI_SWIGLU: [rows, ld_out] activation dtype
   int ld_out;
   const char* name = nullptr;  // kernel-timing label of a decode GEMM (a string literal)
+  LseArgs lse = {};
 };
 
 // ---- decode GEMM: Y[B, N] = X[B, K] . W[N, K]^T for B <= 128 (bf16 MFMA) ----
@@ -218,12 +235,12 @@ struct SampleArgs {
   const int32_t* seq_ids;   // optional [R*G]: Philox sequence id of draw q
 };
 hipError_t sample(const float* logits, int R, int V, int ld, const SampleArgs& a, hipStream_t st);
-// Teacher-forced log-prob of scored row m (global index gi = i0 + m over
-// sequences of Ts scored positions): n = gi / Ts, j = score_from + gi % Ts,
-// logp[m] = z[m, tokens[n*T + j]] - LSE(z[m, :]), z = logits / temperature.
-hipError_t token_logprob(const float* logits, int R, int V, int ld, const int32_t* tokens, int T,
-                         int score_from, int Ts, int i0, float temperature, float* logp,
-                         hipStream_t st);
+// Teacher-forced log-prob of scored row r, log_softmax(z / temperature) at the
+// row's target, from the LM head's EPI_LSE pieces:
+// logp[r] = z_t[r] / temperature - ln2 (M + log2 S) with M = max_s m_s and
+// S = sum_s s_s 2^(m_s - M) over the row's `slots` (max, sum) pairs.
+hipError_t lse_combine(const float* part, int slots, const float* tgt_z, int R,
+                       float temperature, float* logp, hipStream_t st);
 
 // ---- GRPO ---------------------------------------------------------------------------
 hipError_t advantages(const float* r, int P, int G, float eps, float* adv, hipStream_t st);

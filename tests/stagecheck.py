@@ -161,6 +161,23 @@ def logp_bound(z, logp):
     return U * (h_sum + 8.0 + C_EXP + 4.0 * zmax + 3.0 * abs(lse) + abs(float(logp)))
 
 
+def score_logp_bound(z, logp):
+    """Bound on the scoring head's fp32 log-probability given its logits (z = l / T
+    in fp64 here): the product's epilogue scales x = l * fl(log2(e) / T) (c off by
+    2u, each x by u: 3u |z| in natural-log units), takes per 64-column slot the
+    maximum and sum_n 2^(x_n - max) (arguments u |x - max| <= 2u max|z|, exp2 C_EXP u,
+    at most 64 terms in a chain), then the combine rescales each slot by
+    2^(m_s - M) (another 2u max|z| and C_EXP u, one fused multiply-add) and sums
+    V / 64 / 64 slots per lane over 6 reduction levels; log2, M + log2 S, the
+    product by ln 2 (u |LSE| each), z_t = l_t / T (u |z|) and the difference
+    (u |logp|)."""
+    from bounds import C_EXP, U
+    zmax = float(np.max(np.abs(z)))
+    lse = float(np.max(z) + np.log(np.sum(np.exp(z - np.max(z)))))
+    h_sum = 64.0 + np.ceil(len(z) / 64.0) / 64.0 + 6.0 + 2.0
+    return U * (h_sum + 2.0 * C_EXP + 4.0 + 8.0 * zmax + 3.0 * abs(lse) + abs(float(logp)))
+
+
 def sampler_check(logits, toks, logps, temperature, top_k, seed, step, seq_ids,
                   band: float = 1e-5):
     """The oracle sampler on the GPU's own fp32 logits: tokens bit-exact except at a

@@ -25,7 +25,7 @@ from paper_2510_17158_amd.workloads import get, truncated
 from bounds import Report
 from gpu_util import (LOGIT_TOL, NEAR_TIE, assert_report, build_model, check_decode,
                       check_rows, decode_traced, kv_view, require_gpu, sample_rows, say)
-from stagecheck import logp_bound, sampler_check
+from stagecheck import sampler_check, score_logp_bound
 
 pytestmark = pytest.mark.gpu
 
@@ -376,15 +376,15 @@ def test_grouped_scoring_4096_stage_local():
     rng = np.random.default_rng(7)
     hrows = np.sort(np.concatenate([[0, Ts - 1, N * Ts - 1], rng.integers(0, N * Ts, 13)]))
     xrows = hrows // Ts * T + Tp - 1 + hrows % Ts
-    rep, worst = check_rows(cfg, host, t, T, M_call, rows,
-                            head=(hrows, xrows, min(8192, N * Ts)))
+    # the head is one product over the 8192 scored rows
+    rep, worst = check_rows(cfg, host, t, T, M_call, rows, head=(hrows, xrows, N * Ts))
     assert_report(rep, f"scoring 4096 (worst logit err {worst:.2e})")
     lg = t["logits"][hrows]
     lpg = lp.cpu().numpy().ravel()[hrows]
     tgt = seqs.ravel()[(hrows // Ts) * T + Tp + hrows % Ts]
     for i in range(len(hrows)):
         ref = oracle.log_softmax(lg[i])[tgt[i]]
-        assert abs(lpg[i] - ref) <= logp_bound(lg[i], ref), (i, lpg[i], ref)
+        assert abs(lpg[i] - ref) <= score_logp_bound(lg[i], ref), (i, lpg[i], ref)
     model.close()
 
 
