@@ -200,7 +200,11 @@ def kernel_bytes(w) -> dict:
         "gemm_decode_o": n_dec * L * (d * qd * es + B * qd * es + B * d * 4),
         "gemm_decode_swiglu": n_dec * L * (2 * f * d * es + B * d * es + B * f * es),
         "gemm_decode_down": n_dec * L * (d * f * es + B * f * es + B * d * 4),
-        "gemm_decode_lm_head": n_dec * (V * d * es + B * d * es + B * V * 4),
+        # without a top-k cut (bf16) the LM head writes the sampler's 32-byte pieces
+        # per row and 128-id tile instead of the logits
+        "gemm_decode_lm_head": n_dec * (V * d * es + B * d * es +
+                                        (B * -(-V // 128) * 32 if es == 2 and (w.top_k <= 0 or w.top_k >= V)
+                                         else B * V * 4)),
     }
     if w.shared_prompt:
         out["attn_prefix"] = n_dec * L * w.n_prompts * w.prompt_len * kv_layer_tok

@@ -222,7 +222,9 @@ int grpo_prefill(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_len,
  *              kernels additionally never touch positions >= max_len.
  *   tok_out    int32 [B, n_steps];  logp_out  fp32 [B, n_steps]
  *   trace      NULL or the intermediates of the last step (see grpo_trace)
- * B <= 128 for bf16 models.  With n_steps >= 2 and no trace the step is
+ * B <= 128 for bf16 models.  On bf16 models without a top-k cut the draw is
+ * fused into the LM head (its logits are not stored; the same tokens as the
+ * sampler on those logits).  With n_steps >= 2 and no trace the step is
  * captured once as a HIP graph and replayed n_steps times; the graph is kept in
  * the model handle and recaptured when an argument changes, so a handle must
  * not be used from two threads at once.  GRPO_INVALID_ARG for seq_ids out of

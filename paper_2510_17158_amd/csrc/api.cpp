@@ -250,6 +250,23 @@ int gemm_dec(const void* Xf, int B, const uint16_t* Wf, int N, int K, float* out
   return e == hipSuccess ? GRPO_OK : gemm_fail(e);
 }
 
+// The decode LM head with the sampling epilogue: per-tile pieces of the draw
+// `sa` describes into part ([B][*tiles][8]); the logits into `logits` too if set.
+int gemm_dec_sample(const void* Xf, int B, const uint16_t* Wf, int N, int K, const SampleArgs& sa,
+                    float* part, float* logits, int* tiles, hipStream_t st) {
+  const DecodePlan p = decode_plan(B, N, K, EPI_PARTIAL, decode_target(), 1);
+  EpiArgs ep{logits, nullptr, N, "gemm_decode_lm_head"};
+  ep.smp.temperature = sa.temperature;
+  ep.smp.seed = sa.seed;
+  ep.smp.step = sa.step;
+  ep.smp.step_ctr = sa.step_ctr;
+  ep.smp.seq_ids = sa.seq_ids;
+  ep.smp.part = part;
+  *tiles = p.tiles;
+  const hipError_t e = gemm_decode_bf16((const uint16_t*)Xf, B, Wf, N, K, EPI_SAMPLE, ep, p, st);
+  return e == hipSuccess ? GRPO_OK : gemm_fail(e);
+}
+
 // residual projection: the product is left in *pend for the next RMSNorm to add
 int gemm_dec_resid(const void* Xf, int B, const uint16_t* Wf, int N, int K, GemmScratch s,
                    Partials* pend, hipStream_t st, const char* name) {
@@ -337,7 +354,8 @@ StepWS take_step(Bump& b, const grpo_config& c, int rows, int act_rows, size_t p
 
 struct RolloutWS {
   StepWS s;
-  float* logits;
+  float* logits;       // the LM head's logits (sampling with a top-k cut, fp32 models)
+  float* spart;        // the sampling epilogue's per-tile pieces [B][tiles][8] (bf16)
   float* attn_part;
   int32_t* step_ctr;   // decode steps done by the replayed graph
   int32_t* slots;      // [B] cache slot / Philox sequence id of each row (seq_ids)
@@ -346,6 +364,8 @@ RolloutWS take_rollout(Bump& b, const grpo_config& c, int B, int max_len) {
   RolloutWS w;
   w.s = take_step(b, c, B, c.dtype == GRPO_F32 ? B : decode_nb(B), decode_scratch(c, B), B);
   w.logits = b.take<float>((size_t)B * c.vocab);
+  // tiles of at least 32 vocabulary rows (16 rb, rb >= 2)
+  w.spart = b.take<float>(c.dtype == GRPO_F32 ? 0 : (size_t)B * ((c.vocab + 31) / 32) * 8);
   w.attn_part = b.take<float>(
       c.dtype == GRPO_F32 ? 0
                           : decode_attn_part_floats_max(B, c.n_heads, c.n_kv_heads, c.head_dim,
@@ -1112,6 +1132,29 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
     if ((rc = trace(TRM(tr, x), c.n_layers, B, d, w.s.x, TR_F32, d, B, rows, st)) ||
         (rc = trace(TRM(tr, h_final), 0, B, d, w.s.h, act, pk ? act_ld : d, B, rows, st)))
       return rc;
+    SampleArgs sa{};
+    sa.temperature = s->temperature; sa.top_k = s->top_k; sa.seed = s->seed;
+    sa.G = 1; sa.out_stride = n_steps;
+    sa.tok_state = tok; sa.pos_state = pos; sa.seq_ids = slots;
+    if (graph) {
+      sa.step = step0; sa.step_ctr = w.step_ctr;
+      sa.tok_out = tok_out; sa.logp_out = logp_out;
+    } else {
+      sa.step = step0 + step; sa.step_ctr = nullptr;
+      sa.tok_out = tok_out + step; sa.logp_out = logp_out + step;
+    }
+    // without a top-k cut the LM head's epilogue reduces its logits to the
+    // sampler's per-tile pieces (the logits are stored only for a trace)
+    if (pk && (s->top_k <= 0 || s->top_k >= c.vocab)) {
+      float* lg = TRM(tr, logits) ? w.logits : nullptr;
+      int tiles = 0;
+      if ((rc = gemm_dec_sample(w.s.h, B, D.lm_head, c.vocab, d, sa, w.spart, lg, &tiles, st)))
+        return rc;
+      if ((rc = trace(TRM(tr, logits), 0, B, c.vocab, w.logits, TR_F32, c.vocab, B, rows, st)))
+        return rc;
+      HIPCHK(sample_combine(w.spart, tiles, B, c.vocab, sa, st));
+      return GRPO_OK;
+    }
     if (pk) {
       const float* res;
       int ns;
@@ -1125,17 +1168,6 @@ static int rollout(const grpo_model* m, void* kv, int32_t n_seqs, int32_t max_le
     }
     if ((rc = trace(TRM(tr, logits), 0, B, c.vocab, w.logits, TR_F32, c.vocab, B, rows, st)))
       return rc;
-    SampleArgs sa{};
-    sa.temperature = s->temperature; sa.top_k = s->top_k; sa.seed = s->seed;
-    sa.G = 1; sa.out_stride = n_steps;
-    sa.tok_state = tok; sa.pos_state = pos; sa.seq_ids = slots;
-    if (graph) {
-      sa.step = step0; sa.step_ctr = w.step_ctr;
-      sa.tok_out = tok_out; sa.logp_out = logp_out;
-    } else {
-      sa.step = step0 + step; sa.step_ctr = nullptr;
-      sa.tok_out = tok_out + step; sa.logp_out = logp_out + step;
-    }
     HIPCHK(sample(w.logits, B, c.vocab, c.vocab, sa, st));
     return GRPO_OK;
   };

@@ -115,3 +115,29 @@ __device__ __forceinline__ void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" :
 __device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
+
+// ---- sampling draws (the sampler and the decode LM head's sampling epilogue) ------
+// Philox4x32-10 (Salmon et al., SC'11): counter c, key (k0, k1), ten rounds.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+  }
+  return c;
+}
+// Gumbel-max key of logit x at temperature T from one Philox word w:
+// u = (2 (w >> 9) + 1) 2^-24 in (0, 1), key = x / T - ln(-ln u).
+__device__ __forceinline__ float gumbel_key(float x, float T, uint32_t w) {
+  const float u = (float)(2u * (w >> 9) + 1u) * 5.9604644775390625e-8f;   // 2^-24
+  return x / T - logf(-logf(u));
+}
+// (value desc, id asc) arg-max merge
+__device__ __forceinline__ void better(float& bv, int& bi, float v, int i) {
+  if (v > bv || (v == bv && i < bi)) { bv = v; bi = i; }
+}
+

@@ -51,7 +51,13 @@ struct DArgs {
   const bf16_t* W;    // fragment order [K/32][N/16]
   int B, N, K, kper, tiles;
   float* out_f32; bf16_t* out_act; int ld_out;
+  DecSample smp;      // EPI_SAMPLE
 };
+
+// Gumbel-max merge carrying the winner's logit: (key desc, id asc)
+__device__ __forceinline__ void better_g(float& gk, int& gi, float& gz, float k, int i, float z) {
+  if (k > gk || (k == gk && i < gi)) { gk = k; gi = i; gz = z; }
+}
 
 // ring slot S <- step i (clamped to the last step: the repeat is never used)
 #define DG_LOAD(S, i)                                                           \
@@ -170,6 +176,73 @@ void k_gemm_decode(DArgs a) {
         *(u32x4_t*)(a.out_act + act_frag_index(b, n, NB)) = w;
       }
     }
+  } else if (EPI == EPI_SAMPLE) {
+    // the tile's pieces of the sampler (DecSample): four threads per batch row,
+    // thread t taking rows (vocabulary ids) 4 RB t .. 4 RB t + 4 RB - 1 in groups
+    // of four (one Philox block each); the four merged by shuffles in a fixed order
+    const bool greedy = !(a.smp.temperature > 0.f);
+    const float T = greedy ? 1.f : a.smp.temperature;
+    const int step = a.smp.step + (a.smp.step_ctr ? *a.smp.step_ctr : 0);
+    const uint32_t k0 = (uint32_t)a.smp.seed, k1 = (uint32_t)(a.smp.seed >> 32);
+    for (int i = tid; i < 4 * NB; i += NT) {       // whole waves (NB >= 16)
+      const int b = i >> 2, t4 = i & 3;
+      const bool live = b < a.B;
+      float x[RB][4];
+      float m = -INFINITY;
+      int mi = 0x7fffffff;
+#pragma unroll
+      for (int q = 0; q < RB; ++q) {
+        const int r = (t4 * RB + q) * 4, n0 = tile * ROWS + r;
+        const f32x4_t v = val4(b, r);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          x[q][e] = n0 + e < a.N ? v[e] : -INFINITY;
+          better(m, mi, x[q][e], n0 + e);
+        }
+        if (a.out_f32 && live && n0 < a.N)
+          *(f32x4_t*)(a.out_f32 + (size_t)b * a.ld_out + n0) = v;
+      }
+#pragma unroll
+      for (int o = 1; o < 4; o <<= 1) {
+        const float om = __shfl_xor(m, o, 64);
+        const int oi = __shfl_xor(mi, o, 64);
+        better(m, mi, om, oi);
+      }
+      const float zm = m / T;
+      float sum = 0.f;
+#pragma unroll
+      for (int q = 0; q < RB; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sum += __expf(x[q][e] / T - zm);
+      sum += __shfl_xor(sum, 1, 64);
+      sum += __shfl_xor(sum, 2, 64);
+      float gk = -INFINITY, gz = 0.f;
+      int gi = 0x7fffffff;
+      if (!greedy) {
+        const int pid = live ? (a.smp.seq_ids ? a.smp.seq_ids[b] : b) : 0;
+#pragma unroll
+        for (int q = 0; q < RB; ++q) {
+          const int n0 = tile * ROWS + (t4 * RB + q) * 4;
+          const uint4 w = philox4x32_10(
+              make_uint4((uint32_t)(n0 >> 2), (uint32_t)step, (uint32_t)pid, 0u), k0, k1);
+          const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (n0 + e < a.N) better_g(gk, gi, gz, gumbel_key(x[q][e], T, ws[e]), n0 + e, x[q][e]);
+        }
+#pragma unroll
+        for (int o = 1; o < 4; o <<= 1) {
+          const float ok = __shfl_xor(gk, o, 64), oz = __shfl_xor(gz, o, 64);
+          const int oi = __shfl_xor(gi, o, 64);
+          better_g(gk, gi, gz, ok, oi, oz);
+        }
+      }
+      if (live && t4 == 0) {
+        float* o = a.smp.part + ((size_t)b * a.tiles + tile) * 8;
+        *(f32x4_t*)o = (f32x4_t){m, sum, __int_as_float(mi), gk};
+        *(f32x4_t*)(o + 4) = (f32x4_t){__int_as_float(gi), gz, 0.f, 0.f};
+      }
+    }
   } else {
     float* out = a.out_f32 + (size_t)ks * a.B * a.ld_out;
     for (int i = tid; i < ROWS / 4 * NB; i += NT) {
@@ -189,6 +262,9 @@ hipError_t launch_rb(const DArgs& a, int epi, int grid, const char* name, hipStr
   if (epi == EPI_SWIGLU) {
     Prof pf(name ? name : "gemm_decode_swiglu", st);
     k_gemm_decode<NB, RB, D, EPI_SWIGLU><<<grid, NT, 0, st>>>(a);
+  } else if (epi == EPI_SAMPLE) {
+    Prof pf(name ? name : "gemm_decode_sample", st);
+    k_gemm_decode<NB, RB, D, EPI_SAMPLE><<<grid, NT, 0, st>>>(a);
   } else {
     Prof pf(name ? name : "gemm_decode", st);
     k_gemm_decode<NB, RB, D, EPI_PARTIAL><<<grid, NT, 0, st>>>(a);
@@ -284,9 +360,11 @@ hipError_t gemm_decode_bf16(const uint16_t* Xf, int B, const uint16_t* Wf, int N
                             EpiArgs ep, const DecodePlan& p, hipStream_t st) {
   if (B < 1 || B > p.nb || p.nb != decode_nb(B) || N % 16 || K % KGRAN || p.splits < 1 ||
       p.tiles * 16 * p.rb < N ||
-      (K / p.splits) % KGRAN || (epi == EPI_SWIGLU && (N % 32 || ep.ld_out != N / 2)))
+      (K / p.splits) % KGRAN || (epi == EPI_SWIGLU && (N % 32 || ep.ld_out != N / 2)) ||
+      (epi == EPI_SAMPLE && (p.splits != 1 || !ep.smp.part || (ep.out_f32 && ep.ld_out < N))))
     return hipErrorInvalidValue;
   DArgs a;
+  a.smp = ep.smp;
   a.X = (const bf16_t*)Xf; a.W = (const bf16_t*)Wf;
   a.B = B; a.N = N; a.K = K; a.kper = K / p.splits; a.tiles = p.tiles;
   a.out_f32 = ep.out_f32; a.out_act = (bf16_t*)ep.out_act; a.ld_out = ep.ld_out;

@@ -22,7 +22,10 @@ bool profiling();
 // PARTIAL (decode GEMM only): out[split] = this split's share of X W^T, the
 // consumer adds the splits;  LSE (row-tile GEMMs, the scoring LM head): the
 // product's log-sum-exp pieces per row instead of the product (LseArgs).
-enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_PARTIAL = 3, EPI_LSE = 4 };
+// SAMPLE (decode GEMM, the LM head): the sampler's pieces per row and output tile
+// instead of the logits (DecSample).
+enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_PARTIAL = 3, EPI_LSE = 4,
+           EPI_SAMPLE = 5 };
 constexpr int kMaxSplits = 16;
 
 // Up to three weight matrices stacked along the output dimension: output row r
@@ -54,6 +57,23 @@ struct LseArgs {
 };
 inline int lse_slots(int N) { return (N + 63) / 64; }
 
+// EPI_SAMPLE: for batch row b and output tile s (weight rows = vocabulary ids
+// 16 rb s .. 16 rb s + 16 rb - 1 below N) of logits x, at part[(b tiles + s) 8]:
+//   0 m = max x,  1 sum exp(x / T - m / T),  2-3 arg-max of x (value, id bits),
+//   4-6 Gumbel-max over the tile (key, id bits, its x), the key of id v being
+//   gumbel_key(x_v, T, word v % 4 of Philox block (v / 4, step, pid, 0), key seed)
+// with step = step + *step_ctr (if set) and pid = seq_ids[b] (NULL: b); greedy
+// (temperature <= 0) skips the keys and reads T as 1.  out_f32, if set, also
+// receives the logits [B][ld_out] (a trace).
+struct DecSample {
+  float temperature = 0.f;
+  uint64_t seed = 0;
+  int step = 0;
+  const int32_t* step_ctr = nullptr;
+  const int32_t* seq_ids = nullptr;
+  float* part = nullptr;
+};
+
 struct EpiArgs {
   float* out_f32;       // EPI_STORE: [rows, ld_out] fp32;  EPI_RESID: residual [rows, ld_out]
                         // EPI_LSE: [rows, ld_out slots] (max, sum) pairs
@@ -61,6 +81,7 @@ struct EpiArgs {
   int ld_out;
   const char* name = nullptr;  // kernel-timing label of a decode GEMM (a string literal)
   LseArgs lse = {};
+  DecSample smp = {};
 };
 
 // ---- decode GEMM: Y[B, N] = X[B, K] . W[N, K]^T for B <= 128 (bf16 MFMA) ----
@@ -235,6 +256,13 @@ struct SampleArgs {
   const int32_t* seq_ids;   // optional [R*G]: Philox sequence id of draw q
 };
 hipError_t sample(const float* logits, int R, int V, int ld, const SampleArgs& a, hipStream_t st);
+// The same draw (no top-k cut, one draw per row) from the EPI_SAMPLE pieces of
+// R rows over `tiles` output tiles: the token of the best Gumbel key (greedy:
+// the arg-max), logp = x_tok / T - (M / T + log S) with M the largest tile
+// maximum and S = sum over tiles s of sum_s exp(m_s / T - M / T); the same outputs and state
+// updates as `sample`.
+hipError_t sample_combine(const float* part, int tiles, int R, int V, const SampleArgs& a,
+                          hipStream_t st);
 // Teacher-forced log-prob of scored row r, log_softmax(z / temperature) at the
 // row's target, from the LM head's EPI_LSE pieces:
 // logp[r] = z_t[r] / temperature - ln2 (M + log2 S) with M = max_s m_s and

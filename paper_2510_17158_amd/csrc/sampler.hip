@@ -19,27 +19,9 @@ namespace {
 
 constexpr int NT = 256;
 
-__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
-#pragma unroll
-  for (int r = 0; r < 10; ++r) {
-    if (r) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
-    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
-    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
-    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
-    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
-    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
-  }
-  return c;
-}
-
 __device__ __forceinline__ uint32_t order_key(float f) {
   const uint32_t u = __float_as_uint(f);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-// (value desc, id asc) arg-max merge
-__device__ __forceinline__ void better(float& bv, int& bi, float v, int i) {
-  if (v > bv || (v == bv && i < bi)) { bv = v; bi = i; }
 }
 
 template <int NTH = NT>
@@ -152,9 +134,7 @@ __global__ __launch_bounds__(NT) void k_sample(const float* __restrict__ logits,
           const uint32_t u = order_key(li);
           if (!(u > thr || (u == thr && i <= cut))) continue;
         }
-        const float uu = (float)(2u * (ws[j] >> 9) + 1u) * 5.9604644775390625e-8f;  // 2^-24
-        const float key = li / T - logf(-logf(uu));
-        better(gv, gi, key, i);
+        better(gv, gi, gumbel_key(li, T, ws[j]), i);
       }
     }
     block_argmax(gv, gi, shv, shi);
@@ -294,9 +274,7 @@ __global__ __launch_bounds__(NTR) void k_sample_reg(const float* __restrict__ lo
             const uint32_t u = order_key(li);
             ok = ok && (u > thr || (u == thr && i <= cut));
           }
-          const float uu = (float)(2u * (ws[e] >> 9) + 1u) * 5.9604644775390625e-8f;  // 2^-24
-          const float key = li / T - logf(-logf(uu));
-          if (ok) better(gv, gi, key, i);
+          if (ok) better(gv, gi, gumbel_key(li, T, ws[e]), i);
         }
       }
     }
@@ -312,7 +290,68 @@ __global__ __launch_bounds__(NTR) void k_sample_reg(const float* __restrict__ lo
   }
 }
 
+// One wave per row over the decode LM head's per-tile pieces (tiles read
+// lane-strided, merged in a fixed order): the arg-max, the log-sum-exp and the
+// Gumbel-max of the whole vocabulary, then the sampler's outputs.
+__global__ __launch_bounds__(256) void k_sample_combine(const float* __restrict__ part, int tiles,
+                                                        int R, int V, SampleArgs a) {
+  const int r = blockIdx.x * 4 + threadIdx.x / 64, lane = threadIdx.x % 64;
+  if (r >= R) return;                      // whole waves
+  const bool greedy = !(a.temperature > 0.f);
+  const float T = greedy ? 1.f : a.temperature;
+  const float* p = part + (size_t)r * tiles * 8;
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int t = lane; t < tiles; t += 64) better(bv, bi, p[t * 8], __float_as_int(p[t * 8 + 2]));
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(bv, o, 64);
+    const int oi = __shfl_xor(bi, o, 64);
+    better(bv, bi, ov, oi);
+  }
+  const float zmax = bv / T;
+  float s = 0.f;
+  for (int t = lane; t < tiles; t += 64) s = fmaf(p[t * 8 + 1], __expf(p[t * 8] / T - zmax), s);
+  s = wave_sum(s);
+  int tok = bi;
+  float xt = bv;
+  if (!greedy) {
+    float gk = -INFINITY, gz = 0.f;
+    int gi = 0x7fffffff;
+    for (int t = lane; t < tiles; t += 64) {
+      const float k = p[t * 8 + 3];
+      const int i = __float_as_int(p[t * 8 + 4]);
+      if (k > gk || (k == gk && i < gi)) { gk = k; gi = i; gz = p[t * 8 + 5]; }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ok = __shfl_xor(gk, o, 64), oz = __shfl_xor(gz, o, 64);
+      const int oi = __shfl_xor(gi, o, 64);
+      if (ok > gk || (ok == gk && oi < gi)) { gk = ok; gi = oi; gz = oz; }
+    }
+    tok = gi;
+    xt = gz;
+  }
+  if (lane == 0) {
+    const int col = a.step_ctr ? *a.step_ctr : 0;
+    tok = clampi(tok, 0, V - 1);
+    a.tok_out[(size_t)r * a.out_stride + col] = tok;
+    a.logp_out[(size_t)r * a.out_stride + col] = xt / T - (zmax + logf(s));
+    if (a.tok_state) a.tok_state[r] = tok;
+    if (a.pos_state) a.pos_state[r] += 1;
+  }
+}
+
 }  // namespace
+
+hipError_t sample_combine(const float* part, int tiles, int R, int V, const SampleArgs& a,
+                          hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  if (tiles < 1 || a.G != 1 || (a.top_k > 0 && a.top_k < V)) return hipErrorInvalidValue;
+  Prof pf("sample", st);
+  k_sample_combine<<<(R + 3) / 4, 256, 0, st>>>(part, tiles, R, V, a);
+  return hipGetLastError();
+}
 
 hipError_t sample(const float* logits, int R, int V, int ld, const SampleArgs& a, hipStream_t st) {
   if (R <= 0) return hipSuccess;

@@ -149,16 +149,21 @@ def gemms_rows(cfg, M: int) -> dict:
 
 
 def logp_bound(z, logp):
-    """Bound on the GPU's fp32 log-probability z_tok - LSE(z) given its logits:
-    z = l / T (u |z|), exponent arguments z - max (u |z - m|), the exponentials
-    (C_EXP u), a sum of V positive terms read by at least 256 threads (at most V / 256
-    per thread, then 16 reduction levels), the log and the final subtractions
-    (u each of |LSE| and |logp|)."""
+    """Bound on the GPU's fp32 log-probability z_tok - LSE(z) of a draw given its
+    logits, for both ways the draw is made.  The sampler kernel: z = l / T (u |z|),
+    exponent arguments z - max (u |z - m|), the exponentials (C_EXP u), a sum of V
+    positive terms read by at least 256 threads (at most V / 256 per thread, then
+    16 reduction levels), the log and the final subtractions (u each of |LSE| and
+    |logp|).  The decode LM head's sampling epilogue: per output tile of at most
+    128 ids four threads sum at most 32 terms each over 2 shuffle levels, and the
+    combine rescales every tile by exp(m_s / T - M / T) (argument 2u max|z|,
+    C_EXP u, one fused multiply-add) and sums V / 32 / 64 tiles per lane over 6
+    levels.  The bound takes each term's larger value."""
     from bounds import C_EXP, U
     zmax = float(np.max(np.abs(z)))
     lse = float(np.max(z) + np.log(np.sum(np.exp(z - np.max(z)))))
-    h_sum = len(z) / 256.0 + 16.0
-    return U * (h_sum + 8.0 + C_EXP + 4.0 * zmax + 3.0 * abs(lse) + abs(float(logp)))
+    h_sum = max(len(z) / 256.0 + 16.0, 32.0 + 2.0 + np.ceil(len(z) / 32.0 / 64.0) + 6.0 + 1.0)
+    return U * (h_sum + 8.0 + 2.0 * C_EXP + 6.0 * zmax + 3.0 * abs(lse) + abs(float(logp)))
 
 
 def score_logp_bound(z, logp):
