@@ -579,6 +579,7 @@ struct BackwardWS {
   float* xa; void* h2; float* gu; void* a; float2* cs;
   float* dx; float* dxa; void* dxe; float* da; void* dgu; float* dh; float* dof; void* doe;
   float* dqkv; void* dqkve; float* rr; float* part;
+  uint32_t* ekeys;                // the embedding gradient's sorted (token, position) keys
   void* tA; void* tB;             // transposed gradient / activation operands [rows][Tp]
   float* S; float* dP; float* stats; void* dS; void* PT; void* dST; void* qT; void* doT; void* kT;
   float* tk; float* tv;           // per-head dk, dv before the sum over each group
@@ -629,6 +630,7 @@ BackwardWS take_backward(Bump& b, const grpo_config& c, int T) {
   w.dqkve = b.take<char>((size_t)T * ldqkv * es);
   w.rr = b.take<float>((size_t)std::max(T, R));
   w.part = b.take<float>((size_t)((std::max(T, R) + 63) / 64) * d);
+  w.ekeys = b.take<uint32_t>((size_t)T);
   const int rowsA = std::max(std::max(2 * f, ldqkv), d);
   const int rowsB = std::max(std::max(f, d), qd);
   w.tA = b.take<char>((size_t)rowsA * Tp * es);
@@ -1735,7 +1737,7 @@ int grpo_policy_backward(const grpo_model* m, const int32_t* tokens, int32_t N, 
                          w.rr, w.part, g->attn_norm[l], st));
       std::swap(w.dx, w.dxa);
     }
-    HIPCHK(embed_bwd(tk, w.dx, T, d, g->tok_emb, st));
+    HIPCHK(embed_bwd(tk, w.dx, T, d, c.vocab, w.ekeys, g->tok_emb, st));
   }
   g_err.clear();
   return GRPO_OK;

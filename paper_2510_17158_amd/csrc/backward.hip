@@ -253,13 +253,49 @@ __global__ __launch_bounds__(256) void k_sum_heads(const float* __restrict__ tmp
   out[t * ldo + (size_t)g * hd + e] = s;
 }
 
-// Embedding gradient: demb[tok[t]] += dx[t] (fp32 atomics).
-__global__ __launch_bounds__(256) void k_embed_bwd(const int32_t* __restrict__ tok,
+// Embedding gradient demb[tok[t]] += dx[t] without atomics, in a fixed order:
+// the keys (tok[t] << 14) | t are sorted (one workgroup, bitonic in LDS), then
+// every run of equal tokens is summed in increasing t by the workgroup at its
+// first sorted index, which alone owns that embedding row in this call.
+constexpr int kEmbedKeyBits = 14;                    // t < 16384
+constexpr int kEmbedSortMax = 1 << kEmbedKeyBits;    // keys sorted in LDS
+
+__global__ __launch_bounds__(1024) void k_embed_sort(const int32_t* __restrict__ tok, int T, int V,
+                                                     uint32_t* __restrict__ keys) {
+  __shared__ uint32_t k[kEmbedSortMax];
+  int n = 1;
+  while (n < T) n <<= 1;
+  for (int i = threadIdx.x; i < n; i += 1024)
+    k[i] = i < T ? ((uint32_t)clampi(tok[i], 0, V - 1) << kEmbedKeyBits) | (uint32_t)i
+                 : 0xffffffffu;
+  __syncthreads();
+  for (int w = 2; w <= n; w <<= 1)
+    for (int j = w >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < n; i += 1024) {
+        const int l = i ^ j;
+        if (l > i) {
+          const uint32_t a = k[i], b = k[l];
+          if ((a > b) == ((i & w) == 0)) { k[i] = b; k[l] = a; }
+        }
+      }
+      __syncthreads();
+    }
+  for (int i = threadIdx.x; i < T; i += 1024) keys[i] = k[i];
+}
+
+__global__ __launch_bounds__(256) void k_embed_bwd(const uint32_t* __restrict__ keys, int T,
                                                    const float* __restrict__ dx, int d,
                                                    float* __restrict__ demb) {
-  const int t = blockIdx.x;
-  const size_t row = (size_t)tok[t] * d;
-  for (int k = threadIdx.x; k < d; k += 256) atomicAdd(demb + row + k, dx[(size_t)t * d + k]);
+  const int i = blockIdx.x;
+  const uint32_t v = keys[i] >> kEmbedKeyBits;
+  if (i > 0 && (keys[i - 1] >> kEmbedKeyBits) == v) return;   // not the run's first
+  float* row = demb + (size_t)v * d;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    float acc = 0.f;
+    for (int j = i; j < T && (keys[j] >> kEmbedKeyBits) == v; ++j)
+      acc += dx[(size_t)(keys[j] & (kEmbedSortMax - 1)) * d + c];
+    row[c] += acc;
+  }
 }
 
 __global__ __launch_bounds__(256) void k_fill_f32(float* p, size_t n, float v) {
@@ -402,10 +438,13 @@ hipError_t sum_heads(const float* tmp, int T, int hd, int gq, int groups, float*
   return hipGetLastError();
 }
 
-hipError_t embed_bwd(const int32_t* tok, const float* dx, int T, int d, float* demb, hipStream_t st) {
+hipError_t embed_bwd(const int32_t* tok, const float* dx, int T, int d, int V, uint32_t* keys,
+                     float* demb, hipStream_t st) {
   if (T <= 0) return hipSuccess;
+  if (T > kEmbedSortMax || V < 1 || V > (1 << (32 - kEmbedKeyBits))) return hipErrorInvalidValue;
   Prof pf("embed_bwd", st);
-  k_embed_bwd<<<T, 256, 0, st>>>(tok, dx, d, demb);
+  k_embed_sort<<<1, 1024, 0, st>>>(tok, T, V, keys);
+  k_embed_bwd<<<T, 256, 0, st>>>(keys, T, dx, d, demb);
   return hipGetLastError();
 }
 

@@ -311,7 +311,11 @@ hipError_t attn_softmax_bwd(int dtype, const float* S, const float* dP, int T, i
                             hipStream_t st);
 hipError_t sum_heads(const float* tmp, int T, int hd, int gq, int groups, float* out, int ldo,
                      hipStream_t st);
-hipError_t embed_bwd(const int32_t* tok, const float* dx, int T, int d, float* demb, hipStream_t st);
+// demb[tok[t]] += dx[t] for t < T <= 16384 (V <= 2^18), without atomics: the
+// (token, t) keys are sorted into `keys` [T] and each token's rows summed in
+// increasing t, then added to its embedding row.
+hipError_t embed_bwd(const int32_t* tok, const float* dx, int T, int d, int V, uint32_t* keys,
+                     float* demb, hipStream_t st);
 hipError_t fill_f32(float* p, size_t n, float v, hipStream_t st);
 hipError_t cast_f32(const float* in, size_t n, int dtype, void* out, hipStream_t st);
 hipError_t adamw(int dtype, void* param, float* master, float* m, float* v, const float* grad,
