@@ -388,8 +388,9 @@ typedef struct grpo_grads {
  * the embedding gather.  Each sequence's forward is recomputed (its layer
  * inputs kept), the rounding points of the bf16 forward pass gradients
  * straight through.  Gradients accumulate in fp32; data-gradient operands are
- * the model dtype (bf16 products on the matrix cores).  The embedding rows are
- * added with fp32 atomics (order not fixed); every other sum has a fixed order.
+ * the model dtype (bf16 products on the matrix cores).  Every sum has a fixed
+ * order, the embedding rows' included (positions grouped by token, then added
+ * in position order): results are bit-deterministic.
  * Workspace: grpo_workspace_bytes(GRPO_OP_BACKWARD, N, T) (it holds transposed
  * copies of every weight matrix).  GRPO_INVALID_ARG for a NULL gradient buffer
  * or score_from outside [1, T); GRPO_UNSUPPORTED for T above 16384. */

@@ -15,9 +15,9 @@
 // The causal upper triangle is computed and zeroed.
 //
 // Gradients accumulate in fp32; GEMM operands are the model's dtype (bf16
-// products on MFMA, fp32 on the vector units for fp32 models).  The embedding
-// gradient is a scatter-add with fp32 atomics (its summation order is not
-// fixed); every other reduction runs in a fixed order.
+// products on MFMA, fp32 on the vector units for fp32 models).  Every reduction
+// runs in a fixed order, the embedding gradient's scatter-add included (its
+// positions are sorted by token first): the result is bit-deterministic.
 #include "common.h"
 #include "kernels.h"
 
