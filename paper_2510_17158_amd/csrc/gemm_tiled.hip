@@ -150,6 +150,22 @@ __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
   }
 
   // ---- epilogue ----
+  // the residual's values are all loaded before any is written back (one memory
+  // round trip; the compiler cannot tell the addresses apart)
+  float old[4][4][4];
+  if (EPI == EPI_RESID) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = tm * BM + wm * 64 + i * 16 + (lane >> 4) * 4 + v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = tn * BN + wn * 64 + j * 16 + (lane & 15);
+          old[i][v][j] = (m < a.M && n < a.N) ? a.out_f32[(size_t)m * a.ld_out + n] : 0.f;
+        }
+      }
+  }
   if (EPI == EPI_LSE) {
     // slot tn * 2 + wn = the wave's 64 columns; a row's 64 values sit in the 16
     // lanes of its lane group (4 columns each): in-lane, then across the group
@@ -207,7 +223,7 @@ __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
           const int n = tn * BN + wn * 64 + j * 16 + (lane & 15);
           if (n < a.N) {
             float* o = a.out_f32 + (size_t)m * a.ld_out + n;
-            if (EPI == EPI_RESID) *o += acc[i][j][v];
+            if (EPI == EPI_RESID) *o = old[i][v][j] + acc[i][j][v];
             else *o = acc[i][j][v];
           }
         }
@@ -434,6 +450,21 @@ __global__ __launch_bounds__(256) void k_gemm_big(TArgs a) {
     float* stg = reinterpret_cast<float*>(&lds[0][0][0]) + wave * 32 * SR;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
+      // the residual's 16 pieces of these 32 rows are all loaded before any is
+      // written back (one memory round trip instead of one per piece: the
+      // compiler cannot tell the pieces' addresses apart)
+      float4 w[16];
+      if (EPI == EPI_RESID) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const int idx = lane + 64 * k, row = idx >> 5, c4 = (idx & 31) * 4;
+          const int m = m0 + wm * 128 + i * 32 + row;
+          const int n = tn * GB + wn * 128 + c4;
+          w[k] = (m >= tm * GB && n < a.N)
+                     ? *(const float4*)(a.out_f32 + (size_t)m * a.ld_out + n)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r)
 #pragma unroll
@@ -447,12 +478,10 @@ __global__ __launch_bounds__(256) void k_gemm_big(TArgs a) {
         const float4 v = *(const float4*)(stg + row * SR + c4);
         if (m >= tm * GB && n < a.N) {
           float4* o = (float4*)(a.out_f32 + (size_t)m * a.ld_out + n);
-          if (EPI == EPI_RESID) {
-            const float4 w = *o;
-            *o = make_float4(w.x + v.x, w.y + v.y, w.z + v.z, w.w + v.w);
-          } else {
+          if (EPI == EPI_RESID)
+            *o = make_float4(w[k].x + v.x, w[k].y + v.y, w[k].z + v.z, w[k].w + v.w);
+          else
             *o = v;
-          }
         }
       }
     }
@@ -553,6 +582,17 @@ __global__ __launch_bounds__(256) void k_gemm_f32(FArgs a) {
     }
     return;
   }
+  // the residual's values are all loaded before any is written back
+  float old[4][4];
+  if (a.epi == EPI_RESID) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
+        old[i][j] = (m < a.M && n < a.N) ? a.out_f32[(size_t)m * a.ld_out + n] : 0.f;
+      }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = m0 + ty * 4 + i;
@@ -567,7 +607,7 @@ __global__ __launch_bounds__(256) void k_gemm_f32(FArgs a) {
         }
       } else if (n < a.N) {
         float* o = a.out_f32 + (size_t)m * a.ld_out + n;
-        if (a.epi == EPI_RESID) *o += acc[i][j];
+        if (a.epi == EPI_RESID) *o = old[i][j] + acc[i][j];
         else *o = acc[i][j];
       }
     }
