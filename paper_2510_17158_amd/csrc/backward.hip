@@ -135,7 +135,7 @@ __global__ __launch_bounds__(256) void k_swiglu_fwd(const float* __restrict__ gu
   if (i >= (size_t)T * F) return;
   const size_t t = i / F, n = i % F;
   const float gt = gu[t * 2 * F + n], up = gu[t * 2 * F + F + n];
-  stf(a, i, gt / (1.f + __expf(-gt)) * up);
+  stf(a, i, silu_mul(gt, up));
 }
 template <typename TO>
 __global__ __launch_bounds__(256) void k_swiglu_bwd(const float* __restrict__ gu,

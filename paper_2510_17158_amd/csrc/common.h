@@ -86,6 +86,12 @@ __device__ __forceinline__ float block_max(float v, float* sh) {
 
 __device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
 
+// SwiGLU's silu(g) * u in fp32: g / (1 + e^-g) with the hardware exponential and
+// reciprocal (each within about 1 ulp), then the product by u.
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  return g * __builtin_amdgcn_rcpf(1.f + __expf(-g)) * u;
+}
+
 // ---- fragment order of the decode GEMM's activations ---------------------------
 // Element (b, k) of an activation [nb][K] (nb: the padded batch, a multiple of 16)
 // stored as MFMA B-operand fragments: fragment (k / 32, b / 16) is 1 KB, lane

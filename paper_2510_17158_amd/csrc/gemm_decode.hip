@@ -168,7 +168,7 @@ void k_gemm_decode(DArgs a) {
         for (int h = 0; h < 2; ++h) {
           const f32x4_t gt = val4(b, rg + 4 * h), up = val4(b, rg + 8 + 4 * h);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) y[4 * h + e] = gt[e] / (1.f + __expf(-gt[e])) * up[e];
+          for (int e = 0; e < 4; ++e) y[4 * h + e] = silu_mul(gt[e], up[e]);
         }
         u32x4_t w;
 #pragma unroll

@@ -214,7 +214,7 @@ __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
           const int n = tn * 64 + wn * 32 + j * 16 + (lane & 15);
           if (n < a.n1) {
             const float gt = acc[i][j][v], up = acc[i][j + 2][v];
-            a.out_act[(size_t)m * a.ld_out + n] = f2bf(gt / (1.f + __expf(-gt)) * up);
+            a.out_act[(size_t)m * a.ld_out + n] = f2bf(silu_mul(gt, up));
           }
         }
       } else {
@@ -429,13 +429,16 @@ __global__ __launch_bounds__(256) void k_gemm_big(TArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const float gt = acc[i][j][r], up = acc[i][j + 2][r];
-          stg[((r / 4) * 8 + (lane >> 5) * 4 + (r % 4)) * SR + j * 32 + (lane & 31)] =
-              f2bf(gt / (1.f + __expf(-gt)) * up);
-        }
+      for (int r = 0; r < 16; ++r) {
+        // the two outputs of the lane's column pair, rounded together (hardware RNE)
+        const uint32_t y = __builtin_bit_cast(
+            uint32_t, __builtin_convertvector((f32x2_t){silu_mul(acc[i][0][r], acc[i][2][r]),
+                                                        silu_mul(acc[i][1][r], acc[i][3][r])},
+                                              bf16x2_t));
+        bf16_t* row = stg + ((r / 4) * 8 + (lane >> 5) * 4 + (r % 4)) * SR + (lane & 31);
+        row[0] = (bf16_t)(y & 0xffffu);
+        row[32] = (bf16_t)(y >> 16);
+      }
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         const int idx = lane + 64 * k, row = idx >> 3, c8 = (idx & 7) * 8;
@@ -603,7 +606,7 @@ __global__ __launch_bounds__(256) void k_gemm_f32(FArgs a) {
       if (swiglu) {
         if (n < a.n1) {
           const float gt = acc[i][j];
-          a.out_act[(size_t)m * a.ld_out + n] = gt / (1.f + __expf(-gt)) * acc2[i][j];
+          a.out_act[(size_t)m * a.ld_out + n] = silu_mul(gt, acc2[i][j]);
         }
       } else if (n < a.N) {
         float* o = a.out_f32 + (size_t)m * a.ld_out + n;

@@ -223,7 +223,8 @@ def rope_bound(lo, hi, Elo, Ehi, pos, theta, hd):
 def swiglu_bound(g, up, Eg, Eu):
     """a = silu(g) * up in fp32 with a hardware exponential: the inputs' bounds
     through the derivatives, plus the evaluation (exp argument u|g|, exp C_EXP u,
-    1 + e, the division and the product)."""
+    then 4u for the rest: 1 + e (u/2), the hardware reciprocal (within 1 ulp,
+    u) or an IEEE division (u/2), and the products by g and up (u/2 each))."""
     sg = 1.0 / (1.0 + np.exp(-g))
     silu = g * sg
     y = silu * up
