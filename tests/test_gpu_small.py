@@ -191,6 +191,25 @@ def test_grouped_decode_stage_local(name, P, G, Tp, prefix, steps):
     model.close()
 
 
+@pytest.mark.parametrize("temperature,top_k", [(0.0, 0), (0.7, 0), (1.0, 32000), (0.9, 50)])
+def test_decode_draw_variants_stage_local(temperature, top_k):
+    """bf16 decode under each way a draw is made: greedy and Gumbel-max without a
+    cut (and top-k = V, the same) are fused into the LM head's epilogue, a top-k
+    cut reads the stored logits.  Prefill and two traced decode steps, grouped,
+    each stage against the oracle, and the oracle sampler on the GPU's logits
+    reproducing the tokens and log-probs."""
+    require_gpu()
+    w = truncated(get("small"), 2, n_prompts=2, group=4, prompt_len=90, new_tokens=3,
+                  temperature=temperature, top_k=top_k)
+    say("draw variants", temperature, top_k)
+    host, model = build_model(w.model, w.master_seed, gain_noise=0.1)
+    it = _iteration(w, model)
+    _prefill_checked(w, host, model, it, label=f"prefill T={temperature} k={top_k}")
+    _decode_checked(w, host, model, it, 2, group=w.group, prefix_len=w.prompt_len,
+                    label=f"decode T={temperature} k={top_k}")
+    model.close()
+
+
 @pytest.mark.parametrize("group", [0, 4])
 def test_ragged_positions_stage_local(small, group):
     """One batch whose rows decode at different positions (1 .. 9 steps back from
