@@ -81,6 +81,31 @@ def copy_ceiling_gbs(torch) -> float:
     return 2 * (1 << 30) / (best / 1e3) / 1e9
 
 
+def gemm_ceiling_tflops(torch, n: int = 8192) -> float:
+    """Dense bf16 matrix-core rate the device sustains right after the step: the
+    vendor library's n x n x n product (torch.mm, contiguous operands), the best
+    of 5 timed calls after two untimed.  Under dense matrix work the engine clock
+    drops below the 2.4 GHz of the spec peak (and varies with the power state by
+    some 15% between runs), so this ceiling is what a GEMM-bound phase can be
+    compared against beside that peak."""
+    g = torch.Generator(device="cuda").manual_seed(0)
+    a = torch.randn(n, n, device="cuda", generator=g).to(torch.bfloat16)
+    b = torch.randn(n, n, device="cuda", generator=g).to(torch.bfloat16)
+    c = torch.mm(a, b)
+    c = torch.mm(a, b)
+    best = float("inf")
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        torch.mm(a, b, out=c)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del a, b, c
+    torch.cuda.empty_cache()
+    return 2.0 * n ** 3 / (best / 1e3) / 1e12
+
+
 def decode_bytes_per_step(w, ctx_avg: float) -> float:
     """Algorithmic HBM bytes of one decode step: every weight once (embedding rows
     aside), the KV of every context position once, the new K/V written.  With the
@@ -424,6 +449,11 @@ def main():
     cc = copy_ceiling_gbs(torch)
     out["copy_ceiling_gbs"] = cc
     out["decode_step_copy_frac"] = out["decode_step_gbs"] / cc
+    # scoring against the measured dense-GEMM rate as well as the spec peak
+    if w.score and c.dtype == 1:
+        gc = gemm_ceiling_tflops(torch)
+        out["gemm_ceiling_tflops"] = gc
+        out["score_gemm_ceiling_frac"] = out["score_tflops"] / gc
     # per-kernel times from a profiled replica of the step (HIP events around
     # every launch, on the launch stream); the dominant decode kernel sets the
     # roofline line
