@@ -743,7 +743,7 @@ int attn_bwd(const grpo_model* m, BackwardWS& w, int T, hipStream_t st) {
   for (int h0 = 0; h0 < H; h0 += w.hb) {
     const int nb = std::min(w.hb, H - h0), g0 = h0 / gq;
     // S = q_h k_g^T, dP = do_h v_g^T (raw products, fp32)
-    GemmBatch sb{nb, (size_t)hd, (size_t)Tp * hd, TT, gq};
+    GemmBatch sb{nb, (size_t)hd, (size_t)Tp * hd, TT, gq, 1};   // causal: lower tiles only
     if ((rc = gemm_bt(m, (char*)w.q + (size_t)h0 * hd * es, qd, T,
                       one(kb + (size_t)g0 * Tp * hd * es), T, hd, EPI_STORE,
                       EpiArgs{w.S, nullptr, Tp}, sb, st)))
@@ -754,7 +754,7 @@ int attn_bwd(const grpo_model* m, BackwardWS& w, int T, hipStream_t st) {
       return rc;
     HIPCHK(attn_softmax_bwd(c.dtype, w.S, w.dP, T, Tp, nb, scale, w.stats, w.dS, w.dST, w.PT, st));
     // dq_h = dS'_h k_g (K = key positions)
-    GemmBatch qb{nb, TT, hT, (size_t)hd, gq};
+    GemmBatch qb{nb, TT, hT, (size_t)hd, gq, 2};   // dS' is zero past each row
     if ((rc = gemm_bt(m, w.dS, Tp, T, one((char*)w.kT + (size_t)g0 * hT * es), hd, Tp, EPI_STORE,
                       EpiArgs{w.dqkv + (size_t)h0 * hd, nullptr, ldqkv}, qb, st)))
       return rc;
@@ -763,7 +763,7 @@ int attn_bwd(const grpo_model* m, BackwardWS& w, int T, hipStream_t st) {
                      Tp, nb, st));
     HIPCHK(transpose(e, e, (char*)w.doe + (size_t)h0 * hd * es, qd, hd, T, hd, w.doT, Tp, hT, 0,
                      1, Tp, nb, st));
-    GemmBatch kb2{nb, PP, hT, (size_t)T * hd, 1};
+    GemmBatch kb2{nb, PP, hT, (size_t)T * hd, 1, 3};   // dS'^T, P^T zero before each row
     if ((rc = gemm_bt(m, w.dST, Tp, T, one(w.qT), hd, Tp, EPI_STORE, EpiArgs{w.tk, nullptr, hd},
                       kb2, st)) ||
         (rc = gemm_bt(m, w.PT, Tp, T, one(w.doT), hd, Tp, EPI_STORE, EpiArgs{w.tv, nullptr, hd},

@@ -78,6 +78,12 @@ __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
   const int gsize = min(a.tiles_m - first_m, group);
   const int tm = first_m + (bid % per_group) % gsize;
   const int tn = (bid % per_group) / gsize;
+  // causal products (GemmBatch::tri): tiles above the diagonal, and the k range
+  // where X is zero, are skipped (the skipped products are exact zeros)
+  if (a.bt.tri == 1 && tn * BN > tm * BM + BM - 1) return;
+  int kt0 = 0, nk = a.K / BK;
+  if (a.bt.tri == 2) nk = min(nk, (tm * BM + BM + BK - 1) / BK);
+  if (a.bt.tri == 3) kt0 = min(tm * BM / BK, nk);
 
   // loader mapping: 4 x 16-byte loads per operand per thread (128 rows x 64 cols)
   const bf16_t* ap[4];
@@ -100,12 +106,11 @@ __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
-  const int nk = a.K / BK;
-  {
+  if (kt0 < nk) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      ra[i] = *(const u32x4_t*)(ap[i] + 0);
-      rb[i] = *(const u32x4_t*)(bp[i] + 0);
+      ra[i] = *(const u32x4_t*)(ap[i] + kt0 * BK);
+      rb[i] = *(const u32x4_t*)(bp[i] + kt0 * BK);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -114,8 +119,8 @@ __global__ __launch_bounds__(NT) void k_gemm_tiled(TArgs a) {
     }
   }
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
+  for (int kt = kt0; kt < nk; ++kt) {
+    const int buf = (kt - kt0) & 1;
     if (kt + 1 < nk) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -644,7 +649,7 @@ hipError_t gemm_tiled_bf16(const uint16_t* X, int ldx, int M, WStack W, int N, i
   const bool aligned = out16 && (epi == EPI_SWIGLU
                            ? W.n1 % 128 == 0
                            : N % GB == 0 && (W.n1 >= N || W.n1 % GB == 0) && (W.n2 >= N || W.n2 % GB == 0));
-  if (M >= kBigTileRows && aligned && bt.count == 1) {
+  if (M >= kBigTileRows && aligned && bt.count == 1 && bt.tri == 0) {
     a.tiles_m = (M + GB - 1) / GB;
     a.tiles_n = epi == EPI_SWIGLU ? (N + 127) / 128 : (N + GB - 1) / GB;
     // super-tiles of 4 x 8 tiles, a whole number of rounds of 8 (one per XCD)

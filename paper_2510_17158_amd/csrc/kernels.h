@@ -36,11 +36,18 @@ struct WStack {
 };
 
 // A batch of products with the same shape: product b reads X + b sx, the
-// weights + (b / wdiv) sw and writes out + b so (elements).
+// weights + (b / wdiv) sw and writes out + b so (elements).  tri (a hint the
+// row-tile kernels use, always correct to ignore) for causal products whose
+// output rows m pair with columns or k-indices n <= m: 1 = output tiles lying
+// wholly above the diagonal (every column > every row) are not computed (nor
+// written: their consumer never reads them); 2 = X[m][k] is zero for k > m, so
+// each row tile's k loop ends after its last row; 3 = X[m][k] is zero for
+// k < m, so each row tile's k loop starts at its first row.
 struct GemmBatch {
   int count = 1;
   size_t sx = 0, sw = 0, so = 0;
   int wdiv = 1;
+  int tri = 0;
 };
 
 // EPI_LSE: for product row r (logits z = X W^T of the row, scaled x = c z with
