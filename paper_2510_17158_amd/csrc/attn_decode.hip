@@ -225,6 +225,35 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     }
   }
 
+  // The prompt chunks' partials (folding): issued here, without branches, so
+  // that their latency overlaps the reductions below.  Chunk c of the shared
+  // length is used when c < nused; an unused chunk's loads re-read chunk 0 and
+  // count as (max -inf, sum 0, output 0) in the merge.  Thread i < MAX_CHUNKS * MAXG
+  // loads the (max, sum) pair of chunk i / MAXG, head i % MAXG (shared by every
+  // head-dim element: kept in LDS); every thread loads the output elements of
+  // its NIT (head, element) pairs.
+  constexpr int NIT = (MAXG * HD + 255) / 256;
+  __shared__ __attribute__((aligned(8))) float2 fml[MAX_CHUNKS][MAXG];
+  float co[NIT][MAX_CHUNKS];
+  float2 cml = make_float2(-INFINITY, 0.f);
+  const int nused = fold ? min(ga.chunks, (base + ga.span_p - 1) / ga.span_p) : 0;
+  if (fold) {
+    const size_t rh = ((size_t)src * H + g * GQ) * S;   // partial row of head 0, chunk 0
+    if (tid < MAX_CHUNKS * MAXG) {
+      const int c = tid / MAXG, h = tid % MAXG;
+      const bool u = c < nused && h < GQ;
+      const float2 v = *(const float2*)(part_ml + (rh + (size_t)min(h, GQ - 1) * S + (u ? c : 0)) * 2);
+      cml = u ? v : make_float2(-INFINITY, 0.f);
+    }
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int i = min(tid + 256 * it, GQ * HD - 1);
+      const float* pr = part_o + (rh + (size_t)(i / HD) * S) * HD + i % HD;
+#pragma unroll
+      for (int c = 0; c < MAX_CHUNKS; ++c) co[it][c] = pr[(size_t)(c < nused ? c : 0) * HD];
+    }
+  }
+
   // wave totals: o over the positions of a load instruction, l over the k-groups
 #pragma unroll
   for (int h = 0; h < MAXG; ++h)
@@ -248,10 +277,13 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
         for (int e = 0; e < 8; ++e) red[wave][h * HD + hg * 8 + e] = o[h][e];
       }
   }
+  if (fold && tid < MAX_CHUNKS * MAXG) fml[tid / MAXG][tid % MAXG] = cml;
   __syncthreads();
   // merge the 4 waves (fixed order)
-#pragma unroll 2
-  for (int i = tid; i < GQ * HD; i += 256) {
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int i = tid + 256 * it;
+    if (i >= GQ * HD) break;
     const int h = i / HD, e = i % HD;
     const float M = fmaxf(fmaxf(wm[0][h], wm[1][h]), fmaxf(wm[2][h], wm[3][h]));
     float x = 0.f, L = 0.f;
@@ -262,28 +294,19 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
       L = fmaf(c, wl[w][h], L);
     }
     if (fold) {
-      // the prompt chunks below the shared length (partial rows 0 .. chunks-1),
-      // all loads issued before any is used
-      const size_t r0 = ((size_t)src * H + g * GQ + h) * S;
-      float cm[MAX_CHUNKS], cl[MAX_CHUNKS], co[MAX_CHUNKS];
-#pragma unroll
-      for (int c = 0; c < MAX_CHUNKS; ++c) {
-        const bool u = c < ga.chunks && c * ga.span_p < base;
-        cm[c] = u ? part_ml[(r0 + c) * 2] : -INFINITY;
-        cl[c] = u ? part_ml[(r0 + c) * 2 + 1] : 0.f;
-        co[c] = u ? part_o[(r0 + c) * HD + e] : 0.f;
-      }
+      // the prompt chunks below the shared length (partial rows 0 .. chunks-1)
       float Mt = M;
 #pragma unroll
-      for (int c = 0; c < MAX_CHUNKS; ++c) Mt = fmaxf(Mt, cm[c]);
+      for (int c = 0; c < MAX_CHUNKS; ++c) Mt = fmaxf(Mt, fml[c][h].x);
       const float sc = __expf(M - Mt);
       x *= sc;
       L *= sc;
 #pragma unroll
       for (int c = 0; c < MAX_CHUNKS; ++c) {
-        const float w = __expf(cm[c] - Mt);   // 0 for unused chunks
-        x = fmaf(co[c], w, x);
-        L = fmaf(cl[c], w, L);
+        const float2 ml = fml[c][h];
+        const float w = __expf(ml.x - Mt);   // 0 for unused chunks
+        x = fmaf(c < nused ? co[it][c] : 0.f, w, x);
+        L = fmaf(ml.y, w, L);
       }
     }
     if (S == 1 || fold) {
