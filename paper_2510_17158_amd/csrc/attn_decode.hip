@@ -48,10 +48,19 @@ struct DecodeGroup { int G, prefix_len, n_sub, chunks, span_p; };
 
 // Positions the group of batch row b shares: prefix_len, cut to the context
 // every member has reached (so a shared position exists for all of them).
+// The members' positions are read eight at a time (indices past the group
+// repeat its last member), all eight loads in flight together.
 __device__ __forceinline__ int group_shared(const int32_t* __restrict__ pos, int grp,
                                             const DecodeGroup& ga, int max_len) {
   int pl = ga.prefix_len;
-  for (int i = 0; i < ga.G; ++i) pl = min(pl, min(pos[grp * ga.G + i], max_len - 1) + 1);
+  const int32_t* pg = pos + grp * ga.G;
+  for (int i0 = 0; i0 < ga.G; i0 += 8) {
+    int v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = pg[min(i0 + u, ga.G - 1)];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) pl = min(pl, min(v[u], max_len - 1) + 1);
+  }
   return pl;
 }
 
