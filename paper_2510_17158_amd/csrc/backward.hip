@@ -211,9 +211,15 @@ __global__ __launch_bounds__(256) void k_attn_tiles(const float* __restrict__ S,
                                                     const float* __restrict__ dP,
                                                     const float* __restrict__ stats, int T, int Tp,
                                                     float s, TO* __restrict__ dS,
-                                                    TO* __restrict__ dST, TO* __restrict__ PT) {
+                                                    TO* __restrict__ dST, TO* __restrict__ PT,
+                                                    int band) {
   __shared__ float tp[BT][BT + 1], td[BT][BT + 1];
   const int j0 = blockIdx.x * BT, i0 = blockIdx.y * BT, b = blockIdx.z;
+  // band > 0: the products that read these outputs take causal hints with row
+  // tiles of `band` rows (their k ranges end, or start, at their own row tile),
+  // so a tile above the diagonal is read only inside its row tile's band; the
+  // others are not written at all
+  if (band && j0 > i0 && j0 / band != i0 / band) return;
   const size_t base = (size_t)b * T * Tp;
   const bool live = j0 <= i0 + BT - 1 && i0 < T;     // some (i, j) with j <= i < T
   for (int e = threadIdx.x; e < BT * BT; e += 256) {
@@ -420,12 +426,15 @@ hipError_t attn_softmax_bwd(int dtype, const float* S, const float* dP, int T, i
   Prof pf("attn_softmax_bwd", st);
   k_attn_row_stats<<<dim3(T, batch), 256, 0, st>>>(S, dP, T, Tp, scale, stats);
   const dim3 grid(Tp / BT, Tp / BT, batch);
+  // fp32 models' products read every tile (zeros above the diagonal written);
+  // bf16 models' batched products run on the tiled GEMM, which honours the hints
+  static_assert(kTiledRows % BT == 0, "band of whole tiles");
   if (dtype == 0)
     k_attn_tiles<float><<<grid, 256, 0, st>>>(S, dP, stats, T, Tp, scale, (float*)dS, (float*)dST,
-                                              (float*)PT);
+                                              (float*)PT, 0);
   else
     k_attn_tiles<bf16_t><<<grid, 256, 0, st>>>(S, dP, stats, T, Tp, scale, (bf16_t*)dS,
-                                               (bf16_t*)dST, (bf16_t*)PT);
+                                               (bf16_t*)dST, (bf16_t*)PT, kTiledRows);
   return hipGetLastError();
 }
 

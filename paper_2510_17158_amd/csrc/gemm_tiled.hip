@@ -21,6 +21,7 @@ namespace grpo {
 namespace {
 
 constexpr int NT = 256, BM = 128, BN = 128, BK = 64, LROW = BK + 8;
+static_assert(BM == kTiledRows && BM % BK == 0, "the causal hints' band");
 constexpr int kBigTileRows = 1024;   // rows from which the 256 x 256 tiles are used
 
 struct TArgs {

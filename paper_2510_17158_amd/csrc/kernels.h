@@ -36,19 +36,25 @@ struct WStack {
 };
 
 // A batch of products with the same shape: product b reads X + b sx, the
-// weights + (b / wdiv) sw and writes out + b so (elements).  tri (a hint the
-// row-tile kernels use, always correct to ignore) for causal products whose
-// output rows m pair with columns or k-indices n <= m: 1 = output tiles lying
-// wholly above the diagonal (every column > every row) are not computed (nor
-// written: their consumer never reads them); 2 = X[m][k] is zero for k > m, so
-// each row tile's k loop ends after its last row; 3 = X[m][k] is zero for
-// k < m, so each row tile's k loop starts at its first row.
+// weights + (b / wdiv) sw and writes out + b so (elements).  tri, for causal
+// products whose output rows m pair with columns or k-indices n <= m: 1 = output
+// tiles lying wholly above the diagonal (every column > every row) are not
+// computed (nor written: their consumer never reads them); 2 = X[m][k] is zero
+// for k > m, and each row tile's k loop ends after its last row; 3 = X[m][k] is
+// zero for k < m, and each row tile's k loop starts at its first row.  The bf16
+// row-tile kernel honours tri (its callers may leave X unwritten outside the
+// band of kTiledRows rows its row tiles still read); the fp32 kernel ignores it
+// (its callers write the zeros).
 struct GemmBatch {
   int count = 1;
   size_t sx = 0, sw = 0, so = 0;
   int wdiv = 1;
   int tri = 0;
 };
+// Row-tile height of the bf16 row-tile kernel (batched products always run on
+// it): with tri 2 or 3 a row tile reads X only inside this band around the
+// diagonal.
+constexpr int kTiledRows = 128;
 
 // EPI_LSE: for product row r (logits z = X W^T of the row, scaled x = c z with
 // c = log2(e) / temperature) and each 64-column slot s (columns 64 s .. 64 s + 63
