@@ -29,14 +29,56 @@ constexpr int BT = 64;    // transpose tile
 
 // out[c][r] = in[r][c] (r < R, c < C); out columns R .. Rpad-1 are zero.
 // Batch element b: in + b * in_bs, out + (b / div) * s1 + (b % div) * s2.
+// vec (16-byte aligned rows and batch offsets on both sides): a tile inside
+// [0, R) x [0, C) is read and written in 16-byte pieces (all loads in flight
+// together, a 64-element output row by 8 or 16 lanes); edge tiles element-wise.
 template <typename TI, typename TO>
 __global__ __launch_bounds__(256) void k_transpose(const TI* __restrict__ in, int ldi, size_t in_bs,
                                                    int R, int C, TO* __restrict__ out, int ldo,
-                                                   size_t s1, size_t s2, int div, int Rpad) {
+                                                   size_t s1, size_t s2, int div, int Rpad,
+                                                   int vec) {
   __shared__ float tile[BT][BT + 1];
   const int b = blockIdx.z, r0 = blockIdx.x * BT, c0 = blockIdx.y * BT;
   in += (size_t)b * in_bs;
   out += (size_t)(b / div) * s1 + (size_t)(b % div) * s2;
+  if (vec && r0 + BT <= R && c0 + BT <= C) {
+    constexpr int VI = 16 / sizeof(TI), TPI = BT / VI, RPI = 256 / TPI;
+    u32x4_t v[BT / RPI];
+#pragma unroll
+    for (int p = 0; p < BT / RPI; ++p) {
+      const int r = p * RPI + threadIdx.x / TPI, c = (threadIdx.x % TPI) * VI;
+      v[p] = *(const u32x4_t*)(in + (size_t)(r0 + r) * ldi + c0 + c);
+    }
+#pragma unroll
+    for (int p = 0; p < BT / RPI; ++p) {
+      const int r = p * RPI + threadIdx.x / TPI, c = (threadIdx.x % TPI) * VI;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if constexpr (sizeof(TI) == 4) {
+          tile[r][c + k] = __uint_as_float(v[p][k]);
+        } else {
+          tile[r][c + 2 * k] = __uint_as_float(v[p][k] << 16);
+          tile[r][c + 2 * k + 1] = __uint_as_float(v[p][k] & 0xffff0000u);
+        }
+      }
+    }
+    __syncthreads();
+    constexpr int VO = 16 / sizeof(TO), TPO = BT / VO, RPO = 256 / TPO;
+#pragma unroll
+    for (int p = 0; p < BT / RPO; ++p) {
+      const int c = p * RPO + threadIdx.x / TPO, r = (threadIdx.x % TPO) * VO;
+      u32x4_t w;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if constexpr (sizeof(TO) == 4)
+          w[k] = __float_as_uint(tile[r + k][c]);
+        else
+          w[k] = (uint32_t)f2bf(tile[r + 2 * k][c]) | ((uint32_t)f2bf(tile[r + 2 * k + 1][c]) << 16);
+      }
+      *(u32x4_t*)(out + (size_t)(c0 + c) * ldo + r0 + r) = w;
+    }
+    return;
+  }
   for (int i = threadIdx.x; i < BT * BT; i += 256) {
     const int r = i / BT, c = i % BT;
     tile[r][c] = (r0 + r < R && c0 + c < C) ? ldf(in, (size_t)(r0 + r) * ldi + c0 + c) : 0.f;
@@ -212,7 +254,7 @@ __global__ __launch_bounds__(256) void k_attn_tiles(const float* __restrict__ S,
                                                     const float* __restrict__ stats, int T, int Tp,
                                                     float s, TO* __restrict__ dS,
                                                     TO* __restrict__ dST, TO* __restrict__ PT,
-                                                    int band) {
+                                                    int band, int vec) {
   __shared__ float tp[BT][BT + 1], td[BT][BT + 1];
   const int j0 = blockIdx.x * BT, i0 = blockIdx.y * BT, b = blockIdx.z;
   // band > 0: the products that read these outputs take causal hints with row
@@ -222,6 +264,72 @@ __global__ __launch_bounds__(256) void k_attn_tiles(const float* __restrict__ S,
   if (band && j0 > i0 && j0 / band != i0 / band) return;
   const size_t base = (size_t)b * T * Tp;
   const bool live = j0 <= i0 + BT - 1 && i0 < T;     // some (i, j) with j <= i < T
+  if constexpr (sizeof(TO) == 2) {
+    if (vec && i0 + BT <= T) {
+      // 16-byte pieces: lane quarter q of row r takes columns 8 q .. 8 q + 7 and
+      // 32 + 8 q .. 32 + 8 q + 7 (the same arithmetic as the element-wise path)
+      const int r = threadIdx.x / 4, q = threadIdx.x % 4, i = i0 + r;
+      float p[2][8], ds[2][8];
+      if (live) {
+        const float* st = stats + ((size_t)b * T + i) * 3;
+        const size_t o = base + (size_t)i * Tp + j0 + 8 * q;
+        f32x4_t sv[2][2], dv[2][2];
+#pragma unroll
+        for (int g = 0; g < 2; ++g)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            sv[g][h] = *(const f32x4_t*)(S + o + 32 * g + 4 * h);
+            dv[g][h] = *(const f32x4_t*)(dP + o + 32 * g + 4 * h);
+          }
+        const float m = st[0], rs = st[1], dd = st[2];
+#pragma unroll
+        for (int g = 0; g < 2; ++g)
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            const int j = j0 + 32 * g + 8 * q + k;
+            const float pv = __expf(sv[g][k / 4][k % 4] * s - m) * rs;
+            const float dsv = pv * (dv[g][k / 4][k % 4] - dd) * s;
+            p[g][k] = j <= i ? pv : 0.f;
+            ds[g][k] = j <= i ? dsv : 0.f;
+          }
+      } else {
+#pragma unroll
+        for (int g = 0; g < 2; ++g)
+#pragma unroll
+          for (int k = 0; k < 8; ++k) p[g][k] = ds[g][k] = 0.f;
+      }
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        u32x4_t w;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          w[k] = (uint32_t)f2bf(ds[g][2 * k]) | ((uint32_t)f2bf(ds[g][2 * k + 1]) << 16);
+        *(u32x4_t*)(dS + base + (size_t)i * Tp + j0 + 32 * g + 8 * q) = w;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          tp[r][32 * g + 8 * q + k] = p[g][k];
+          td[r][32 * g + 8 * q + k] = ds[g][k];
+        }
+      }
+      __syncthreads();
+      // transposed: output row j0 + c, columns i0 + 8 u .. i0 + 8 u + 7
+      const size_t tb = (size_t)b * Tp * Tp;
+#pragma unroll
+      for (int pass = 0; pass < 2; ++pass) {
+        const int c = pass * 32 + threadIdx.x / 8, u = threadIdx.x % 8;
+        u32x4_t wp, wd;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          wp[k] = (uint32_t)f2bf(tp[8 * u + 2 * k][c]) | ((uint32_t)f2bf(tp[8 * u + 2 * k + 1][c]) << 16);
+          wd[k] = (uint32_t)f2bf(td[8 * u + 2 * k][c]) | ((uint32_t)f2bf(td[8 * u + 2 * k + 1][c]) << 16);
+        }
+        const size_t o = tb + (size_t)(j0 + c) * Tp + i0 + 8 * u;
+        *(u32x4_t*)(PT + o) = wp;
+        *(u32x4_t*)(dST + o) = wd;
+      }
+      return;
+    }
+  }
   for (int e = threadIdx.x; e < BT * BT; e += 256) {
     const int r = e / BT, c = e % BT, i = i0 + r, j = j0 + c;
     float p = 0.f, ds = 0.f;
@@ -347,15 +455,19 @@ hipError_t transpose(int tin, int tout, const void* in, int ldi, size_t in_bs, i
   if (Rpad < R || div < 1) return hipErrorInvalidValue;
   dim3 grid((Rpad + BT - 1) / BT, (C + BT - 1) / BT, batch);
   Prof pf("transpose", st);
+  const size_t ei = tin == 0 ? 4 : 2, eo = tout == 0 ? 4 : 2;
+  const int vec = (uintptr_t)in % 16 == 0 && (uintptr_t)out % 16 == 0 && ldi * ei % 16 == 0 &&
+                  in_bs * ei % 16 == 0 && ldo * eo % 16 == 0 && s1 * eo % 16 == 0 &&
+                  s2 * eo % 16 == 0;
   if (tin == 0 && tout == 0)
     k_transpose<float, float><<<grid, 256, 0, st>>>((const float*)in, ldi, in_bs, R, C, (float*)out,
-                                                    ldo, s1, s2, div, Rpad);
+                                                    ldo, s1, s2, div, Rpad, vec);
   else if (tin == 0)
     k_transpose<float, bf16_t><<<grid, 256, 0, st>>>((const float*)in, ldi, in_bs, R, C,
-                                                     (bf16_t*)out, ldo, s1, s2, div, Rpad);
+                                                     (bf16_t*)out, ldo, s1, s2, div, Rpad, vec);
   else if (tout == 1)
     k_transpose<bf16_t, bf16_t><<<grid, 256, 0, st>>>((const bf16_t*)in, ldi, in_bs, R, C,
-                                                      (bf16_t*)out, ldo, s1, s2, div, Rpad);
+                                                      (bf16_t*)out, ldo, s1, s2, div, Rpad, vec);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -429,12 +541,15 @@ hipError_t attn_softmax_bwd(int dtype, const float* S, const float* dP, int T, i
   // fp32 models' products read every tile (zeros above the diagonal written);
   // bf16 models' batched products run on the tiled GEMM, which honours the hints
   static_assert(kTiledRows % BT == 0, "band of whole tiles");
+  // bf16 outputs in 16-byte pieces when every row start is 16-byte aligned
+  const int vec = (uintptr_t)S % 16 == 0 && (uintptr_t)dP % 16 == 0 && (uintptr_t)dS % 16 == 0 &&
+                  (uintptr_t)dST % 16 == 0 && (uintptr_t)PT % 16 == 0;
   if (dtype == 0)
     k_attn_tiles<float><<<grid, 256, 0, st>>>(S, dP, stats, T, Tp, scale, (float*)dS, (float*)dST,
-                                              (float*)PT, 0);
+                                              (float*)PT, 0, 0);
   else
     k_attn_tiles<bf16_t><<<grid, 256, 0, st>>>(S, dP, stats, T, Tp, scale, (bf16_t*)dS,
-                                               (bf16_t*)dST, (bf16_t*)PT, kTiledRows);
+                                               (bf16_t*)dST, (bf16_t*)PT, kTiledRows, vec);
   return hipGetLastError();
 }
 
