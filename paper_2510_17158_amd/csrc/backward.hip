@@ -227,20 +227,37 @@ __global__ __launch_bounds__(256) void k_attn_row_stats(const float* __restrict_
   const size_t row = ((size_t)b * T + i) * Tp;
   const float* sr = S + row;
   const float* dr = dP + row;
-  float m = -INFINITY;
-  for (int j = threadIdx.x; j <= i; j += 256) m = fmaxf(m, sr[j] * s);
-  m = block_max<256>(m, sh);
-  float l = 0.f, dd = 0.f;
-  for (int j = threadIdx.x; j <= i; j += 256) {
-    const float e = __expf(sr[j] * s - m);
-    l += e;
-    dd = fmaf(e, dr[j], dd);
+  // one pass: each thread reads 4 consecutive columns per step (16-byte loads;
+  // columns past i, still inside the row's Tp, are masked) and keeps its own
+  // running maximum, with its sums rescaled when that moves; the threads' sums
+  // are then brought to the row maximum and added in a fixed order
+  float m = -INFINITY, l = 0.f, dd = 0.f;
+  for (int j4 = 4 * threadIdx.x; j4 <= i; j4 += 1024) {
+    const f32x4_t sv = *(const f32x4_t*)(sr + j4), dv = *(const f32x4_t*)(dr + j4);
+    float x[4], mx = m;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      x[k] = j4 + k <= i ? sv[k] * s : -INFINITY;
+      mx = fmaxf(mx, x[k]);
+    }
+    const float c = __expf(m - mx);   // 0 while m is -inf
+    l *= c;
+    dd *= c;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float e = __expf(x[k] - mx);   // 0 for masked columns
+      l += e;
+      dd = fmaf(e, j4 + k <= i ? dv[k] : 0.f, dd);
+    }
+    m = mx;
   }
-  l = block_sum<256>(l, sh);
-  dd = block_sum<256>(dd, sh);
+  const float M = block_max<256>(m, sh);
+  const float w = m == -INFINITY ? 0.f : __expf(m - M);
+  const float L = block_sum<256>(l * w, sh);
+  const float DD = block_sum<256>(dd * w, sh);
   if (threadIdx.x == 0) {
     float* o = stats + ((size_t)b * T + i) * 3;
-    o[0] = m; o[1] = 1.f / l; o[2] = dd / l;
+    o[0] = M; o[1] = 1.f / L; o[2] = DD / L;
   }
 }
 
