@@ -391,6 +391,10 @@ typedef struct grpo_grads {
  * the model dtype (bf16 products on the matrix cores).  Every sum has a fixed
  * order, the embedding rows' included (positions grouped by token, then added
  * in position order): results are bit-deterministic.
+ * Where a layer's wq, wk and wv gradients are adjacent in memory (wk right
+ * after wq, wv right after wk), and likewise its w_gate and w_up gradients,
+ * each group's weight gradient is one product (the same sums, so the same
+ * bits); otherwise one product per tensor.
  * Workspace: grpo_workspace_bytes(GRPO_OP_BACKWARD, N, T) (it holds transposed
  * copies of every weight matrix).  GRPO_INVALID_ARG for a NULL gradient buffer
  * or score_from outside [1, T); GRPO_UNSUPPORTED for T above 16384. */

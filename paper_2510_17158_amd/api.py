@@ -429,12 +429,29 @@ WEIGHT_NAMES_LAYER = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate",
 
 
 class Grads:
-    """fp32 gradient accumulators shaped like a model's weights (zeroed)."""
+    """fp32 gradient accumulators shaped like a model's weights (zeroed).  Each
+    layer's q, k and v gradients are views of one buffer in that order, and so
+    are its gate and up gradients: the backward then forms each group's weight
+    gradient in a single product."""
+
+    GROUPS = (("wq", "wk", "wv"), ("w_gate", "w_up"))
 
     def __init__(self, model: "Model"):
-        self.t = {k: torch.zeros(v.shape, dtype=torch.float32, device=v.device)
-                  for k, v in model.weights.items()}
         L = model.cfg.n_layers
+        self.t = {}
+        for i in range(L):
+            for grp in self.GROUPS:
+                names = [f"l{i}.{n}" for n in grp]
+                ws = [model.weights[n] for n in names]
+                flat = torch.zeros(sum(w.numel() for w in ws), dtype=torch.float32,
+                                   device=ws[0].device)
+                off = 0
+                for n, w in zip(names, ws):
+                    self.t[n] = flat[off:off + w.numel()].view(w.shape)
+                    off += w.numel()
+        for k, v in model.weights.items():
+            if k not in self.t:
+                self.t[k] = torch.zeros(v.shape, dtype=torch.float32, device=v.device)
         self._arrays = {n: (C.c_void_p * L)(*[_ptr(self.t[f"l{i}.{n}"]) for i in range(L)])
                         for n in WEIGHT_NAMES_LAYER}
         self.struct = GradsStruct(_ptr(self.t["tok_emb"]),

@@ -1700,11 +1700,16 @@ int grpo_policy_backward(const grpo_model* m, const int32_t* tokens, int32_t N, 
       // gate / up: dgu^T h2 for each half, dh2 = dgu [Wg; Wu]
       HIPCHK(transpose(e, e, w.dgu, 2 * f, 0, T, 2 * f, w.tA, Tp, 0, 0, 1, Tp, 1, st));
       HIPCHK(transpose(e, e, w.h2, d, 0, T, d, w.tB, Tp, 0, 0, 1, Tp, 1, st));
-      if ((rc = gemm_rows(m, w.tA, Tp, f, one(w.tB), d, Tp, EPI_RESID,
-                          EpiArgs{g->w_gate[l], nullptr, d}, st)) ||
-          (rc = gemm_rows(m, (char*)w.tA + (size_t)f * Tp * es, Tp, f, one(w.tB), d, Tp, EPI_RESID,
-                          EpiArgs{g->w_up[l], nullptr, d}, st)))
+      if (g->w_up[l] == g->w_gate[l] + (size_t)f * d) {   // adjacent: one product
+        if ((rc = gemm_rows(m, w.tA, Tp, 2 * f, one(w.tB), d, Tp, EPI_RESID,
+                            EpiArgs{g->w_gate[l], nullptr, d}, st)))
+          return rc;
+      } else if ((rc = gemm_rows(m, w.tA, Tp, f, one(w.tB), d, Tp, EPI_RESID,
+                                 EpiArgs{g->w_gate[l], nullptr, d}, st)) ||
+                 (rc = gemm_rows(m, (char*)w.tA + (size_t)f * Tp * es, Tp, f, one(w.tB), d, Tp,
+                                 EPI_RESID, EpiArgs{g->w_up[l], nullptr, d}, st))) {
         return rc;
+      }
       if ((rc = gemm_rows(m, w.dgu, 2 * f, T, one(w.WguT[l]), d, 2 * f, EPI_STORE,
                           EpiArgs{w.dh, nullptr, d}, st)))
         return rc;
@@ -1723,13 +1728,18 @@ int grpo_policy_backward(const grpo_model* m, const int32_t* tokens, int32_t N, 
       // q, k, v projections: dqkv^T h into the three gradients, dh = dqkv [Wq; Wk; Wv]
       HIPCHK(transpose(e, e, w.dqkve, ldqkv, 0, T, ldqkv, w.tA, Tp, 0, 0, 1, Tp, 1, st));
       HIPCHK(transpose(e, e, w.h, d, 0, T, d, w.tB, Tp, 0, 0, 1, Tp, 1, st));
-      if ((rc = gemm_rows(m, w.tA, Tp, qd, one(w.tB), d, Tp, EPI_RESID,
-                          EpiArgs{g->wq[l], nullptr, d}, st)) ||
-          (rc = gemm_rows(m, (char*)w.tA + (size_t)qd * Tp * es, Tp, kvd, one(w.tB), d, Tp,
-                          EPI_RESID, EpiArgs{g->wk[l], nullptr, d}, st)) ||
-          (rc = gemm_rows(m, (char*)w.tA + (size_t)(qd + kvd) * Tp * es, Tp, kvd, one(w.tB), d, Tp,
-                          EPI_RESID, EpiArgs{g->wv[l], nullptr, d}, st)))
+      if (g->wk[l] == g->wq[l] + (size_t)qd * d && g->wv[l] == g->wk[l] + (size_t)kvd * d) {
+        if ((rc = gemm_rows(m, w.tA, Tp, ldqkv, one(w.tB), d, Tp, EPI_RESID,
+                            EpiArgs{g->wq[l], nullptr, d}, st)))   // adjacent: one product
+          return rc;
+      } else if ((rc = gemm_rows(m, w.tA, Tp, qd, one(w.tB), d, Tp, EPI_RESID,
+                                 EpiArgs{g->wq[l], nullptr, d}, st)) ||
+                 (rc = gemm_rows(m, (char*)w.tA + (size_t)qd * Tp * es, Tp, kvd, one(w.tB), d, Tp,
+                                 EPI_RESID, EpiArgs{g->wk[l], nullptr, d}, st)) ||
+                 (rc = gemm_rows(m, (char*)w.tA + (size_t)(qd + kvd) * Tp * es, Tp, kvd,
+                                 one(w.tB), d, Tp, EPI_RESID, EpiArgs{g->wv[l], nullptr, d}, st))) {
         return rc;
+      }
       if ((rc = gemm_rows(m, w.dqkve, ldqkv, T, one(w.WqkvT[l]), d, ldqkv, EPI_STORE,
                           EpiArgs{w.dh, nullptr, d}, st)))
         return rc;
