@@ -35,8 +35,8 @@ BF16_PEAK_TFLOPS = 2500.0
 # 64 sequences).
 ATTN_TRAFFIC = {
     "source": "paper_2510_17158_amd/csrc/attn_decode.hip",
-    "sha256": "3035248a273ad777715056aedf518f0fd3c09527947fdc947ae5955717643d59",
-    "fixed_fetch_kib": 4586.2, "per_position_fetch_kib": 128.297, "fetch_scale": 2.0,
+    "sha256": "1ec040d050f79730846e1096a8da8d617d7cfff157bd5963b4c2d78c117bf392",
+    "fixed_fetch_kib": 4536.8, "per_position_fetch_kib": 129.882, "fetch_scale": 2.0,
     "write_kib": 512.0, "write_scale": 1.0,
     "position_bytes": 64 * 4096,
 }
@@ -79,6 +79,26 @@ def copy_ceiling_gbs(torch) -> float:
     del src, dst
     torch.cuda.empty_cache()
     return 2 * (1 << 30) / (best / 1e3) / 1e9
+
+
+def read_ceiling_gbs(torch) -> float:
+    """HBM read rate of a plain streaming reduction: torch's fp32 sum over 4 GiB of
+    bf16 (bytes read per second; the one-float result aside), the best of 5 timed
+    sums after one untimed.  The decode step reads almost everything it moves, so
+    this is the ceiling it compares with beside the spec peak."""
+    x = torch.ones(1 << 31, dtype=torch.bfloat16, device="cuda")
+    s = x.sum(dtype=torch.float32)
+    best = float("inf")
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        s = x.sum(dtype=torch.float32)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del x, s
+    torch.cuda.empty_cache()
+    return 2 * (1 << 31) / (best / 1e3) / 1e9
 
 
 def gemm_ceiling_tflops(torch, n: int = 8192) -> float:
@@ -445,10 +465,14 @@ def main():
         out["scored_tokens_per_s"] = n_models * w.batch * w.total_len / (phases[2] / 1e3)
         out["score_tflops"] = n_models * sf / (phases[2] / 1e3) / 1e12
         out["score_mfma_frac"] = out["score_tflops"] / BF16_PEAK_TFLOPS
-    # the decode step against a measured stream-copy ceiling as well as the spec peak
+    # the decode step against measured stream-copy and stream-read ceilings as well
+    # as the spec peak
     cc = copy_ceiling_gbs(torch)
     out["copy_ceiling_gbs"] = cc
     out["decode_step_copy_frac"] = out["decode_step_gbs"] / cc
+    rc = read_ceiling_gbs(torch)
+    out["read_ceiling_gbs"] = rc
+    out["decode_step_read_frac"] = out["decode_step_gbs"] / rc
     # scoring against the measured dense-GEMM rate as well as the spec peak
     if w.score and c.dtype == 1:
         gc = gemm_ceiling_tflops(torch)
