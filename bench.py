@@ -82,23 +82,28 @@ def copy_ceiling_gbs(torch) -> float:
 
 
 def read_ceiling_gbs(torch) -> float:
-    """HBM read rate of a plain streaming reduction: torch's fp32 sum over 4 GiB of
-    bf16 (bytes read per second; the one-float result aside), the best of 5 timed
-    sums after one untimed.  The decode step reads almost everything it moves, so
-    this is the ceiling it compares with beside the spec peak."""
-    x = torch.ones(1 << 31, dtype=torch.bfloat16, device="cuda")
-    s = x.sum(dtype=torch.float32)
+    """HBM read rate of the vendor library's memory-bound kernel of the decode
+    step's own kind: a bf16 matrix-vector product (torch.mv) over a 4 GiB matrix
+    (matrix bytes per second; the vector and the result aside), the best of 5
+    timed products after one untimed.  The decode step reads almost everything it
+    moves, so this is the ceiling it compares with beside the spec peak (a plain
+    full-tensor sum reads at little more than half this rate, a device copy, read
+    plus write, at about 0.8 of it)."""
+    rows, cols = 1 << 16, 1 << 15
+    a = torch.ones(rows, cols, dtype=torch.bfloat16, device="cuda")
+    v = torch.ones(cols, dtype=torch.bfloat16, device="cuda")
+    y = torch.mv(a, v)
     best = float("inf")
     for _ in range(5):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        s = x.sum(dtype=torch.float32)
+        y = torch.mv(a, v)
         e1.record()
         torch.cuda.synchronize()
         best = min(best, e0.elapsed_time(e1))
-    del x, s
+    del a, v, y
     torch.cuda.empty_cache()
-    return 2 * (1 << 31) / (best / 1e3) / 1e9
+    return 2 * rows * cols / (best / 1e3) / 1e9
 
 
 def gemm_ceiling_tflops(torch, n: int = 8192) -> float:
