@@ -275,7 +275,9 @@ hipError_t launch_rb(const DArgs& a, int epi, int grid, const char* name, hipStr
 template <int NB>
 hipError_t launch_nb(const DArgs& a, int epi, int grid, int rb, const char* name, hipStream_t st) {
   if constexpr (NB >= 128) {
-    return rb == 2 ? launch_rb<NB, 2>(a, epi, grid, name, st) : hipErrorInvalidValue;
+    return rb == 2   ? launch_rb<NB, 2>(a, epi, grid, name, st)
+           : rb == 4 ? launch_rb<NB, 4>(a, epi, grid, name, st)
+                     : hipErrorInvalidValue;
   } else {
     switch (rb) {
       case 4: return launch_rb<NB, 4>(a, epi, grid, name, st);
@@ -329,20 +331,25 @@ static int decode_splits(int tiles, int K, int epi, int target_wgs, int max_spli
   return splits;
 }
 
-// Tile height: of 4, 6, 7 and 8 blocks of 16 rows (2 at nb = 128, for
-// registers), the one whose grid fills the compute units most evenly (workgroups
-// over the next multiple of 256); on ties fewer splits (less partial traffic),
-// then the taller tile (fewer activation reloads).  At the 7B shape: QKV 6 (64
-// tiles x 4 splits), SwiGLU 7 (256 tiles), O and down 4 (64 x 4), LM head 8.
+// Tile height: of 4, 6, 7 and 8 blocks of 16 rows, the one whose grid fills
+// the compute units most evenly (workgroups over the next multiple of 256); on
+// ties fewer splits (less partial traffic), then the taller tile (fewer
+// activation reloads).  At the 7B shape: QKV 6 (64 tiles x 4 splits), SwiGLU 7
+// (256 tiles), O and down 4 (64 x 4), LM head 8.  At nb = 128 the accumulators
+// of a taller tile leave room for one wave per SIMD only: 4 blocks for weight
+// matrices of 32 MiB or more (a long stream, where four times the activation
+// reuse pays; 1B shape: SwiGLU, down and the LM head 15-20% faster), else 2
+// (QKV and O of the 1B shape were 10-25% slower at 4).
 DecodePlan decode_plan(int B, int N, int K, int epi, int target_wgs, int max_splits) {
   DecodePlan p{};
   p.nb = decode_nb(B);
   if (target_wgs <= 0) target_wgs = 512;
   const int blocks = N / 16;
   const int cands[4] = {4, 6, 7, 8};
+  const int rb128 = (size_t)N * K * 2 >= ((size_t)32 << 20) ? 4 : 2;
   double best = -1.0;
   for (int c = 0; c < (p.nb >= 128 ? 1 : 4); ++c) {
-    const int rb = p.nb >= 128 ? 2 : cands[c];
+    const int rb = p.nb >= 128 ? rb128 : cands[c];
     const int tiles = (blocks + rb - 1) / rb;
     const int splits = decode_splits(tiles, K, epi, target_wgs, max_splits);
     const long wgs = (long)tiles * splits;
