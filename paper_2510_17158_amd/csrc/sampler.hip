@@ -159,7 +159,8 @@ __global__ __launch_bounds__(NTR) void k_sample_reg(const float* __restrict__ lo
   __shared__ float sh[NTR / 64];
   __shared__ float shv[NTR / 64];
   __shared__ int shi[NTR / 64];
-  __shared__ int hist[256];
+  __shared__ int hist[NTR / 64][256];   // one histogram per wave
+  __shared__ int hsum[256];
   __shared__ uint32_t s_prefix;
   __shared__ int s_krem, s_eq, s_cut;
   const int r = blockIdx.x, gdraw = blockIdx.y;
@@ -212,8 +213,9 @@ __global__ __launch_bounds__(NTR) void k_sample_reg(const float* __restrict__ lo
     if (use_k) {
       uint32_t prefix = 0, pmask = 0;
       int krem = a.top_k;
+      const int wave = tid / 64, lane = tid % 64;
       for (int shift = 24; shift >= 0; shift -= 8) {
-        for (int i = tid; i < 256; i += NTR) hist[i] = 0;
+        for (int i = tid; i < (NTR / 64) * 256; i += NTR) (&hist[0][0])[i] = 0;
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < R4; ++j)
@@ -221,18 +223,49 @@ __global__ __launch_bounds__(NTR) void k_sample_reg(const float* __restrict__ lo
           for (int e = 0; e < 4; ++e) {
             const uint32_t u = order_key(x[j][e]);
             if (4 * (tid + NTR * j) + e < V && (u & pmask) == prefix)
-              atomicAdd(&hist[(u >> shift) & 255], 1);
+              atomicAdd(&hist[wave][(u >> shift) & 255], 1);
           }
         __syncthreads();
-        if (tid == 0) {
-          int cum = 0, sel = 0;
-          for (int bin = 255; bin >= 0; --bin) {
-            if (cum + hist[bin] >= krem) { sel = bin; break; }
-            cum += hist[bin];
+        for (int b = tid; b < 256; b += NTR) {
+          int t = 0;
+#pragma unroll
+          for (int w = 0; w < NTR / 64; ++w) t += hist[w][b];
+          hsum[b] = t;
+        }
+        __syncthreads();
+        // the highest bin whose count, added to those of all higher bins, reaches
+        // krem: lane l holds bins 255 - 4 l .. 252 - 4 l, the counts above its
+        // first bin come from a scan over the lanes
+        if (wave == 0) {
+          const int* hb = hsum + 252 - 4 * lane;   // this lane's bins, hb[3] the highest
+          const int own = hb[0] + hb[1] + hb[2] + hb[3];
+          int above = own;   // inclusive scan over lanes 0 .. lane
+#pragma unroll
+          for (int off = 1; off < 64; off <<= 1) {
+            const int v = __shfl_up(above, off, 64);
+            if (lane >= off) above += v;
           }
-          s_krem = krem - cum;
-          s_eq = hist[sel];
-          s_prefix = prefix | ((uint32_t)sel << shift);
+          int cum = above - own, sel = -1, before = 0;
+#pragma unroll
+          for (int q = 3; q >= 0; --q) {
+            const int cq = hb[q];
+            if (sel < 0 && cum + cq >= krem) { sel = 252 - 4 * lane + q; before = cum; }
+            cum += cq;
+          }
+          const unsigned long long found = __ballot(sel >= 0);
+          if (found) {
+            const int first = __ffsll((long long)found) - 1;
+            sel = __shfl(sel, first, 64);
+            before = __shfl(before, first, 64);
+          } else {   // not reached: every count summed, the lowest bin
+            sel = 0;
+            before = __shfl(above, 63, 64);
+          }
+          if (lane == 0) {
+            s_krem = krem - before;
+            s_eq = hsum[sel];
+            s_prefix = prefix | ((uint32_t)sel << shift);
+          }
         }
         __syncthreads();
         krem = s_krem;
