@@ -3,6 +3,8 @@
 fp32 tolerance 1e-4; every stage of a prefill and a decode step against the
 oracle on the GPU's own inputs within the bounds of its fp32 arithmetic; the
 sampler on the GPU's logits for sampled decoding."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -129,6 +131,32 @@ def test_tiny_sampler_on_gpu_logits(tiny, temperature, top_k):
                      forced=np.concatenate([it.tok0.cpu().numpy()[:, None], toks], 1))
     ok = ref["margin"][:, 1:] > 2 * TOL / temperature
     assert np.array_equal(toks[ok], ref["own_tokens"][:, 1:][ok])
+
+
+@pytest.mark.parametrize("temperature,top_k", [(1.0, 0), (0.8, 50), (0.0, 0), (1.2, 1)])
+def test_large_vocab_sampler_on_gpu_logits(temperature, top_k):
+    """Vocabularies above 32768 ids take the sampler's streaming kernel (the row's
+    logits read on every pass instead of held in registers): its tokens and
+    log-probs against the oracle sampler on the GPU's own logits, at vocabulary
+    40000 (one layer of the tiny widths), for a draw without a cut, a top-k cut,
+    greedy and top-1."""
+    require_gpu()
+    w = get("tiny")
+    w = w.with_(model=dataclasses.replace(w.model, vocab=40000, n_layers=1),
+                temperature=temperature, top_k=top_k, new_tokens=5)
+    say("large-vocabulary sampler", temperature, top_k)
+    host, model = build_model(w.model, w.master_seed, gain_noise=0.1)
+    seed = synth.make_seed(w) ^ 0x2545F491
+    it = GrpoIteration(w, model, None, synth.make_prompts(w), synth.make_rewards(w), seed)
+    it.prefill()
+    toks, lps, logits = _stepwise(it, w.new_tokens - 1)
+    assert np.all((toks >= 0) & (toks < w.model.vocab))
+    near_total = 0
+    for s in range(toks.shape[1]):
+        near_total += sampler_check(logits[:, s], toks[:, s], lps[:, s], temperature, top_k, seed,
+                                    1 + s, np.arange(it.B), band=NEAR_TIE)
+    say("near ties", near_total)
+    model.close()
 
 
 def test_tiny_resume_and_determinism(tiny):
