@@ -17,7 +17,7 @@ import torch
 
 import oracle
 from paper_2510_17158_amd import api
-from paper_2510_17158_amd.workloads import DTYPE_F32, M7B, SMALL, TINY
+from paper_2510_17158_amd.workloads import DTYPE_F32, M32B, M7B, SMALL, TINY
 
 from gpu_util import build_model, require_gpu, say
 
@@ -40,6 +40,9 @@ def _grads_oracle(cfg, host, tokens, sf, temp, dlogp):
     (dataclasses.replace(SMALL, n_layers=1), 2, 64, 1, 0.8),
     # the 7B width (head_dim 128, GQ 4, vocab 32000), one layer, 2048 positions
     (dataclasses.replace(M7B, n_layers=1), 1, 2048, 1024, 1.0),
+    # the 32B width (GQ 5: head batches of whole 5-head groups, vocab 152064), one
+    # layer, a ragged length
+    (dataclasses.replace(M32B, n_layers=1), 1, 200, 77, 0.9),
 ])
 def test_policy_backward_matches_oracle(cfg, N, T, sf, temp):
     require_gpu()
