@@ -8,9 +8,9 @@ own normed rows, every scored row's log-prob against log_softmax of those
 logits within the bound of the fused arithmetic (stagecheck.score_logp_bound),
 and the log-probs end to end against the oracle's teacher-forced scoring.
 The cases cover the three product kernels (256 x 256 tiles: >= 1024 rows and a
-vocabulary in multiples of 256; 128 x 128 tiles; fp32), vocabularies that end
-inside a 64-column slot or leave a tile's second half past the last column,
-and temperatures other than 1 (0 scores at 1)."""
+vocabulary in multiples of 256, 32000 and 152064 ids; 128 x 128 tiles; fp32),
+vocabularies that end inside a 64-column slot or leave a tile's second half
+past the last column, and temperatures other than 1 (0 scores at 1)."""
 import dataclasses
 
 import numpy as np
@@ -31,6 +31,7 @@ T1 = dataclasses.replace(TINY, n_layers=1)
 CASES = [
     # cfg, sequences, T, score_from, temperature; scored rows = N (T - score_from)
     (S1, 2, 1100, 500, 1.3),                                 # 1200 rows, V 32000: 256 x 256
+    (dataclasses.replace(S1, vocab=152064), 2, 600, 80, 1.1),  # 1040 rows, the 32B vocabulary
     (dataclasses.replace(S1, vocab=1040), 2, 1100, 500, 0.7),  # 128 x 128, last tile half empty
     (dataclasses.replace(S1, vocab=4000), 3, 150, 20, 1.0),    # 390 rows, V % 64 = 32
     (dataclasses.replace(T1, vocab=1000), 2, 90, 30, 0.8),     # fp32, V % 64 = 40
