@@ -596,8 +596,12 @@ BackwardWS take_backward(Bump& b, const grpo_config& c, int T) {
   const int Tp = round64(T);
   w.Tp = Tp;
   const size_t TT = (size_t)T * Tp, PP = (size_t)Tp * Tp;
-  const size_t per_head = TT * (8 + es) + PP * 2 * es + (size_t)hd * Tp * 2 * es +
-                          (size_t)T * hd * 8 + (size_t)T * 12;
+  // fp32 models keep S and dP (fp32) and the row statistics per head; bf16
+  // models form the scores inside the fused kernel
+  const bool fp32_scores = c.dtype == GRPO_F32;
+  const size_t per_head = TT * ((fp32_scores ? 8 : 0) + es) + PP * 2 * es +
+                          (size_t)hd * Tp * 2 * es + (size_t)T * hd * 8 +
+                          (fp32_scores ? (size_t)T * 12 : 0);
   int groups = (int)std::max<size_t>(1, kAttnBwdBytes / (per_head * gq));
   groups = std::min(groups, c.n_kv_heads);
   while (c.n_kv_heads % groups) --groups;
@@ -636,9 +640,9 @@ BackwardWS take_backward(Bump& b, const grpo_config& c, int T) {
   w.tA = b.take<char>((size_t)rowsA * Tp * es);
   w.tB = b.take<char>((size_t)rowsB * Tp * es);
   const int hb = w.hb;
-  w.S = b.take<float>(hb * TT);
-  w.dP = b.take<float>(hb * TT);
-  w.stats = b.take<float>((size_t)hb * T * 3);
+  w.S = b.take<float>(fp32_scores ? hb * TT : 0);
+  w.dP = b.take<float>(fp32_scores ? hb * TT : 0);
+  w.stats = b.take<float>(fp32_scores ? (size_t)hb * T * 3 : 0);
   w.dS = b.take<char>(hb * TT * es);
   w.PT = b.take<char>(hb * PP * es);
   w.dST = b.take<char>(hb * PP * es);
@@ -742,17 +746,25 @@ int attn_bwd(const grpo_model* m, BackwardWS& w, int T, hipStream_t st) {
   HIPCHK(transpose(e, e, w.kb, hd, (size_t)Tp * hd, T, hd, w.kT, Tp, hT, 0, 1, Tp, Hk, st));
   for (int h0 = 0; h0 < H; h0 += w.hb) {
     const int nb = std::min(w.hb, H - h0), g0 = h0 / gq;
-    // S = q_h k_g^T, dP = do_h v_g^T (raw products, fp32)
-    GemmBatch sb{nb, (size_t)hd, (size_t)Tp * hd, TT, gq, 1};   // causal: lower tiles only
-    if ((rc = gemm_bt(m, (char*)w.q + (size_t)h0 * hd * es, qd, T,
-                      one(kb + (size_t)g0 * Tp * hd * es), T, hd, EPI_STORE,
-                      EpiArgs{w.S, nullptr, Tp}, sb, st)))
-      return rc;
-    if ((rc = gemm_bt(m, (char*)w.doe + (size_t)h0 * hd * es, qd, T,
-                      one(vb + (size_t)g0 * Tp * hd * es), T, hd, EPI_STORE,
-                      EpiArgs{w.dP, nullptr, Tp}, sb, st)))
-      return rc;
-    HIPCHK(attn_softmax_bwd(c.dtype, w.S, w.dP, T, Tp, nb, scale, w.stats, w.dS, w.dST, w.PT, st));
+    if (c.dtype == GRPO_BF16) {
+      // P and dS' straight from q, do, k and v (the scores formed twice, never stored)
+      HIPCHK(attn_scores_bwd((char*)w.q + (size_t)h0 * hd * es, (char*)w.doe + (size_t)h0 * hd * es,
+                             qd, kb + (size_t)g0 * Tp * hd * es, vb + (size_t)g0 * Tp * hd * es, gq,
+                             T, Tp, nb, hd, scale, w.dS, w.dST, w.PT, st));
+    } else {
+      // S = q_h k_g^T, dP = do_h v_g^T (raw products, fp32)
+      GemmBatch sb{nb, (size_t)hd, (size_t)Tp * hd, TT, gq, 1};   // causal: lower tiles only
+      if ((rc = gemm_bt(m, (char*)w.q + (size_t)h0 * hd * es, qd, T,
+                        one(kb + (size_t)g0 * Tp * hd * es), T, hd, EPI_STORE,
+                        EpiArgs{w.S, nullptr, Tp}, sb, st)))
+        return rc;
+      if ((rc = gemm_bt(m, (char*)w.doe + (size_t)h0 * hd * es, qd, T,
+                        one(vb + (size_t)g0 * Tp * hd * es), T, hd, EPI_STORE,
+                        EpiArgs{w.dP, nullptr, Tp}, sb, st)))
+        return rc;
+      HIPCHK(attn_softmax_bwd(c.dtype, w.S, w.dP, T, Tp, nb, scale, w.stats, w.dS, w.dST, w.PT,
+                              st));
+    }
     // dq_h = dS'_h k_g (K = key positions)
     GemmBatch qb{nb, TT, hT, (size_t)hd, gq, 2};   // dS' is zero past each row
     if ((rc = gemm_bt(m, w.dS, Tp, T, one((char*)w.kT + (size_t)g0 * hT * es), hd, Tp, EPI_STORE,

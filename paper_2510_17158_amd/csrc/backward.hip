@@ -370,6 +370,210 @@ __global__ __launch_bounds__(256) void k_attn_tiles(const float* __restrict__ S,
   }
 }
 
+// Pass 1 and 2 of the attention backward for bf16 models with the scores never
+// stored.  One workgroup per (64-query block, head of the batch), wave w the
+// queries 16 w .. 16 w + 15 of the block.  For every key block at or below the
+// diagonal, S = q k^T and dP = do v^T come from the matrix cores (16x16x32 bf16
+// products, fp32 sums over the head dimension in k-step order; the block's K and
+// V rows staged in LDS, the next block's rows loaded into registers meanwhile).
+// The first pass keeps each lane's running maximum of S s and its rescaled sums
+// of e^(S s - max) and e^(S s - max) dP over its own columns; the 16 lanes of a
+// row then combine theirs in a fixed butterfly, so every lane holds the row's
+// max m, 1/l and D = sum P dP.  The second pass forms P = e^(S s - m) / l and
+// dS' = P (dP - D) s (the tile kernel's expressions) and writes them as that
+// kernel does: dS' by rows, P^T and dS'^T through LDS, in 16-byte pieces.  Above
+// the diagonal only the band tile the causal products read (row tiles of
+// kTiledRows) is written, as zeros.  Rows at or past T are zeros (their query
+// loads re-read row T - 1); key rows past T are read from the padded K and V
+// (within Tp) and masked.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_bwd_scores(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ dO, int ldq,
+    const bf16_t* __restrict__ kb, const bf16_t* __restrict__ vb, int gq, int T, int Tp, float s,
+    bf16_t* __restrict__ dS, bf16_t* __restrict__ dST, bf16_t* __restrict__ PT) {
+  constexpr int QS = HD / 32;            // MFMA k-steps over the head dimension
+  constexpr int KROW = HD + 8;           // LDS row of a K or V tile (16-byte pad)
+  constexpr int PR = HD / 8;             // 16-byte pieces per row
+  constexpr int PPT = 64 * PR / 256;     // pieces per thread and tile
+  static_assert(kTiledRows == 128, "band of two 64-row blocks");
+  __shared__ __attribute__((aligned(16))) bf16_t ks[64 * KROW];
+  __shared__ __attribute__((aligned(16))) bf16_t vs[64 * KROW];
+  __shared__ float tp[64][65], td[64][65];
+
+  const int nqb = Tp / 64;
+  const int qb = nqb - 1 - (int)blockIdx.x, b = blockIdx.y;
+  const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
+  const int j = lane & 15, lg = lane >> 4;
+  const int i0 = qb * 64;
+  const bf16_t* kg = kb + (size_t)(b / gq) * Tp * HD;
+  const bf16_t* vg = vb + (size_t)(b / gq) * Tp * HD;
+  bf16_t* dSb = dS + (size_t)b * T * Tp;
+  const size_t tb = (size_t)b * Tp * Tp;
+  const u32x4_t zero = {0u, 0u, 0u, 0u};
+
+  // the band tile above the diagonal (read by the causal products): zeros
+  if (qb % 2 == 0 && qb + 1 < nqb) {
+    const int j0 = i0 + 64;
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+      const int r = pass * 32 + tid / 8, u = tid % 8;
+      if (i0 + r < T) *(u32x4_t*)(dSb + (size_t)(i0 + r) * Tp + j0 + 8 * u) = zero;
+      *(u32x4_t*)(PT + tb + (size_t)(j0 + r) * Tp + i0 + 8 * u) = zero;
+      *(u32x4_t*)(dST + tb + (size_t)(j0 + r) * Tp + i0 + 8 * u) = zero;
+    }
+  }
+
+  // A operands: this lane's query row (clamped below T), k-step st taking the
+  // head-dimension elements 32 st + 8 lg .. 32 st + 8 lg + 7
+  const int qrow = min(i0 + 16 * wave + j, T - 1);
+  bf16x8_t qa[QS], da[QS];
+#pragma unroll
+  for (int st = 0; st < QS; ++st) {
+    qa[st] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(q + (size_t)qrow * ldq + b * HD + 32 * st + 8 * lg));
+    da[st] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(dO + (size_t)qrow * ldq + b * HD + 32 * st + 8 * lg));
+  }
+
+  // key block jb: piece p of a tile is row p / PR, elements (p % PR) 8 ..
+  u32x4_t pk[PPT], pv[PPT];
+  auto fetch = [&](int jb) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < PPT; ++u) {
+      const int p = tid + 256 * u, row = p / PR, col = (p % PR) * 8;
+      pk[u] = *(const u32x4_t*)(kg + (size_t)(jb * 64 + row) * HD + col);
+      pv[u] = *(const u32x4_t*)(vg + (size_t)(jb * 64 + row) * HD + col);
+    }
+  };
+  auto stash = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < PPT; ++u) {
+      const int p = tid + 256 * u, row = p / PR, col = (p % PR) * 8;
+      *(u32x4_t*)(ks + row * KROW + col) = pk[u];
+      *(u32x4_t*)(vs + row * KROW + col) = pv[u];
+    }
+  };
+  // S and dP of the staged block: column block c holds keys 16 c .. 16 c + 15;
+  // lane (j, lg) gets rows 4 lg .. 4 lg + 3 of its wave's queries, column j
+  f32x4_t as[4], ap[4];
+  auto products = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      f32x4_t x = {0.f, 0.f, 0.f, 0.f}, y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < QS; ++st) {
+        const bf16x8_t kf = *(const bf16x8_t*)(ks + (16 * c + j) * KROW + 32 * st + 8 * lg);
+        const bf16x8_t vf = *(const bf16x8_t*)(vs + (16 * c + j) * KROW + 32 * st + 8 * lg);
+        x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[st], kf, x, 0, 0, 0);
+        y = __builtin_amdgcn_mfma_f32_16x16x32_bf16(da[st], vf, y, 0, 0, 0);
+      }
+      as[c] = x;
+      ap[c] = y;
+    }
+  };
+
+  // pass 1: row statistics
+  float m[4], l[4], dd[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) { m[v] = -INFINITY; l[v] = 0.f; dd[v] = 0.f; }
+  fetch(0);
+  for (int jb = 0; jb <= qb; ++jb) {
+    __syncthreads();
+    stash();
+    __syncthreads();
+    if (jb < qb) fetch(jb + 1);
+    products();
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int i = i0 + 16 * wave + 4 * lg + v;
+      float x[4], mx = m[v];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        x[c] = jb * 64 + 16 * c + j <= i ? as[c][v] * s : -INFINITY;
+        mx = fmaxf(mx, x[c]);
+      }
+      if (mx != -INFINITY) {
+        const float cf = __expf(m[v] - mx);   // 0 while m is -inf
+        l[v] *= cf;
+        dd[v] *= cf;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const float e = __expf(x[c] - mx);   // 0 for masked keys
+          l[v] += e;
+          dd[v] = fmaf(e, x[c] != -INFINITY ? ap[c][v] : 0.f, dd[v]);
+        }
+        m[v] = mx;
+      }
+    }
+  }
+  float il[4], D[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const float m2 = __shfl_xor(m[v], off, 64), l2 = __shfl_xor(l[v], off, 64),
+                  d2 = __shfl_xor(dd[v], off, 64);
+      const float M = fmaxf(m[v], m2);
+      const float a = m[v] == -INFINITY ? 0.f : __expf(m[v] - M);
+      const float c2 = m2 == -INFINITY ? 0.f : __expf(m2 - M);
+      l[v] = l[v] * a + l2 * c2;
+      dd[v] = dd[v] * a + d2 * c2;
+      m[v] = M;
+    }
+    il[v] = 1.f / l[v];
+    D[v] = dd[v] / l[v];
+  }
+
+  // pass 2: P and dS' of every block, written as the tile kernel writes them
+  fetch(0);
+  for (int jb = 0; jb <= qb; ++jb) {
+    __syncthreads();
+    stash();
+    __syncthreads();
+    if (jb < qb) fetch(jb + 1);
+    products();
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int r = 16 * wave + 4 * lg + v, i = i0 + r;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const bool ok = jb * 64 + 16 * c + j <= i && i < T;
+        const float pv_ = __expf(as[c][v] * s - m[v]) * il[v];
+        const float dsv = pv_ * (ap[c][v] - D[v]) * s;
+        tp[r][16 * c + j] = ok ? pv_ : 0.f;
+        td[r][16 * c + j] = ok ? dsv : 0.f;
+      }
+    }
+    __syncthreads();
+    const int j0 = jb * 64;
+    {
+      const int r = tid / 4, qq = tid % 4, i = i0 + r;
+      if (i < T) {
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          u32x4_t w;
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            w[k] = (uint32_t)f2bf(td[r][32 * g + 8 * qq + 2 * k]) |
+                   ((uint32_t)f2bf(td[r][32 * g + 8 * qq + 2 * k + 1]) << 16);
+          *(u32x4_t*)(dSb + (size_t)i * Tp + j0 + 32 * g + 8 * qq) = w;
+        }
+      }
+    }
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+      const int c = pass * 32 + tid / 8, u = tid % 8;
+      u32x4_t wp, wd;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        wp[k] = (uint32_t)f2bf(tp[8 * u + 2 * k][c]) | ((uint32_t)f2bf(tp[8 * u + 2 * k + 1][c]) << 16);
+        wd[k] = (uint32_t)f2bf(td[8 * u + 2 * k][c]) | ((uint32_t)f2bf(td[8 * u + 2 * k + 1][c]) << 16);
+      }
+      const size_t o = tb + (size_t)(j0 + c) * Tp + i0 + 8 * u;
+      *(u32x4_t*)(PT + o) = wp;
+      *(u32x4_t*)(dST + o) = wd;
+    }
+  }
+}
+
 // Sum over each kv group's heads: out[t][g hd + e] = sum_j tmp[g gq + j][t][e].
 __global__ __launch_bounds__(256) void k_sum_heads(const float* __restrict__ tmp, int T, int hd,
                                                    int gq, int groups, float* __restrict__ out,
@@ -567,6 +771,27 @@ hipError_t attn_softmax_bwd(int dtype, const float* S, const float* dP, int T, i
   else
     k_attn_tiles<bf16_t><<<grid, 256, 0, st>>>(S, dP, stats, T, Tp, scale, (bf16_t*)dS,
                                                (bf16_t*)dST, (bf16_t*)PT, kTiledRows, vec);
+  return hipGetLastError();
+}
+
+hipError_t attn_scores_bwd(const void* q, const void* dO, int ldq, const void* kb, const void* vb,
+                          int gq, int T, int Tp, int batch, int hd, float scale, void* dS,
+                          void* dST, void* PT, hipStream_t st) {
+  if (T <= 0 || batch <= 0) return hipSuccess;
+  auto a16 = [](const void* p) { return (uintptr_t)p % 16 == 0; };
+  if (Tp % 64 || Tp < T || (hd != 64 && hd != 128) || gq < 1 || batch % gq || ldq % 8 ||
+      !a16(q) || !a16(dO) || !a16(kb) || !a16(vb) || !a16(dS) || !a16(dST) || !a16(PT))
+    return hipErrorInvalidValue;
+  Prof pf("attn_scores_bwd", st);
+  const dim3 grid(Tp / 64, batch);
+  if (hd == 128)
+    k_attn_bwd_scores<128><<<grid, 256, 0, st>>>((const bf16_t*)q, (const bf16_t*)dO, ldq,
+                                                 (const bf16_t*)kb, (const bf16_t*)vb, gq, T, Tp,
+                                                 scale, (bf16_t*)dS, (bf16_t*)dST, (bf16_t*)PT);
+  else
+    k_attn_bwd_scores<64><<<grid, 256, 0, st>>>((const bf16_t*)q, (const bf16_t*)dO, ldq,
+                                                (const bf16_t*)kb, (const bf16_t*)vb, gq, T, Tp,
+                                                scale, (bf16_t*)dS, (bf16_t*)dST, (bf16_t*)PT);
   return hipGetLastError();
 }
 

@@ -322,6 +322,14 @@ hipError_t rope_bwd(int dtype, float* dqkv, int T, int heads, int n_rot, int hd,
 hipError_t attn_softmax_bwd(int dtype, const float* S, const float* dP, int T, int Tp, int batch,
                             float scale, float* stats, void* dS, void* dST, void* PT,
                             hipStream_t st);
+// bf16 models: the same outputs as the score products and attn_softmax_bwd
+// together, from q, dO ([T][ldq], head b at column b hd) and the batch's K and V
+// ([batch / gq][Tp][hd], head b reading group b / gq), the scores formed on the
+// matrix cores twice and never stored; above the diagonal only the band tiles
+// the causal products read (kTiledRows) are written.
+hipError_t attn_scores_bwd(const void* q, const void* dO, int ldq, const void* kb, const void* vb,
+                          int gq, int T, int Tp, int batch, int hd, float scale, void* dS,
+                          void* dST, void* PT, hipStream_t st);
 hipError_t sum_heads(const float* tmp, int T, int hd, int gq, int groups, float* out, int ldo,
                      hipStream_t st);
 // demb[tok[t]] += dx[t] for t < T <= 16384 (V <= 2^18), without atomics: the
