@@ -27,6 +27,12 @@ namespace {
 
 constexpr int BT = 64;    // transpose tile
 
+// two finite fp32 values rounded to bf16 (round to nearest even, the hardware
+// conversion: the same bits as f2bf for finite inputs), a in the low half
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
+
 // out[c][r] = in[r][c] (r < R, c < C); out columns R .. Rpad-1 are zero.
 // Batch element b: in + b * in_bs, out + (b / div) * s1 + (b % div) * s2.
 // vec (16-byte aligned rows and batch offsets on both sides): a tile inside
@@ -552,8 +558,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd_scores(
           u32x4_t w;
 #pragma unroll
           for (int k = 0; k < 4; ++k)
-            w[k] = (uint32_t)f2bf(td[r][32 * g + 8 * qq + 2 * k]) |
-                   ((uint32_t)f2bf(td[r][32 * g + 8 * qq + 2 * k + 1]) << 16);
+            w[k] = pack_bf16x2(td[r][32 * g + 8 * qq + 2 * k], td[r][32 * g + 8 * qq + 2 * k + 1]);
           *(u32x4_t*)(dSb + (size_t)i * Tp + j0 + 32 * g + 8 * qq) = w;
         }
       }
@@ -564,8 +569,8 @@ __global__ __launch_bounds__(256) void k_attn_bwd_scores(
       u32x4_t wp, wd;
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        wp[k] = (uint32_t)f2bf(tp[8 * u + 2 * k][c]) | ((uint32_t)f2bf(tp[8 * u + 2 * k + 1][c]) << 16);
-        wd[k] = (uint32_t)f2bf(td[8 * u + 2 * k][c]) | ((uint32_t)f2bf(td[8 * u + 2 * k + 1][c]) << 16);
+        wp[k] = pack_bf16x2(tp[8 * u + 2 * k][c], tp[8 * u + 2 * k + 1][c]);
+        wd[k] = pack_bf16x2(td[8 * u + 2 * k][c], td[8 * u + 2 * k + 1][c]);
       }
       const size_t o = tb + (size_t)(j0 + c) * Tp + i0 + 8 * u;
       *(u32x4_t*)(PT + o) = wp;
