@@ -79,7 +79,7 @@ __global__ __launch_bounds__(256) void k_transpose(const TI* __restrict__ in, in
         if constexpr (sizeof(TO) == 4)
           w[k] = __float_as_uint(tile[r + k][c]);
         else
-          w[k] = (uint32_t)f2bf(tile[r + 2 * k][c]) | ((uint32_t)f2bf(tile[r + 2 * k + 1][c]) << 16);
+          w[k] = pack_bf16x2(tile[r + 2 * k][c], tile[r + 2 * k + 1][c]);
       }
       *(u32x4_t*)(out + (size_t)(c0 + c) * ldo + r0 + r) = w;
     }
@@ -487,13 +487,14 @@ __global__ __launch_bounds__(256) void k_attn_bwd_scores(
     __syncthreads();
     if (jb < qb) fetch(jb + 1);
     products();
+    const bool diag = jb == qb;   // below it every key precedes every query
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int i = i0 + 16 * wave + 4 * lg + v;
       float x[4], mx = m[v];
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        x[c] = jb * 64 + 16 * c + j <= i ? as[c][v] * s : -INFINITY;
+        x[c] = !diag || jb * 64 + 16 * c + j <= i ? as[c][v] * s : -INFINITY;
         mx = fmaxf(mx, x[c]);
       }
       if (mx != -INFINITY) {
@@ -536,12 +537,13 @@ __global__ __launch_bounds__(256) void k_attn_bwd_scores(
     __syncthreads();
     if (jb < qb) fetch(jb + 1);
     products();
+    const bool diag = jb == qb;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int r = 16 * wave + 4 * lg + v, i = i0 + r;
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        const bool ok = jb * 64 + 16 * c + j <= i && i < T;
+        const bool ok = (!diag || jb * 64 + 16 * c + j <= i) && i < T;
         const float pv_ = __expf(as[c][v] * s - m[v]) * il[v];
         const float dsv = pv_ * (ap[c][v] - D[v]) * s;
         tp[r][16 * c + j] = ok ? pv_ : 0.f;
