@@ -38,6 +38,8 @@ def _grads_oracle(cfg, host, tokens, sf, temp, dlogp):
     (dataclasses.replace(TINY, n_kv_heads=2), 1, 130, 7, 0.7),
     (dataclasses.replace(SMALL, n_layers=2), 1, 200, 100, 1.0),
     (dataclasses.replace(SMALL, n_layers=1), 2, 64, 1, 0.8),
+    # bf16 below one 64-position block: query rows past T clamped and zeroed
+    (dataclasses.replace(SMALL, n_layers=1), 1, 10, 3, 1.0),
     # the 7B width (head_dim 128, GQ 4, vocab 32000), one layer, 2048 positions
     (dataclasses.replace(M7B, n_layers=1), 1, 2048, 1024, 1.0),
     # the 32B width (GQ 5: head batches of whole 5-head groups, vocab 152064), one
