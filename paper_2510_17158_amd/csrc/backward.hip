@@ -314,89 +314,18 @@ __global__ __launch_bounds__(256) void k_attn_row_stats(const float* __restrict_
 // Pass 2, one 64 x 64 tile (query rows i0.., key columns j0..) per workgroup:
 // P = e^(S s - m) / l and dS' = P (dP - D) s on j <= i < T (zero elsewhere),
 // written as dS' [T][Tp] (rows i) and, through LDS, as P^T and dS'^T [Tp][Tp]
-// (rows j, columns i; zero for i >= T).
-template <typename TO>
+// (rows j, columns i; zero for i >= T).  fp32 models only: their products read
+// every tile, so every tile is written, the zeros above the diagonal included.
 __global__ __launch_bounds__(256) void k_attn_tiles(const float* __restrict__ S,
                                                     const float* __restrict__ dP,
                                                     const float* __restrict__ stats, int T, int Tp,
-                                                    float s, TO* __restrict__ dS,
-                                                    TO* __restrict__ dST, TO* __restrict__ PT,
-                                                    int band, int vec) {
+                                                    float s, float* __restrict__ dS,
+                                                    float* __restrict__ dST,
+                                                    float* __restrict__ PT) {
   __shared__ float tp[BT][BT + 1], td[BT][BT + 1];
   const int j0 = blockIdx.x * BT, i0 = blockIdx.y * BT, b = blockIdx.z;
-  // band > 0: the products that read these outputs take causal hints with row
-  // tiles of `band` rows (their k ranges end, or start, at their own row tile),
-  // so a tile above the diagonal is read only inside its row tile's band; the
-  // others are not written at all
-  if (band && j0 > i0 && j0 / band != i0 / band) return;
   const size_t base = (size_t)b * T * Tp;
   const bool live = j0 <= i0 + BT - 1 && i0 < T;     // some (i, j) with j <= i < T
-  if constexpr (sizeof(TO) == 2) {
-    if (vec && i0 + BT <= T) {
-      // 16-byte pieces: lane quarter q of row r takes columns 8 q .. 8 q + 7 and
-      // 32 + 8 q .. 32 + 8 q + 7 (the same arithmetic as the element-wise path)
-      const int r = threadIdx.x / 4, q = threadIdx.x % 4, i = i0 + r;
-      float p[2][8], ds[2][8];
-      if (live) {
-        const float* st = stats + ((size_t)b * T + i) * 3;
-        const size_t o = base + (size_t)i * Tp + j0 + 8 * q;
-        f32x4_t sv[2][2], dv[2][2];
-#pragma unroll
-        for (int g = 0; g < 2; ++g)
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            sv[g][h] = *(const f32x4_t*)(S + o + 32 * g + 4 * h);
-            dv[g][h] = *(const f32x4_t*)(dP + o + 32 * g + 4 * h);
-          }
-        const float m = st[0], rs = st[1], dd = st[2];
-#pragma unroll
-        for (int g = 0; g < 2; ++g)
-#pragma unroll
-          for (int k = 0; k < 8; ++k) {
-            const int j = j0 + 32 * g + 8 * q + k;
-            const float pv = __expf(sv[g][k / 4][k % 4] * s - m) * rs;
-            const float dsv = pv * (dv[g][k / 4][k % 4] - dd) * s;
-            p[g][k] = j <= i ? pv : 0.f;
-            ds[g][k] = j <= i ? dsv : 0.f;
-          }
-      } else {
-#pragma unroll
-        for (int g = 0; g < 2; ++g)
-#pragma unroll
-          for (int k = 0; k < 8; ++k) p[g][k] = ds[g][k] = 0.f;
-      }
-#pragma unroll
-      for (int g = 0; g < 2; ++g) {
-        u32x4_t w;
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-          w[k] = (uint32_t)f2bf(ds[g][2 * k]) | ((uint32_t)f2bf(ds[g][2 * k + 1]) << 16);
-        *(u32x4_t*)(dS + base + (size_t)i * Tp + j0 + 32 * g + 8 * q) = w;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          tp[r][32 * g + 8 * q + k] = p[g][k];
-          td[r][32 * g + 8 * q + k] = ds[g][k];
-        }
-      }
-      __syncthreads();
-      // transposed: output row j0 + c, columns i0 + 8 u .. i0 + 8 u + 7
-      const size_t tb = (size_t)b * Tp * Tp;
-#pragma unroll
-      for (int pass = 0; pass < 2; ++pass) {
-        const int c = pass * 32 + threadIdx.x / 8, u = threadIdx.x % 8;
-        u32x4_t wp, wd;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          wp[k] = (uint32_t)f2bf(tp[8 * u + 2 * k][c]) | ((uint32_t)f2bf(tp[8 * u + 2 * k + 1][c]) << 16);
-          wd[k] = (uint32_t)f2bf(td[8 * u + 2 * k][c]) | ((uint32_t)f2bf(td[8 * u + 2 * k + 1][c]) << 16);
-        }
-        const size_t o = tb + (size_t)(j0 + c) * Tp + i0 + 8 * u;
-        *(u32x4_t*)(PT + o) = wp;
-        *(u32x4_t*)(dST + o) = wd;
-      }
-      return;
-    }
-  }
   for (int e = threadIdx.x; e < BT * BT; e += 256) {
     const int r = e / BT, c = e % BT, i = i0 + r, j = j0 + c;
     float p = 0.f, ds = 0.f;
@@ -406,7 +335,7 @@ __global__ __launch_bounds__(256) void k_attn_tiles(const float* __restrict__ S,
       p = __expf(S[o] * s - st[0]) * st[1];
       ds = p * (dP[o] - st[2]) * s;
     }
-    if (i < T) stf(dS, base + (size_t)i * Tp + j, ds);
+    if (i < T) dS[base + (size_t)i * Tp + j] = ds;
     tp[r][c] = p;
     td[r][c] = ds;
   }
@@ -415,8 +344,8 @@ __global__ __launch_bounds__(256) void k_attn_tiles(const float* __restrict__ S,
   for (int e = threadIdx.x; e < BT * BT; e += 256) {
     const int c = e / BT, r = e % BT;
     const size_t o = tb + (size_t)(j0 + c) * Tp + i0 + r;
-    stf(PT, o, tp[r][c]);
-    stf(dST, o, td[r][c]);
+    PT[o] = tp[r][c];
+    dST[o] = td[r][c];
   }
 }
 
@@ -819,22 +748,13 @@ hipError_t attn_softmax_bwd(int dtype, const float* S, const float* dP, int T, i
                             float scale, float* stats, void* dS, void* dST, void* PT,
                             hipStream_t st) {
   if (T <= 0 || batch <= 0) return hipSuccess;
-  if (Tp % BT || Tp < T) return hipErrorInvalidValue;
+  // fp32 models only: bf16 models form the scores inside attn_scores_bwd
+  if (dtype != 0 || Tp % BT || Tp < T) return hipErrorInvalidValue;
   Prof pf("attn_softmax_bwd", st);
   k_attn_row_stats<<<dim3(T, batch), 256, 0, st>>>(S, dP, T, Tp, scale, stats);
   const dim3 grid(Tp / BT, Tp / BT, batch);
-  // fp32 models' products read every tile (zeros above the diagonal written);
-  // bf16 models' batched products run on the tiled GEMM, which honours the hints
-  static_assert(kTiledRows % BT == 0, "band of whole tiles");
-  // bf16 outputs in 16-byte pieces when every row start is 16-byte aligned
-  const int vec = (uintptr_t)S % 16 == 0 && (uintptr_t)dP % 16 == 0 && (uintptr_t)dS % 16 == 0 &&
-                  (uintptr_t)dST % 16 == 0 && (uintptr_t)PT % 16 == 0;
-  if (dtype == 0)
-    k_attn_tiles<float><<<grid, 256, 0, st>>>(S, dP, stats, T, Tp, scale, (float*)dS, (float*)dST,
-                                              (float*)PT, 0, 0);
-  else
-    k_attn_tiles<bf16_t><<<grid, 256, 0, st>>>(S, dP, stats, T, Tp, scale, (bf16_t*)dS,
-                                               (bf16_t*)dST, (bf16_t*)PT, kTiledRows, vec);
+  k_attn_tiles<<<grid, 256, 0, st>>>(S, dP, stats, T, Tp, scale, (float*)dS, (float*)dST,
+                                     (float*)PT);
   return hipGetLastError();
 }
 

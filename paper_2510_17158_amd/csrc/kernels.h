@@ -319,6 +319,7 @@ hipError_t swiglu_bwd(int dtype, const float* gu, const float* da, int T, int F,
                       hipStream_t st);
 hipError_t rope_bwd(int dtype, float* dqkv, int T, int heads, int n_rot, int hd, const float2* cs,
                     void* out, hipStream_t st);
+// fp32 models (dtype 0 only): softmax backward from the stored S and dP products
 hipError_t attn_softmax_bwd(int dtype, const float* S, const float* dP, int T, int Tp, int batch,
                             float scale, float* stats, void* dS, void* dST, void* PT,
                             hipStream_t st);
