@@ -39,12 +39,14 @@ ATTN_TRAFFIC = {
     "fixed_fetch_kib": 4536.8, "per_position_fetch_kib": 129.882, "fetch_scale": 2.0,
     "write_kib": 512.0, "write_scale": 1.0,
     "position_bytes": 64 * 4096,
+    "batch": 64,
 }
 
 
-def attn_traffic(algorithmic_bytes_per_launch: float):
+def attn_traffic(algorithmic_bytes_per_launch: float, batch: int = 64):
     """Counter-measured HBM bytes per launch of the decode attention at this launch's
-    algorithmic size, or None when the kernel has changed since the counters."""
+    algorithmic size, or None when the kernel has changed since the counters or the
+    batch is not the one they were taken at."""
     import hashlib
     try:
         with open(os.path.join(ROOT, ATTN_TRAFFIC["source"]), "rb") as f:
@@ -53,6 +55,8 @@ def attn_traffic(algorithmic_bytes_per_launch: float):
     except OSError:
         return None
     t = ATTN_TRAFFIC
+    if batch != t["batch"]:
+        return None
     positions = algorithmic_bytes_per_launch / t["position_bytes"]
     fetch = (t["fixed_fetch_kib"] + t["per_position_fetch_kib"] * positions) * t["fetch_scale"]
     return (fetch + t["write_kib"] * t["write_scale"]) * 1024
@@ -503,7 +507,8 @@ def main():
     out["roofline"] = {"bound": "hbm", "achieved": kb[dom] / (t / 1e3) / 1e9,
                        "peak": HBM_PEAK_GBS, "unit": "GB/s",
                        "frac": kb[dom] / (t / 1e3) / 1e9 / HBM_PEAK_GBS,
-                       "traffic": attn_traffic(kb[dom] / n) if dom == "attn_decode" else None,
+                       "traffic": (attn_traffic(kb[dom] / n, w.batch) if dom == "attn_decode"
+                                   else None),
                        "traffic_unit": "bytes per launch",
                        "kernel": dom, "launches": n, "avg_us": 1e3 * t / n,
                        "algorithmic_bytes_per_launch": kb[dom] / n}

@@ -122,6 +122,9 @@ WORKLOADS = {
                    temperature=1.0, prompt_kind="code", tool_spans=3),
     "32b": Workload("32b", 4, M32B, n_prompts=4, group=8, prompt_len=8192, new_tokens=4096,
                     temperature=1.0, prompt_kind="code", tool_spans=12, score=False),
+    # the group size the paper settles on (K = 12, Sec. VI-A) at the 7B shape
+    "7b-k12": Workload("7b-k12", 5, M7B, n_prompts=8, group=12, prompt_len=2048,
+                       new_tokens=2048, temperature=1.0, prompt_kind="code", tool_spans=3),
 }
 
 

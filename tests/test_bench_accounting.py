@@ -83,7 +83,7 @@ def test_update_flops_per_sequence():
 
 def test_attention_traffic_fit():
     """The counter fit (fixed + per generated position) at the mean of 1024
-    generated positions; null when the kernel source changed."""
+    generated positions; null when the kernel source changed or at another batch."""
     b = _bench()
     t = b.ATTN_TRAFFIC
     alg = B * 1024 * 2 * Hk * hd * 2
@@ -93,6 +93,7 @@ def test_attention_traffic_fit():
     if got is not None:
         assert got == pytest.approx(exp)
         assert 1.0 < got / alg < 1.1
+    assert b.attn_traffic(alg * 1.5, 96) is None    # measured at batch 64 only
     saved = dict(t)
     try:
         t["sha256"] = "0" * 64

@@ -174,6 +174,7 @@ def test_full_width_stage_local(name, layers, kw, group):
     ("small", 2, 4, 300, 100, 2),      # only part of the prompt shared
     ("small", 1, 3, 33, 33, 2),        # G not a multiple of the samples per wave
     ("7b", 2, 16, 70, 70, 2),          # GQ 4, G 16: two prefix workgroups per group
+    ("7b", 1, 12, 70, 70, 2),          # G 12 (the paper's K): the second one half full
     ("7b", 4, 8, 520, 520, 2),         # several prompt chunks, ragged last tile
 ])
 def test_grouped_decode_stage_local(name, P, G, Tp, prefix, steps):
