@@ -35,18 +35,23 @@ BF16_PEAK_TFLOPS = 2500.0
 # 64 sequences).
 ATTN_TRAFFIC = {
     "source": "paper_2510_17158_amd/csrc/attn_decode.hip",
-    "sha256": "1ec040d050f79730846e1096a8da8d617d7cfff157bd5963b4c2d78c117bf392",
-    "fixed_fetch_kib": 4536.8, "per_position_fetch_kib": 129.882, "fetch_scale": 2.0,
+    "sha256": "aab7af4188768b85c6d945c3056c0a4b8a16181556b873fe9490bdd91c71ffa3",
+    # rocprofv3 FETCH_SIZE / WRITE_SIZE per dispatch of the per-row decode attention at
+    # batch 64 (7B shape, 2048 shared prompt positions), mean of the 32 layers' launches at
+    # exactly 1024 generated positions: the mean launch of the 7B rollout (positions
+    # 1 .. 2047), read directly; readings at 512 and 1536 put it on their line (0.02%),
+    # so the mean launch's traffic is this one's
+    "batch": 64, "generated_positions": 1024,
+    "fetch_kib": 136342.8, "fetch_scale": 2.0,
     "write_kib": 512.0, "write_scale": 1.0,
     "position_bytes": 64 * 4096,
-    "batch": 64,
 }
 
 
 def attn_traffic(algorithmic_bytes_per_launch: float, batch: int = 64):
-    """Counter-measured HBM bytes per launch of the decode attention at this launch's
-    algorithmic size, or None when the kernel has changed since the counters or the
-    batch is not the one they were taken at."""
+    """Counter-measured HBM bytes per launch of the decode attention, or None when
+    the kernel has changed since the counters, the batch differs, or the launches'
+    mean generated positions are not the measured ones."""
     import hashlib
     try:
         with open(os.path.join(ROOT, ATTN_TRAFFIC["source"]), "rb") as f:
@@ -55,11 +60,10 @@ def attn_traffic(algorithmic_bytes_per_launch: float, batch: int = 64):
     except OSError:
         return None
     t = ATTN_TRAFFIC
-    if batch != t["batch"]:
-        return None
     positions = algorithmic_bytes_per_launch / t["position_bytes"]
-    fetch = (t["fixed_fetch_kib"] + t["per_position_fetch_kib"] * positions) * t["fetch_scale"]
-    return (fetch + t["write_kib"] * t["write_scale"]) * 1024
+    if batch != t["batch"] or abs(positions - t["generated_positions"]) > 0.5:
+        return None
+    return (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024
 
 
 def log(*a):
@@ -345,6 +349,44 @@ def cpu_baseline(w, host, budget_s: float = 20.0) -> dict:
                       f"sequence ({t_fwd + t_head1 + t_headn:.1f} s); fp64 NumPy"}
 
 
+def decode_at(w, ctx: int, steps: int) -> dict:
+    """Counter runs at one decode context: prefill prompts of `ctx` positions,
+    then `steps` grouped decode steps that share only the workload's prompt
+    length, so every per-row attention launch reads ctx - prompt_len generated
+    positions per sequence besides the shared prompt (ctx = prompt_len +
+    new_tokens / 2 is the mean context of the workload's rollout).  The group's
+    rows hold identical prompts, so the shared positions are the same in every
+    member, as grouped decode requires."""
+    import torch
+    from paper_2510_17158_amd import api, synth
+    from paper_2510_17158_amd.runner import GrpoIteration
+    shared = w.prompt_len
+    if not (shared < ctx and steps >= 1 and ctx + steps <= w.max_len):
+        raise SystemExit(f"--decode-at needs {shared} < ctx and ctx + steps <= {w.max_len}")
+    wc = w.with_(prompt_len=ctx, new_tokens=w.total_len - ctx, score=False)
+    c = wc.model
+    host = synth.make_weights(c, wc.master_seed)
+    pol = api.Model(c, api.upload_weights(c, host))
+    del host
+    it = GrpoIteration(wc, pol, None, synth.make_prompts(wc), synth.make_rewards(wc),
+                       synth.make_seed(wc))
+    it.prefill()
+    tok_o = torch.empty(it.B, steps, dtype=torch.int32, device="cuda")
+    lp_o = torch.empty(it.B, steps, dtype=torch.float32, device="cuda")
+    it.tok.copy_(it.tok0)
+    it.pos.fill_(ctx)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    api.rollout_step(pol, it.kv, it.B, it.max_len, it.pos, it.tok, ctx, 1, steps, it.sampling,
+                     tok_o, lp_o, ws=it.ws_roll, group=wc.group, prefix_len=shared)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    assert bool(torch.isfinite(lp_o).all())
+    return {"mode": "decode_at", "workload": w.name, "context": ctx, "shared_prompt": shared,
+            "generated_positions": ctx - shared, "steps": steps, "decode_step_ms": ms,
+            "max_len": it.max_len}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -360,6 +402,10 @@ def main():
     ap.add_argument("--no-kernel-timing", action="store_true",
                     help="skip the replica of the step with per-launch HIP events (no roofline "
                          "line); for hardware-counter runs")
+    ap.add_argument("--decode-at", type=int, default=None, metavar="CTX",
+                    help="only prefill prompts of CTX positions and run --steps grouped decode "
+                         "steps sharing the workload's prompt length (counter runs at one "
+                         "decode context)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy a 1 GiB device buffer 4 times (HBM counter calibration)")
     args = ap.parse_args()
@@ -371,6 +417,12 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": 1 << 30, "copies": 4}), flush=True)
+        return
+    if args.decode_at:
+        from paper_2510_17158_amd.workloads import get
+        import torch
+        torch.cuda.set_device(0)
+        print(json.dumps(decode_at(get(args.workload), args.decode_at, args.steps)), flush=True)
         return
     if os.environ.get("ROCPROF_COUNTER_COLLECTION") and not args.no_kernel_timing:
         # hardware-counter collection rewrites every dispatch; the library then

@@ -221,15 +221,18 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     __builtin_amdgcn_wave_barrier();
   };
 
-  // two tiles in registers: the next one loads while the current one is used;
-  // past the wave's last tile the loads repeat that tile (in bounds, results unused)
+  // two tiles in registers: the next one loads while the current one is used.
+  // Past the wave's last tile the loads still go out (no branch, so the waits
+  // stay those of the steady state) but take tile index nmine, which starts at
+  // or past t1: every lane's position clamps to t1 - 1, so such a load reads one
+  // row of K and V instead of a whole tile (in bounds, results unused).
   if (nmine > 0) {
     Tile ta, tb;
     load(ta, 0);
     for (int i = 0; i < nmine; i += 2) {
-      load(tb, min(i + 1, nmine - 1));
+      load(tb, min(i + 1, nmine));
       compute(ta, i);
-      load(ta, min(i + 2, nmine - 1));
+      load(ta, min(i + 2, nmine));
       if (i + 1 < nmine) compute(tb, i + 1);
     }
   }

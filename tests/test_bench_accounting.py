@@ -81,19 +81,20 @@ def test_update_flops_per_sequence():
     assert 3 * fwd / 1e12 == pytest.approx(186.33, rel=1e-3)
 
 
-def test_attention_traffic_fit():
-    """The counter fit (fixed + per generated position) at the mean of 1024
-    generated positions; null when the kernel source changed or at another batch."""
+def test_attention_traffic_reading():
+    """The counter reading at 1024 generated positions, the mean launch of the 7B
+    rollout; null when the kernel source changed, at another batch or at another
+    mean context."""
     b = _bench()
     t = b.ATTN_TRAFFIC
     alg = B * 1024 * 2 * Hk * hd * 2
-    exp = ((t["fixed_fetch_kib"] + t["per_position_fetch_kib"] * 1024) * t["fetch_scale"]
-           + t["write_kib"] * t["write_scale"]) * 1024
+    exp = (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024
     got = b.attn_traffic(alg)
     if got is not None:
         assert got == pytest.approx(exp)
         assert 1.0 < got / alg < 1.1
     assert b.attn_traffic(alg * 1.5, 96) is None    # measured at batch 64 only
+    assert b.attn_traffic(alg / 2) is None          # and at the 7B rollout's mean context
     saved = dict(t)
     try:
         t["sha256"] = "0" * 64

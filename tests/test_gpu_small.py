@@ -462,3 +462,20 @@ def test_bench_launch_configuration():
     say("rollout vs scoring log-prob difference (reported)", float(np.abs(new - old).max()),
         "mean logp", float(old.mean()))
     model.close()
+
+
+def test_bench_decode_at_context():
+    """bench.py's fixed-context decode mode (hardware-counter runs): prompts
+    prefilled to the context, then grouped steps that share only the workload's
+    prompt length, with finite log-probs."""
+    require_gpu()
+    import importlib.util
+    import os
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    spec = importlib.util.spec_from_file_location("bench_mod", os.path.join(root, "bench.py"))
+    b = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(b)
+    out = b.decode_at(get("small"), 768, 2)
+    say("decode at context", out)
+    assert out["generated_positions"] == 256 and out["steps"] == 2
+    assert out["decode_step_ms"] > 0 and out["max_len"] == 1023
