@@ -367,7 +367,7 @@ hipError_t gemm_decode_bf16(const uint16_t* Xf, int B, const uint16_t* Wf, int N
                             EpiArgs ep, const DecodePlan& p, hipStream_t st) {
   if (B < 1 || B > p.nb || p.nb != decode_nb(B) || N % 16 || K % KGRAN || p.splits < 1 ||
       p.tiles * 16 * p.rb < N ||
-      (K / p.splits) % KGRAN || (epi == EPI_SWIGLU && (N % 32 || ep.ld_out != N / 2)) ||
+      K % p.splits || (K / p.splits) % KGRAN || (epi == EPI_SWIGLU && (N % 32 || ep.ld_out != N / 2)) ||
       (epi == EPI_SAMPLE && (p.splits != 1 || !ep.smp.part || (ep.out_f32 && ep.ld_out < N))))
     return hipErrorInvalidValue;
   DArgs a;
