@@ -321,13 +321,14 @@ int decode_nb(int B) { return B <= 16 ? 16 : B <= 32 ? 32 : B <= 64 ? 64 : 128; 
 // Split-K factor of a plan: the first divisor of K / KGRAN reaching the target
 // grid (SwiGLU needs complete gate and up sums in one workgroup: never split).
 static int decode_splits(int tiles, int K, int epi, int target_wgs, int max_splits) {
+  // the most splits (dividing the K chunks) that keep the grid within the target
+  // (one workgroup per compute unit): a grid past it leaves some units with two
+  // workgroups and others with one (1B QKV: 4 splits, 384 workgroups, 12.9 us;
+  // 2 splits, 192 workgroups, 10.8 us)
   const int nchunk = K / KGRAN;
   int splits = 1;
-  for (int d = 1; epi != EPI_SWIGLU && d <= nchunk && d <= max_splits; ++d) {
-    if (nchunk % d) continue;
-    splits = d;
-    if ((long)tiles * d >= target_wgs) break;
-  }
+  for (int d = 2; epi != EPI_SWIGLU && d <= nchunk && d <= max_splits; ++d)
+    if (nchunk % d == 0 && (long)tiles * d <= target_wgs) splits = d;
   return splits;
 }
 
