@@ -450,7 +450,9 @@ int grpo_token_loss_noalloc(const float* logp, const float* logp_old, const floa
  *   out[4]    context positions per decode-attention span; out[5] spans
  *   out[6]    positions per prompt chunk of a grouped step; out[7] chunks
  *             (both 0 without grouping or for fp32 models)
- * fp32 models: out[0..7] = 0 (they use one fma chain per output).
+ *   out[8]    waves per workgroup of the per-row decode attention (4 or 2:
+ *             a span's 32-position tiles are dealt round-robin to them)
+ * out holds 9 entries.  fp32 models: out[0..8] = 0 (one fma chain per output).
  * GRPO_INVALID_ARG for a NULL pointer or sizes outside the call's ranges. */
 int grpo_decode_structure(const grpo_model* m, int32_t B, int32_t max_len, int32_t G,
                           int32_t prefix_len, int32_t* out);

@@ -368,11 +368,11 @@ def token_loss(logp, logp_old, logp_ref, mask, adv, clip_eps: float, beta: float
 
 def decode_structure(model: Model, B: int, max_len: int, G: int = 0, prefix_len: int = 0) -> dict:
     """grpo_decode_structure as a dict."""
-    out = (C.c_int32 * 8)()
+    out = (C.c_int32 * 9)()
     _check(lib().grpo_decode_structure(model.handle, B, max_len, G, prefix_len, out))
     v = list(out)
     return dict(splits_qkv=v[0], splits_o=v[1], splits_down=v[2], splits_head=v[3], span=v[4],
-                spans=v[5], chunk=v[6], chunks=v[7])
+                spans=v[5], chunk=v[6], chunks=v[7], waves=v[8])
 
 
 def token_loss_noalloc(logp, logp_old, logp_ref, mask, adv, clip_eps: float, beta: float,

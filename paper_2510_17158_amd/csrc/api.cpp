@@ -886,7 +886,7 @@ int grpo_decode_structure(const grpo_model* m, int32_t B, int32_t max_len, int32
   if (B < 1 || B > 128 || max_len < 1 || G < 0 || (G > 0 && B % G) || prefix_len < 0 ||
       prefix_len > max_len)
     return fail(GRPO_INVALID_ARG, "sizes outside the decode step's ranges");
-  for (int i = 0; i < 8; ++i) out[i] = 0;
+  for (int i = 0; i < 9; ++i) out[i] = 0;
   const grpo_config& c = m->cfg;
   if (c.dtype == GRPO_F32) {
     g_err.clear();
@@ -904,6 +904,7 @@ int grpo_decode_structure(const grpo_model* m, int32_t B, int32_t max_len, int32
   out[5] = ap.splits;
   out[6] = grouped ? ap.span_p : 0;
   out[7] = grouped ? ap.chunks : 0;
+  out[8] = ap.waves;
   g_err.clear();
   return GRPO_OK;
 }

@@ -2,7 +2,8 @@
 //
 // bf16: one workgroup per (context span, kv head, sequence); the span is the
 // whole context unless there are too few (sequence, kv head) pairs to fill the
-// chip.  Each of the 4 waves streams tiles of 32 positions (tiles w, w+4, ...)
+// chip.  Each of the 4 waves (2 for grids of twice the workgroups that fit on
+// the chip at once) streams tiles of 32 positions (tiles w, w+4, ...)
 // with the next tile's K and V loads in flight while the current tile is
 // computed, and keeps an online softmax (running max, sum and unnormalised
 // output per query head).  QK^T runs on MFMA with the K tile as the A operand
@@ -71,12 +72,14 @@ struct KVTile {
 };
 
 // ---------------------------------------------------------------- decode, bf16
+// NW waves per workgroup (4; 2 when the grid holds at least twice the
+// workgroups of 4 waves that fit on the chip at once).
 // blockIdx = (span, kv head, batch row); the spans start at the group's shared
 // length when ga.G > 0 and write partial row split_base + span of S.  A grouped
 // step whose generated positions are one span (S = chunks + 1) merges the prompt
 // chunks' partials here and writes the output (no merge kernel).
-template <int HD, int MAXG>
-__global__ __launch_bounds__(256) void k_attn_decode_bf16(
+template <int HD, int MAXG, int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn_decode_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const int32_t* __restrict__ pos, const int32_t* __restrict__ slots, int H, int n_kv,
     int max_len, int S, int span, float scale, float* __restrict__ part_o,
@@ -87,11 +90,13 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   constexpr int PPW = 64 / LPT;       // positions per V load instruction
   constexpr int NVT = DT / PPW;       // V load instructions per tile
   constexpr int NG = DT / 16;         // MFMA position groups per tile
+  constexpr int NT = 64 * NW;         // threads
   using Tile = KVTile<HD, NG, NVT>;
-  __shared__ __attribute__((aligned(16))) float pw[4][DT][MAXG];
-  __shared__ __attribute__((aligned(16))) float pa[4][MAXG];
-  __shared__ float red[4][MAXG * HD];
-  __shared__ float wm[4][MAXG], wl[4][MAXG];
+  static_assert(MAX_CHUNKS * MAXG <= NT, "one thread per prompt chunk and head");
+  __shared__ __attribute__((aligned(16))) float pw[NW][DT][MAXG];
+  __shared__ __attribute__((aligned(16))) float pa[NW][MAXG];
+  __shared__ float red[NW][MAXG * HD];
+  __shared__ float wm[NW][MAXG], wl[NW][MAXG];
 
   const int split = blockIdx.x, g = blockIdx.y;
   const int GQ = H / n_kv;
@@ -108,7 +113,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   if (t0 >= ctx && !fold) return;             // (folding still merges the prompt part)
   const int t1 = min(t0 + span, ctx);
   const int ntiles = t1 > t0 ? (t1 - t0 + DT - 1) / DT : 0;
-  const int nmine = ntiles > wave ? (ntiles - wave + 3) / 4 : 0;
+  const int nmine = ntiles > wave ? (ntiles - wave + NW - 1) / NW : 0;
   const int slot = slots ? slots[src] : src;          // the row's cache slot
   const size_t head_base = ((size_t)slot * n_kv + g) * max_len;
   const bf16_t* kb = kc + head_base * HD;
@@ -128,7 +133,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   }
 
   auto load = [&](Tile& tl, int i) {
-    const int tb = t0 + (wave + 4 * i) * DT;
+    const int tb = t0 + (wave + NW * i) * DT;
 #pragma unroll
     for (int grp = 0; grp < NG; ++grp) {
       const int t = min(tb + grp * 16 + j, t1 - 1);
@@ -152,7 +157,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
 
   auto compute = [&](const Tile& tl, int i) {
-    const int tb = t0 + (wave + 4 * i) * DT;
+    const int tb = t0 + (wave + NW * i) * DT;
     float sv[NG][4];
     float tmax = -INFINITY;
 #pragma unroll
@@ -244,7 +249,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   // loads the (max, sum) pair of chunk i / MAXG, head i % MAXG (shared by every
   // head-dim element: kept in LDS); every thread loads the output elements of
   // its NIT (head, element) pairs.
-  constexpr int NIT = (MAXG * HD + 255) / 256;
+  constexpr int NIT = (MAXG * HD + NT - 1) / NT;
   __shared__ __attribute__((aligned(8))) float2 fml[MAX_CHUNKS][MAXG];
   float co[NIT][MAX_CHUNKS];
   float2 cml = make_float2(-INFINITY, 0.f);
@@ -259,7 +264,7 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
     }
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
-      const int i = min(tid + 256 * it, GQ * HD - 1);
+      const int i = min(tid + NT * it, GQ * HD - 1);
       const float* pr = part_o + (rh + (size_t)(i / HD) * S) * HD + i % HD;
 #pragma unroll
       for (int c = 0; c < MAX_CHUNKS; ++c) co[it][c] = pr[(size_t)(c < nused ? c : 0) * HD];
@@ -291,16 +296,18 @@ __global__ __launch_bounds__(256) void k_attn_decode_bf16(
   }
   if (fold && tid < MAX_CHUNKS * MAXG) fml[tid / MAXG][tid % MAXG] = cml;
   __syncthreads();
-  // merge the 4 waves (fixed order)
+  // merge the NW waves (fixed order)
 #pragma unroll
   for (int it = 0; it < NIT; ++it) {
-    const int i = tid + 256 * it;
+    const int i = tid + NT * it;
     if (i >= GQ * HD) break;
     const int h = i / HD, e = i % HD;
-    const float M = fmaxf(fmaxf(wm[0][h], wm[1][h]), fmaxf(wm[2][h], wm[3][h]));
+    float M = wm[0][h];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) M = fmaxf(M, wm[w][h]);
     float x = 0.f, L = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < NW; ++w) {
       const float c = __expf(wm[w][h] - M);
       x = fmaf(c, red[w][i], x);
       L = fmaf(c, wl[w][h], L);
@@ -606,6 +613,13 @@ DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len, int
   DecodeAttnPlan p{};
   p.tc = ((max_len + want - 1) / want + SPAN_Q - 1) / SPAN_Q * SPAN_Q;
   p.splits = (max_len + p.tc - 1) / p.tc;
+  // two workgroups of 4 waves fit on a compute unit (registers); a grid of at
+  // least twice that would run in two or more rounds, each paying the
+  // workgroups' fixed start and merge, so it takes workgroups of 2 waves (four
+  // per unit, the same 8 waves: 1B, 1024 workgroups, 35.0 -> 33.2 us per
+  // launch).  Between one and two chips' worth (batch 96 at the 7B shape, 768
+  // workgroups) 2 waves would leave 6 waves per unit: 76.1 -> 80.6 us.
+  p.waves = (long)p.splits * n_kv * B >= 2 * kTargetWGs ? 2 : 4;
   p.part_floats = p.splits > 1 ? (size_t)B * H * p.splits * (hd + 2) : 0;
   if (G <= 0 || prefix_len <= 0) return p;
   // grouped: the generated positions keep the spans above (they start at the
@@ -630,14 +644,19 @@ size_t decode_attn_part_floats_max(int B, int H, int n_kv, int hd, int max_len) 
 }
 
 template <int HD, int MAXG>
-static void launch_decode(dim3 grid, hipStream_t st, const void* q, const void* kc,
+static void launch_decode(dim3 grid, int waves, hipStream_t st, const void* q, const void* kc,
                           const void* vc, const int32_t* pos, const int32_t* slots, int H,
                           int n_kv, int max_len, int S, int span, float scale, float* part_o,
                           float* part_ml, void* out, int pack_nb, DecodeGroup ga,
                           int split_base) {
-  k_attn_decode_bf16<HD, MAXG><<<grid, 256, 0, st>>>(
-      (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, slots, H, n_kv, max_len, S,
-      span, scale, part_o, part_ml, (bf16_t*)out, pack_nb, ga, split_base);
+  if (waves == 2)
+    k_attn_decode_bf16<HD, MAXG, 2><<<grid, 128, 0, st>>>(
+        (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, slots, H, n_kv, max_len, S,
+        span, scale, part_o, part_ml, (bf16_t*)out, pack_nb, ga, split_base);
+  else
+    k_attn_decode_bf16<HD, MAXG, 4><<<grid, 256, 0, st>>>(
+        (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, slots, H, n_kv, max_len, S,
+        span, scale, part_o, part_ml, (bf16_t*)out, pack_nb, ga, split_base);
 }
 
 template <int HD>
@@ -663,11 +682,11 @@ static hipError_t attn_decode_hd(const void* q, const void* kc, const void* vc,
     Prof pf("attn_decode", st);
     dim3 grid(p.splits, n_kv, B);
     if (gq <= 4)
-      launch_decode<HD, 4>(grid, st, q, kc, vc, pos, slots, H, n_kv, max_len, S, p.tc, scale,
-                           part_o, part_ml, out, pack_nb, ga, p.chunks);
+      launch_decode<HD, 4>(grid, p.waves, st, q, kc, vc, pos, slots, H, n_kv, max_len, S, p.tc,
+                           scale, part_o, part_ml, out, pack_nb, ga, p.chunks);
     else
-      launch_decode<HD, 8>(grid, st, q, kc, vc, pos, slots, H, n_kv, max_len, S, p.tc, scale,
-                           part_o, part_ml, out, pack_nb, ga, p.chunks);
+      launch_decode<HD, 8>(grid, p.waves, st, q, kc, vc, pos, slots, H, n_kv, max_len, S, p.tc,
+                           scale, part_o, part_ml, out, pack_nb, ga, p.chunks);
   }
   // grouped with one span of generated positions: merged by the per-row kernel
   if (S > 1 && !(grouped && p.splits == 1)) {
@@ -688,7 +707,8 @@ hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
   if (dtype == 0)
     return attn_rows_f32((const float*)q, (const float*)kc, (const float*)vc, pos, slots, B, 1, 1,
                          H, n_kv, hd, max_len, (float*)out, st);
-  if (H % n_kv || H / n_kv > 8 || (hd != 64 && hd != 128)) return hipErrorInvalidValue;
+  if (H % n_kv || H / n_kv > 8 || (hd != 64 && hd != 128) || (p.waves != 2 && p.waves != 4))
+    return hipErrorInvalidValue;
   if (p.G > 0 && (B % p.G || p.chunks < 1 || p.chunks > MAX_CHUNKS || p.n_sub < 1 ||
                   (long)p.n_sub * (32 / (H / n_kv)) < p.G || p.prefix_len > max_len ||
                   (long)p.chunks * p.span_p < p.prefix_len))

@@ -222,6 +222,7 @@ hipError_t rope_kv(int dtype, const float* qkv, int M, void* q_out, const RopeAr
 // buffer the plan needs.
 struct DecodeAttnPlan {
   int tc, splits;
+  int waves;     // waves per workgroup of the per-row kernel (4, or 2 for large grids)
   int G, prefix_len, chunks, span_p, n_sub;
   size_t part_floats;
 };

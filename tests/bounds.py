@@ -247,7 +247,8 @@ def attention_bound(q, Kc, Vc, hd, segments, merges=0):
                 keys; the grouped step's prompt chunks), 32-key steps of two
                 instructions each, at most one rescale per step;
       "decode": the per-row decode kernel: spans of `chunk` positions from
-                `start`, each cut into 32-position tiles dealt to 4 waves; a
+                `start`, each cut into 32-position tiles dealt to the
+                workgroup's waves (a fifth tuple element, 4 when absent); a
                 lane fuses P.V of positions iv * PPW + ts of its tiles in one
                 fma chain (a rescale per tile), lanes then meet in a butterfly;
       "f32":    one fma chain over the positions (fp32 models).
@@ -283,7 +284,7 @@ def attention_bound(q, Kc, Vc, hd, segments, merges=0):
     E = (p * rho) @ np.abs(Vc - o[None, :]) / L
     pv = p[:, None] * Vc
     apv = np.abs(pv)
-    for kind, a0, a1, chunk in segments:
+    for kind, a0, a1, chunk, *rest in segments:
         if a1 <= a0:
             continue
         if kind == "mfma":
@@ -306,8 +307,9 @@ def attention_bound(q, Kc, Vc, hd, segments, merges=0):
                 tiles = (seg.shape[0] + 31) // 32
                 pp = np.pad(seg, ((0, tiles * 32 - seg.shape[0]), (0, 0)))
                 pp = pp.reshape(tiles, nvt, PPW, hd)
-                for w in range(4):
-                    t = pp[w::4]
+                waves = rest[0] if rest else 4
+                for w in range(waves):
+                    t = pp[w::waves]
                     if t.shape[0] == 0:
                         continue
                     chain = t.transpose(2, 0, 1, 3).reshape(PPW, -1, hd)

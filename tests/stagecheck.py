@@ -133,8 +133,8 @@ def decode_segments(ctx: int, st: dict, base: int = 0):
     segs = []
     if base > 0:
         segs.append(("mfma", 0, base, st["chunk"]))
-    segs.append(("decode", base, ctx, st["span"]))
-    merges = 4 + st["spans"] + (st["chunks"] + 1 if base > 0 else 0)
+    segs.append(("decode", base, ctx, st["span"], st["waves"]))
+    merges = st["waves"] + st["spans"] + (st["chunks"] + 1 if base > 0 else 0)
     return segs, merges
 
 

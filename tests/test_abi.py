@@ -242,12 +242,15 @@ def test_decode_structure_query():
     own planner; its arguments are checked."""
     L = api.lib()
     rc, h, keep = _fake_model(get("7b").model)
-    out = (C.c_int32 * 8)()
+    out = (C.c_int32 * 9)()
     assert L.grpo_decode_structure(h, 64, 4095, 8, 2048, out) == api.OK
     v = list(out)
     assert all(x >= 1 for x in v[:6]) and v[3] == 1       # the LM head is never split
     assert v[6] > 0 and v[7] >= 1 and v[6] * v[7] >= 2048
-    assert L.grpo_decode_structure(h, 64, 4095, 0, 0, out) == api.OK and list(out)[6:] == [0, 0]
+    assert v[8] == 4                       # 512 per-row workgroups fit on the chip at once
+    assert L.grpo_decode_structure(h, 96, 4095, 12, 2048, out) == api.OK and out[8] == 4
+    assert L.grpo_decode_structure(h, 128, 4095, 8, 2048, out) == api.OK and out[8] == 2
+    assert L.grpo_decode_structure(h, 64, 4095, 0, 0, out) == api.OK and list(out)[6:8] == [0, 0]
     assert L.grpo_decode_structure(h, 129, 4095, 0, 0, out) == api.INVALID_ARG
     assert L.grpo_decode_structure(h, 64, 4095, 3, 100, out) == api.INVALID_ARG
     assert L.grpo_decode_structure(None, 64, 4095, 0, 0, out) == api.INVALID_ARG

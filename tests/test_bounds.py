@@ -123,6 +123,7 @@ def test_attention_bound_mfma_and_decode_chains():
     K = oracle.round_bf16(rng.standard_normal((ctx, hd)))
     V = oracle.round_bf16(rng.standard_normal((ctx, hd)))
     for segs, merges in (([("mfma", 0, ctx, ctx)], 0), ([("decode", 0, ctx, 256)], 7),
+                         ([("decode", 0, ctx, 256, 2)], 5),
                          ([("mfma", 0, 512, 256), ("decode", 512, ctx, 128)], 24)):
         o, E = attention_bound(q, K, V, hd, segs, merges)
         assert np.all(E < 1e-3 * np.abs(V).mean())

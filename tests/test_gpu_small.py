@@ -155,6 +155,12 @@ def test_small_end_to_end():
     ("small", 1, dict(n_prompts=5, group=1, prompt_len=33, new_tokens=3), 0),
     ("small", 1, dict(n_prompts=16, group=4, prompt_len=20, new_tokens=3), 4),
     ("7b", 1, dict(n_prompts=25, group=4, prompt_len=12, new_tokens=3), 0),
+    # batch 128 at the 1B width: 1024 per-row attention workgroups of 2 waves,
+    # per row (10 tiles a row) and grouped (the prompt chunks merged by 2 waves)
+    ("1b", 1, dict(n_prompts=32, group=4, prompt_len=300, new_tokens=3, temperature=0.8,
+                   top_k=50), 0),
+    ("1b", 1, dict(n_prompts=32, group=4, prompt_len=300, new_tokens=3, temperature=0.8,
+                   top_k=50), 4),
 ])
 def test_full_width_stage_local(name, layers, kw, group):
     """Layer-truncated models at the 1B/7B/32B widths: prefill and decode."""
