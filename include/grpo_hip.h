@@ -447,7 +447,10 @@ int grpo_token_loss_noalloc(const float* logp, const float* logp_old, const floa
  * batch of B rows, a KV capacity max_len and a grouping (G, prefix_len as
  * grpo_rollout_step_grouped; G = 0 for grpo_rollout_step) it writes
  *   out[0..3] split-K factors of the QKV, O, down and LM-head projections
- *   out[4]    context positions per decode-attention span; out[5] spans
+ *   out[4]    planned positions per decode-attention span; out[5] spans (a
+ *             row's positions past its shared length are cut evenly into
+ *             out[5] spans of whole 128-position units, at least one unit;
+ *             the last span runs to the row's end)
  *   out[6]    positions per prompt chunk of a grouped step; out[7] chunks
  *             (both 0 without grouping or for fp32 models)
  *   out[8]    waves per workgroup of the per-row decode attention (4 or 2:

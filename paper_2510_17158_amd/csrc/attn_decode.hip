@@ -65,6 +65,12 @@ __device__ __forceinline__ int group_shared(const int32_t* __restrict__ pos, int
   return pl;
 }
 
+// Positions per span of a row with n positions past its shared length, cut
+// into `spans` spans (the merge kernel recomputes it the same way).
+__device__ __forceinline__ int row_span(int n, int spans) {
+  return max(SPAN_Q, ((n + spans - 1) / spans + SPAN_Q - 1) / SPAN_Q * SPAN_Q);
+}
+
 template <int HD, int NG, int NVT>
 struct KVTile {
   u32x4_t k[NG][HD / 32];
@@ -82,7 +88,7 @@ template <int HD, int MAXG, int NW>
 __global__ __launch_bounds__(64 * NW) void k_attn_decode_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const int32_t* __restrict__ pos, const int32_t* __restrict__ slots, int H, int n_kv,
-    int max_len, int S, int span, float scale, float* __restrict__ part_o,
+    int max_len, int S, float scale, float* __restrict__ part_o,
     float* __restrict__ part_ml, bf16_t* __restrict__ out, int pack_nb, DecodeGroup ga,
     int split_base) {
   constexpr int QSTEPS = HD / 32;     // MFMA k-steps over the head dim
@@ -109,9 +115,13 @@ __global__ __launch_bounds__(64 * NW) void k_attn_decode_bf16(
   const int ctx = min(pos[src], max_len - 1) + 1;
   const int base = ga.G > 0 ? group_shared(pos, src / ga.G, ga, max_len) : 0;
   const bool fold = ga.G > 0 && S == ga.chunks + 1;
-  const int t0 = base + split * span;
+  // the row's positions past `base` cut evenly into the plan's spans (whole
+  // 128-position units, one tile per wave), so that every span has work as the
+  // context grows; the last span runs to the row's end
+  const int rspan = row_span(ctx - base, S - split_base);
+  const int t0 = base + split * rspan;
   if (t0 >= ctx && !fold) return;             // (folding still merges the prompt part)
-  const int t1 = min(t0 + span, ctx);
+  const int t1 = split == S - split_base - 1 ? ctx : min(t0 + rspan, ctx);
   const int ntiles = t1 > t0 ? (t1 - t0 + DT - 1) / DT : 0;
   const int nmine = ntiles > wave ? (ntiles - wave + NW - 1) / NW : 0;
   const int slot = slots ? slots[src] : src;          // the row's cache slot
@@ -578,13 +588,14 @@ template <int HD>
 __global__ __launch_bounds__(HD) void k_attn_combine(const float* __restrict__ part_o,
                                                      const float* __restrict__ part_ml,
                                                      const int32_t* __restrict__ pos, int H,
-                                                     int max_len, int S, int span,
+                                                     int max_len, int S,
                                                      bf16_t* __restrict__ out, int pack_nb,
                                                      DecodeGroup ga, int chunks, int span_p) {
   const int h = blockIdx.x, b = blockIdx.y, e = threadIdx.x;
   const int ctx = min(pos[b], max_len - 1) + 1;
   const int base = ga.G > 0 ? group_shared(pos, b / ga.G, ga, max_len) : 0;
-  auto used = [&](int s) { return s < chunks ? s * span_p < base : base + (s - chunks) * span < ctx; };
+  const int rspan = row_span(ctx - base, S - chunks);
+  auto used = [&](int s) { return s < chunks ? s * span_p < base : base + (s - chunks) * rspan < ctx; };
   const size_t row0 = ((size_t)b * H + h) * S;
   float M = -INFINITY;
   for (int s = 0; s < S; ++s)
@@ -622,9 +633,8 @@ DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len, int
   p.waves = (long)p.splits * n_kv * B >= 2 * kTargetWGs ? 2 : 4;
   p.part_floats = p.splits > 1 ? (size_t)B * H * p.splits * (hd + 2) : 0;
   if (G <= 0 || prefix_len <= 0) return p;
-  // grouped: the generated positions keep the spans above (they start at the
-  // shared length, so they cover at most max_len positions); the prompt is cut
-  // into chunks of whole tiles, about kTargetWGs prefix workgroups in all
+  // grouped: the prompt is cut into chunks of whole tiles, about kTargetWGs
+  // prefix workgroups in all
   const int spb = 32 / std::max(1, H / n_kv);   // samples per prefix workgroup
   p.G = G;
   p.prefix_len = std::min(prefix_len, max_len);
@@ -634,29 +644,42 @@ DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len, int
   const int wc = std::min(std::max(1, (kTargetWGs + gpairs / 2) / gpairs), max_chunks);
   p.span_p = ((p.prefix_len + wc - 1) / wc + DT - 1) / DT * DT;
   p.chunks = (p.prefix_len + p.span_p - 1) / p.span_p;
+  // the per-row spans start at the shared length: sized on the positions past
+  // the prompt (32B: 4095 of a 12287-position cache, two spans of 2048 instead
+  // of one busy span of 6144 and one never reached), the last one open-ended
+  const int gen = std::max(1, max_len - p.prefix_len);
+  const int gspans = std::min(std::max(1, (kTargetWGs + pairs / 2) / pairs),
+                              (gen + SPAN_Q - 1) / SPAN_Q);
+  p.tc = ((gen + gspans - 1) / gspans + SPAN_Q - 1) / SPAN_Q * SPAN_Q;
+  p.splits = (gen + p.tc - 1) / p.tc;
+  p.waves = (long)p.splits * n_kv * B >= 2 * kTargetWGs ? 2 : 4;
   p.part_floats = (size_t)B * H * (p.chunks + p.splits) * (hd + 2);
   return p;
 }
 
 size_t decode_attn_part_floats_max(int B, int H, int n_kv, int hd, int max_len) {
+  // grouped or not, a plan has at most `want` per-row spans (the count the
+  // ungrouped plan aims at; its rounding can only lower it) and MAX_CHUNKS chunks
+  const int pairs = std::max(1, B * n_kv);
+  const int want = std::min(std::max(1, (512 + pairs / 2) / pairs), (max_len + SPAN_Q - 1) / SPAN_Q);
   const DecodeAttnPlan p = decode_attn_plan(B, H, n_kv, hd, max_len);
-  return (size_t)B * H * (MAX_CHUNKS + p.splits) * (hd + 2);
+  return (size_t)B * H * (MAX_CHUNKS + std::max(p.splits, want)) * (hd + 2);
 }
 
 template <int HD, int MAXG>
 static void launch_decode(dim3 grid, int waves, hipStream_t st, const void* q, const void* kc,
                           const void* vc, const int32_t* pos, const int32_t* slots, int H,
-                          int n_kv, int max_len, int S, int span, float scale, float* part_o,
+                          int n_kv, int max_len, int S, float scale, float* part_o,
                           float* part_ml, void* out, int pack_nb, DecodeGroup ga,
                           int split_base) {
   if (waves == 2)
     k_attn_decode_bf16<HD, MAXG, 2><<<grid, 128, 0, st>>>(
         (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, slots, H, n_kv, max_len, S,
-        span, scale, part_o, part_ml, (bf16_t*)out, pack_nb, ga, split_base);
+        scale, part_o, part_ml, (bf16_t*)out, pack_nb, ga, split_base);
   else
     k_attn_decode_bf16<HD, MAXG, 4><<<grid, 256, 0, st>>>(
         (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, slots, H, n_kv, max_len, S,
-        span, scale, part_o, part_ml, (bf16_t*)out, pack_nb, ga, split_base);
+        scale, part_o, part_ml, (bf16_t*)out, pack_nb, ga, split_base);
 }
 
 template <int HD>
@@ -682,16 +705,16 @@ static hipError_t attn_decode_hd(const void* q, const void* kc, const void* vc,
     Prof pf("attn_decode", st);
     dim3 grid(p.splits, n_kv, B);
     if (gq <= 4)
-      launch_decode<HD, 4>(grid, p.waves, st, q, kc, vc, pos, slots, H, n_kv, max_len, S, p.tc,
-                           scale, part_o, part_ml, out, pack_nb, ga, p.chunks);
+      launch_decode<HD, 4>(grid, p.waves, st, q, kc, vc, pos, slots, H, n_kv, max_len, S, scale,
+                           part_o, part_ml, out, pack_nb, ga, p.chunks);
     else
-      launch_decode<HD, 8>(grid, p.waves, st, q, kc, vc, pos, slots, H, n_kv, max_len, S, p.tc,
-                           scale, part_o, part_ml, out, pack_nb, ga, p.chunks);
+      launch_decode<HD, 8>(grid, p.waves, st, q, kc, vc, pos, slots, H, n_kv, max_len, S, scale,
+                           part_o, part_ml, out, pack_nb, ga, p.chunks);
   }
   // grouped with one span of generated positions: merged by the per-row kernel
   if (S > 1 && !(grouped && p.splits == 1)) {
     Prof pf("attn_combine", st);
-    k_attn_combine<HD><<<dim3(H, B), HD, 0, st>>>(part_o, part_ml, pos, H, max_len, S, p.tc,
+    k_attn_combine<HD><<<dim3(H, B), HD, 0, st>>>(part_o, part_ml, pos, H, max_len, S,
                                                   (bf16_t*)out, pack_nb, ga, p.chunks, p.span_p);
   }
   return hipGetLastError();

@@ -133,7 +133,15 @@ def decode_segments(ctx: int, st: dict, base: int = 0):
     segs = []
     if base > 0:
         segs.append(("mfma", 0, base, st["chunk"]))
-    segs.append(("decode", base, ctx, st["span"], st["waves"]))
+    # the per-row spans from `base`: the row's positions past it cut evenly
+    # into whole 128-position units, the last span running to the row's end
+    n, ns = ctx - base, st["spans"]
+    rspan = max(128, -(-(-(-n // ns)) // 128) * 128)
+    for k in range(ns):
+        a0 = base + k * rspan
+        a1 = ctx if k == ns - 1 else min(a0 + rspan, ctx)
+        if a0 < a1:
+            segs.append(("decode", a0, a1, a1 - a0, st["waves"]))
     merges = st["waves"] + st["spans"] + (st["chunks"] + 1 if base > 0 else 0)
     return segs, merges
 
