@@ -366,8 +366,9 @@ __device__ __forceinline__ int kstage_swz(int r) {
 }
 __device__ __forceinline__ int vstage_swz(int r) { return ((r >> 3) & 3) << 1; }
 
-// blockIdx = (chunk, kv head, group x n_sub).  Sub-block u takes the 32 / GQ
-// samples u * (32 / GQ) .. of the group: query column c (two MFMA blocks of 16)
+// blockIdx = (chunk, kv head, group x n_sub).  Sub-block u takes the 16 NCB / GQ
+// samples u * (16 NCB / GQ) .. of the group: query column c (NCB MFMA blocks of
+// 16: 2, or 3 when that keeps a whole group in one sub-block)
 // is head g * GQ + c % GQ of sample c / GQ.  Every wave computes the scores and
 // softmax of all the columns (the same values in each wave) and O^T for its
 // quarter of the head dimension, so a wave reads a quarter of the V^T fragments.
@@ -376,7 +377,7 @@ __device__ __forceinline__ int vstage_swz(int r) { return ((r >> 3) & 3) << 1; }
 // eight scores of its column are positions 8 g .. 8 g + 7: exactly the B operand
 // of O^T += V^T P^T, which takes P as two bf16 terms (hi + lo: no rounding point
 // added) and V^T fragments read transposed from the stage.
-template <int HD>
+template <int HD, int NCB>
 __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     const int32_t* __restrict__ pos, const int32_t* __restrict__ slots, int H, int n_kv,
@@ -400,7 +401,7 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
   const int lg = lane >> 4, j = lane & 15;
   const int group = blockIdx.z / ga.n_sub;
-  const int spb = 32 / GQ;                                   // samples per sub-block
+  const int spb = 16 * NCB / GQ;                             // samples per sub-block
   const int s0 = blockIdx.z % ga.n_sub * spb;                // its first sample
   const int ncols = min(spb, ga.G - s0) * GQ;                // valid columns (> 0)
   const int t0 = split * span;
@@ -414,9 +415,9 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
 
   // Q as the B operand of column block cb: column j -> c = 16 cb + j (zero past
   // ncols); MFMA step st takes piece 4 st + lg
-  bf16x8_t qf[2][QSTEPS];
+  bf16x8_t qf[NCB][QSTEPS];
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
+  for (int cb = 0; cb < NCB; ++cb) {
     const int c = min(16 * cb + j, ncols - 1);
     const bf16_t* qp =
         q + ((size_t)(src + s0 + c / GQ) * H + g * GQ + c % GQ) * HD + lg * 8;
@@ -430,7 +431,7 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
   // the query loads complete before the copies start (the copies are counted by
   // hand below): an empty use of the fragments holds them here
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb)
+  for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
     for (int st = 0; st < QSTEPS; ++st) asm volatile("" ::"v"(qf[cb][st]));
 
@@ -450,37 +451,39 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
     }
   };
 
-  float m[2] = {-1e30f, -1e30f}, l[2] = {0.f, 0.f};   // per column block: column j
-  f32x4_t oacc[HBW][2];   // O^T rows 16 (HBW wave + hb) + 4 lg + v of column j of block cb
+  float m[NCB], l[NCB];   // per column block: column j
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) { m[cb] = -1e30f; l[cb] = 0.f; }
+  f32x4_t oacc[HBW][NCB];   // O^T rows 16 (HBW wave + hb) + 4 lg + v of column j of block cb
 #pragma unroll
   for (int hb = 0; hb < HBW; ++hb)
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) oacc[hb][cb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    for (int cb = 0; cb < NCB; ++cb) oacc[hb][cb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
   auto compute = [&](int stg, int t) __attribute__((always_inline)) {
     const int tb = t0 + t * DT;
     const bf16_t* ksb = &ks[stg][0];
     const uint16_t* vsb = (const uint16_t*)&vs[stg][0];
-    f32x4_t sacc[2][2];   // [b][cb]
+    f32x4_t sacc[2][NCB];   // [b][cb]
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const int row = 8 * (j >> 2) + 4 * b + (j & 3);      // this lane's A row
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) sacc[b][cb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+      for (int cb = 0; cb < NCB; ++cb) sacc[b][cb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < QSTEPS; ++st) {
         const bf16x8_t kf =
             *(const bf16x8_t*)(ksb + row * HD + ((st * 4 + lg) ^ kstage_swz<HD>(row)) * 8);
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
+        for (int cb = 0; cb < NCB; ++cb)
           sacc[b][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[cb][st], sacc[b][cb], 0, 0, 0);
       }
     }
     // lane (j, lg): sacc[b][cb][v] is position 8 lg + 4 b + v of the tile
-    float sv[2][8], mnew[2];
+    float sv[NCB][8], mnew[NCB];
     bool moved = false;
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
+    for (int cb = 0; cb < NCB; ++cb) {
       float tmax = -INFINITY;
 #pragma unroll
       for (int b = 0; b < 2; ++b)
@@ -498,7 +501,7 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
     // rescale only when some column's maximum moved (otherwise the factor is 1)
     if (__builtin_amdgcn_ballot_w64(moved)) {
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) {
+      for (int cb = 0; cb < NCB; ++cb) {
         const float alpha = __expf(m[cb] - mnew[cb]);
         l[cb] *= alpha;
 #pragma unroll
@@ -507,9 +510,9 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
           for (int v = 0; v < 4; ++v) oacc[hb][cb][v] *= alpha;
       }
     }
-    bf16x8_t ph[2], pl[2];
+    bf16x8_t ph[NCB], pl[NCB];
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
+    for (int cb = 0; cb < NCB; ++cb) {
       m[cb] = mnew[cb];
 #pragma unroll
       for (int e = 0; e < 8; e += 2) {
@@ -538,7 +541,7 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
       }
       const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, w);
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) {
+      for (int cb = 0; cb < NCB; ++cb) {
         oacc[hb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph[cb], oacc[hb][cb], 0, 0, 0);
         oacc[hb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[cb], oacc[hb][cb], 0, 0, 0);
       }
@@ -563,7 +566,7 @@ __global__ __launch_bounds__(256) void k_attn_prefix_bf16(
 
   // column c = 16 cb + j: head g * GQ + c % GQ of batch row src + s0 + c / GQ
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
+  for (int cb = 0; cb < NCB; ++cb) {
     float lt = l[cb];
     lt += __shfl_xor(lt, 16, 64);
     lt += __shfl_xor(lt, 32, 64);
@@ -635,7 +638,14 @@ DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len, int
   if (G <= 0 || prefix_len <= 0) return p;
   // grouped: the prompt is cut into chunks of whole tiles, about kTargetWGs
   // prefix workgroups in all
-  const int spb = 32 / std::max(1, H / n_kv);   // samples per prefix workgroup
+  // samples per prefix workgroup: 2 column blocks of 16 (query heads of its
+  // samples), 3 when that takes the whole group in one workgroup where 2 do not
+  // (32B: 8 samples x 5 heads; the paper's K = 12 at 4 heads), so that the
+  // group's prompt K/V is read once
+  const int gq = std::max(1, H / n_kv);
+  const int spb2 = 32 / gq, spb3 = 48 / gq;
+  p.ncb = (G + spb3 - 1) / spb3 < (G + spb2 - 1) / spb2 ? 3 : 2;
+  const int spb = 16 * p.ncb / gq;
   p.G = G;
   p.prefix_len = std::min(prefix_len, max_len);
   p.n_sub = (G + spb - 1) / spb;
@@ -697,9 +707,14 @@ static hipError_t attn_decode_hd(const void* q, const void* kc, const void* vc,
   if (grouped) {
     Prof pf("attn_prefix", st);
     dim3 grid(p.chunks, n_kv, B / p.G * p.n_sub);
-    k_attn_prefix_bf16<HD><<<grid, 256, 0, st>>>(
-        (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, slots, H, n_kv, max_len, S,
-        p.span_p, scale, part_o, part_ml, ga);
+    if (p.ncb == 3)
+      k_attn_prefix_bf16<HD, 3><<<grid, 256, 0, st>>>(
+          (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, slots, H, n_kv, max_len,
+          S, p.span_p, scale, part_o, part_ml, ga);
+    else
+      k_attn_prefix_bf16<HD, 2><<<grid, 256, 0, st>>>(
+          (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, pos, slots, H, n_kv, max_len,
+          S, p.span_p, scale, part_o, part_ml, ga);
   }
   {
     Prof pf("attn_decode", st);
@@ -733,7 +748,8 @@ hipError_t attn_decode(int dtype, const void* q, const void* kc, const void* vc,
   if (H % n_kv || H / n_kv > 8 || (hd != 64 && hd != 128) || (p.waves != 2 && p.waves != 4))
     return hipErrorInvalidValue;
   if (p.G > 0 && (B % p.G || p.chunks < 1 || p.chunks > MAX_CHUNKS || p.n_sub < 1 ||
-                  (long)p.n_sub * (32 / (H / n_kv)) < p.G || p.prefix_len > max_len ||
+                  (p.ncb != 2 && p.ncb != 3) ||
+                  (long)p.n_sub * (16 * p.ncb / (H / n_kv)) < p.G || p.prefix_len > max_len ||
                   (long)p.chunks * p.span_p < p.prefix_len))
     return hipErrorInvalidValue;
   return hd == 128 ? attn_decode_hd<128>(q, kc, vc, pos, slots, B, H, n_kv, max_len, p, part, out,

@@ -224,6 +224,7 @@ struct DecodeAttnPlan {
   int tc, splits;
   int waves;     // waves per workgroup of the per-row kernel (4, or 2 for large grids)
   int G, prefix_len, chunks, span_p, n_sub;
+  int ncb;       // query column blocks of 16 per prefix workgroup (2 or 3)
   size_t part_floats;
 };
 DecodeAttnPlan decode_attn_plan(int B, int H, int n_kv, int hd, int max_len, int G = 0,
