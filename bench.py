@@ -35,14 +35,14 @@ BF16_PEAK_TFLOPS = 2500.0
 # 64 sequences).
 ATTN_TRAFFIC = {
     "source": "paper_2510_17158_amd/csrc/attn_decode.hip",
-    "sha256": "4653c1f3d6a01cd5bb8aea243d4846b2b30e64071260ef4bacfa1a41c1295ef8",
+    "sha256": "43ef04d768466c704263f23bacabddbc355550434d3a6e408908055aaa35092f",
     # rocprofv3 FETCH_SIZE / WRITE_SIZE per dispatch of the per-row decode attention at
     # batch 64 (7B shape, 2048 shared prompt positions), mean of the 32 layers' launches at
     # exactly 1024 generated positions: the mean launch of the 7B rollout (positions
     # 1 .. 2047), read directly; readings at 512 and 1536 put it on their line (0.02%),
     # so the mean launch's traffic is this one's
     "batch": 64, "generated_positions": 1024,
-    "fetch_kib": 136350.5, "fetch_scale": 2.0,
+    "fetch_kib": 136314.7, "fetch_scale": 2.0,
     "write_kib": 512.0, "write_scale": 1.0,
     "position_bytes": 64 * 4096,
 }
